@@ -1,0 +1,56 @@
+"""Plants plausible mistakes in a scratch copy of the oracle (on the CPU) and checks
+that the oracle's pins catch every one of them: a wrong gate, a wrong weight
+block, a dropped bias, swapped gate columns, a sign flip, swapped child
+gradients, a dropped upstream term, a scaled weight gradient, a wrong tanh
+derivative, a lost cell-state pass-through, wrong sort keys and tie-breaks,
+min instead of max in the depth rule, node ids instead of positions as edge
+labels, and overwriting instead of summing fan-out contributions."""
+import os
+import shutil
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+MUTATIONS = [
+    ("cells.py", "c = i * u + fl * cl + fr * cr", "c = i * u + fl * cl + fl * cr"),
+    ("cells.py", 'z += h @ P["W_rec"][k * H:(k + 1) * H]', 'z += h @ P["W_rec"][0:H]'),
+    ("cells.py", 'z = np.array(P["bias"], dtype=np.float64, copy=True)',
+     'z = 0 * np.array(P["bias"], dtype=np.float64, copy=True)'),
+    ("cells.py", "o = sigmoid(z[2 * H:3 * H])\n        u = np.tanh(z[3 * H:4 * H])",
+     "u = np.tanh(z[2 * H:3 * H])\n        o = sigmoid(z[3 * H:4 * H])"),
+    ("cells.py", "            dh * tc * o * (1.0 - o),\n            dct * i * (1.0 - u * u),\n        ])\n        dcs = [dct * fl, dct * fr]",
+     "            -dh * tc * o * (1.0 - o),\n            dct * i * (1.0 - u * u),\n        ])\n        dcs = [dct * fl, dct * fr]"),
+    ("cells.py", "dcs = [dct * fl, dct * fr]", "dcs = [dct * fr, dct * fl]"),
+    ("cells.py", "dct = dc + dh * o * (1.0 - tc * tc)\n        dz = np.concatenate([\n            dct * u * i * (1.0 - i),\n            dct * cl",
+     "dct = dh * o * (1.0 - tc * tc)\n        dz = np.concatenate([\n            dct * u * i * (1.0 - i),\n            dct * cl"),
+    ("cells.py", 'grads["W_in"] = np.outer(x, dz)', 'grads["W_in"] = np.outer(x, dz) * (1 + 1e-3)'),
+    ("cells.py", "dz = dh * (1.0 - h * h)", "dz = dh * (1.0 - h)"),
+    ("cells.py", "dcs = [np.array(dc, dtype=np.float64)] if kind == PROJ", "dcs = [np.zeros(H)] if kind == PROJ"),
+    ("schedule.py", "return (depth[v] - 1) * num_ops + int(node_op[v])",
+     "return int(node_op[v]) * 100000 + depth[v]"),
+    ("schedule.py", "key=lambda v: (key(v), v)", "key=lambda v: (key(v), -v)"),
+    ("schedule.py", "d = max(d, depth[c])", "d = min(d, depth[c]) if d else depth[c]"),
+    ("schedule.py", "child_pos.append(node_pos[c] if c >= 0 else -1)", "child_pos.append(c if c >= 0 else -1)"),
+    ("evaluate.py", "dh[k] += dhs[j]", "dh[k] = dhs[j]"),
+    ("evaluate.py", 'd_table[int(batch["node_input"][v])] += dx', 'd_table[int(batch["node_input"][v])] = dx'),
+]
+
+
+@pytest.mark.parametrize("i", range(len(MUTATIONS)))
+def test_planted_mistake_is_caught(i, tmp_path):
+    fname, old, new = MUTATIONS[i]
+    for d in ("oracle", "tests", "paper_1702_02181_amd"):
+        shutil.copytree(os.path.join(ROOT, d), tmp_path / d,
+                        ignore=shutil.ignore_patterns("*.so", "__pycache__", "_build", "*.o"))
+    shutil.copy(os.path.join(ROOT, "pytest.ini"), tmp_path)
+    p = tmp_path / "oracle" / fname
+    src = p.read_text()
+    assert old in src, "mutation site moved; update the table"
+    p.write_text(src.replace(old, new, 1))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:randomly",
+                        "tests/test_oracle_schedule.py", "tests/test_oracle_cells.py"],
+                       cwd=tmp_path, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"pins missed mutation {i}: {new!r}"
