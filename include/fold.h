@@ -1,0 +1,263 @@
+/*
+ * fold.h -- C ABI of the MI355X dynamic-batching library.
+ *
+ * Dynamic batching (Looks et al., "Deep Learning with Dynamic Computation
+ * Graphs", Section 2) evaluates a batch of computation graphs of different
+ * shapes and sizes by
+ *   1. giving every node a depth (constants have depth 0; a node whose inputs
+ *      have maximum depth d has depth d + 1),
+ *   2. batching together all nodes that run the same operation at the same
+ *      depth,
+ *   3. gathering each batch's inputs by index from the concatenated outputs of
+ *      earlier depths, running the operation once per (depth, operation), and
+ *      concatenating the outputs back,
+ * and back-propagates through the same gathers and concatenations.  This
+ * library exposes that hot path as three calls:
+ *
+ *   fold_schedule   CSR graphs -> per-level, per-operation gather indices
+ *   fold_forward    schedule + parameters + leaf rows -> every node's state
+ *                   and the roots' outputs
+ *   fold_backward   reverse-level pass: gradients scatter-added into child
+ *                   states, weight gradients accumulated
+ *
+ * Conventions shared by every entry point
+ *   - Every call returns FOLD_OK (0) or a negative FOLD_E_* code; the
+ *     matching text is available from fold_last_error() on the calling
+ *     thread.  No C++ exception crosses this boundary.
+ *   - "device" pointers are HIP device allocations on the current device;
+ *     "host" pointers are ordinary host memory.  The caller owns every
+ *     buffer it passes in; the library owns the fold_sched / fold_packed
+ *     handles it returns and everything they point to.
+ *   - All work is enqueued on the given stream.  fold_schedule and
+ *     fold_pack_params synchronise that stream (they read back sizes);
+ *     fold_forward and fold_backward never synchronise and never allocate.
+ *   - Node states live in one pool in SCHEDULE order: row p of a pool holds
+ *     node pos_node[p].  Every row-major float/bf16 matrix the library reads
+ *     or writes has a row stride of fold_row_ld(width) elements; columns
+ *     beyond the width are written as zero (pools) or ignored (inputs).
+ *   - Handles are immutable after creation and may be shared by concurrent
+ *     calls on different streams that use different output buffers.
+ */
+#ifndef FOLD_H_
+#define FOLD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define FOLD_OK 0
+#define FOLD_E_INVALID -1  /* null pointer, negative count, bad dims/dtype, bad op table, broken graph_ptr/child_ptr */
+#define FOLD_E_OP -2       /* node_op out of [0, num_ops) */
+#define FOLD_E_ARITY -3    /* a node's child count differs from its operation's arity */
+#define FOLD_E_CHILD -4    /* child id out of range or in another graph (-1, the zero state, is allowed) */
+#define FOLD_E_INPUT -5    /* input row out of [0, num_inputs), or present/absent against has_input */
+#define FOLD_E_CYCLE -6    /* the graph is not acyclic */
+#define FOLD_E_NOMEM -7    /* device allocation failed */
+#define FOLD_E_DEVICE -8   /* a HIP call failed */
+#define FOLD_E_MISMATCH -9 /* schedule / parameters / workspace inconsistent with each other */
+
+/* ---- operation kinds (the operations of the paper's experiments) ------- */
+enum {
+  FOLD_EMBED = 0,    /* h = table[input]                        (embedding lookup, arity 0, has_input) */
+  FOLD_TREERNN = 1,  /* h = tanh([h_l; h_r] W + b)              (binary TreeRNN cell, arity 2) */
+  FOLD_TREELSTM = 2, /* binary N-ary Tree-LSTM, gates (i|f_l|f_r|o|u); arity 0 with input = leaf
+                        TreeLSTM(x, 0, 0), arity 2 = internal TreeLSTM(x?, h_l, h_r) */
+  FOLD_LSTM = 3,     /* one LSTM step, gates (i|f|o|u), arity 1 (child -1 = zero start state) */
+  FOLD_PROJ = 4      /* h = tanh(h_c P + b), c = c_c            (unary projection, arity 1) */
+};
+
+/* ---- element types of weights, leaf table and h pool ------------------- */
+enum { FOLD_F32 = 0, FOLD_BF16 = 1 };
+
+/* One operation of the op table.  The paper requires every operation to be
+ * specified and enumerated in advance (Section 2); the op id is the index in
+ * the table, and groups of one depth are ordered by it. */
+typedef struct {
+  int32_t kind;      /* FOLD_EMBED .. FOLD_PROJ */
+  int32_t arity;     /* number of node children (CSR entries) */
+  int32_t has_input; /* 1: reads leaf-table row node_input[v] */
+  int32_t param_set; /* index into fold_params.sets */
+} fold_op;
+
+/* A batch of graphs as one disconnected DAG (Section 2), CSR form.
+ * Node ids are global; node order inside a graph is arbitrary.  Children
+ * must belong to the node's own graph; -1 names a zero state. */
+typedef struct {
+  int32_t num_graphs;        /* G >= 0 */
+  int32_t num_nodes;         /* N >= 0 */
+  int32_t num_edges;         /* E >= 0, = child_ptr[N] */
+  int32_t num_ops;           /* >= 1 */
+  int32_t num_inputs;        /* rows of the leaf table that node_input may name */
+  const int32_t* graph_ptr;  /* device [G+1], graph_ptr[0] = 0, graph_ptr[G] = N, nondecreasing */
+  const int32_t* node_op;    /* device [N] */
+  const int32_t* child_ptr;  /* device [N+1], child_ptr[0] = 0, nondecreasing */
+  const int32_t* child_idx;  /* device [E] global node ids or -1 */
+  const int32_t* node_input; /* device [N] leaf-table row, or -1 */
+  const fold_op* ops;        /* host [num_ops] */
+} fold_batch;
+
+typedef struct fold_sched fold_sched;
+typedef struct fold_packed fold_packed;
+
+/* Read-only view of a schedule.  Device arrays are owned by the schedule. */
+typedef struct {
+  int32_t num_nodes, num_edges, num_graphs, num_ops;
+  int32_t num_levels; /* D = maximum depth = number of batched steps */
+  int32_t num_groups; /* non-empty (depth, op) groups */
+  int32_t num_roots;  /* nodes that are nobody's child */
+  int32_t max_parents;
+  /* device, int32 */
+  const int32_t* depth;           /* [N]   depth of node v (leaf operations: 1) */
+  const int32_t* node_pos;        /* [N]   pool row of node v */
+  const int32_t* pos_node;        /* [N]   node at pool row p */
+  const int32_t* level_ptr;       /* [D+1] rows of depth <= l end at level_ptr[l] */
+  const int32_t* group_level;     /* [num_groups] */
+  const int32_t* group_op;        /* [num_groups] */
+  const int32_t* group_row_begin; /* [num_groups] first pool row of the group */
+  const int32_t* group_rows;      /* [num_groups] */
+  const int32_t* group_idx_off;   /* [num_groups] offset of the group's edges in child_pos */
+  const int32_t* child_pos;       /* [E]   pool row of child k of the group's row r at
+                                     group_idx_off + r * arity + k, or -1 (zero state) */
+  const int32_t* input_idx;       /* [N]   leaf-table row read by pool row p, or -1 */
+  const int32_t* root_pos;        /* [num_roots] pool rows of the roots, ascending node id */
+  /* host copies */
+  const int32_t* h_level_ptr;
+  const int32_t* h_group_level;
+  const int32_t* h_group_op;
+  const int32_t* h_group_row_begin;
+  const int32_t* h_group_rows;
+  const int32_t* h_group_idx_off;
+} fold_sched_info;
+
+/* Schedule a batch (Section 2, the greedy scheduling algorithm):
+ * validates the CSR (codes above), computes every node's depth on the GPU
+ * (cycles -> FOLD_E_CYCLE), sorts the nodes by the key (depth - 1) * num_ops
+ * + op with ties kept in node-id order (a stable counting sort), and emits
+ * the per-group gather indices.  The edge label of the paper (index i into
+ * the concatenated outputs of depth d) is the pool row minus
+ * level_ptr[d - 1]; pass-throughs are unnecessary because the pool keeps
+ * every level.  Synchronises `stream` twice (error flag and depth, then the
+ * group table).  On success *out is a new handle to free with
+ * fold_sched_free; on error *out is NULL. */
+int32_t fold_schedule(const fold_batch* batch, hipStream_t stream, fold_sched** out);
+int32_t fold_sched_get_info(const fold_sched* sched, fold_sched_info* out);
+int32_t fold_sched_free(fold_sched* sched);
+
+/* Parameters of one operation family, canonical row-major layout, device
+ * memory, element type fold_params.dtype (bias always fp32).  G gate blocks
+ * (Tree-LSTM 5, LSTM 4, TreeRNN / PROJ 1, EMBED 0) of `hidden` columns each,
+ * in the order given under FOLD_TREELSTM / FOLD_LSTM. */
+typedef struct {
+  int32_t kind;
+  int32_t in_dim;    /* width of the leaf-table rows the ops read (EMBED: = hidden) */
+  int32_t arity;     /* child slots covered by W_rec */
+  const void* W_in;  /* [in_dim, G*hidden] or NULL when in_dim == 0 */
+  const void* W_rec; /* [arity*hidden, G*hidden]; rows k*hidden.. belong to child k */
+  const float* bias; /* [G*hidden] (NULL for EMBED) */
+} fold_param_set;
+
+typedef struct {
+  int32_t dtype;  /* FOLD_F32 or FOLD_BF16 */
+  int32_t hidden; /* H */
+  int32_t num_sets;
+  const fold_param_set* sets; /* host [num_sets] */
+} fold_params;
+
+/* Copy the parameters into the library's MFMA-friendly layouts (gate blocks
+ * interleaved per 32 hidden units, K padded per input segment, transposed
+ * copies for the backward).  Reads the caller's arrays once; synchronises. */
+int32_t fold_pack_params(const fold_params* params, hipStream_t stream, fold_packed** out);
+int32_t fold_packed_free(fold_packed* packed);
+
+/* Row stride, in elements, that the library uses for a row of `width`
+ * elements (pools, root outputs, gradients of node states, leaf tables). */
+int32_t fold_row_ld(int32_t width);
+
+/* Workspace needed by fold_forward (saved gate activations for the
+ * backward) and by fold_backward (the same region plus per-node gradient
+ * accumulators).  One buffer of bwd_bytes serves both calls. */
+int32_t fold_workspace_size(const fold_sched* sched, const fold_packed* packed,
+                            size_t* fwd_bytes, size_t* bwd_bytes);
+
+/* Forward pass over every level: for each (depth, op) group in order, gather
+ * the children's (h, c) rows and the leaf-table rows by index, contract
+ * with the operation's weights on the matrix cores, apply the cell, and
+ * write the group's rows of the pools.
+ *   leaf_table  device [leaf_rows, fold_row_ld(in_dim)] of dtype (may be NULL
+ *               if no op has an input)
+ *   h_pool      device [N, fold_row_ld(H)] of dtype (written)
+ *   c_pool      device [N, fold_row_ld(H)] fp32 (written)
+ *   roots_out   device [num_roots, fold_row_ld(H)] of dtype (written; NULL skips)
+ *   ws          device workspace of >= fwd_bytes; receives the activations
+ *               fold_backward needs (NULL with ws_bytes 0: inference only)
+ * Asynchronous; allocates nothing. */
+int32_t fold_forward(const fold_sched* sched, const fold_packed* packed,
+                     const void* leaf_table, int64_t leaf_rows,
+                     void* h_pool, float* c_pool, void* roots_out,
+                     void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Gradients of one parameter set, canonical layout, fp32, device memory.
+ * Accumulated (+=): the caller zeroes them.  NULL skips that tensor. */
+typedef struct {
+  float* dW_in;  /* [in_dim, G*H] */
+  float* dW_rec; /* [arity*H, G*H] */
+  float* dbias;  /* [G*H] */
+} fold_param_grads;
+
+typedef struct {
+  int32_t num_sets;              /* must equal the packed parameters' */
+  const fold_param_grads* sets;  /* host [num_sets] */
+  float* d_leaf_table;           /* device [leaf_rows, fold_row_ld(in_dim)] fp32, += ; or NULL */
+} fold_grads;
+
+/* Backward pass, levels in reverse order.  The upstream gradient is
+ * dh_roots on the roots (row r = root r, in ascending node id) plus, if
+ * given, dh_nodes on every pool row; the roots' cell states get none.
+ * For each group: dz from the saved gates, dz . W^T scatter-added into the
+ * children's (h, c) gradients (every parent lies at a greater depth, so a
+ * child's gradient is complete before its own level runs) and into the leaf
+ * table rows; then the weight gradients dW += X^T dz, db += sum dz.
+ *   h_pool, c_pool, ws   exactly as left by fold_forward with this schedule
+ *   dh_roots             device [num_roots, ld(H)] fp32 or NULL
+ *   dh_nodes             device [N, ld(H)] fp32 (pool order) or NULL
+ *   dh_out, dc_out       device [N, ld(H)] fp32 (pool order) or NULL: receive every
+ *                        node's total upstream gradient of h and c
+ * Asynchronous; allocates nothing. */
+int32_t fold_backward(const fold_sched* sched, const fold_packed* packed,
+                      const void* leaf_table, int64_t leaf_rows,
+                      const void* h_pool, const float* c_pool,
+                      const float* dh_roots, const float* dh_nodes,
+                      const fold_grads* grads, float* dh_out, float* dc_out,
+                      void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---- per-kernel timing (profiling aid) ----------------------------------
+ * While enabled, every kernel the library launches is bracketed by a pair of
+ * HIP events recorded on the launch stream, under a short kernel-class name
+ * (e.g. "cell_fwd.treelstm.f32").  fold_profile_read waits for the recorded
+ * events, returns one entry per class (launch count, summed and largest
+ * duration in milliseconds), and clears the record.  Enabling costs one
+ * event pair per launch; disabled (the default) it costs nothing. */
+typedef struct {
+  char name[48];
+  int64_t launches;
+  double total_ms;
+  double max_ms;
+} fold_kernel_stat;
+
+int32_t fold_profile_enable(int32_t on);
+int32_t fold_profile_read(fold_kernel_stat* out, int32_t capacity, int32_t* count);
+
+/* Text of the last error on the calling thread ("" if none). */
+const char* fold_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FOLD_H_ */

@@ -1,0 +1,618 @@
+// C ABI of the library: argument checking, handles, workspace layout and the level loops that drive
+// the kernels.  Every entry point catches everything, so no C++ exception leaves the library.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstring>
+#include <exception>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "internal.h"
+
+namespace fold {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+void set_error(const std::string& msg) { g_last_error = msg; }
+void clear_error() { g_last_error.clear(); }
+
+// ---------------------------------------------------------------- kernel timing
+
+namespace {
+std::atomic<bool> g_prof_on{false};
+std::mutex g_prof_mu;
+struct ProfRec {
+  std::string name;
+  hipEvent_t a, b;
+};
+std::vector<ProfRec> g_prof_recs;
+std::vector<hipEvent_t> g_prof_free;
+
+hipEvent_t prof_event() {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof_free.empty()) {
+    hipEvent_t e = g_prof_free.back();
+    g_prof_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+}  // namespace
+
+ProfScope::ProfScope(const char* name, hipStream_t st) : name_(name), st_(st) {
+  if (!g_prof_on.load(std::memory_order_relaxed)) return;
+  hipEvent_t a = prof_event(), b = prof_event();
+  if (!a || !b) return;
+  start_ = a;
+  stop_ = b;
+  (void)hipEventRecord(a, st);
+}
+
+ProfScope::~ProfScope() {
+  if (!start_) return;
+  (void)hipEventRecord(static_cast<hipEvent_t>(stop_), st_);
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_recs.push_back({name_, static_cast<hipEvent_t>(start_), static_cast<hipEvent_t>(stop_)});
+}
+
+namespace {
+
+int fail(int code, const std::string& msg) {
+  set_error(msg);
+  return code;
+}
+
+bool valid_kind(int k) { return k >= FOLD_EMBED && k <= FOLD_PROJ; }
+
+// child slots an operation family's recurrent weights cover
+int slots_of(int kind) {
+  switch (kind) {
+    case FOLD_TREERNN: return 2;
+    case FOLD_TREELSTM: return 2;
+    case FOLD_LSTM: return 1;
+    case FOLD_PROJ: return 1;
+    default: return 0;
+  }
+}
+
+int check_op_table(const fold_op* ops, int n) {
+  for (int i = 0; i < n; ++i) {
+    const fold_op& o = ops[i];
+    if (!valid_kind(o.kind) || o.param_set < 0 || (o.has_input != 0 && o.has_input != 1) || o.arity < 0)
+      return fail(FOLD_E_INVALID, "op " + std::to_string(i) + ": bad kind, param_set or has_input");
+    bool ok = true;
+    switch (o.kind) {
+      case FOLD_EMBED: ok = o.arity == 0 && o.has_input == 1; break;
+      case FOLD_TREERNN: ok = o.arity == 2; break;
+      case FOLD_TREELSTM: ok = (o.arity == 2) || (o.arity == 0 && o.has_input == 1); break;
+      case FOLD_LSTM: ok = o.arity == 1; break;
+      case FOLD_PROJ: ok = o.arity == 1 && o.has_input == 0; break;
+      default: ok = false;
+    }
+    if (!ok) return fail(FOLD_E_INVALID, "op " + std::to_string(i) + ": arity / has_input not valid for its kind");
+  }
+  return FOLD_OK;
+}
+
+// the single leaf-table width every op with an input reads (0 if none); -1 if they disagree
+int table_width(const Sched& s, const Packed& p) {
+  int w = 0;
+  for (const fold_op& o : s.ops) {
+    if (!o.has_input) continue;
+    const int d = p.sets[o.param_set].in_dim;
+    if (w == 0) w = d;
+    else if (w != d) return -1;
+  }
+  return w;
+}
+
+int check_compat(const Sched& s, const Packed& p) {
+  for (size_t i = 0; i < s.ops.size(); ++i) {
+    const fold_op& o = s.ops[i];
+    if (o.param_set >= (int)p.sets.size())
+      return fail(FOLD_E_MISMATCH, "op " + std::to_string(i) + " names a missing parameter set");
+    const PackedSet& ps = p.sets[o.param_set];
+    if (ps.kind != o.kind) return fail(FOLD_E_MISMATCH, "op " + std::to_string(i) + ": parameter set of another kind");
+    if (o.arity > ps.arity) return fail(FOLD_E_MISMATCH, "op " + std::to_string(i) + ": more children than W_rec covers");
+    if (o.has_input && ps.in_dim <= 0) return fail(FOLD_E_MISMATCH, "op " + std::to_string(i) + ": reads an input but has no W_in");
+    if (o.kind == FOLD_EMBED && ps.in_dim != p.H) return fail(FOLD_E_MISMATCH, "embedding width must equal hidden");
+  }
+  if (table_width(s, p) < 0) return fail(FOLD_E_MISMATCH, "ops with an input disagree on its width");
+  return FOLD_OK;
+}
+
+}  // namespace
+
+WsLayout workspace_layout(const Sched& s, const Packed& p) {
+  WsLayout w;
+  int gmax = 1;
+  for (const fold_op& o : s.ops) gmax = std::max(gmax, gates_of(o.kind));
+  w.gstride = gmax * p.HP;
+  const size_t N = (size_t)s.N;
+  auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+  w.gates_off = 0;
+  w.gates_bytes = al(N * w.gstride * sizeof(float));
+  w.dh_off = w.gates_bytes;
+  w.dc_off = w.dh_off + al(N * p.ld * sizeof(float));
+  w.acc_bytes = w.dc_off + al(N * p.ld * sizeof(float)) - w.dh_off;
+  size_t part = 0, bpart = 0;
+  for (int o = 0; o < s.num_ops; ++o) {
+    const fold_op& op = s.ops[o];
+    if (op.kind == FOLD_EMBED || op.param_set >= (int)p.sets.size()) continue;
+    const int count = s.h_op_row_ptr[o + 1] - s.h_op_row_ptr[o];
+    const PackedSet& ps = p.sets[op.param_set];
+    const int Nw = ps.G * p.HP;
+    if (op.arity > 0) {
+      WgradSplit sp = wgrad_split(count, op.arity * p.HP, Nw);
+      part = std::max(part, (size_t)sp.nchunk * op.arity * p.HP * Nw);
+    }
+    if (op.has_input && ps.INP > 0) {
+      WgradSplit sp = wgrad_split(count, ps.INP, Nw);
+      part = std::max(part, (size_t)sp.nchunk * ps.INP * Nw);
+    }
+    bpart = std::max(bpart, (size_t)((count + 4095) / 4096) * Nw);
+  }
+  w.part_off = w.dh_off + w.acc_bytes;
+  w.part_bytes = al(part * sizeof(float));
+  w.bpart_off = w.part_off + w.part_bytes;
+  w.bpart_bytes = al(bpart * sizeof(float));
+  w.fwd_bytes = w.gates_bytes;
+  w.bwd_bytes = w.bpart_off + w.bpart_bytes;
+  return w;
+}
+
+int32_t pack_impl(const fold_params* prm, hipStream_t st, fold_packed** out) {
+  auto* h = new fold_packed();
+  Packed& P = h->p;
+  P.dtype = prm->dtype;
+  P.H = prm->hidden;
+  P.HP = round_up(prm->hidden, kPadK);
+  P.ld = row_ld(prm->hidden);
+  (void)hipGetDevice(&P.device);
+  const size_t es = prm->dtype == FOLD_BF16 ? 2 : 4;
+  auto bail = [&](int code, const std::string& m) {
+    packed_destroy_impl(h);
+    return fail(code, m);
+  };
+  auto dalloc = [&](size_t bytes, void** ptr) -> bool {
+    *ptr = nullptr;
+    if (bytes == 0) return true;
+    if (hipMalloc(ptr, bytes) != hipSuccess) return false;
+    P.allocs.push_back(*ptr);
+    return true;
+  };
+  for (int i = 0; i < prm->num_sets; ++i) {
+    const fold_param_set& s = prm->sets[i];
+    PackedSet ps;
+    ps.kind = s.kind;
+    ps.in_dim = s.in_dim;
+    ps.arity = s.arity;
+    ps.G = gates_of(s.kind);
+    if (s.kind != FOLD_EMBED) {
+      ps.INP = (s.in_dim > 0) ? round_up(s.in_dim, kPadK) : 0;
+      ps.Kf = ps.INP + s.arity * P.HP;
+      ps.Nf = ps.G * P.HP;
+      const size_t nf = (size_t)ps.Nf * ps.Kf;
+      const size_t nbr = (size_t)s.arity * P.HP * ps.G * P.HP;
+      const size_t nbi = (size_t)ps.INP * ps.G * P.HP;
+      if (!dalloc(nf * es, &ps.Wf) || !dalloc(nbr * es, &ps.Wb_rec) || !dalloc(nbi * es, &ps.Wb_in) ||
+          !dalloc((size_t)ps.G * P.HP * sizeof(float), reinterpret_cast<void**>(&ps.bias)))
+        return bail(FOLD_E_NOMEM, "fold_pack_params: out of device memory");
+      launch_pack(P.dtype, 0, ps.G, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr, ps.Wf, nf, st);
+      if (nbr) launch_pack(P.dtype, 1, ps.G, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr, ps.Wb_rec, nbr, st);
+      if (nbi) launch_pack(P.dtype, 2, ps.G, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr, ps.Wb_in, nbi, st);
+      launch_pack(P.dtype, 3, ps.G, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, nullptr, nullptr, s.bias, ps.bias,
+                  (size_t)ps.G * P.HP, st);
+    }
+    P.sets.push_back(ps);
+  }
+  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess)
+    return bail(FOLD_E_DEVICE, "fold_pack_params: device error while packing");
+  *out = h;
+  return FOLD_OK;
+}
+
+void packed_destroy_impl(fold_packed* h) {
+  if (!h) return;
+  for (void* q : h->p.allocs) (void)hipFree(q);
+  delete h;
+}
+
+int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, void* h_pool,
+                     float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st) {
+  const WsLayout L = workspace_layout(s, p);
+  float* gates = nullptr;
+  if (ws) {
+    if (ws_bytes < L.fwd_bytes) return fail(FOLD_E_MISMATCH, "fold_forward: workspace too small");
+    gates = reinterpret_cast<float*>(static_cast<char*>(ws) + L.gates_off);
+  }
+  const int tw = table_width(s, p);
+  const int tld = row_ld(tw);
+  for (int g = 0; g < s.num_groups; ++g) {
+    const fold_op& op = s.ops[s.h_op[g]];
+    const PackedSet& ps = p.sets[op.param_set];
+    if (op.kind == FOLD_EMBED) {
+      launch_embed_fwd(p.dtype, s.h_rows[g], s.h_row_begin[g], p.H, p.ld, tld, table, s.input_idx, h_pool, c_pool, st);
+      continue;
+    }
+    FwdArgs a;
+    a.rows = s.h_rows[g];
+    a.row_begin = s.h_row_begin[g];
+    a.idx_off = s.h_idx_off[g];
+    a.arity = op.arity;
+    a.has_input = op.has_input;
+    a.H = p.H;
+    a.HP = p.HP;
+    a.ld = p.ld;
+    a.in_dim = ps.in_dim;
+    a.INP = ps.INP;
+    a.tld = tld;
+    a.Kf = ps.Kf;
+    a.table = table;
+    a.h_pool = h_pool;
+    a.c_pool = c_pool;
+    a.child_pos = s.child_pos;
+    a.input_idx = s.input_idx;
+    a.Wf = ps.Wf;
+    a.bias = ps.bias;
+    a.gates = gates;
+    a.gstride = L.gstride;
+    launch_cell_fwd(p.dtype, op.kind, a, st);
+  }
+  if (roots_out) launch_roots(p.dtype, s.R, p.ld, s.root_pos, h_pool, roots_out, st);
+  (void)table_rows;
+  if (hipGetLastError() != hipSuccess) return fail(FOLD_E_DEVICE, "fold_forward: kernel launch failed");
+  return FOLD_OK;
+}
+
+int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, const void* h_pool,
+                      const float* c_pool, const float* dh_roots, const float* dh_nodes, const fold_grads* grads,
+                      float* dh_out, float* dc_out, void* ws, size_t ws_bytes, hipStream_t st) {
+  const WsLayout L = workspace_layout(s, p);
+  if (!ws || ws_bytes < L.bwd_bytes) return fail(FOLD_E_MISMATCH, "fold_backward: workspace too small");
+  char* wsb = static_cast<char*>(ws);
+  float* gates = reinterpret_cast<float*>(wsb + L.gates_off);
+  float* dh = dh_out ? dh_out : reinterpret_cast<float*>(wsb + L.dh_off);
+  float* dc = dc_out ? dc_out : reinterpret_cast<float*>(wsb + L.dc_off);
+  float* part = reinterpret_cast<float*>(wsb + L.part_off);
+  float* bpart = reinterpret_cast<float*>(wsb + L.bpart_off);
+  const int tw = table_width(s, p);
+  const int tld = row_ld(tw);
+  float* d_table = grads ? grads->d_leaf_table : nullptr;
+
+  launch_bwd_init(s.N, s.R, p.ld, dh_nodes, dh_roots, s.root_pos, dh, dc, st);
+  for (int g = s.num_groups - 1; g >= 0; --g) {
+    const fold_op& op = s.ops[s.h_op[g]];
+    const PackedSet& ps = p.sets[op.param_set];
+    BwdCellArgs b;
+    b.rows = s.h_rows[g];
+    b.row_begin = s.h_row_begin[g];
+    b.idx_off = s.h_idx_off[g];
+    b.arity = op.arity;
+    b.H = p.H;
+    b.HP = p.HP;
+    b.ld = p.ld;
+    b.gstride = L.gstride;
+    b.c_pool = c_pool;
+    b.gates = gates;
+    b.dh = dh;
+    b.dc = dc;
+    b.child_pos = s.child_pos;
+    b.input_idx = s.input_idx;
+    b.d_table = d_table;
+    b.tld = tld;
+    launch_cell_bwd(op.kind, b, st);
+    if (op.kind == FOLD_EMBED) continue;
+    DxArgs d;
+    d.rows = b.rows;
+    d.row_begin = b.row_begin;
+    d.idx_off = b.idx_off;
+    d.arity = op.arity;
+    d.H = p.H;
+    d.HP = p.HP;
+    d.ld = p.ld;
+    d.gstride = L.gstride;
+    d.Kb = ps.G * p.HP;
+    d.dz = gates;
+    d.dh = dh;
+    d.child_pos = s.child_pos;
+    d.d_table = d_table;
+    d.input_idx = s.input_idx;
+    d.in_dim = ps.in_dim;
+    d.tld = tld;
+    if (op.arity > 0) {
+      d.mode = 0;
+      d.Nb = op.arity * p.HP;
+      d.Wb = ps.Wb_rec;
+      launch_bwd_dx(p.dtype, d, st);
+    }
+    if (op.has_input && d_table && ps.INP > 0) {
+      d.mode = 1;
+      d.Nb = ps.INP;
+      d.Wb = ps.Wb_in;
+      launch_bwd_dx(p.dtype, d, st);
+    }
+  }
+  // weight gradients: one deferred contraction per (op, input segment)
+  if (grads) {
+    for (int o = 0; o < s.num_ops; ++o) {
+      const fold_op& op = s.ops[o];
+      if (op.kind == FOLD_EMBED) continue;
+      const int count = s.h_op_row_ptr[o + 1] - s.h_op_row_ptr[o];
+      if (count <= 0) continue;
+      const PackedSet& ps = p.sets[op.param_set];
+      const fold_param_grads& pg = grads->sets[op.param_set];
+      const int Nw = ps.G * p.HP;
+      WgArgs w;
+      w.op_rows = s.op_rows + s.h_op_row_ptr[o];
+      w.count = count;
+      w.pos_group = s.pos_group;
+      w.g_row_begin = s.g_row_begin;
+      w.g_idx_off = s.g_idx_off;
+      w.arity = op.arity;
+      w.H = p.H;
+      w.HP = p.HP;
+      w.ld = p.ld;
+      w.in_dim = ps.in_dim;
+      w.tld = tld;
+      w.gstride = L.gstride;
+      w.Nw = Nw;
+      w.child_pos = s.child_pos;
+      w.input_idx = s.input_idx;
+      w.dz = gates;
+      w.partial = part;
+      if (op.arity > 0 && pg.dW_rec) {
+        w.seg = 1;
+        w.Kw = op.arity * p.HP;
+        w.src = h_pool;
+        WgradSplit sp = wgrad_split(count, w.Kw, Nw);
+        w.chunk = sp.chunk;
+        w.nchunk = sp.nchunk;
+        launch_wgrad(p.dtype, w, st);
+        launch_wgrad_reduce(part, sp.nchunk, w.Kw, Nw, 1, p.H, p.HP, ps.in_dim, ps.G, pg.dW_rec, st);
+      }
+      if (op.has_input && ps.INP > 0 && pg.dW_in) {
+        w.seg = 0;
+        w.Kw = ps.INP;
+        w.src = table;
+        WgradSplit sp = wgrad_split(count, w.Kw, Nw);
+        w.chunk = sp.chunk;
+        w.nchunk = sp.nchunk;
+        launch_wgrad(p.dtype, w, st);
+        launch_wgrad_reduce(part, sp.nchunk, w.Kw, Nw, 0, p.H, p.HP, ps.in_dim, ps.G, pg.dW_in, st);
+      }
+      if (pg.dbias) {
+        const int chunk = 4096, nchunk = (count + chunk - 1) / chunk;
+        launch_bias_grad(w.op_rows, count, chunk, nchunk, gates, L.gstride, Nw, bpart, ps.G, p.H, p.HP, pg.dbias, st);
+      }
+    }
+  }
+  (void)table_rows;
+  if (hipGetLastError() != hipSuccess) return fail(FOLD_E_DEVICE, "fold_backward: kernel launch failed");
+  return FOLD_OK;
+}
+
+}  // namespace fold
+
+using namespace fold;
+
+#define FOLD_GUARD_BEGIN try {
+#define FOLD_GUARD_END                                                      \
+  }                                                                         \
+  catch (const std::exception& e) {                                         \
+    return fail(FOLD_E_INVALID, std::string("internal error: ") + e.what()); \
+  }                                                                         \
+  catch (...) {                                                             \
+    return fail(FOLD_E_INVALID, "internal error");                          \
+  }
+
+extern "C" {
+
+const char* fold_last_error(void) { return fold::g_last_error.c_str(); }
+
+int32_t fold_profile_enable(int32_t on) {
+  fold::g_prof_on.store(on != 0);
+  return FOLD_OK;
+}
+
+int32_t fold_profile_read(fold_kernel_stat* out, int32_t capacity, int32_t* count) {
+  FOLD_GUARD_BEGIN
+  if (!count || (capacity > 0 && !out)) return fail(FOLD_E_INVALID, "fold_profile_read: NULL argument");
+  std::vector<fold::ProfRec> recs;
+  {
+    std::lock_guard<std::mutex> lk(fold::g_prof_mu);
+    recs.swap(fold::g_prof_recs);
+  }
+  std::map<std::string, fold_kernel_stat> agg;
+  std::vector<std::string> order;
+  int32_t rc = FOLD_OK;
+  for (auto& r : recs) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) rc = FOLD_E_DEVICE;
+    auto it = agg.find(r.name);
+    if (it == agg.end()) {
+      fold_kernel_stat st{};
+      std::strncpy(st.name, r.name.c_str(), sizeof(st.name) - 1);
+      it = agg.emplace(r.name, st).first;
+      order.push_back(r.name);
+    }
+    it->second.launches += 1;
+    it->second.total_ms += ms;
+    it->second.max_ms = std::max(it->second.max_ms, (double)ms);
+  }
+  {
+    std::lock_guard<std::mutex> lk(fold::g_prof_mu);
+    for (auto& r : recs) {
+      fold::g_prof_free.push_back(r.a);
+      fold::g_prof_free.push_back(r.b);
+    }
+  }
+  int32_t n = 0;
+  for (const auto& name : order) {
+    if (n < capacity) out[n] = agg[name];
+    ++n;
+  }
+  *count = n;
+  if (rc != FOLD_OK) return fail(rc, "fold_profile_read: event query failed");
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
+int32_t fold_row_ld(int32_t width) { return width < 0 ? 0 : row_ld(width); }
+
+int32_t fold_schedule(const fold_batch* b, hipStream_t st, fold_sched** out) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!out) return fail(FOLD_E_INVALID, "fold_schedule: out is NULL");
+  *out = nullptr;
+  if (!b) return fail(FOLD_E_INVALID, "fold_schedule: batch is NULL");
+  if (b->num_graphs < 0 || b->num_nodes < 0 || b->num_edges < 0 || b->num_ops < 1 || b->num_inputs < 0)
+    return fail(FOLD_E_INVALID, "fold_schedule: negative count or no operations");
+  if (!b->ops || !b->graph_ptr || (b->num_nodes > 0 && (!b->node_op || !b->child_ptr || !b->node_input)) ||
+      (b->num_edges > 0 && !b->child_idx) || !b->child_ptr)
+    return fail(FOLD_E_INVALID, "fold_schedule: NULL array");
+  int rc = check_op_table(b->ops, b->num_ops);
+  if (rc != FOLD_OK) return rc;
+  return schedule_impl(b, st, out);
+  FOLD_GUARD_END
+}
+
+int32_t fold_sched_get_info(const fold_sched* h, fold_sched_info* o) {
+  FOLD_GUARD_BEGIN
+  if (!h || !o) return fail(FOLD_E_INVALID, "fold_sched_get_info: NULL argument");
+  const Sched& s = h->s;
+  o->num_nodes = s.N;
+  o->num_edges = s.E;
+  o->num_graphs = s.G;
+  o->num_ops = s.num_ops;
+  o->num_levels = s.D;
+  o->num_groups = s.num_groups;
+  o->num_roots = s.R;
+  o->max_parents = s.max_parents;
+  o->depth = s.depth;
+  o->node_pos = s.node_pos;
+  o->pos_node = s.pos_node;
+  o->level_ptr = s.level_ptr;
+  o->group_level = s.g_level;
+  o->group_op = s.g_op;
+  o->group_row_begin = s.g_row_begin;
+  o->group_rows = s.g_rows;
+  o->group_idx_off = s.g_idx_off;
+  o->child_pos = s.child_pos;
+  o->input_idx = s.input_idx;
+  o->root_pos = s.root_pos;
+  o->h_level_ptr = s.h_level_ptr.data();
+  o->h_group_level = s.h_level.data();
+  o->h_group_op = s.h_op.data();
+  o->h_group_row_begin = s.h_row_begin.data();
+  o->h_group_rows = s.h_rows.data();
+  o->h_group_idx_off = s.h_idx_off.data();
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
+int32_t fold_sched_free(fold_sched* h) {
+  FOLD_GUARD_BEGIN
+  sched_destroy_impl(h);
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
+int32_t fold_pack_params(const fold_params* prm, hipStream_t st, fold_packed** out) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!out) return fail(FOLD_E_INVALID, "fold_pack_params: out is NULL");
+  *out = nullptr;
+  if (!prm || !prm->sets || prm->num_sets < 1) return fail(FOLD_E_INVALID, "fold_pack_params: no parameter sets");
+  if (prm->dtype != FOLD_F32 && prm->dtype != FOLD_BF16) return fail(FOLD_E_INVALID, "fold_pack_params: bad dtype");
+  if (prm->hidden < 1) return fail(FOLD_E_INVALID, "fold_pack_params: hidden must be positive");
+  for (int i = 0; i < prm->num_sets; ++i) {
+    const fold_param_set& s = prm->sets[i];
+    const std::string at = "fold_pack_params: set " + std::to_string(i) + ": ";
+    if (!valid_kind(s.kind)) return fail(FOLD_E_INVALID, at + "bad kind");
+    if (s.in_dim < 0) return fail(FOLD_E_INVALID, at + "negative in_dim");
+    if (s.kind == FOLD_EMBED) {
+      if (s.in_dim != prm->hidden) return fail(FOLD_E_INVALID, at + "embedding width must equal hidden");
+      continue;
+    }
+    if (s.arity != slots_of(s.kind)) return fail(FOLD_E_INVALID, at + "arity must be the kind's child slots");
+    if (!s.bias) return fail(FOLD_E_INVALID, at + "bias is NULL");
+    if (s.in_dim > 0 && !s.W_in) return fail(FOLD_E_INVALID, at + "W_in is NULL");
+    if (!s.W_rec) return fail(FOLD_E_INVALID, at + "W_rec is NULL");
+  }
+  return pack_impl(prm, st, out);
+  FOLD_GUARD_END
+}
+
+int32_t fold_packed_free(fold_packed* h) {
+  FOLD_GUARD_BEGIN
+  packed_destroy_impl(h);
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
+int32_t fold_workspace_size(const fold_sched* sh, const fold_packed* ph, size_t* fwd_bytes, size_t* bwd_bytes) {
+  FOLD_GUARD_BEGIN
+  if (!sh || !ph) return fail(FOLD_E_INVALID, "fold_workspace_size: NULL handle");
+  int rc = check_compat(sh->s, ph->p);
+  if (rc != FOLD_OK) return rc;
+  WsLayout L = workspace_layout(sh->s, ph->p);
+  if (fwd_bytes) *fwd_bytes = L.fwd_bytes;
+  if (bwd_bytes) *bwd_bytes = L.bwd_bytes;
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
+int32_t fold_forward(const fold_sched* sh, const fold_packed* ph, const void* table, int64_t table_rows,
+                     void* h_pool, float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!sh || !ph) return fail(FOLD_E_INVALID, "fold_forward: NULL handle");
+  const Sched& s = sh->s;
+  const Packed& p = ph->p;
+  int rc = check_compat(s, p);
+  if (rc != FOLD_OK) return rc;
+  if (s.N > 0 && (!h_pool || !c_pool)) return fail(FOLD_E_INVALID, "fold_forward: NULL pool");
+  if (table_width(s, p) > 0 && s.N > 0) {
+    if (!table) return fail(FOLD_E_INVALID, "fold_forward: leaf table is NULL");
+    if (table_rows < s.num_inputs) return fail(FOLD_E_MISMATCH, "fold_forward: leaf table has fewer rows than the batch names");
+  }
+  return forward_impl(s, p, table, table_rows, h_pool, c_pool, roots_out, ws, ws_bytes, st);
+  FOLD_GUARD_END
+}
+
+int32_t fold_backward(const fold_sched* sh, const fold_packed* ph, const void* table, int64_t table_rows,
+                      const void* h_pool, const float* c_pool, const float* dh_roots, const float* dh_nodes,
+                      const fold_grads* grads, float* dh_out, float* dc_out, void* ws, size_t ws_bytes,
+                      hipStream_t st) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!sh || !ph) return fail(FOLD_E_INVALID, "fold_backward: NULL handle");
+  const Sched& s = sh->s;
+  const Packed& p = ph->p;
+  int rc = check_compat(s, p);
+  if (rc != FOLD_OK) return rc;
+  if (s.N > 0 && (!h_pool || !c_pool)) return fail(FOLD_E_INVALID, "fold_backward: NULL pool");
+  if (grads && grads->num_sets != (int)p.sets.size())
+    return fail(FOLD_E_MISMATCH, "fold_backward: gradient sets differ from parameter sets");
+  if (grads && grads->num_sets > 0 && !grads->sets) return fail(FOLD_E_INVALID, "fold_backward: NULL gradient sets");
+  if (table_width(s, p) > 0 && s.N > 0) {
+    if (!table) return fail(FOLD_E_INVALID, "fold_backward: leaf table is NULL");
+    if (table_rows < s.num_inputs) return fail(FOLD_E_MISMATCH, "fold_backward: leaf table has fewer rows than the batch names");
+  }
+  return backward_impl(s, p, table, table_rows, h_pool, c_pool, dh_roots, dh_nodes, grads, dh_out, dc_out, ws,
+                       ws_bytes, st);
+  FOLD_GUARD_END
+}
+
+}  // extern "C"

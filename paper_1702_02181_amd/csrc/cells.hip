@@ -1,0 +1,443 @@
+// Batched cells of one (depth, op) group, gfx950.
+//
+// Forward (Section 2: gather -> operation -> concat, one launch per group):
+//   a workgroup owns BM pool rows of the group and one block of 32 hidden units.  It gathers the
+//   rows' inputs -- leaf-table rows by input_idx and the children's h rows by child_pos -- into LDS,
+//   contracts them with the packed weights on the matrix cores (all G gate blocks of its 32 units,
+//   so every lane ends up holding i, f, o, u, ... of the same (row, unit)), applies the cell in
+//   registers and writes h, c (and the activations the backward needs) straight into the pools.
+// Backward:
+//   k_cell_bwd  elementwise dz of every row from the saved activations; dc of the children
+//               scatter-added; EMBED rows scatter dh into the leaf-table gradient
+//   k_bwd_dx    dz . W^T on the matrix cores, scatter-added into the children's dh (or into the
+//               leaf-table gradient for the input segment)
+// Cells (gate blocks in column order):
+//   TREELSTM (i|f_l|f_r|o|u): c = i*u + f_l*c_l + f_r*c_r, h = o*tanh(c)   (Tai et al. N-ary, N = 2)
+//   LSTM     (i|f|o|u):       c = i*u + f*c_p,             h = o*tanh(c)
+//   TREERNN / PROJ:           h = tanh(z); PROJ passes the child's c through
+
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+#include "internal.h"
+#include "mfma.h"
+
+namespace fold {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+template <int KIND>
+struct Gates {
+  static constexpr int G = KIND == FOLD_TREELSTM ? 5 : (KIND == FOLD_LSTM ? 4 : 1);
+};
+
+// ---------------------------------------------------------------- forward
+
+template <typename T, int KIND, int MT>
+__global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
+  using M = Mma<T>;
+  constexpr int G = Gates<KIND>::G;
+  constexpr int BK = M::BK, VEC = M::VEC, VPR = BK / VEC, PITCH = BK + M::PAD;
+  constexpr int BM = 4 * 32 * MT;  // four waves stacked along the rows
+  constexpr int BN = G * 32;       // G gate blocks of 32 units
+  __shared__ __attribute__((aligned(16))) T As[BM * PITCH];
+  __shared__ __attribute__((aligned(16))) T Bs[BN * PITCH];
+  __shared__ int srow[BM];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int m0 = blockIdx.x * BM;
+  const int ub = blockIdx.y;  // hidden units ub*32 .. ub*32+31
+  const T* W = static_cast<const T*>(a.Wf) + (size_t)ub * BN * a.Kf;
+
+  f32x16 acc[MT][G];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mt][g][r] = 0.f;
+
+  const int nseg = a.has_input + a.arity;
+  for (int seg = 0; seg < nseg; ++seg) {
+    const bool is_in = a.has_input && seg == 0;
+    const int k = is_in ? 0 : seg - a.has_input;  // child slot
+    const int width = is_in ? a.in_dim : a.H;
+    const int padw = is_in ? a.INP : a.HP;
+    const int kbase = is_in ? 0 : a.INP + k * a.HP;
+    const T* src = is_in ? static_cast<const T*>(a.table) : static_cast<const T*>(a.h_pool);
+    const int sld = is_in ? a.tld : a.ld;
+    __syncthreads();
+    for (int r = tid; r < BM; r += kThreads) {
+      const int row = m0 + r;
+      int sr = -1;
+      if (row < a.rows) sr = is_in ? a.input_idx[a.row_begin + row] : a.child_pos[a.idx_off + row * a.arity + k];
+      srow[r] = sr;
+    }
+    __syncthreads();
+    for (int kc = 0; kc < padw; kc += BK) {
+      for (int i = tid; i < BM * VPR; i += kThreads) {
+        const int r = i / VPR, v = i - r * VPR;
+        const int sr = srow[r];
+        uint4 x = make_uint4(0u, 0u, 0u, 0u);
+        if (sr >= 0) x = load_row_vec<T>(src + (size_t)sr * sld, kc + v * VEC, width);
+        *reinterpret_cast<uint4*>(&As[r * PITCH + v * VEC]) = x;
+      }
+      for (int i = tid; i < BN * VPR; i += kThreads) {
+        const int n = i / VPR, v = i - n * VPR;
+        *reinterpret_cast<uint4*>(&Bs[n * PITCH + v * VEC]) =
+            *reinterpret_cast<const uint4*>(W + (size_t)n * a.Kf + kbase + kc + v * VEC);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int ks = 0; ks < BK; ks += M::KSTEP) {
+        typename M::frag af[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+          af[mt] = M::load(&As[(wave * 32 * MT + mt * 32 + (lane & 31)) * PITCH + ks + (lane >> 5) * M::KPL]);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const typename M::frag bf = M::load(&Bs[(g * 32 + (lane & 31)) * PITCH + ks + (lane >> 5) * M::KPL]);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) acc[mt][g] = M::mma(af[mt], bf, acc[mt][g]);
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  // epilogue: the cell, in registers
+  const int j = ub * 32 + (lane & 31);
+  float bz[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) bz[g] = a.bias[g * a.HP + j];
+  T* hp = static_cast<T*>(a.h_pool);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m0 + wave * 32 * MT + mt * 32 + acc_row(r, lane);
+      if (row >= a.rows) continue;
+      const size_t p = (size_t)(a.row_begin + row);
+      if (j >= a.H) {
+        if (j < a.ld) {
+          hp[p * a.ld + j] = from_f32<T>(0.f);
+          a.c_pool[p * a.ld + j] = 0.f;
+        }
+        continue;
+      }
+      float z[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) z[g] = acc[mt][g][r] + bz[g];
+      float h, c;
+      float* gs = a.gates ? a.gates + p * a.gstride + j : nullptr;
+      if constexpr (KIND == FOLD_TREELSTM) {
+        const float i_ = sigmoidf_(z[0]), fl = sigmoidf_(z[1]), fr = sigmoidf_(z[2]), o = sigmoidf_(z[3]);
+        const float u = tanhf(z[4]);
+        float cl = 0.f, cr = 0.f;
+        if (a.arity == 2) {
+          const int pl = a.child_pos[a.idx_off + row * 2], pr = a.child_pos[a.idx_off + row * 2 + 1];
+          if (pl >= 0) cl = a.c_pool[(size_t)pl * a.ld + j];
+          if (pr >= 0) cr = a.c_pool[(size_t)pr * a.ld + j];
+        }
+        c = i_ * u + fl * cl + fr * cr;
+        h = o * tanhf(c);
+        if (gs) {
+          gs[0] = i_;
+          gs[a.HP] = fl;
+          gs[2 * a.HP] = fr;
+          gs[3 * a.HP] = o;
+          gs[4 * a.HP] = u;
+        }
+      } else if constexpr (KIND == FOLD_LSTM) {
+        const float i_ = sigmoidf_(z[0]), f = sigmoidf_(z[1]), o = sigmoidf_(z[2]);
+        const float u = tanhf(z[3]);
+        const int pc = a.child_pos[a.idx_off + row];
+        const float cp = pc >= 0 ? a.c_pool[(size_t)pc * a.ld + j] : 0.f;
+        c = i_ * u + f * cp;
+        h = o * tanhf(c);
+        if (gs) {
+          gs[0] = i_;
+          gs[a.HP] = f;
+          gs[2 * a.HP] = o;
+          gs[3 * a.HP] = u;
+        }
+      } else {
+        h = tanhf(z[0]);
+        c = 0.f;
+        if constexpr (KIND == FOLD_PROJ) {
+          const int pc = a.child_pos[a.idx_off + row];
+          c = pc >= 0 ? a.c_pool[(size_t)pc * a.ld + j] : 0.f;
+        }
+        if (gs) gs[0] = h;
+      }
+      hp[p * a.ld + j] = from_f32<T>(h);
+      a.c_pool[p * a.ld + j] = c;
+    }
+  }
+}
+
+template <typename T>
+__global__ void k_embed_fwd(int rows, int row_begin, int H, int ld, int tld, const T* table,
+                            const int* input_idx, T* h_pool, float* c_pool) {
+  const int row = blockIdx.x;
+  const size_t p = (size_t)(row_begin + row);
+  const int ti = input_idx[p];
+  for (int j = threadIdx.x; j < ld; j += blockDim.x) {
+    h_pool[p * ld + j] = j < H ? table[(size_t)ti * tld + j] : from_f32<T>(0.f);
+    c_pool[p * ld + j] = 0.f;
+  }
+}
+
+template <typename T>
+__global__ void k_roots(int ld, const int* root_pos, const T* h_pool, T* out) {
+  const int r = blockIdx.x;
+  const size_t p = (size_t)root_pos[r];
+  for (int j = threadIdx.x; j < ld; j += blockDim.x) out[(size_t)r * ld + j] = h_pool[p * ld + j];
+}
+
+// ---------------------------------------------------------------- backward, elementwise
+
+__global__ void k_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* dh_roots,
+                           const int* root_pos, float* dh, float* dc) {
+  const size_t total = (size_t)N * ld;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    dh[i] = dh_nodes ? dh_nodes[i] : 0.f;
+    dc[i] = 0.f;
+  }
+}
+
+// roots are distinct rows, so adding their upstream gradient needs no atomics
+__global__ void k_bwd_roots(int ld, const float* dh_roots, const int* root_pos, float* dh) {
+  const int r = blockIdx.x;
+  const size_t p = (size_t)root_pos[r];
+  for (int j = threadIdx.x; j < ld; j += blockDim.x) dh[p * ld + j] += dh_roots[(size_t)r * ld + j];
+}
+
+template <int KIND>
+__global__ void k_cell_bwd(BwdCellArgs a) {
+  constexpr int G = Gates<KIND>::G;
+  const int row = blockIdx.x;
+  const size_t p = (size_t)(a.row_begin + row);
+  float* gb = a.gates + p * a.gstride;
+  int c0 = -1, c1 = -1;
+  if (a.arity >= 1) c0 = a.child_pos[a.idx_off + row * a.arity];
+  if (a.arity >= 2) c1 = a.child_pos[a.idx_off + row * a.arity + 1];
+  for (int j = threadIdx.x; j < a.HP; j += blockDim.x) {
+    if (j >= a.H) {
+      if constexpr (KIND != FOLD_EMBED) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) gb[g * a.HP + j] = 0.f;
+      }
+      continue;
+    }
+    const float dh = a.dh[p * a.ld + j];
+    if constexpr (KIND == FOLD_EMBED) {
+      if (a.d_table) unsafeAtomicAdd(&a.d_table[(size_t)a.input_idx[p] * a.tld + j], dh);
+    } else if constexpr (KIND == FOLD_TREELSTM) {
+      const float dc = a.dc[p * a.ld + j];
+      const float i_ = gb[j], fl = gb[a.HP + j], fr = gb[2 * a.HP + j], o = gb[3 * a.HP + j], u = gb[4 * a.HP + j];
+      const float tc = tanhf(a.c_pool[p * a.ld + j]);
+      const float cl = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
+      const float cr = c1 >= 0 ? a.c_pool[(size_t)c1 * a.ld + j] : 0.f;
+      const float dct = dc + dh * o * (1.f - tc * tc);
+      gb[j] = dct * u * i_ * (1.f - i_);
+      gb[a.HP + j] = dct * cl * fl * (1.f - fl);
+      gb[2 * a.HP + j] = dct * cr * fr * (1.f - fr);
+      gb[3 * a.HP + j] = dh * tc * o * (1.f - o);
+      gb[4 * a.HP + j] = dct * i_ * (1.f - u * u);
+      if (c0 >= 0) unsafeAtomicAdd(&a.dc[(size_t)c0 * a.ld + j], dct * fl);
+      if (c1 >= 0) unsafeAtomicAdd(&a.dc[(size_t)c1 * a.ld + j], dct * fr);
+    } else if constexpr (KIND == FOLD_LSTM) {
+      const float dc = a.dc[p * a.ld + j];
+      const float i_ = gb[j], f = gb[a.HP + j], o = gb[2 * a.HP + j], u = gb[3 * a.HP + j];
+      const float tc = tanhf(a.c_pool[p * a.ld + j]);
+      const float cp = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
+      const float dct = dc + dh * o * (1.f - tc * tc);
+      gb[j] = dct * u * i_ * (1.f - i_);
+      gb[a.HP + j] = dct * cp * f * (1.f - f);
+      gb[2 * a.HP + j] = dh * tc * o * (1.f - o);
+      gb[3 * a.HP + j] = dct * i_ * (1.f - u * u);
+      if (c0 >= 0) unsafeAtomicAdd(&a.dc[(size_t)c0 * a.ld + j], dct * f);
+    } else {
+      const float h = gb[j];
+      gb[j] = dh * (1.f - h * h);
+      if constexpr (KIND == FOLD_PROJ) {
+        const float dc = a.dc[p * a.ld + j];
+        if (c0 >= 0) unsafeAtomicAdd(&a.dc[(size_t)c0 * a.ld + j], dc);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- backward, dz . W^T
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_bwd_dx(DxArgs a) {
+  using M = Mma<T>;
+  constexpr int BK = M::BK, VEC = M::VEC, VPR = BK / VEC, PITCH = BK + M::PAD;
+  constexpr int BM = 128, BN = 64;  // four waves of 32 rows x 64 columns
+  __shared__ __attribute__((aligned(16))) T As[BM * PITCH];
+  __shared__ __attribute__((aligned(16))) T Bs[BN * PITCH];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const T* W = static_cast<const T*>(a.Wb) + (size_t)n0 * a.Kb;
+  f32x16 acc[2];
+  for (int t = 0; t < 2; ++t)
+    for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
+  for (int kc = 0; kc < a.Kb; kc += BK) {
+    for (int i = tid; i < BM * VPR; i += kThreads) {
+      const int r = i / VPR, v = i - r * VPR, row = m0 + r;
+      uint4 x = make_uint4(0u, 0u, 0u, 0u);
+      if (row < a.rows)
+        x = pack_from_f32<T>(a.dz + (size_t)(a.row_begin + row) * a.gstride + kc + v * VEC, VEC);
+      *reinterpret_cast<uint4*>(&As[r * PITCH + v * VEC]) = x;
+    }
+    for (int i = tid; i < BN * VPR; i += kThreads) {
+      const int n = i / VPR, v = i - n * VPR;
+      *reinterpret_cast<uint4*>(&Bs[n * PITCH + v * VEC]) =
+          *reinterpret_cast<const uint4*>(W + (size_t)n * a.Kb + kc + v * VEC);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < BK; ks += M::KSTEP) {
+      const typename M::frag af = M::load(&As[(wave * 32 + (lane & 31)) * PITCH + ks + (lane >> 5) * M::KPL]);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const typename M::frag bf = M::load(&Bs[(t * 32 + (lane & 31)) * PITCH + ks + (lane >> 5) * M::KPL]);
+        acc[t] = M::mma(af, bf, acc[t]);
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int n = n0 + t * 32 + (lane & 31);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m0 + wave * 32 + acc_row(r, lane);
+      if (row >= a.rows) continue;
+      const float v = acc[t][r];
+      if (a.mode == 0) {
+        const int k = n / a.HP, jin = n - k * a.HP;
+        if (jin >= a.H) continue;
+        const int cp = a.child_pos[a.idx_off + row * a.arity + k];
+        if (cp >= 0) unsafeAtomicAdd(&a.dh[(size_t)cp * a.ld + jin], v);
+      } else {
+        if (n >= a.in_dim) continue;
+        const int ti = a.input_idx[a.row_begin + row];
+        unsafeAtomicAdd(&a.d_table[(size_t)ti * a.tld + n], v);
+      }
+    }
+  }
+}
+
+inline unsigned cdiv(long long a, long long b) { return (unsigned)((a + b - 1) / b); }
+
+template <typename T>
+void cell_fwd_t(int kind, const FwdArgs& a, hipStream_t st) {
+  const int MT = (sizeof(T) == 2 && a.rows > 128) ? 2 : 1;
+  const int BM = 128 * MT;
+  dim3 grid(cdiv(a.rows, BM), a.HP / 32);
+#define FOLD_LAUNCH_FWD(KIND, MTV) \
+  hipLaunchKernelGGL((k_cell_fwd<T, KIND, MTV>), grid, dim3(kThreads), 0, st, a)
+  switch (kind) {
+    case FOLD_TREELSTM:
+      if (MT == 2) FOLD_LAUNCH_FWD(FOLD_TREELSTM, 2); else FOLD_LAUNCH_FWD(FOLD_TREELSTM, 1);
+      break;
+    case FOLD_LSTM:
+      if (MT == 2) FOLD_LAUNCH_FWD(FOLD_LSTM, 2); else FOLD_LAUNCH_FWD(FOLD_LSTM, 1);
+      break;
+    case FOLD_TREERNN:
+      if (MT == 2) FOLD_LAUNCH_FWD(FOLD_TREERNN, 2); else FOLD_LAUNCH_FWD(FOLD_TREERNN, 1);
+      break;
+    case FOLD_PROJ:
+      if (MT == 2) FOLD_LAUNCH_FWD(FOLD_PROJ, 2); else FOLD_LAUNCH_FWD(FOLD_PROJ, 1);
+      break;
+    default:
+      break;
+  }
+#undef FOLD_LAUNCH_FWD
+}
+
+}  // namespace
+
+const char* kind_name(int kind, int dtype) {
+  static const char* n32[] = {"cell_fwd.embed.f32", "cell_fwd.treernn.f32", "cell_fwd.treelstm.f32",
+                              "cell_fwd.lstm.f32", "cell_fwd.proj.f32"};
+  static const char* n16[] = {"cell_fwd.embed.bf16", "cell_fwd.treernn.bf16", "cell_fwd.treelstm.bf16",
+                              "cell_fwd.lstm.bf16", "cell_fwd.proj.bf16"};
+  if (kind < 0 || kind > 4) return "cell_fwd";
+  return dtype == FOLD_BF16 ? n16[kind] : n32[kind];
+}
+
+void launch_cell_fwd(int dtype, int kind, const FwdArgs& a, hipStream_t st) {
+  if (a.rows <= 0) return;
+  ProfScope prof(kind_name(kind, dtype), st);
+  if (dtype == FOLD_BF16)
+    cell_fwd_t<uint16_t>(kind, a, st);
+  else
+    cell_fwd_t<float>(kind, a, st);
+}
+
+void launch_embed_fwd(int dtype, int rows, int row_begin, int H, int ld, int tld, const void* table,
+                      const int* input_idx, void* h_pool, float* c_pool, hipStream_t st) {
+  if (rows <= 0) return;
+  ProfScope prof("embed_fwd", st);
+  if (dtype == FOLD_BF16)
+    hipLaunchKernelGGL(k_embed_fwd<uint16_t>, dim3(rows), dim3(256), 0, st, rows, row_begin, H, ld, tld,
+                       static_cast<const uint16_t*>(table), input_idx, static_cast<uint16_t*>(h_pool), c_pool);
+  else
+    hipLaunchKernelGGL(k_embed_fwd<float>, dim3(rows), dim3(256), 0, st, rows, row_begin, H, ld, tld,
+                       static_cast<const float*>(table), input_idx, static_cast<float*>(h_pool), c_pool);
+}
+
+void launch_roots(int dtype, int R, int ld, const int* root_pos, const void* h_pool, void* out, hipStream_t st) {
+  if (R <= 0) return;
+  ProfScope prof("roots", st);
+  if (dtype == FOLD_BF16)
+    hipLaunchKernelGGL(k_roots<uint16_t>, dim3(R), dim3(256), 0, st, ld, root_pos,
+                       static_cast<const uint16_t*>(h_pool), static_cast<uint16_t*>(out));
+  else
+    hipLaunchKernelGGL(k_roots<float>, dim3(R), dim3(256), 0, st, ld, root_pos, static_cast<const float*>(h_pool),
+                       static_cast<float*>(out));
+}
+
+void launch_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* dh_roots, const int* root_pos,
+                     float* dh, float* dc, hipStream_t st) {
+  if (N <= 0) return;
+  ProfScope prof("bwd_init", st);
+  const size_t total = (size_t)N * ld;
+  const unsigned blocks = (unsigned)std::min<size_t>((total + 255) / 256, 65536);
+  hipLaunchKernelGGL(k_bwd_init, dim3(blocks), dim3(256), 0, st, N, R, ld, dh_nodes, dh_roots, root_pos, dh, dc);
+  if (dh_roots && R > 0) hipLaunchKernelGGL(k_bwd_roots, dim3(R), dim3(256), 0, st, ld, dh_roots, root_pos, dh);
+}
+
+void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
+  if (a.rows <= 0) return;
+  static const char* names[] = {"cell_bwd.embed", "cell_bwd.treernn", "cell_bwd.treelstm", "cell_bwd.lstm",
+                                "cell_bwd.proj"};
+  ProfScope prof(kind >= 0 && kind <= 4 ? names[kind] : "cell_bwd", st);
+  dim3 grid(a.rows), block(256);
+  switch (kind) {
+    case FOLD_EMBED: hipLaunchKernelGGL(k_cell_bwd<FOLD_EMBED>, grid, block, 0, st, a); break;
+    case FOLD_TREERNN: hipLaunchKernelGGL(k_cell_bwd<FOLD_TREERNN>, grid, block, 0, st, a); break;
+    case FOLD_TREELSTM: hipLaunchKernelGGL(k_cell_bwd<FOLD_TREELSTM>, grid, block, 0, st, a); break;
+    case FOLD_LSTM: hipLaunchKernelGGL(k_cell_bwd<FOLD_LSTM>, grid, block, 0, st, a); break;
+    case FOLD_PROJ: hipLaunchKernelGGL(k_cell_bwd<FOLD_PROJ>, grid, block, 0, st, a); break;
+    default: break;
+  }
+}
+
+void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st) {
+  if (a.rows <= 0 || a.Nb <= 0) return;
+  ProfScope prof(dtype == FOLD_BF16 ? "bwd_dx.bf16" : "bwd_dx.f32", st);
+  dim3 grid(cdiv(a.rows, 128), a.Nb / 64);
+  if (dtype == FOLD_BF16)
+    hipLaunchKernelGGL(k_bwd_dx<uint16_t>, grid, dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL(k_bwd_dx<float>, grid, dim3(kThreads), 0, st, a);
+}
+
+}  // namespace fold

@@ -1,0 +1,140 @@
+// Internal definitions shared by the library's HIP sources (gfx950 / CDNA4 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "fold.h"
+
+namespace fold {
+
+// ---------------------------------------------------------------- constants
+
+constexpr int kWave = 64;          // CDNA wavefront
+constexpr int kUnit = 32;          // hidden units per MFMA output tile column block
+constexpr int kPadK = 64;          // every K segment (input width, hidden) is padded to this
+constexpr int kMaxGates = 5;
+
+inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
+inline int64_t round_up64(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+inline int gates_of(int kind) {
+  switch (kind) {
+    case FOLD_TREERNN: return 1;
+    case FOLD_TREELSTM: return 5;
+    case FOLD_LSTM: return 4;
+    case FOLD_PROJ: return 1;
+    default: return 0;
+  }
+}
+
+inline int row_ld(int width) { return round_up(width < 1 ? 1 : width, 8); }
+
+// ---------------------------------------------------------------- error state
+
+void set_error(const std::string& msg);
+void clear_error();
+
+#define FOLD_HIP_CHECK(expr)                                                        \
+  do {                                                                              \
+    hipError_t e_ = (expr);                                                         \
+    if (e_ != hipSuccess) {                                                         \
+      ::fold::set_error(std::string(#expr) + ": " + hipGetErrorString(e_));         \
+      return FOLD_E_DEVICE;                                                         \
+    }                                                                               \
+  } while (0)
+
+// ---------------------------------------------------------------- kernel timing
+
+// Records a HIP event pair around the launches made while it is alive, if profiling is on.
+class ProfScope {
+ public:
+  ProfScope(const char* name, hipStream_t st);
+  ~ProfScope();
+  ProfScope(const ProfScope&) = delete;
+  ProfScope& operator=(const ProfScope&) = delete;
+
+ private:
+  const char* name_;
+  hipStream_t st_;
+  void* start_ = nullptr;
+  void* stop_ = nullptr;
+};
+
+// ---------------------------------------------------------------- handles
+
+struct Sched {
+  int N = 0, E = 0, G = 0, num_ops = 0, D = 0, num_groups = 0, R = 0, max_parents = 0, num_inputs = 0;
+  int device = 0;
+  std::vector<fold_op> ops;
+  // one device allocation holds every int array below
+  void* blob = nullptr;
+  int32_t *depth = nullptr, *node_pos = nullptr, *pos_node = nullptr, *level_ptr = nullptr;
+  int32_t *g_level = nullptr, *g_op = nullptr, *g_row_begin = nullptr, *g_rows = nullptr,
+          *g_idx_off = nullptr;
+  int32_t *child_pos = nullptr, *input_idx = nullptr, *root_pos = nullptr;
+  int32_t *pos_group = nullptr;   // [N] group of every pool row
+  int32_t *op_rows = nullptr;     // [N] pool rows sorted by (op, row)
+  void* blob3 = nullptr;          // level / group table (device copy)
+  std::vector<int32_t> h_level_ptr, h_level, h_op, h_row_begin, h_rows, h_idx_off;
+  std::vector<int32_t> h_op_row_ptr;  // [num_ops + 1] ranges of op_rows
+};
+
+// Packed weights of one parameter set.
+struct PackedSet {
+  int kind = 0, in_dim = 0, arity = 0, G = 0;
+  int INP = 0;        // input segment width padded to kPadK (0 if no W_in)
+  int Kf = 0;         // forward K = INP + arity * HP
+  int Nf = 0;         // forward N = G * HP (gate blocks interleaved per kUnit units)
+  // forward weights, n-major [Nf][Kf] (element type of the params)
+  void* Wf = nullptr;
+  // backward, n-major, K = G * HP in canonical gate-block order:
+  void* Wb_rec = nullptr;  // [arity * HP][G * HP]
+  void* Wb_in = nullptr;   // [INP][G * HP]
+  float* bias = nullptr;   // [G * HP] fp32, zero padded
+};
+
+struct Packed {
+  int dtype = 0, H = 0, HP = 0, ld = 0;
+  int device = 0;
+  std::vector<PackedSet> sets;
+  std::vector<void*> allocs;
+};
+
+}  // namespace fold
+
+struct fold_sched { fold::Sched s; };
+struct fold_packed { fold::Packed p; };
+
+// ---------------------------------------------------------------- device helpers
+namespace fold {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN kept quiet)
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float sigmoidf_(float x) {
+  // 1 / (1 + e^-x), written so that neither branch overflows
+  if (x >= 0.f) {
+    float e = expf(-x);
+    return 1.f / (1.f + e);
+  }
+  float e = expf(x);
+  return e / (1.f + e);
+}
+
+}  // namespace fold

@@ -1,0 +1,119 @@
+// Host-side entry points between the library's translation units.
+#pragma once
+
+#include "common.h"
+
+namespace fold {
+
+int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out);
+void sched_destroy_impl(fold_sched* h);
+
+int32_t pack_impl(const fold_params* p, hipStream_t st, fold_packed** out);
+void packed_destroy_impl(fold_packed* h);
+
+// Workspace layout shared by the forward and backward passes.
+struct WsLayout {
+  int gstride = 0;           // floats per pool row of saved gates / dz: Gmax * HP
+  size_t gates_off = 0, gates_bytes = 0;
+  size_t dh_off = 0, dc_off = 0, acc_bytes = 0;
+  size_t part_off = 0, part_bytes = 0;   // weight-gradient partial tiles
+  size_t bpart_off = 0, bpart_bytes = 0; // bias partial sums
+  size_t fwd_bytes = 0, bwd_bytes = 0;
+};
+WsLayout workspace_layout(const Sched& s, const Packed& p);
+
+// Weight-gradient work split: rows of one op reduced in `nchunk` chunks of `chunk` rows.
+struct WgradSplit {
+  int nchunk = 0, chunk = 0;
+};
+WgradSplit wgrad_split(int count, int Kw, int Nw);
+
+int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, void* h_pool,
+                     float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st);
+int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows,
+                      const void* h_pool, const float* c_pool, const float* dh_roots, const float* dh_nodes,
+                      const fold_grads* grads, float* dh_out, float* dc_out, void* ws, size_t ws_bytes,
+                      hipStream_t st);
+
+// ---- kernel launchers (cells.hip) ----
+struct FwdArgs {
+  int rows, row_begin, idx_off, arity, has_input;
+  int H, HP, ld;
+  int in_dim, INP, tld;
+  int Kf;
+  const void* table;
+  void* h_pool;
+  float* c_pool;
+  const int* child_pos;
+  const int* input_idx;
+  const void* Wf;
+  const float* bias;
+  float* gates;
+  int gstride;
+};
+void launch_cell_fwd(int dtype, int kind, const FwdArgs& a, hipStream_t st);
+void launch_embed_fwd(int dtype, int rows, int row_begin, int H, int ld, int tld, const void* table,
+                      const int* input_idx, void* h_pool, float* c_pool, hipStream_t st);
+void launch_roots(int dtype, int R, int ld, const int* root_pos, const void* h_pool, void* roots_out,
+                  hipStream_t st);
+
+struct BwdCellArgs {
+  int rows, row_begin, idx_off, arity;
+  int H, HP, ld, gstride;
+  const float* c_pool;
+  float* gates;  // saved activations in, dz out
+  const float* dh;
+  float* dc;
+  const int* child_pos;
+  const int* input_idx;
+  float* d_table;
+  int tld;
+};
+void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st);
+void launch_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* dh_roots, const int* root_pos,
+                     float* dh, float* dc, hipStream_t st);
+
+struct DxArgs {
+  int rows, row_begin, idx_off, arity;
+  int H, HP, ld, gstride, Kb, Nb;
+  const float* dz;
+  const void* Wb;
+  int mode;  // 0: scatter into children's dh, 1: into leaf-table rows
+  float* dh;
+  const int* child_pos;
+  float* d_table;
+  const int* input_idx;
+  int in_dim, tld;
+};
+void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st);
+
+// ---- weight gradients (wgrad.hip) ----
+struct WgArgs {
+  const int* op_rows;
+  int count;
+  const int* pos_group;
+  const int* g_row_begin;
+  const int* g_idx_off;
+  int arity;
+  int seg;  // 0: input rows from the leaf table, 1: children's h rows
+  int H, HP, ld, in_dim, tld, gstride;
+  int Kw, Nw;
+  const void* src;
+  const int* child_pos;
+  const int* input_idx;
+  const float* dz;
+  int chunk, nchunk;
+  float* partial;
+};
+void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st);
+void launch_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP, int in_dim,
+                         int G, float* dW, hipStream_t st);
+void launch_bias_grad(const int* op_rows, int count, int chunk, int nchunk, const float* dz, int gstride,
+                      int Nw, float* bpart, int G, int H, int HP, float* dbias, hipStream_t st);
+
+// ---- packing (pack.hip) ----
+void launch_pack(int dtype, int mode, int G, int H, int HP, int in_dim, int INP, int arity, int Kf,
+                 const void* W_in, const void* W_rec, const float* bias, void* dst, size_t count,
+                 hipStream_t st);
+
+}  // namespace fold

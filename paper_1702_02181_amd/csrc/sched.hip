@@ -1,0 +1,733 @@
+// GPU scheduler for dynamic batching (Section 2 of the paper, the greedy
+// scheduling algorithm), gfx950.
+//
+//   validate   CSR structure, op ids, arity, child range / same graph, inputs
+//   depth      one workgroup per graph runs Kahn's algorithm bottom-up over the
+//              graph's reverse edges in LDS: a node whose children are all done
+//              gets depth 1 + max(child depths) (the zero state -1 and leaf-table
+//              rows are depth-0 constants).  Unprocessed nodes mean a cycle.
+//   sort       stable LSD radix sort (8-bit digits) of the node ids by the key
+//              (depth - 1) * num_ops + op: ties stay in node-id order
+//   emit       group table, level_ptr, child_pos (pool rows of every edge),
+//              input_idx and root rows
+// All results are integers and bit-exact by construction.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+
+#include "common.h"
+#include "internal.h"
+
+namespace fold {
+
+namespace {
+
+constexpr unsigned long long kNoErr = ~0ull;
+constexpr int kBlock = 256;
+constexpr int kMaxOps = 64;
+constexpr int kDepthLdsInts = 8192;  // 32 KiB per workgroup; larger graphs use global scratch
+constexpr int kScanItems = 8;        // items per thread in device-wide scans
+constexpr int kScanTile = kBlock * kScanItems;
+constexpr int kRadixItems = 8;
+constexpr int kRadixTile = kBlock * kRadixItems;
+
+struct OpTable {
+  int n;
+  int arity[kMaxOps];
+  int has_input[kMaxOps];
+};
+
+// error word: ((node + 1) << 8) | (-code); structural errors use node + 1 = 0.  atomicMin keeps the
+// lowest node with an error and, within it, the first check in the order op, arity, child, input.
+__device__ __forceinline__ void report(unsigned long long* err, int node_plus_1, int code) {
+  unsigned long long w = ((unsigned long long)(unsigned)node_plus_1 << 8) | (unsigned long long)(-code);
+  atomicMin(err, w);
+}
+
+// ---------------------------------------------------------------- block scan helpers
+
+// exclusive scan of one int per thread over a 256-thread block; returns the prefix, *total = sum
+__device__ int block_exscan_256(int x, int* total) {
+  __shared__ int wsum[kBlock / kWave];
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x / kWave;
+  int v = x;
+  for (int d = 1; d < kWave; d <<= 1) {
+    int y = __shfl_up(v, d, kWave);
+    if (lane >= d) v += y;
+  }
+  if (lane == kWave - 1) wsum[w] = v;
+  __syncthreads();
+  int pre = 0, tot = 0;
+  for (int i = 0; i < kBlock / kWave; ++i) {
+    int s = wsum[i];
+    if (i < w) pre += s;
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return pre + v - x;
+}
+
+// in-place exclusive scan of a[0..n) (generic pointer: LDS or global), a[n] = total
+__device__ void block_exscan_array(int* a, int n) {
+  const int t = threadIdx.x;
+  const int chunk = (n + kBlock - 1) / kBlock;
+  const int lo = min(n, t * chunk), hi = min(n, lo + chunk);
+  int s = 0;
+  for (int i = lo; i < hi; ++i) s += a[i];
+  int tot;
+  int pre = block_exscan_256(s, &tot);
+  __syncthreads();
+  for (int i = lo; i < hi; ++i) {
+    int v = a[i];
+    a[i] = pre;
+    pre += v;
+  }
+  if (t == 0) a[n] = tot;
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------- validation
+
+__global__ void k_check_struct(const int* gp, int G, const int* cp, int N, int E, unsigned long long* err) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) {
+    if (gp[0] != 0 || gp[G] != N || cp[0] != 0 || cp[N] != E) report(err, 0, FOLD_E_INVALID);
+  }
+  if (i < G) {
+    int a = gp[i], b = gp[i + 1];
+    if (a < 0 || b > N || a > b) report(err, 0, FOLD_E_INVALID);
+  }
+  if (i < N) {
+    int a = cp[i], b = cp[i + 1];
+    if (a < 0 || b > E || a > b) report(err, 0, FOLD_E_INVALID);
+  }
+}
+
+__global__ void k_node_graph(const int* gp, int* node_graph, const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int g = blockIdx.x;
+  for (int v = gp[g] + threadIdx.x; v < gp[g + 1]; v += blockDim.x) node_graph[v] = g;
+}
+
+__global__ void k_check_nodes(const int* node_op, const int* cp, const int* ci, const int* node_input,
+                              const int* node_graph, int N, int num_inputs, OpTable ops,
+                              unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= N) return;
+  const int op = node_op[v];
+  if (op < 0 || op >= ops.n) { report(err, v + 1, FOLD_E_OP); return; }
+  const int a = cp[v], b = cp[v + 1];
+  if (b - a != ops.arity[op]) { report(err, v + 1, FOLD_E_ARITY); return; }
+  const int gv = node_graph[v];
+  for (int j = a; j < b; ++j) {
+    int c = ci[j];
+    if (c == -1) continue;
+    if (c < 0 || c >= N || node_graph[c] != gv) { report(err, v + 1, FOLD_E_CHILD); return; }
+  }
+  const int inp = node_input[v];
+  if (ops.has_input[op]) {
+    if (inp < 0 || inp >= num_inputs) report(err, v + 1, FOLD_E_INPUT);
+  } else if (inp != -1) {
+    report(err, v + 1, FOLD_E_INPUT);
+  }
+}
+
+// ---------------------------------------------------------------- depth (one workgroup per graph)
+
+// meta[0] = max depth, meta[1] = max number of parents of a node
+__global__ __launch_bounds__(kBlock) void k_depth(const int* gp, const int* cp, const int* ci, int* depth,
+                                                  int* indeg, int* scratch, unsigned long long* err,
+                                                  int* meta) {
+  if (*err != kNoErr) return;
+  extern __shared__ int lds[];
+  __shared__ int qn[2];
+  const int g = blockIdx.x, t = threadIdx.x;
+  const int g0 = gp[g], n = gp[g + 1] - g0;
+  if (n == 0) return;
+  const int e0 = cp[g0], e = cp[g0 + n] - e0;
+  const long long need = 6LL * n + 1 + e;
+  int* base = (need <= kDepthLdsInts) ? lds : scratch + (6LL * g0 + g + e0);
+  int* pend = base;         // [n] children not yet done
+  int* dep = pend + n;      // [n]
+  int* pptr = dep + n;      // [n+1] parent-list offsets (counts, then exclusive scan)
+  int* pfill = pptr + n + 1;  // [n]
+  int* q0 = pfill + n;      // [n]
+  int* q1 = q0 + n;         // [n]
+  int* plist = q1 + n;      // [e]
+
+  for (int v = t; v < n; v += kBlock) { pptr[v] = 0; pfill[v] = 0; dep[v] = 0; }
+  if (t == 0) { qn[0] = 0; qn[1] = 0; }
+  __syncthreads();
+  for (int v = t; v < n; v += kBlock) {
+    int cnt = 0;
+    for (int j = cp[g0 + v]; j < cp[g0 + v + 1]; ++j) {
+      int c = ci[j];
+      if (c >= 0) { ++cnt; atomicAdd(&pptr[c - g0], 1); }
+    }
+    pend[v] = cnt;
+  }
+  __syncthreads();
+  block_exscan_array(pptr, n);
+  for (int v = t; v < n; v += kBlock) {
+    for (int j = cp[g0 + v]; j < cp[g0 + v + 1]; ++j) {
+      int c = ci[j];
+      if (c >= 0) {
+        int s = atomicAdd(&pfill[c - g0], 1);
+        plist[pptr[c - g0] + s] = v;
+      }
+    }
+  }
+  __syncthreads();
+  int local_maxpar = 0;
+  for (int v = t; v < n; v += kBlock) {
+    indeg[g0 + v] = pfill[v];
+    local_maxpar = max(local_maxpar, pfill[v]);
+    if (pend[v] == 0) {
+      dep[v] = 1;
+      q0[atomicAdd(&qn[0], 1)] = v;
+    }
+  }
+  __syncthreads();
+  int processed = 0, cur = 0;
+  while (true) {
+    const int cnt = qn[cur];
+    if (cnt == 0) break;
+    processed += cnt;
+    int* Q = cur ? q1 : q0;
+    int* NQ = cur ? q0 : q1;
+    for (int i = t; i < cnt; i += kBlock) {
+      const int v = Q[i];
+      const int dv = dep[v] + 1;
+      for (int k = pptr[v]; k < pptr[v + 1]; ++k) {
+        const int p = plist[k];
+        atomicMax(&dep[p], dv);
+        if (atomicSub(&pend[p], 1) == 1) NQ[atomicAdd(&qn[cur ^ 1], 1)] = p;
+      }
+    }
+    __syncthreads();
+    if (t == 0) qn[cur] = 0;
+    __syncthreads();
+    cur ^= 1;
+  }
+  if (processed < n) {
+    if (t == 0) report(err, g0 + 1, FOLD_E_CYCLE);
+    return;
+  }
+  int local_max = 0;
+  for (int v = t; v < n; v += kBlock) {
+    depth[g0 + v] = dep[v];
+    local_max = max(local_max, dep[v]);
+  }
+  atomicMax(&meta[0], local_max);
+  atomicMax(&meta[1], local_maxpar);
+}
+
+// ---------------------------------------------------------------- device-wide exclusive scan
+
+__global__ void k_scan_reduce(const int* in, int n, int* partial) {
+  const int b = blockIdx.x, t = threadIdx.x;
+  const long long base = (long long)b * kScanTile + (long long)t * kScanItems;
+  int s = 0;
+  for (int i = 0; i < kScanItems; ++i) {
+    long long j = base + i;
+    if (j < n) s += in[j];
+  }
+  int tot;
+  block_exscan_256(s, &tot);
+  if (t == 0) partial[b] = tot;
+}
+
+// single block: exclusive scan of partial[0..nb) in place, *total = sum
+__global__ void k_scan_partials(int* partial, int nb, int* total) {
+  int carry = 0;
+  for (int base = 0; base < nb; base += kBlock) {
+    const int i = base + threadIdx.x;
+    const int x = i < nb ? partial[i] : 0;
+    int tot;
+    const int pre = block_exscan_256(x, &tot);
+    if (i < nb) partial[i] = carry + pre;
+    carry += tot;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *total = carry;
+}
+
+__global__ void k_scan_down(const int* in, int n, const int* partial, int* out) {
+  const int b = blockIdx.x, t = threadIdx.x;
+  const long long base = (long long)b * kScanTile + (long long)t * kScanItems;
+  int v[kScanItems];
+  int s = 0;
+  for (int i = 0; i < kScanItems; ++i) {
+    long long j = base + i;
+    v[i] = j < n ? in[j] : 0;
+    s += v[i];
+  }
+  int tot;
+  int pre = block_exscan_256(s, &tot) + partial[b];
+  for (int i = 0; i < kScanItems; ++i) {
+    long long j = base + i;
+    if (j < n) out[j] = pre;
+    pre += v[i];
+  }
+}
+
+// exclusive scan in -> out (may alias), total -> *total (device); temp holds >= ceil(n / tile) ints
+void scan_exclusive(const int* in, int* out, int n, int* total, int* temp, hipStream_t st) {
+  const int nb = std::max(1, (n + kScanTile - 1) / kScanTile);
+  hipLaunchKernelGGL(k_scan_reduce, dim3(nb), dim3(kBlock), 0, st, in, n, temp);
+  hipLaunchKernelGGL(k_scan_partials, dim3(1), dim3(kBlock), 0, st, temp, nb, total);
+  hipLaunchKernelGGL(k_scan_down, dim3(nb), dim3(kBlock), 0, st, in, n, temp, out);
+}
+
+// ---------------------------------------------------------------- stable LSD radix sort
+
+__global__ void k_make_keys(const int* depth, const int* node_op, int N, int num_ops, unsigned* keys,
+                            int* vals) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= N) return;
+  keys[v] = (unsigned)((depth[v] - 1) * num_ops + node_op[v]);
+  vals[v] = v;
+}
+
+// counts[d * B + b] = number of items of tile b whose digit is d
+__global__ void k_radix_count(const unsigned* keys, int n, int shift, int* counts, int B) {
+  __shared__ int hist[256];
+  const int b = blockIdx.x, t = threadIdx.x;
+  hist[t] = 0;
+  __syncthreads();
+  const long long base = (long long)b * kRadixTile;
+  for (int r = 0; r < kRadixItems; ++r) {
+    long long i = base + (long long)r * kBlock + t;
+    if (i < n) atomicAdd(&hist[(keys[i] >> shift) & 255u], 1);
+  }
+  __syncthreads();
+  counts[t * B + b] = hist[t];
+}
+
+// Scatter in tile order.  Items of a round are ranked among equal digits by a wave-level match
+// (one ballot per digit bit) plus the counts of earlier waves; rounds go in item order, so the
+// scatter is stable.
+__global__ __launch_bounds__(kBlock) void k_radix_scatter(const unsigned* keys_in, const int* vals_in,
+                                                          unsigned* keys_out, int* vals_out,
+                                                          const int* offsets, int n, int shift, int B) {
+  __shared__ int base[256];
+  __shared__ int wcnt[kBlock / kWave][256];
+  const int b = blockIdx.x, t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  base[t] = offsets[t * B + b];
+  for (int i = 0; i < kBlock / kWave; ++i) wcnt[i][t] = 0;
+  __syncthreads();
+  const long long start = (long long)b * kRadixTile;
+  const unsigned long long lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int r = 0; r < kRadixItems; ++r) {
+    const long long i = start + (long long)r * kBlock + t;
+    const bool valid = i < n;
+    const unsigned k = valid ? keys_in[i] : 0u;
+    const int d = valid ? (int)((k >> shift) & 255u) : 256;  // 256 marks padding
+    unsigned long long m = ~0ull;
+    for (int bit = 0; bit < 9; ++bit) {
+      const int on = (d >> bit) & 1;
+      const unsigned long long bal = __ballot(on);
+      m &= on ? bal : ~bal;
+    }
+    const int lrank = __popcll(m & lt_mask);
+    if (valid && lrank == 0) wcnt[w][d] = __popcll(m);
+    __syncthreads();
+    if (valid) {
+      int pre = 0;
+      for (int j = 0; j < w; ++j) pre += wcnt[j][d];
+      const int pos = base[d] + pre + lrank;
+      keys_out[pos] = k;
+      vals_out[pos] = vals_in[i];
+    }
+    __syncthreads();
+    int tot = 0;
+    for (int j = 0; j < kBlock / kWave; ++j) { tot += wcnt[j][t]; wcnt[j][t] = 0; }
+    base[t] += tot;
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------- emission
+
+__global__ void k_post_sort(const unsigned* keys, const int* vals, int N, int num_ops, int* pos_node,
+                            int* node_pos, int* flag, int* level_ptr) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= N) return;
+  const int v = vals[p];
+  pos_node[p] = v;
+  node_pos[v] = p;
+  const unsigned k = keys[p];
+  const bool start = (p == 0) || (keys[p - 1] != k);
+  flag[p] = start ? 1 : 0;
+  const int lvl = (int)(k / (unsigned)num_ops) + 1;
+  if (p == 0 || (int)(keys[p - 1] / (unsigned)num_ops) + 1 != lvl) level_ptr[lvl - 1] = p;
+  if (p == N - 1) level_ptr[lvl] = N;
+}
+
+__global__ void k_group_starts(const unsigned* keys, const int* flag, const int* exs, int N, int num_ops,
+                               int* gid, int* g_level, int* g_op, int* g_row_begin) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= N) return;
+  const int g = exs[p] + flag[p] - 1;
+  gid[p] = g;
+  if (flag[p]) {
+    g_row_begin[g] = p;
+    g_level[g] = (int)(keys[p] / (unsigned)num_ops) + 1;
+    g_op[g] = (int)(keys[p] % (unsigned)num_ops);
+  }
+}
+
+// ng = number of groups (device); rows and rows * arity of each group
+__global__ void k_group_rows(const int* ng_ptr, int N, const int* g_row_begin, const int* g_op, OpTable ops,
+                             int* g_rows, int* g_edges) {
+  const int g = blockIdx.x * blockDim.x + threadIdx.x;
+  const int ng = *ng_ptr;
+  if (g >= ng) {
+    g_edges[g] = 0;
+    return;
+  }
+  const int end = (g + 1 < ng) ? g_row_begin[g + 1] : N;
+  const int rows = end - g_row_begin[g];
+  g_rows[g] = rows;
+  g_edges[g] = rows * ops.arity[g_op[g]];
+}
+
+__global__ void k_emit(const int* pos_node, const int* node_pos, const int* gid, const int* g_row_begin,
+                       const int* g_op, const int* g_idx_off, const int* cp, const int* ci,
+                       const int* node_input, int N, OpTable ops, int* child_pos, int* input_idx) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= N) return;
+  const int v = pos_node[p];
+  const int g = gid[p];
+  const int a = ops.arity[g_op[g]];
+  const int off = g_idx_off[g] + (p - g_row_begin[g]) * a;
+  const int c0 = cp[v];
+  for (int k = 0; k < a; ++k) {
+    const int c = ci[c0 + k];
+    child_pos[off + k] = c >= 0 ? node_pos[c] : -1;
+  }
+  input_idx[p] = node_input[v];
+}
+
+__global__ void k_root_flags(const int* indeg, int N, int* flag) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v < N) flag[v] = indeg[v] == 0 ? 1 : 0;
+}
+
+__global__ void k_root_emit(const int* flag, const int* rank, const int* node_pos, int N, int* root_pos) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v < N && flag[v]) root_pos[rank[v]] = node_pos[v];
+}
+
+__global__ void k_op_rows(const int* pos_group, const int* g_row_begin, const int* g_oprow, int N,
+                          int* op_rows) {
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= N) return;
+  const int g = pos_group[p];
+  op_rows[g_oprow[g] + (p - g_row_begin[g])] = p;
+}
+
+inline dim3 grid_for(long long n) { return dim3((unsigned)std::max(1LL, (n + kBlock - 1) / kBlock)); }
+
+// stream-ordered temporaries, freed at scope exit
+struct Temp {
+  hipStream_t st;
+  std::vector<void*> ptrs;
+  explicit Temp(hipStream_t s) : st(s) {}
+  ~Temp() {
+    for (void* p : ptrs) (void)hipFreeAsync(p, st);
+  }
+  template <class T>
+  hipError_t alloc(T** p, size_t count) {
+    void* q = nullptr;
+    hipError_t e = hipMallocAsync(&q, std::max<size_t>(count, 1) * sizeof(T), st);
+    if (e == hipSuccess) {
+      ptrs.push_back(q);
+      *p = static_cast<T*>(q);
+    }
+    return e;
+  }
+};
+
+int decode_error(unsigned long long w, std::string* msg) {
+  const int code = -(int)(w & 0xffull);
+  const long long node = (long long)(w >> 8) - 1;
+  const char* what = "invalid batch";
+  switch (code) {
+    case FOLD_E_INVALID: what = "graph_ptr / child_ptr malformed"; break;
+    case FOLD_E_OP: what = "node_op out of range"; break;
+    case FOLD_E_ARITY: what = "child count differs from the operation's arity"; break;
+    case FOLD_E_CHILD: what = "child out of range or in another graph"; break;
+    case FOLD_E_INPUT: what = "node_input inconsistent with has_input or out of range"; break;
+    case FOLD_E_CYCLE: what = "graph contains a cycle"; break;
+    default: break;
+  }
+  *msg = std::string("fold_schedule: ") + what + (node >= 0 ? " (node " + std::to_string(node) + ")" : "");
+  return code;
+}
+
+void init_pool_once(int device) {
+  static bool done[64] = {false};
+  if (device < 0 || device >= 64 || done[device]) return;
+  hipMemPool_t pool;
+  if (hipDeviceGetDefaultMemPool(&pool, device) == hipSuccess) {
+    uint64_t thr = ~0ull;
+    (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+  }
+  done[device] = true;
+}
+
+}  // namespace
+
+void sched_destroy_impl(fold_sched* h);
+static void sched_destroy(fold_sched* h) { sched_destroy_impl(h); }
+
+int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
+  const int N = b->num_nodes, E = b->num_edges, G = b->num_graphs, K = b->num_ops;
+  if (K > kMaxOps) {
+    set_error("fold_schedule: at most 64 operations are supported");
+    return FOLD_E_INVALID;
+  }
+  OpTable ops{};
+  ops.n = K;
+  for (int i = 0; i < K; ++i) {
+    ops.arity[i] = b->ops[i].arity;
+    ops.has_input[i] = b->ops[i].has_input;
+  }
+  int device = 0;
+  FOLD_HIP_CHECK(hipGetDevice(&device));
+  init_pool_once(device);
+
+  auto* h = new fold_sched();
+  Sched& s = h->s;
+  s.N = N; s.E = E; s.G = G; s.num_ops = K; s.device = device; s.num_inputs = b->num_inputs;
+  s.ops.assign(b->ops, b->ops + K);
+  auto fail = [&](int code) {
+    sched_destroy(h);
+    return code;
+  };
+
+  // persistent arrays sized by N and E
+  const size_t n1 = (size_t)N * 7 + (size_t)E + 8;
+  if (hipMalloc(&s.blob, n1 * sizeof(int)) != hipSuccess) {
+    set_error("fold_schedule: out of device memory");
+    return fail(FOLD_E_NOMEM);
+  }
+  int* q = static_cast<int*>(s.blob);
+  s.depth = q; q += N;
+  s.node_pos = q; q += N;
+  s.pos_node = q; q += N;
+  s.input_idx = q; q += N;
+  s.root_pos = q; q += N;
+  s.child_pos = q; q += E;
+  s.pos_group = q; q += N;
+  s.op_rows = q; q += N;
+
+  Temp tmp(st);
+  unsigned long long* err = nullptr;
+  int* meta = nullptr;       // [0] max depth, [1] max parents, [2] num groups, [3] num roots
+  int* node_graph = nullptr;
+  int* indeg = nullptr;
+  int* scratch = nullptr;
+  const long long scratch_ints = 6LL * N + G + E + 1;
+  if (tmp.alloc(&err, 1) || tmp.alloc(&meta, 4) || tmp.alloc(&node_graph, N) || tmp.alloc(&indeg, N) ||
+      tmp.alloc(&scratch, (size_t)scratch_ints)) {
+    set_error("fold_schedule: out of device memory (temporaries)");
+    return fail(FOLD_E_NOMEM);
+  }
+  if (hipMemsetAsync(err, 0xff, sizeof(unsigned long long), st) != hipSuccess ||
+      hipMemsetAsync(meta, 0, 4 * sizeof(int), st) != hipSuccess) {
+    set_error("fold_schedule: hipMemsetAsync failed");
+    return fail(FOLD_E_DEVICE);
+  }
+  hipLaunchKernelGGL(k_check_struct, grid_for(std::max(G + 1, N + 1)), dim3(kBlock), 0, st, b->graph_ptr, G,
+                     b->child_ptr, N, E, err);
+  if (G > 0)
+    hipLaunchKernelGGL(k_node_graph, dim3(G), dim3(kBlock), 0, st, b->graph_ptr, node_graph, err);
+  if (N > 0) {
+    hipLaunchKernelGGL(k_check_nodes, grid_for(N), dim3(kBlock), 0, st, b->node_op, b->child_ptr,
+                       b->child_idx, b->node_input, node_graph, N, b->num_inputs, ops, err);
+  }
+  if (G > 0)
+    hipLaunchKernelGGL(k_depth, dim3(G), dim3(kBlock), kDepthLdsInts * sizeof(int), st, b->graph_ptr,
+                       b->child_ptr, b->child_idx, s.depth, indeg, scratch, err, meta);
+  if (hipGetLastError() != hipSuccess) {
+    set_error("fold_schedule: kernel launch failed");
+    return fail(FOLD_E_DEVICE);
+  }
+  struct {
+    unsigned long long err;
+    int meta[4];
+  } hb{};
+  if (hipMemcpyAsync(&hb.err, err, sizeof(hb.err), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipMemcpyAsync(hb.meta, meta, sizeof(hb.meta), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess) {
+    set_error("fold_schedule: device error while validating");
+    return fail(FOLD_E_DEVICE);
+  }
+  if (hb.err != kNoErr) {
+    std::string msg;
+    int code = decode_error(hb.err, &msg);
+    set_error(msg);
+    return fail(code);
+  }
+  const int D = (N > 0) ? hb.meta[0] : 0;
+  s.D = D;
+  s.max_parents = hb.meta[1];
+
+  // level / group table (sized by D), laid out contiguously for one read-back
+  const long long cap = std::max(1LL, (long long)D * K);
+  if (cap > (1LL << 30)) {
+    set_error("fold_schedule: depth * num_ops too large");
+    return fail(FOLD_E_INVALID);
+  }
+  const size_t n2 = 4 + (size_t)(D + 1) + 6 * (size_t)cap;
+  int* blob2 = nullptr;
+  if (tmp.alloc(&blob2, n2)) {
+    set_error("fold_schedule: out of device memory");
+    return fail(FOLD_E_NOMEM);
+  }
+  int* m2 = blob2;  // [0] num groups, [1] num roots
+  int* d_level_ptr = m2 + 4;
+  int* d_level = d_level_ptr + (D + 1);
+  int* d_op = d_level + cap;
+  int* d_row_begin = d_op + cap;
+  int* d_rows = d_row_begin + cap;
+  int* d_idx_off = d_rows + cap;
+  int* d_edges = d_idx_off + cap;
+
+  if (N > 0) {
+    unsigned *ka, *kb;
+    int *va, *vb, *flag, *exs, *radix_counts, *scan_tmp;
+    int* gid = s.pos_group;
+    const int B = (N + kRadixTile - 1) / kRadixTile;
+    const long long rc = 256LL * B;
+    const long long scan_tmp_n = std::max<long long>(rc, N) / kScanTile + 2;
+    if (tmp.alloc(&ka, N) || tmp.alloc(&kb, N) || tmp.alloc(&va, N) || tmp.alloc(&vb, N) ||
+        tmp.alloc(&flag, N) || tmp.alloc(&exs, N) || tmp.alloc(&radix_counts, rc) ||
+        tmp.alloc(&scan_tmp, scan_tmp_n)) {
+      set_error("fold_schedule: out of device memory (sort)");
+      return fail(FOLD_E_NOMEM);
+    }
+    hipLaunchKernelGGL(k_make_keys, grid_for(N), dim3(kBlock), 0, st, s.depth, b->node_op, N, K, ka, va);
+    const unsigned long long max_key = (unsigned long long)D * K - 1;
+    int bits = 1;
+    while (bits < 32 && (max_key >> bits)) ++bits;
+    const int passes = (bits + 7) / 8;
+    for (int ps = 0; ps < passes; ++ps) {
+      const int shift = 8 * ps;
+      hipLaunchKernelGGL(k_radix_count, dim3(B), dim3(kBlock), 0, st, ka, N, shift, radix_counts, B);
+      scan_exclusive(radix_counts, radix_counts, (int)rc, meta + 2, scan_tmp, st);
+      hipLaunchKernelGGL(k_radix_scatter, dim3(B), dim3(kBlock), 0, st, ka, va, kb, vb, radix_counts, N,
+                         shift, B);
+      std::swap(ka, kb);
+      std::swap(va, vb);
+    }
+    hipLaunchKernelGGL(k_post_sort, grid_for(N), dim3(kBlock), 0, st, ka, va, N, K, s.pos_node, s.node_pos,
+                       flag, d_level_ptr);
+    scan_exclusive(flag, exs, N, m2 + 0, scan_tmp, st);
+    hipLaunchKernelGGL(k_group_starts, grid_for(N), dim3(kBlock), 0, st, ka, flag, exs, N, K, gid, d_level,
+                       d_op, d_row_begin);
+    hipLaunchKernelGGL(k_group_rows, grid_for(cap), dim3(kBlock), 0, st, m2 + 0, N, d_row_begin, d_op, ops,
+                       d_rows, d_edges);
+    // idx_off = exclusive scan of rows * arity over the groups (entries past num_groups are unused)
+    scan_exclusive(d_edges, d_idx_off, (int)cap, m2 + 2, scan_tmp, st);
+    hipLaunchKernelGGL(k_emit, grid_for(N), dim3(kBlock), 0, st, s.pos_node, s.node_pos, gid, d_row_begin,
+                       d_op, d_idx_off, b->child_ptr, b->child_idx, b->node_input, N, ops, s.child_pos,
+                       s.input_idx);
+    hipLaunchKernelGGL(k_root_flags, grid_for(N), dim3(kBlock), 0, st, indeg, N, flag);
+    scan_exclusive(flag, exs, N, m2 + 1, scan_tmp, st);
+    hipLaunchKernelGGL(k_root_emit, grid_for(N), dim3(kBlock), 0, st, flag, exs, s.node_pos, N, s.root_pos);
+    if (hipGetLastError() != hipSuccess) {
+      set_error("fold_schedule: kernel launch failed");
+      return fail(FOLD_E_DEVICE);
+    }
+  }
+  std::vector<int> hbuf(n2, 0);
+  if (N > 0) {
+    if (hipMemcpyAsync(hbuf.data(), blob2, n2 * sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess) {
+      set_error("fold_schedule: device error while scheduling");
+      return fail(FOLD_E_DEVICE);
+    }
+  }
+  const int ng = N > 0 ? hbuf[0] : 0;
+  s.num_groups = ng;
+  s.R = N > 0 ? hbuf[1] : 0;
+  const int* hl = hbuf.data() + 4;
+  s.h_level_ptr.assign(hl, hl + D + 1);
+  const int* hg = hl + (D + 1);
+  s.h_level.assign(hg, hg + ng);
+  s.h_op.assign(hg + cap, hg + cap + ng);
+  s.h_row_begin.assign(hg + 2 * cap, hg + 2 * cap + ng);
+  s.h_rows.assign(hg + 3 * cap, hg + 3 * cap + ng);
+  s.h_idx_off.assign(hg + 4 * cap, hg + 4 * cap + ng);
+  if (N == 0) s.h_level_ptr.assign(1, 0);
+
+  // rows of every op in (op, row) order: per-group offsets into op_rows
+  const int ngc = std::max(ng, 1);
+  std::vector<int> oprow_off(ngc, 0);
+  s.h_op_row_ptr.assign(K + 1, 0);
+  for (int g = 0; g < ng; ++g) s.h_op_row_ptr[s.h_op[g] + 1] += s.h_rows[g];
+  for (int o = 0; o < K; ++o) s.h_op_row_ptr[o + 1] += s.h_op_row_ptr[o];
+  {
+    std::vector<int> fillp(s.h_op_row_ptr.begin(), s.h_op_row_ptr.end() - 1);
+    for (int g = 0; g < ng; ++g) {
+      oprow_off[g] = fillp[s.h_op[g]];
+      fillp[s.h_op[g]] += s.h_rows[g];
+    }
+  }
+
+  // compact device copy of the level / group table owned by the schedule
+  const size_t n3 = (size_t)(D + 1) + 6 * (size_t)ngc;
+  void* blob3 = nullptr;
+  if (hipMalloc(&blob3, n3 * sizeof(int)) != hipSuccess) {
+    set_error("fold_schedule: out of device memory");
+    return fail(FOLD_E_NOMEM);
+  }
+  s.blob3 = blob3;
+  std::vector<int> pack(n3, 0);
+  std::copy(s.h_level_ptr.begin(), s.h_level_ptr.end(), pack.begin());
+  int* pp = pack.data() + (D + 1);
+  std::copy(s.h_level.begin(), s.h_level.end(), pp);
+  std::copy(s.h_op.begin(), s.h_op.end(), pp + ngc);
+  std::copy(s.h_row_begin.begin(), s.h_row_begin.end(), pp + 2 * ngc);
+  std::copy(s.h_rows.begin(), s.h_rows.end(), pp + 3 * ngc);
+  std::copy(s.h_idx_off.begin(), s.h_idx_off.end(), pp + 4 * ngc);
+  std::copy(oprow_off.begin(), oprow_off.end(), pp + 5 * ngc);
+  if (hipMemcpy(blob3, pack.data(), n3 * sizeof(int), hipMemcpyHostToDevice) != hipSuccess) {
+    set_error("fold_schedule: copy of the group table failed");
+    return fail(FOLD_E_DEVICE);
+  }
+  int* b3 = static_cast<int*>(blob3);
+  s.level_ptr = b3;
+  s.g_level = b3 + (D + 1);
+  s.g_op = s.g_level + ngc;
+  s.g_row_begin = s.g_op + ngc;
+  s.g_rows = s.g_row_begin + ngc;
+  s.g_idx_off = s.g_rows + ngc;
+  const int* g_oprow = s.g_idx_off + ngc;
+  if (N > 0) {
+    hipLaunchKernelGGL(k_op_rows, grid_for(N), dim3(kBlock), 0, st, s.pos_group, s.g_row_begin, g_oprow, N,
+                       s.op_rows);
+    if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess) {
+      set_error("fold_schedule: device error while listing rows per op");
+      return fail(FOLD_E_DEVICE);
+    }
+  }
+  *out = h;
+  return FOLD_OK;
+}
+
+void sched_destroy_impl(fold_sched* h) {
+  if (!h) return;
+  if (h->s.blob) (void)hipFree(h->s.blob);
+  if (h->s.blob3) (void)hipFree(h->s.blob3);
+  delete h;
+}
+
+}  // namespace fold

@@ -1,0 +1,332 @@
+"""Thin Python binding of the C ABI in ``include/fold.h`` (ctypes).
+
+Argument marshalling only: every step of the hot path runs in the HIP library.
+PyTorch provides device memory (``tensor.data_ptr()``) and streams
+(``torch.cuda.current_stream().cuda_stream``).  If ``libfold.so`` is missing the
+binding raises -- there is no fallback.
+
+The functions keep the ABI's names:
+    fold_schedule, fold_sched_get_info, fold_sched_free,
+    fold_pack_params, fold_packed_free, fold_workspace_size,
+    fold_forward, fold_backward, fold_row_ld, fold_last_error
+``Batch`` / ``Schedule`` / ``Packed`` / ``Run`` wrap them for tensors.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, byref, c_int32, c_int64, c_size_t, c_void_p
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfold.so")
+
+FOLD_OK = 0
+ERRORS = {-1: "FOLD_E_INVALID", -2: "FOLD_E_OP", -3: "FOLD_E_ARITY", -4: "FOLD_E_CHILD",
+          -5: "FOLD_E_INPUT", -6: "FOLD_E_CYCLE", -7: "FOLD_E_NOMEM", -8: "FOLD_E_DEVICE",
+          -9: "FOLD_E_MISMATCH"}
+FOLD_EMBED, FOLD_TREERNN, FOLD_TREELSTM, FOLD_LSTM, FOLD_PROJ = 0, 1, 2, 3, 4
+FOLD_F32, FOLD_BF16 = 0, 1
+GATES = {FOLD_EMBED: 0, FOLD_TREERNN: 1, FOLD_TREELSTM: 5, FOLD_LSTM: 4, FOLD_PROJ: 1}
+
+
+class fold_op(ctypes.Structure):
+    _fields_ = [("kind", c_int32), ("arity", c_int32), ("has_input", c_int32), ("param_set", c_int32)]
+
+
+class fold_batch(ctypes.Structure):
+    _fields_ = [("num_graphs", c_int32), ("num_nodes", c_int32), ("num_edges", c_int32),
+                ("num_ops", c_int32), ("num_inputs", c_int32),
+                ("graph_ptr", c_void_p), ("node_op", c_void_p), ("child_ptr", c_void_p),
+                ("child_idx", c_void_p), ("node_input", c_void_p), ("ops", POINTER(fold_op))]
+
+
+_I32P = c_void_p
+
+
+class fold_sched_info(ctypes.Structure):
+    _fields_ = [("num_nodes", c_int32), ("num_edges", c_int32), ("num_graphs", c_int32),
+                ("num_ops", c_int32), ("num_levels", c_int32), ("num_groups", c_int32),
+                ("num_roots", c_int32), ("max_parents", c_int32),
+                ("depth", _I32P), ("node_pos", _I32P), ("pos_node", _I32P), ("level_ptr", _I32P),
+                ("group_level", _I32P), ("group_op", _I32P), ("group_row_begin", _I32P),
+                ("group_rows", _I32P), ("group_idx_off", _I32P), ("child_pos", _I32P),
+                ("input_idx", _I32P), ("root_pos", _I32P),
+                ("h_level_ptr", POINTER(c_int32)), ("h_group_level", POINTER(c_int32)),
+                ("h_group_op", POINTER(c_int32)), ("h_group_row_begin", POINTER(c_int32)),
+                ("h_group_rows", POINTER(c_int32)), ("h_group_idx_off", POINTER(c_int32))]
+
+
+class fold_param_set(ctypes.Structure):
+    _fields_ = [("kind", c_int32), ("in_dim", c_int32), ("arity", c_int32),
+                ("W_in", c_void_p), ("W_rec", c_void_p), ("bias", c_void_p)]
+
+
+class fold_params(ctypes.Structure):
+    _fields_ = [("dtype", c_int32), ("hidden", c_int32), ("num_sets", c_int32),
+                ("sets", POINTER(fold_param_set))]
+
+
+class fold_param_grads(ctypes.Structure):
+    _fields_ = [("dW_in", c_void_p), ("dW_rec", c_void_p), ("dbias", c_void_p)]
+
+
+class fold_grads(ctypes.Structure):
+    _fields_ = [("num_sets", c_int32), ("sets", POINTER(fold_param_grads)), ("d_leaf_table", c_void_p)]
+
+
+class fold_kernel_stat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("launches", c_int64), ("total_ms", ctypes.c_double),
+                ("max_ms", ctypes.c_double)]
+
+
+class FoldError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+EXPORTS = ["fold_schedule", "fold_sched_get_info", "fold_sched_free", "fold_pack_params",
+           "fold_packed_free", "fold_row_ld", "fold_workspace_size", "fold_forward",
+           "fold_backward", "fold_last_error", "fold_profile_enable", "fold_profile_read"]
+
+_lib = None
+
+
+def lib():
+    """Load libfold.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_1702_02181_amd.build_lib.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    L.fold_last_error.restype = ctypes.c_char_p
+    L.fold_last_error.argtypes = []
+    L.fold_row_ld.restype = c_int32
+    L.fold_row_ld.argtypes = [c_int32]
+    L.fold_schedule.restype = c_int32
+    L.fold_schedule.argtypes = [POINTER(fold_batch), c_void_p, POINTER(c_void_p)]
+    L.fold_sched_get_info.restype = c_int32
+    L.fold_sched_get_info.argtypes = [c_void_p, POINTER(fold_sched_info)]
+    L.fold_sched_free.restype = c_int32
+    L.fold_sched_free.argtypes = [c_void_p]
+    L.fold_pack_params.restype = c_int32
+    L.fold_pack_params.argtypes = [POINTER(fold_params), c_void_p, POINTER(c_void_p)]
+    L.fold_packed_free.restype = c_int32
+    L.fold_packed_free.argtypes = [c_void_p]
+    L.fold_workspace_size.restype = c_int32
+    L.fold_workspace_size.argtypes = [c_void_p, c_void_p, POINTER(c_size_t), POINTER(c_size_t)]
+    L.fold_forward.restype = c_int32
+    L.fold_forward.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,
+                               c_void_p, c_size_t, c_void_p]
+    L.fold_backward.restype = c_int32
+    L.fold_backward.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,
+                                c_void_p, POINTER(fold_grads), c_void_p, c_void_p, c_void_p, c_size_t,
+                                c_void_p]
+    L.fold_profile_enable.restype = c_int32
+    L.fold_profile_enable.argtypes = [c_int32]
+    L.fold_profile_read.restype = c_int32
+    L.fold_profile_read.argtypes = [POINTER(fold_kernel_stat), c_int32, POINTER(c_int32)]
+    _lib = L
+    return L
+
+
+def _check(rc: int):
+    if rc != FOLD_OK:
+        raise FoldError(rc, lib().fold_last_error().decode())
+
+
+def fold_last_error() -> str:
+    return lib().fold_last_error().decode()
+
+
+def fold_profile_enable(on: bool):
+    _check(lib().fold_profile_enable(1 if on else 0))
+
+
+def fold_profile_read() -> dict:
+    """{kernel class: (launches, total_ms, max_ms)}; waits for the recorded events and clears them."""
+    cap = 128
+    arr = (fold_kernel_stat * cap)()
+    n = c_int32()
+    _check(lib().fold_profile_read(arr, cap, byref(n)))
+    return {arr[i].name.decode(): (int(arr[i].launches), float(arr[i].total_ms), float(arr[i].max_ms))
+            for i in range(min(n.value, cap))}
+
+
+def fold_row_ld(width: int) -> int:
+    return int(lib().fold_row_ld(int(width)))
+
+
+def _ptr(t):
+    return None if t is None else c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return c_void_p(s.cuda_stream)
+
+
+# ----------------------------------------------------------------------------- raw calls
+
+def fold_schedule(batch: fold_batch, stream=None) -> c_void_p:
+    h = c_void_p()
+    _check(lib().fold_schedule(byref(batch), _stream(stream), byref(h)))
+    return h
+
+
+def fold_sched_get_info(handle) -> fold_sched_info:
+    info = fold_sched_info()
+    _check(lib().fold_sched_get_info(handle, byref(info)))
+    return info
+
+
+def fold_sched_free(handle):
+    _check(lib().fold_sched_free(handle))
+
+
+def fold_pack_params(params: fold_params, stream=None) -> c_void_p:
+    h = c_void_p()
+    _check(lib().fold_pack_params(byref(params), _stream(stream), byref(h)))
+    return h
+
+
+def fold_packed_free(handle):
+    _check(lib().fold_packed_free(handle))
+
+
+def fold_workspace_size(sched, packed):
+    f, b = c_size_t(), c_size_t()
+    _check(lib().fold_workspace_size(sched, packed, byref(f), byref(b)))
+    return int(f.value), int(b.value)
+
+
+def fold_forward(sched, packed, leaf_table, leaf_rows, h_pool, c_pool, roots_out, ws, ws_bytes, stream=None):
+    _check(lib().fold_forward(sched, packed, _ptr(leaf_table), int(leaf_rows), _ptr(h_pool), _ptr(c_pool),
+                              _ptr(roots_out), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def fold_backward(sched, packed, leaf_table, leaf_rows, h_pool, c_pool, dh_roots, dh_nodes, grads,
+                  dh_out, dc_out, ws, ws_bytes, stream=None):
+    _check(lib().fold_backward(sched, packed, _ptr(leaf_table), int(leaf_rows), _ptr(h_pool), _ptr(c_pool),
+                               _ptr(dh_roots), _ptr(dh_nodes), None if grads is None else byref(grads),
+                               _ptr(dh_out), _ptr(dc_out), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+# ----------------------------------------------------------------------------- tensor wrappers
+
+def _dev_copy_to_host(ptr: int, count: int) -> np.ndarray:
+    """Copy `count` int32 from a library-owned device array to host (the schedule call has synchronised)."""
+    out = np.empty(count, dtype=np.int32)
+    if count:
+        rc = _hip().hipMemcpy(c_void_p(out.ctypes.data), c_void_p(ptr), c_size_t(4 * count), 2)
+        if rc != 0:
+            raise RuntimeError(f"hipMemcpy failed ({rc})")
+    return out
+
+
+_hiplib = None
+
+
+def _hip():
+    global _hiplib
+    if _hiplib is None:
+        _hiplib = ctypes.CDLL("libamdhip64.so")
+        _hiplib.hipMemcpy.restype = ctypes.c_int
+        _hiplib.hipMemcpy.argtypes = [c_void_p, c_void_p, c_size_t, ctypes.c_int]
+    return _hiplib
+
+
+class Schedule:
+    """fold_schedule over int32 CUDA tensors; frees the handle when collected."""
+
+    def __init__(self, graph_ptr, node_op, child_ptr, child_idx, node_input, ops, num_inputs, stream=None):
+        self._keep = (graph_ptr, node_op, child_ptr, child_idx, node_input)
+        self._ops = (fold_op * len(ops))(*[fold_op(*o) for o in ops])
+        b = fold_batch()
+        b.num_graphs = graph_ptr.numel() - 1
+        b.num_nodes = node_op.numel()
+        b.num_edges = child_idx.numel()
+        b.num_ops = len(ops)
+        b.num_inputs = int(num_inputs)
+        b.graph_ptr, b.node_op, b.child_ptr = _ptr(graph_ptr), _ptr(node_op), _ptr(child_ptr)
+        b.child_idx = _ptr(child_idx) if child_idx.numel() else c_void_p(graph_ptr.data_ptr())
+        b.node_input = _ptr(node_input)
+        b.ops = self._ops
+        self.batch = b
+        self.handle = fold_schedule(b, stream)
+        self.info = fold_sched_get_info(self.handle)
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value:
+            try:
+                fold_sched_free(h)
+            except Exception:
+                pass
+            self.handle = None
+
+    @property
+    def num_levels(self):
+        return self.info.num_levels
+
+    def host_groups(self) -> dict:
+        i = self.info
+        ng = i.num_groups
+
+        def arr(p, n):
+            return np.ctypeslib.as_array(p, shape=(n,)).copy() if n else np.zeros(0, np.int32)
+        return dict(level_ptr=arr(i.h_level_ptr, i.num_levels + 1), group_level=arr(i.h_group_level, ng),
+                    group_op=arr(i.h_group_op, ng), group_row_begin=arr(i.h_group_row_begin, ng),
+                    group_rows=arr(i.h_group_rows, ng), group_idx_off=arr(i.h_group_idx_off, ng))
+
+    def arrays(self) -> dict:
+        """Every schedule array, copied to host numpy (device arrays and the host group table)."""
+        i = self.info
+        n, e, ng, D, R = i.num_nodes, i.num_edges, i.num_groups, i.num_levels, i.num_roots
+        out = dict(num_levels=D, num_groups=ng, num_roots=R, max_parents=i.max_parents)
+        for name, cnt in (("depth", n), ("node_pos", n), ("pos_node", n), ("level_ptr", D + 1),
+                          ("group_level", ng), ("group_op", ng), ("group_row_begin", ng), ("group_rows", ng),
+                          ("group_idx_off", ng), ("child_pos", e), ("input_idx", n), ("root_pos", R)):
+            p = getattr(i, name)
+            out[name] = _dev_copy_to_host(p, cnt) if p else np.zeros(0, np.int32)
+        out["host"] = self.host_groups()
+        return out
+
+
+class Packed:
+    """fold_pack_params over CUDA tensors (weights of the params' dtype, fp32 biases)."""
+
+    def __init__(self, dtype: int, hidden: int, sets, stream=None):
+        # sets: list of dict(kind, in_dim, arity, W_in, W_rec, bias) with tensors or None
+        self._keep = sets
+        arr = (fold_param_set * len(sets))()
+        for k, s in enumerate(sets):
+            arr[k] = fold_param_set(s["kind"], s["in_dim"], s["arity"], _ptr(s.get("W_in")),
+                                    _ptr(s.get("W_rec")), _ptr(s.get("bias")))
+        self._sets = arr
+        p = fold_params(dtype, hidden, len(sets), arr)
+        self.handle = fold_pack_params(p, stream)
+        self.dtype, self.hidden, self.num_sets = dtype, hidden, len(sets)
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value:
+            try:
+                fold_packed_free(h)
+            except Exception:
+                pass
+            self.handle = None
+
+
+def make_grads(sets_tensors, d_leaf_table=None) -> fold_grads:
+    """sets_tensors: list of (dW_in, dW_rec, dbias) fp32 CUDA tensors or None."""
+    arr = (fold_param_grads * len(sets_tensors))()
+    for k, (a, b, c) in enumerate(sets_tensors):
+        arr[k] = fold_param_grads(_ptr(a), _ptr(b), _ptr(c))
+    g = fold_grads(len(sets_tensors), arr, _ptr(d_leaf_table))
+    g._keep = (arr, sets_tensors, d_leaf_table)
+    return g

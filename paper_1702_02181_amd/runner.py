@@ -1,0 +1,140 @@
+"""Marshal a generated workload onto the GPU and drive the library through the binding.
+
+Used by the tests, ``bench.py`` and the smoke check: it only moves arrays
+between host and device and calls the C ABI; all arithmetic happens in the
+HIP kernels."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import fold as F
+from . import gen
+
+
+def bf16_tensor(x: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(gen.to_bf16_bits(np.ascontiguousarray(x, np.float32)).view(np.int16)).view(torch.bfloat16)
+
+
+def pad_cols(x: np.ndarray, ld: int) -> np.ndarray:
+    x = np.asarray(x, np.float32)
+    if x.shape[1] == ld:
+        return np.ascontiguousarray(x)
+    out = np.zeros((x.shape[0], ld), np.float32)
+    out[:, :x.shape[1]] = x
+    return out
+
+
+class DeviceRun:
+    def __init__(self, w: gen.Workload, device: str = "cuda", stream=None, with_backward=None):
+        self.w = w
+        self.device = device
+        self.stream = stream
+        H = w.hidden
+        self.H = H
+        self.ld = F.fold_row_ld(H)
+        self.bf16 = w.dtype == "bf16"
+        self.fdtype = F.FOLD_BF16 if self.bf16 else F.FOLD_F32
+        self.tdtype = torch.bfloat16 if self.bf16 else torch.float32
+        i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.int32)).to(device)
+        self.graph_ptr, self.node_op = i32(w.graph_ptr), i32(w.node_op)
+        self.child_ptr, self.child_idx, self.node_input = i32(w.child_ptr), i32(w.child_idx), i32(w.node_input)
+        self.ops = [(o.kind, o.arity, o.has_input, o.param_set) for o in w.ops]
+        self.leaf_rows = int(w.leaf_table.shape[0])
+        self.sched = F.Schedule(self.graph_ptr, self.node_op, self.child_ptr, self.child_idx, self.node_input,
+                                self.ops, self.leaf_rows, stream)
+        self.set_tensors = []
+        for p in w.params:
+            self.set_tensors.append(dict(
+                kind=p.kind, in_dim=p.in_dim, arity=p.arity,
+                W_in=None if p.W_in is None else self._wt(p.W_in),
+                W_rec=None if p.W_rec is None else self._wt(p.W_rec),
+                bias=None if p.kind == gen.KIND_EMBED else torch.from_numpy(p.bias.astype(np.float32)).to(device)))
+        self.packed = F.Packed(self.fdtype, H, self.set_tensors, stream)
+        in_dim = int(w.leaf_table.shape[1])
+        self.tld = F.fold_row_ld(in_dim)
+        tab = pad_cols(w.leaf_table, self.tld)
+        self.table = (bf16_tensor(tab) if self.bf16 else torch.from_numpy(tab)).to(device)
+        N, R = w.num_nodes, self.sched.info.num_roots
+        self.N, self.R = N, R
+        self.h_pool = torch.zeros((max(N, 1), self.ld), dtype=self.tdtype, device=device)
+        self.c_pool = torch.zeros((max(N, 1), self.ld), dtype=torch.float32, device=device)
+        self.roots = torch.zeros((max(R, 1), self.ld), dtype=self.tdtype, device=device)
+        self.fwd_bytes, self.bwd_bytes = F.fold_workspace_size(self.sched.handle, self.packed.handle)
+        backward = w.backward if with_backward is None else with_backward
+        self.ws_bytes = self.bwd_bytes if backward else self.fwd_bytes
+        self.ws = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=device)
+        self.grads = None
+        self.dh_roots = None
+        self.dh_nodes = None
+
+    def _wt(self, a):
+        a = np.ascontiguousarray(a, np.float32)
+        return (bf16_tensor(a) if self.bf16 else torch.from_numpy(a)).to(self.device)
+
+    # ------------------------------------------------------------------ calls
+    def forward(self):
+        F.fold_forward(self.sched.handle, self.packed.handle, self.table, self.leaf_rows, self.h_pool,
+                       self.c_pool, self.roots, self.ws, self.ws_bytes, self.stream)
+
+    def alloc_grads(self, table_grad=True):
+        sets = []
+        for p in self.w.params:
+            g = gen.NUM_GATES[p.kind] * self.H
+            if p.kind == gen.KIND_EMBED:
+                sets.append((None, None, None))
+                continue
+            z = lambda *s: torch.zeros(s, dtype=torch.float32, device=self.device)
+            sets.append((z(p.in_dim, g) if p.W_in is not None else None,
+                         z(p.arity * self.H, g) if p.W_rec is not None else None, z(g)))
+        self.grad_tensors = sets
+        self.d_table = (torch.zeros((self.leaf_rows, self.tld), dtype=torch.float32, device=self.device)
+                        if table_grad else None)
+        self.grads = F.make_grads(sets, self.d_table)
+        return sets
+
+    def set_upstream(self, dh_roots: np.ndarray, dh_nodes_node_order: np.ndarray | None = None):
+        self.dh_roots = torch.from_numpy(pad_cols(dh_roots, self.ld)).to(self.device) if self.R else None
+        if dh_nodes_node_order is not None:
+            node_pos = self.sched_arrays()["node_pos"]
+            pool = np.zeros((self.N, self.ld), np.float32)
+            pool[node_pos, :self.H] = dh_nodes_node_order
+            self.dh_nodes = torch.from_numpy(pool).to(self.device)
+        else:
+            self.dh_nodes = None
+
+    def zero_grads(self):
+        for t in self.grad_tensors:
+            for x in t:
+                if x is not None:
+                    x.zero_()
+        if self.d_table is not None:
+            self.d_table.zero_()
+
+    def backward(self, dh_out=None, dc_out=None):
+        F.fold_backward(self.sched.handle, self.packed.handle, self.table, self.leaf_rows, self.h_pool,
+                        self.c_pool, self.dh_roots, self.dh_nodes, self.grads, dh_out, dc_out, self.ws,
+                        self.ws_bytes, self.stream)
+
+    # ------------------------------------------------------------------ results
+    def sched_arrays(self):
+        if not hasattr(self, "_sa"):
+            self._sa = self.sched.arrays()
+        return self._sa
+
+    def node_states(self):
+        """h, c in node order as float64 [N, H]."""
+        torch.cuda.synchronize()
+        node_pos = self.sched_arrays()["node_pos"]
+        h = self.h_pool.float().cpu().numpy()[:self.N, :self.H].astype(np.float64)
+        c = self.c_pool.cpu().numpy()[:self.N, :self.H].astype(np.float64)
+        return h[node_pos], c[node_pos]
+
+    def weight_grads(self):
+        torch.cuda.synchronize()
+        out = []
+        for t in self.grad_tensors:
+            out.append({k: (None if x is None else x.cpu().numpy().astype(np.float64))
+                        for k, x in zip(("W_in", "W_rec", "bias"), t)})
+        dt = None if self.d_table is None else self.d_table.cpu().numpy()[:, :self.w.leaf_table.shape[1]].astype(np.float64)
+        return out, dt

@@ -1,0 +1,90 @@
+"""Helpers of the GPU parity tests: run a workload through the C ABI and through the oracle,
+and compare with the documented metric.  Tolerances (max relative error per row, see
+oracle.compare): 1e-5 for fp32 workloads, 2e-2 for bf16 matrix-core workloads."""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import compare, evaluate as EV, schedule as S
+from tests._helpers import oracle_batch, oracle_params
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+SCHED_KEYS = ("depth", "node_pos", "pos_node", "level_ptr", "group_level", "group_op", "group_row_begin",
+              "group_rows", "group_idx_off", "child_pos", "input_idx", "root_pos")
+
+
+def oracle_schedule(w):
+    b = oracle_batch(w)
+    return S.reference_schedule(b["node_op"], b["child_ptr"], b["child_idx"], b["node_input"], b["ops"])
+
+
+def assert_schedule_equal(gpu: dict, ref: dict):
+    assert gpu["num_levels"] == ref["num_levels"]
+    for k in SCHED_KEYS:
+        assert np.array_equal(np.asarray(gpu[k]), np.asarray(ref[k])), k
+    host = gpu["host"]
+    for k in ("level_ptr", "group_level", "group_op", "group_row_begin", "group_rows", "group_idx_off"):
+        assert np.array_equal(host[k], ref[k]), "host " + k
+
+
+def run_device(w, dh_nodes=None, table_grad=False, backward=None):
+    import torch
+    from paper_1702_02181_amd.runner import DeviceRun
+    backward = w.backward if backward is None else backward
+    dev = DeviceRun(w, with_backward=backward)
+    dev.forward()
+    out = {}
+    if backward:
+        dev.alloc_grads(table_grad)
+        dev.set_upstream(w.dh_roots, dh_nodes)
+        dh_out = torch.zeros((dev.N, dev.ld), dtype=torch.float32, device="cuda")
+        dc_out = torch.zeros_like(dh_out)
+        dev.backward(dh_out, dc_out)
+        torch.cuda.synchronize()
+        node_pos = dev.sched_arrays()["node_pos"]
+        out["dh"] = dh_out.cpu().numpy()[:, :dev.H][node_pos].astype(np.float64)
+        out["dc"] = dc_out.cpu().numpy()[:, :dev.H][node_pos].astype(np.float64)
+        out["grads"], out["d_table"] = dev.weight_grads()
+    out["h"], out["c"] = dev.node_states()
+    torch.cuda.synchronize()
+    ld = dev.ld
+    roots = dev.roots.float().cpu().numpy()[:dev.R, :dev.H].astype(np.float64)
+    out["roots"] = roots
+    out["sched"] = dev.sched_arrays()
+    out["dev"] = dev
+    return out
+
+
+def run_oracle(w, dh_nodes=None, table_grad=False, backward=None):
+    backward = w.backward if backward is None else backward
+    b, P = oracle_batch(w), oracle_params(w)
+    f = EV.forward(b, P, w.hidden, w.leaf_table)
+    out = {"h": f["h"], "c": f["c"], "roots_nodes": EV.roots(b)}
+    if backward:
+        bw = EV.backward(b, P, w.hidden, w.leaf_table, f, w.dh_roots.astype(np.float64), dh_nodes,
+                         want_table_grad=table_grad)
+        out.update(dh=bw["dh"], dc=bw["dc"], grads=bw["grads"], d_table=bw["d_table"])
+    return out
+
+
+def compare_all(w, g, o, tol=None, check_backward=None, table_grad=False):
+    tol = TOL[w.dtype] if tol is None else tol
+    errs = {}
+    errs["h"] = compare.rel_err(g["h"], o["h"])
+    errs["c"] = compare.rel_err(g["c"], o["c"])
+    errs["roots"] = compare.rel_err(g["roots"], o["h"][o["roots_nodes"]])
+    check_backward = w.backward if check_backward is None else check_backward
+    if check_backward:
+        errs["dh"] = compare.rel_err(g["dh"], o["dh"])
+        errs["dc"] = compare.rel_err(g["dc"], o["dc"])
+        for s, (gg, oo) in enumerate(zip(g["grads"], o["grads"])):
+            for name in ("W_in", "W_rec", "bias"):
+                if gg.get(name) is None or oo.get(name) is None:
+                    continue
+                errs[f"set{s}.{name}"] = compare.rel_err(gg[name], oo[name], whole=True)
+        if table_grad:
+            errs["d_table"] = compare.rel_err(g["d_table"], o["d_table"], whole=True)
+    bad = {k: v for k, v in errs.items() if not (v <= tol)}
+    assert not bad, f"over tolerance {tol}: {bad} (all: {errs})"
+    return errs
