@@ -112,6 +112,19 @@ def main():
     from paper_1702_02181_amd.runner import DeviceRun
 
     torch.cuda.set_device(0)
+    # achievable peaks on this GPU (MFMA loop, stream copy), next to the datasheet figures
+    probes = {}
+    try:
+        probes["mfma_f32_tflops"] = round(F.fold_probe_mfma(F.FOLD_F32), 1)
+        probes["mfma_bf16_tflops"] = round(F.fold_probe_mfma(F.FOLD_BF16), 1)
+        nbytes = 1 << 30
+        src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        probes["copy_gbs"] = round(F.fold_probe_copy(dst, src, nbytes), 1)
+        del src, dst
+    except Exception as e:  # probes are diagnostics; the bench line does not depend on them
+        probes["error"] = str(e)
+    print(f"[bench] probes {probes}", file=sys.stderr, flush=True)
     print(f"[bench] generating config {args.config}", file=sys.stderr, flush=True)
     w = gen.make_config(args.config)
     table_grad = args.config in (3, 5)  # trainable embedding tables; config 2 / 4 leaf rows are data
@@ -210,6 +223,7 @@ def main():
         "config": {"workload": w.name, "graphs": w.num_graphs, "nodes": N, "levels": dev.sched.num_levels,
                    "hidden": w.hidden, "pass": "forward+backward" if w.backward else "forward"},
         "schedule_ms": None if schedule_ms is None else round(schedule_ms, 3),
+        "peaks": {"datasheet": PEAKS, "measured": probes},
         "roofline": roofline,
         "step_mfma_frac": round(total_flops / (ms_per_step * 1e-3) / 1e12 / step_peak, 4),
         "kernels": kernels,

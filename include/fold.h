@@ -253,6 +253,16 @@ typedef struct {
 int32_t fold_profile_enable(int32_t on);
 int32_t fold_profile_read(fold_kernel_stat* out, int32_t capacity, int32_t* count);
 
+/* ---- achievable peaks (diagnostics) --------------------------------------
+ * fold_probe_mfma times a loop of independent 32x32 MFMA instructions
+ * (fp32 32x32x2 or bf16 32x32x16) on every compute unit and returns the
+ * sustained dense TFLOP/s; fold_probe_copy copies `bytes` (a multiple of 16,
+ * both buffers 16-byte aligned, caller-owned device memory) five times with
+ * 16-byte loads and stores and returns read+write GB/s.  Both synchronise
+ * `stream`; fold_probe_mfma allocates a small output buffer. */
+int32_t fold_probe_mfma(int32_t dtype, hipStream_t stream, double* tflops);
+int32_t fold_probe_copy(void* dst, const void* src, size_t bytes, hipStream_t stream, double* gbs);
+
 /* Text of the last error on the calling thread ("" if none). */
 const char* fold_last_error(void);
 

@@ -152,15 +152,18 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
     const int count = s.h_op_row_ptr[o + 1] - s.h_op_row_ptr[o];
     const PackedSet& ps = p.sets[op.param_set];
     const int Nw = ps.G * p.HP;
+    size_t nb = (size_t)((count + 511) / 512);
     if (op.arity > 0) {
       WgradSplit sp = wgrad_split(count, op.arity * p.HP, Nw);
       part = std::max(part, (size_t)sp.nchunk * op.arity * p.HP * Nw);
+      nb = std::max(nb, (size_t)sp.nchunk);
     }
     if (op.has_input && ps.INP > 0) {
       WgradSplit sp = wgrad_split(count, ps.INP, Nw);
       part = std::max(part, (size_t)sp.nchunk * ps.INP * Nw);
+      nb = std::max(nb, (size_t)sp.nchunk);
     }
-    bpart = std::max(bpart, (size_t)((count + 4095) / 4096) * Nw);
+    bpart = std::max(bpart, nb * Nw);
   }
   w.part_off = w.dh_off + w.acc_bytes;
   w.part_bytes = al(part * sizeof(float));
@@ -353,13 +356,12 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       const PackedSet& ps = p.sets[op.param_set];
       const fold_param_grads& pg = grads->sets[op.param_set];
       const int Nw = ps.G * p.HP;
+      const int off = s.h_op_row_ptr[o];
       WgArgs w;
-      w.op_rows = s.op_rows + s.h_op_row_ptr[o];
+      w.op_rows = s.op_rows + off;
+      w.op_cpos = s.op_cpos + 2 * (size_t)off;
+      w.op_inp = s.op_inp + off;
       w.count = count;
-      w.pos_group = s.pos_group;
-      w.g_row_begin = s.g_row_begin;
-      w.g_idx_off = s.g_idx_off;
-      w.arity = op.arity;
       w.H = p.H;
       w.HP = p.HP;
       w.ld = p.ld;
@@ -367,33 +369,30 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       w.tld = tld;
       w.gstride = L.gstride;
       w.Nw = Nw;
-      w.child_pos = s.child_pos;
-      w.input_idx = s.input_idx;
       w.dz = gates;
       w.partial = part;
-      if (op.arity > 0 && pg.dW_rec) {
-        w.seg = 1;
-        w.Kw = op.arity * p.HP;
-        w.src = h_pool;
-        WgradSplit sp = wgrad_split(count, w.Kw, Nw);
+      bool bias_done = false;
+      auto run = [&](int seg, int Kw, const void* src, float* dW) {
+        w.seg = seg;
+        w.Kw = Kw;
+        w.src = src;
+        const WgradSplit sp = wgrad_split(count, Kw, Nw);
         w.chunk = sp.chunk;
         w.nchunk = sp.nchunk;
+        w.bpart = (pg.dbias && !bias_done) ? bpart : nullptr;
         launch_wgrad(p.dtype, w, st);
-        launch_wgrad_reduce(part, sp.nchunk, w.Kw, Nw, 1, p.H, p.HP, ps.in_dim, ps.G, pg.dW_rec, st);
-      }
-      if (op.has_input && ps.INP > 0 && pg.dW_in) {
-        w.seg = 0;
-        w.Kw = ps.INP;
-        w.src = table;
-        WgradSplit sp = wgrad_split(count, w.Kw, Nw);
-        w.chunk = sp.chunk;
-        w.nchunk = sp.nchunk;
-        launch_wgrad(p.dtype, w, st);
-        launch_wgrad_reduce(part, sp.nchunk, w.Kw, Nw, 0, p.H, p.HP, ps.in_dim, ps.G, pg.dW_in, st);
-      }
-      if (pg.dbias) {
-        const int chunk = 4096, nchunk = (count + chunk - 1) / chunk;
-        launch_bias_grad(w.op_rows, count, chunk, nchunk, gates, L.gstride, Nw, bpart, ps.G, p.H, p.HP, pg.dbias, st);
+        launch_wgrad_reduce(part, sp.nchunk, Kw, Nw, seg, p.H, p.HP, ps.in_dim, ps.G, dW, st);
+        if (w.bpart) {
+          launch_bias_reduce(bpart, sp.nchunk, Nw, p.H, p.HP, pg.dbias, st);
+          bias_done = true;
+        }
+      };
+      if (op.arity > 0 && pg.dW_rec) run(1, op.arity * p.HP, h_pool, pg.dW_rec);
+      if (op.has_input && ps.INP > 0 && pg.dW_in) run(0, ps.INP, table, pg.dW_in);
+      if (pg.dbias && !bias_done) {
+        const int chunk = 512, nchunk = (count + chunk - 1) / chunk;
+        launch_bias_partial(w.op_rows, count, chunk, nchunk, gates, L.gstride, Nw, bpart, st);
+        launch_bias_reduce(bpart, nchunk, Nw, p.H, p.HP, pg.dbias, st);
       }
     }
   }
@@ -419,6 +418,24 @@ using namespace fold;
 extern "C" {
 
 const char* fold_last_error(void) { return fold::g_last_error.c_str(); }
+
+int32_t fold_probe_mfma(int32_t dtype, hipStream_t st, double* tflops) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!tflops || (dtype != FOLD_F32 && dtype != FOLD_BF16)) return fail(FOLD_E_INVALID, "fold_probe_mfma: bad argument");
+  return probe_mfma(dtype, st, tflops);
+  FOLD_GUARD_END
+}
+
+int32_t fold_probe_copy(void* dst, const void* src, size_t bytes, hipStream_t st, double* gbs) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!dst || !src || !gbs || bytes < 16 || (bytes % 16) != 0 || (reinterpret_cast<uintptr_t>(dst) % 16) != 0 ||
+      (reinterpret_cast<uintptr_t>(src) % 16) != 0)
+    return fail(FOLD_E_INVALID, "fold_probe_copy: NULL, unaligned or non-multiple-of-16 buffers");
+  return probe_copy(dst, src, bytes, st, gbs);
+  FOLD_GUARD_END
+}
 
 int32_t fold_profile_enable(int32_t on) {
   fold::g_prof_on.store(on != 0);

@@ -35,77 +35,104 @@ struct Gates {
 
 // ---------------------------------------------------------------- forward
 
+// stage c of the forward K loop: input segment (INP wide) first, then one HP-wide segment per child
+struct FwdStages {
+  int cin, chp, has_input, INP, HP;
+  __device__ __forceinline__ void at(int c, int bk, int& seg, int& kc, int& kbase) const {
+    if (c < cin) {
+      seg = 0;
+      kc = c * bk;
+      kbase = 0;
+    } else {
+      const int cc = c - cin, k = cc / chp;
+      seg = has_input + k;
+      kc = (cc - k * chp) * bk;
+      kbase = INP + k * HP;
+    }
+  }
+};
+
+// gathered rows: leaf-table rows (input segment) or children's h rows, row indices from LDS
+template <typename T, int BM, int VROW>
+struct FwdA {
+  using raw = Raw4;
+  const T* table;
+  const T* pool;
+  int tld, ld, in_dim, H, has_input;
+  FwdStages st;
+  const int (*srow)[BM];
+  __device__ __forceinline__ raw fetch(int c, int i) const {
+    constexpr int BK = Mma<T>::BK, VEC = Mma<T>::VEC;
+    int seg, kc, kbase;
+    st.at(c, BK, seg, kc, kbase);
+    const int r = i / VROW, v = i - r * VROW;
+    const int sr = srow[seg][r];
+    const bool is_in = has_input && seg == 0;
+    const int width = is_in ? in_dim : H;
+    const int col = kc + v * VEC;
+    const int nv = sr >= 0 ? min(max(width - col, 0), VEC) : 0;
+    const T* base = is_in ? table : pool;
+    const size_t off = nv > 0 ? (size_t)sr * (is_in ? tld : ld) + col : 0;
+    return {*reinterpret_cast<const uint4*>(base + off), nv};
+  }
+  __device__ __forceinline__ uint4 put(const raw& r) const { return finish<T>(r); }
+};
+
+// packed weights, n-major, always in range
+template <typename T, int VROW>
+struct WeightB {
+  using raw = Raw4;
+  const T* W;
+  int ldk;
+  FwdStages st;
+  __device__ __forceinline__ raw fetch(int c, int i) const {
+    constexpr int BK = Mma<T>::BK, VEC = Mma<T>::VEC;
+    int seg, kc, kbase;
+    st.at(c, BK, seg, kc, kbase);
+    const int n = i / VROW, v = i - n * VROW;
+    return {*reinterpret_cast<const uint4*>(W + (size_t)n * ldk + kbase + kc + v * VEC), VEC};
+  }
+  __device__ __forceinline__ uint4 put(const raw& r) const { return r.x; }
+};
+
 template <typename T, int KIND, int MT>
 __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   using M = Mma<T>;
   constexpr int G = Gates<KIND>::G;
-  constexpr int BK = M::BK, VEC = M::VEC, VPR = BK / VEC, PITCH = BK + M::PAD;
   constexpr int BM = 4 * 32 * MT;  // four waves stacked along the rows
   constexpr int BN = G * 32;       // G gate blocks of 32 units
-  __shared__ __attribute__((aligned(16))) T As[BM * PITCH];
-  __shared__ __attribute__((aligned(16))) T Bs[BN * PITCH];
-  __shared__ int srow[BM];
+  using TA = Tile<T, BM, kRK>;
+  using TB = Tile<T, BN, kRK>;
+  __shared__ __attribute__((aligned(16))) T As[TA::ELEMS];
+  __shared__ __attribute__((aligned(16))) T Bs[TB::ELEMS];
+  __shared__ int srow[3][BM];  // source row of every tile row, per input segment
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = blockIdx.x * BM;
   const int ub = blockIdx.y;  // hidden units ub*32 .. ub*32+31
-  const T* W = static_cast<const T*>(a.Wf) + (size_t)ub * BN * a.Kf;
-
-  f32x16 acc[MT][G];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[mt][g][r] = 0.f;
 
   const int nseg = a.has_input + a.arity;
   for (int seg = 0; seg < nseg; ++seg) {
     const bool is_in = a.has_input && seg == 0;
-    const int k = is_in ? 0 : seg - a.has_input;  // child slot
-    const int width = is_in ? a.in_dim : a.H;
-    const int padw = is_in ? a.INP : a.HP;
-    const int kbase = is_in ? 0 : a.INP + k * a.HP;
-    const T* src = is_in ? static_cast<const T*>(a.table) : static_cast<const T*>(a.h_pool);
-    const int sld = is_in ? a.tld : a.ld;
-    __syncthreads();
+    const int k = seg - a.has_input;
     for (int r = tid; r < BM; r += kThreads) {
       const int row = m0 + r;
       int sr = -1;
       if (row < a.rows) sr = is_in ? a.input_idx[a.row_begin + row] : a.child_pos[a.idx_off + row * a.arity + k];
-      srow[r] = sr;
-    }
-    __syncthreads();
-    for (int kc = 0; kc < padw; kc += BK) {
-      for (int i = tid; i < BM * VPR; i += kThreads) {
-        const int r = i / VPR, v = i - r * VPR;
-        const int sr = srow[r];
-        uint4 x = make_uint4(0u, 0u, 0u, 0u);
-        if (sr >= 0) x = load_row_vec<T>(src + (size_t)sr * sld, kc + v * VEC, width);
-        *reinterpret_cast<uint4*>(&As[r * PITCH + v * VEC]) = x;
-      }
-      for (int i = tid; i < BN * VPR; i += kThreads) {
-        const int n = i / VPR, v = i - n * VPR;
-        *reinterpret_cast<uint4*>(&Bs[n * PITCH + v * VEC]) =
-            *reinterpret_cast<const uint4*>(W + (size_t)n * a.Kf + kbase + kc + v * VEC);
-      }
-      __syncthreads();
-#pragma unroll
-      for (int ks = 0; ks < BK; ks += M::KSTEP) {
-        typename M::frag af[MT];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-          af[mt] = M::load(&As[(wave * 32 * MT + mt * 32 + (lane & 31)) * PITCH + ks + (lane >> 5) * M::KPL]);
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const typename M::frag bf = M::load(&Bs[(g * 32 + (lane & 31)) * PITCH + ks + (lane >> 5) * M::KPL]);
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) acc[mt][g] = M::mma(af[mt], bf, acc[mt][g]);
-        }
-      }
-      __syncthreads();
+      srow[seg][r] = sr;
     }
   }
+  __syncthreads();
+
+  FwdStages st{a.has_input ? a.INP / M::BK : 0, a.HP / M::BK, a.has_input, a.INP, a.HP};
+  const int nchunks = st.cin + a.arity * st.chp;
+  FwdA<T, BM, TA::VROW> la{static_cast<const T*>(a.table), static_cast<const T*>(a.h_pool), a.tld, a.ld,
+                           a.in_dim, a.H, a.has_input, st, srow};
+  WeightB<T, TB::VROW> lb{static_cast<const T*>(a.Wf) + (size_t)ub * BN * a.Kf, a.Kf, st};
+  NoIndex ix;
+  f32x16 acc[MT][G];
+  zero_acc(acc);
+  mainloop<T, TA, TB, MT, G>(nchunks, la, lb, ix, As, Bs, acc, wave * 32 * MT, 0);
 
   // epilogue: the cell, in registers
   const int j = ub * 32 + (lane & 31);
@@ -134,7 +161,7 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
       float* gs = a.gates ? a.gates + p * a.gstride + j : nullptr;
       if constexpr (KIND == FOLD_TREELSTM) {
         const float i_ = sigmoidf_(z[0]), fl = sigmoidf_(z[1]), fr = sigmoidf_(z[2]), o = sigmoidf_(z[3]);
-        const float u = tanhf(z[4]);
+        const float u = tanhf_(z[4]);
         float cl = 0.f, cr = 0.f;
         if (a.arity == 2) {
           const int pl = a.child_pos[a.idx_off + row * 2], pr = a.child_pos[a.idx_off + row * 2 + 1];
@@ -142,7 +169,7 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
           if (pr >= 0) cr = a.c_pool[(size_t)pr * a.ld + j];
         }
         c = i_ * u + fl * cl + fr * cr;
-        h = o * tanhf(c);
+        h = o * tanhf_(c);
         if (gs) {
           gs[0] = i_;
           gs[a.HP] = fl;
@@ -152,11 +179,11 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
         }
       } else if constexpr (KIND == FOLD_LSTM) {
         const float i_ = sigmoidf_(z[0]), f = sigmoidf_(z[1]), o = sigmoidf_(z[2]);
-        const float u = tanhf(z[3]);
+        const float u = tanhf_(z[3]);
         const int pc = a.child_pos[a.idx_off + row];
         const float cp = pc >= 0 ? a.c_pool[(size_t)pc * a.ld + j] : 0.f;
         c = i_ * u + f * cp;
-        h = o * tanhf(c);
+        h = o * tanhf_(c);
         if (gs) {
           gs[0] = i_;
           gs[a.HP] = f;
@@ -164,7 +191,7 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
           gs[3 * a.HP] = u;
         }
       } else {
-        h = tanhf(z[0]);
+        h = tanhf_(z[0]);
         c = 0.f;
         if constexpr (KIND == FOLD_PROJ) {
           const int pc = a.child_pos[a.idx_off + row];
@@ -238,7 +265,7 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
     } else if constexpr (KIND == FOLD_TREELSTM) {
       const float dc = a.dc[p * a.ld + j];
       const float i_ = gb[j], fl = gb[a.HP + j], fr = gb[2 * a.HP + j], o = gb[3 * a.HP + j], u = gb[4 * a.HP + j];
-      const float tc = tanhf(a.c_pool[p * a.ld + j]);
+      const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cl = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
       const float cr = c1 >= 0 ? a.c_pool[(size_t)c1 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
@@ -252,7 +279,7 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
     } else if constexpr (KIND == FOLD_LSTM) {
       const float dc = a.dc[p * a.ld + j];
       const float i_ = gb[j], f = gb[a.HP + j], o = gb[2 * a.HP + j], u = gb[3 * a.HP + j];
-      const float tc = tanhf(a.c_pool[p * a.ld + j]);
+      const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cp = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
       gb[j] = dct * u * i_ * (1.f - i_);
@@ -273,61 +300,91 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
 
 // ---------------------------------------------------------------- backward, dz . W^T
 
-template <typename T>
+// rows of fp32 dz, converted to the operand type when written to LDS
+template <typename T, int VROW>
+struct DzRows;
+
+template <int VROW>
+struct DzRows<float, VROW> {
+  using raw = Raw4;
+  const float* dz;
+  int gstride, row_begin, rows, m0;
+  __device__ __forceinline__ raw fetch(int c, int i) const {
+    const int r = i / VROW, v = i - r * VROW, row = m0 + r;
+    const int ok = row < rows;
+    const float* p = dz + (size_t)(row_begin + (ok ? row : 0)) * gstride + c * 32 + v * 4;
+    return {*reinterpret_cast<const uint4*>(p), ok ? 4 : 0};
+  }
+  __device__ __forceinline__ uint4 put(const raw& r) const { return finish<float>(r); }
+};
+
+template <int VROW>
+struct DzRows<uint16_t, VROW> {
+  using raw = Raw8;
+  const float* dz;
+  int gstride, row_begin, rows, m0;
+  __device__ __forceinline__ raw fetch(int c, int i) const {
+    const int r = i / VROW, v = i - r * VROW, row = m0 + r;
+    const int ok = row < rows;
+    const float* p = dz + (size_t)(row_begin + (ok ? row : 0)) * gstride + c * 64 + v * 8;
+    return {reinterpret_cast<const uint4*>(p)[0], reinterpret_cast<const uint4*>(p)[1], ok ? 8 : 0};
+  }
+  __device__ __forceinline__ uint4 put(const raw& r) const { return finish_bf16(r); }
+};
+
+// packed backward weights W^T, n-major, rows past Nb read as zero
+template <typename T, int VROW>
+struct WeightRows {
+  using raw = Raw4;
+  const T* W;
+  int Kb, Nb, n0;
+  __device__ __forceinline__ raw fetch(int c, int i) const {
+    constexpr int BK = Mma<T>::BK, VEC = Mma<T>::VEC;
+    const int n = i / VROW, v = i - n * VROW;
+    const int ok = n0 + n < Nb;
+    return {*reinterpret_cast<const uint4*>(W + (size_t)(ok ? n0 + n : 0) * Kb + c * BK + v * VEC), ok ? VEC : 0};
+  }
+  __device__ __forceinline__ uint4 put(const raw& r) const { return finish<T>(r); }
+};
+
+template <typename T, int MT>
 __global__ __launch_bounds__(kThreads) void k_bwd_dx(DxArgs a) {
   using M = Mma<T>;
-  constexpr int BK = M::BK, VEC = M::VEC, VPR = BK / VEC, PITCH = BK + M::PAD;
-  constexpr int BM = 128, BN = 64;  // four waves of 32 rows x 64 columns
-  __shared__ __attribute__((aligned(16))) T As[BM * PITCH];
-  __shared__ __attribute__((aligned(16))) T Bs[BN * PITCH];
+  constexpr int TN = 4;
+  constexpr int BM = 4 * 32 * MT, BN = 32 * TN;  // four waves of 32*MT rows x 128 columns
+  using TA = Tile<T, BM, kRK>;
+  using TB = Tile<T, BN, kRK>;
+  __shared__ __attribute__((aligned(16))) T As[TA::ELEMS];
+  __shared__ __attribute__((aligned(16))) T Bs[TB::ELEMS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
-  const T* W = static_cast<const T*>(a.Wb) + (size_t)n0 * a.Kb;
-  f32x16 acc[2];
-  for (int t = 0; t < 2; ++t)
-    for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
-  for (int kc = 0; kc < a.Kb; kc += BK) {
-    for (int i = tid; i < BM * VPR; i += kThreads) {
-      const int r = i / VPR, v = i - r * VPR, row = m0 + r;
-      uint4 x = make_uint4(0u, 0u, 0u, 0u);
-      if (row < a.rows)
-        x = pack_from_f32<T>(a.dz + (size_t)(a.row_begin + row) * a.gstride + kc + v * VEC, VEC);
-      *reinterpret_cast<uint4*>(&As[r * PITCH + v * VEC]) = x;
-    }
-    for (int i = tid; i < BN * VPR; i += kThreads) {
-      const int n = i / VPR, v = i - n * VPR;
-      *reinterpret_cast<uint4*>(&Bs[n * PITCH + v * VEC]) =
-          *reinterpret_cast<const uint4*>(W + (size_t)n * a.Kb + kc + v * VEC);
-    }
-    __syncthreads();
+  DzRows<T, TA::VROW> la{a.dz, a.gstride, a.row_begin, a.rows, m0};
+  WeightRows<T, TB::VROW> lb{static_cast<const T*>(a.Wb), a.Kb, a.Nb, n0};
+  NoIndex ix;
+  f32x16 acc[MT][TN];
+  zero_acc(acc);
+  mainloop<T, TA, TB, MT, TN>(a.Kb / M::BK, la, lb, ix, As, Bs, acc, wave * 32 * MT, 0);
 #pragma unroll
-    for (int ks = 0; ks < BK; ks += M::KSTEP) {
-      const typename M::frag af = M::load(&As[(wave * 32 + (lane & 31)) * PITCH + ks + (lane >> 5) * M::KPL]);
+  for (int tm = 0; tm < MT; ++tm) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const typename M::frag bf = M::load(&Bs[(t * 32 + (lane & 31)) * PITCH + ks + (lane >> 5) * M::KPL]);
-        acc[t] = M::mma(af, bf, acc[t]);
-      }
-    }
-    __syncthreads();
-  }
+    for (int tn = 0; tn < TN; ++tn) {
+      const int n = n0 + tn * 32 + (lane & 31);
+      if (n >= a.Nb) continue;
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int n = n0 + t * 32 + (lane & 31);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = m0 + wave * 32 + acc_row(r, lane);
-      if (row >= a.rows) continue;
-      const float v = acc[t][r];
-      if (a.mode == 0) {
-        const int k = n / a.HP, jin = n - k * a.HP;
-        if (jin >= a.H) continue;
-        const int cp = a.child_pos[a.idx_off + row * a.arity + k];
-        if (cp >= 0) unsafeAtomicAdd(&a.dh[(size_t)cp * a.ld + jin], v);
-      } else {
-        if (n >= a.in_dim) continue;
-        const int ti = a.input_idx[a.row_begin + row];
-        unsafeAtomicAdd(&a.d_table[(size_t)ti * a.tld + n], v);
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wave * 32 * MT + tm * 32 + acc_row(r, lane);
+        if (row >= a.rows) continue;
+        const float v = acc[tm][tn][r];
+        if (a.mode == 0) {
+          const int k = n / a.HP, jin = n - k * a.HP;
+          if (jin >= a.H) continue;
+          const int cp = a.child_pos[a.idx_off + row * a.arity + k];
+          if (cp >= 0) unsafeAtomicAdd(&a.dh[(size_t)cp * a.ld + jin], v);
+        } else {
+          if (n >= a.in_dim) continue;
+          const int ti = a.input_idx[a.row_begin + row];
+          unsafeAtomicAdd(&a.d_table[(size_t)ti * a.tld + n], v);
+        }
       }
     }
   }
@@ -337,7 +394,7 @@ inline unsigned cdiv(long long a, long long b) { return (unsigned)((a + b - 1) /
 
 template <typename T>
 void cell_fwd_t(int kind, const FwdArgs& a, hipStream_t st) {
-  const int MT = (sizeof(T) == 2 && a.rows > 128) ? 2 : 1;
+  const int MT = a.rows > 128 ? 2 : 1;
   const int BM = 128 * MT;
   dim3 grid(cdiv(a.rows, BM), a.HP / 32);
 #define FOLD_LAUNCH_FWD(KIND, MTV) \
@@ -433,11 +490,15 @@ void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
 void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st) {
   if (a.rows <= 0 || a.Nb <= 0) return;
   ProfScope prof(dtype == FOLD_BF16 ? "bwd_dx.bf16" : "bwd_dx.f32", st);
-  dim3 grid(cdiv(a.rows, 128), a.Nb / 64);
-  if (dtype == FOLD_BF16)
-    hipLaunchKernelGGL(k_bwd_dx<uint16_t>, grid, dim3(kThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL(k_bwd_dx<float>, grid, dim3(kThreads), 0, st, a);
+  const int MT = a.rows > 128 ? 2 : 1;
+  dim3 grid(cdiv(a.rows, 128 * MT), cdiv(a.Nb, 128));
+  if (dtype == FOLD_BF16) {
+    if (MT == 2) hipLaunchKernelGGL((k_bwd_dx<uint16_t, 2>), grid, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_bwd_dx<uint16_t, 1>), grid, dim3(kThreads), 0, st, a);
+  } else {
+    if (MT == 2) hipLaunchKernelGGL((k_bwd_dx<float, 2>), grid, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_bwd_dx<float, 1>), grid, dim3(kThreads), 0, st, a);
+  }
 }
 
 }  // namespace fold

@@ -78,6 +78,8 @@ struct Sched {
   int32_t *child_pos = nullptr, *input_idx = nullptr, *root_pos = nullptr;
   int32_t *pos_group = nullptr;   // [N] group of every pool row
   int32_t *op_rows = nullptr;     // [N] pool rows sorted by (op, row)
+  int32_t *op_cpos = nullptr;     // [2N] child pool rows of op_rows[q] at 2q + k (-1 past the arity)
+  int32_t *op_inp = nullptr;      // [N] leaf-table row of op_rows[q], or -1
   void* blob3 = nullptr;          // level / group table (device copy)
   std::vector<int32_t> h_level_ptr, h_level, h_op, h_row_begin, h_rows, h_idx_off;
   std::vector<int32_t> h_op_row_ptr;  // [num_ops + 1] ranges of op_rows
@@ -127,14 +129,11 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
   return (uint16_t)(u >> 16);
 }
 
-__device__ __forceinline__ float sigmoidf_(float x) {
-  // 1 / (1 + e^-x), written so that neither branch overflows
-  if (x >= 0.f) {
-    float e = expf(-x);
-    return 1.f / (1.f + e);
-  }
-  float e = expf(x);
-  return e / (1.f + e);
-}
+// Gate nonlinearities on the hardware exp2 / reciprocal units (v_exp_f32, v_rcp_f32, about one ulp
+// each): sigma(x) = 1 / (1 + e^-x); for x -> -inf, e^-x overflows to +inf and the reciprocal gives 0.
+// tanh(x) = 2 sigma(2x) - 1, absolute error a few 1e-7 (relative error grows only as tanh -> 0).
+__device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
+__device__ __forceinline__ float sigmoidf_(float x) { return __builtin_amdgcn_rcpf(1.f + fast_exp(-x)); }
+__device__ __forceinline__ float tanhf_(float x) { return 2.f * sigmoidf_(2.f * x) - 1.f; }
 
 }  // namespace fold

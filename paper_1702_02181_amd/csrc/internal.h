@@ -89,27 +89,29 @@ void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st);
 
 // ---- weight gradients (wgrad.hip) ----
 struct WgArgs {
-  const int* op_rows;
+  const int* op_rows;  // rows of this op (pool rows), count of them
+  const int* op_cpos;  // [2 * count] children's pool rows per op row
+  const int* op_inp;   // [count] leaf-table row per op row
   int count;
-  const int* pos_group;
-  const int* g_row_begin;
-  const int* g_idx_off;
-  int arity;
   int seg;  // 0: input rows from the leaf table, 1: children's h rows
   int H, HP, ld, in_dim, tld, gstride;
   int Kw, Nw;
   const void* src;
-  const int* child_pos;
-  const int* input_idx;
   const float* dz;
   int chunk, nchunk;
-  float* partial;
+  float* partial;  // [nchunk][Kw][Nw]
+  float* bpart;    // [nchunk][Nw] column sums of dz per chunk, or NULL
 };
 void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st);
 void launch_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP, int in_dim,
                          int G, float* dW, hipStream_t st);
-void launch_bias_grad(const int* op_rows, int count, int chunk, int nchunk, const float* dz, int gstride,
-                      int Nw, float* bpart, int G, int H, int HP, float* dbias, hipStream_t st);
+void launch_bias_partial(const int* op_rows, int count, int chunk, int nchunk, const float* dz, int gstride,
+                         int Nw, float* bpart, hipStream_t st);
+void launch_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, float* dbias, hipStream_t st);
+
+// ---- achievable-peak probes (diag.hip) ----
+int32_t probe_mfma(int dtype, hipStream_t st, double* tflops);
+int32_t probe_copy(void* dst, const void* src, size_t bytes, hipStream_t st, double* gbs);
 
 // ---- packing (pack.hip) ----
 void launch_pack(int dtype, int mode, int G, int H, int HP, int in_dim, int INP, int arity, int Kf,

@@ -4,8 +4,7 @@
 //   fp32 operands  v_mfma_f32_32x32x2_f32   (K = 2 per instruction, one element per lane)
 //   bf16 operands  v_mfma_f32_32x32x16_bf16 (K = 16 per instruction, eight elements per lane)
 // Operand fragments: lane l supplies row (l % 32) of A and column (l % 32) of B, for the
-// K slice starting at (l / 32) * KPL.  Both A and B tiles live in LDS as [row][k] with k
-// contiguous, so the two fragment loads are the same access pattern.
+// K slice starting at (l / 32) * KPL.
 // Result: lane l, register r holds C[8 * (r / 4) + 4 * (l / 32) + (r % 4)][l % 32].
 #pragma once
 
@@ -22,7 +21,6 @@ struct Mma<float> {
   static constexpr int KSTEP = 2;  // K per instruction
   static constexpr int KPL = 1;    // K elements per lane per instruction
   static constexpr int VEC = 4;    // elements per 16-byte vector
-  static constexpr int PAD = 4;    // row padding in LDS (keeps 16-byte alignment)
   typedef float frag;
   __device__ static __forceinline__ frag load(const float* p) { return *p; }
   __device__ static __forceinline__ f32x16 mma(frag a, frag b, f32x16 c) {
@@ -36,7 +34,6 @@ struct Mma<uint16_t> {
   static constexpr int KSTEP = 16;
   static constexpr int KPL = 8;
   static constexpr int VEC = 8;
-  static constexpr int PAD = 8;
   typedef bf16x8 frag;
   __device__ static __forceinline__ frag load(const uint16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
   __device__ static __forceinline__ f32x16 mma(frag a, frag b, f32x16 c) {
@@ -46,62 +43,6 @@ struct Mma<uint16_t> {
 
 // row of the 32x32 result tile held by register r of lane `lane`
 __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
-
-// 16-byte load of elements [col, col + VEC) of a row; elements at or beyond `width` read as zero.
-// The caller guarantees col + VEC <= the row's allocated stride.
-template <typename T>
-__device__ __forceinline__ uint4 load_row_vec(const T* row, int col, int width) {
-  constexpr int VEC = 16 / sizeof(T);
-  uint4 v = make_uint4(0u, 0u, 0u, 0u);
-  if (col >= width) return v;
-  v = *reinterpret_cast<const uint4*>(row + col);
-  const int valid = width - col;
-  if (valid < VEC) {
-    uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    if (sizeof(T) == 4) {
-      for (int e = 0; e < 4; ++e)
-        if (e >= valid) w[e] = 0u;
-    } else {
-      for (int e = 0; e < 8; ++e)
-        if (e >= valid) w[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-    }
-    v = make_uint4(w[0], w[1], w[2], w[3]);
-  }
-  return v;
-}
-
-// 16 bytes of LDS operand from fp32 source values: 4 floats (T = float) or 8 floats rounded to bf16.
-template <typename T>
-__device__ __forceinline__ uint4 pack_from_f32(const float* src, int valid);
-
-template <>
-__device__ __forceinline__ uint4 pack_from_f32<float>(const float* src, int valid) {
-  uint4 v = make_uint4(0u, 0u, 0u, 0u);
-  if (valid >= 4) {
-    float4 f = *reinterpret_cast<const float4*>(src);
-    v = make_uint4(__float_as_uint(f.x), __float_as_uint(f.y), __float_as_uint(f.z), __float_as_uint(f.w));
-  } else {
-    uint32_t w[4] = {0u, 0u, 0u, 0u};
-    for (int e = 0; e < valid; ++e) w[e] = __float_as_uint(src[e]);
-    v = make_uint4(w[0], w[1], w[2], w[3]);
-  }
-  return v;
-}
-
-template <>
-__device__ __forceinline__ uint4 pack_from_f32<uint16_t>(const float* src, int valid) {
-  float f[8];
-  if (valid >= 8) {
-    float4 a = *reinterpret_cast<const float4*>(src);
-    float4 b = *reinterpret_cast<const float4*>(src + 4);
-    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
-  } else {
-    for (int e = 0; e < 8; ++e) f[e] = e < valid ? src[e] : 0.f;
-  }
-  uint32_t w[4];
-  for (int e = 0; e < 4; ++e) w[e] = (uint32_t)f2bf(f[2 * e]) | ((uint32_t)f2bf(f[2 * e + 1]) << 16);
-  return make_uint4(w[0], w[1], w[2], w[3]);
-}
 
 template <typename T>
 __device__ __forceinline__ float to_f32(T x);
@@ -116,5 +57,188 @@ template <>
 __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <>
 __device__ __forceinline__ uint16_t from_f32<uint16_t>(float x) { return f2bf(x); }
+
+// ---------------------------------------------------------------- LDS tiles
+
+// Layouts of one LDS stage holding ROWS rows (M or N side of the output) by BK values of K:
+//   kRK   [row][k], filled by 16-byte vectors that run along k          (both operands of the
+//         forward cell and of dz . W^T: rows gathered from the pools, weights n-major)
+//   kKR   [k][row], filled by vectors along rows; fp32 only (one K value per lane and
+//         instruction, so the fragment read is one dword per lane)   (fp32 weight gradients)
+//   kRKT  [row][k], filled by vectors along rows scattered element by element
+//         (bf16 weight gradients, whose operands arrive row-major in K)
+enum { kRK = 0, kKR = 1, kRKT = 2 };
+
+template <typename T, int ROWS, int LAYOUT>
+struct Tile {
+  using M = Mma<T>;
+  static constexpr int BK = M::BK, VEC = M::VEC;
+  static constexpr int NVEC = ROWS * BK / VEC;
+  static constexpr int PT = NVEC / 256;  // vectors per thread and stage
+  static_assert(NVEC % 256 == 0, "tile must split evenly over 256 threads");
+  static_assert(LAYOUT != kKR || sizeof(T) == 4, "k-major tiles are fp32 only");
+  static constexpr int VROW = LAYOUT == kRK ? BK / VEC : ROWS / VEC;  // vectors per source line
+  // fp32 [row][k]: rows of 34 dwords (8-byte aligned, written as two 8-byte halves); bf16 [row][k]:
+  // rows of 72 halves (16-byte aligned).  k-major rows of ROWS + 32 dwords keep a fragment read
+  // (32 consecutive rows at k, then at k + 1) on distinct banks.
+  static constexpr int PITCH = LAYOUT == kKR ? ROWS + 32 : (sizeof(T) == 4 ? BK + 2 : BK + 8);
+  static constexpr int ELEMS = LAYOUT == kKR ? BK * PITCH : ROWS * PITCH;
+
+  __device__ static __forceinline__ void store(T* lds, int i, uint4 x) {
+    const int a = i / VROW, b = i - a * VROW;
+    if constexpr (LAYOUT == kRK) {
+      T* d = lds + a * PITCH + b * VEC;
+      if constexpr (sizeof(T) == 4) {
+        reinterpret_cast<uint2*>(d)[0] = make_uint2(x.x, x.y);
+        reinterpret_cast<uint2*>(d)[1] = make_uint2(x.z, x.w);
+      } else {
+        *reinterpret_cast<uint4*>(d) = x;
+      }
+    } else if constexpr (LAYOUT == kKR) {
+      *reinterpret_cast<uint4*>(lds + a * PITCH + b * VEC) = x;
+    } else {
+      const T* e = reinterpret_cast<const T*>(&x);
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) lds[(b * VEC + q) * PITCH + a] = e[q];
+    }
+  }
+
+  __device__ static __forceinline__ typename M::frag frag(const T* lds, int row, int k) {
+    if constexpr (LAYOUT == kKR)
+      return lds[k * PITCH + row];
+    else
+      return M::load(lds + row * PITCH + k);
+  }
+};
+
+// acc[TM][TN] += A(rows of this wave) . B(cols of this wave)^T over one LDS stage.
+template <typename T, class TA, class TB, int TM, int TN>
+__device__ __forceinline__ void mma_stage(const T* As, const T* Bs, f32x16 (&acc)[TM][TN], int arow0, int brow0,
+                                          int lane) {
+  using M = Mma<T>;
+#pragma unroll
+  for (int ks = 0; ks < M::BK; ks += M::KSTEP) {
+    const int k = ks + (lane >> 5) * M::KPL;
+    typename M::frag a[TM], b[TN];
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) a[tm] = TA::frag(As, arow0 + tm * 32 + (lane & 31), k);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) b[tn] = TB::frag(Bs, brow0 + tn * 32 + (lane & 31), k);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = M::mma(a[tm], b[tn], acc[tm][tn]);
+  }
+}
+
+// ---------------------------------------------------------------- prefetch registers
+// Loads issued for the next stage must not be followed by branches that consume them, or the compiler
+// waits for each load before the next one is issued.  So every fetch loads unconditionally from an
+// address that is always valid (out-of-range rows and columns are clamped to a real element) and
+// records how many of the fetched elements are real; masking and conversion happen when the registers
+// are written to LDS, one stage later.
+struct Raw4 {  // 16 bytes of operand data, nv leading elements valid
+  uint4 x;
+  int nv;
+};
+struct Raw8 {  // eight fp32 values that become eight bf16, nv leading elements valid
+  uint4 x0, x1;
+  int nv;
+};
+
+// zero the elements of a 16-byte vector of T from index nv on
+template <typename T>
+__device__ __forceinline__ uint4 mask_tail(uint4 v, int nv) {
+  constexpr int VEC = 16 / sizeof(T);
+  if (nv >= VEC) return v;
+  uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  if constexpr (sizeof(T) == 4) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = e < nv ? w[e] : 0u;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t lo = (2 * e < nv) ? 0x0000ffffu : 0u, hi = (2 * e + 1 < nv) ? 0xffff0000u : 0u;
+      w[e] &= lo | hi;
+    }
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// an operand already in the LDS element type
+template <typename T>
+__device__ __forceinline__ uint4 finish(const Raw4& r) {
+  return mask_tail<T>(r.x, r.nv);
+}
+
+// fp32 values rounded to bf16 (round to nearest even)
+__device__ __forceinline__ uint4 finish_bf16(const Raw8& r) {
+  const uint32_t in[8] = {r.x0.x, r.x0.y, r.x0.z, r.x0.w, r.x1.x, r.x1.y, r.x1.z, r.x1.w};
+  uint32_t w[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float a = 2 * e < r.nv ? __uint_as_float(in[2 * e]) : 0.f;
+    const float b = 2 * e + 1 < r.nv ? __uint_as_float(in[2 * e + 1]) : 0.f;
+    w[e] = (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// Row indices that a kernel reads from global memory before it can fetch a stage (the weight
+// gradients' gathered rows) travel two stages ahead: loaded into registers at stage c, written to
+// one of three LDS slots at the end of stage c, read by the fetch of stage c + 2 issued during
+// stage c + 1.  Kernels without such indices use NoIndex.
+struct NoIndex {
+  __device__ void prologue(int) {}
+  __device__ void load(int) {}
+  __device__ void store(int) {}
+};
+
+// ---------------------------------------------------------------- the K loop
+
+// K loop over `nchunks` LDS stages.  The global loads of stage c+1 are issued (into registers)
+// right after stage c becomes visible in LDS, so their latency hides behind stage c's MFMAs.
+// la / lb: fetch(c, i) -> raw registers of the i-th 16-byte vector of stage c; put(raw) -> uint4.
+template <typename T, class TA, class TB, int TM, int TN, class LA, class LB, class IX>
+__device__ __forceinline__ void mainloop(int nchunks, LA& la, LB& lb, IX& ix, T* As, T* Bs,
+                                         f32x16 (&acc)[TM][TN], int arow0, int brow0) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  ix.prologue(nchunks);
+  typename LA::raw ra[TA::PT];
+  typename LB::raw rb[TB::PT];
+  if (nchunks > 0) {
+#pragma unroll
+    for (int i = 0; i < TA::PT; ++i) ra[i] = la.fetch(0, tid + i * 256);
+#pragma unroll
+    for (int i = 0; i < TB::PT; ++i) rb[i] = lb.fetch(0, tid + i * 256);
+  }
+  for (int c = 0; c < nchunks; ++c) {
+    if (c + 2 < nchunks) ix.load(c + 2);
+#pragma unroll
+    for (int i = 0; i < TA::PT; ++i) TA::store(As, tid + i * 256, la.put(ra[i]));
+#pragma unroll
+    for (int i = 0; i < TB::PT; ++i) TB::store(Bs, tid + i * 256, lb.put(rb[i]));
+    __syncthreads();
+    if (c + 1 < nchunks) {
+#pragma unroll
+      for (int i = 0; i < TA::PT; ++i) ra[i] = la.fetch(c + 1, tid + i * 256);
+#pragma unroll
+      for (int i = 0; i < TB::PT; ++i) rb[i] = lb.fetch(c + 1, tid + i * 256);
+    }
+    mma_stage<T, TA, TB, TM, TN>(As, Bs, acc, arow0, brow0, lane);
+    if (c + 2 < nchunks) ix.store(c + 2);
+    __syncthreads();
+  }
+}
+
+template <int TM, int TN>
+__device__ __forceinline__ void zero_acc(f32x16 (&acc)[TM][TN]) {
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[tm][tn][r] = 0.f;
+}
 
 }  // namespace fold

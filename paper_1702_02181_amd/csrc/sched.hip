@@ -423,12 +423,19 @@ __global__ void k_root_emit(const int* flag, const int* rank, const int* node_po
   if (v < N && flag[v]) root_pos[rank[v]] = node_pos[v];
 }
 
-__global__ void k_op_rows(const int* pos_group, const int* g_row_begin, const int* g_oprow, int N,
-                          int* op_rows) {
+__global__ void k_op_rows(const int* pos_group, const int* g_row_begin, const int* g_oprow, const int* g_op,
+                          const int* g_idx_off, const int* child_pos, const int* input_idx, OpTable ops, int N,
+                          int* op_rows, int* op_cpos, int* op_inp) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= N) return;
   const int g = pos_group[p];
-  op_rows[g_oprow[g] + (p - g_row_begin[g])] = p;
+  const int r = p - g_row_begin[g];
+  const int q = g_oprow[g] + r;
+  const int a = ops.arity[g_op[g]];
+  op_rows[q] = p;
+  op_cpos[2 * q] = a > 0 ? child_pos[g_idx_off[g] + r * a] : -1;
+  op_cpos[2 * q + 1] = a > 1 ? child_pos[g_idx_off[g] + r * a + 1] : -1;
+  op_inp[q] = input_idx[p];
 }
 
 inline dim3 grid_for(long long n) { return dim3((unsigned)std::max(1LL, (n + kBlock - 1) / kBlock)); }
@@ -488,6 +495,11 @@ static void sched_destroy(fold_sched* h) { sched_destroy_impl(h); }
 
 int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   const int N = b->num_nodes, E = b->num_edges, G = b->num_graphs, K = b->num_ops;
+  for (int i = 0; i < K; ++i)
+    if (b->ops[i].arity > 2) {
+      set_error("fold_schedule: operations take at most two children");
+      return FOLD_E_INVALID;
+    }
   if (K > kMaxOps) {
     set_error("fold_schedule: at most 64 operations are supported");
     return FOLD_E_INVALID;
@@ -512,7 +524,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   };
 
   // persistent arrays sized by N and E
-  const size_t n1 = (size_t)N * 7 + (size_t)E + 8;
+  const size_t n1 = (size_t)N * 10 + (size_t)E + 8;
   if (hipMalloc(&s.blob, n1 * sizeof(int)) != hipSuccess) {
     set_error("fold_schedule: out of device memory");
     return fail(FOLD_E_NOMEM);
@@ -526,6 +538,8 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   s.child_pos = q; q += E;
   s.pos_group = q; q += N;
   s.op_rows = q; q += N;
+  s.op_cpos = q; q += 2 * (size_t)N;
+  s.op_inp = q; q += N;
 
   Temp tmp(st);
   unsigned long long* err = nullptr;
@@ -712,8 +726,8 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   s.g_idx_off = s.g_rows + ngc;
   const int* g_oprow = s.g_idx_off + ngc;
   if (N > 0) {
-    hipLaunchKernelGGL(k_op_rows, grid_for(N), dim3(kBlock), 0, st, s.pos_group, s.g_row_begin, g_oprow, N,
-                       s.op_rows);
+    hipLaunchKernelGGL(k_op_rows, grid_for(N), dim3(kBlock), 0, st, s.pos_group, s.g_row_begin, g_oprow, s.g_op,
+                       s.g_idx_off, s.child_pos, s.input_idx, ops, N, s.op_rows, s.op_cpos, s.op_inp);
     if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess) {
       set_error("fold_schedule: device error while listing rows per op");
       return fail(FOLD_E_DEVICE);

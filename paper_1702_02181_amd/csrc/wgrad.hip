@@ -23,82 +23,184 @@ namespace fold {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTile = 64;
+
+// Workgroup tile: 128 weight rows (m) x 256 gate columns (n); waves 2 x 2, each 64 x 128.
+constexpr int kTM = 128, kTN = 256;
+
+// Row indices of the pool rows a stage reduces over (pool row, child 0 / input row, child 1),
+// loaded two stages ahead into one of three LDS slots.
+template <int BK>
+struct WgIndex {
+  int (*slots)[3][BK];
+  const int* op_rows;
+  const int* op_cpos;
+  const int* op_inp;
+  int lo, hi, seg;
+  int rp, r0, r1, ok;
+  __device__ __forceinline__ void load(int c) {
+    const int t = threadIdx.x % BK;  // every thread loads (no branch around the loads); BK of them store
+    const int r = lo + c * BK + t;
+    ok = r < hi;
+    const int rc = ok ? r : lo;
+    rp = op_rows[rc];
+    if (seg) {
+      r0 = op_cpos[2 * rc];
+      r1 = op_cpos[2 * rc + 1];
+    } else {
+      r0 = op_inp[rc];
+      r1 = -1;
+    }
+  }
+  __device__ __forceinline__ void store(int c) {
+    const int t = threadIdx.x;
+    if (t < BK) {
+      slots[c % 3][0][t] = ok ? rp : -1;
+      slots[c % 3][1][t] = ok ? r0 : -1;
+      slots[c % 3][2][t] = ok ? r1 : -1;
+    }
+  }
+  __device__ __forceinline__ void prologue(int nst) {
+    for (int c = 0; c < 2 && c < nst; ++c) {
+      load(c);
+      store(c);
+    }
+    __syncthreads();
+  }
+};
+
+// X^T operand: gathered children's h rows (seg 1) or leaf-table rows (seg 0)
+template <typename T, int BK, int VROW>
+struct WgX {
+  using raw = Raw4;
+  const T* src;
+  int sld, width, HP, Kw, m0, seg;
+  int (*slots)[3][BK];
+  __device__ __forceinline__ raw fetch(int c, int i) const {
+    constexpr int VEC = Mma<T>::VEC;
+    const int kk = i / VROW, v = i - kk * VROW;
+    const int m = m0 + v * VEC;
+    const int k = seg ? min(m / HP, 1) : 0;
+    const int jin = seg ? m - k * HP : m;
+    const int s = slots[c % 3][1 + k][kk];
+    const int nv = (s >= 0 && m < Kw) ? min(max(width - jin, 0), VEC) : 0;
+    const size_t off = nv > 0 ? (size_t)s * sld + jin : 0;
+    return {*reinterpret_cast<const uint4*>(src + off), nv};
+  }
+  __device__ __forceinline__ uint4 put(const raw& r) const { return finish<T>(r); }
+};
+
+// dz^T operand; the fp32 values also feed the bias column sums
+template <typename T, int BK, int VROW>
+struct WgDz;
+
+template <int BK, int VROW>
+struct WgDz<float, BK, VROW> {
+  using raw = Raw4;
+  const float* dz;
+  int gstride, Nw, n0;
+  int (*slots)[3][BK];
+  bool bias;
+  float bsum[4];
+  __device__ __forceinline__ raw fetch(int c, int i) const {
+    const int kk = i / VROW, v = i - kk * VROW;
+    const int p = slots[c % 3][0][kk];
+    const int n = n0 + v * 4;
+    const int ok = p >= 0 && n < Nw;
+    return {*reinterpret_cast<const uint4*>(dz + (ok ? (size_t)p * gstride + n : 0)), ok ? 4 : 0};
+  }
+  __device__ __forceinline__ uint4 put(const raw& r) {
+    const uint4 x = finish<float>(r);
+    if (bias) {
+      bsum[0] += __uint_as_float(x.x);
+      bsum[1] += __uint_as_float(x.y);
+      bsum[2] += __uint_as_float(x.z);
+      bsum[3] += __uint_as_float(x.w);
+    }
+    return x;
+  }
+};
+
+template <int BK, int VROW>
+struct WgDz<uint16_t, BK, VROW> {
+  using raw = Raw8;
+  const float* dz;
+  int gstride, Nw, n0;
+  int (*slots)[3][BK];
+  bool bias;
+  float bsum[8];
+  __device__ __forceinline__ raw fetch(int c, int i) const {
+    const int kk = i / VROW, v = i - kk * VROW;
+    const int p = slots[c % 3][0][kk];
+    const int n = n0 + v * 8;
+    const int ok = p >= 0 && n < Nw;
+    const float* q = dz + (ok ? (size_t)p * gstride + n : 0);
+    return {reinterpret_cast<const uint4*>(q)[0], reinterpret_cast<const uint4*>(q)[1], ok ? 8 : 0};
+  }
+  __device__ __forceinline__ uint4 put(const raw& r) {
+    if (bias && r.nv > 0) {
+      const uint32_t in[8] = {r.x0.x, r.x0.y, r.x0.z, r.x0.w, r.x1.x, r.x1.y, r.x1.z, r.x1.w};
+#pragma unroll
+      for (int q = 0; q < 8; ++q) bsum[q] += __uint_as_float(in[q]);
+    }
+    return finish_bf16(r);
+  }
+};
 
 template <typename T>
 __global__ __launch_bounds__(kThreads) void k_wgrad(WgArgs a) {
   using M = Mma<T>;
-  constexpr int BK = M::BK, VEC = M::VEC, PITCH = BK + M::PAD;
-  __shared__ __attribute__((aligned(16))) T As[kTile * PITCH];  // As[m][k] = X[row k][m]
-  __shared__ __attribute__((aligned(16))) T Bs[kTile * PITCH];  // Bs[n][k] = dz[row k][n]
-  __shared__ int prow[BK], srow[BK];
+  constexpr int BK = M::BK, VEC = M::VEC;
+  constexpr int LAY = sizeof(T) == 4 ? kKR : kRKT;
+  using TA = Tile<T, kTM, LAY>;  // X^T: weight rows x pool rows
+  using TB = Tile<T, kTN, LAY>;  // dz^T: gate columns x pool rows
+  __shared__ __attribute__((aligned(16))) T As[TA::ELEMS];
+  __shared__ __attribute__((aligned(16))) T Bs[TB::ELEMS];
+  __shared__ int slots[3][3][BK];
+  __shared__ float red[256 / TB::VROW][kTN];
+
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wn = wave >> 1;
   const int chunk_id = blockIdx.x;
-  const int m0 = blockIdx.y * kTile, n0 = blockIdx.z * kTile;
-  const int k = a.seg ? m0 / a.HP : 0;
-  const int jin0 = a.seg ? m0 - k * a.HP : m0;
-  const int width = a.seg ? a.H : a.in_dim;
-  const int sld = a.seg ? a.ld : a.tld;
-  const T* src = static_cast<const T*>(a.src);
+  const int m0 = blockIdx.y * kTM, n0 = blockIdx.z * kTN;
   const int lo = chunk_id * a.chunk, hi = min(a.count, lo + a.chunk);
+  const bool do_bias = a.bpart != nullptr && blockIdx.y == 0;
 
-  f32x16 acc;
-  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  WgIndex<BK> ix{slots, a.op_rows, a.op_cpos, a.op_inp, lo, hi, a.seg, 0, 0, 0, 0};
+  WgX<T, BK, TA::VROW> la{static_cast<const T*>(a.src), a.seg ? a.ld : a.tld, a.seg ? a.H : a.in_dim, a.HP,
+                          a.Kw, m0, a.seg, slots};
+  WgDz<T, BK, TB::VROW> lb{a.dz, a.gstride, a.Nw, n0, slots, do_bias, {}};
+#pragma unroll
+  for (int q = 0; q < VEC; ++q) lb.bsum[q] = 0.f;
+  f32x16 acc[2][4];
+  zero_acc(acc);
+  const int nst = (hi - lo + BK - 1) / BK;
+  mainloop<T, TA, TB, 2, 4>(nst, la, lb, ix, As, Bs, acc, wm * 64, wn * 128);
 
-  for (int r0 = lo; r0 < hi; r0 += BK) {
-    if (tid < BK) {
-      const int i = r0 + tid;
-      int p = -1, s = -1;
-      if (i < hi) {
-        p = a.op_rows[i];
-        if (a.seg) {
-          const int g = a.pos_group[p];
-          s = a.child_pos[a.g_idx_off[g] + (p - a.g_row_begin[g]) * a.arity + k];
-        } else {
-          s = a.input_idx[p];
-        }
-      }
-      prow[tid] = p;
-      srow[tid] = s;
-    }
-    __syncthreads();
-    constexpr int AV = kTile / VEC;  // vectors per row of the X tile
-    for (int i = tid; i < BK * AV; i += kThreads) {
-      const int kk = i / AV, v = i - kk * AV;
-      const int s = srow[kk];
-      uint4 x = make_uint4(0u, 0u, 0u, 0u);
-      if (s >= 0) x = load_row_vec<T>(src + (size_t)s * sld, jin0 + v * VEC, width);
-      const T* e = reinterpret_cast<const T*>(&x);
-#pragma unroll
-      for (int q = 0; q < VEC; ++q) As[(v * VEC + q) * PITCH + kk] = e[q];
-    }
-    constexpr int BV = kTile / 4;  // float4 per row of the dz tile
-    for (int i = tid; i < BK * BV; i += kThreads) {
-      const int kk = i / BV, v = i - kk * BV;
-      const int p = prow[kk];
-      float4 f = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (p >= 0) f = *reinterpret_cast<const float4*>(a.dz + (size_t)p * a.gstride + n0 + v * 4);
-      Bs[(v * 4 + 0) * PITCH + kk] = from_f32<T>(f.x);
-      Bs[(v * 4 + 1) * PITCH + kk] = from_f32<T>(f.y);
-      Bs[(v * 4 + 2) * PITCH + kk] = from_f32<T>(f.z);
-      Bs[(v * 4 + 3) * PITCH + kk] = from_f32<T>(f.w);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int ks = 0; ks < BK; ks += M::KSTEP) {
-      const typename M::frag af = M::load(&As[(wm * 32 + (lane & 31)) * PITCH + ks + (lane >> 5) * M::KPL]);
-      const typename M::frag bf = M::load(&Bs[(wn * 32 + (lane & 31)) * PITCH + ks + (lane >> 5) * M::KPL]);
-      acc = M::mma(af, bf, acc);
-    }
-    __syncthreads();
-  }
   float* out = a.partial + (size_t)chunk_id * a.Kw * a.Nw;
-  const int n = n0 + wn * 32 + (lane & 31);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int m = m0 + wm * 32 + acc_row(r, lane);
-    out[(size_t)m * a.Nw + n] = acc[r];
+  for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < 4; ++tn) {
+      const int n = n0 + wn * 128 + tn * 32 + (lane & 31);
+      if (n >= a.Nw) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 64 + tm * 32 + acc_row(r, lane);
+        if (m < a.Kw) out[(size_t)m * a.Nw + n] = acc[tm][tn][r];
+      }
+    }
+  if (do_bias) {
+    // every thread's dz vectors share one column group (TB::VROW divides the block), so the column
+    // sums finish with a fixed-order reduction over the threads of that group
+    const int v = tid % TB::VROW, j = tid / TB::VROW;
+#pragma unroll
+    for (int q = 0; q < VEC; ++q) red[j][v * VEC + q] = lb.bsum[q];
+    __syncthreads();
+    for (int col = tid; col < kTN; col += kThreads) {
+      float s = 0.f;
+      for (int jj = 0; jj < 256 / TB::VROW; ++jj) s += red[jj][col];
+      if (n0 + col < a.Nw) a.bpart[(size_t)chunk_id * a.Nw + n0 + col] = s;
+    }
   }
 }
 
@@ -152,9 +254,9 @@ __global__ void k_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int
 WgradSplit wgrad_split(int count, int Kw, int Nw) {
   WgradSplit w;
   if (count <= 0 || Kw <= 0 || Nw <= 0) return w;
-  const long long tiles = (long long)(Kw / kTile) * (Nw / kTile);
-  long long want = (2048 + tiles - 1) / tiles;  // enough workgroups to fill the chip
-  long long most = std::max(1, (count + 255) / 256);
+  const long long tiles = (long long)((Kw + kTM - 1) / kTM) * ((Nw + kTN - 1) / kTN);
+  const long long want = (1024 + tiles - 1) / tiles;  // enough workgroups to fill the chip
+  const long long most = std::max(1, (count + 511) / 512);
   w.nchunk = (int)std::max(1LL, std::min(want, most));
   w.chunk = round_up((count + w.nchunk - 1) / w.nchunk, 64);
   w.nchunk = (count + w.chunk - 1) / w.chunk;
@@ -164,7 +266,7 @@ WgradSplit wgrad_split(int count, int Kw, int Nw) {
 void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st) {
   if (a.count <= 0) return;
   ProfScope prof(dtype == FOLD_BF16 ? "wgrad.bf16" : "wgrad.f32", st);
-  dim3 grid(a.nchunk, a.Kw / kTile, a.Nw / kTile);
+  dim3 grid(a.nchunk, (a.Kw + kTM - 1) / kTM, (a.Nw + kTN - 1) / kTN);
   if (dtype == FOLD_BF16)
     hipLaunchKernelGGL(k_wgrad<uint16_t>, grid, dim3(kThreads), 0, st, a);
   else
@@ -180,12 +282,17 @@ void launch_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int s
                      G, dW);
 }
 
-void launch_bias_grad(const int* op_rows, int count, int chunk, int nchunk, const float* dz, int gstride, int Nw,
-                      float* bpart, int G, int H, int HP, float* dbias, hipStream_t st) {
+void launch_bias_partial(const int* op_rows, int count, int chunk, int nchunk, const float* dz, int gstride, int Nw,
+                         float* bpart, hipStream_t st) {
   if (count <= 0) return;
-  ProfScope prof("bias_grad", st);
+  ProfScope prof("bias_partial", st);
   hipLaunchKernelGGL(k_bias_partial, dim3(nchunk, (Nw + 255) / 256), dim3(256), 0, st, op_rows, count, chunk, dz,
                      gstride, Nw, bpart);
+}
+
+void launch_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, float* dbias, hipStream_t st) {
+  if (nchunk <= 0) return;
+  ProfScope prof("bias_reduce", st);
   hipLaunchKernelGGL(k_bias_reduce, dim3((Nw + 255) / 256), dim3(256), 0, st, bpart, nchunk, Nw, H, HP, dbias);
 }
 

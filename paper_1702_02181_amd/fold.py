@@ -89,7 +89,8 @@ class FoldError(RuntimeError):
 
 EXPORTS = ["fold_schedule", "fold_sched_get_info", "fold_sched_free", "fold_pack_params",
            "fold_packed_free", "fold_row_ld", "fold_workspace_size", "fold_forward",
-           "fold_backward", "fold_last_error", "fold_profile_enable", "fold_profile_read"]
+           "fold_backward", "fold_last_error", "fold_profile_enable", "fold_profile_read",
+           "fold_probe_mfma", "fold_probe_copy"]
 
 _lib = None
 
@@ -129,6 +130,10 @@ def lib():
     L.fold_profile_enable.argtypes = [c_int32]
     L.fold_profile_read.restype = c_int32
     L.fold_profile_read.argtypes = [POINTER(fold_kernel_stat), c_int32, POINTER(c_int32)]
+    L.fold_probe_mfma.restype = c_int32
+    L.fold_probe_mfma.argtypes = [c_int32, c_void_p, POINTER(ctypes.c_double)]
+    L.fold_probe_copy.restype = c_int32
+    L.fold_probe_copy.argtypes = [c_void_p, c_void_p, c_size_t, c_void_p, POINTER(ctypes.c_double)]
     _lib = L
     return L
 
@@ -154,6 +159,18 @@ def fold_profile_read() -> dict:
     _check(lib().fold_profile_read(arr, cap, byref(n)))
     return {arr[i].name.decode(): (int(arr[i].launches), float(arr[i].total_ms), float(arr[i].max_ms))
             for i in range(min(n.value, cap))}
+
+
+def fold_probe_mfma(dtype: int, stream=None) -> float:
+    t = ctypes.c_double()
+    _check(lib().fold_probe_mfma(int(dtype), _stream(stream), byref(t)))
+    return float(t.value)
+
+
+def fold_probe_copy(dst, src, nbytes: int, stream=None) -> float:
+    g = ctypes.c_double()
+    _check(lib().fold_probe_copy(_ptr(dst), _ptr(src), int(nbytes), _stream(stream), byref(g)))
+    return float(g.value)
 
 
 def fold_row_ld(width: int) -> int:
