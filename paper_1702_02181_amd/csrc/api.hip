@@ -142,7 +142,18 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
   auto al = [](size_t x) { return (x + 255) / 256 * 256; };
   w.gates_off = 0;
   w.gates_bytes = al(N * w.gstride * sizeof(float));
-  w.dh_off = w.gates_bytes;
+  size_t zp = 0;
+  for (int g = 0; g < s.num_groups; ++g) {
+    const fold_op& op = s.ops[s.h_op[g]];
+    if (op.kind == FOLD_EMBED || op.param_set >= (int)p.sets.size()) continue;
+    const PackedSet& ps = p.sets[op.param_set];
+    const FwdPlan pl = fwd_plan(s.h_rows[g], p.HP, op.has_input ? ps.INP : 0, op.arity,
+                                p.dtype == FOLD_BF16 ? 2 : 4, true);
+    if (pl.ksplit > 1) zp = std::max(zp, (size_t)pl.ksplit * s.h_rows[g] * ps.G * p.HP);
+  }
+  w.zpart_off = w.gates_bytes;
+  w.zpart_bytes = al(zp * sizeof(float));
+  w.dh_off = w.zpart_off + w.zpart_bytes;
   w.dc_off = w.dh_off + al(N * p.ld * sizeof(float));
   w.acc_bytes = w.dc_off + al(N * p.ld * sizeof(float)) - w.dh_off;
   size_t part = 0, bpart = 0;
@@ -169,7 +180,7 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
   w.part_bytes = al(part * sizeof(float));
   w.bpart_off = w.part_off + w.part_bytes;
   w.bpart_bytes = al(bpart * sizeof(float));
-  w.fwd_bytes = w.gates_bytes;
+  w.fwd_bytes = w.gates_bytes + w.zpart_bytes;
   w.bwd_bytes = w.bpart_off + w.bpart_bytes;
   return w;
 }
@@ -235,9 +246,11 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
                      float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st) {
   const WsLayout L = workspace_layout(s, p);
   float* gates = nullptr;
+  float* zpart = nullptr;
   if (ws) {
     if (ws_bytes < L.fwd_bytes) return fail(FOLD_E_MISMATCH, "fold_forward: workspace too small");
     gates = reinterpret_cast<float*>(static_cast<char*>(ws) + L.gates_off);
+    zpart = reinterpret_cast<float*>(static_cast<char*>(ws) + L.zpart_off);
   }
   const int tw = table_width(s, p);
   const int tld = row_ld(tw);
@@ -270,6 +283,7 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
     a.bias = ps.bias;
     a.gates = gates;
     a.gstride = L.gstride;
+    a.zpart = zpart;
     launch_cell_fwd(p.dtype, op.kind, a, st);
   }
   if (roots_out) launch_roots(p.dtype, s.R, p.ld, s.root_pos, h_pool, roots_out, st);

@@ -28,6 +28,8 @@ namespace {
 
 constexpr int kThreads = 256;
 
+inline unsigned cdiv(long long a, long long b) { return (unsigned)((a + b - 1) / b); }
+
 template <int KIND>
 struct Gates {
   static constexpr int G = KIND == FOLD_TREELSTM ? 5 : (KIND == FOLD_LSTM ? 4 : 1);
@@ -61,10 +63,11 @@ struct FwdA {
   int tld, ld, in_dim, H, has_input;
   FwdStages st;
   const int (*srow)[BM];
+  int c0;  // first stage of this workgroup's K slice
   __device__ __forceinline__ raw fetch(int c, int i) const {
     constexpr int BK = Mma<T>::BK, VEC = Mma<T>::VEC;
     int seg, kc, kbase;
-    st.at(c, BK, seg, kc, kbase);
+    st.at(c + c0, BK, seg, kc, kbase);
     const int r = i / VROW, v = i - r * VROW;
     const int sr = srow[seg][r];
     const bool is_in = has_input && seg == 0;
@@ -85,17 +88,79 @@ struct WeightB {
   const T* W;
   int ldk;
   FwdStages st;
+  int c0;
   __device__ __forceinline__ raw fetch(int c, int i) const {
     constexpr int BK = Mma<T>::BK, VEC = Mma<T>::VEC;
     int seg, kc, kbase;
-    st.at(c, BK, seg, kc, kbase);
+    st.at(c + c0, BK, seg, kc, kbase);
     const int n = i / VROW, v = i - n * VROW;
     return {*reinterpret_cast<const uint4*>(W + (size_t)n * ldk + kbase + kc + v * VEC), VEC};
   }
   __device__ __forceinline__ uint4 put(const raw& r) const { return r.x; }
 };
 
-template <typename T, int KIND, int MT>
+// The cell on one (row, unit) given z (bias included): writes h, c and the saved activations.
+template <typename T, int KIND>
+__device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const float* z) {
+  const size_t p = (size_t)(a.row_begin + row);
+  float h, c;
+  float* gs = a.gates ? a.gates + p * a.gstride + j : nullptr;
+  if constexpr (KIND == FOLD_TREELSTM) {
+    const float i_ = sigmoidf_(z[0]), fl = sigmoidf_(z[1]), fr = sigmoidf_(z[2]), o = sigmoidf_(z[3]);
+    const float u = tanhf_(z[4]);
+    float cl = 0.f, cr = 0.f;
+    if (a.arity == 2) {
+      const int pl = a.child_pos[a.idx_off + row * 2], pr = a.child_pos[a.idx_off + row * 2 + 1];
+      if (pl >= 0) cl = a.c_pool[(size_t)pl * a.ld + j];
+      if (pr >= 0) cr = a.c_pool[(size_t)pr * a.ld + j];
+    }
+    c = i_ * u + fl * cl + fr * cr;
+    h = o * tanhf_(c);
+    if (gs) {
+      gs[0] = i_;
+      gs[a.HP] = fl;
+      gs[2 * a.HP] = fr;
+      gs[3 * a.HP] = o;
+      gs[4 * a.HP] = u;
+    }
+  } else if constexpr (KIND == FOLD_LSTM) {
+    const float i_ = sigmoidf_(z[0]), f = sigmoidf_(z[1]), o = sigmoidf_(z[2]);
+    const float u = tanhf_(z[3]);
+    const int pc = a.child_pos[a.idx_off + row];
+    const float cp = pc >= 0 ? a.c_pool[(size_t)pc * a.ld + j] : 0.f;
+    c = i_ * u + f * cp;
+    h = o * tanhf_(c);
+    if (gs) {
+      gs[0] = i_;
+      gs[a.HP] = f;
+      gs[2 * a.HP] = o;
+      gs[3 * a.HP] = u;
+    }
+  } else {
+    h = tanhf_(z[0]);
+    c = 0.f;
+    if constexpr (KIND == FOLD_PROJ) {
+      const int pc = a.child_pos[a.idx_off + row];
+      c = pc >= 0 ? a.c_pool[(size_t)pc * a.ld + j] : 0.f;
+    }
+    if (gs) gs[0] = h;
+  }
+  static_cast<T*>(a.h_pool)[p * a.ld + j] = from_f32<T>(h);
+  a.c_pool[p * a.ld + j] = c;
+}
+
+// pad columns of the pools (H <= j < ld) are written as zero
+template <typename T>
+__device__ __forceinline__ void pad_out(const FwdArgs& a, int row, int j) {
+  const size_t p = (size_t)(a.row_begin + row);
+  static_cast<T*>(a.h_pool)[p * a.ld + j] = from_f32<T>(0.f);
+  a.c_pool[p * a.ld + j] = 0.f;
+}
+
+// SPLIT: the K loop is cut into gridDim.z slices; each workgroup writes its partial z (no bias) to
+// a.zpart[slice][row][g * HP + j] and k_cell_epi finishes the cell.  Used for narrow levels, whose
+// few row tiles would otherwise leave most compute units idle for a whole K loop.
+template <typename T, int KIND, int MT, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   using M = Mma<T>;
   constexpr int G = Gates<KIND>::G;
@@ -125,83 +190,77 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   __syncthreads();
 
   FwdStages st{a.has_input ? a.INP / M::BK : 0, a.HP / M::BK, a.has_input, a.INP, a.HP};
-  const int nchunks = st.cin + a.arity * st.chp;
+  const int nst = st.cin + a.arity * st.chp;
+  int c0 = 0, c1 = nst;
+  if constexpr (SPLIT) {
+    const int per = (nst + gridDim.z - 1) / gridDim.z;
+    c0 = min(nst, (int)blockIdx.z * per);
+    c1 = min(nst, c0 + per);
+  }
   FwdA<T, BM, TA::VROW> la{static_cast<const T*>(a.table), static_cast<const T*>(a.h_pool), a.tld, a.ld,
-                           a.in_dim, a.H, a.has_input, st, srow};
-  WeightB<T, TB::VROW> lb{static_cast<const T*>(a.Wf) + (size_t)ub * BN * a.Kf, a.Kf, st};
+                           a.in_dim, a.H, a.has_input, st, srow, c0};
+  WeightB<T, TB::VROW> lb{static_cast<const T*>(a.Wf) + (size_t)ub * BN * a.Kf, a.Kf, st, c0};
   NoIndex ix;
   f32x16 acc[MT][G];
   zero_acc(acc);
-  mainloop<T, TA, TB, MT, G>(nchunks, la, lb, ix, As, Bs, acc, wave * 32 * MT, 0);
+  mainloop<T, TA, TB, MT, G>(c1 - c0, la, lb, ix, As, Bs, acc, wave * 32 * MT, 0);
 
-  // epilogue: the cell, in registers
   const int j = ub * 32 + (lane & 31);
+  if constexpr (SPLIT) {
+    const int zs = G * a.HP;
+    float* zp = a.zpart + (size_t)blockIdx.z * a.rows * zs + j;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wave * 32 * MT + mt * 32 + acc_row(r, lane);
+        if (row >= a.rows) continue;
+#pragma unroll
+        for (int g = 0; g < G; ++g) zp[(size_t)row * zs + g * a.HP] = acc[mt][g][r];
+      }
+    return;
+  }
+  // epilogue: the cell, in registers
   float bz[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) bz[g] = a.bias[g * a.HP + j];
-  T* hp = static_cast<T*>(a.h_pool);
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = m0 + wave * 32 * MT + mt * 32 + acc_row(r, lane);
       if (row >= a.rows) continue;
-      const size_t p = (size_t)(a.row_begin + row);
       if (j >= a.H) {
-        if (j < a.ld) {
-          hp[p * a.ld + j] = from_f32<T>(0.f);
-          a.c_pool[p * a.ld + j] = 0.f;
-        }
+        if (j < a.ld) pad_out<T>(a, row, j);
         continue;
       }
       float z[G];
 #pragma unroll
       for (int g = 0; g < G; ++g) z[g] = acc[mt][g][r] + bz[g];
-      float h, c;
-      float* gs = a.gates ? a.gates + p * a.gstride + j : nullptr;
-      if constexpr (KIND == FOLD_TREELSTM) {
-        const float i_ = sigmoidf_(z[0]), fl = sigmoidf_(z[1]), fr = sigmoidf_(z[2]), o = sigmoidf_(z[3]);
-        const float u = tanhf_(z[4]);
-        float cl = 0.f, cr = 0.f;
-        if (a.arity == 2) {
-          const int pl = a.child_pos[a.idx_off + row * 2], pr = a.child_pos[a.idx_off + row * 2 + 1];
-          if (pl >= 0) cl = a.c_pool[(size_t)pl * a.ld + j];
-          if (pr >= 0) cr = a.c_pool[(size_t)pr * a.ld + j];
-        }
-        c = i_ * u + fl * cl + fr * cr;
-        h = o * tanhf_(c);
-        if (gs) {
-          gs[0] = i_;
-          gs[a.HP] = fl;
-          gs[2 * a.HP] = fr;
-          gs[3 * a.HP] = o;
-          gs[4 * a.HP] = u;
-        }
-      } else if constexpr (KIND == FOLD_LSTM) {
-        const float i_ = sigmoidf_(z[0]), f = sigmoidf_(z[1]), o = sigmoidf_(z[2]);
-        const float u = tanhf_(z[3]);
-        const int pc = a.child_pos[a.idx_off + row];
-        const float cp = pc >= 0 ? a.c_pool[(size_t)pc * a.ld + j] : 0.f;
-        c = i_ * u + f * cp;
-        h = o * tanhf_(c);
-        if (gs) {
-          gs[0] = i_;
-          gs[a.HP] = f;
-          gs[2 * a.HP] = o;
-          gs[3 * a.HP] = u;
-        }
-      } else {
-        h = tanhf_(z[0]);
-        c = 0.f;
-        if constexpr (KIND == FOLD_PROJ) {
-          const int pc = a.child_pos[a.idx_off + row];
-          c = pc >= 0 ? a.c_pool[(size_t)pc * a.ld + j] : 0.f;
-        }
-        if (gs) gs[0] = h;
-      }
-      hp[p * a.ld + j] = from_f32<T>(h);
-      a.c_pool[p * a.ld + j] = c;
+      cell_out<T, KIND>(a, row, j, z);
     }
+  }
+}
+
+// finish a K-split level: sum the slices' partial z, add the bias, apply the cell
+template <typename T, int KIND>
+__global__ void k_cell_epi(FwdArgs a, int nsplit) {
+  constexpr int G = Gates<KIND>::G;
+  const int row = blockIdx.x;
+  const int zs = G * a.HP;
+  for (int j = threadIdx.x; j < a.HP; j += blockDim.x) {
+    if (j >= a.H) {
+      if (j < a.ld) pad_out<T>(a, row, j);
+      continue;
+    }
+    float z[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float v = a.bias[g * a.HP + j];
+      for (int sp = 0; sp < nsplit; ++sp) v += a.zpart[((size_t)sp * a.rows + row) * zs + g * a.HP + j];
+      z[g] = v;
+    }
+    cell_out<T, KIND>(a, row, j, z);
   }
 }
 
@@ -308,11 +367,11 @@ template <int VROW>
 struct DzRows<float, VROW> {
   using raw = Raw4;
   const float* dz;
-  int gstride, row_begin, rows, m0;
+  int gstride, row_begin, rows, m0, c0;
   __device__ __forceinline__ raw fetch(int c, int i) const {
     const int r = i / VROW, v = i - r * VROW, row = m0 + r;
     const int ok = row < rows;
-    const float* p = dz + (size_t)(row_begin + (ok ? row : 0)) * gstride + c * 32 + v * 4;
+    const float* p = dz + (size_t)(row_begin + (ok ? row : 0)) * gstride + (c + c0) * 32 + v * 4;
     return {*reinterpret_cast<const uint4*>(p), ok ? 4 : 0};
   }
   __device__ __forceinline__ uint4 put(const raw& r) const { return finish<float>(r); }
@@ -322,11 +381,11 @@ template <int VROW>
 struct DzRows<uint16_t, VROW> {
   using raw = Raw8;
   const float* dz;
-  int gstride, row_begin, rows, m0;
+  int gstride, row_begin, rows, m0, c0;
   __device__ __forceinline__ raw fetch(int c, int i) const {
     const int r = i / VROW, v = i - r * VROW, row = m0 + r;
     const int ok = row < rows;
-    const float* p = dz + (size_t)(row_begin + (ok ? row : 0)) * gstride + c * 64 + v * 8;
+    const float* p = dz + (size_t)(row_begin + (ok ? row : 0)) * gstride + (c + c0) * 64 + v * 8;
     return {reinterpret_cast<const uint4*>(p)[0], reinterpret_cast<const uint4*>(p)[1], ok ? 8 : 0};
   }
   __device__ __forceinline__ uint4 put(const raw& r) const { return finish_bf16(r); }
@@ -337,12 +396,13 @@ template <typename T, int VROW>
 struct WeightRows {
   using raw = Raw4;
   const T* W;
-  int Kb, Nb, n0;
+  int Kb, Nb, n0, c0;
   __device__ __forceinline__ raw fetch(int c, int i) const {
     constexpr int BK = Mma<T>::BK, VEC = Mma<T>::VEC;
     const int n = i / VROW, v = i - n * VROW;
     const int ok = n0 + n < Nb;
-    return {*reinterpret_cast<const uint4*>(W + (size_t)(ok ? n0 + n : 0) * Kb + c * BK + v * VEC), ok ? VEC : 0};
+    return {*reinterpret_cast<const uint4*>(W + (size_t)(ok ? n0 + n : 0) * Kb + (c + c0) * BK + v * VEC),
+            ok ? VEC : 0};
   }
   __device__ __forceinline__ uint4 put(const raw& r) const { return finish<T>(r); }
 };
@@ -358,12 +418,14 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx(DxArgs a) {
   __shared__ __attribute__((aligned(16))) T Bs[TB::ELEMS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
-  DzRows<T, TA::VROW> la{a.dz, a.gstride, a.row_begin, a.rows, m0};
-  WeightRows<T, TB::VROW> lb{static_cast<const T*>(a.Wb), a.Kb, a.Nb, n0};
+  const int nst = a.Kb / M::BK, per = (nst + gridDim.z - 1) / gridDim.z;
+  const int c0 = min(nst, (int)blockIdx.z * per), c1 = min(nst, c0 + per);
+  DzRows<T, TA::VROW> la{a.dz, a.gstride, a.row_begin, a.rows, m0, c0};
+  WeightRows<T, TB::VROW> lb{static_cast<const T*>(a.Wb), a.Kb, a.Nb, n0, c0};
   NoIndex ix;
   f32x16 acc[MT][TN];
   zero_acc(acc);
-  mainloop<T, TA, TB, MT, TN>(a.Kb / M::BK, la, lb, ix, As, Bs, acc, wave * 32 * MT, 0);
+  mainloop<T, TA, TB, MT, TN>(c1 - c0, la, lb, ix, As, Bs, acc, wave * 32 * MT, 0);
 #pragma unroll
   for (int tm = 0; tm < MT; ++tm) {
 #pragma unroll
@@ -390,32 +452,31 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx(DxArgs a) {
   }
 }
 
-inline unsigned cdiv(long long a, long long b) { return (unsigned)((a + b - 1) / b); }
+
+template <typename T, int KIND>
+void cell_fwd_kind(const FwdArgs& a, hipStream_t st) {
+  const FwdPlan pl = fwd_plan(a.rows, a.HP, a.has_input ? a.INP : 0, a.arity, sizeof(T), a.zpart != nullptr);
+  const int BM = 128 * pl.mt;
+  dim3 grid(cdiv(a.rows, BM), a.HP / 32, pl.ksplit);
+  if (pl.ksplit > 1) {
+    if (pl.mt == 2) hipLaunchKernelGGL((k_cell_fwd<T, KIND, 2, true>), grid, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, true>), grid, dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((k_cell_epi<T, KIND>), dim3(a.rows), dim3(256), 0, st, a, pl.ksplit);
+  } else {
+    if (pl.mt == 2) hipLaunchKernelGGL((k_cell_fwd<T, KIND, 2, false>), grid, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, false>), grid, dim3(kThreads), 0, st, a);
+  }
+}
 
 template <typename T>
 void cell_fwd_t(int kind, const FwdArgs& a, hipStream_t st) {
-  const int MT = a.rows > 128 ? 2 : 1;
-  const int BM = 128 * MT;
-  dim3 grid(cdiv(a.rows, BM), a.HP / 32);
-#define FOLD_LAUNCH_FWD(KIND, MTV) \
-  hipLaunchKernelGGL((k_cell_fwd<T, KIND, MTV>), grid, dim3(kThreads), 0, st, a)
   switch (kind) {
-    case FOLD_TREELSTM:
-      if (MT == 2) FOLD_LAUNCH_FWD(FOLD_TREELSTM, 2); else FOLD_LAUNCH_FWD(FOLD_TREELSTM, 1);
-      break;
-    case FOLD_LSTM:
-      if (MT == 2) FOLD_LAUNCH_FWD(FOLD_LSTM, 2); else FOLD_LAUNCH_FWD(FOLD_LSTM, 1);
-      break;
-    case FOLD_TREERNN:
-      if (MT == 2) FOLD_LAUNCH_FWD(FOLD_TREERNN, 2); else FOLD_LAUNCH_FWD(FOLD_TREERNN, 1);
-      break;
-    case FOLD_PROJ:
-      if (MT == 2) FOLD_LAUNCH_FWD(FOLD_PROJ, 2); else FOLD_LAUNCH_FWD(FOLD_PROJ, 1);
-      break;
-    default:
-      break;
+    case FOLD_TREELSTM: cell_fwd_kind<T, FOLD_TREELSTM>(a, st); break;
+    case FOLD_LSTM: cell_fwd_kind<T, FOLD_LSTM>(a, st); break;
+    case FOLD_TREERNN: cell_fwd_kind<T, FOLD_TREERNN>(a, st); break;
+    case FOLD_PROJ: cell_fwd_kind<T, FOLD_PROJ>(a, st); break;
+    default: break;
   }
-#undef FOLD_LAUNCH_FWD
 }
 
 }  // namespace
@@ -490,8 +551,9 @@ void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
 void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st) {
   if (a.rows <= 0 || a.Nb <= 0) return;
   ProfScope prof(dtype == FOLD_BF16 ? "bwd_dx.bf16" : "bwd_dx.f32", st);
-  const int MT = a.rows > 128 ? 2 : 1;
-  dim3 grid(cdiv(a.rows, 128 * MT), cdiv(a.Nb, 128));
+  const DxPlan pl = dx_plan(a.rows, a.Nb, a.Kb, dtype == FOLD_BF16 ? 2 : 4);
+  const int MT = pl.mt;
+  dim3 grid(cdiv(a.rows, 128 * MT), cdiv(a.Nb, 128), pl.ksplit);
   if (dtype == FOLD_BF16) {
     if (MT == 2) hipLaunchKernelGGL((k_bwd_dx<uint16_t, 2>), grid, dim3(kThreads), 0, st, a);
     else hipLaunchKernelGGL((k_bwd_dx<uint16_t, 1>), grid, dim3(kThreads), 0, st, a);

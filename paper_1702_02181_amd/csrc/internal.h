@@ -1,6 +1,8 @@
 // Host-side entry points between the library's translation units.
 #pragma once
 
+#include <algorithm>
+
 #include "common.h"
 
 namespace fold {
@@ -15,6 +17,7 @@ void packed_destroy_impl(fold_packed* h);
 struct WsLayout {
   int gstride = 0;           // floats per pool row of saved gates / dz: Gmax * HP
   size_t gates_off = 0, gates_bytes = 0;
+  size_t zpart_off = 0, zpart_bytes = 0;  // K-split partial sums of narrow forward levels
   size_t dh_off = 0, dc_off = 0, acc_bytes = 0;
   size_t part_off = 0, part_bytes = 0;   // weight-gradient partial tiles
   size_t bpart_off = 0, bpart_bytes = 0; // bias partial sums
@@ -50,8 +53,48 @@ struct FwdArgs {
   const float* bias;
   float* gates;
   int gstride;
+  float* zpart;  // workspace for K-split partial sums, or NULL (no split)
 };
 void launch_cell_fwd(int dtype, int kind, const FwdArgs& a, hipStream_t st);
+
+// Tiling of one forward group: row tile of 128 * mt rows, K loop cut into ksplit slices.  Wide
+// groups use 256-row tiles; groups too narrow to give every compute unit a workgroup use 128-row
+// tiles and, if still short, split K (partial sums in the workspace, then an epilogue kernel).
+struct FwdPlan {
+  int mt = 1, ksplit = 1;
+};
+inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bool can_split) {
+  const int BK = esize == 4 ? 32 : 64;
+  const int nst = inp_used / BK + arity * (HP / BK);
+  const long long ub = HP / 32;
+  FwdPlan p;
+  p.mt = ((long long)(rows + 255) / 256) * ub >= 256 ? 2 : 1;
+  const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * ub;
+  if (can_split && base < 192 && nst >= 4) {
+    const long long want = (256 + base - 1) / base;
+    p.ksplit = (int)std::min<long long>(want, nst / 2);
+  }
+  return p;
+}
+
+// dz . W^T tiling: 128 * mt rows x 128 columns, K cut into ksplit slices (partial products are
+// scatter-added, so slices need no extra pass).
+struct DxPlan {
+  int mt = 1, ksplit = 1;
+};
+inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize) {
+  const int BK = esize == 4 ? 32 : 64;
+  const int nst = Kb / BK;
+  const long long nb = (Nb + 127) / 128;
+  DxPlan p;
+  p.mt = ((long long)(rows + 255) / 256) * nb >= 256 ? 2 : 1;
+  const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * nb;
+  if (base < 192 && nst >= 4) {
+    const long long want = (256 + base - 1) / base;
+    p.ksplit = (int)std::min<long long>(want, nst / 2);
+  }
+  return p;
+}
 void launch_embed_fwd(int dtype, int rows, int row_begin, int H, int ld, int tld, const void* table,
                       const int* input_idx, void* h_pool, float* c_pool, hipStream_t st);
 void launch_roots(int dtype, int R, int ld, const int* root_pos, const void* h_pool, void* roots_out,
