@@ -1,0 +1,79 @@
+"""Parity at the full workload sizes, in the launch configuration bench.py times.
+
+The oracle cannot evaluate a whole 130 k - 2 M node batch node by node in test time,
+so these tests sample graphs and rely on two properties that hold at any size:
+  * batching invariance: a graph's states inside the full batch equal those of the
+    graph evaluated alone (dynamic batching only rewrites the computation);
+  * linearity of the backward pass in the upstream gradient: with the root
+    gradients of every non-sampled graph set to zero, those graphs contribute exactly
+    nothing, so the full-batch weight gradients equal the oracle's gradients of the
+    sampled graphs alone, and every node outside them gets an exact zero gradient.
+"""
+import numpy as np
+import pytest
+
+from oracle import compare
+from paper_1702_02181_amd import gen
+from tests import gpu_common as C
+
+pytestmark = pytest.mark.gpu
+
+
+def _sampled_parity(w, sample, table_grad):
+    tol = C.TOL[w.dtype]
+    rpg = gen.roots_per_graph(w.graph_ptr, w.child_idx)
+    roff = np.concatenate([[0], np.cumsum(rpg)])
+    dh = np.zeros_like(w.dh_roots)
+    for g in sample:
+        dh[roff[g]:roff[g + 1]] = w.dh_roots[roff[g]:roff[g + 1]]
+    w.dh_roots = dh
+    g_out = C.run_device(w, table_grad=table_grad)
+    sub = gen.subset(w, sample)
+    o = C.run_oracle(sub, table_grad=table_grad)
+    gp = w.graph_ptr
+    rows = np.concatenate([np.arange(gp[g], gp[g + 1]) for g in sample])
+    errs = {
+        "h": compare.rel_err(g_out["h"][rows], o["h"]),
+        "c": compare.rel_err(g_out["c"][rows], o["c"]),
+        "dh": compare.rel_err(g_out["dh"][rows], o["dh"]),
+        "dc": compare.rel_err(g_out["dc"][rows], o["dc"]),
+    }
+    mask = np.ones(w.num_nodes, bool)
+    mask[rows] = False
+    assert np.all(g_out["dh"][mask] == 0) and np.all(g_out["dc"][mask] == 0)
+    for s, (gg, oo) in enumerate(zip(g_out["grads"], o["grads"])):
+        for name in ("W_in", "W_rec", "bias"):
+            if gg.get(name) is None or oo.get(name) is None:
+                continue
+            errs[f"set{s}.{name}"] = compare.rel_err(gg[name], oo[name], whole=True)
+    if table_grad:
+        errs["d_table"] = compare.rel_err(g_out["d_table"], o["d_table"], whole=True)
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, (bad, errs)
+    return errs
+
+
+def test_config2_full_bench_workload():
+    w = gen.config2()
+    _sampled_parity(w, [0, 97, 255], table_grad=False)
+
+
+def test_config3_full():
+    w = gen.config3()
+    _sampled_parity(w, [0, 511, 1023], table_grad=True)
+
+
+def test_config4_full():
+    w = gen.config4()
+    # the longest chain and two others
+    sizes = np.diff(w.graph_ptr)
+    _sampled_parity(w, [int(np.argmax(sizes)), 1, 300], table_grad=False)
+
+
+def test_config5_full():
+    w = gen.config5()
+    # one balanced tree with shared sub-expressions and the deepest caterpillar
+    sizes = np.diff(w.graph_ptr)
+    odd = np.arange(1, w.num_graphs, 2)
+    deepest = int(odd[np.argmax(sizes[odd])])
+    _sampled_parity(w, [0, deepest], table_grad=True)
