@@ -30,6 +30,15 @@ constexpr int kThreads = 256;
 
 inline unsigned cdiv(long long a, long long b) { return (unsigned)((a + b - 1) / b); }
 
+// dst += v for a node-gradient element: a plain read-add-write when the element has exactly one
+// writer in the launch (a child with one parent edge), else a hardware fp32 atomic add.
+__device__ __forceinline__ void scatter_add(float* dst, float v, bool single) {
+  if (single)
+    *dst += v;
+  else
+    unsafeAtomicAdd(dst, v);
+}
+
 template <int KIND>
 struct Gates {
   static constexpr int G = KIND == FOLD_TREELSTM ? 5 : (KIND == FOLD_LSTM ? 4 : 1);
@@ -173,8 +182,22 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   __shared__ int srow[3][BM];  // source row of every tile row, per input segment
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int m0 = blockIdx.x * BM;
-  const int ub = blockIdx.y;  // hidden units ub*32 .. ub*32+31
+  // co-locate on one XCD the workgroups that share the larger operand: the gathered rows of a row
+  // tile (wide levels) or the weight slice of a unit block (narrow levels)
+  const int R = (a.rows + BM - 1) / BM, UB = a.HP / 32;
+  int tx, ty, ub, rt, kz;
+  if (a.share_rows) {
+    if (!xcd_tile(UB * a.ksplit, R, tx, ty)) return;
+    rt = ty;
+    ub = tx % UB;
+    kz = tx / UB;
+  } else {
+    if (!xcd_tile(R * a.ksplit, UB, tx, ty)) return;
+    ub = ty;
+    rt = tx % R;
+    kz = tx / R;
+  }
+  const int m0 = rt * BM;  // ub: hidden units ub*32 .. ub*32+31
 
   const int nseg = a.has_input + a.arity;
   for (int seg = 0; seg < nseg; ++seg) {
@@ -193,8 +216,8 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   const int nst = st.cin + a.arity * st.chp;
   int c0 = 0, c1 = nst;
   if constexpr (SPLIT) {
-    const int per = (nst + gridDim.z - 1) / gridDim.z;
-    c0 = min(nst, (int)blockIdx.z * per);
+    const int per = (nst + a.ksplit - 1) / a.ksplit;
+    c0 = min(nst, kz * per);
     c1 = min(nst, c0 + per);
   }
   FwdA<T, BM, TA::VROW> la{static_cast<const T*>(a.table), static_cast<const T*>(a.h_pool), a.tld, a.ld,
@@ -208,7 +231,7 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   const int j = ub * 32 + (lane & 31);
   if constexpr (SPLIT) {
     const int zs = G * a.HP;
-    float* zp = a.zpart + (size_t)blockIdx.z * a.rows * zs + j;
+    float* zp = a.zpart + (size_t)kz * a.rows * zs + j;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -310,6 +333,7 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
   int c0 = -1, c1 = -1;
   if (a.arity >= 1) c0 = a.child_pos[a.idx_off + row * a.arity];
   if (a.arity >= 2) c1 = a.child_pos[a.idx_off + row * a.arity + 1];
+  const bool s0 = c0 >= 0 && a.npar[c0] == 1, s1 = c1 >= 0 && a.npar[c1] == 1;
   for (int j = threadIdx.x; j < a.HP; j += blockDim.x) {
     if (j >= a.H) {
       if constexpr (KIND != FOLD_EMBED) {
@@ -333,8 +357,8 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       gb[2 * a.HP + j] = dct * cr * fr * (1.f - fr);
       gb[3 * a.HP + j] = dh * tc * o * (1.f - o);
       gb[4 * a.HP + j] = dct * i_ * (1.f - u * u);
-      if (c0 >= 0) unsafeAtomicAdd(&a.dc[(size_t)c0 * a.ld + j], dct * fl);
-      if (c1 >= 0) unsafeAtomicAdd(&a.dc[(size_t)c1 * a.ld + j], dct * fr);
+      if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dct * fl, s0);
+      if (c1 >= 0) scatter_add(&a.dc[(size_t)c1 * a.ld + j], dct * fr, s1);
     } else if constexpr (KIND == FOLD_LSTM) {
       const float dc = a.dc[p * a.ld + j];
       const float i_ = gb[j], f = gb[a.HP + j], o = gb[2 * a.HP + j], u = gb[3 * a.HP + j];
@@ -345,13 +369,13 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       gb[a.HP + j] = dct * cp * f * (1.f - f);
       gb[2 * a.HP + j] = dh * tc * o * (1.f - o);
       gb[3 * a.HP + j] = dct * i_ * (1.f - u * u);
-      if (c0 >= 0) unsafeAtomicAdd(&a.dc[(size_t)c0 * a.ld + j], dct * f);
+      if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dct * f, s0);
     } else {
       const float h = gb[j];
       gb[j] = dh * (1.f - h * h);
       if constexpr (KIND == FOLD_PROJ) {
         const float dc = a.dc[p * a.ld + j];
-        if (c0 >= 0) unsafeAtomicAdd(&a.dc[(size_t)c0 * a.ld + j], dc);
+        if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dc, s0);
       }
     }
   }
@@ -407,7 +431,21 @@ struct WeightRows {
   __device__ __forceinline__ uint4 put(const raw& r) const { return finish<T>(r); }
 };
 
-template <typename T, int MT>
+// scatter one element of dz . W^T: mode 0 into the child's dh, mode 1 into the leaf-table gradient
+__device__ __forceinline__ void dx_scatter(const DxArgs& a, int row, int n, float v) {
+  if (a.mode == 0) {
+    const int k = n / a.HP, jin = n - k * a.HP;
+    if (jin >= a.H) return;
+    const int cp = a.child_pos[a.idx_off + row * a.arity + k];
+    if (cp >= 0) scatter_add(&a.dh[(size_t)cp * a.ld + jin], v, a.npar[cp] == 1);
+  } else {
+    if (n >= a.in_dim) return;
+    const int ti = a.input_idx[a.row_begin + row];
+    unsafeAtomicAdd(&a.d_table[(size_t)ti * a.tld + n], v);
+  }
+}
+
+template <typename T, int MT, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void k_bwd_dx(DxArgs a) {
   using M = Mma<T>;
   constexpr int TN = 4;
@@ -417,9 +455,24 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx(DxArgs a) {
   __shared__ __attribute__((aligned(16))) T As[TA::ELEMS];
   __shared__ __attribute__((aligned(16))) T Bs[TB::ELEMS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
-  const int nst = a.Kb / M::BK, per = (nst + gridDim.z - 1) / gridDim.z;
-  const int c0 = min(nst, (int)blockIdx.z * per), c1 = min(nst, c0 + per);
+  // co-locate the workgroups that share the larger operand (a row tile's dz rows or a column tile's
+  // weight slice) on one XCD
+  const int R = (a.rows + BM - 1) / BM, NT = (a.Nb + BN - 1) / BN;
+  int tx, ty, nt, rt, kz;
+  if (a.share_rows) {
+    if (!xcd_tile(NT * a.ksplit, R, tx, ty)) return;
+    rt = ty;
+    nt = tx % NT;
+    kz = tx / NT;
+  } else {
+    if (!xcd_tile(R * a.ksplit, NT, tx, ty)) return;
+    nt = ty;
+    rt = tx % R;
+    kz = tx / R;
+  }
+  const int m0 = rt * BM, n0 = nt * BN;
+  const int nst = a.Kb / M::BK, per = (nst + a.ksplit - 1) / a.ksplit;
+  const int c0 = min(nst, kz * per), c1 = min(nst, c0 + per);
   DzRows<T, TA::VROW> la{a.dz, a.gstride, a.row_begin, a.rows, m0, c0};
   WeightRows<T, TB::VROW> lb{static_cast<const T*>(a.Wb), a.Kb, a.Nb, n0, c0};
   NoIndex ix;
@@ -436,28 +489,35 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx(DxArgs a) {
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wave * 32 * MT + tm * 32 + acc_row(r, lane);
         if (row >= a.rows) continue;
-        const float v = acc[tm][tn][r];
-        if (a.mode == 0) {
-          const int k = n / a.HP, jin = n - k * a.HP;
-          if (jin >= a.H) continue;
-          const int cp = a.child_pos[a.idx_off + row * a.arity + k];
-          if (cp >= 0) unsafeAtomicAdd(&a.dh[(size_t)cp * a.ld + jin], v);
-        } else {
-          if (n >= a.in_dim) continue;
-          const int ti = a.input_idx[a.row_begin + row];
-          unsafeAtomicAdd(&a.d_table[(size_t)ti * a.tld + n], v);
-        }
+        if constexpr (SPLIT)
+          a.xpart[((size_t)kz * a.rows + row) * a.Nb + n] = acc[tm][tn][r];
+        else
+          dx_scatter(a, row, n, acc[tm][tn][r]);
       }
     }
   }
 }
 
+// finish a K-split dz . W^T launch: sum the slices, then scatter
+__global__ void k_dx_epi(DxArgs a, int nsplit) {
+  const int row = blockIdx.x;
+  for (int n = threadIdx.x; n < a.Nb; n += blockDim.x) {
+    float v = 0.f;
+    for (int sp = 0; sp < nsplit; ++sp) v += a.xpart[((size_t)sp * a.rows + row) * a.Nb + n];
+    dx_scatter(a, row, n, v);
+  }
+}
 
 template <typename T, int KIND>
-void cell_fwd_kind(const FwdArgs& a, hipStream_t st) {
-  const FwdPlan pl = fwd_plan(a.rows, a.HP, a.has_input ? a.INP : 0, a.arity, sizeof(T), a.zpart != nullptr);
+void cell_fwd_kind(const FwdArgs& a0, hipStream_t st) {
+  const FwdPlan pl = fwd_plan(a0.rows, a0.HP, a0.has_input ? a0.INP : 0, a0.arity, sizeof(T), a0.zpart != nullptr);
+  FwdArgs a = a0;
+  a.ksplit = pl.ksplit;
   const int BM = 128 * pl.mt;
-  dim3 grid(cdiv(a.rows, BM), a.HP / 32, pl.ksplit);
+  const int G = Gates<KIND>::G;
+  a.share_rows = a.rows >= G * a.HP;  // gathered rows outweigh the weights
+  const int R = (int)cdiv(a.rows, BM), UB = a.HP / 32;
+  dim3 grid(a.share_rows ? xcd_grid(UB * pl.ksplit, R) : xcd_grid(R * pl.ksplit, UB));
   if (pl.ksplit > 1) {
     if (pl.mt == 2) hipLaunchKernelGGL((k_cell_fwd<T, KIND, 2, true>), grid, dim3(kThreads), 0, st, a);
     else hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, true>), grid, dim3(kThreads), 0, st, a);
@@ -548,19 +608,27 @@ void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
   }
 }
 
-void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st) {
-  if (a.rows <= 0 || a.Nb <= 0) return;
+void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
+  if (a0.rows <= 0 || a0.Nb <= 0) return;
+  DxArgs a = a0;
   ProfScope prof(dtype == FOLD_BF16 ? "bwd_dx.bf16" : "bwd_dx.f32", st);
-  const DxPlan pl = dx_plan(a.rows, a.Nb, a.Kb, dtype == FOLD_BF16 ? 2 : 4);
+  const DxPlan pl = dx_plan(a.rows, a.Nb, a.Kb, dtype == FOLD_BF16 ? 2 : 4, a.xpart != nullptr);
   const int MT = pl.mt;
-  dim3 grid(cdiv(a.rows, 128 * MT), cdiv(a.Nb, 128), pl.ksplit);
+  a.ksplit = pl.ksplit;
+  a.share_rows = a.rows >= a.Nb;
+  const int R = (int)cdiv(a.rows, 128 * MT), NT = (int)cdiv(a.Nb, 128);
+  dim3 grid(a.share_rows ? xcd_grid(NT * pl.ksplit, R) : xcd_grid(R * pl.ksplit, NT));
+#define FOLD_DX(T_, MT_, S_) hipLaunchKernelGGL((k_bwd_dx<T_, MT_, S_>), grid, dim3(kThreads), 0, st, a)
+  const bool split = pl.ksplit > 1;
   if (dtype == FOLD_BF16) {
-    if (MT == 2) hipLaunchKernelGGL((k_bwd_dx<uint16_t, 2>), grid, dim3(kThreads), 0, st, a);
-    else hipLaunchKernelGGL((k_bwd_dx<uint16_t, 1>), grid, dim3(kThreads), 0, st, a);
+    if (MT == 2) { if (split) FOLD_DX(uint16_t, 2, true); else FOLD_DX(uint16_t, 2, false); }
+    else { if (split) FOLD_DX(uint16_t, 1, true); else FOLD_DX(uint16_t, 1, false); }
   } else {
-    if (MT == 2) hipLaunchKernelGGL((k_bwd_dx<float, 2>), grid, dim3(kThreads), 0, st, a);
-    else hipLaunchKernelGGL((k_bwd_dx<float, 1>), grid, dim3(kThreads), 0, st, a);
+    if (MT == 2) { if (split) FOLD_DX(float, 2, true); else FOLD_DX(float, 2, false); }
+    else { if (split) FOLD_DX(float, 1, true); else FOLD_DX(float, 1, false); }
   }
+#undef FOLD_DX
+  if (split) hipLaunchKernelGGL(k_dx_epi, dim3(a.rows), dim3(256), 0, st, a, pl.ksplit);
 }
 
 }  // namespace fold

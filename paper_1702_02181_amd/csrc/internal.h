@@ -18,6 +18,7 @@ struct WsLayout {
   int gstride = 0;           // floats per pool row of saved gates / dz: Gmax * HP
   size_t gates_off = 0, gates_bytes = 0;
   size_t zpart_off = 0, zpart_bytes = 0;  // K-split partial sums of narrow forward levels
+  size_t xpart_off = 0, xpart_bytes = 0;  // K-split partial products of narrow dz . W^T launches
   size_t dh_off = 0, dc_off = 0, acc_bytes = 0;
   size_t part_off = 0, part_bytes = 0;   // weight-gradient partial tiles
   size_t bpart_off = 0, bpart_bytes = 0; // bias partial sums
@@ -54,6 +55,8 @@ struct FwdArgs {
   float* gates;
   int gstride;
   float* zpart;  // workspace for K-split partial sums, or NULL (no split)
+  int ksplit;    // set by the launcher
+  int share_rows;  // set by the launcher: co-locate the workgroups of a row tile (else of a unit block)
 };
 void launch_cell_fwd(int dtype, int kind, const FwdArgs& a, hipStream_t st);
 
@@ -77,19 +80,19 @@ inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bo
   return p;
 }
 
-// dz . W^T tiling: 128 * mt rows x 128 columns, K cut into ksplit slices (partial products are
-// scatter-added, so slices need no extra pass).
+// dz . W^T tiling: 128 * mt rows x 128 columns, K cut into ksplit slices (partial products in the
+// workspace, summed and scattered by an epilogue kernel).
 struct DxPlan {
   int mt = 1, ksplit = 1;
 };
-inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize) {
+inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
   const int BK = esize == 4 ? 32 : 64;
   const int nst = Kb / BK;
   const long long nb = (Nb + 127) / 128;
   DxPlan p;
   p.mt = ((long long)(rows + 255) / 256) * nb >= 256 ? 2 : 1;
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * nb;
-  if (base < 192 && nst >= 4) {
+  if (can_split && base < 192 && nst >= 4) {
     const long long want = (256 + base - 1) / base;
     p.ksplit = (int)std::min<long long>(want, nst / 2);
   }
@@ -109,6 +112,7 @@ struct BwdCellArgs {
   float* dc;
   const int* child_pos;
   const int* input_idx;
+  const int* npar;  // parent edges per pool row: 1 -> plain read-add-write, else atomic add
   float* d_table;
   int tld;
 };
@@ -127,6 +131,10 @@ struct DxArgs {
   float* d_table;
   const int* input_idx;
   int in_dim, tld;
+  const int* npar;  // parent edges per pool row
+  float* xpart;     // workspace for K-split partial products, or NULL (no split)
+  int ksplit;       // set by the launcher
+  int share_rows;   // set by the launcher: co-locate the workgroups of a row tile (else of a column tile)
 };
 void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st);
 

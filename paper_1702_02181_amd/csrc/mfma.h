@@ -41,6 +41,20 @@ struct Mma<uint16_t> {
   }
 };
 
+// Workgroups of a launch are handed to the 8 XCDs round-robin in launch order, and every XCD has its
+// own L2.  A launch of X * round_up(Y, 8) workgroups is decoded so that all X workgroups of one y run
+// on the same XCD and are dispatched back to back there: XCD k owns y in [k*Y8/8, (k+1)*Y8/8).  The
+// operand those X workgroups share (a row tile's gathered rows, a weight slice, a row chunk) is then
+// fetched into that XCD's L2 once.  Returns false for the padding workgroups (y >= Y), which exit.
+__device__ __forceinline__ bool xcd_tile(int X, int Y, int& x, int& y) {
+  const int L = blockIdx.x;
+  const int per = (Y + 7) >> 3, xcd = L & 7, slot = L >> 3;
+  x = slot % X;
+  y = xcd * per + slot / X;
+  return y < Y;
+}
+inline int xcd_grid(int X, int Y) { return X * (((Y + 7) >> 3) << 3); }
+
 // row of the 32x32 result tile held by register r of lane `lane`
 __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 

@@ -398,7 +398,8 @@ __global__ void k_group_rows(const int* ng_ptr, int N, const int* g_row_begin, c
 
 __global__ void k_emit(const int* pos_node, const int* node_pos, const int* gid, const int* g_row_begin,
                        const int* g_op, const int* g_idx_off, const int* cp, const int* ci,
-                       const int* node_input, int N, OpTable ops, int* child_pos, int* input_idx) {
+                       const int* node_input, const int* indeg, int N, OpTable ops, int* child_pos,
+                       int* input_idx, int* pos_npar) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= N) return;
   const int v = pos_node[p];
@@ -411,6 +412,7 @@ __global__ void k_emit(const int* pos_node, const int* node_pos, const int* gid,
     child_pos[off + k] = c >= 0 ? node_pos[c] : -1;
   }
   input_idx[p] = node_input[v];
+  pos_npar[p] = indeg[v];
 }
 
 __global__ void k_root_flags(const int* indeg, int N, int* flag) {
@@ -524,7 +526,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   };
 
   // persistent arrays sized by N and E
-  const size_t n1 = (size_t)N * 10 + (size_t)E + 8;
+  const size_t n1 = (size_t)N * 11 + (size_t)E + 8;
   if (hipMalloc(&s.blob, n1 * sizeof(int)) != hipSuccess) {
     set_error("fold_schedule: out of device memory");
     return fail(FOLD_E_NOMEM);
@@ -537,6 +539,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   s.root_pos = q; q += N;
   s.child_pos = q; q += E;
   s.pos_group = q; q += N;
+  s.pos_npar = q; q += N;
   s.op_rows = q; q += N;
   s.op_cpos = q; q += 2 * (size_t)N;
   s.op_inp = q; q += N;
@@ -651,8 +654,8 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
     // idx_off = exclusive scan of rows * arity over the groups (entries past num_groups are unused)
     scan_exclusive(d_edges, d_idx_off, (int)cap, m2 + 2, scan_tmp, st);
     hipLaunchKernelGGL(k_emit, grid_for(N), dim3(kBlock), 0, st, s.pos_node, s.node_pos, gid, d_row_begin,
-                       d_op, d_idx_off, b->child_ptr, b->child_idx, b->node_input, N, ops, s.child_pos,
-                       s.input_idx);
+                       d_op, d_idx_off, b->child_ptr, b->child_idx, b->node_input, indeg, N, ops, s.child_pos,
+                       s.input_idx, s.pos_npar);
     hipLaunchKernelGGL(k_root_flags, grid_for(N), dim3(kBlock), 0, st, indeg, N, flag);
     scan_exclusive(flag, exs, N, m2 + 1, scan_tmp, st);
     hipLaunchKernelGGL(k_root_emit, grid_for(N), dim3(kBlock), 0, st, flag, exs, s.node_pos, N, s.root_pos);

@@ -160,10 +160,14 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave & 1, wn = wave >> 1;
-  const int chunk_id = blockIdx.x;
-  const int m0 = blockIdx.y * kTM, n0 = blockIdx.z * kTN;
+  // all tiles of one row chunk read the same X and dz rows: keep them on one XCD
+  const int NT = (a.Nw + kTN - 1) / kTN, MTm = (a.Kw + kTM - 1) / kTM;
+  int tx, chunk_id;
+  if (!xcd_tile(MTm * NT, a.nchunk, tx, chunk_id)) return;
+  const int mt_ = tx % MTm;
+  const int m0 = mt_ * kTM, n0 = (tx / MTm) * kTN;
   const int lo = chunk_id * a.chunk, hi = min(a.count, lo + a.chunk);
-  const bool do_bias = a.bpart != nullptr && blockIdx.y == 0;
+  const bool do_bias = a.bpart != nullptr && mt_ == 0;
 
   WgIndex<BK> ix{slots, a.op_rows, a.op_cpos, a.op_inp, lo, hi, a.seg, 0, 0, 0, 0};
   WgX<T, BK, TA::VROW> la{static_cast<const T*>(a.src), a.seg ? a.ld : a.tld, a.seg ? a.H : a.in_dim, a.HP,
@@ -255,7 +259,8 @@ WgradSplit wgrad_split(int count, int Kw, int Nw) {
   WgradSplit w;
   if (count <= 0 || Kw <= 0 || Nw <= 0) return w;
   const long long tiles = (long long)((Kw + kTM - 1) / kTM) * ((Nw + kTN - 1) / kTN);
-  const long long want = (1024 + tiles - 1) / tiles;  // enough workgroups to fill the chip
+  // enough workgroups to fill the chip, and chunks in multiples of the 8 XCDs (one XCD per chunk)
+  const long long want = std::max(8LL, ((1024 + tiles - 1) / tiles + 7) / 8 * 8);
   const long long most = std::max(1, (count + 511) / 512);
   w.nchunk = (int)std::max(1LL, std::min(want, most));
   w.chunk = round_up((count + w.nchunk - 1) / w.nchunk, 64);
@@ -266,7 +271,7 @@ WgradSplit wgrad_split(int count, int Kw, int Nw) {
 void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st) {
   if (a.count <= 0) return;
   ProfScope prof(dtype == FOLD_BF16 ? "wgrad.bf16" : "wgrad.f32", st);
-  dim3 grid(a.nchunk, (a.Kw + kTM - 1) / kTM, (a.Nw + kTN - 1) / kTN);
+  dim3 grid(xcd_grid(((a.Kw + kTM - 1) / kTM) * ((a.Nw + kTN - 1) / kTN), a.nchunk));
   if (dtype == FOLD_BF16)
     hipLaunchKernelGGL(k_wgrad<uint16_t>, grid, dim3(kThreads), 0, st, a);
   else
