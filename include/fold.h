@@ -33,8 +33,11 @@
  *     fold_forward and fold_backward never synchronise and never allocate.
  *   - Node states live in one pool in SCHEDULE order: row p of a pool holds
  *     node pos_node[p].  Every row-major float/bf16 matrix the library reads
- *     or writes has a row stride of fold_row_ld(width) elements; columns
- *     beyond the width are written as zero (pools) or ignored (inputs).
+ *     or writes has a row stride of fold_row_ld(width) elements (width
+ *     rounded up to 64); columns beyond the width are written as zero
+ *     (pools) and must hold zeros in inputs (the leaf table): the kernels
+ *     load whole 128-byte row segments and meet those columns with zero
+ *     weights, so any finite value there is harmless and NaN / Inf is not.
  *   - Handles are immutable after creation and may be shared by concurrent
  *     calls on different streams that use different output buffers.
  */
@@ -176,7 +179,8 @@ int32_t fold_pack_params(const fold_params* params, hipStream_t stream, fold_pac
 int32_t fold_packed_free(fold_packed* packed);
 
 /* Row stride, in elements, that the library uses for a row of `width`
- * elements (pools, root outputs, gradients of node states, leaf tables). */
+ * elements (pools, root outputs, gradients of node states, leaf tables):
+ * width rounded up to a multiple of 64. */
 int32_t fold_row_ld(int32_t width);
 
 /* Workspace needed by fold_forward (saved gate activations for the

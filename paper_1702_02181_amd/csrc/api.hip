@@ -245,6 +245,13 @@ int32_t pack_impl(const fold_params* prm, hipStream_t st, fold_packed** out) {
     }
     P.sets.push_back(ps);
   }
+  // the zero row spans the widest K any kernel reads: G * HP (dz rows), INP, HP
+  size_t zw = (size_t)P.HP;
+  for (const PackedSet& ps : P.sets) zw = std::max(zw, (size_t)std::max(ps.G * P.HP, ps.INP));
+  P.zero_bytes = zw * sizeof(float);
+  if (!dalloc(P.zero_bytes, &P.zero)) return bail(FOLD_E_NOMEM, "fold_pack_params: out of device memory");
+  if (hipMemsetAsync(P.zero, 0, P.zero_bytes, st) != hipSuccess)
+    return bail(FOLD_E_DEVICE, "fold_pack_params: device error while packing");
   if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess)
     return bail(FOLD_E_DEVICE, "fold_pack_params: device error while packing");
   *out = h;
@@ -298,6 +305,7 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
     a.bias = ps.bias;
     a.gates = gates;
     a.gstride = L.gstride;
+    a.zero = p.zero;
     a.zpart = zpart;
     launch_cell_fwd(p.dtype, op.kind, a, st);
   }
@@ -365,6 +373,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     d.tld = tld;
     d.npar = s.pos_npar;
     d.xpart = reinterpret_cast<float*>(wsb + L.xpart_off);
+    d.zero = p.zero;
     if (op.arity > 0) {
       d.mode = 0;
       d.Nb = op.arity * p.HP;

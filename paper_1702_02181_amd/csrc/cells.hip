@@ -20,6 +20,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "dma.h"
 #include "mfma.h"
 
 namespace fold {
@@ -46,66 +47,51 @@ struct Gates {
 
 // ---------------------------------------------------------------- forward
 
-// stage c of the forward K loop: input segment (INP wide) first, then one HP-wide segment per child
-struct FwdStages {
-  int cin, chp, has_input, INP, HP;
-  __device__ __forceinline__ void at(int c, int bk, int& seg, int& kc, int& kbase) const {
-    if (c < cin) {
-      seg = 0;
-      kc = c * bk;
-      kbase = 0;
-    } else {
-      const int cc = c - cin, k = cc / chp;
-      seg = has_input + k;
-      kc = (cc - k * chp) * bk;
-      kbase = INP + k * HP;
-    }
-  }
-};
-
-// gathered rows: leaf-table rows (input segment) or children's h rows, row indices from LDS
-template <typename T, int BM, int VROW>
-struct FwdA {
-  using raw = Raw4;
-  const T* table;
-  const T* pool;
-  int tld, ld, in_dim, H, has_input;
-  FwdStages st;
+// Direct loads of one forward stage (128 bytes of K) for one wave: the gathered A rows of its share of
+// the row tile (leaf-table rows by input_idx for the input segment, the children's h rows by child_pos
+// after it; absent rows read the zero row) and its share of the weight slice's rows.
+template <typename T, int BM, int PA, int PB>
+struct FwdIssue {
+  const FwdArgs& a;
   const int (*srow)[BM];
-  int c0;  // first stage of this workgroup's K slice
-  __device__ __forceinline__ raw fetch(int c, int i) const {
-    constexpr int BK = Mma<T>::BK, VEC = Mma<T>::VEC;
-    int seg, kc, kbase;
-    st.at(c + c0, BK, seg, kc, kbase);
-    const int r = i / VROW, v = i - r * VROW;
-    const int sr = srow[seg][r];
-    const bool is_in = has_input && seg == 0;
-    const int width = is_in ? in_dim : H;
-    const int col = kc + v * VEC;
-    const int nv = sr >= 0 ? min(max(width - col, 0), VEC) : 0;
-    const T* base = is_in ? table : pool;
-    const size_t off = nv > 0 ? (size_t)sr * (is_in ? tld : ld) + col : 0;
-    return {*reinterpret_cast<const uint4*>(base + off), nv};
+  const char* wrow;  // this lane's weight row (first stage), unit included
+  int wstep;         // bytes from one instruction's weight rows to the next (8 rows)
+  int wskip;         // weight columns before the first segment read: the set's input block when
+                     // this op reads no input
+  int c0, inp, wave, lr, lu;
+  int cur_seg = -1;
+  const char* rp[PA];  // this lane's A row in the current segment, unit included
+  __device__ __forceinline__ void reload(int seg) {
+    constexpr int es = sizeof(T);
+    const bool is_in = a.has_input && seg == 0;
+    const char* base = static_cast<const char*>(is_in ? a.table : a.h_pool);
+    const size_t stride = (size_t)(is_in ? a.tld : a.ld) * es;
+    const char* zero = static_cast<const char*>(a.zero) + lu * 16;
+#pragma unroll
+    for (int i = 0; i < PA; ++i) {
+      const int sr = srow[seg][8 * (wave * PA + i) + lr];
+      rp[i] = sr >= 0 ? base + (size_t)sr * stride + lu * 16 : zero;
+    }
+    cur_seg = seg;
   }
-  __device__ __forceinline__ uint4 put(const raw& r) const { return finish<T>(r); }
-};
-
-// packed weights, n-major, always in range
-template <typename T, int VROW>
-struct WeightB {
-  using raw = Raw4;
-  const T* W;
-  int ldk;
-  FwdStages st;
-  int c0;
-  __device__ __forceinline__ raw fetch(int c, int i) const {
-    constexpr int BK = Mma<T>::BK, VEC = Mma<T>::VEC;
-    int seg, kc, kbase;
-    st.at(c + c0, BK, seg, kc, kbase);
-    const int n = i / VROW, v = i - n * VROW;
-    return {*reinterpret_cast<const uint4*>(W + (size_t)n * ldk + kbase + kc + v * VEC), VEC};
+  __device__ __forceinline__ void operator()(int c, char* Ad, char* Bd) {
+    constexpr int es = sizeof(T), BK = 128 / es;
+    const int kabs = (c0 + c) * BK;
+    int seg, kc;
+    if (kabs < inp) {
+      seg = 0;
+      kc = kabs;
+    } else {
+      const int k = (kabs - inp) / a.HP;
+      seg = a.has_input + k;
+      kc = kabs - inp - k * a.HP;
+    }
+    if (seg != cur_seg) reload(seg);
+#pragma unroll
+    for (int i = 0; i < PA; ++i) dma16(rp[i] + kc * es, Ad + (wave * PA + i) * 1024);
+#pragma unroll
+    for (int i = 0; i < PB; ++i) dma16(wrow + i * wstep + (kabs + wskip) * es, Bd + (wave * PB + i) * 1024);
   }
-  __device__ __forceinline__ uint4 put(const raw& r) const { return r.x; }
 };
 
 // The cell on one (row, unit) given z (bias included): writes h, c and the saved activations.
@@ -171,17 +157,15 @@ __device__ __forceinline__ void pad_out(const FwdArgs& a, int row, int j) {
 // few row tiles would otherwise leave most compute units idle for a whole K loop.
 template <typename T, int KIND, int MT, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
-  using M = Mma<T>;
   constexpr int G = Gates<KIND>::G;
   constexpr int BM = 4 * 32 * MT;  // four waves stacked along the rows
   constexpr int BN = G * 32;       // G gate blocks of 32 units
-  using TA = Tile<T, BM, kRK>;
-  using TB = Tile<T, BN, kRK>;
-  __shared__ __attribute__((aligned(16))) T As[TA::ELEMS];
-  __shared__ __attribute__((aligned(16))) T Bs[TB::ELEMS];
-  __shared__ int srow[3][BM];  // source row of every tile row, per input segment
+  constexpr int PA = BM / 32, PB = BN / 32;  // direct-load instructions per wave and stage
+  constexpr int BK = 128 / sizeof(T);
+  __shared__ __attribute__((aligned(16))) char A0[BM * 128], A1[BM * 128], B0[BN * 128], B1[BN * 128];
+  __shared__ int srow[3][BM];  // source row of every tile row, per input segment (-1: zero row)
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
   // co-locate on one XCD the workgroups that share the larger operand: the gathered rows of a row
   // tile (wide levels) or the weight slice of a unit block (narrow levels)
   const int R = (a.rows + BM - 1) / BM, UB = a.HP / 32;
@@ -212,21 +196,22 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   }
   __syncthreads();
 
-  FwdStages st{a.has_input ? a.INP / M::BK : 0, a.HP / M::BK, a.has_input, a.INP, a.HP};
-  const int nst = st.cin + a.arity * st.chp;
+  const int inp = a.has_input ? a.INP : 0;
+  const int nst = (inp + a.arity * a.HP) / BK;
   int c0 = 0, c1 = nst;
   if constexpr (SPLIT) {
     const int per = (nst + a.ksplit - 1) / a.ksplit;
     c0 = min(nst, kz * per);
     c1 = min(nst, c0 + per);
   }
-  FwdA<T, BM, TA::VROW> la{static_cast<const T*>(a.table), static_cast<const T*>(a.h_pool), a.tld, a.ld,
-                           a.in_dim, a.H, a.has_input, st, srow, c0};
-  WeightB<T, TB::VROW> lb{static_cast<const T*>(a.Wf) + (size_t)ub * BN * a.Kf, a.Kf, st, c0};
-  NoIndex ix;
+  const int lr = row_of_lane(lane), lu = unit_of_lane(lane);
+  const char* wrow = static_cast<const char*>(a.Wf) +
+                     ((size_t)ub * BN + 8 * wave * PB + lr) * a.Kf * sizeof(T) + lu * 16;
+  FwdIssue<T, BM, PA, PB> issue{a, srow, wrow, 8 * a.Kf * (int)sizeof(T), a.has_input ? 0 : a.INP, c0, inp,
+                                wave, lr, lu};
   f32x16 acc[MT][G];
   zero_acc(acc);
-  mainloop<T, TA, TB, MT, G>(c1 - c0, la, lb, ix, As, Bs, acc, wave * 32 * MT, 0);
+  row_loop<T, MT, G>(c1 - c0, issue, A0, A1, B0, B1, acc, wave * 32 * MT, 0, lane);
 
   const int j = ub * 32 + (lane & 31);
   if constexpr (SPLIT) {
@@ -445,6 +430,72 @@ __device__ __forceinline__ void dx_scatter(const DxArgs& a, int row, int n, floa
   }
 }
 
+// dz . W^T for one tile of 128 * MT rows x 128 columns of the children's (or the input's) gradient:
+// dz rows (fp32 for fp32 parameters) and the packed W^T rows are loaded straight into LDS.
+template <int MT, bool SPLIT>
+__global__ __launch_bounds__(kThreads) void k_bwd_dx_f32(DxArgs a) {
+  constexpr int TN = 4;
+  constexpr int BM = 4 * 32 * MT, BN = 32 * TN;  // four waves of 32*MT rows x 128 columns
+  constexpr int PA = BM / 32, PB = BN / 32;
+  __shared__ __attribute__((aligned(16))) char A0[BM * 128], A1[BM * 128], B0[BN * 128], B1[BN * 128];
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  // co-locate the workgroups that share the larger operand (a row tile's dz rows or a column tile's
+  // weight slice) on one XCD
+  const int R = (a.rows + BM - 1) / BM, NT = (a.Nb + BN - 1) / BN;
+  int tx, ty, nt, rt, kz;
+  if (a.share_rows) {
+    if (!xcd_tile(NT * a.ksplit, R, tx, ty)) return;
+    rt = ty;
+    nt = tx % NT;
+    kz = tx / NT;
+  } else {
+    if (!xcd_tile(R * a.ksplit, NT, tx, ty)) return;
+    nt = ty;
+    rt = tx % R;
+    kz = tx / R;
+  }
+  const int m0 = rt * BM, n0 = nt * BN;
+  const int nst = a.Kb / 32, per = (nst + a.ksplit - 1) / a.ksplit;
+  const int c0 = min(nst, kz * per), c1 = min(nst, c0 + per);
+  const int lr = row_of_lane(lane), lu = unit_of_lane(lane);
+  const char* zero = static_cast<const char*>(a.zero) + lu * 16;
+  FixedRowsIssue<PA, PB> issue;
+  issue.wave = wave;
+#pragma unroll
+  for (int i = 0; i < PA; ++i) {
+    const int row = m0 + 8 * (wave * PA + i) + lr;
+    issue.ap[i] = row < a.rows ? reinterpret_cast<const char*>(a.dz + (size_t)(a.row_begin + row) * a.gstride) +
+                                     c0 * 128 + lu * 16
+                               : zero;
+  }
+  const char* wb = static_cast<const char*>(a.Wb);
+#pragma unroll
+  for (int i = 0; i < PB; ++i) {
+    const int n = n0 + 8 * (wave * PB + i) + lr;
+    issue.bp[i] = n < a.Nb ? wb + (size_t)n * a.Kb * 4 + c0 * 128 + lu * 16 : zero;
+  }
+  f32x16 acc[MT][TN];
+  zero_acc(acc);
+  row_loop<float, MT, TN>(c1 - c0, issue, A0, A1, B0, B1, acc, wave * 32 * MT, 0, lane);
+#pragma unroll
+  for (int tm = 0; tm < MT; ++tm) {
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int n = n0 + tn * 32 + (lane & 31);
+      if (n >= a.Nb) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wave * 32 * MT + tm * 32 + acc_row(r, lane);
+        if (row >= a.rows) continue;
+        if constexpr (SPLIT)
+          a.xpart[((size_t)kz * a.rows + row) * a.Nb + n] = acc[tm][tn][r];
+        else
+          dx_scatter(a, row, n, acc[tm][tn][r]);
+      }
+    }
+  }
+}
+
 template <typename T, int MT, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void k_bwd_dx(DxArgs a) {
   using M = Mma<T>;
@@ -620,14 +671,16 @@ void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
   dim3 grid(a.share_rows ? xcd_grid(NT * pl.ksplit, R) : xcd_grid(R * pl.ksplit, NT));
 #define FOLD_DX(T_, MT_, S_) hipLaunchKernelGGL((k_bwd_dx<T_, MT_, S_>), grid, dim3(kThreads), 0, st, a)
   const bool split = pl.ksplit > 1;
+#define FOLD_DX32(MT_, S_) hipLaunchKernelGGL((k_bwd_dx_f32<MT_, S_>), grid, dim3(kThreads), 0, st, a)
   if (dtype == FOLD_BF16) {
     if (MT == 2) { if (split) FOLD_DX(uint16_t, 2, true); else FOLD_DX(uint16_t, 2, false); }
     else { if (split) FOLD_DX(uint16_t, 1, true); else FOLD_DX(uint16_t, 1, false); }
   } else {
-    if (MT == 2) { if (split) FOLD_DX(float, 2, true); else FOLD_DX(float, 2, false); }
-    else { if (split) FOLD_DX(float, 1, true); else FOLD_DX(float, 1, false); }
+    if (MT == 2) { if (split) FOLD_DX32(2, true); else FOLD_DX32(2, false); }
+    else { if (split) FOLD_DX32(1, true); else FOLD_DX32(1, false); }
   }
 #undef FOLD_DX
+#undef FOLD_DX32
   if (split) hipLaunchKernelGGL(k_dx_epi, dim3(a.rows), dim3(256), 0, st, a, pl.ksplit);
 }
 

@@ -31,7 +31,9 @@ inline int gates_of(int kind) {
   }
 }
 
-inline int row_ld(int width) { return round_up(width < 1 ? 1 : width, 8); }
+// Row stride of every row the kernels read (pools, leaf table, gradients): whole K segments, so a stage
+// of 128 bytes never runs past a row and the pad columns (zero) meet zero weights.
+inline int row_ld(int width) { return round_up(width < 1 ? 1 : width, kPadK); }
 
 // ---------------------------------------------------------------- error state
 
@@ -103,6 +105,8 @@ struct PackedSet {
 struct Packed {
   int dtype = 0, H = 0, HP = 0, ld = 0;
   int device = 0;
+  void* zero = nullptr;  // zero_bytes of zeros: the row every absent operand row (child slot -1, tile
+  size_t zero_bytes = 0; // rows past the end) is loaded from
   std::vector<PackedSet> sets;
   std::vector<void*> allocs;
 };

@@ -54,6 +54,7 @@ struct FwdArgs {
   const float* bias;
   float* gates;
   int gstride;
+  const void* zero;  // a zero row at least as wide as any K the kernels read (16-byte aligned)
   float* zpart;  // workspace for K-split partial sums, or NULL (no split)
   int ksplit;    // set by the launcher
   int share_rows;  // set by the launcher: co-locate the workgroups of a row tile (else of a unit block)
@@ -71,7 +72,7 @@ inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bo
   const int nst = inp_used / BK + arity * (HP / BK);
   const long long ub = HP / 32;
   FwdPlan p;
-  p.mt = ((long long)(rows + 255) / 256) * ub >= 256 ? 2 : 1;
+  p.mt = 1;
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * ub;
   if (can_split && base < 192 && nst >= 4) {
     const long long want = (256 + base - 1) / base;
@@ -90,7 +91,8 @@ inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
   const int nst = Kb / BK;
   const long long nb = (Nb + 127) / 128;
   DxPlan p;
-  p.mt = ((long long)(rows + 255) / 256) * nb >= 256 ? 2 : 1;
+  // fp32: 128-row tiles, two workgroups per compute unit; bf16: 256-row tiles on wide levels
+  p.mt = esize == 4 ? 1 : (((long long)(rows + 255) / 256) * nb >= 256 ? 2 : 1);
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * nb;
   if (can_split && base < 192 && nst >= 4) {
     const long long want = (256 + base - 1) / base;
@@ -125,6 +127,7 @@ struct DxArgs {
   int H, HP, ld, gstride, Kb, Nb;
   const float* dz;
   const void* Wb;
+  const void* zero;  // a zero row at least as wide as any K the kernels read
   int mode;  // 0: scatter into children's dh, 1: into leaf-table rows
   float* dh;
   const int* child_pos;

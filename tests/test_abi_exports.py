@@ -44,5 +44,5 @@ def test_library_loads_and_binding_matches(lib_path):
         assert hasattr(L, n)
     assert sorted(F.EXPORTS) == declared_functions()
     # pure host helpers, no device work
-    assert F.fold_row_ld(300) == 304 and F.fold_row_ld(256) == 256 and F.fold_row_ld(1) == 8
+    assert F.fold_row_ld(300) == 320 and F.fold_row_ld(256) == 256 and F.fold_row_ld(1) == 64
     assert F.fold_last_error() == ""
