@@ -180,14 +180,14 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
     const int Nw = ps.G * p.HP;
     size_t nb = (size_t)((count + 511) / 512);
     if (op.arity > 0) {
-      WgradSplit sp = wgrad_split(count, op.arity * p.HP, Nw);
+      WgradSplit sp = wgrad_split(count, op.arity * p.HP, Nw, p.dtype);
       part = std::max(part, (size_t)sp.nchunk * op.arity * p.HP * Nw);
-      nb = std::max(nb, (size_t)sp.nchunk);
+      nb = std::max(nb, (size_t)sp.bparts);
     }
     if (op.has_input && ps.INP > 0) {
-      WgradSplit sp = wgrad_split(count, ps.INP, Nw);
+      WgradSplit sp = wgrad_split(count, ps.INP, Nw, p.dtype);
       part = std::max(part, (size_t)sp.nchunk * ps.INP * Nw);
-      nb = std::max(nb, (size_t)sp.nchunk);
+      nb = std::max(nb, (size_t)sp.bparts);
     }
     bpart = std::max(bpart, nb * Nw);
   }
@@ -412,19 +412,20 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       w.Nw = Nw;
       w.dz = gates;
       w.partial = part;
+      w.zero = p.zero;
       bool bias_done = false;
       auto run = [&](int seg, int Kw, const void* src, float* dW) {
         w.seg = seg;
         w.Kw = Kw;
         w.src = src;
-        const WgradSplit sp = wgrad_split(count, Kw, Nw);
+        const WgradSplit sp = wgrad_split(count, Kw, Nw, p.dtype);
         w.chunk = sp.chunk;
         w.nchunk = sp.nchunk;
         w.bpart = (pg.dbias && !bias_done) ? bpart : nullptr;
         launch_wgrad(p.dtype, w, st);
         launch_wgrad_reduce(part, sp.nchunk, Kw, Nw, seg, p.H, p.HP, ps.in_dim, ps.G, dW, st);
         if (w.bpart) {
-          launch_bias_reduce(bpart, sp.nchunk, Nw, p.H, p.HP, pg.dbias, st);
+          launch_bias_reduce(bpart, sp.bparts, Nw, p.H, p.HP, pg.dbias, st);
           bias_done = true;
         }
       };

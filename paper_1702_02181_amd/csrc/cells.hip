@@ -54,23 +54,22 @@ template <typename T, int BM, int PA, int PB>
 struct FwdIssue {
   const FwdArgs& a;
   const int (*srow)[BM];
-  const char* wrow;  // this lane's weight row (first stage), unit included
-  int wstep;         // bytes from one instruction's weight rows to the next (8 rows)
-  int wskip;         // weight columns before the first segment read: the set's input block when
-                     // this op reads no input
-  int c0, inp, wave, lr, lu;
+  int wskip;  // weight columns before the first segment read: the set's input block when this op
+              // reads no input
+  int c0, inp, wave, lr;
   int cur_seg = -1;
-  const char* rp[PA];  // this lane's A row in the current segment, unit included
+  const char* wp[PB];  // this lane's weight row per instruction (first stage), unit included
+  const char* rp[PA];  // this lane's A row per instruction in the current segment, unit included
   __device__ __forceinline__ void reload(int seg) {
     constexpr int es = sizeof(T);
     const bool is_in = a.has_input && seg == 0;
     const char* base = static_cast<const char*>(is_in ? a.table : a.h_pool);
     const size_t stride = (size_t)(is_in ? a.tld : a.ld) * es;
-    const char* zero = static_cast<const char*>(a.zero) + lu * 16;
 #pragma unroll
     for (int i = 0; i < PA; ++i) {
       const int sr = srow[seg][8 * (wave * PA + i) + lr];
-      rp[i] = sr >= 0 ? base + (size_t)sr * stride + lu * 16 : zero;
+      const int lu16 = unit_of_lane(threadIdx.x & 63, wave * PA + i) * 16;
+      rp[i] = (sr >= 0 ? base + (size_t)sr * stride : static_cast<const char*>(a.zero)) + lu16;
     }
     cur_seg = seg;
   }
@@ -90,7 +89,7 @@ struct FwdIssue {
 #pragma unroll
     for (int i = 0; i < PA; ++i) dma16(rp[i] + kc * es, Ad + (wave * PA + i) * 1024);
 #pragma unroll
-    for (int i = 0; i < PB; ++i) dma16(wrow + i * wstep + (kabs + wskip) * es, Bd + (wave * PB + i) * 1024);
+    for (int i = 0; i < PB; ++i) dma16(wp[i] + (kabs + wskip) * es, Bd + (wave * PB + i) * 1024);
   }
 };
 
@@ -204,11 +203,12 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
     c0 = min(nst, kz * per);
     c1 = min(nst, c0 + per);
   }
-  const int lr = row_of_lane(lane), lu = unit_of_lane(lane);
-  const char* wrow = static_cast<const char*>(a.Wf) +
-                     ((size_t)ub * BN + 8 * wave * PB + lr) * a.Kf * sizeof(T) + lu * 16;
-  FwdIssue<T, BM, PA, PB> issue{a, srow, wrow, 8 * a.Kf * (int)sizeof(T), a.has_input ? 0 : a.INP, c0, inp,
-                                wave, lr, lu};
+  const int lr = row_of_lane(lane);
+  FwdIssue<T, BM, PA, PB> issue{a, srow, a.has_input ? 0 : a.INP, c0, inp, wave, lr};
+#pragma unroll
+  for (int i = 0; i < PB; ++i)
+    issue.wp[i] = static_cast<const char*>(a.Wf) + ((size_t)ub * BN + 8 * (wave * PB + i) + lr) * a.Kf * sizeof(T) +
+                  unit_of_lane(lane, wave * PB + i) * 16;
   f32x16 acc[MT][G];
   zero_acc(acc);
   row_loop<T, MT, G>(c1 - c0, issue, A0, A1, B0, B1, acc, wave * 32 * MT, 0, lane);
@@ -457,22 +457,24 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx_f32(DxArgs a) {
   const int m0 = rt * BM, n0 = nt * BN;
   const int nst = a.Kb / 32, per = (nst + a.ksplit - 1) / a.ksplit;
   const int c0 = min(nst, kz * per), c1 = min(nst, c0 + per);
-  const int lr = row_of_lane(lane), lu = unit_of_lane(lane);
-  const char* zero = static_cast<const char*>(a.zero) + lu * 16;
+  const int lr = row_of_lane(lane);
+  const char* zero = static_cast<const char*>(a.zero);
   FixedRowsIssue<PA, PB> issue;
   issue.wave = wave;
 #pragma unroll
   for (int i = 0; i < PA; ++i) {
     const int row = m0 + 8 * (wave * PA + i) + lr;
-    issue.ap[i] = row < a.rows ? reinterpret_cast<const char*>(a.dz + (size_t)(a.row_begin + row) * a.gstride) +
-                                     c0 * 128 + lu * 16
-                               : zero;
+    const int lu16 = unit_of_lane(lane, wave * PA + i) * 16;
+    issue.ap[i] = (row < a.rows ? reinterpret_cast<const char*>(a.dz + (size_t)(a.row_begin + row) * a.gstride) +
+                                      c0 * 128
+                                : zero) + lu16;
   }
   const char* wb = static_cast<const char*>(a.Wb);
 #pragma unroll
   for (int i = 0; i < PB; ++i) {
     const int n = n0 + 8 * (wave * PB + i) + lr;
-    issue.bp[i] = n < a.Nb ? wb + (size_t)n * a.Kb * 4 + c0 * 128 + lu * 16 : zero;
+    const int lu16 = unit_of_lane(lane, wave * PB + i) * 16;
+    issue.bp[i] = (n < a.Nb ? wb + (size_t)n * a.Kb * 4 + c0 * 128 : zero) + lu16;
   }
   f32x16 acc[MT][TN];
   zero_acc(acc);

@@ -24,14 +24,17 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 
 // ---------------------------------------------------------------- row tiles
 // A stage of a row operand: ROWS rows x 128 bytes of K (32 fp32 or 64 bf16 values).  Row r's 16-byte
-// unit u sits in unit slot 8 r + (u ^ (r & 7)), so eight consecutive rows reading the same unit hit
-// eight distinct 16-byte bank groups (a 16-byte LDS read is served eight lanes at a time).  Wave
-// instruction t fills rows 8 t .. 8 t + 7: lane l fetches unit (l & 7) ^ (l >> 3) of row 8 t + (l >> 3).
+// unit u sits in unit slot 8 r + (u ^ ((r >> 1) & 7)).  A 16-byte LDS read is served for 16 lanes at a
+// time over 64 banks (16 groups of 16 bytes); sixteen consecutive rows reading the same unit land in
+// slots whose (r & 1, u ^ ((r >> 1) & 7)) are all distinct, i.e. in 16 distinct bank groups.  Wave
+// instruction t fills rows 8 t .. 8 t + 7: lane l fetches unit (l & 7) ^ swz(8 t + (l >> 3)) of row
+// 8 t + (l >> 3).
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ int row_of_lane(int lane) { return lane >> 3; }
-__device__ __forceinline__ int unit_of_lane(int lane) { return (lane & 7) ^ (lane >> 3); }
+__device__ __forceinline__ int unit_of_lane(int lane, int t) { return (lane & 7) ^ swz(8 * t + (lane >> 3)); }
 
 // byte offset of row r, unit u in a row tile
-__device__ __forceinline__ int rt_off(int r, int u) { return (r * 8 + (u ^ (r & 7))) * 16; }
+__device__ __forceinline__ int rt_off(int r, int u) { return (r * 8 + (u ^ swz(r))) * 16; }
 
 // acc[TM][TN] += A . B^T over one 128-byte stage of K, A rows arow0 + 32 tm + (lane % 32), B rows
 // brow0 + 32 tn + (lane % 32).  The K order inside the stage is permuted the same way for A and B:

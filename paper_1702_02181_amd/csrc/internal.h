@@ -29,8 +29,9 @@ WsLayout workspace_layout(const Sched& s, const Packed& p);
 // Weight-gradient work split: rows of one op reduced in `nchunk` chunks of `chunk` rows.
 struct WgradSplit {
   int nchunk = 0, chunk = 0;
+  int bparts = 0;  // rows of bias partial sums the launch writes
 };
-WgradSplit wgrad_split(int count, int Kw, int Nw);
+WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype);
 
 int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, void* h_pool,
                      float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st);
@@ -154,7 +155,8 @@ struct WgArgs {
   const float* dz;
   int chunk, nchunk;
   float* partial;  // [nchunk][Kw][Nw]
-  float* bpart;    // [nchunk][Nw] column sums of dz per chunk, or NULL
+  float* bpart;    // [bparts][Nw] column sums of dz (see WgradSplit), or NULL
+  const void* zero;  // a zero row at least 16 bytes past any column the kernels read
 };
 void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st);
 void launch_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP, int in_dim,

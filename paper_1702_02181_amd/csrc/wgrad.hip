@@ -16,6 +16,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "dma.h"
 #include "mfma.h"
 
 namespace fold {
@@ -26,6 +27,7 @@ constexpr int kThreads = 256;
 
 // Workgroup tile: 128 weight rows (m) x 256 gate columns (n); waves 2 x 2, each 64 x 128.
 constexpr int kTM = 128, kTN = 256;
+constexpr int kWgNW = 128;  // fp32 tile columns (two workgroups per compute unit)
 
 // Row indices of the pool rows a stage reduces over (pool row, child 0 / input row, child 1),
 // loaded two stages ahead into one of three LDS slots.
@@ -208,6 +210,179 @@ __global__ __launch_bounds__(kThreads) void k_wgrad(WgArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- fp32: direct loads into LDS
+// A stage is 32 op rows.  X^T tile: the 32 rows x 128 weight rows (512 bytes a row), dz^T tile: the 32
+// rows x NW gate columns.  Both are loaded straight into LDS, row-major in the op rows; a fragment read
+// (one K value per lane and instruction) is then one dword per lane, 32 consecutive columns per half
+// wave.  Odd rows have their 16-byte units permuted by ^ 8 so that the two half waves, which read
+// rows 2 s and 2 s + 1, hit different halves of the 64 banks.
+template <int NW>
+struct WgDma {
+  static constexpr int TM = 2, TN = NW / 64;      // wave tile 64 x NW / 2 (waves 2 x 2)
+  static constexpr int ABYTES = 32 * kTM * 4, BBYTES = 32 * NW * 4;
+  static constexpr int PA = ABYTES / 4096, PB = BBYTES / 4096;  // instructions per wave and stage
+  static constexpr int BLANES = NW / 4;           // lanes per dz row in one instruction
+};
+
+template <int NW>
+__global__ __launch_bounds__(kThreads) void k_wgrad_f32(WgArgs a) {
+  using D = WgDma<NW>;
+  constexpr int TM = D::TM, TN = D::TN, PA = D::PA, PB = D::PB;
+  __shared__ __attribute__((aligned(16))) char A0[D::ABYTES], A1[D::ABYTES], B0[D::BBYTES], B1[D::BBYTES];
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  const int wm = wave & 1, wn = wave >> 1, h = lane >> 5, l32 = lane & 31;
+  // all tiles of one row chunk read the same X and dz rows: keep them on one XCD
+  const int NT = (a.Nw + NW - 1) / NW, MTm = (a.Kw + kTM - 1) / kTM;
+  int tx, chunk_id;
+  if (!xcd_tile(MTm * NT, a.nchunk, tx, chunk_id)) return;
+  const int mt_ = tx % MTm, nt = tx / MTm;
+  const int m0 = mt_ * kTM, n0 = nt * NW;
+  const int lo = chunk_id * a.chunk, hi = min(a.count, lo + a.chunk);
+  const int nst = (hi - lo + 31) / 32;
+  const char* zero = static_cast<const char*>(a.zero);
+  const char* xbase = static_cast<const char*>(a.src);
+  const size_t xstride = (size_t)(a.seg ? a.ld : a.tld) * 4, dstride = (size_t)a.gstride * 4;
+
+  // per instruction: the op row inside the stage and the byte column this lane fetches
+  int amr[PA], acol[PA], achild[PA], bmr[PB], bcol[PB];
+  bool aok[PA], bok[PB];
+#pragma unroll
+  for (int i = 0; i < PA; ++i) {
+    const int t = wave * PA + i;
+    amr[i] = 2 * t + (lane >> 5);
+    const int u = (lane & 31) ^ (8 * (lane >> 5));
+    const int kw = m0 + 4 * u;
+    const int k = a.seg ? min(kw / a.HP, 1) : 0;
+    achild[i] = k;
+    acol[i] = (a.seg ? kw - k * a.HP : kw) * 4;
+    aok[i] = kw < a.Kw;
+  }
+#pragma unroll
+  for (int i = 0; i < PB; ++i) {
+    const int t = wave * PB + i;
+    bmr[i] = t * (64 / D::BLANES) + lane / D::BLANES;
+    const int u = (lane % D::BLANES) ^ (8 * (bmr[i] & 1));
+    const int n = n0 + 4 * u;
+    bcol[i] = n * 4;
+    bok[i] = n < a.Nw;
+  }
+  // Row indices of a stage: X rows (children's or leaf-table rows) and dz rows, loaded from a clamped
+  // (always valid) position; whether the row is real is kept apart and applied when the loads are
+  // issued, so no branch waits on an index load.
+  struct Idx {
+    int a[PA], b[PB];
+    bool va[PA], vb[PB];
+  };
+  auto load_idx = [&](int c, Idx& x) {
+#pragma unroll
+    for (int i = 0; i < PA; ++i) {
+      const int r = lo + c * 32 + amr[i];
+      const int rc = min(r, hi - 1);
+      x.a[i] = a.seg ? a.op_cpos[2 * rc + achild[i]] : a.op_inp[rc];
+      x.va[i] = r < hi && aok[i];
+    }
+#pragma unroll
+    for (int i = 0; i < PB; ++i) {
+      const int r = lo + c * 32 + bmr[i];
+      x.b[i] = a.op_rows[min(r, hi - 1)];
+      x.vb[i] = r < hi && bok[i];
+    }
+  };
+  auto issue = [&](const Idx& x, char* Ad, char* Bd) {
+#pragma unroll
+    for (int i = 0; i < PA; ++i)
+      dma16(x.va[i] && x.a[i] >= 0 ? xbase + (size_t)x.a[i] * xstride + acol[i] : zero, Ad + (wave * PA + i) * 1024);
+#pragma unroll
+    for (int i = 0; i < PB; ++i)
+      dma16(x.vb[i] ? reinterpret_cast<const char*>(a.dz) + (size_t)x.b[i] * dstride + bcol[i] : zero,
+            Bd + (wave * PB + i) * 1024);
+  };
+  // fragment byte offsets (row 2 s + h adds (2 s + h) * row bytes)
+  int aoff[TM], boff[TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int kw = wm * 64 + tm * 32 + l32;
+    aoff[tm] = h * (kTM * 4) + ((kw >> 2) ^ (8 * h)) * 16 + (kw & 3) * 4;
+  }
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+    const int n = wn * (NW / 2) + tn * 32 + l32;
+    boff[tn] = h * (NW * 4) + ((n >> 2) ^ (8 * h)) * 16 + (n & 3) * 4;
+  }
+  // bias column sums: thread tid sums column tid % NW over the stage rows r with r % MTm == mt_ and
+  // (r / MTm) % (256 / NW) == tid / NW, so the chunk's rows are split over its MTm row tiles
+  const bool do_bias = a.bpart != nullptr;
+  const int bc = tid % NW, bg = tid / NW;
+  const int bcoff = ((bc >> 2)) * 16 + (bc & 3) * 4;
+  float bsum = 0.f;
+
+  f32x16 acc[TM][TN];
+  zero_acc(acc);
+  auto stage = [&](const char* As, const char* Bs) {
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+      float av[TM], bv[TN];
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) av[tm] = *reinterpret_cast<const float*>(As + aoff[tm] + s * 2 * kTM * 4);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) bv[tn] = *reinterpret_cast<const float*>(Bs + boff[tn] + s * 2 * NW * 4);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[tm], bv[tn], acc[tm][tn], 0, 0, 0);
+    }
+    if (do_bias) {
+      for (int r = mt_ + MTm * bg; r < 32; r += MTm * (256 / NW))
+        bsum += *reinterpret_cast<const float*>(Bs + r * NW * 4 + (((bc >> 2) ^ (8 * (r & 1))) * 16) + (bc & 3) * 4);
+    }
+  };
+  (void)bcoff;
+
+  if (nst > 0) {
+    Idx iC, iN;
+    load_idx(0, iC);
+    vm_wait();
+    issue(iC, A0, B0);
+    if (nst > 1) load_idx(1, iN);
+    vm_wait();
+    __syncthreads();
+    int c = 0;
+    for (; c + 2 <= nst; c += 2) {
+      issue(iN, A1, B1);
+      if (c + 2 < nst) load_idx(c + 2, iC);
+      __builtin_amdgcn_sched_barrier(0);
+      stage(A0, B0);
+      vm_wait();
+      __syncthreads();
+      if (c + 2 < nst) {
+        issue(iC, A0, B0);
+        if (c + 3 < nst) load_idx(c + 3, iN);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      stage(A1, B1);
+      vm_wait();
+      __syncthreads();
+    }
+    if (c < nst) stage(A0, B0);
+  }
+
+  float* out = a.partial + (size_t)chunk_id * a.Kw * a.Nw;
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int n = n0 + wn * (NW / 2) + tn * 32 + l32;
+      if (n >= a.Nw) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 64 + tm * 32 + acc_row(r, lane);
+        if (m < a.Kw) out[(size_t)m * a.Nw + n] = acc[tm][tn][r];
+      }
+    }
+  if (do_bias && n0 + bc < a.Nw)
+    a.bpart[((size_t)(chunk_id * MTm + mt_) * (256 / NW) + bg) * a.Nw + n0 + bc] = bsum;
+}
+
 // dW[row, col] += sum over chunks of partial[chunk, m, n], (m, n) in the padded layout
 __global__ void k_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP,
                                int in_dim, int G, float* dW) {
@@ -255,27 +430,32 @@ __global__ void k_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int
 
 }  // namespace
 
-WgradSplit wgrad_split(int count, int Kw, int Nw) {
+WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype) {
   WgradSplit w;
   if (count <= 0 || Kw <= 0 || Nw <= 0) return w;
-  const long long tiles = (long long)((Kw + kTM - 1) / kTM) * ((Nw + kTN - 1) / kTN);
+  const int tn = dtype == FOLD_BF16 ? kTN : kWgNW;
+  const long long tiles = (long long)((Kw + kTM - 1) / kTM) * ((Nw + tn - 1) / tn);
   // enough workgroups to fill the chip, and chunks in multiples of the 8 XCDs (one XCD per chunk)
   const long long want = std::max(8LL, ((1024 + tiles - 1) / tiles + 7) / 8 * 8);
   const long long most = std::max(1, (count + 511) / 512);
   w.nchunk = (int)std::max(1LL, std::min(want, most));
   w.chunk = round_up((count + w.nchunk - 1) / w.nchunk, 64);
   w.nchunk = (count + w.chunk - 1) / w.chunk;
+  // bias partial rows: one per chunk (bf16), one per (chunk, weight-row tile, thread group) (fp32)
+  w.bparts = dtype == FOLD_BF16 ? w.nchunk : w.nchunk * ((Kw + kTM - 1) / kTM) * (256 / kWgNW);
   return w;
 }
 
 void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st) {
   if (a.count <= 0) return;
   ProfScope prof(dtype == FOLD_BF16 ? "wgrad.bf16" : "wgrad.f32", st);
-  dim3 grid(xcd_grid(((a.Kw + kTM - 1) / kTM) * ((a.Nw + kTN - 1) / kTN), a.nchunk));
-  if (dtype == FOLD_BF16)
+  if (dtype == FOLD_BF16) {
+    dim3 grid(xcd_grid(((a.Kw + kTM - 1) / kTM) * ((a.Nw + kTN - 1) / kTN), a.nchunk));
     hipLaunchKernelGGL(k_wgrad<uint16_t>, grid, dim3(kThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL(k_wgrad<float>, grid, dim3(kThreads), 0, st, a);
+  } else {
+    dim3 grid(xcd_grid(((a.Kw + kTM - 1) / kTM) * ((a.Nw + kWgNW - 1) / kWgNW), a.nchunk));
+    hipLaunchKernelGGL(k_wgrad_f32<kWgNW>, grid, dim3(kThreads), 0, st, a);
+  }
 }
 
 void launch_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP, int in_dim,
