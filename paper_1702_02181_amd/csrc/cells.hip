@@ -94,8 +94,9 @@ struct FwdIssue {
 };
 
 // The cell on one (row, unit) given z (bias included): writes h, c and the saved activations.
+// p0, p1: pool rows of child 0 / child 1 (-1: zero state)
 template <typename T, int KIND>
-__device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const float* z) {
+__device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const float* z, int p0, int p1) {
   const size_t p = (size_t)(a.row_begin + row);
   float h, c;
   float* gs = a.gates ? a.gates + p * a.gstride + j : nullptr;
@@ -103,11 +104,8 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
     const float i_ = sigmoidf_(z[0]), fl = sigmoidf_(z[1]), fr = sigmoidf_(z[2]), o = sigmoidf_(z[3]);
     const float u = tanhf_(z[4]);
     float cl = 0.f, cr = 0.f;
-    if (a.arity == 2) {
-      const int pl = a.child_pos[a.idx_off + row * 2], pr = a.child_pos[a.idx_off + row * 2 + 1];
-      if (pl >= 0) cl = a.c_pool[(size_t)pl * a.ld + j];
-      if (pr >= 0) cr = a.c_pool[(size_t)pr * a.ld + j];
-    }
+    if (p0 >= 0) cl = a.c_pool[(size_t)p0 * a.ld + j];
+    if (p1 >= 0) cr = a.c_pool[(size_t)p1 * a.ld + j];
     c = i_ * u + fl * cl + fr * cr;
     h = o * tanhf_(c);
     if (gs) {
@@ -120,8 +118,7 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
   } else if constexpr (KIND == FOLD_LSTM) {
     const float i_ = sigmoidf_(z[0]), f = sigmoidf_(z[1]), o = sigmoidf_(z[2]);
     const float u = tanhf_(z[3]);
-    const int pc = a.child_pos[a.idx_off + row];
-    const float cp = pc >= 0 ? a.c_pool[(size_t)pc * a.ld + j] : 0.f;
+    const float cp = p0 >= 0 ? a.c_pool[(size_t)p0 * a.ld + j] : 0.f;
     c = i_ * u + f * cp;
     h = o * tanhf_(c);
     if (gs) {
@@ -134,8 +131,7 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
     h = tanhf_(z[0]);
     c = 0.f;
     if constexpr (KIND == FOLD_PROJ) {
-      const int pc = a.child_pos[a.idx_off + row];
-      c = pc >= 0 ? a.c_pool[(size_t)pc * a.ld + j] : 0.f;
+      c = p0 >= 0 ? a.c_pool[(size_t)p0 * a.ld + j] : 0.f;
     }
     if (gs) gs[0] = h;
   }
@@ -236,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = m0 + wave * 32 * MT + mt * 32 + acc_row(r, lane);
+      const int rl = wave * 32 * MT + mt * 32 + acc_row(r, lane), row = m0 + rl;
       if (row >= a.rows) continue;
       if (j >= a.H) {
         if (j < a.ld) pad_out<T>(a, row, j);
@@ -245,7 +241,10 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
       float z[G];
 #pragma unroll
       for (int g = 0; g < G; ++g) z[g] = acc[mt][g][r] + bz[g];
-      cell_out<T, KIND>(a, row, j, z);
+      // the children's pool rows are already in LDS (the gather's row table)
+      const int p0 = a.arity >= 1 ? srow[a.has_input][rl] : -1;
+      const int p1 = a.arity >= 2 ? srow[a.has_input + 1][rl] : -1;
+      cell_out<T, KIND>(a, row, j, z, p0, p1);
     }
   }
 }
@@ -256,6 +255,8 @@ __global__ void k_cell_epi(FwdArgs a, int nsplit) {
   constexpr int G = Gates<KIND>::G;
   const int row = blockIdx.x;
   const int zs = G * a.HP;
+  const int p0 = a.arity >= 1 ? a.child_pos[a.idx_off + row * a.arity] : -1;
+  const int p1 = a.arity >= 2 ? a.child_pos[a.idx_off + row * a.arity + 1] : -1;
   for (int j = threadIdx.x; j < a.HP; j += blockDim.x) {
     if (j >= a.H) {
       if (j < a.ld) pad_out<T>(a, row, j);
@@ -268,7 +269,7 @@ __global__ void k_cell_epi(FwdArgs a, int nsplit) {
       for (int sp = 0; sp < nsplit; ++sp) v += a.zpart[((size_t)sp * a.rows + row) * zs + g * a.HP + j];
       z[g] = v;
     }
-    cell_out<T, KIND>(a, row, j, z);
+    cell_out<T, KIND>(a, row, j, z, p0, p1);
   }
 }
 
@@ -438,6 +439,8 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx_f32(DxArgs a) {
   constexpr int BM = 4 * 32 * MT, BN = 32 * TN;  // four waves of 32*MT rows x 128 columns
   constexpr int PA = BM / 32, PB = BN / 32;
   __shared__ __attribute__((aligned(16))) char A0[BM * 128], A1[BM * 128], B0[BN * 128], B1[BN * 128];
+  __shared__ int tgt[2][BM];  // per tile row: child k's pool row (mode 0) or the leaf-table row (mode 1)
+  __shared__ char sgl[2][BM];  // the child has one parent edge: plain read-add-write
   const int lane = threadIdx.x & 63, wave = wave_id();
   // co-locate the workgroups that share the larger operand (a row tile's dz rows or a column tile's
   // weight slice) on one XCD
@@ -455,6 +458,26 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx_f32(DxArgs a) {
     kz = tx / R;
   }
   const int m0 = rt * BM, n0 = nt * BN;
+  if constexpr (!SPLIT) {
+    // scatter targets of the tile's rows, published by the K loop's first barrier
+    for (int i = threadIdx.x; i < 2 * BM; i += kThreads) {
+      const int k = i / BM, rl = i - k * BM, row = m0 + rl;
+      int t = -1;
+      char one = 0;
+      if (row < a.rows) {
+        if (a.mode == 0) {
+          if (k < a.arity) {
+            t = a.child_pos[a.idx_off + row * a.arity + k];
+            one = t >= 0 && a.npar[t] == 1;
+          }
+        } else if (k == 0) {
+          t = a.input_idx[a.row_begin + row];
+        }
+      }
+      tgt[k][rl] = t;
+      sgl[k][rl] = one;
+    }
+  }
   const int nst = a.Kb / 32, per = (nst + a.ksplit - 1) / a.ksplit;
   const int c0 = min(nst, kz * per), c1 = min(nst, c0 + per);
   const int lr = row_of_lane(lane);
@@ -485,14 +508,22 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx_f32(DxArgs a) {
     for (int tn = 0; tn < TN; ++tn) {
       const int n = n0 + tn * 32 + (lane & 31);
       if (n >= a.Nb) continue;
+      const int k = a.mode == 0 ? n / a.HP : 0, jin = a.mode == 0 ? n - k * a.HP : n;
+      if (jin >= (a.mode == 0 ? a.H : a.in_dim)) continue;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wave * 32 * MT + tm * 32 + acc_row(r, lane);
+        const int rl = wave * 32 * MT + tm * 32 + acc_row(r, lane), row = m0 + rl;
         if (row >= a.rows) continue;
-        if constexpr (SPLIT)
+        if constexpr (SPLIT) {
           a.xpart[((size_t)kz * a.rows + row) * a.Nb + n] = acc[tm][tn][r];
-        else
-          dx_scatter(a, row, n, acc[tm][tn][r]);
+        } else {
+          const int t = tgt[k][rl];
+          if (t < 0) continue;
+          if (a.mode == 0)
+            scatter_add(&a.dh[(size_t)t * a.ld + jin], acc[tm][tn][r], sgl[k][rl]);
+          else
+            unsafeAtomicAdd(&a.d_table[(size_t)t * a.tld + jin], acc[tm][tn][r]);
+        }
       }
     }
   }

@@ -418,14 +418,21 @@ __global__ void k_bias_partial(const int* op_rows, int count, int chunk, const f
   bpart[(size_t)c * Nw + n] = s;
 }
 
-__global__ void k_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, float* dbias) {
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
-  if (n >= Nw) return;
+// db[col] += sum over partial rows, 64 columns per block: four thread groups sum interleaved partial
+// rows, then the four sums are added in a fixed order (the result does not depend on scheduling)
+__global__ void k_bias_reduce(const float* bpart, int nparts, int Nw, int H, int HP, float* dbias) {
+  __shared__ float red[4][64];
+  const int cg = threadIdx.x & 63, pg = threadIdx.x >> 6;
+  const int n = blockIdx.x * 64 + cg;
+  float s = 0.f;
+  if (n < Nw)
+    for (int c = pg; c < nparts; c += 4) s += bpart[(size_t)c * Nw + n];
+  red[pg][cg] = s;
+  __syncthreads();
+  if (pg != 0 || n >= Nw) return;
   const int g = n / HP, j = n - g * HP;
   if (j >= H) return;
-  float s = 0.f;
-  for (int c = 0; c < nchunk; ++c) s += bpart[(size_t)c * Nw + n];
-  dbias[g * H + j] += s;
+  dbias[g * H + j] += (red[0][cg] + red[1][cg]) + (red[2][cg] + red[3][cg]);
 }
 
 }  // namespace
@@ -478,7 +485,7 @@ void launch_bias_partial(const int* op_rows, int count, int chunk, int nchunk, c
 void launch_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, float* dbias, hipStream_t st) {
   if (nchunk <= 0) return;
   ProfScope prof("bias_reduce", st);
-  hipLaunchKernelGGL(k_bias_reduce, dim3((Nw + 255) / 256), dim3(256), 0, st, bpart, nchunk, Nw, H, HP, dbias);
+  hipLaunchKernelGGL(k_bias_reduce, dim3((Nw + 63) / 64), dim3(256), 0, st, bpart, nchunk, Nw, H, HP, dbias);
 }
 
 }  // namespace fold
