@@ -93,19 +93,22 @@ struct FwdIssue {
   }
 };
 
-// The cell on one (row, unit) given z (bias included): writes h, c and the saved activations.
-// p0, p1: pool rows of child 0 / child 1 (-1: zero state)
+// children whose cell state a cell reads
+template <int KIND>
+struct CKids {
+  static constexpr int N = KIND == FOLD_TREELSTM ? 2 : ((KIND == FOLD_LSTM || KIND == FOLD_PROJ) ? 1 : 0);
+};
+
+// The cell on one (row, unit) given z (bias included) and the children's c (0 for the zero state):
+// writes h, c and the saved activations.
 template <typename T, int KIND>
-__device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const float* z, int p0, int p1) {
+__device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const float* z, float cl, float cr) {
   const size_t p = (size_t)(a.row_begin + row);
   float h, c;
   float* gs = a.gates ? a.gates + p * a.gstride + j : nullptr;
   if constexpr (KIND == FOLD_TREELSTM) {
     const float i_ = sigmoidf_(z[0]), fl = sigmoidf_(z[1]), fr = sigmoidf_(z[2]), o = sigmoidf_(z[3]);
     const float u = tanhf_(z[4]);
-    float cl = 0.f, cr = 0.f;
-    if (p0 >= 0) cl = a.c_pool[(size_t)p0 * a.ld + j];
-    if (p1 >= 0) cr = a.c_pool[(size_t)p1 * a.ld + j];
     c = i_ * u + fl * cl + fr * cr;
     h = o * tanhf_(c);
     if (gs) {
@@ -118,8 +121,7 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
   } else if constexpr (KIND == FOLD_LSTM) {
     const float i_ = sigmoidf_(z[0]), f = sigmoidf_(z[1]), o = sigmoidf_(z[2]);
     const float u = tanhf_(z[3]);
-    const float cp = p0 >= 0 ? a.c_pool[(size_t)p0 * a.ld + j] : 0.f;
-    c = i_ * u + f * cp;
+    c = i_ * u + f * cl;
     h = o * tanhf_(c);
     if (gs) {
       gs[0] = i_;
@@ -130,9 +132,8 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
   } else {
     h = tanhf_(z[0]);
     c = 0.f;
-    if constexpr (KIND == FOLD_PROJ) {
-      c = p0 >= 0 ? a.c_pool[(size_t)p0 * a.ld + j] : 0.f;
-    }
+    if constexpr (KIND == FOLD_PROJ) c = cl;
+    (void)cr;
     if (gs) gs[0] = h;
   }
   static_cast<T*>(a.h_pool)[p * a.ld + j] = from_f32<T>(h);
@@ -224,10 +225,28 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
       }
     return;
   }
-  // epilogue: the cell, in registers
+  // epilogue: the cell, in registers.  The children's c of every row this lane finishes is loaded
+  // first, all at once (pool rows from the LDS row table; absent children and rows past the end read
+  // the zero row), so the loads overlap instead of each waiting its turn.
+  constexpr int NK = CKids<KIND>::N;
   float bz[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) bz[g] = a.bias[g * a.HP + j];
+  float cc[MT][16][NK > 0 ? NK : 1];
+  if constexpr (NK > 0) {
+    const float* zf = static_cast<const float*>(a.zero) + j;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl = wave * 32 * MT + mt * 32 + acc_row(r, lane);
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {
+          const int p = k < a.arity ? srow[a.has_input + k][rl] : -1;
+          cc[mt][r][k] = *(p >= 0 ? a.c_pool + (size_t)p * a.ld + j : zf);
+        }
+      }
+  }
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
@@ -241,10 +260,8 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
       float z[G];
 #pragma unroll
       for (int g = 0; g < G; ++g) z[g] = acc[mt][g][r] + bz[g];
-      // the children's pool rows are already in LDS (the gather's row table)
-      const int p0 = a.arity >= 1 ? srow[a.has_input][rl] : -1;
-      const int p1 = a.arity >= 2 ? srow[a.has_input + 1][rl] : -1;
-      cell_out<T, KIND>(a, row, j, z, p0, p1);
+      const float cl = NK > 0 ? cc[mt][r][0] : 0.f, cr = NK > 1 ? cc[mt][r][NK > 1 ? 1 : 0] : 0.f;
+      cell_out<T, KIND>(a, row, j, z, cl, cr);
     }
   }
 }
@@ -257,6 +274,9 @@ __global__ void k_cell_epi(FwdArgs a, int nsplit) {
   const int zs = G * a.HP;
   const int p0 = a.arity >= 1 ? a.child_pos[a.idx_off + row * a.arity] : -1;
   const int p1 = a.arity >= 2 ? a.child_pos[a.idx_off + row * a.arity + 1] : -1;
+  const float* zf = static_cast<const float*>(a.zero);
+  const float* c0r = p0 >= 0 ? a.c_pool + (size_t)p0 * a.ld : zf;
+  const float* c1r = p1 >= 0 ? a.c_pool + (size_t)p1 * a.ld : zf;
   for (int j = threadIdx.x; j < a.HP; j += blockDim.x) {
     if (j >= a.H) {
       if (j < a.ld) pad_out<T>(a, row, j);
@@ -269,7 +289,7 @@ __global__ void k_cell_epi(FwdArgs a, int nsplit) {
       for (int sp = 0; sp < nsplit; ++sp) v += a.zpart[((size_t)sp * a.rows + row) * zs + g * a.HP + j];
       z[g] = v;
     }
-    cell_out<T, KIND>(a, row, j, z, p0, p1);
+    cell_out<T, KIND>(a, row, j, z, c0r[j], c1r[j]);
   }
 }
 
