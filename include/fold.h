@@ -167,7 +167,7 @@ typedef struct {
 
 typedef struct {
   int32_t dtype;  /* FOLD_F32 or FOLD_BF16 */
-  int32_t hidden; /* H */
+  int32_t hidden; /* H, 1 .. 4096 */
   int32_t num_sets;
   const fold_param_set* sets; /* host [num_sets] */
 } fold_params;

@@ -352,6 +352,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     b.npar = s.pos_npar;
     b.d_table = d_table;
     b.tld = tld;
+    b.dz_bf16 = p.dtype == FOLD_BF16;
     launch_cell_bwd(op.kind, b, st);
     if (op.kind == FOLD_EMBED) continue;
     DxArgs d;
@@ -433,7 +434,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       if (op.has_input && ps.INP > 0 && pg.dW_in) run(0, ps.INP, table, pg.dW_in);
       if (pg.dbias && !bias_done) {
         const int chunk = 512, nchunk = (count + chunk - 1) / chunk;
-        launch_bias_partial(w.op_rows, count, chunk, nchunk, gates, L.gstride, Nw, bpart, st);
+        launch_bias_partial(w.op_rows, count, chunk, nchunk, gates, L.gstride, Nw, p.dtype == FOLD_BF16, bpart, st);
         launch_bias_reduce(bpart, nchunk, Nw, p.H, p.HP, pg.dbias, st);
       }
     }
@@ -594,7 +595,8 @@ int32_t fold_pack_params(const fold_params* prm, hipStream_t st, fold_packed** o
   *out = nullptr;
   if (!prm || !prm->sets || prm->num_sets < 1) return fail(FOLD_E_INVALID, "fold_pack_params: no parameter sets");
   if (prm->dtype != FOLD_F32 && prm->dtype != FOLD_BF16) return fail(FOLD_E_INVALID, "fold_pack_params: bad dtype");
-  if (prm->hidden < 1) return fail(FOLD_E_INVALID, "fold_pack_params: hidden must be positive");
+  if (prm->hidden < 1 || prm->hidden > kMaxHidden)
+    return fail(FOLD_E_INVALID, "fold_pack_params: hidden must be in 1.." + std::to_string(kMaxHidden));
   for (int i = 0; i < prm->num_sets; ++i) {
     const fold_param_set& s = prm->sets[i];
     const std::string at = "fold_pack_params: set " + std::to_string(i) + ": ";

@@ -330,9 +330,14 @@ __global__ void k_bwd_roots(int ld, const float* dh_roots, const int* root_pos, 
   for (int j = threadIdx.x; j < ld; j += blockDim.x) dh[p * ld + j] += dh_roots[(size_t)r * ld + j];
 }
 
-template <int KIND>
+// dz of one row from its saved activations.  fp32 parameters: dz overwrites the activations in place
+// (each thread rewrites only the elements it read).  bf16 parameters: dz goes to the first G*HP bf16
+// slots of the row, the matrix-core operand of dz . W^T and of the weight gradients; the row is first
+// read completely, the bf16 values are staged in LDS (dynamic, G*HP halves) and then written out.
+template <int KIND, bool BF>
 __global__ void k_cell_bwd(BwdCellArgs a) {
   constexpr int G = Gates<KIND>::G;
+  extern __shared__ __attribute__((aligned(16))) uint16_t sdz[];
   const int row = blockIdx.x;
   const size_t p = (size_t)(a.row_begin + row);
   float* gb = a.gates + p * a.gstride;
@@ -340,11 +345,17 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
   if (a.arity >= 1) c0 = a.child_pos[a.idx_off + row * a.arity];
   if (a.arity >= 2) c1 = a.child_pos[a.idx_off + row * a.arity + 1];
   const bool s0 = c0 >= 0 && a.npar[c0] == 1, s1 = c1 >= 0 && a.npar[c1] == 1;
+  auto put = [&](int g, int j, float v) {
+    if constexpr (BF)
+      sdz[g * a.HP + j] = f2bf(v);
+    else
+      gb[g * a.HP + j] = v;
+  };
   for (int j = threadIdx.x; j < a.HP; j += blockDim.x) {
     if (j >= a.H) {
       if constexpr (KIND != FOLD_EMBED) {
 #pragma unroll
-        for (int g = 0; g < G; ++g) gb[g * a.HP + j] = 0.f;
+        for (int g = 0; g < G; ++g) put(g, j, 0.f);
       }
       continue;
     }
@@ -358,11 +369,11 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       const float cl = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
       const float cr = c1 >= 0 ? a.c_pool[(size_t)c1 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
-      gb[j] = dct * u * i_ * (1.f - i_);
-      gb[a.HP + j] = dct * cl * fl * (1.f - fl);
-      gb[2 * a.HP + j] = dct * cr * fr * (1.f - fr);
-      gb[3 * a.HP + j] = dh * tc * o * (1.f - o);
-      gb[4 * a.HP + j] = dct * i_ * (1.f - u * u);
+      put(0, j, dct * u * i_ * (1.f - i_));
+      put(1, j, dct * cl * fl * (1.f - fl));
+      put(2, j, dct * cr * fr * (1.f - fr));
+      put(3, j, dh * tc * o * (1.f - o));
+      put(4, j, dct * i_ * (1.f - u * u));
       if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dct * fl, s0);
       if (c1 >= 0) scatter_add(&a.dc[(size_t)c1 * a.ld + j], dct * fr, s1);
     } else if constexpr (KIND == FOLD_LSTM) {
@@ -371,71 +382,29 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cp = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
-      gb[j] = dct * u * i_ * (1.f - i_);
-      gb[a.HP + j] = dct * cp * f * (1.f - f);
-      gb[2 * a.HP + j] = dh * tc * o * (1.f - o);
-      gb[3 * a.HP + j] = dct * i_ * (1.f - u * u);
+      put(0, j, dct * u * i_ * (1.f - i_));
+      put(1, j, dct * cp * f * (1.f - f));
+      put(2, j, dh * tc * o * (1.f - o));
+      put(3, j, dct * i_ * (1.f - u * u));
       if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dct * f, s0);
     } else {
       const float h = gb[j];
-      gb[j] = dh * (1.f - h * h);
+      put(0, j, dh * (1.f - h * h));
       if constexpr (KIND == FOLD_PROJ) {
         const float dc = a.dc[p * a.ld + j];
         if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dc, s0);
       }
     }
   }
+  if constexpr (BF && KIND != FOLD_EMBED) {
+    __syncthreads();  // every read of the row's activations is done and the staged dz is complete
+    uint4* dst = reinterpret_cast<uint4*>(gb);
+    const uint4* src = reinterpret_cast<const uint4*>(sdz);
+    for (int v = threadIdx.x; v < G * a.HP / 8; v += blockDim.x) dst[v] = src[v];
+  }
 }
 
 // ---------------------------------------------------------------- backward, dz . W^T
-
-// rows of fp32 dz, converted to the operand type when written to LDS
-template <typename T, int VROW>
-struct DzRows;
-
-template <int VROW>
-struct DzRows<float, VROW> {
-  using raw = Raw4;
-  const float* dz;
-  int gstride, row_begin, rows, m0, c0;
-  __device__ __forceinline__ raw fetch(int c, int i) const {
-    const int r = i / VROW, v = i - r * VROW, row = m0 + r;
-    const int ok = row < rows;
-    const float* p = dz + (size_t)(row_begin + (ok ? row : 0)) * gstride + (c + c0) * 32 + v * 4;
-    return {*reinterpret_cast<const uint4*>(p), ok ? 4 : 0};
-  }
-  __device__ __forceinline__ uint4 put(const raw& r) const { return finish<float>(r); }
-};
-
-template <int VROW>
-struct DzRows<uint16_t, VROW> {
-  using raw = Raw8;
-  const float* dz;
-  int gstride, row_begin, rows, m0, c0;
-  __device__ __forceinline__ raw fetch(int c, int i) const {
-    const int r = i / VROW, v = i - r * VROW, row = m0 + r;
-    const int ok = row < rows;
-    const float* p = dz + (size_t)(row_begin + (ok ? row : 0)) * gstride + (c + c0) * 64 + v * 8;
-    return {reinterpret_cast<const uint4*>(p)[0], reinterpret_cast<const uint4*>(p)[1], ok ? 8 : 0};
-  }
-  __device__ __forceinline__ uint4 put(const raw& r) const { return finish_bf16(r); }
-};
-
-// packed backward weights W^T, n-major, rows past Nb read as zero
-template <typename T, int VROW>
-struct WeightRows {
-  using raw = Raw4;
-  const T* W;
-  int Kb, Nb, n0, c0;
-  __device__ __forceinline__ raw fetch(int c, int i) const {
-    constexpr int BK = Mma<T>::BK, VEC = Mma<T>::VEC;
-    const int n = i / VROW, v = i - n * VROW;
-    const int ok = n0 + n < Nb;
-    return {*reinterpret_cast<const uint4*>(W + (size_t)(ok ? n0 + n : 0) * Kb + (c + c0) * BK + v * VEC),
-            ok ? VEC : 0};
-  }
-  __device__ __forceinline__ uint4 put(const raw& r) const { return finish<T>(r); }
-};
 
 // scatter one element of dz . W^T: mode 0 into the child's dh, mode 1 into the leaf-table gradient
 __device__ __forceinline__ void dx_scatter(const DxArgs& a, int row, int n, float v) {
@@ -452,9 +421,10 @@ __device__ __forceinline__ void dx_scatter(const DxArgs& a, int row, int n, floa
 }
 
 // dz . W^T for one tile of 128 * MT rows x 128 columns of the children's (or the input's) gradient:
-// dz rows (fp32 for fp32 parameters) and the packed W^T rows are loaded straight into LDS.
-template <int MT, bool SPLIT>
-__global__ __launch_bounds__(kThreads) void k_bwd_dx_f32(DxArgs a) {
+// dz rows (fp32, or bf16 at the start of each row for bf16 parameters) and the packed W^T rows are
+// loaded straight into LDS.
+template <typename T, int MT, bool SPLIT>
+__global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
   constexpr int TN = 4;
   constexpr int BM = 4 * 32 * MT, BN = 32 * TN;  // four waves of 32*MT rows x 128 columns
   constexpr int PA = BM / 32, PB = BN / 32;
@@ -498,7 +468,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx_f32(DxArgs a) {
       sgl[k][rl] = one;
     }
   }
-  const int nst = a.Kb / 32, per = (nst + a.ksplit - 1) / a.ksplit;
+  const int nst = a.Kb * (int)sizeof(T) / 128, per = (nst + a.ksplit - 1) / a.ksplit;
   const int c0 = min(nst, kz * per), c1 = min(nst, c0 + per);
   const int lr = row_of_lane(lane);
   const char* zero = static_cast<const char*>(a.zero);
@@ -517,11 +487,11 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx_f32(DxArgs a) {
   for (int i = 0; i < PB; ++i) {
     const int n = n0 + 8 * (wave * PB + i) + lr;
     const int lu16 = unit_of_lane(lane, wave * PB + i) * 16;
-    issue.bp[i] = (n < a.Nb ? wb + (size_t)n * a.Kb * 4 + c0 * 128 : zero) + lu16;
+    issue.bp[i] = (n < a.Nb ? wb + (size_t)n * a.Kb * sizeof(T) + c0 * 128 : zero) + lu16;
   }
   f32x16 acc[MT][TN];
   zero_acc(acc);
-  row_loop<float, MT, TN>(c1 - c0, issue, A0, A1, B0, B1, acc, wave * 32 * MT, 0, lane);
+  row_loop<T, MT, TN>(c1 - c0, issue, A0, A1, B0, B1, acc, wave * 32 * MT, 0, lane);
 #pragma unroll
   for (int tm = 0; tm < MT; ++tm) {
 #pragma unroll
@@ -544,59 +514,6 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx_f32(DxArgs a) {
           else
             unsafeAtomicAdd(&a.d_table[(size_t)t * a.tld + jin], acc[tm][tn][r]);
         }
-      }
-    }
-  }
-}
-
-template <typename T, int MT, bool SPLIT>
-__global__ __launch_bounds__(kThreads) void k_bwd_dx(DxArgs a) {
-  using M = Mma<T>;
-  constexpr int TN = 4;
-  constexpr int BM = 4 * 32 * MT, BN = 32 * TN;  // four waves of 32*MT rows x 128 columns
-  using TA = Tile<T, BM, kRK>;
-  using TB = Tile<T, BN, kRK>;
-  __shared__ __attribute__((aligned(16))) T As[TA::ELEMS];
-  __shared__ __attribute__((aligned(16))) T Bs[TB::ELEMS];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // co-locate the workgroups that share the larger operand (a row tile's dz rows or a column tile's
-  // weight slice) on one XCD
-  const int R = (a.rows + BM - 1) / BM, NT = (a.Nb + BN - 1) / BN;
-  int tx, ty, nt, rt, kz;
-  if (a.share_rows) {
-    if (!xcd_tile(NT * a.ksplit, R, tx, ty)) return;
-    rt = ty;
-    nt = tx % NT;
-    kz = tx / NT;
-  } else {
-    if (!xcd_tile(R * a.ksplit, NT, tx, ty)) return;
-    nt = ty;
-    rt = tx % R;
-    kz = tx / R;
-  }
-  const int m0 = rt * BM, n0 = nt * BN;
-  const int nst = a.Kb / M::BK, per = (nst + a.ksplit - 1) / a.ksplit;
-  const int c0 = min(nst, kz * per), c1 = min(nst, c0 + per);
-  DzRows<T, TA::VROW> la{a.dz, a.gstride, a.row_begin, a.rows, m0, c0};
-  WeightRows<T, TB::VROW> lb{static_cast<const T*>(a.Wb), a.Kb, a.Nb, n0, c0};
-  NoIndex ix;
-  f32x16 acc[MT][TN];
-  zero_acc(acc);
-  mainloop<T, TA, TB, MT, TN>(c1 - c0, la, lb, ix, As, Bs, acc, wave * 32 * MT, 0);
-#pragma unroll
-  for (int tm = 0; tm < MT; ++tm) {
-#pragma unroll
-    for (int tn = 0; tn < TN; ++tn) {
-      const int n = n0 + tn * 32 + (lane & 31);
-      if (n >= a.Nb) continue;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wave * 32 * MT + tm * 32 + acc_row(r, lane);
-        if (row >= a.rows) continue;
-        if constexpr (SPLIT)
-          a.xpart[((size_t)kz * a.rows + row) * a.Nb + n] = acc[tm][tn][r];
-        else
-          dx_scatter(a, row, n, acc[tm][tn][r]);
       }
     }
   }
@@ -702,14 +619,19 @@ void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
                                 "cell_bwd.proj"};
   ProfScope prof(kind >= 0 && kind <= 4 ? names[kind] : "cell_bwd", st);
   dim3 grid(a.rows), block(256);
+  const size_t lds = a.dz_bf16 ? (size_t)gates_of(kind) * a.HP * sizeof(uint16_t) : 0;
+#define FOLD_CB(K_)                                                                          \
+  if (a.dz_bf16) hipLaunchKernelGGL((k_cell_bwd<K_, true>), grid, block, lds, st, a);        \
+  else hipLaunchKernelGGL((k_cell_bwd<K_, false>), grid, block, 0, st, a);
   switch (kind) {
-    case FOLD_EMBED: hipLaunchKernelGGL(k_cell_bwd<FOLD_EMBED>, grid, block, 0, st, a); break;
-    case FOLD_TREERNN: hipLaunchKernelGGL(k_cell_bwd<FOLD_TREERNN>, grid, block, 0, st, a); break;
-    case FOLD_TREELSTM: hipLaunchKernelGGL(k_cell_bwd<FOLD_TREELSTM>, grid, block, 0, st, a); break;
-    case FOLD_LSTM: hipLaunchKernelGGL(k_cell_bwd<FOLD_LSTM>, grid, block, 0, st, a); break;
-    case FOLD_PROJ: hipLaunchKernelGGL(k_cell_bwd<FOLD_PROJ>, grid, block, 0, st, a); break;
+    case FOLD_EMBED: hipLaunchKernelGGL((k_cell_bwd<FOLD_EMBED, false>), grid, block, 0, st, a); break;
+    case FOLD_TREERNN: FOLD_CB(FOLD_TREERNN) break;
+    case FOLD_TREELSTM: FOLD_CB(FOLD_TREELSTM) break;
+    case FOLD_LSTM: FOLD_CB(FOLD_LSTM) break;
+    case FOLD_PROJ: FOLD_CB(FOLD_PROJ) break;
     default: break;
   }
+#undef FOLD_CB
 }
 
 void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
@@ -722,18 +644,16 @@ void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
   a.share_rows = a.rows >= a.Nb;
   const int R = (int)cdiv(a.rows, 128 * MT), NT = (int)cdiv(a.Nb, 128);
   dim3 grid(a.share_rows ? xcd_grid(NT * pl.ksplit, R) : xcd_grid(R * pl.ksplit, NT));
-#define FOLD_DX(T_, MT_, S_) hipLaunchKernelGGL((k_bwd_dx<T_, MT_, S_>), grid, dim3(kThreads), 0, st, a)
+#define FOLD_DX(T_, MT_, S_) hipLaunchKernelGGL((k_bwd_dx2<T_, MT_, S_>), grid, dim3(kThreads), 0, st, a)
   const bool split = pl.ksplit > 1;
-#define FOLD_DX32(MT_, S_) hipLaunchKernelGGL((k_bwd_dx_f32<MT_, S_>), grid, dim3(kThreads), 0, st, a)
   if (dtype == FOLD_BF16) {
     if (MT == 2) { if (split) FOLD_DX(uint16_t, 2, true); else FOLD_DX(uint16_t, 2, false); }
     else { if (split) FOLD_DX(uint16_t, 1, true); else FOLD_DX(uint16_t, 1, false); }
   } else {
-    if (MT == 2) { if (split) FOLD_DX32(2, true); else FOLD_DX32(2, false); }
-    else { if (split) FOLD_DX32(1, true); else FOLD_DX32(1, false); }
+    if (MT == 2) { if (split) FOLD_DX(float, 2, true); else FOLD_DX(float, 2, false); }
+    else { if (split) FOLD_DX(float, 1, true); else FOLD_DX(float, 1, false); }
   }
 #undef FOLD_DX
-#undef FOLD_DX32
   if (split) hipLaunchKernelGGL(k_dx_epi, dim3(a.rows), dim3(256), 0, st, a, pl.ksplit);
 }
 

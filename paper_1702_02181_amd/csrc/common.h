@@ -17,6 +17,7 @@ constexpr int kWave = 64;          // CDNA wavefront
 constexpr int kUnit = 32;          // hidden units per MFMA output tile column block
 constexpr int kPadK = 64;          // every K segment (input width, hidden) is padded to this
 constexpr int kMaxGates = 5;
+constexpr int kMaxHidden = 4096;   // the backward stages one row's bf16 dz (G * HP halves) in LDS
 
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 inline int64_t round_up64(int64_t x, int64_t m) { return (x + m - 1) / m * m; }

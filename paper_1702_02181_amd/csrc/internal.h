@@ -118,6 +118,7 @@ struct BwdCellArgs {
   const int* npar;  // parent edges per pool row: 1 -> plain read-add-write, else atomic add
   float* d_table;
   int tld;
+  int dz_bf16;  // write dz as bf16 (the operand type of bf16 parameters)
 };
 void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st);
 void launch_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* dh_roots, const int* root_pos,
@@ -162,7 +163,7 @@ void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st);
 void launch_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP, int in_dim,
                          int G, float* dW, hipStream_t st);
 void launch_bias_partial(const int* op_rows, int count, int chunk, int nchunk, const float* dz, int gstride,
-                         int Nw, float* bpart, hipStream_t st);
+                         int Nw, int bf, float* bpart, hipStream_t st);
 void launch_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, float* dbias, hipStream_t st);
 
 // ---- achievable-peak probes (diag.hip) ----

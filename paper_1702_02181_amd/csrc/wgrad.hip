@@ -26,189 +26,8 @@ namespace {
 constexpr int kThreads = 256;
 
 // Workgroup tile: 128 weight rows (m) x 256 gate columns (n); waves 2 x 2, each 64 x 128.
-constexpr int kTM = 128, kTN = 256;
+constexpr int kTM = 128;  // weight rows per tile
 constexpr int kWgNW = 128;  // fp32 tile columns (two workgroups per compute unit)
-
-// Row indices of the pool rows a stage reduces over (pool row, child 0 / input row, child 1),
-// loaded two stages ahead into one of three LDS slots.
-template <int BK>
-struct WgIndex {
-  int (*slots)[3][BK];
-  const int* op_rows;
-  const int* op_cpos;
-  const int* op_inp;
-  int lo, hi, seg;
-  int rp, r0, r1, ok;
-  __device__ __forceinline__ void load(int c) {
-    const int t = threadIdx.x % BK;  // every thread loads (no branch around the loads); BK of them store
-    const int r = lo + c * BK + t;
-    ok = r < hi;
-    const int rc = ok ? r : lo;
-    rp = op_rows[rc];
-    if (seg) {
-      r0 = op_cpos[2 * rc];
-      r1 = op_cpos[2 * rc + 1];
-    } else {
-      r0 = op_inp[rc];
-      r1 = -1;
-    }
-  }
-  __device__ __forceinline__ void store(int c) {
-    const int t = threadIdx.x;
-    if (t < BK) {
-      slots[c % 3][0][t] = ok ? rp : -1;
-      slots[c % 3][1][t] = ok ? r0 : -1;
-      slots[c % 3][2][t] = ok ? r1 : -1;
-    }
-  }
-  __device__ __forceinline__ void prologue(int nst) {
-    for (int c = 0; c < 2 && c < nst; ++c) {
-      load(c);
-      store(c);
-    }
-    __syncthreads();
-  }
-};
-
-// X^T operand: gathered children's h rows (seg 1) or leaf-table rows (seg 0)
-template <typename T, int BK, int VROW>
-struct WgX {
-  using raw = Raw4;
-  const T* src;
-  int sld, width, HP, Kw, m0, seg;
-  int (*slots)[3][BK];
-  __device__ __forceinline__ raw fetch(int c, int i) const {
-    constexpr int VEC = Mma<T>::VEC;
-    const int kk = i / VROW, v = i - kk * VROW;
-    const int m = m0 + v * VEC;
-    const int k = seg ? min(m / HP, 1) : 0;
-    const int jin = seg ? m - k * HP : m;
-    const int s = slots[c % 3][1 + k][kk];
-    const int nv = (s >= 0 && m < Kw) ? min(max(width - jin, 0), VEC) : 0;
-    const size_t off = nv > 0 ? (size_t)s * sld + jin : 0;
-    return {*reinterpret_cast<const uint4*>(src + off), nv};
-  }
-  __device__ __forceinline__ uint4 put(const raw& r) const { return finish<T>(r); }
-};
-
-// dz^T operand; the fp32 values also feed the bias column sums
-template <typename T, int BK, int VROW>
-struct WgDz;
-
-template <int BK, int VROW>
-struct WgDz<float, BK, VROW> {
-  using raw = Raw4;
-  const float* dz;
-  int gstride, Nw, n0;
-  int (*slots)[3][BK];
-  bool bias;
-  float bsum[4];
-  __device__ __forceinline__ raw fetch(int c, int i) const {
-    const int kk = i / VROW, v = i - kk * VROW;
-    const int p = slots[c % 3][0][kk];
-    const int n = n0 + v * 4;
-    const int ok = p >= 0 && n < Nw;
-    return {*reinterpret_cast<const uint4*>(dz + (ok ? (size_t)p * gstride + n : 0)), ok ? 4 : 0};
-  }
-  __device__ __forceinline__ uint4 put(const raw& r) {
-    const uint4 x = finish<float>(r);
-    if (bias) {
-      bsum[0] += __uint_as_float(x.x);
-      bsum[1] += __uint_as_float(x.y);
-      bsum[2] += __uint_as_float(x.z);
-      bsum[3] += __uint_as_float(x.w);
-    }
-    return x;
-  }
-};
-
-template <int BK, int VROW>
-struct WgDz<uint16_t, BK, VROW> {
-  using raw = Raw8;
-  const float* dz;
-  int gstride, Nw, n0;
-  int (*slots)[3][BK];
-  bool bias;
-  float bsum[8];
-  __device__ __forceinline__ raw fetch(int c, int i) const {
-    const int kk = i / VROW, v = i - kk * VROW;
-    const int p = slots[c % 3][0][kk];
-    const int n = n0 + v * 8;
-    const int ok = p >= 0 && n < Nw;
-    const float* q = dz + (ok ? (size_t)p * gstride + n : 0);
-    return {reinterpret_cast<const uint4*>(q)[0], reinterpret_cast<const uint4*>(q)[1], ok ? 8 : 0};
-  }
-  __device__ __forceinline__ uint4 put(const raw& r) {
-    if (bias && r.nv > 0) {
-      const uint32_t in[8] = {r.x0.x, r.x0.y, r.x0.z, r.x0.w, r.x1.x, r.x1.y, r.x1.z, r.x1.w};
-#pragma unroll
-      for (int q = 0; q < 8; ++q) bsum[q] += __uint_as_float(in[q]);
-    }
-    return finish_bf16(r);
-  }
-};
-
-template <typename T>
-__global__ __launch_bounds__(kThreads) void k_wgrad(WgArgs a) {
-  using M = Mma<T>;
-  constexpr int BK = M::BK, VEC = M::VEC;
-  constexpr int LAY = sizeof(T) == 4 ? kKR : kRKT;
-  using TA = Tile<T, kTM, LAY>;  // X^T: weight rows x pool rows
-  using TB = Tile<T, kTN, LAY>;  // dz^T: gate columns x pool rows
-  __shared__ __attribute__((aligned(16))) T As[TA::ELEMS];
-  __shared__ __attribute__((aligned(16))) T Bs[TB::ELEMS];
-  __shared__ int slots[3][3][BK];
-  __shared__ float red[256 / TB::VROW][kTN];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
-  // all tiles of one row chunk read the same X and dz rows: keep them on one XCD
-  const int NT = (a.Nw + kTN - 1) / kTN, MTm = (a.Kw + kTM - 1) / kTM;
-  int tx, chunk_id;
-  if (!xcd_tile(MTm * NT, a.nchunk, tx, chunk_id)) return;
-  const int mt_ = tx % MTm;
-  const int m0 = mt_ * kTM, n0 = (tx / MTm) * kTN;
-  const int lo = chunk_id * a.chunk, hi = min(a.count, lo + a.chunk);
-  const bool do_bias = a.bpart != nullptr && mt_ == 0;
-
-  WgIndex<BK> ix{slots, a.op_rows, a.op_cpos, a.op_inp, lo, hi, a.seg, 0, 0, 0, 0};
-  WgX<T, BK, TA::VROW> la{static_cast<const T*>(a.src), a.seg ? a.ld : a.tld, a.seg ? a.H : a.in_dim, a.HP,
-                          a.Kw, m0, a.seg, slots};
-  WgDz<T, BK, TB::VROW> lb{a.dz, a.gstride, a.Nw, n0, slots, do_bias, {}};
-#pragma unroll
-  for (int q = 0; q < VEC; ++q) lb.bsum[q] = 0.f;
-  f32x16 acc[2][4];
-  zero_acc(acc);
-  const int nst = (hi - lo + BK - 1) / BK;
-  mainloop<T, TA, TB, 2, 4>(nst, la, lb, ix, As, Bs, acc, wm * 64, wn * 128);
-
-  float* out = a.partial + (size_t)chunk_id * a.Kw * a.Nw;
-#pragma unroll
-  for (int tm = 0; tm < 2; ++tm)
-#pragma unroll
-    for (int tn = 0; tn < 4; ++tn) {
-      const int n = n0 + wn * 128 + tn * 32 + (lane & 31);
-      if (n >= a.Nw) continue;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * 64 + tm * 32 + acc_row(r, lane);
-        if (m < a.Kw) out[(size_t)m * a.Nw + n] = acc[tm][tn][r];
-      }
-    }
-  if (do_bias) {
-    // every thread's dz vectors share one column group (TB::VROW divides the block), so the column
-    // sums finish with a fixed-order reduction over the threads of that group
-    const int v = tid % TB::VROW, j = tid / TB::VROW;
-#pragma unroll
-    for (int q = 0; q < VEC; ++q) red[j][v * VEC + q] = lb.bsum[q];
-    __syncthreads();
-    for (int col = tid; col < kTN; col += kThreads) {
-      float s = 0.f;
-      for (int jj = 0; jj < 256 / TB::VROW; ++jj) s += red[jj][col];
-      if (n0 + col < a.Nw) a.bpart[(size_t)chunk_id * a.Nw + n0 + col] = s;
-    }
-  }
-}
 
 // ---------------------------------------------------------------- fp32: direct loads into LDS
 // A stage is 32 op rows.  X^T tile: the 32 rows x 128 weight rows (512 bytes a row), dz^T tile: the 32
@@ -383,6 +202,162 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_f32(WgArgs a) {
     a.bpart[((size_t)(chunk_id * MTm + mt_) * (256 / NW) + bg) * a.Nw + n0 + bc] = bsum;
 }
 
+// ---------------------------------------------------------------- bf16: direct loads + transposing reads
+// A stage is 64 op rows.  X^T tile: 64 rows x 128 weight rows (256 bytes a row), dz^T tile: 64 rows x
+// 128 gate columns of bf16 dz.  The bf16 MFMA operand is, per lane, eight consecutive op rows of one
+// column; ds_read_b64_tr_b16 delivers them from the row-major tile: each group of 16 lanes addresses a
+// block of 4 rows x 16 columns (lane i: row i / 4, columns 4 (i % 4) .. + 3) and lane i receives the 4
+// values of column i.  Row m's 16-byte units are permuted by ^ 4 (m & 3), so the 4 rows of a block
+// fall into different 64-byte bank ranges.
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_t;
+#define FOLD_LDS_AS __attribute__((address_space(3)))
+
+__device__ __forceinline__ int wg16_off(int m, int col) {
+  return m * 256 + (((col >> 3) ^ (4 * (m & 3))) << 4) + (col & 7) * 2;
+}
+
+__device__ __forceinline__ uint2 ld_tr16(const char* lds, int off) {
+  const bf16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((FOLD_LDS_AS bf16x4_t*)(lds + off));
+  return __builtin_bit_cast(uint2, v);
+}
+
+__global__ __launch_bounds__(kThreads) void k_wgrad_bf16(WgArgs a) {
+  constexpr int NW = 128, TM = 2, TN = 2, BYTES = 64 * 256, PA = BYTES / 4096, PB = BYTES / 4096;
+  __shared__ __attribute__((aligned(16))) char A0[BYTES], A1[BYTES], B0[BYTES], B1[BYTES];
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  const int wm = wave & 1, wn = wave >> 1;
+  const int NT = (a.Nw + NW - 1) / NW, MTm = (a.Kw + kTM - 1) / kTM;
+  int tx, chunk_id;
+  if (!xcd_tile(MTm * NT, a.nchunk, tx, chunk_id)) return;
+  const int mt_ = tx % MTm, nt = tx / MTm;
+  const int m0 = mt_ * kTM, n0 = nt * NW;
+  const int lo = chunk_id * a.chunk, hi = min(a.count, lo + a.chunk);
+  const int nst = (hi - lo + 63) / 64;
+  const char* zero = static_cast<const char*>(a.zero);
+  const char* xbase = static_cast<const char*>(a.src);
+  const size_t xstride = (size_t)(a.seg ? a.ld : a.tld) * 2, dstride = (size_t)a.gstride * 4;
+
+  // per instruction: the op row inside the stage (4 t + lane / 16) and this lane's byte column
+  const int msub = lane >> 4, u = (lane & 15) ^ (4 * (msub & 3));
+  const int kw = m0 + 8 * u, nw = n0 + 8 * u;
+  const int achild = a.seg ? min(kw / a.HP, 1) : 0;
+  const int acol = (a.seg ? kw - achild * a.HP : kw) * 2, bcol = nw * 2;
+  const bool aok = kw < a.Kw, bok = nw < a.Nw;
+  struct Idx {
+    int a[PA], b[PB];
+    bool va[PA], vb[PB];
+  };
+  auto load_idx = [&](int c, Idx& x) {
+#pragma unroll
+    for (int i = 0; i < PA; ++i) {
+      const int r = lo + c * 64 + 4 * (wave * PA + i) + msub;
+      const int rc = min(r, hi - 1);
+      x.a[i] = a.seg ? a.op_cpos[2 * rc + achild] : a.op_inp[rc];
+      x.va[i] = r < hi && aok;
+      x.b[i] = a.op_rows[rc];
+      x.vb[i] = r < hi && bok;
+    }
+  };
+  auto issue = [&](const Idx& x, char* Ad, char* Bd) {
+#pragma unroll
+    for (int i = 0; i < PA; ++i)
+      dma16(x.va[i] && x.a[i] >= 0 ? xbase + (size_t)x.a[i] * xstride + acol : zero, Ad + (wave * PA + i) * 1024);
+#pragma unroll
+    for (int i = 0; i < PB; ++i)
+      dma16(x.vb[i] ? reinterpret_cast<const char*>(a.dz) + (size_t)x.b[i] * dstride + bcol : zero,
+            Bd + (wave * PB + i) * 1024);
+  };
+  // transposing-read offsets: group g = lane / 16 serves rows (g & 1) * 16 .. + 15 of its 32-row
+  // fragment and K half g >> 1; lane i of the group addresses row i / 4, columns 4 (i % 4) .. + 3
+  const int g = lane >> 4, gi = lane & 15;
+  int aoff[TM], boff[TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) aoff[tm] = wm * 64 + tm * 32 + 16 * (g & 1) + 4 * (gi & 3);
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) boff[tn] = wn * 64 + tn * 32 + 16 * (g & 1) + 4 * (gi & 3);
+  const int mrow = 8 * (g >> 1) + (gi >> 2);  // + 16 s + 4 j
+  // bias column sums: thread tid sums column tid % 128 over the stage rows r with r % MTm == mt_ and
+  // (r / MTm) % 2 == tid / 128
+  const bool do_bias = a.bpart != nullptr;
+  const int bc = tid & 127, bg = tid >> 7;
+  float bsum = 0.f;
+
+  f32x16 acc[TM][TN];
+  zero_acc(acc);
+  auto stage = [&](const char* As, const char* Bs) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      uint4 af[TM], bf[TN];
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) {
+        const uint2 lo2 = ld_tr16(As, wg16_off(16 * s + mrow, aoff[tm]));
+        const uint2 hi2 = ld_tr16(As, wg16_off(16 * s + mrow + 4, aoff[tm]));
+        af[tm] = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
+      }
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const uint2 lo2 = ld_tr16(Bs, wg16_off(16 * s + mrow, boff[tn]));
+        const uint2 hi2 = ld_tr16(Bs, wg16_off(16 * s + mrow + 4, boff[tn]));
+        bf[tn] = make_uint4(lo2.x, lo2.y, hi2.x, hi2.y);
+      }
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+          acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[tm]),
+                                                               __builtin_bit_cast(bf16x8, bf[tn]), acc[tm][tn], 0,
+                                                               0, 0);
+    }
+    if (do_bias) {
+      for (int r = mt_ + MTm * bg; r < 64; r += 2 * MTm)
+        bsum += bf2f(*reinterpret_cast<const uint16_t*>(Bs + wg16_off(r, bc)));
+    }
+  };
+
+  if (nst > 0) {
+    Idx iC, iN;
+    load_idx(0, iC);
+    vm_wait();
+    issue(iC, A0, B0);
+    if (nst > 1) load_idx(1, iN);
+    vm_wait();
+    __syncthreads();
+    int c = 0;
+    for (; c + 2 <= nst; c += 2) {
+      issue(iN, A1, B1);
+      if (c + 2 < nst) load_idx(c + 2, iC);
+      __builtin_amdgcn_sched_barrier(0);
+      stage(A0, B0);
+      vm_wait();
+      __syncthreads();
+      if (c + 2 < nst) {
+        issue(iC, A0, B0);
+        if (c + 3 < nst) load_idx(c + 3, iN);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      stage(A1, B1);
+      vm_wait();
+      __syncthreads();
+    }
+    if (c < nst) stage(A0, B0);
+  }
+
+  float* out = a.partial + (size_t)chunk_id * a.Kw * a.Nw;
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int n = n0 + wn * 64 + tn * 32 + (lane & 31);
+      if (n >= a.Nw) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 64 + tm * 32 + acc_row(r, lane);
+        if (m < a.Kw) out[(size_t)m * a.Nw + n] = acc[tm][tn][r];
+      }
+    }
+  if (do_bias && n0 + bc < a.Nw) a.bpart[((size_t)(chunk_id * MTm + mt_) * 2 + bg) * a.Nw + n0 + bc] = bsum;
+}
+
 // dW[row, col] += sum over chunks of partial[chunk, m, n], (m, n) in the padded layout
 __global__ void k_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP,
                                int in_dim, int G, float* dW) {
@@ -407,14 +382,18 @@ __global__ void k_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw,
   }
 }
 
+// column sums of dz (fp32, or bf16 at the start of each row) over one chunk of an op's rows
 __global__ void k_bias_partial(const int* op_rows, int count, int chunk, const float* dz, int gstride, int Nw,
-                               float* bpart) {
+                               int bf, float* bpart) {
   const int c = blockIdx.x;
   const int n = blockIdx.y * blockDim.x + threadIdx.x;
   if (n >= Nw) return;
   const int lo = c * chunk, hi = min(count, lo + chunk);
   float s = 0.f;
-  for (int i = lo; i < hi; ++i) s += dz[(size_t)op_rows[i] * gstride + n];
+  for (int i = lo; i < hi; ++i) {
+    const float* row = dz + (size_t)op_rows[i] * gstride;
+    s += bf ? bf2f(reinterpret_cast<const uint16_t*>(row)[n]) : row[n];
+  }
   bpart[(size_t)c * Nw + n] = s;
 }
 
@@ -440,7 +419,7 @@ __global__ void k_bias_reduce(const float* bpart, int nparts, int Nw, int H, int
 WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype) {
   WgradSplit w;
   if (count <= 0 || Kw <= 0 || Nw <= 0) return w;
-  const int tn = dtype == FOLD_BF16 ? kTN : kWgNW;
+  const int tn = dtype == FOLD_BF16 ? 128 : kWgNW;
   const long long tiles = (long long)((Kw + kTM - 1) / kTM) * ((Nw + tn - 1) / tn);
   // enough workgroups to fill the chip, and chunks in multiples of the 8 XCDs (one XCD per chunk)
   const long long want = std::max(8LL, ((1024 + tiles - 1) / tiles + 7) / 8 * 8);
@@ -448,8 +427,8 @@ WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype) {
   w.nchunk = (int)std::max(1LL, std::min(want, most));
   w.chunk = round_up((count + w.nchunk - 1) / w.nchunk, 64);
   w.nchunk = (count + w.chunk - 1) / w.chunk;
-  // bias partial rows: one per chunk (bf16), one per (chunk, weight-row tile, thread group) (fp32)
-  w.bparts = dtype == FOLD_BF16 ? w.nchunk : w.nchunk * ((Kw + kTM - 1) / kTM) * (256 / kWgNW);
+  // bias partial rows: one per (chunk, weight-row tile, thread group)
+  w.bparts = w.nchunk * ((Kw + kTM - 1) / kTM) * (dtype == FOLD_BF16 ? 2 : 256 / kWgNW);
   return w;
 }
 
@@ -457,8 +436,8 @@ void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st) {
   if (a.count <= 0) return;
   ProfScope prof(dtype == FOLD_BF16 ? "wgrad.bf16" : "wgrad.f32", st);
   if (dtype == FOLD_BF16) {
-    dim3 grid(xcd_grid(((a.Kw + kTM - 1) / kTM) * ((a.Nw + kTN - 1) / kTN), a.nchunk));
-    hipLaunchKernelGGL(k_wgrad<uint16_t>, grid, dim3(kThreads), 0, st, a);
+    dim3 grid(xcd_grid(((a.Kw + kTM - 1) / kTM) * ((a.Nw + 127) / 128), a.nchunk));
+    hipLaunchKernelGGL(k_wgrad_bf16, grid, dim3(kThreads), 0, st, a);
   } else {
     dim3 grid(xcd_grid(((a.Kw + kTM - 1) / kTM) * ((a.Nw + kWgNW - 1) / kWgNW), a.nchunk));
     hipLaunchKernelGGL(k_wgrad_f32<kWgNW>, grid, dim3(kThreads), 0, st, a);
@@ -475,11 +454,11 @@ void launch_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int s
 }
 
 void launch_bias_partial(const int* op_rows, int count, int chunk, int nchunk, const float* dz, int gstride, int Nw,
-                         float* bpart, hipStream_t st) {
+                         int bf, float* bpart, hipStream_t st) {
   if (count <= 0) return;
   ProfScope prof("bias_partial", st);
   hipLaunchKernelGGL(k_bias_partial, dim3(nchunk, (Nw + 255) / 256), dim3(256), 0, st, op_rows, count, chunk, dz,
-                     gstride, Nw, bpart);
+                     gstride, Nw, bf, bpart);
 }
 
 void launch_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, float* dbias, hipStream_t st) {
