@@ -9,15 +9,24 @@ Inputs are synthetic and seeded, and resident in HBM before the timed region.
 
 Prints ONE JSON line: nodes/s over the timed steps, the roofline of the dominant
 kernel (algorithmic FLOPs per launch / average launch time, live HIP events), the
-schedule time, and the CPU oracle timed on a bounded sample on this host.
+schedule time, and the CPU oracle timed on a bounded sample on this host.  A step is
+one replay of the whole forward + backward recorded as a HIP graph (gradients zeroed
+inside it); the same step issued call by call is timed beside it.
 
     python bench.py [--steps K] [--warmup W] [--config 1..5] [--no-cpu]
+    python bench.py --traffic-from FETCH.csv WRITE.csv [--traffic-kernel CLASS]
+        turns two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this bench into the
+        HBM-traffic record that profiles/ keeps for the dominant kernel class
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
+import re
 import statistics
 import sys
 import time
@@ -30,6 +39,96 @@ PEAKS = {  # MI355X datasheet, dense
     "bf16_mfma_tflops": 2500.0,
     "hbm_gbs": 8000.0,
 }
+
+
+# Sources whose code decides a kernel class's kernels: a traffic record is valid only while they are
+# unchanged.
+CLASS_SOURCES = {
+    "cell_fwd": ("cells.hip", "dma.h", "mfma.h", "common.h", "internal.h"),
+    "bwd_dx": ("cells.hip", "dma.h", "mfma.h", "common.h", "internal.h"),
+    "wgrad": ("wgrad.hip", "dma.h", "mfma.h", "common.h", "internal.h"),
+}
+COPY_KERNEL = "k_probe_copy"
+TRAFFIC_TAG = "traffic-record:"
+KIND_IDS = {"embed": 0, "treernn": 1, "treelstm": 2, "lstm": 3, "proj": 4}
+CTYPE = {"f32": "float", "bf16": "unsigned short"}
+
+
+def class_of(name: str) -> str:
+    return name.split(".")[0]
+
+
+def rocprof_role(kernel_class: str, name: str):
+    """Role of a rocprofv3 kernel name in one launch of a library kernel class ("cell_fwd.treelstm.f32",
+    "bwd_dx.bf16", "wgrad.f32"): "main" (exactly one dispatch per launch of the class), "extra" (the
+    K-split epilogue or reduction that belongs to it) or None."""
+    parts = kernel_class.split(".")
+    cls, dt = parts[0], CTYPE[parts[-1]]
+    if cls == "cell_fwd":
+        kind = KIND_IDS[parts[1]]
+        if re.search(rf"k_cell_fwd<{dt}, {kind}, ", name):
+            return "main"
+        if re.search(rf"k_cell_epi<{dt}, {kind}>", name):
+            return "extra"
+    elif cls == "bwd_dx":
+        if re.search(rf"k_bwd_dx2<{dt}, ", name):
+            return "main"
+        if "k_dx_epi" in name:
+            return "extra"
+    elif cls == "wgrad":
+        if re.search(r"k_wgrad_(f32|bf16)\b|k_wgrad<", name):
+            return "main"
+    return None
+
+
+def sources_sha256(cls: str) -> str:
+    h = hashlib.sha256()
+    for f in CLASS_SOURCES[cls]:
+        with open(os.path.join(ROOT, "paper_1702_02181_amd", "csrc", f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def traffic_record(kernel: str, workload: str):
+    """The HBM-traffic record of `kernel` on `workload` kept under profiles/, if the kernel's sources are
+    unchanged since the counters were taken; else None."""
+    want = sources_sha256(class_of(kernel))
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        for line in open(path):
+            if TRAFFIC_TAG not in line:
+                continue
+            rec = json.loads(line.split(TRAFFIC_TAG, 1)[1].strip().strip("`").strip())
+            if rec.get("kernel") == kernel and rec.get("workload") == workload and rec.get("sources_sha256") == want:
+                return rec
+    return None
+
+
+def traffic_from_counters(fetch_csv: str, write_csv: str, kernel: str, workload: str) -> dict:
+    """HBM bytes per launch of a kernel class from a FETCH_SIZE run and a WRITE_SIZE run (rocprofv3 csv,
+    KiB per dispatch), each scaled by what the same counter reads for the copy probe, which reads and
+    writes PROBE_BYTES per dispatch.  Launches are counted by the class's main kernel."""
+    cls = class_of(kernel)
+    out = {"kernel": kernel, "workload": workload}
+    for what, path in (("fetch", fetch_csv), ("write", write_csv)):
+        copy, kib, launches = [], 0.0, 0
+        for r in csv.DictReader(open(path)):
+            name, v = r["Kernel_Name"], float(r["Counter_Value"])
+            if COPY_KERNEL in name:
+                copy.append(v)
+            role = rocprof_role(kernel, name)
+            if role:
+                kib += v
+                launches += role == "main"
+        factor = (PROBE_BYTES / 1024.0) / statistics.median(copy)
+        out[f"{what}_factor"] = round(factor, 4)
+        out[f"{what}_launches"] = launches
+        out[f"{what}_bytes_per_launch"] = round(kib * 1024.0 * factor / launches)
+    out["bytes_per_launch"] = out["fetch_bytes_per_launch"] + out["write_bytes_per_launch"]
+    out["sources_sha256"] = sources_sha256(cls)
+    return out
+
+
+PROBE_BYTES = 1 << 30
 
 
 def flops_by_kernel(w, sched_host, table_grad: bool) -> dict:
@@ -97,7 +196,15 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--profile-only", action="store_true", help="skip the oracle leg and the schedule timing")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--traffic-kernel", default=None)
     args = ap.parse_args()
+    if args.traffic_from:
+        from paper_1702_02181_amd import gen as _gen
+        w = _gen.make_config(args.config)
+        rec = traffic_from_counters(args.traffic_from[0], args.traffic_from[1], args.traffic_kernel, w.name)
+        print(TRAFFIC_TAG, json.dumps(rec))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the dynamic-batching path here is a single-GPU build "
               "(graphs would shard across GPUs with one all-reduce of weight gradients; not built).",
@@ -115,9 +222,10 @@ def main():
     # achievable peaks on this GPU (MFMA loop, stream copy), next to the datasheet figures
     probes = {}
     try:
+        # the copy probe doubles as the calibration kernel of the HBM byte counters (PROBE_BYTES a dispatch)
         probes["mfma_f32_tflops"] = round(F.fold_probe_mfma(F.FOLD_F32), 1)
         probes["mfma_bf16_tflops"] = round(F.fold_probe_mfma(F.FOLD_BF16), 1)
-        nbytes = 1 << 30
+        nbytes = PROBE_BYTES
         src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         probes["copy_gbs"] = round(F.fold_probe_copy(dst, src, nbytes), 1)
@@ -158,18 +266,27 @@ def main():
 
     print(f"[bench] N={N} levels={dev.sched.num_levels} groups={len(host['group_op'])} warmup={args.warmup}",
           file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = e0.elapsed_time(e1) / args.steps
-    print(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step", file=sys.stderr, flush=True)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    # the step as issued call by call, then recorded once as a HIP graph and replayed
+    eager_ms = timed(step)
+    graph = dev.make_graph(backward=w.backward, zero_grads=True)
+    graph_ms = timed(graph.launch)
+    ms_per_step = graph_ms
+    print(f"[bench] timed {args.steps} steps: graph {graph_ms:.3f} ms/step, eager {eager_ms:.3f} ms/step "
+          f"({graph.num_nodes} graph nodes)", file=sys.stderr, flush=True)
 
     # per-kernel durations over a second timed region (event pair around every launch)
     F.fold_profile_enable(True)
@@ -195,9 +312,13 @@ def main():
         avg_s = (stats[dom][1] / args.steps) / launches * 1e-3
         per_launch = flops[dom] / launches
         ach = per_launch / avg_s / 1e12
+        rec = traffic_record(dom, w.name)
         roofline = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
-                    "frac": round(ach / peak, 4), "traffic": None,
-                    "flops_per_launch": per_launch, "avg_launch_us": round(avg_s * 1e6, 2)}
+                    "frac": round(ach / peak, 4), "traffic": None if rec is None else rec["bytes_per_launch"],
+                    "traffic_unit": "bytes per launch (HBM read + write, rocprofv3 FETCH_SIZE / WRITE_SIZE "
+                                    "scaled by the copy probe)",
+                    "flops_per_launch": per_launch, "launches_per_step": launches,
+                    "avg_launch_us": round(avg_s * 1e6, 2)}
     total_flops = sum(flops.values())
     step_peak = PEAKS["bf16_mfma_tflops"] if w.dtype == "bf16" else PEAKS["f32_mfma_tflops"]
 
@@ -215,6 +336,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "eager_ms_per_step": round(eager_ms, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -223,6 +345,7 @@ def main():
         "config": {"workload": w.name, "graphs": w.num_graphs, "nodes": N, "levels": dev.sched.num_levels,
                    "hidden": w.hidden, "pass": "forward+backward" if w.backward else "forward"},
         "schedule_ms": None if schedule_ms is None else round(schedule_ms, 3),
+        "graph_nodes": graph.num_nodes,
         "peaks": {"datasheet": PEAKS, "measured": probes},
         "roofline": roofline,
         "step_mfma_frac": round(total_flops / (ms_per_step * 1e-3) / 1e12 / step_peak, 4),

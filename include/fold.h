@@ -240,6 +240,58 @@ int32_t fold_backward(const fold_sched* sched, const fold_packed* packed,
                       const fold_grads* grads, float* dh_out, float* dc_out,
                       void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- a whole step as one HIP graph ----------------------------------------
+ * The level loop (Section 2: one batched iteration per depth, so a batch of
+ * depth D costs O(D) launches instead of one per node) still issues a few
+ * launches per (depth, operation) group.  For deep batches of narrow levels
+ * the host launch cost and the gaps between dependent launches dominate.
+ * fold_graph_create records, once, exactly the launches that fold_forward
+ * (and, with FOLD_STEP_BACKWARD, fold_backward) would enqueue with the
+ * buffers below, and instantiates them as a HIP graph; fold_graph_launch
+ * submits that step on any stream with one call.
+ *   - The buffers are bound at creation: every launch reads and writes the
+ *     same device memory (contents may change between launches, addresses
+ *     may not).  Recreate the graph to use other buffers.
+ *   - With FOLD_STEP_ZERO_GRADS the step first zeroes every gradient tensor
+ *     in `grads` (dW_in, dW_rec, dbias of each set, d_leaf_table of
+ *     leaf_rows rows), so a launch yields the gradients of this step alone;
+ *     without it they accumulate across launches as with fold_backward.
+ *   - The recorded step holds kernel nodes only (no memset or copy nodes),
+ *     allocates nothing and never synchronises when launched.
+ *   - Launches of one graph must not overlap (they share the buffers): keep
+ *     them on one stream or order them with events.
+ * fold_graph_create synchronises nothing but returns only after
+ * instantiation; it fails with the same codes as fold_forward /
+ * fold_backward for inconsistent arguments, FOLD_E_DEVICE if capture or
+ * instantiation fails, and leaves *out NULL on error.  The graph must be
+ * launched on the device that was current at creation (FOLD_E_MISMATCH
+ * otherwise).  The schedule and parameter handles must outlive the graph. */
+typedef struct fold_graph fold_graph;
+
+typedef struct {
+  const void* leaf_table; /* as fold_forward */
+  int64_t leaf_rows;
+  void* h_pool;
+  float* c_pool;
+  void* roots_out;        /* or NULL */
+  const float* dh_roots;  /* as fold_backward (used with FOLD_STEP_BACKWARD) */
+  const float* dh_nodes;
+  const fold_grads* grads; /* read at creation; the host arrays may be freed afterwards */
+  float* dh_out;
+  float* dc_out;
+  void* ws;               /* >= fwd_bytes (forward only) or bwd_bytes */
+  size_t ws_bytes;
+} fold_step_buffers;
+
+#define FOLD_STEP_BACKWARD 1   /* record fold_backward after fold_forward */
+#define FOLD_STEP_ZERO_GRADS 2 /* zero the gradients first (needs FOLD_STEP_BACKWARD) */
+
+int32_t fold_graph_create(const fold_sched* sched, const fold_packed* packed, const fold_step_buffers* buffers,
+                          int32_t flags, fold_graph** out);
+int32_t fold_graph_launch(const fold_graph* graph, hipStream_t stream);
+int32_t fold_graph_num_nodes(const fold_graph* graph, int32_t* nodes); /* kernel nodes recorded */
+int32_t fold_graph_free(fold_graph* graph);
+
 /* ---- per-kernel timing (profiling aid) ----------------------------------
  * While enabled, every kernel the library launches is bracketed by a pair of
  * HIP events recorded on the launch stream, under a short kernel-class name

@@ -49,8 +49,14 @@ hipEvent_t prof_event() {
 }
 }  // namespace
 
+namespace {
+thread_local bool g_capturing = false;  // launches are being recorded into a graph: no event pairs
+}
+
+void set_capturing(bool on) { g_capturing = on; }
+
 ProfScope::ProfScope(const char* name, hipStream_t st) : name_(name), st_(st) {
-  if (!g_prof_on.load(std::memory_order_relaxed)) return;
+  if (!g_prof_on.load(std::memory_order_relaxed) || g_capturing) return;
   hipEvent_t a = prof_event(), b = prof_event();
   if (!a || !b) return;
   start_ = a;
@@ -132,6 +138,29 @@ int check_compat(const Sched& s, const Packed& p) {
 }
 
 }  // namespace
+
+int check_forward_args(const Sched& s, const Packed& p, const void* table, int64_t table_rows,
+                       const void* h_pool, const void* c_pool, const char* who) {
+  int rc = check_compat(s, p);
+  if (rc != FOLD_OK) return rc;
+  const std::string w(who);
+  if (s.N > 0 && (!h_pool || !c_pool)) return fail(FOLD_E_INVALID, w + ": NULL pool");
+  if (table_width(s, p) > 0 && s.N > 0) {
+    if (!table) return fail(FOLD_E_INVALID, w + ": leaf table is NULL");
+    if (table_rows < s.num_inputs) return fail(FOLD_E_MISMATCH, w + ": leaf table has fewer rows than the batch names");
+  }
+  return FOLD_OK;
+}
+
+int check_grads(const Packed& p, const fold_grads* grads, const char* who) {
+  const std::string w(who);
+  if (grads && grads->num_sets != (int)p.sets.size())
+    return fail(FOLD_E_MISMATCH, w + ": gradient sets differ from parameter sets");
+  if (grads && grads->num_sets > 0 && !grads->sets) return fail(FOLD_E_INVALID, w + ": NULL gradient sets");
+  return FOLD_OK;
+}
+
+int leaf_table_width(const Sched& s, const Packed& p) { return table_width(s, p); }
 
 WsLayout workspace_layout(const Sched& s, const Packed& p) {
   WsLayout w;
@@ -641,13 +670,8 @@ int32_t fold_forward(const fold_sched* sh, const fold_packed* ph, const void* ta
   if (!sh || !ph) return fail(FOLD_E_INVALID, "fold_forward: NULL handle");
   const Sched& s = sh->s;
   const Packed& p = ph->p;
-  int rc = check_compat(s, p);
+  int rc = check_forward_args(s, p, table, table_rows, h_pool, c_pool, "fold_forward");
   if (rc != FOLD_OK) return rc;
-  if (s.N > 0 && (!h_pool || !c_pool)) return fail(FOLD_E_INVALID, "fold_forward: NULL pool");
-  if (table_width(s, p) > 0 && s.N > 0) {
-    if (!table) return fail(FOLD_E_INVALID, "fold_forward: leaf table is NULL");
-    if (table_rows < s.num_inputs) return fail(FOLD_E_MISMATCH, "fold_forward: leaf table has fewer rows than the batch names");
-  }
   return forward_impl(s, p, table, table_rows, h_pool, c_pool, roots_out, ws, ws_bytes, st);
   FOLD_GUARD_END
 }
@@ -661,16 +685,10 @@ int32_t fold_backward(const fold_sched* sh, const fold_packed* ph, const void* t
   if (!sh || !ph) return fail(FOLD_E_INVALID, "fold_backward: NULL handle");
   const Sched& s = sh->s;
   const Packed& p = ph->p;
-  int rc = check_compat(s, p);
+  int rc = check_forward_args(s, p, table, table_rows, h_pool, c_pool, "fold_backward");
   if (rc != FOLD_OK) return rc;
-  if (s.N > 0 && (!h_pool || !c_pool)) return fail(FOLD_E_INVALID, "fold_backward: NULL pool");
-  if (grads && grads->num_sets != (int)p.sets.size())
-    return fail(FOLD_E_MISMATCH, "fold_backward: gradient sets differ from parameter sets");
-  if (grads && grads->num_sets > 0 && !grads->sets) return fail(FOLD_E_INVALID, "fold_backward: NULL gradient sets");
-  if (table_width(s, p) > 0 && s.N > 0) {
-    if (!table) return fail(FOLD_E_INVALID, "fold_backward: leaf table is NULL");
-    if (table_rows < s.num_inputs) return fail(FOLD_E_MISMATCH, "fold_backward: leaf table has fewer rows than the batch names");
-  }
+  rc = check_grads(p, grads, "fold_backward");
+  if (rc != FOLD_OK) return rc;
   return backward_impl(s, p, table, table_rows, h_pool, c_pool, dh_roots, dh_nodes, grads, dh_out, dc_out, ws,
                        ws_bytes, st);
   FOLD_GUARD_END

@@ -305,6 +305,12 @@ __global__ void k_embed_fwd(int rows, int row_begin, int H, int ld, int tld, con
   }
 }
 
+// plain fill kernel (used where a memset node would be recorded into a graph)
+__global__ void k_zero_f32(float* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0.f;
+}
+
 template <typename T>
 __global__ void k_roots(int ld, const int* root_pos, const T* h_pool, T* out) {
   const int r = blockIdx.x;
@@ -590,6 +596,13 @@ void launch_embed_fwd(int dtype, int rows, int row_begin, int H, int ld, int tld
   else
     hipLaunchKernelGGL(k_embed_fwd<float>, dim3(rows), dim3(256), 0, st, rows, row_begin, H, ld, tld,
                        static_cast<const float*>(table), input_idx, static_cast<float*>(h_pool), c_pool);
+}
+
+void launch_zero_f32(float* p, size_t n, hipStream_t st) {
+  if (!p || n == 0) return;
+  ProfScope prof("zero_grads", st);
+  const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 8192);
+  hipLaunchKernelGGL(k_zero_f32, dim3(blocks), dim3(256), 0, st, p, n);
 }
 
 void launch_roots(int dtype, int R, int ld, const int* root_pos, const void* h_pool, void* out, hipStream_t st) {

@@ -33,6 +33,14 @@ struct WgradSplit {
 };
 WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype);
 
+// Argument checks shared by fold_forward, fold_backward and fold_graph_create (set the error text).
+int check_forward_args(const Sched& s, const Packed& p, const void* table, int64_t table_rows,
+                       const void* h_pool, const void* c_pool, const char* who);
+int check_grads(const Packed& p, const fold_grads* grads, const char* who);
+int leaf_table_width(const Sched& s, const Packed& p);
+// While set on this thread, kernel launchers record no profiling events (stream capture in progress).
+void set_capturing(bool on);
+
 int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, void* h_pool,
                      float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st);
 int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows,
@@ -103,6 +111,7 @@ inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
 }
 void launch_embed_fwd(int dtype, int rows, int row_begin, int H, int ld, int tld, const void* table,
                       const int* input_idx, void* h_pool, float* c_pool, hipStream_t st);
+void launch_zero_f32(float* p, size_t n, hipStream_t st);
 void launch_roots(int dtype, int R, int ld, const int* root_pos, const void* h_pool, void* roots_out,
                   hipStream_t st);
 

@@ -8,8 +8,9 @@ binding raises -- there is no fallback.
 The functions keep the ABI's names:
     fold_schedule, fold_sched_get_info, fold_sched_free,
     fold_pack_params, fold_packed_free, fold_workspace_size,
-    fold_forward, fold_backward, fold_row_ld, fold_last_error
-``Batch`` / ``Schedule`` / ``Packed`` / ``Run`` wrap them for tensors.
+    fold_forward, fold_backward, fold_row_ld, fold_last_error,
+    fold_graph_create, fold_graph_launch, fold_graph_num_nodes, fold_graph_free
+``Schedule`` / ``Packed`` / ``StepGraph`` wrap them for tensors.
 """
 from __future__ import annotations
 
@@ -76,6 +77,16 @@ class fold_grads(ctypes.Structure):
     _fields_ = [("num_sets", c_int32), ("sets", POINTER(fold_param_grads)), ("d_leaf_table", c_void_p)]
 
 
+class fold_step_buffers(ctypes.Structure):
+    _fields_ = [("leaf_table", c_void_p), ("leaf_rows", c_int64), ("h_pool", c_void_p), ("c_pool", c_void_p),
+                ("roots_out", c_void_p), ("dh_roots", c_void_p), ("dh_nodes", c_void_p),
+                ("grads", POINTER(fold_grads)), ("dh_out", c_void_p), ("dc_out", c_void_p),
+                ("ws", c_void_p), ("ws_bytes", c_size_t)]
+
+
+FOLD_STEP_BACKWARD, FOLD_STEP_ZERO_GRADS = 1, 2
+
+
 class fold_kernel_stat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 48), ("launches", c_int64), ("total_ms", ctypes.c_double),
                 ("max_ms", ctypes.c_double)]
@@ -90,7 +101,8 @@ class FoldError(RuntimeError):
 EXPORTS = ["fold_schedule", "fold_sched_get_info", "fold_sched_free", "fold_pack_params",
            "fold_packed_free", "fold_row_ld", "fold_workspace_size", "fold_forward",
            "fold_backward", "fold_last_error", "fold_profile_enable", "fold_profile_read",
-           "fold_probe_mfma", "fold_probe_copy"]
+           "fold_probe_mfma", "fold_probe_copy", "fold_graph_create", "fold_graph_launch",
+           "fold_graph_num_nodes", "fold_graph_free"]
 
 _lib = None
 
@@ -126,6 +138,14 @@ def lib():
     L.fold_backward.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,
                                 c_void_p, POINTER(fold_grads), c_void_p, c_void_p, c_void_p, c_size_t,
                                 c_void_p]
+    L.fold_graph_create.restype = c_int32
+    L.fold_graph_create.argtypes = [c_void_p, c_void_p, POINTER(fold_step_buffers), c_int32, POINTER(c_void_p)]
+    L.fold_graph_launch.restype = c_int32
+    L.fold_graph_launch.argtypes = [c_void_p, c_void_p]
+    L.fold_graph_num_nodes.restype = c_int32
+    L.fold_graph_num_nodes.argtypes = [c_void_p, POINTER(c_int32)]
+    L.fold_graph_free.restype = c_int32
+    L.fold_graph_free.argtypes = [c_void_p]
     L.fold_profile_enable.restype = c_int32
     L.fold_profile_enable.argtypes = [c_int32]
     L.fold_profile_read.restype = c_int32
@@ -231,6 +251,26 @@ def fold_backward(sched, packed, leaf_table, leaf_rows, h_pool, c_pool, dh_roots
     _check(lib().fold_backward(sched, packed, _ptr(leaf_table), int(leaf_rows), _ptr(h_pool), _ptr(c_pool),
                                _ptr(dh_roots), _ptr(dh_nodes), None if grads is None else byref(grads),
                                _ptr(dh_out), _ptr(dc_out), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def fold_graph_create(sched, packed, buffers: fold_step_buffers, flags: int) -> c_void_p:
+    h = c_void_p()
+    _check(lib().fold_graph_create(sched, packed, byref(buffers), int(flags), byref(h)))
+    return h
+
+
+def fold_graph_launch(graph, stream=None):
+    _check(lib().fold_graph_launch(graph, _stream(stream)))
+
+
+def fold_graph_num_nodes(graph) -> int:
+    n = c_int32()
+    _check(lib().fold_graph_num_nodes(graph, byref(n)))
+    return int(n.value)
+
+
+def fold_graph_free(graph):
+    _check(lib().fold_graph_free(graph))
 
 
 # ----------------------------------------------------------------------------- tensor wrappers
@@ -347,3 +387,36 @@ def make_grads(sets_tensors, d_leaf_table=None) -> fold_grads:
     g = fold_grads(len(sets_tensors), arr, _ptr(d_leaf_table))
     g._keep = (arr, sets_tensors, d_leaf_table)
     return g
+
+
+class StepGraph:
+    """fold_graph_create over CUDA tensors: one recorded forward (+ backward) step.  Keeps every
+    tensor it was built on alive; frees the graph when collected."""
+
+    def __init__(self, sched, packed, leaf_table, leaf_rows, h_pool, c_pool, roots_out, ws, ws_bytes,
+                 backward=False, dh_roots=None, dh_nodes=None, grads=None, dh_out=None, dc_out=None,
+                 zero_grads=False):
+        self._keep = (sched, packed, leaf_table, h_pool, c_pool, roots_out, ws, dh_roots, dh_nodes, grads,
+                      dh_out, dc_out)
+        b = fold_step_buffers()
+        b.leaf_table, b.leaf_rows = _ptr(leaf_table), int(leaf_rows)
+        b.h_pool, b.c_pool, b.roots_out = _ptr(h_pool), _ptr(c_pool), _ptr(roots_out)
+        b.dh_roots, b.dh_nodes = _ptr(dh_roots), _ptr(dh_nodes)
+        b.grads = None if grads is None else ctypes.pointer(grads)
+        b.dh_out, b.dc_out = _ptr(dh_out), _ptr(dc_out)
+        b.ws, b.ws_bytes = _ptr(ws), int(ws_bytes)
+        flags = (FOLD_STEP_BACKWARD if backward else 0) | (FOLD_STEP_ZERO_GRADS if zero_grads else 0)
+        self.handle = fold_graph_create(sched.handle, packed.handle, b, flags)
+        self.num_nodes = fold_graph_num_nodes(self.handle)
+
+    def launch(self, stream=None):
+        fold_graph_launch(self.handle, stream)
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value:
+            try:
+                fold_graph_free(h)
+            except Exception:
+                pass
+            self.handle = None

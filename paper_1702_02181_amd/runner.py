@@ -116,6 +116,14 @@ class DeviceRun:
                         self.c_pool, self.dh_roots, self.dh_nodes, self.grads, dh_out, dc_out, self.ws,
                         self.ws_bytes, self.stream)
 
+    def make_graph(self, backward=None, zero_grads=True, dh_out=None, dc_out=None):
+        """Record one step (forward, then backward with the gradients zeroed first) as a HIP graph."""
+        backward = self.w.backward if backward is None else backward
+        return F.StepGraph(self.sched, self.packed, self.table, self.leaf_rows, self.h_pool, self.c_pool,
+                           self.roots, self.ws, self.ws_bytes, backward=backward, dh_roots=self.dh_roots,
+                           dh_nodes=self.dh_nodes, grads=self.grads if backward else None, dh_out=dh_out,
+                           dc_out=dc_out, zero_grads=zero_grads and backward)
+
     # ------------------------------------------------------------------ results
     def sched_arrays(self):
         if not hasattr(self, "_sa"):
