@@ -22,6 +22,7 @@
 #include "internal.h"
 #include "dma.h"
 #include "mfma.h"
+#include "wide.h"
 
 namespace fold {
 
@@ -105,6 +106,8 @@ template <typename T, int KIND>
 __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const float* z, float cl, float cr) {
   const size_t p = (size_t)(a.row_begin + row);
   float h, c;
+  // saved activations stay fp32 whatever the parameters' type: the backward multiplies dc by the
+  // forget gates level after level, so their rounding would accumulate along deep chains
   float* gs = a.gates ? a.gates + p * a.gstride + j : nullptr;
   if constexpr (KIND == FOLD_TREELSTM) {
     const float i_ = sigmoidf_(z[0]), fl = sigmoidf_(z[1]), fr = sigmoidf_(z[2]), o = sigmoidf_(z[3]);
@@ -162,11 +165,11 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   __shared__ int srow[3][BM];  // source row of every tile row, per input segment (-1: zero row)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
-  // co-locate on one XCD the workgroups that share the larger operand: the gathered rows of a row
-  // tile (wide levels) or the weight slice of a unit block (narrow levels)
+  // co-locate on one XCD the workgroups that share the larger operand: the gathered rows of a row tile
+  // or the weight slice of a unit block
   const int R = (a.rows + BM - 1) / BM, UB = a.HP / 32;
   int tx, ty, ub, rt, kz;
-  if (a.share_rows) {
+  if (a.map == kMapRows) {
     if (!xcd_tile(UB * a.ksplit, R, tx, ty)) return;
     rt = ty;
     ub = tx % UB;
@@ -266,6 +269,162 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- forward, wide levels
+// 256 rows per workgroup, each wave 64 rows x the G gate blocks of one unit block, 64-byte K stages
+// (see wide.h).  NW = 8: two unit blocks (64 hidden units) per workgroup of 8 waves and three stages in
+// flight; waves 0-3 issue all loads (4 instructions of gathered A rows and G of weight rows each).
+// NW = 4 (fp32): one unit block per workgroup of 4 waves and one stage in flight, so that two
+// workgroups share a compute unit and one's epilogue overlaps the other's matrix work; every wave loads
+// 4 instructions of A rows and every fourth instruction of the 2 G of weight rows.
+
+template <typename T, int G, int NW>
+struct WideFwdIssue {
+  static constexpr int NBI = NW == 8 ? G : (2 * G + 3) / 4;  // weight-row instructions per wave, at most
+  const FwdArgs& a;
+  const int (*srow)[wide::kRows];
+  int wskip, inp, wave, nb, cur_seg = -1;
+  const char* wp[NBI];  // this lane's weight row per instruction, unit included (K offset 0)
+  int wslot[NBI];       // the instruction's 1 KB slot in the weight tile
+  const char* rp[4];    // this lane's A row per instruction in the current segment, unit included
+  __device__ __forceinline__ void reload(int seg) {
+    constexpr int es = sizeof(T);
+    const bool is_in = a.has_input && seg == 0;
+    const char* base = static_cast<const char*>(is_in ? a.table : a.h_pool);
+    const size_t stride = (size_t)(is_in ? a.tld : a.ld) * es;
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int sr = srow[seg][64 * wave + 16 * i + wide::lane_row(lane)];
+      rp[i] = (sr >= 0 ? base + (size_t)sr * stride : static_cast<const char*>(a.zero)) + wide::lane_unit(lane) * 16;
+    }
+    cur_seg = seg;
+  }
+  __device__ __forceinline__ void operator()(int c, char* slot) {
+    constexpr int es = sizeof(T), BK = 64 / es, BOFF = wide::kRows * 64;
+    const int kabs = c * BK;
+    int seg, kc;
+    if (kabs < inp) {
+      seg = 0;
+      kc = kabs;
+    } else {
+      const int k = (kabs - inp) / a.HP;
+      seg = a.has_input + k;
+      kc = kabs - inp - k * a.HP;
+    }
+    if (seg != cur_seg) reload(seg);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16_untracked(rp[i] + kc * es, slot + (4 * wave + i) * 1024);
+#pragma unroll
+    for (int i = 0; i < NBI; ++i)
+      if (i < nb) dma16_untracked(wp[i] + (kabs + wskip) * es, slot + BOFF + wslot[i] * 1024);
+  }
+};
+
+template <typename T, int KIND, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void k_cell_fwd_w(FwdArgs a) {
+  constexpr int G = Gates<KIND>::G;
+  constexpr int NTH = NW * 64;
+  constexpr int UPW = NW / 4;  // unit blocks per workgroup
+  constexpr int BM = wide::kRows, BN = UPW * G * 32;
+  constexpr int BOFF = BM * 64, SLOT = (BM + BN) * 64;
+  constexpr int NSLOT = NW == 8 ? wide::kSlots : 2;
+  constexpr int MT = 2;  // 32-row blocks per wave
+  __shared__ __attribute__((aligned(16))) char ring[NSLOT * SLOT];
+  __shared__ int srow[3][BM];  // source row of every tile row, per input segment (-1: zero row)
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  const int wr = wave & 3, wc = wave >> 2;
+  const int R = (a.rows + BM - 1) / BM, NU = a.HP / (32 * UPW);  // row tiles, unit-block groups
+  int up, rt;
+  if (a.map == kMapOwnCols) {
+    xcd_cols(NU, up, rt);
+    if (rt >= R) return;
+  } else {
+    int tx, ty;
+    if (!xcd_tile(NU, R, tx, ty)) return;
+    up = tx;
+    rt = ty;
+  }
+  const int m0 = rt * BM;
+  const int nseg = a.has_input + a.arity;
+  for (int i = tid; i < nseg * BM; i += NTH) {
+    const int seg = i / BM, r = i - seg * BM, row = m0 + r;
+    const bool is_in = a.has_input && seg == 0;
+    int sr = -1;
+    if (row < a.rows)
+      sr = is_in ? a.input_idx[a.row_begin + row] : a.child_pos[a.idx_off + row * a.arity + (seg - a.has_input)];
+    srow[seg][r] = sr;
+  }
+  __syncthreads();
+
+  constexpr int BK = 64 / sizeof(T);
+  const int inp = a.has_input ? a.INP : 0;
+  const int nst = (inp + a.arity * a.HP) / BK;
+  using Issue = WideFwdIssue<T, G, NW>;
+  Issue issue{a, srow, a.has_input ? 0 : a.INP, inp, wr, 0};
+  issue.nb = NW == 8 ? G : (2 * G - wr + 3) / 4;
+#pragma unroll
+  for (int i = 0; i < Issue::NBI; ++i) {
+    const int slot = NW == 8 ? G * wr + i : wr + 4 * i;  // 16-row group of the weight tile
+    issue.wslot[i] = slot;
+    issue.wp[i] = static_cast<const char*>(a.Wf) +
+                  ((size_t)up * BN + 16 * min(slot, BN / 16 - 1) + wide::lane_row(lane)) * a.Kf * sizeof(T) +
+                  wide::lane_unit(lane) * 16;
+  }
+  f32x16 acc[MT][G];
+  zero_acc(acc);
+  if constexpr (NW == 8) {
+    const bool loads = wave < 4;
+    struct Gate {
+      Issue& is;
+      bool on;
+      __device__ __forceinline__ void operator()(int c, char* slot) {
+        if (on) is(c, slot);
+      }
+    } gate{issue, loads};
+    wide::loop<T, MT, G, 4 + G, SLOT, BOFF>(nst, gate, loads, ring, acc, wr * 64, wc * G * 32, lane);
+  } else {
+    wide::loop2<T, MT, G, SLOT, BOFF>(nst, issue, ring, acc, wr * 64, 0, lane);
+  }
+
+  // epilogue: the cell in registers, one 32-row block at a time (children's c loaded for the block first)
+  constexpr int NK = CKids<KIND>::N;
+  const int j = (UPW * up + wc) * 32 + (lane & 31);
+  float bz[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) bz[g] = a.bias[g * a.HP + j];
+  const float* zf = static_cast<const float*>(a.zero) + j;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    float cc[16][NK > 0 ? NK : 1];
+    if constexpr (NK > 0) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl = wr * 64 + mt * 32 + acc_row(r, lane);
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {
+          const int p = k < a.arity ? srow[a.has_input + k][rl] : -1;
+          cc[r][k] = *(p >= 0 ? a.c_pool + (size_t)p * a.ld + j : zf);
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl = wr * 64 + mt * 32 + acc_row(r, lane), row = m0 + rl;
+      if (row >= a.rows) continue;
+      if (j >= a.H) {
+        if (j < a.ld) pad_out<T>(a, row, j);
+        continue;
+      }
+      float z[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) z[g] = acc[mt][g][r] + bz[g];
+      const float cl = NK > 0 ? cc[r][0] : 0.f, cr = NK > 1 ? cc[r][NK > 1 ? 1 : 0] : 0.f;
+      cell_out<T, KIND>(a, row, j, z, cl, cr);
+    }
+  }
+}
+
 // finish a K-split level: sum the slices' partial z, add the bias, apply the cell
 template <typename T, int KIND>
 __global__ void k_cell_epi(FwdArgs a, int nsplit) {
@@ -347,6 +506,7 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
   const int row = blockIdx.x;
   const size_t p = (size_t)(a.row_begin + row);
   float* gb = a.gates + p * a.gstride;
+  auto gate = [&](int g, int j) -> float { return gb[g * a.HP + j]; };  // saved activations (fp32)
   int c0 = -1, c1 = -1;
   if (a.arity >= 1) c0 = a.child_pos[a.idx_off + row * a.arity];
   if (a.arity >= 2) c1 = a.child_pos[a.idx_off + row * a.arity + 1];
@@ -370,7 +530,7 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       if (a.d_table) unsafeAtomicAdd(&a.d_table[(size_t)a.input_idx[p] * a.tld + j], dh);
     } else if constexpr (KIND == FOLD_TREELSTM) {
       const float dc = a.dc[p * a.ld + j];
-      const float i_ = gb[j], fl = gb[a.HP + j], fr = gb[2 * a.HP + j], o = gb[3 * a.HP + j], u = gb[4 * a.HP + j];
+      const float i_ = gate(0, j), fl = gate(1, j), fr = gate(2, j), o = gate(3, j), u = gate(4, j);
       const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cl = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
       const float cr = c1 >= 0 ? a.c_pool[(size_t)c1 * a.ld + j] : 0.f;
@@ -384,7 +544,7 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       if (c1 >= 0) scatter_add(&a.dc[(size_t)c1 * a.ld + j], dct * fr, s1);
     } else if constexpr (KIND == FOLD_LSTM) {
       const float dc = a.dc[p * a.ld + j];
-      const float i_ = gb[j], f = gb[a.HP + j], o = gb[2 * a.HP + j], u = gb[3 * a.HP + j];
+      const float i_ = gate(0, j), f = gate(1, j), o = gate(2, j), u = gate(3, j);
       const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cp = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
@@ -394,7 +554,7 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       put(3, j, dct * i_ * (1.f - u * u));
       if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dct * f, s0);
     } else {
-      const float h = gb[j];
+      const float h = gate(0, j);
       put(0, j, dh * (1.f - h * h));
       if constexpr (KIND == FOLD_PROJ) {
         const float dc = a.dc[p * a.ld + j];
@@ -442,7 +602,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
   // weight slice) on one XCD
   const int R = (a.rows + BM - 1) / BM, NT = (a.Nb + BN - 1) / BN;
   int tx, ty, nt, rt, kz;
-  if (a.share_rows) {
+  if (a.map == kMapRows) {
     if (!xcd_tile(NT * a.ksplit, R, tx, ty)) return;
     rt = ty;
     nt = tx % NT;
@@ -525,6 +685,101 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
   }
 }
 
+// dz . W^T on wide levels: 256 rows x 256 columns per workgroup of 8 waves (each 64 x 128), 64-byte K
+// stages, three in flight (see wide.h).  Waves 0-3 issue the loads: 4 instructions of dz rows and 4 of
+// W^T rows each.
+template <typename T>
+__global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
+  constexpr int BM = wide::kRows, BN = 256, TM = 2, TN = 4, NL = 8;
+  constexpr int BOFF = BM * 64, SLOT = (BM + BN) * 64;
+  __shared__ __attribute__((aligned(16))) char ring[wide::kSlots * SLOT];
+  __shared__ int tgt[2][BM];   // per tile row: child k's pool row (mode 0) or the leaf-table row (mode 1)
+  __shared__ char sgl[2][BM];  // the child has one parent edge: plain read-add-write
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  const int wr = wave & 3, wc = wave >> 2;
+  const int R = (a.rows + BM - 1) / BM, NT = (a.Nb + BN - 1) / BN;
+  int nt, rt;
+  if (a.map == kMapOwnCols) {
+    xcd_cols(NT, nt, rt);
+    if (rt >= R) return;
+  } else {
+    int tx, ty;
+    if (!xcd_tile(NT, R, tx, ty)) return;
+    nt = tx;
+    rt = ty;
+  }
+  const int m0 = rt * BM, n0 = nt * BN;
+  for (int i = tid; i < 2 * BM; i += wide::kThreads) {
+    const int k = i / BM, rl = i - k * BM, row = m0 + rl;
+    int t = -1;
+    char one = 0;
+    if (row < a.rows) {
+      if (a.mode == 0) {
+        if (k < a.arity) {
+          t = a.child_pos[a.idx_off + row * a.arity + k];
+          one = t >= 0 && a.npar[t] == 1;
+        }
+      } else if (k == 0) {
+        t = a.input_idx[a.row_begin + row];
+      }
+    }
+    tgt[k][rl] = t;
+    sgl[k][rl] = one;
+  }
+  // published by the K loop's first barrier
+
+  const int nst = a.Kb * (int)sizeof(T) / 64;
+  const bool loads = wave < 4;
+  const char* zero = static_cast<const char*>(a.zero);
+  const char* wb = static_cast<const char*>(a.Wb);
+  struct Issue {
+    const char* ap[4];
+    const char* bp[4];
+    bool on;
+    __device__ __forceinline__ void operator()(int c, char* slot) const {
+      if (!on) return;
+      const int w = wave_id(), off = c * 64;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dma16_untracked(ap[i] + off, slot + (4 * w + i) * 1024);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dma16_untracked(bp[i] + off, slot + BOFF + (4 * w + i) * 1024);
+    }
+  } issue;
+  issue.on = loads;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int lu16 = wide::lane_unit(lane) * 16;
+    const int row = m0 + 64 * wr + 16 * i + wide::lane_row(lane);
+    issue.ap[i] = (row < a.rows ? reinterpret_cast<const char*>(a.dz + (size_t)(a.row_begin + row) * a.gstride) : zero) + lu16;
+    const int n = n0 + 64 * wr + 16 * i + wide::lane_row(lane);
+    issue.bp[i] = (n < a.Nb ? wb + (size_t)n * a.Kb * sizeof(T) : zero) + lu16;
+  }
+  f32x16 acc[TM][TN];
+  zero_acc(acc);
+  wide::loop<T, TM, TN, NL, SLOT, BOFF>(nst, issue, loads, ring, acc, wr * 64, wc * 128, lane);
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int n = n0 + wc * 128 + tn * 32 + (lane & 31);
+      if (n >= a.Nb) continue;
+      const int k = a.mode == 0 ? n / a.HP : 0, jin = a.mode == 0 ? n - k * a.HP : n;
+      if (jin >= (a.mode == 0 ? a.H : a.in_dim)) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl = wr * 64 + tm * 32 + acc_row(r, lane), row = m0 + rl;
+        if (row >= a.rows) continue;
+        const int t = tgt[k][rl];
+        if (t < 0) continue;
+        if (a.mode == 0)
+          scatter_add(&a.dh[(size_t)t * a.ld + jin], acc[tm][tn][r], sgl[k][rl]);
+        else
+          unsafeAtomicAdd(&a.d_table[(size_t)t * a.tld + jin], acc[tm][tn][r]);
+      }
+    }
+  }
+}
+
 // finish a K-split dz . W^T launch: sum the slices, then scatter
 __global__ void k_dx_epi(DxArgs a, int nsplit) {
   const int row = blockIdx.x;
@@ -539,12 +794,23 @@ template <typename T, int KIND>
 void cell_fwd_kind(const FwdArgs& a0, hipStream_t st) {
   const FwdPlan pl = fwd_plan(a0.rows, a0.HP, a0.has_input ? a0.INP : 0, a0.arity, sizeof(T), a0.zpart != nullptr);
   FwdArgs a = a0;
+  if (pl.wide) {
+    // bf16: 8 waves, two unit blocks, three stages in flight; fp32: 4 waves, one unit block, two
+    // workgroups per compute unit
+    constexpr int NW = sizeof(T) == 2 ? 8 : 4;
+    const int R = (int)cdiv(a.rows, wide::kRows), NU = a.HP / (32 * (NW / 4));
+    a.ksplit = 1;
+    a.map = NU % 8 == 0 ? kMapOwnCols : kMapRows;
+    dim3 grid(a.map == kMapOwnCols ? NU * R : xcd_grid(NU, R));
+    hipLaunchKernelGGL((k_cell_fwd_w<T, KIND, NW>), grid, dim3(NW * 64), 0, st, a);
+    return;
+  }
   a.ksplit = pl.ksplit;
   const int BM = 128 * pl.mt;
   const int G = Gates<KIND>::G;
-  a.share_rows = a.rows >= G * a.HP;  // gathered rows outweigh the weights
   const int R = (int)cdiv(a.rows, BM), UB = a.HP / 32;
-  dim3 grid(a.share_rows ? xcd_grid(UB * pl.ksplit, R) : xcd_grid(R * pl.ksplit, UB));
+  a.map = a.rows >= G * a.HP ? kMapRows : kMapCols;  // gathered rows outweigh the weights: share row tiles
+  dim3 grid(a.map == kMapRows ? xcd_grid(UB * pl.ksplit, R) : xcd_grid(R * pl.ksplit, UB));
   if (pl.ksplit > 1) {
     if (pl.mt == 2) hipLaunchKernelGGL((k_cell_fwd<T, KIND, 2, true>), grid, dim3(kThreads), 0, st, a);
     else hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, true>), grid, dim3(kThreads), 0, st, a);
@@ -652,11 +918,22 @@ void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
   DxArgs a = a0;
   ProfScope prof(dtype == FOLD_BF16 ? "bwd_dx.bf16" : "bwd_dx.f32", st);
   const DxPlan pl = dx_plan(a.rows, a.Nb, a.Kb, dtype == FOLD_BF16 ? 2 : 4, a.xpart != nullptr);
+  if (pl.wide) {
+    const int R = (int)cdiv(a.rows, wide::kRows), NT = (int)cdiv(a.Nb, 256);
+    a.ksplit = 1;
+    a.map = NT % 8 == 0 ? kMapOwnCols : kMapRows;
+    dim3 grid(a.map == kMapOwnCols ? NT * R : xcd_grid(NT, R));
+    if (dtype == FOLD_BF16)
+      hipLaunchKernelGGL(k_bwd_dx_w<uint16_t>, grid, dim3(wide::kThreads), 0, st, a);
+    else
+      hipLaunchKernelGGL(k_bwd_dx_w<float>, grid, dim3(wide::kThreads), 0, st, a);
+    return;
+  }
   const int MT = pl.mt;
   a.ksplit = pl.ksplit;
-  a.share_rows = a.rows >= a.Nb;
   const int R = (int)cdiv(a.rows, 128 * MT), NT = (int)cdiv(a.Nb, 128);
-  dim3 grid(a.share_rows ? xcd_grid(NT * pl.ksplit, R) : xcd_grid(R * pl.ksplit, NT));
+  a.map = a.rows >= a.Nb ? kMapRows : kMapCols;
+  dim3 grid(a.map == kMapRows ? xcd_grid(NT * pl.ksplit, R) : xcd_grid(R * pl.ksplit, NT));
 #define FOLD_DX(T_, MT_, S_) hipLaunchKernelGGL((k_bwd_dx2<T_, MT_, S_>), grid, dim3(kThreads), 0, st, a)
   const bool split = pl.ksplit > 1;
   if (dtype == FOLD_BF16) {

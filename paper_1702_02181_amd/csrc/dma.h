@@ -17,8 +17,30 @@ __device__ __forceinline__ void dma16(const void* src, void* lds) {
   __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
 }
 
+// The same load issued as inline assembly, which the compiler does not track.  Its own tracking of
+// direct-to-LDS loads keeps only a few of them apart and otherwise waits for all of them before any LDS
+// read, which would drain a pipeline that keeps two stages in flight.  A kernel using it waits for its
+// loads explicitly (vm_wait / vm_wait_n) before the barrier that publishes them.
+__device__ __forceinline__ void dma16_untracked(const void* src, void* lds) {
+  const uint32_t base = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(base), "v"(src) : "memory", "m0");
+}
+
 // wait until this wave's global loads, direct-to-LDS ones included, have landed
 __device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// wait until at most N of this wave's global loads are still outstanding (loads complete in order)
+template <int N>
+__device__ __forceinline__ void vm_wait_n() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Workgroup barrier without the release fence of __syncthreads(), which waits for every outstanding
+// global load of the wave -- the stages still in flight included.  Callers wait for what must have
+// landed (vm_wait_n) themselves; LDS reads of the previous stage are complete because the matrix
+// instructions that consumed them were issued before the barrier.
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 

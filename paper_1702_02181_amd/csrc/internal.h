@@ -66,22 +66,26 @@ struct FwdArgs {
   const void* zero;  // a zero row at least as wide as any K the kernels read (16-byte aligned)
   float* zpart;  // workspace for K-split partial sums, or NULL (no split)
   int ksplit;    // set by the launcher
-  int share_rows;  // set by the launcher: co-locate the workgroups of a row tile (else of a unit block)
+  int map;         // set by the launcher: workgroup order over the XCDs (kMapRows, kMapCols, kMapOwnCols)
 };
 void launch_cell_fwd(int dtype, int kind, const FwdArgs& a, hipStream_t st);
 
-// Tiling of one forward group: row tile of 128 * mt rows, K loop cut into ksplit slices.  Wide
-// groups use 256-row tiles; groups too narrow to give every compute unit a workgroup use 128-row
-// tiles and, if still short, split K (partial sums in the workspace, then an epilogue kernel).
+// Tiling of one forward group.  Wide groups (at least one workgroup per compute unit) use the wide
+// kernel: 256 rows x 2 unit blocks per workgroup of 8 waves.  Narrower groups use 128-row tiles of one
+// unit block and, if still short of workgroups, split K (partial sums in the workspace, then an
+// epilogue kernel).
 struct FwdPlan {
   int mt = 1, ksplit = 1;
+  bool wide = false;  // 256 rows x 2 unit blocks per workgroup of 8 waves
 };
 inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bool can_split) {
   const int BK = esize == 4 ? 32 : 64;
   const int nst = inp_used / BK + arity * (HP / BK);
   const long long ub = HP / 32;
   FwdPlan p;
-  p.mt = 1;
+  // wide tiles once they give every compute unit a workgroup
+  p.wide = ((long long)(rows + 255) / 256) * (ub / 2) >= 256;
+  if (p.wide) return p;
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * ub;
   if (can_split && base < 192 && nst >= 4) {
     const long long want = (256 + base - 1) / base;
@@ -90,16 +94,21 @@ inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bo
   return p;
 }
 
-// dz . W^T tiling: 128 * mt rows x 128 columns, K cut into ksplit slices (partial products in the
-// workspace, summed and scattered by an epilogue kernel).
+// dz . W^T tiling: wide groups use 256 x 256 tiles (8 waves); others 128 * mt rows x 128 columns, K
+// cut into ksplit slices (partial products in the workspace, summed and scattered by an epilogue
+// kernel).
 struct DxPlan {
   int mt = 1, ksplit = 1;
+  bool wide = false;  // 256 x 256 tiles per workgroup of 8 waves
 };
 inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
   const int BK = esize == 4 ? 32 : 64;
   const int nst = Kb / BK;
   const long long nb = (Nb + 127) / 128;
   DxPlan p;
+  // wide tiles once they give every compute unit a workgroup
+  p.wide = ((long long)(rows + 255) / 256) * ((Nb + 255) / 256) >= 256;
+  if (p.wide) return p;
   // fp32: 128-row tiles, two workgroups per compute unit; bf16: 256-row tiles on wide levels
   p.mt = esize == 4 ? 1 : (((long long)(rows + 255) / 256) * nb >= 256 ? 2 : 1);
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * nb;
@@ -148,7 +157,7 @@ struct DxArgs {
   const int* npar;  // parent edges per pool row
   float* xpart;     // workspace for K-split partial products, or NULL (no split)
   int ksplit;       // set by the launcher
-  int share_rows;   // set by the launcher: co-locate the workgroups of a row tile (else of a column tile)
+  int map;          // set by the launcher: workgroup order over the XCDs (kMapRows, kMapCols, kMapOwnCols)
 };
 void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st);
 

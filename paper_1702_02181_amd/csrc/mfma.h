@@ -55,6 +55,18 @@ __device__ __forceinline__ bool xcd_tile(int X, int Y, int& x, int& y) {
 }
 inline int xcd_grid(int X, int Y) { return X * (((Y + 7) >> 3) << 3); }
 
+// Wide launches over C column tiles (C a multiple of 8) and R row tiles, launched as C * R workgroups:
+// XCD k owns column tiles [k C / 8, (k + 1) C / 8) of every row tile, so the weight slice those
+// columns read stays in its L2 while the row tiles stream past (row tiles in launch order).
+__device__ __forceinline__ void xcd_cols(int C, int& col, int& row) {
+  const int L = blockIdx.x, per = C >> 3, slot = L >> 3;
+  col = (L & 7) * per + slot % per;
+  row = slot / per;
+}
+
+// how a launch orders its workgroups over the XCDs
+enum { kMapRows = 0, kMapCols = 1, kMapOwnCols = 2 };
+
 // row of the 32x32 result tile held by register r of lane `lane`
 __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
