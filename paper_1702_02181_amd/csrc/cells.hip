@@ -270,22 +270,18 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------- forward, wide levels
-// 256 rows per workgroup, each wave 64 rows x the G gate blocks of one unit block, 64-byte K stages
-// (see wide.h).  NW = 8: two unit blocks (64 hidden units) per workgroup of 8 waves and three stages in
-// flight; waves 0-3 issue all loads (4 instructions of gathered A rows and G of weight rows each).
-// NW = 4 (fp32): one unit block per workgroup of 4 waves and one stage in flight, so that two
-// workgroups share a compute unit and one's epilogue overlaps the other's matrix work; every wave loads
-// 4 instructions of A rows and every fourth instruction of the 2 G of weight rows.
+// 256 rows x 2 unit blocks (all G gate blocks of 64 hidden units) per workgroup of 8 waves, each wave
+// 64 rows x the G gate blocks of one unit block; 64-byte K stages, three in flight (see wide.h).  Waves
+// 0-3 issue the loads of a stage: 4 instructions of gathered A rows (64 tile rows) and G of weight rows
+// (16 G of the 64 G rows in the tile) each.
 
-template <typename T, int G, int NW>
+template <typename T, int G>
 struct WideFwdIssue {
-  static constexpr int NBI = NW == 8 ? G : (2 * G + 3) / 4;  // weight-row instructions per wave, at most
   const FwdArgs& a;
   const int (*srow)[wide::kRows];
-  int wskip, inp, wave, nb, cur_seg = -1;
-  const char* wp[NBI];  // this lane's weight row per instruction, unit included (K offset 0)
-  int wslot[NBI];       // the instruction's 1 KB slot in the weight tile
-  const char* rp[4];    // this lane's A row per instruction in the current segment, unit included
+  int wskip, inp, wave, cur_seg = -1;
+  const char* wp[G];  // this lane's weight row per instruction, unit included (K offset 0)
+  const char* rp[4];  // this lane's A row per instruction in the current segment, unit included
   __device__ __forceinline__ void reload(int seg) {
     constexpr int es = sizeof(T);
     const bool is_in = a.has_input && seg == 0;
@@ -315,39 +311,37 @@ struct WideFwdIssue {
 #pragma unroll
     for (int i = 0; i < 4; ++i) dma16_untracked(rp[i] + kc * es, slot + (4 * wave + i) * 1024);
 #pragma unroll
-    for (int i = 0; i < NBI; ++i)
-      if (i < nb) dma16_untracked(wp[i] + (kabs + wskip) * es, slot + BOFF + wslot[i] * 1024);
+    for (int i = 0; i < G; ++i) dma16_untracked(wp[i] + (kabs + wskip) * es, slot + BOFF + (G * wave + i) * 1024);
   }
 };
 
-template <typename T, int KIND, int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void k_cell_fwd_w(FwdArgs a) {
+// workgroup -> (row tile, column group) for the wide kernels: kMapOwnCols (column groups a multiple of
+// 8: each XCD keeps its own groups) or kMapRows (the column groups of a row tile on one XCD)
+__device__ __forceinline__ bool wide_tile(int map, int R, int NC, int& rt, int& nc) {
+  if (map == kMapOwnCols) {
+    xcd_cols(NC, nc, rt);
+    return rt < R;
+  }
+  return xcd_tile(NC, R, nc, rt);
+}
+
+template <typename T, int KIND>
+__global__ __launch_bounds__(wide::kThreads) void k_cell_fwd_w(FwdArgs a) {
   constexpr int G = Gates<KIND>::G;
-  constexpr int NTH = NW * 64;
-  constexpr int UPW = NW / 4;  // unit blocks per workgroup
-  constexpr int BM = wide::kRows, BN = UPW * G * 32;
+  constexpr int BM = wide::kRows, BN = 2 * G * 32;
   constexpr int BOFF = BM * 64, SLOT = (BM + BN) * 64;
-  constexpr int NSLOT = NW == 8 ? wide::kSlots : 2;
   constexpr int MT = 2;  // 32-row blocks per wave
-  __shared__ __attribute__((aligned(16))) char ring[NSLOT * SLOT];
+  __shared__ __attribute__((aligned(16))) char ring[wide::kSlots * SLOT];
   __shared__ int srow[3][BM];  // source row of every tile row, per input segment (-1: zero row)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
   const int wr = wave & 3, wc = wave >> 2;
-  const int R = (a.rows + BM - 1) / BM, NU = a.HP / (32 * UPW);  // row tiles, unit-block groups
-  int up, rt;
-  if (a.map == kMapOwnCols) {
-    xcd_cols(NU, up, rt);
-    if (rt >= R) return;
-  } else {
-    int tx, ty;
-    if (!xcd_tile(NU, R, tx, ty)) return;
-    up = tx;
-    rt = ty;
-  }
+  const int R = (a.rows + BM - 1) / BM, NU = a.HP / 64;  // row tiles, unit-block pairs
+  int rt, up;
+  if (!wide_tile(a.map, R, NU, rt, up)) return;
   const int m0 = rt * BM;
   const int nseg = a.has_input + a.arity;
-  for (int i = tid; i < nseg * BM; i += NTH) {
+  for (int i = tid; i < nseg * BM; i += wide::kThreads) {
     const int seg = i / BM, r = i - seg * BM, row = m0 + r;
     const bool is_in = a.has_input && seg == 0;
     int sr = -1;
@@ -360,36 +354,27 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   constexpr int BK = 64 / sizeof(T);
   const int inp = a.has_input ? a.INP : 0;
   const int nst = (inp + a.arity * a.HP) / BK;
-  using Issue = WideFwdIssue<T, G, NW>;
-  Issue issue{a, srow, a.has_input ? 0 : a.INP, inp, wr, 0};
-  issue.nb = NW == 8 ? G : (2 * G - wr + 3) / 4;
+  const bool loads = wave < 4;
+  WideFwdIssue<T, G> issue{a, srow, a.has_input ? 0 : a.INP, inp, wr};
 #pragma unroll
-  for (int i = 0; i < Issue::NBI; ++i) {
-    const int slot = NW == 8 ? G * wr + i : wr + 4 * i;  // 16-row group of the weight tile
-    issue.wslot[i] = slot;
+  for (int i = 0; i < G; ++i)
     issue.wp[i] = static_cast<const char*>(a.Wf) +
-                  ((size_t)up * BN + 16 * min(slot, BN / 16 - 1) + wide::lane_row(lane)) * a.Kf * sizeof(T) +
+                  ((size_t)up * BN + 16 * (G * wr + i) + wide::lane_row(lane)) * a.Kf * sizeof(T) +
                   wide::lane_unit(lane) * 16;
-  }
   f32x16 acc[MT][G];
   zero_acc(acc);
-  if constexpr (NW == 8) {
-    const bool loads = wave < 4;
-    struct Gate {
-      Issue& is;
-      bool on;
-      __device__ __forceinline__ void operator()(int c, char* slot) {
-        if (on) is(c, slot);
-      }
-    } gate{issue, loads};
-    wide::loop<T, MT, G, 4 + G, SLOT, BOFF>(nst, gate, loads, ring, acc, wr * 64, wc * G * 32, lane);
-  } else {
-    wide::loop2<T, MT, G, SLOT, BOFF>(nst, issue, ring, acc, wr * 64, 0, lane);
-  }
+  struct Gate {
+    WideFwdIssue<T, G>& is;
+    bool on;
+    __device__ __forceinline__ void operator()(int c, char* slot) {
+      if (on) is(c, slot);
+    }
+  } gate{issue, loads};
+  wide::loop<T, MT, G, 4 + G, SLOT, BOFF>(nst, gate, loads, ring, acc, wr * 64, wc * G * 32, lane);
 
+  const int j = (2 * up + wc) * 32 + (lane & 31);
   // epilogue: the cell in registers, one 32-row block at a time (children's c loaded for the block first)
   constexpr int NK = CKids<KIND>::N;
-  const int j = (UPW * up + wc) * 32 + (lane & 31);
   float bz[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) bz[g] = a.bias[g * a.HP + j];
@@ -699,15 +684,7 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
   const int wr = wave & 3, wc = wave >> 2;
   const int R = (a.rows + BM - 1) / BM, NT = (a.Nb + BN - 1) / BN;
   int nt, rt;
-  if (a.map == kMapOwnCols) {
-    xcd_cols(NT, nt, rt);
-    if (rt >= R) return;
-  } else {
-    int tx, ty;
-    if (!xcd_tile(NT, R, tx, ty)) return;
-    nt = tx;
-    rt = ty;
-  }
+  if (!wide_tile(a.map, R, NT, rt, nt)) return;
   const int m0 = rt * BM, n0 = nt * BN;
   for (int i = tid; i < 2 * BM; i += wide::kThreads) {
     const int k = i / BM, rl = i - k * BM, row = m0 + rl;
@@ -795,14 +772,11 @@ void cell_fwd_kind(const FwdArgs& a0, hipStream_t st) {
   const FwdPlan pl = fwd_plan(a0.rows, a0.HP, a0.has_input ? a0.INP : 0, a0.arity, sizeof(T), a0.zpart != nullptr);
   FwdArgs a = a0;
   if (pl.wide) {
-    // bf16: 8 waves, two unit blocks, three stages in flight; fp32: 4 waves, one unit block, two
-    // workgroups per compute unit
-    constexpr int NW = sizeof(T) == 2 ? 8 : 4;
-    const int R = (int)cdiv(a.rows, wide::kRows), NU = a.HP / (32 * (NW / 4));
+    const int R = (int)cdiv(a.rows, wide::kRows), NU = a.HP / 64;
     a.ksplit = 1;
     a.map = NU % 8 == 0 ? kMapOwnCols : kMapRows;
     dim3 grid(a.map == kMapOwnCols ? NU * R : xcd_grid(NU, R));
-    hipLaunchKernelGGL((k_cell_fwd_w<T, KIND, NW>), grid, dim3(NW * 64), 0, st, a);
+    hipLaunchKernelGGL((k_cell_fwd_w<T, KIND>), grid, dim3(wide::kThreads), 0, st, a);
     return;
   }
   a.ksplit = pl.ksplit;

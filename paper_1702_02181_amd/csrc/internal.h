@@ -83,7 +83,8 @@ inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bo
   const int nst = inp_used / BK + arity * (HP / BK);
   const long long ub = HP / 32;
   FwdPlan p;
-  // wide tiles once they give every compute unit a workgroup
+  // wide tiles once they give every compute unit a workgroup (narrower levels: the K-split of
+  // partial sums through the workspace costs more than a wide tile gains)
   p.wide = ((long long)(rows + 255) / 256) * (ub / 2) >= 256;
   if (p.wide) return p;
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * ub;
@@ -106,7 +107,8 @@ inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
   const int nst = Kb / BK;
   const long long nb = (Nb + 127) / 128;
   DxPlan p;
-  // wide tiles once they give every compute unit a workgroup
+  // wide tiles once they give every compute unit a workgroup (narrower levels: the K-split of
+  // partial sums through the workspace costs more than a wide tile gains)
   p.wide = ((long long)(rows + 255) / 256) * ((Nb + 255) / 256) >= 256;
   if (p.wide) return p;
   // fp32: 128-row tiles, two workgroups per compute unit; bf16: 256-row tiles on wide levels

@@ -98,24 +98,6 @@ __device__ __forceinline__ void loop(int nst, ISSUE& issue, bool loads, char* ri
   }
 }
 
-// Double-buffered variant for workgroups that keep one stage in flight (two slots): at stage c every
-// loading wave waits for all its loads (stage c is the only one outstanding), one barrier publishes
-// stage c and frees the slot stage c + 1 overwrites.  Used where the stage's matrix work is long enough
-// to cover a load (fp32) and two workgroups per compute unit are wanted.
-template <typename T, int TM, int TN, int SLOT, int BOFF, class ISSUE>
-__device__ __forceinline__ void loop2(int nst, ISSUE& issue, char* ring, f32x16 (&acc)[TM][TN], int arow0,
-                                      int brow0, int lane) {
-  if (nst > 0) issue(0, ring);
-  for (int c = 0; c < nst; ++c) {
-    vm_wait();
-    wg_barrier();
-    if (c + 1 < nst) issue(c + 1, ring + ((c + 1) & 1) * SLOT);
-    __builtin_amdgcn_sched_barrier(0);
-    const char* s = ring + (c & 1) * SLOT;
-    mma<T, TM, TN>(s, s + BOFF, acc, arow0, brow0, lane);
-  }
-}
-
 }  // namespace wide
 
 }  // namespace fold
