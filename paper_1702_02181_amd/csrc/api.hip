@@ -451,6 +451,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
         const WgradSplit sp = wgrad_split(count, Kw, Nw, p.dtype);
         w.chunk = sp.chunk;
         w.nchunk = sp.nchunk;
+        w.wide = sp.wide;
         w.bpart = (pg.dbias && !bias_done) ? bpart : nullptr;
         launch_wgrad(p.dtype, w, st);
         launch_wgrad_reduce(part, sp.nchunk, Kw, Nw, seg, p.H, p.HP, ps.in_dim, ps.G, dW, st);

@@ -29,7 +29,8 @@ WsLayout workspace_layout(const Sched& s, const Packed& p);
 // Weight-gradient work split: rows of one op reduced in `nchunk` chunks of `chunk` rows.
 struct WgradSplit {
   int nchunk = 0, chunk = 0;
-  int bparts = 0;  // rows of bias partial sums the launch writes
+  int bparts = 0;     // rows of bias partial sums the launch writes
+  bool wide = false;  // 256 x 256 tiles (bf16, many rows)
 };
 WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype);
 
@@ -175,6 +176,7 @@ struct WgArgs {
   const void* src;
   const float* dz;
   int chunk, nchunk;
+  int wide;        // 256 x 256 tiles (WgradSplit::wide)
   float* partial;  // [nchunk][Kw][Nw]
   float* bpart;    // [bparts][Nw] column sums of dz (see WgradSplit), or NULL
   const void* zero;  // a zero row at least 16 bytes past any column the kernels read

@@ -18,6 +18,7 @@
 #include "internal.h"
 #include "dma.h"
 #include "mfma.h"
+#include "wide.h"
 
 namespace fold {
 
@@ -358,6 +359,173 @@ __global__ __launch_bounds__(kThreads) void k_wgrad_bf16(WgArgs a) {
   if (do_bias && n0 + bc < a.Nw) a.bpart[((size_t)(chunk_id * MTm + mt_) * 2 + bg) * a.Nw + n0 + bc] = bsum;
 }
 
+// ---------------------------------------------------------------- bf16, wide: 256 x 256 tiles
+// 8 waves, each 64 weight rows x 128 gate columns; a stage is 32 op rows (two MFMA K steps): X^T tile
+// 32 x 256 weight rows and dz^T tile 32 x 256 columns, 512 bytes an op row, 128 FLOP per operand byte.
+// Four stage slots keep three stages in flight (untracked direct loads, waves 0-3: 4 instructions of X
+// and 4 of dz rows each, two op rows per instruction).  The op rows' indices (pool row of dz, children's
+// or leaf-table row of X) reach LDS through an index ring three stages ahead of the data, loaded by
+// wave 4 alone (two 4-byte-per-lane direct loads per stage), so every wait counts only its own loads.
+// Row m's 16-byte units are permuted by ^ 4 (m & 3) for the transposing reads (as the 128-column
+// kernel above).
+
+// lane l of the wave copies 4 bytes from src to lds + 4 l
+__device__ __forceinline__ void dma4_untracked(const void* src, void* lds) {
+  const uint32_t base = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(base), "v"(src) : "memory", "m0");
+}
+
+__device__ __forceinline__ int wgw_off(int r, int col) {
+  return r * 512 + (((col >> 3) ^ (4 * (r & 3))) << 4) + (col & 7) * 2;
+}
+
+__global__ __launch_bounds__(wide::kThreads) void k_wgrad_bf16_w(WgArgs a) {
+  constexpr int TB = 256, TM = 2, TN = 4, NL = 8;
+  constexpr int ABYTES = 32 * 512, SLOT = 2 * ABYTES;  // X^T then dz^T
+  constexpr int NIDX = 8, IBYTES = 512;  // index ring: per stage [op_rows 32 | op_inp 32 | op_cpos 64] ints
+  __shared__ __attribute__((aligned(16))) char ring[wide::kSlots * SLOT];
+  __shared__ __attribute__((aligned(16))) int iring[NIDX][IBYTES / 4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  const int wr = wave & 3, wc = wave >> 2;
+  const int NT = (a.Nw + TB - 1) / TB, MTm = (a.Kw + TB - 1) / TB;
+  int tx, chunk_id;
+  if (!xcd_tile(MTm * NT, a.nchunk, tx, chunk_id)) return;
+  const int mt_ = tx % MTm, nt = tx / MTm;
+  const int m0 = mt_ * TB, n0 = nt * TB;
+  const int lo = chunk_id * a.chunk, hi = min(a.count, lo + a.chunk);
+  const int nst = (hi - lo + 31) / 32;
+  const char* zero = static_cast<const char*>(a.zero);
+  const char* xbase = static_cast<const char*>(a.src);
+  const size_t xstride = (size_t)(a.seg ? a.ld : a.tld) * 2, dstride = (size_t)a.gstride * 4;
+
+  // index loads (wave 4): stage c's indices into ring slot c % NIDX
+  auto issue_idx = [&](int c) {
+    const int q0 = lo + c * 32;
+    int* slot = iring[c % NIDX];
+    const int r = lane & 31;
+    const int qa = min(q0 + r, hi - 1);
+    dma4_untracked(lane < 32 ? a.op_rows + qa : a.op_inp + qa, slot);
+    const int qc = min(2 * q0 + lane, 2 * hi - 1);
+    dma4_untracked(a.op_cpos + qc, slot + 64);
+  };
+  // this lane's unit of an op row: weight-row column (A) and gate column (B) it fetches
+  const int u = lane & 31;
+  auto issue = [&](int c, char* sl) {
+    const int* ix = iring[c % NIDX];
+    const int q0 = lo + c * 32;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 2 * (4 * wr + i) + (lane >> 5);  // op row within the stage
+      const int gu = u ^ (4 * (r & 3));              // global 16-byte unit of the tile row
+      const bool live = q0 + r < hi;
+      // X^T: weight rows m0 + 8 gu .. + 7
+      const int m = m0 + 8 * gu;
+      const int child = a.seg ? min(m / a.HP, 1) : 0;
+      const int xi = a.seg ? ix[64 + 2 * r + child] : ix[32 + r];
+      const int col = a.seg ? m - child * a.HP : m;
+      const bool xa = live && m < a.Kw && xi >= 0;
+      dma16_untracked(xa ? xbase + (size_t)xi * xstride + (size_t)col * 2 : zero, sl + (4 * wr + i) * 1024);
+      // dz^T: gate columns n0 + 8 gu .. + 7
+      const int n = n0 + 8 * gu;
+      const bool da = live && n < a.Nw;
+      dma16_untracked(da ? reinterpret_cast<const char*>(a.dz) + (size_t)ix[r] * dstride + (size_t)n * 2 : zero,
+                      sl + ABYTES + (4 * wr + i) * 1024);
+    }
+  };
+
+  // transposing-read offsets (see k_wgrad_bf16): group g = lane / 16, lane gi of the group
+  const int g = lane >> 4, gi = lane & 15;
+  int aoff[TM], boff[TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) aoff[tm] = wr * 64 + tm * 32 + 16 * (g & 1) + 4 * (gi & 3);
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) boff[tn] = wc * 128 + tn * 32 + 16 * (g & 1) + 4 * (gi & 3);
+  const int mrow = 8 * (g >> 1) + (gi >> 2);
+  // bias column sums (tiles of the first weight-row tile only): thread t sums column t % 256 over
+  // the stage rows 16 (t / 256) .. + 15
+  const bool do_bias = a.bpart != nullptr && mt_ == 0;
+  const int bc = tid & 255, bg = tid >> 8;
+  float bsum = 0.f;
+
+  f32x16 acc[TM][TN];
+  zero_acc(acc);
+  const bool dloads = wave < 4, iloads = wave == 4;
+  if (nst > 0) {
+    if (iloads) {
+      for (int c = 0; c < min(nst, 6); ++c) issue_idx(c);
+      if (nst > 5) vm_wait_n<6>();  // indices of stages 0-2 landed, 3-5 in flight
+      else if (nst > 4) vm_wait_n<4>();
+      else if (nst > 3) vm_wait_n<2>();
+      else vm_wait();
+    }
+    wg_barrier();
+    if (dloads)
+      for (int c = 0; c < min(nst, 3); ++c) issue(c, ring + c * SLOT);
+    for (int c = 0; c < nst; ++c) {
+      if (dloads) {
+        if (c + 2 < nst) vm_wait_n<2 * NL>();
+        else if (c + 1 < nst) vm_wait_n<NL>();
+        else vm_wait();
+      }
+      if (iloads) {  // indices of stage c + 3 (issued at stage c - 3) landed; c + 4, c + 5 may be in flight
+        const int later = min(2, max(0, nst - 1 - (c + 3)));
+        if (later == 2) vm_wait_n<4>();
+        else if (later == 1) vm_wait_n<2>();
+        else vm_wait();
+      }
+      wg_barrier();
+      if (dloads && c + 3 < nst) issue(c + 3, ring + ((c + 3) & 3) * SLOT);
+      if (iloads && c + 6 < nst) issue_idx(c + 6);
+      __builtin_amdgcn_sched_barrier(0);
+      const char* As = ring + (c & 3) * SLOT;
+      const char* Bs = As + ABYTES;
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        uint4 af[TM], bf[TN];
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) {
+          const uint2 l2 = ld_tr16(As, wgw_off(16 * s + mrow, aoff[tm]));
+          const uint2 h2 = ld_tr16(As, wgw_off(16 * s + mrow + 4, aoff[tm]));
+          af[tm] = make_uint4(l2.x, l2.y, h2.x, h2.y);
+        }
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) {
+          const uint2 l2 = ld_tr16(Bs, wgw_off(16 * s + mrow, boff[tn]));
+          const uint2 h2 = ld_tr16(Bs, wgw_off(16 * s + mrow + 4, boff[tn]));
+          bf[tn] = make_uint4(l2.x, l2.y, h2.x, h2.y);
+        }
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+            acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[tm]),
+                                                                 __builtin_bit_cast(bf16x8, bf[tn]), acc[tm][tn],
+                                                                 0, 0, 0);
+      }
+      if (do_bias) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) bsum += bf2f(*reinterpret_cast<const uint16_t*>(Bs + wgw_off(16 * bg + r, bc)));
+      }
+    }
+  }
+
+  float* out = a.partial + (size_t)chunk_id * a.Kw * a.Nw;
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int n = n0 + wc * 128 + tn * 32 + (lane & 31);
+      if (n >= a.Nw) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wr * 64 + tm * 32 + acc_row(r, lane);
+        if (m < a.Kw) out[(size_t)m * a.Nw + n] = acc[tm][tn][r];
+      }
+    }
+  if (do_bias && n0 + bc < a.Nw) a.bpart[((size_t)chunk_id * 2 + bg) * a.Nw + n0 + bc] = bsum;
+}
+
 // dW[row, col] += sum over chunks of partial[chunk, m, n], (m, n) in the padded layout
 __global__ void k_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP,
                                int in_dim, int G, float* dW) {
@@ -419,6 +587,18 @@ __global__ void k_bias_reduce(const float* bpart, int nparts, int Nw, int H, int
 WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype) {
   WgradSplit w;
   if (count <= 0 || Kw <= 0 || Nw <= 0) return w;
+  // bf16 ops with many rows: 256 x 256 tiles (twice the operand reuse of 128 x 128)
+  w.wide = dtype == FOLD_BF16 && count >= 65536;
+  if (w.wide) {
+    const long long tiles = (long long)((Kw + 255) / 256) * ((Nw + 255) / 256);
+    const long long want = std::max(8LL, ((512 + tiles - 1) / tiles + 7) / 8 * 8);
+    const long long most = std::max(1, (count + 1023) / 1024);
+    w.nchunk = (int)std::max(1LL, std::min(want, most));
+    w.chunk = round_up((count + w.nchunk - 1) / w.nchunk, 32);
+    w.nchunk = (count + w.chunk - 1) / w.chunk;
+    w.bparts = w.nchunk * 2;
+    return w;
+  }
   const int tn = dtype == FOLD_BF16 ? 128 : kWgNW;
   const long long tiles = (long long)((Kw + kTM - 1) / kTM) * ((Nw + tn - 1) / tn);
   // enough workgroups to fill the chip, and chunks in multiples of the 8 XCDs (one XCD per chunk)
@@ -435,7 +615,10 @@ WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype) {
 void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st) {
   if (a.count <= 0) return;
   ProfScope prof(dtype == FOLD_BF16 ? "wgrad.bf16" : "wgrad.f32", st);
-  if (dtype == FOLD_BF16) {
+  if (a.wide) {
+    dim3 grid(xcd_grid(((a.Kw + 255) / 256) * ((a.Nw + 255) / 256), a.nchunk));
+    hipLaunchKernelGGL(k_wgrad_bf16_w, grid, dim3(wide::kThreads), 0, st, a);
+  } else if (dtype == FOLD_BF16) {
     dim3 grid(xcd_grid(((a.Kw + kTM - 1) / kTM) * ((a.Nw + 127) / 128), a.nchunk));
     hipLaunchKernelGGL(k_wgrad_bf16, grid, dim3(kThreads), 0, st, a);
   } else {
