@@ -44,9 +44,9 @@ PEAKS = {  # MI355X datasheet, dense
 # Sources whose code decides a kernel class's kernels: a traffic record is valid only while they are
 # unchanged.
 CLASS_SOURCES = {
-    "cell_fwd": ("cells.hip", "dma.h", "mfma.h", "common.h", "internal.h"),
-    "bwd_dx": ("cells.hip", "dma.h", "mfma.h", "common.h", "internal.h"),
-    "wgrad": ("wgrad.hip", "dma.h", "mfma.h", "common.h", "internal.h"),
+    "cell_fwd": ("cells.hip", "dma.h", "mfma.h", "wide.h", "common.h", "internal.h"),
+    "bwd_dx": ("cells.hip", "dma.h", "mfma.h", "wide.h", "common.h", "internal.h"),
+    "wgrad": ("wgrad.hip", "dma.h", "mfma.h", "wide.h", "common.h", "internal.h"),
 }
 COPY_KERNEL = "k_probe_copy"
 TRAFFIC_TAG = "traffic-record:"
@@ -66,17 +66,17 @@ def rocprof_role(kernel_class: str, name: str):
     cls, dt = parts[0], CTYPE[parts[-1]]
     if cls == "cell_fwd":
         kind = KIND_IDS[parts[1]]
-        if re.search(rf"k_cell_fwd<{dt}, {kind}, ", name):
+        if re.search(rf"k_cell_fwd(_w)?<{dt}, {kind}[,>]", name):
             return "main"
         if re.search(rf"k_cell_epi<{dt}, {kind}>", name):
             return "extra"
     elif cls == "bwd_dx":
-        if re.search(rf"k_bwd_dx2<{dt}, ", name):
+        if re.search(rf"k_bwd_dx(2|_w)<{dt}[,>]", name):
             return "main"
         if "k_dx_epi" in name:
             return "extra"
     elif cls == "wgrad":
-        if re.search(r"k_wgrad_(f32|bf16)\b|k_wgrad<", name):
+        if re.search(r"k_wgrad_(f32|bf16)(_w)?\b|k_wgrad<", name):
             return "main"
     return None
 
