@@ -73,8 +73,6 @@ def rocprof_role(kernel_class: str, name: str):
     elif cls == "bwd_dx":
         if re.search(rf"k_bwd_dx(2|_w)<{dt}[,>]", name):
             return "main"
-        if "k_dx_epi" in name:
-            return "extra"
     elif cls == "wgrad":
         if re.search(r"k_wgrad_(f32|bf16)(_w)?\b|k_wgrad<", name):
             return "main"

@@ -182,22 +182,7 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
   }
   w.zpart_off = w.gates_bytes;
   w.zpart_bytes = al(zp * sizeof(float));
-  size_t xp = 0;
-  for (int g = 0; g < s.num_groups; ++g) {
-    const fold_op& op = s.ops[s.h_op[g]];
-    if (op.kind == FOLD_EMBED || op.param_set >= (int)p.sets.size()) continue;
-    const PackedSet& ps = p.sets[op.param_set];
-    const int es = p.dtype == FOLD_BF16 ? 2 : 4;
-    const int Kb = ps.G * p.HP;
-    for (int Nb : {op.arity * p.HP, op.has_input ? ps.INP : 0}) {
-      if (Nb <= 0) continue;
-      const DxPlan pl = dx_plan(s.h_rows[g], Nb, Kb, es, true);
-      if (pl.ksplit > 1) xp = std::max(xp, (size_t)pl.ksplit * s.h_rows[g] * Nb);
-    }
-  }
-  w.xpart_off = w.zpart_off + w.zpart_bytes;
-  w.xpart_bytes = al(xp * sizeof(float));
-  w.dh_off = w.xpart_off + w.xpart_bytes;
+  w.dh_off = w.zpart_off + w.zpart_bytes;
   w.dc_off = w.dh_off + al(N * p.ld * sizeof(float));
   w.acc_bytes = w.dc_off + al(N * p.ld * sizeof(float)) - w.dh_off;
   size_t part = 0, bpart = 0;
@@ -402,7 +387,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     d.in_dim = ps.in_dim;
     d.tld = tld;
     d.npar = s.pos_npar;
-    d.xpart = reinterpret_cast<float*>(wsb + L.xpart_off);
+    d.can_split = 1;
     d.zero = p.zero;
     if (op.arity > 0) {
       d.mode = 0;

@@ -557,19 +557,6 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
 
 // ---------------------------------------------------------------- backward, dz . W^T
 
-// scatter one element of dz . W^T: mode 0 into the child's dh, mode 1 into the leaf-table gradient
-__device__ __forceinline__ void dx_scatter(const DxArgs& a, int row, int n, float v) {
-  if (a.mode == 0) {
-    const int k = n / a.HP, jin = n - k * a.HP;
-    if (jin >= a.H) return;
-    const int cp = a.child_pos[a.idx_off + row * a.arity + k];
-    if (cp >= 0) scatter_add(&a.dh[(size_t)cp * a.ld + jin], v, a.npar[cp] == 1);
-  } else {
-    if (n >= a.in_dim) return;
-    const int ti = a.input_idx[a.row_begin + row];
-    unsafeAtomicAdd(&a.d_table[(size_t)ti * a.tld + n], v);
-  }
-}
 
 // dz . W^T for one tile of 128 * MT rows x 128 columns of the children's (or the input's) gradient:
 // dz rows (fp32, or bf16 at the start of each row for bf16 parameters) and the packed W^T rows are
@@ -599,7 +586,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
     kz = tx / R;
   }
   const int m0 = rt * BM, n0 = nt * BN;
-  if constexpr (!SPLIT) {
+  {
     // scatter targets of the tile's rows, published by the K loop's first barrier
     for (int i = threadIdx.x; i < 2 * BM; i += kThreads) {
       const int k = i / BM, rl = i - k * BM, row = m0 + rl;
@@ -655,16 +642,13 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
       for (int r = 0; r < 16; ++r) {
         const int rl = wave * 32 * MT + tm * 32 + acc_row(r, lane), row = m0 + rl;
         if (row >= a.rows) continue;
-        if constexpr (SPLIT) {
-          a.xpart[((size_t)kz * a.rows + row) * a.Nb + n] = acc[tm][tn][r];
-        } else {
-          const int t = tgt[k][rl];
-          if (t < 0) continue;
-          if (a.mode == 0)
-            scatter_add(&a.dh[(size_t)t * a.ld + jin], acc[tm][tn][r], sgl[k][rl]);
-          else
-            unsafeAtomicAdd(&a.d_table[(size_t)t * a.tld + jin], acc[tm][tn][r]);
-        }
+        // K slices of one element add into it concurrently: atomics whenever K is split
+        const int t = tgt[k][rl];
+        if (t < 0) continue;
+        if (a.mode == 0)
+          scatter_add(&a.dh[(size_t)t * a.ld + jin], acc[tm][tn][r], !SPLIT && sgl[k][rl]);
+        else
+          unsafeAtomicAdd(&a.d_table[(size_t)t * a.tld + jin], acc[tm][tn][r]);
       }
     }
   }
@@ -757,15 +741,6 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
   }
 }
 
-// finish a K-split dz . W^T launch: sum the slices, then scatter
-__global__ void k_dx_epi(DxArgs a, int nsplit) {
-  const int row = blockIdx.x;
-  for (int n = threadIdx.x; n < a.Nb; n += blockDim.x) {
-    float v = 0.f;
-    for (int sp = 0; sp < nsplit; ++sp) v += a.xpart[((size_t)sp * a.rows + row) * a.Nb + n];
-    dx_scatter(a, row, n, v);
-  }
-}
 
 template <typename T, int KIND>
 void cell_fwd_kind(const FwdArgs& a0, hipStream_t st) {
@@ -891,7 +866,7 @@ void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
   if (a0.rows <= 0 || a0.Nb <= 0) return;
   DxArgs a = a0;
   ProfScope prof(dtype == FOLD_BF16 ? "bwd_dx.bf16" : "bwd_dx.f32", st);
-  const DxPlan pl = dx_plan(a.rows, a.Nb, a.Kb, dtype == FOLD_BF16 ? 2 : 4, a.xpart != nullptr);
+  const DxPlan pl = dx_plan(a.rows, a.Nb, a.Kb, dtype == FOLD_BF16 ? 2 : 4, a.can_split != 0);
   if (pl.wide) {
     const int R = (int)cdiv(a.rows, wide::kRows), NT = (int)cdiv(a.Nb, 256);
     a.ksplit = 1;
@@ -918,7 +893,6 @@ void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
     else { if (split) FOLD_DX(float, 1, true); else FOLD_DX(float, 1, false); }
   }
 #undef FOLD_DX
-  if (split) hipLaunchKernelGGL(k_dx_epi, dim3(a.rows), dim3(256), 0, st, a, pl.ksplit);
 }
 
 }  // namespace fold

@@ -18,7 +18,6 @@ struct WsLayout {
   int gstride = 0;           // floats per pool row of saved gates / dz: Gmax * HP
   size_t gates_off = 0, gates_bytes = 0;
   size_t zpart_off = 0, zpart_bytes = 0;  // K-split partial sums of narrow forward levels
-  size_t xpart_off = 0, xpart_bytes = 0;  // K-split partial products of narrow dz . W^T launches
   size_t dh_off = 0, dc_off = 0, acc_bytes = 0;
   size_t part_off = 0, part_bytes = 0;   // weight-gradient partial tiles
   size_t bpart_off = 0, bpart_bytes = 0; // bias partial sums
@@ -97,8 +96,7 @@ inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bo
 }
 
 // dz . W^T tiling: wide groups use 256 x 256 tiles (8 waves); others 128 * mt rows x 128 columns, K
-// cut into ksplit slices (partial products in the workspace, summed and scattered by an epilogue
-// kernel).
+// cut into ksplit slices that add their partial products into the targets atomically.
 struct DxPlan {
   int mt = 1, ksplit = 1;
   bool wide = false;  // 256 x 256 tiles per workgroup of 8 waves
@@ -158,7 +156,7 @@ struct DxArgs {
   const int* input_idx;
   int in_dim, tld;
   const int* npar;  // parent edges per pool row
-  float* xpart;     // workspace for K-split partial products, or NULL (no split)
+  int can_split;    // K may be split across workgroups (slices add into the targets atomically)
   int ksplit;       // set by the launcher
   int map;          // set by the launcher: workgroup order over the XCDs (kMapRows, kMapCols, kMapOwnCols)
 };
