@@ -584,31 +584,37 @@ __global__ void k_bias_reduce(const float* bpart, int nparts, int Nw, int H, int
 
 }  // namespace
 
+// Chunks of an op's rows: a multiple of 8 (each XCD reduces whole chunks, all tiles of a chunk on one
+// XCD) chosen so that an XCD's workgroups fill its resident slots in whole rounds (a launch of 2.2 rounds
+// runs as 3), with chunks of at least min_rows rows.
+static int wgrad_chunks(long long tiles, int count, int min_rows, int slots_per_xcd) {
+  const long long most8 = std::max(1, count / (8 * min_rows));  // chunks per XCD at most
+  int best = 1;
+  double best_eff = 0.0;
+  for (int c8 = 1; c8 <= std::min<long long>(most8, 32); ++c8) {
+    const long long wg = tiles * c8;
+    const double eff = (double)wg / (double)(((wg + slots_per_xcd - 1) / slots_per_xcd) * slots_per_xcd);
+    if (eff > best_eff + 1e-9) {
+      best = c8;
+      best_eff = eff;
+    }
+    if (eff >= 0.9 && wg >= slots_per_xcd) break;
+  }
+  return 8 * best;
+}
+
 WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype) {
   WgradSplit w;
   if (count <= 0 || Kw <= 0 || Nw <= 0) return w;
-  // bf16 ops with many rows: 256 x 256 tiles (twice the operand reuse of 128 x 128)
+  // bf16 ops with many rows: 256 x 256 tiles (twice the operand reuse of 128 x 128), one workgroup per CU
   w.wide = dtype == FOLD_BF16 && count >= 65536;
-  if (w.wide) {
-    const long long tiles = (long long)((Kw + 255) / 256) * ((Nw + 255) / 256);
-    const long long want = std::max(8LL, ((512 + tiles - 1) / tiles + 7) / 8 * 8);
-    const long long most = std::max(1, (count + 1023) / 1024);
-    w.nchunk = (int)std::max(1LL, std::min(want, most));
-    w.chunk = round_up((count + w.nchunk - 1) / w.nchunk, 32);
-    w.nchunk = (count + w.chunk - 1) / w.chunk;
-    w.bparts = w.nchunk * 2;
-    return w;
-  }
-  const int tn = dtype == FOLD_BF16 ? 128 : kWgNW;
-  const long long tiles = (long long)((Kw + kTM - 1) / kTM) * ((Nw + tn - 1) / tn);
-  // enough workgroups to fill the chip, and chunks in multiples of the 8 XCDs (one XCD per chunk)
-  const long long want = std::max(8LL, ((1024 + tiles - 1) / tiles + 7) / 8 * 8);
-  const long long most = std::max(1, (count + 511) / 512);
-  w.nchunk = (int)std::max(1LL, std::min(want, most));
+  const long long tiles = w.wide ? (long long)((Kw + 255) / 256) * ((Nw + 255) / 256)
+                                 : (long long)((Kw + kTM - 1) / kTM) * ((Nw + 127) / 128);
+  w.nchunk = wgrad_chunks(tiles, count, w.wide ? 1024 : 512, w.wide ? 32 : 64);
   w.chunk = round_up((count + w.nchunk - 1) / w.nchunk, 64);
   w.nchunk = (count + w.chunk - 1) / w.chunk;
   // bias partial rows: one per (chunk, weight-row tile, thread group)
-  w.bparts = w.nchunk * ((Kw + kTM - 1) / kTM) * (dtype == FOLD_BF16 ? 2 : 256 / kWgNW);
+  w.bparts = w.wide ? w.nchunk * 2 : w.nchunk * ((Kw + kTM - 1) / kTM) * (dtype == FOLD_BF16 ? 2 : 256 / kWgNW);
   return w;
 }
 
