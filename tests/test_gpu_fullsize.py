@@ -77,3 +77,41 @@ def test_config5_full():
     odd = np.arange(1, w.num_graphs, 2)
     deepest = int(odd[np.argmax(sizes[odd])])
     _sampled_parity(w, [0, deepest], table_grad=True)
+
+
+def test_wide_kernels_bf16_h512_dag_with_node_gradients():
+    """A batch that sends the wide kernels through the combinations the five workloads leave out:
+    hidden 512 bf16 (two unit blocks per workgroup, 8 unit-block pairs: XCDs own column groups in the
+    forward, row-shared order in dz . W^T with 4 column tiles), leaf levels of ~157 k rows (wide
+    weight gradients of both ops, wide leaf-table gradient), caterpillar tails of a few hundred rows
+    (K-split with atomic slices), shared sub-expressions, and an upstream gradient on every node of
+    the sampled graphs.  Sampled parity as above (graph order, linearity)."""
+    w = gen.config5(num_graphs=512, hidden=512, vocab=2000, spine_range=(200, 511))
+    sizes = np.diff(w.graph_ptr)
+    odd = np.arange(1, w.num_graphs, 2)
+    sample = [2, int(odd[np.argmax(sizes[odd])])]
+    rpg = gen.roots_per_graph(w.graph_ptr, w.child_idx)
+    roff = np.concatenate([[0], np.cumsum(rpg)])
+    dh = np.zeros_like(w.dh_roots)
+    for g in sample:
+        dh[roff[g]:roff[g + 1]] = w.dh_roots[roff[g]:roff[g + 1]]
+    w.dh_roots = dh
+    gp = w.graph_ptr
+    rows = np.concatenate([np.arange(gp[g], gp[g + 1]) for g in sample])
+    dh_nodes = np.zeros((w.num_nodes, w.hidden), np.float32)
+    dh_nodes[rows] = np.random.default_rng(11).standard_normal((rows.shape[0], w.hidden)).astype(np.float32)
+    g_out = C.run_device(w, dh_nodes=dh_nodes, table_grad=True)
+    sub = gen.subset(w, sample)
+    o = C.run_oracle(sub, dh_nodes=dh_nodes[rows].astype(np.float64), table_grad=True)
+    tol = C.TOL[w.dtype]
+    errs = {k: compare.rel_err(g_out[k][rows], o[k]) for k in ("h", "c", "dh", "dc")}
+    mask = np.ones(w.num_nodes, bool)
+    mask[rows] = False
+    assert np.all(g_out["dh"][mask] == 0) and np.all(g_out["dc"][mask] == 0)
+    for s, (gg, oo) in enumerate(zip(g_out["grads"], o["grads"])):
+        for name in ("W_in", "W_rec", "bias"):
+            if gg.get(name) is not None and oo.get(name) is not None:
+                errs[f"set{s}.{name}"] = compare.rel_err(gg[name], oo[name], whole=True)
+    errs["d_table"] = compare.rel_err(g_out["d_table"], o["d_table"], whole=True)
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, (bad, errs)
