@@ -442,23 +442,32 @@ __global__ void k_op_rows(const int* pos_group, const int* g_row_begin, const in
 
 inline dim3 grid_for(long long n) { return dim3((unsigned)std::max(1LL, (n + kBlock - 1) / kBlock)); }
 
-// stream-ordered temporaries, freed at scope exit
+// Stream-ordered temporaries of one phase: the sizes are declared first (reserve), then one allocation
+// from the device's pool backs them all (commit); freed at scope exit.  One allocation per phase keeps
+// the host cost of a schedule independent of how many temporaries it uses.
 struct Temp {
   hipStream_t st;
   std::vector<void*> ptrs;
+  std::vector<std::pair<void**, size_t>> want;
+  size_t bytes = 0;
   explicit Temp(hipStream_t s) : st(s) {}
   ~Temp() {
     for (void* p : ptrs) (void)hipFreeAsync(p, st);
   }
   template <class T>
-  hipError_t alloc(T** p, size_t count) {
+  void reserve(T** p, size_t count) {
+    want.push_back({reinterpret_cast<void**>(p), bytes});
+    bytes += (std::max<size_t>(count, 1) * sizeof(T) + 255) / 256 * 256;
+  }
+  hipError_t commit() {
     void* q = nullptr;
-    hipError_t e = hipMallocAsync(&q, std::max<size_t>(count, 1) * sizeof(T), st);
-    if (e == hipSuccess) {
-      ptrs.push_back(q);
-      *p = static_cast<T*>(q);
-    }
-    return e;
+    hipError_t e = hipMallocAsync(&q, std::max<size_t>(bytes, 256), st);
+    if (e != hipSuccess) return e;
+    ptrs.push_back(q);
+    for (auto& w : want) *w.first = static_cast<char*>(q) + w.second;
+    want.clear();
+    bytes = 0;
+    return hipSuccess;
   }
 };
 
@@ -545,20 +554,29 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   s.op_inp = q; q += N;
 
   Temp tmp(st);
-  unsigned long long* err = nullptr;
-  int* meta = nullptr;       // [0] max depth, [1] max parents, [2] num groups, [3] num roots
+  // the error word and meta (max depth, max parents, num groups, num roots) side by side: one read-back
+  struct ErrMeta {
+    unsigned long long err;
+    int meta[4];
+  };
+  ErrMeta* em = nullptr;
   int* node_graph = nullptr;
   int* indeg = nullptr;
   int* scratch = nullptr;
   const long long scratch_ints = 6LL * N + G + E + 1;
-  if (tmp.alloc(&err, 1) || tmp.alloc(&meta, 4) || tmp.alloc(&node_graph, N) || tmp.alloc(&indeg, N) ||
-      tmp.alloc(&scratch, (size_t)scratch_ints)) {
+  tmp.reserve(&em, 1);
+  tmp.reserve(&node_graph, N);
+  tmp.reserve(&indeg, N);
+  tmp.reserve(&scratch, (size_t)scratch_ints);
+  if (tmp.commit() != hipSuccess) {
     set_error("fold_schedule: out of device memory (temporaries)");
     return fail(FOLD_E_NOMEM);
   }
-  if (hipMemsetAsync(err, 0xff, sizeof(unsigned long long), st) != hipSuccess ||
-      hipMemsetAsync(meta, 0, 4 * sizeof(int), st) != hipSuccess) {
-    set_error("fold_schedule: hipMemsetAsync failed");
+  unsigned long long* err = &em->err;
+  int* meta = em->meta;
+  const ErrMeta em0{~0ull, {0, 0, 0, 0}};
+  if (hipMemcpyAsync(em, &em0, sizeof(em0), hipMemcpyHostToDevice, st) != hipSuccess) {
+    set_error("fold_schedule: could not initialise the error word");
     return fail(FOLD_E_DEVICE);
   }
   hipLaunchKernelGGL(k_check_struct, grid_for(std::max(G + 1, N + 1)), dim3(kBlock), 0, st, b->graph_ptr, G,
@@ -576,12 +594,8 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
     set_error("fold_schedule: kernel launch failed");
     return fail(FOLD_E_DEVICE);
   }
-  struct {
-    unsigned long long err;
-    int meta[4];
-  } hb{};
-  if (hipMemcpyAsync(&hb.err, err, sizeof(hb.err), hipMemcpyDeviceToHost, st) != hipSuccess ||
-      hipMemcpyAsync(hb.meta, meta, sizeof(hb.meta), hipMemcpyDeviceToHost, st) != hipSuccess ||
+  ErrMeta hb{};
+  if (hipMemcpyAsync(&hb, em, sizeof(hb), hipMemcpyDeviceToHost, st) != hipSuccess ||
       hipStreamSynchronize(st) != hipSuccess) {
     set_error("fold_schedule: device error while validating");
     return fail(FOLD_E_DEVICE);
@@ -604,7 +618,23 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   }
   const size_t n2 = 4 + (size_t)(D + 1) + 6 * (size_t)cap;
   int* blob2 = nullptr;
-  if (tmp.alloc(&blob2, n2)) {
+  unsigned *ka = nullptr, *kb = nullptr;
+  int *va = nullptr, *vb = nullptr, *flag = nullptr, *exs = nullptr, *radix_counts = nullptr, *scan_tmp = nullptr;
+  const int B = (N + kRadixTile - 1) / kRadixTile;
+  const long long rc = 256LL * B;
+  const long long scan_tmp_n = std::max<long long>(std::max<long long>(rc, N), cap) / kScanTile + 2;
+  tmp.reserve(&blob2, n2);
+  if (N > 0) {
+    tmp.reserve(&ka, N);
+    tmp.reserve(&kb, N);
+    tmp.reserve(&va, N);
+    tmp.reserve(&vb, N);
+    tmp.reserve(&flag, N);
+    tmp.reserve(&exs, N);
+    tmp.reserve(&radix_counts, rc);
+    tmp.reserve(&scan_tmp, scan_tmp_n);
+  }
+  if (tmp.commit() != hipSuccess) {
     set_error("fold_schedule: out of device memory");
     return fail(FOLD_E_NOMEM);
   }
@@ -618,18 +648,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   int* d_edges = d_idx_off + cap;
 
   if (N > 0) {
-    unsigned *ka, *kb;
-    int *va, *vb, *flag, *exs, *radix_counts, *scan_tmp;
     int* gid = s.pos_group;
-    const int B = (N + kRadixTile - 1) / kRadixTile;
-    const long long rc = 256LL * B;
-    const long long scan_tmp_n = std::max<long long>(rc, N) / kScanTile + 2;
-    if (tmp.alloc(&ka, N) || tmp.alloc(&kb, N) || tmp.alloc(&va, N) || tmp.alloc(&vb, N) ||
-        tmp.alloc(&flag, N) || tmp.alloc(&exs, N) || tmp.alloc(&radix_counts, rc) ||
-        tmp.alloc(&scan_tmp, scan_tmp_n)) {
-      set_error("fold_schedule: out of device memory (sort)");
-      return fail(FOLD_E_NOMEM);
-    }
     hipLaunchKernelGGL(k_make_keys, grid_for(N), dim3(kBlock), 0, st, s.depth, b->node_op, N, K, ka, va);
     const unsigned long long max_key = (unsigned long long)D * K - 1;
     int bits = 1;
@@ -716,7 +735,9 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   std::copy(s.h_rows.begin(), s.h_rows.end(), pp + 3 * ngc);
   std::copy(s.h_idx_off.begin(), s.h_idx_off.end(), pp + 4 * ngc);
   std::copy(oprow_off.begin(), oprow_off.end(), pp + 5 * ngc);
-  if (hipMemcpy(blob3, pack.data(), n3 * sizeof(int), hipMemcpyHostToDevice) != hipSuccess) {
+  // stream-ordered upload (a pageable source is staged before the call returns); the final
+  // synchronisation below covers it
+  if (hipMemcpyAsync(blob3, pack.data(), n3 * sizeof(int), hipMemcpyHostToDevice, st) != hipSuccess) {
     set_error("fold_schedule: copy of the group table failed");
     return fail(FOLD_E_DEVICE);
   }
@@ -731,10 +752,10 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   if (N > 0) {
     hipLaunchKernelGGL(k_op_rows, grid_for(N), dim3(kBlock), 0, st, s.pos_group, s.g_row_begin, g_oprow, s.g_op,
                        s.g_idx_off, s.child_pos, s.input_idx, ops, N, s.op_rows, s.op_cpos, s.op_inp);
-    if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess) {
-      set_error("fold_schedule: device error while listing rows per op");
-      return fail(FOLD_E_DEVICE);
-    }
+  }
+  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess) {
+    set_error("fold_schedule: device error while listing rows per op");
+    return fail(FOLD_E_DEVICE);
   }
   *out = h;
   return FOLD_OK;
