@@ -157,6 +157,123 @@ def flops_by_kernel(w, sched_host, table_grad: bool) -> dict:
     return out
 
 
+NARROW_S = 2e-6  # a level pass whose roofline time is below this is reported as time per pass
+
+
+def pass_work(w, host, table_grad: bool) -> dict:
+    """Algorithmic FLOPs and HBM bytes of every level pass of one step (weights counted once per pass).
+
+    Keys: ("fwd", group), ("bwd", group) -- the cell's backward and dz . W^T of one (depth, op) group --
+    and ("wgrad", op), the deferred weight-gradient contraction of one operation over all its rows.
+    Per node, with S = state bytes (h, plus fp32 c for cells that carry one) and S_g = its fp32
+    gradient: forward reads the input row and the children's states and writes S; backward reads S_g
+    and the children's states and writes the children's S_g (plus the leaf-table gradient row).
+    Saved activations are implementation overhead, not counted."""
+    from paper_1702_02181_amd import gen
+    H = w.hidden
+    bh = 2 if w.dtype == "bf16" else 4
+    out = {}
+    op_rows = {}
+    for g, (op_id, rows) in enumerate(zip(host["group_op"], host["group_rows"])):
+        op, rows = w.ops[int(op_id)], int(rows)
+        op_rows[int(op_id)] = op_rows.get(int(op_id), 0) + rows
+        if op.kind == gen.KIND_EMBED:
+            out[("fwd", g)] = (0.0, float(rows * 2 * H * bh))
+            if w.backward and table_grad:
+                out[("bwd", g)] = (0.0, float(rows * 4 * H))
+            continue
+        G = gen.NUM_GATES[op.kind]
+        din = w.params[op.param_set].in_dim if op.has_input else 0
+        has_c = op.kind in (gen.KIND_TREELSTM, gen.KIND_LSTM, gen.KIND_PROJ)
+        s_node = H * (bh + (4 if has_c else 0))
+        sg_node = 4 * H * (2 if has_c else 1)
+        k_in = din + op.arity * H
+        out[("fwd", g)] = (2.0 * rows * k_in * G * H,
+                           float(rows * (din * bh + op.arity * s_node + s_node) + k_in * G * H * bh + G * H * 4))
+        if w.backward:
+            k_dx = op.arity * H + (din if table_grad else 0)
+            out[("bwd", g)] = (2.0 * rows * G * H * k_dx,
+                               float(rows * (sg_node + op.arity * (s_node + sg_node) + (din * 4 if table_grad else 0))
+                                     + k_dx * G * H * bh))
+    if w.backward:
+        for o, count in op_rows.items():
+            op = w.ops[o]
+            if op.kind == gen.KIND_EMBED:
+                continue
+            G = gen.NUM_GATES[op.kind]
+            k_in = (w.params[op.param_set].in_dim if op.has_input else 0) + op.arity * H
+            out[("wgrad", o)] = (2.0 * count * k_in * G * H,
+                                 float(count * (k_in + G * H) * bh + (k_in + 1) * G * H * 4))
+    return out
+
+
+def pass_of(name: str, group: int, op: int):
+    """The level pass a profiled launch belongs to (None: set-up, roots)."""
+    cls = class_of(name)
+    if group >= 0 and cls in ("cell_fwd", "embed_fwd"):
+        return ("fwd", group)
+    if group >= 0 and cls in ("cell_bwd", "bwd_dx"):
+        return ("bwd", group)
+    if group < 0 and op >= 0 and cls in ("wgrad", "wgrad_reduce", "bias_partial", "bias_reduce"):
+        return ("wgrad", op)
+    return None
+
+
+def level_classes(work: dict, launches: list, steps: int, peak_tflops: float, hbm_gbs: float) -> dict:
+    """Roofline per class of level pass.  A pass is MFMA-bound ("wide") when its FLOPs at the matrix
+    peak take at least as long as its bytes at the HBM peak, else "gather"-bound; a pass whose roofline
+    time is under NARROW_S is "narrow" and reported as time per pass.  frac = sum of roofline times /
+    sum of measured times over the class (time-weighted); also split by pass kind."""
+    meas = {}
+    other = 0.0
+    for name, group, op, ms in launches:
+        key = pass_of(name, group, op)
+        if key is None:
+            other += ms
+        else:
+            meas[key] = meas.get(key, 0.0) + ms / steps
+    cls = {c: {"passes": 0, "ms_per_step": 0.0, "roofline_ms": 0.0, "flops": 0.0, "bytes": 0.0, "by_pass": {}}
+           for c in ("wide", "gather", "narrow")}
+    for key, (F, B) in work.items():
+        if key not in meas:
+            continue
+        t_m, t_h = F / (peak_tflops * 1e12), B / (hbm_gbs * 1e9)
+        roof = max(t_m, t_h)
+        c = "narrow" if roof < NARROW_S else ("wide" if t_m >= t_h else "gather")
+        d = cls[c]
+        d["passes"] += 1
+        d["ms_per_step"] += meas[key]
+        d["roofline_ms"] += roof * 1e3
+        d["flops"] += F
+        d["bytes"] += B
+        bp = d["by_pass"].setdefault(key[0], [0, 0.0, 0.0])
+        bp[0] += 1
+        bp[1] += meas[key]
+        bp[2] += roof * 1e3
+    out = {}
+    for c, d in cls.items():
+        if d["passes"] == 0:
+            continue
+        t = d["ms_per_step"] * 1e-3
+        e = {"passes": d["passes"], "ms_per_step": round(d["ms_per_step"], 4)}
+        if c == "narrow":
+            e["us_per_pass"] = round(d["ms_per_step"] * 1e3 / d["passes"], 2)
+        else:
+            e["bound"] = "mfma" if c == "wide" else "hbm"
+            e["frac"] = round(d["roofline_ms"] / d["ms_per_step"], 4)
+            if c == "wide":
+                e["achieved_tflops"] = round(d["flops"] / t / 1e12, 1)
+                e["peak_tflops"] = peak_tflops
+            else:
+                e["achieved_gbs"] = round(d["bytes"] / t / 1e9, 1)
+                e["peak_gbs"] = hbm_gbs
+            e["by_pass"] = {k: {"passes": v[0], "ms_per_step": round(v[1], 4), "frac": round(v[2] / v[1], 4)}
+                            for k, v in sorted(d["by_pass"].items())}
+        out[c] = e
+    out["other_ms_per_step"] = round(other / steps, 4)
+    return out
+
+
 def cpu_baseline(w, budget_s: float):
     """The oracle as it stands, single thread, on whole graphs of the workload until ~budget_s."""
     from threadpoolctl import threadpool_limits
@@ -291,8 +408,12 @@ def main():
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
-    stats = F.fold_profile_read()
+    launch_times = F.fold_profile_read_launches()
     F.fold_profile_enable(False)
+    stats = {}
+    for name, _g, _o, ms in launch_times:
+        n, tot, mx = stats.get(name, (0, 0.0, 0.0))
+        stats[name] = (n + 1, tot + ms, max(mx, ms))
     flops = flops_by_kernel(w, host, table_grad)
     kernels = {}
     for name, (launches, total_ms, max_ms) in stats.items():
@@ -319,6 +440,7 @@ def main():
                     "avg_launch_us": round(avg_s * 1e6, 2)}
     total_flops = sum(flops.values())
     step_peak = PEAKS["bf16_mfma_tflops"] if w.dtype == "bf16" else PEAKS["f32_mfma_tflops"]
+    classes = level_classes(pass_work(w, host, table_grad), launch_times, args.steps, step_peak, PEAKS["hbm_gbs"])
 
     cpu = None
     if not args.no_cpu and not args.profile_only:
@@ -347,6 +469,7 @@ def main():
         "peaks": {"datasheet": PEAKS, "measured": probes},
         "roofline": roofline,
         "step_mfma_frac": round(total_flops / (ms_per_step * 1e-3) / 1e12 / step_peak, 4),
+        "level_classes": classes,
         "kernels": kernels,
         "cpu_baseline": cpu,
     }

@@ -309,6 +309,25 @@ typedef struct {
 int32_t fold_profile_enable(int32_t on);
 int32_t fold_profile_read(fold_kernel_stat* out, int32_t capacity, int32_t* count);
 
+/* The same records one by one, in launch order, each with the schedule group
+ * it ran for (its index in the group table; -1 for launches of no single
+ * group: gradient set-up, roots, the per-operation weight gradients) and its
+ * operation id (-1 if none).  This splits a step's time by level and by
+ * (depth, op) group (Section 2: one batched operation per group).
+ * Writes min(capacity, records) entries to `out` (caller-owned host array),
+ * sets *count to the number of records taken, and clears them all, as
+ * fold_profile_read does.  With capacity 0 (`out` may be NULL) it only sets
+ * *count and keeps the records.  FOLD_E_INVALID for NULL arguments;
+ * FOLD_E_DEVICE if an event could not be read. */
+typedef struct {
+  char name[48];
+  int32_t group;
+  int32_t op;
+  double ms;
+} fold_launch_time;
+
+int32_t fold_profile_read_launches(fold_launch_time* out, int32_t capacity, int32_t* count);
+
 /* ---- achievable peaks (diagnostics) --------------------------------------
  * fold_probe_mfma times a loop of independent 32x32 MFMA instructions
  * (fp32 32x32x2 or bf16 32x32x16) on every compute unit and returns the

@@ -31,8 +31,10 @@ std::atomic<bool> g_prof_on{false};
 std::mutex g_prof_mu;
 struct ProfRec {
   std::string name;
+  int group, op;
   hipEvent_t a, b;
 };
+thread_local int g_tag_group = -1, g_tag_op = -1;
 std::vector<ProfRec> g_prof_recs;
 std::vector<hipEvent_t> g_prof_free;
 
@@ -55,6 +57,11 @@ thread_local bool g_capturing = false;  // launches are being recorded into a gr
 
 void set_capturing(bool on) { g_capturing = on; }
 
+void prof_tag(int group, int op) {
+  g_tag_group = group;
+  g_tag_op = op;
+}
+
 ProfScope::ProfScope(const char* name, hipStream_t st) : name_(name), st_(st) {
   if (!g_prof_on.load(std::memory_order_relaxed) || g_capturing) return;
   hipEvent_t a = prof_event(), b = prof_event();
@@ -68,7 +75,8 @@ ProfScope::~ProfScope() {
   if (!start_) return;
   (void)hipEventRecord(static_cast<hipEvent_t>(stop_), st_);
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  g_prof_recs.push_back({name_, static_cast<hipEvent_t>(start_), static_cast<hipEvent_t>(stop_)});
+  g_prof_recs.push_back(
+      {name_, g_tag_group, g_tag_op, static_cast<hipEvent_t>(start_), static_cast<hipEvent_t>(stop_)});
 }
 
 namespace {
@@ -278,9 +286,15 @@ void packed_destroy_impl(fold_packed* h) {
   delete h;
 }
 
+// clears the launch tag when a pass returns, whichever way it returns
+struct TagScope {
+  ~TagScope() { prof_tag(-1, -1); }
+};
+
 int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, void* h_pool,
                      float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st) {
   const WsLayout L = workspace_layout(s, p);
+  TagScope tags;
   float* gates = nullptr;
   float* zpart = nullptr;
   if (ws) {
@@ -293,6 +307,7 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
   for (int g = 0; g < s.num_groups; ++g) {
     const fold_op& op = s.ops[s.h_op[g]];
     const PackedSet& ps = p.sets[op.param_set];
+    prof_tag(g, s.h_op[g]);
     if (op.kind == FOLD_EMBED) {
       launch_embed_fwd(p.dtype, s.h_rows[g], s.h_row_begin[g], p.H, p.ld, tld, table, s.input_idx, h_pool, c_pool, st);
       continue;
@@ -323,6 +338,7 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
     a.zpart = zpart;
     launch_cell_fwd(p.dtype, op.kind, a, st);
   }
+  prof_tag(-1, -1);
   if (roots_out) launch_roots(p.dtype, s.R, p.ld, s.root_pos, h_pool, roots_out, st);
   (void)table_rows;
   if (hipGetLastError() != hipSuccess) return fail(FOLD_E_DEVICE, "fold_forward: kernel launch failed");
@@ -334,6 +350,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
                       float* dh_out, float* dc_out, void* ws, size_t ws_bytes, hipStream_t st) {
   const WsLayout L = workspace_layout(s, p);
   if (!ws || ws_bytes < L.bwd_bytes) return fail(FOLD_E_MISMATCH, "fold_backward: workspace too small");
+  TagScope tags;
   char* wsb = static_cast<char*>(ws);
   float* gates = reinterpret_cast<float*>(wsb + L.gates_off);
   float* dh = dh_out ? dh_out : reinterpret_cast<float*>(wsb + L.dh_off);
@@ -348,6 +365,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
   for (int g = s.num_groups - 1; g >= 0; --g) {
     const fold_op& op = s.ops[s.h_op[g]];
     const PackedSet& ps = p.sets[op.param_set];
+    prof_tag(g, s.h_op[g]);
     BwdCellArgs b;
     b.rows = s.h_rows[g];
     b.row_begin = s.h_row_begin[g];
@@ -407,6 +425,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     for (int o = 0; o < s.num_ops; ++o) {
       const fold_op& op = s.ops[o];
       if (op.kind == FOLD_EMBED) continue;
+      prof_tag(-1, o);
       const int count = s.h_op_row_ptr[o + 1] - s.h_op_row_ptr[o];
       if (count <= 0) continue;
       const PackedSet& ps = p.sets[op.param_set];
@@ -473,6 +492,29 @@ using namespace fold;
     return fail(FOLD_E_INVALID, "internal error");                          \
   }
 
+namespace {
+// Takes every profiling record made so far, waits for its events, returns the durations (ms) and
+// recycles the events.  Returns FOLD_E_DEVICE if an event could not be read (its duration is 0).
+int32_t drain_prof(std::vector<fold::ProfRec>& recs, std::vector<float>& ms) {
+  {
+    std::lock_guard<std::mutex> lk(fold::g_prof_mu);
+    recs.swap(fold::g_prof_recs);
+  }
+  int32_t rc = FOLD_OK;
+  ms.assign(recs.size(), 0.f);
+  for (size_t i = 0; i < recs.size(); ++i) {
+    if (hipEventSynchronize(recs[i].b) != hipSuccess || hipEventElapsedTime(&ms[i], recs[i].a, recs[i].b) != hipSuccess)
+      rc = FOLD_E_DEVICE;
+  }
+  std::lock_guard<std::mutex> lk(fold::g_prof_mu);
+  for (auto& r : recs) {
+    fold::g_prof_free.push_back(r.a);
+    fold::g_prof_free.push_back(r.b);
+  }
+  return rc;
+}
+}  // namespace
+
 extern "C" {
 
 const char* fold_last_error(void) { return fold::g_last_error.c_str(); }
@@ -504,16 +546,13 @@ int32_t fold_profile_read(fold_kernel_stat* out, int32_t capacity, int32_t* coun
   FOLD_GUARD_BEGIN
   if (!count || (capacity > 0 && !out)) return fail(FOLD_E_INVALID, "fold_profile_read: NULL argument");
   std::vector<fold::ProfRec> recs;
-  {
-    std::lock_guard<std::mutex> lk(fold::g_prof_mu);
-    recs.swap(fold::g_prof_recs);
-  }
+  std::vector<float> dur;
+  const int32_t rc = drain_prof(recs, dur);
   std::map<std::string, fold_kernel_stat> agg;
   std::vector<std::string> order;
-  int32_t rc = FOLD_OK;
-  for (auto& r : recs) {
-    float ms = 0.f;
-    if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) rc = FOLD_E_DEVICE;
+  for (size_t i = 0; i < recs.size(); ++i) {
+    const auto& r = recs[i];
+    const float ms = dur[i];
     auto it = agg.find(r.name);
     if (it == agg.end()) {
       fold_kernel_stat st{};
@@ -525,13 +564,6 @@ int32_t fold_profile_read(fold_kernel_stat* out, int32_t capacity, int32_t* coun
     it->second.total_ms += ms;
     it->second.max_ms = std::max(it->second.max_ms, (double)ms);
   }
-  {
-    std::lock_guard<std::mutex> lk(fold::g_prof_mu);
-    for (auto& r : recs) {
-      fold::g_prof_free.push_back(r.a);
-      fold::g_prof_free.push_back(r.b);
-    }
-  }
   int32_t n = 0;
   for (const auto& name : order) {
     if (n < capacity) out[n] = agg[name];
@@ -539,6 +571,32 @@ int32_t fold_profile_read(fold_kernel_stat* out, int32_t capacity, int32_t* coun
   }
   *count = n;
   if (rc != FOLD_OK) return fail(rc, "fold_profile_read: event query failed");
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
+int32_t fold_profile_read_launches(fold_launch_time* out, int32_t capacity, int32_t* count) {
+  FOLD_GUARD_BEGIN
+  if (!count || (capacity > 0 && !out)) return fail(FOLD_E_INVALID, "fold_profile_read_launches: NULL argument");
+  if (capacity == 0) {  // count only; the records stay
+    std::lock_guard<std::mutex> lk(fold::g_prof_mu);
+    *count = (int32_t)fold::g_prof_recs.size();
+    return FOLD_OK;
+  }
+  std::vector<fold::ProfRec> recs;
+  std::vector<float> dur;
+  const int32_t rc = drain_prof(recs, dur);
+  const int32_t n = (int32_t)recs.size();
+  for (int32_t i = 0; i < n && i < capacity; ++i) {
+    fold_launch_time t{};
+    std::strncpy(t.name, recs[i].name.c_str(), sizeof(t.name) - 1);
+    t.group = recs[i].group;
+    t.op = recs[i].op;
+    t.ms = dur[i];
+    out[i] = t;
+  }
+  *count = n;
+  if (rc != FOLD_OK) return fail(rc, "fold_profile_read_launches: event query failed");
   return FOLD_OK;
   FOLD_GUARD_END
 }

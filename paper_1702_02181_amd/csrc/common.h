@@ -52,6 +52,10 @@ void clear_error();
 
 // ---------------------------------------------------------------- kernel timing
 
+// Schedule group and op that the launches issued next on this thread belong to (-1: none); kept
+// with every profiling record.
+void prof_tag(int group, int op);
+
 // Records a HIP event pair around the launches made while it is alive, if profiling is on.
 class ProfScope {
  public:

@@ -92,6 +92,10 @@ class fold_kernel_stat(ctypes.Structure):
                 ("max_ms", ctypes.c_double)]
 
 
+class fold_launch_time(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("group", c_int32), ("op", c_int32), ("ms", ctypes.c_double)]
+
+
 class FoldError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"{ERRORS.get(code, code)}: {msg}")
@@ -101,6 +105,7 @@ class FoldError(RuntimeError):
 EXPORTS = ["fold_schedule", "fold_sched_get_info", "fold_sched_free", "fold_pack_params",
            "fold_packed_free", "fold_row_ld", "fold_workspace_size", "fold_forward",
            "fold_backward", "fold_last_error", "fold_profile_enable", "fold_profile_read",
+           "fold_profile_read_launches",
            "fold_probe_mfma", "fold_probe_copy", "fold_graph_create", "fold_graph_launch",
            "fold_graph_num_nodes", "fold_graph_free"]
 
@@ -150,6 +155,8 @@ def lib():
     L.fold_profile_enable.argtypes = [c_int32]
     L.fold_profile_read.restype = c_int32
     L.fold_profile_read.argtypes = [POINTER(fold_kernel_stat), c_int32, POINTER(c_int32)]
+    L.fold_profile_read_launches.restype = c_int32
+    L.fold_profile_read_launches.argtypes = [POINTER(fold_launch_time), c_int32, POINTER(c_int32)]
     L.fold_probe_mfma.restype = c_int32
     L.fold_probe_mfma.argtypes = [c_int32, c_void_p, POINTER(ctypes.c_double)]
     L.fold_probe_copy.restype = c_int32
@@ -179,6 +186,17 @@ def fold_profile_read() -> dict:
     _check(lib().fold_profile_read(arr, cap, byref(n)))
     return {arr[i].name.decode(): (int(arr[i].launches), float(arr[i].total_ms), float(arr[i].max_ms))
             for i in range(min(n.value, cap))}
+
+
+def fold_profile_read_launches() -> list:
+    """[(kernel class, group, op, ms)] in launch order; waits for the recorded events and clears them."""
+    n = c_int32()
+    _check(lib().fold_profile_read_launches(None, 0, byref(n)))  # count only
+    cap = n.value
+    arr = (fold_launch_time * max(cap, 1))()
+    _check(lib().fold_profile_read_launches(arr, cap, byref(n)) if cap else 0)
+    return [(arr[i].name.decode(), int(arr[i].group), int(arr[i].op), float(arr[i].ms))
+            for i in range(min(n.value, cap))]
 
 
 def fold_probe_mfma(dtype: int, stream=None) -> float:

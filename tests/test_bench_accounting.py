@@ -1,0 +1,83 @@
+"""Host logic of bench.py's per-level-pass roofline: the work of each pass and its class."""
+import types
+
+import pytest
+
+import bench
+from paper_1702_02181_amd import gen
+
+
+def _treelstm_workload(H, dtype, backward=True):
+    return types.SimpleNamespace(
+        hidden=H, dtype=dtype, backward=backward,
+        ops=[gen.OpSpec(gen.KIND_TREELSTM, 0, 1, 0), gen.OpSpec(gen.KIND_TREELSTM, 2, 0, 0)],
+        params=[types.SimpleNamespace(in_dim=H)])
+
+
+def test_pass_work_treelstm_counts():
+    H = 64
+    w = _treelstm_workload(H, "f32")
+    host = dict(group_op=[0, 1], group_rows=[4, 2])
+    work = bench.pass_work(w, host, table_grad=False)
+    S, Sg = 8 * H, 8 * H  # fp32 h + fp32 c; fp32 gradients of both
+    # leaf: 4 rows, input width H, 5 gates
+    assert work[("fwd", 0)] == (2.0 * 4 * H * 5 * H, 4 * (4 * H + S) + H * 5 * H * 4 + 5 * H * 4)
+    # leaf backward without a trainable table: only the cell's elementwise part
+    assert work[("bwd", 0)] == (0.0, 4 * Sg)
+    # internal: 2 rows, two children
+    assert work[("fwd", 1)] == (2.0 * 2 * 2 * H * 5 * H, 2 * (2 * S + S) + 2 * H * 5 * H * 4 + 5 * H * 4)
+    assert work[("bwd", 1)] == (2.0 * 2 * 5 * H * 2 * H, 2 * (Sg + 2 * (S + Sg)) + 2 * H * 5 * H * 4)
+    # weight gradients per op over all its rows
+    assert work[("wgrad", 0)][0] == 2.0 * 4 * H * 5 * H
+    assert work[("wgrad", 1)][0] == 2.0 * 2 * 2 * H * 5 * H
+
+
+def test_pass_work_bf16_state_bytes_and_table_grad():
+    H = 32
+    w = _treelstm_workload(H, "bf16")
+    host = dict(group_op=[0], group_rows=[3])
+    work = bench.pass_work(w, host, table_grad=True)
+    S = H * (2 + 4)  # bf16 h, fp32 c
+    assert work[("fwd", 0)][1] == 3 * (2 * H + S) + H * 5 * H * 2 + 5 * H * 4
+    # with a trainable table the leaf backward contracts dz with W_in^T and writes the table row
+    assert work[("bwd", 0)] == (2.0 * 3 * 5 * H * H, 3 * (8 * H + 4 * H) + H * 5 * H * 2)
+
+
+def test_pass_of_routes_launches():
+    assert bench.pass_of("cell_fwd.treelstm.f32", 3, 1) == ("fwd", 3)
+    assert bench.pass_of("embed_fwd", 0, 0) == ("fwd", 0)
+    assert bench.pass_of("cell_bwd.treelstm", 3, 1) == ("bwd", 3)
+    assert bench.pass_of("bwd_dx.bf16", 2, 1) == ("bwd", 2)
+    assert bench.pass_of("wgrad.bf16", -1, 1) == ("wgrad", 1)
+    assert bench.pass_of("wgrad_reduce", -1, 0) == ("wgrad", 0)
+    assert bench.pass_of("bwd_init", -1, -1) is None
+    assert bench.pass_of("roots", -1, -1) is None
+
+
+def test_level_classes_split_and_fractions():
+    P, BW = 100.0, 1000.0  # TFLOP/s, GB/s
+    work = {
+        ("fwd", 0): (1e9, 1e6),     # 10 us of MFMA vs 1 us of HBM: wide
+        ("fwd", 1): (1e6, 1e7),     # 0.01 us vs 10 us: gather
+        ("bwd", 1): (1e6, 1e3),     # roofline 0.01 us: narrow
+        ("wgrad", 0): (2e9, 1e6),   # 20 us: wide
+    }
+    steps = 2
+    launches = [
+        ("cell_fwd.treelstm.f32", 0, 0, 0.020), ("cell_fwd.treelstm.f32", 0, 0, 0.020),   # 20 us a step
+        ("cell_fwd.treelstm.f32", 1, 1, 0.025), ("cell_fwd.treelstm.f32", 1, 1, 0.025),   # 25 us
+        ("cell_bwd.treelstm", 1, 1, 0.004), ("cell_bwd.treelstm", 1, 1, 0.004),           # 4 us
+        ("wgrad.f32", -1, 0, 0.015), ("wgrad_reduce", -1, 0, 0.005),                      # 20 us a step
+        ("wgrad.f32", -1, 0, 0.015), ("wgrad_reduce", -1, 0, 0.005),
+        ("bwd_init", -1, -1, 0.002), ("bwd_init", -1, -1, 0.002),
+    ]
+    c = bench.level_classes(work, launches, steps, P, BW)
+    assert c["wide"]["passes"] == 2
+    assert c["wide"]["ms_per_step"] == pytest.approx(0.040)
+    assert c["wide"]["frac"] == pytest.approx((0.010 + 0.020) / 0.040)
+    assert c["wide"]["by_pass"]["fwd"]["frac"] == pytest.approx(0.5)
+    assert c["wide"]["by_pass"]["wgrad"]["frac"] == pytest.approx(1.0)
+    assert c["gather"]["passes"] == 1 and c["gather"]["frac"] == pytest.approx(0.010 / 0.025)
+    assert c["gather"]["achieved_gbs"] == pytest.approx(1e7 / 25e-6 / 1e9, rel=1e-3)
+    assert c["narrow"]["passes"] == 1 and c["narrow"]["us_per_pass"] == pytest.approx(4.0)
+    assert c["other_ms_per_step"] == pytest.approx(0.002)

@@ -162,3 +162,42 @@ def test_graph_argument_errors():
     F.fold_graph_launch(h)
     torch.cuda.synchronize()
     F.fold_graph_free(h)
+
+
+def test_profile_launch_records_carry_group_and_op():
+    """Per-launch timing records name the (depth, op) group of every forward and backward cell launch in
+    schedule order (backward in reverse), and the op of every weight-gradient launch."""
+    import torch
+    from paper_1702_02181_amd.runner import DeviceRun
+    w = gen.config4(num_graphs=6)
+    dev = DeviceRun(w)
+    dev.alloc_grads(False)
+    dev.set_upstream(w.dh_roots)
+    host = dev.sched.host_groups()
+    ng = len(host["group_op"])
+    dev.forward()
+    torch.cuda.synchronize()
+    F.fold_profile_read_launches()  # drop anything recorded before
+    F.fold_profile_enable(True)
+    try:
+        dev.zero_grads()
+        dev.forward()
+        dev.backward()
+        torch.cuda.synchronize()
+        recs = F.fold_profile_read_launches()
+    finally:
+        F.fold_profile_enable(False)
+    assert F.fold_profile_read_launches() == []
+    fwd = [(g, o) for n, g, o, _ in recs if n.startswith("cell_fwd.")]
+    assert fwd == [(g, int(host["group_op"][g])) for g in range(ng)]
+    bwd_cell = [(g, o) for n, g, o, _ in recs if n.startswith("cell_bwd.")]
+    assert bwd_cell == [(g, int(host["group_op"][g])) for g in reversed(range(ng))]
+    for n, g, o, ms in recs:
+        assert ms >= 0.0
+        if n.startswith("bwd_dx."):
+            assert 0 <= g < ng and o == int(host["group_op"][g])
+        if n.startswith("wgrad"):
+            assert g == -1 and 0 <= o < len(w.ops)
+        if n in ("bwd_init", "roots", "zero_grads"):
+            assert g == -1 and o == -1
+    assert {o for n, g, o, _ in recs if n.startswith("wgrad.")} == {int(x) for x in set(host["group_op"])}
