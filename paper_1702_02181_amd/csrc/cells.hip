@@ -656,7 +656,8 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
 
 // dz . W^T on wide levels: 256 rows x 256 columns per workgroup of 8 waves (each 64 x 128), 64-byte K
 // stages, three in flight (see wide.h).  Waves 0-3 issue the loads: 4 instructions of dz rows and 4 of
-// W^T rows each.
+// W^T rows each.  With gridDim.y = ksplit > 1 workgroup (x, y) takes the y-th slice of the K stages and
+// adds its partial product into the targets atomically (mid-size levels, too few tiles to fill the GPU).
 template <typename T>
 __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
   constexpr int BM = wide::kRows, BN = 256, TM = 2, TN = 4, NL = 8;
@@ -689,7 +690,9 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
   }
   // published by the K loop's first barrier
 
-  const int nst = a.Kb * (int)sizeof(T) / 64;
+  const int nst_all = a.Kb * (int)sizeof(T) / 64, per = (nst_all + a.ksplit - 1) / a.ksplit;
+  const int c0 = min(nst_all, (int)blockIdx.y * per), nst = min(nst_all, c0 + per) - c0;
+  const bool split = a.ksplit > 1;
   const bool loads = wave < 4;
   const char* zero = static_cast<const char*>(a.zero);
   const char* wb = static_cast<const char*>(a.Wb);
@@ -711,9 +714,11 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
   for (int i = 0; i < 4; ++i) {
     const int lu16 = wide::lane_unit(lane) * 16;
     const int row = m0 + 64 * wr + 16 * i + wide::lane_row(lane);
-    issue.ap[i] = (row < a.rows ? reinterpret_cast<const char*>(a.dz + (size_t)(a.row_begin + row) * a.gstride) : zero) + lu16;
+    issue.ap[i] = (row < a.rows ? reinterpret_cast<const char*>(a.dz + (size_t)(a.row_begin + row) * a.gstride) +
+                                      c0 * 64
+                                : zero) + lu16;
     const int n = n0 + 64 * wr + 16 * i + wide::lane_row(lane);
-    issue.bp[i] = (n < a.Nb ? wb + (size_t)n * a.Kb * sizeof(T) : zero) + lu16;
+    issue.bp[i] = (n < a.Nb ? wb + (size_t)n * a.Kb * sizeof(T) + c0 * 64 : zero) + lu16;
   }
   f32x16 acc[TM][TN];
   zero_acc(acc);
@@ -733,7 +738,7 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
         const int t = tgt[k][rl];
         if (t < 0) continue;
         if (a.mode == 0)
-          scatter_add(&a.dh[(size_t)t * a.ld + jin], acc[tm][tn][r], sgl[k][rl]);
+          scatter_add(&a.dh[(size_t)t * a.ld + jin], acc[tm][tn][r], !split && sgl[k][rl]);
         else
           unsafeAtomicAdd(&a.d_table[(size_t)t * a.tld + jin], acc[tm][tn][r]);
       }
@@ -869,9 +874,10 @@ void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
   const DxPlan pl = dx_plan(a.rows, a.Nb, a.Kb, dtype == FOLD_BF16 ? 2 : 4, a.can_split != 0);
   if (pl.wide) {
     const int R = (int)cdiv(a.rows, wide::kRows), NT = (int)cdiv(a.Nb, 256);
-    a.ksplit = 1;
+    a.ksplit = pl.ksplit;
     a.map = NT % 8 == 0 ? kMapOwnCols : kMapRows;
-    dim3 grid(a.map == kMapOwnCols ? NT * R : xcd_grid(NT, R));
+    // K slices along y: gridDim.x is a multiple of 8, so every slice of a tile runs on the tile's XCD
+    dim3 grid(a.map == kMapOwnCols ? NT * R : xcd_grid(NT, R), pl.ksplit);
     if (dtype == FOLD_BF16)
       hipLaunchKernelGGL(k_bwd_dx_w<uint16_t>, grid, dim3(wide::kThreads), 0, st, a);
     else

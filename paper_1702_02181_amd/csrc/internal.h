@@ -95,8 +95,8 @@ inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bo
   return p;
 }
 
-// dz . W^T tiling: wide groups use 256 x 256 tiles (8 waves); others 128 * mt rows x 128 columns, K
-// cut into ksplit slices that add their partial products into the targets atomically.
+// dz . W^T tiling: wide groups use 256 x 256 tiles (8 waves); others 128 * mt rows x 128 columns.  In
+// both, K may be cut into ksplit slices that add their partial products into the targets atomically.
 struct DxPlan {
   int mt = 1, ksplit = 1;
   bool wide = false;  // 256 x 256 tiles per workgroup of 8 waves
@@ -106,10 +106,19 @@ inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
   const int nst = Kb / BK;
   const long long nb = (Nb + 127) / 128;
   DxPlan p;
-  // wide tiles once they give every compute unit a workgroup (narrower levels: the K-split of
-  // partial sums through the workspace costs more than a wide tile gains)
-  p.wide = ((long long)(rows + 255) / 256) * ((Nb + 255) / 256) >= 256;
+  // wide tiles once they give every compute unit a workgroup
+  const long long wt = ((long long)(rows + 255) / 256) * ((Nb + 255) / 256);
+  p.wide = wt >= 256;
   if (p.wide) return p;
+  // bf16 levels whose wide tiles fill at least half the compute units, with a long K (at least 64
+  // stages of 64 bytes): wide tiles with K cut in two (measured: faster than the narrow tiles there;
+  // more slices, narrower levels or shorter K lose more to the atomic adds of the slices than the wide
+  // tiles gain)
+  if (can_split && esize == 2 && wt * 2 >= 256 && Kb * esize / 64 >= 64) {
+    p.wide = true;
+    p.ksplit = 2;
+    return p;
+  }
   // fp32: 128-row tiles, two workgroups per compute unit; bf16: 256-row tiles on wide levels
   p.mt = esize == 4 ? 1 : (((long long)(rows + 255) / 256) * nb >= 256 ? 2 : 1);
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * nb;

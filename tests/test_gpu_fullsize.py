@@ -115,3 +115,20 @@ def test_wide_kernels_bf16_h512_dag_with_node_gradients():
     errs["d_table"] = compare.rel_err(g_out["d_table"], o["d_table"], whole=True)
     bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, (bad, errs)
+
+
+def test_wide_dx_two_k_slices_bf16():
+    """dz . W^T of bf16 levels whose 256 x 256 tiles fill between half and all of the compute units runs as
+    wide tiles with K in two slices added atomically into the children's dh.  H = 512 balanced-tree levels
+    of 8-16 k rows have 128-255 such tiles.  Sampled parity as above."""
+    from paper_1702_02181_amd.runner import DeviceRun
+    w = gen.config5(num_graphs=256, hidden=512, vocab=2000, spine_range=(200, 511))
+    dev = DeviceRun(w)
+    host = dev.sched.host_groups()
+    del dev
+    nt = (2 * w.hidden + 255) // 256
+    tiles = [((int(r) + 255) // 256) * nt for r, op in zip(host["group_rows"], host["group_op"])
+             if w.ops[int(op)].arity == 2]
+    assert any(128 <= t < 256 for t in tiles), tiles
+    sizes = np.diff(w.graph_ptr)
+    _sampled_parity(w, [0, 1 + 2 * int(np.argmax(sizes[1::2]))], table_grad=True)
