@@ -129,6 +129,15 @@ def traffic_from_counters(fetch_csv: str, write_csv: str, kernel: str, workload:
 PROBE_BYTES = 1 << 30
 
 
+def live_gates(op) -> int:
+    """Gate blocks an operation's cells compute: a Tree-LSTM leaf's forget gates multiply the zero state
+    (no children), so they are dead arithmetic and neither computed nor counted."""
+    from paper_1702_02181_amd import gen
+    if op.kind == gen.KIND_TREELSTM and op.arity == 0:
+        return 3
+    return gen.NUM_GATES[op.kind]
+
+
 def flops_by_kernel(w, sched_host, table_grad: bool) -> dict:
     """Algorithmic FLOPs of one forward + backward, by kernel class (2 FLOPs per multiply-add)."""
     from paper_1702_02181_amd import gen
@@ -146,7 +155,7 @@ def flops_by_kernel(w, sched_host, table_grad: bool) -> dict:
         op = w.ops[op_id]
         if op.kind == gen.KIND_EMBED:
             continue
-        G = gen.NUM_GATES[op.kind]
+        G = live_gates(op)
         ps = w.params[op.param_set]
         k_in = (ps.in_dim if op.has_input else 0) + op.arity * H
         name = gen.KIND_NAMES[op.kind]
@@ -182,7 +191,7 @@ def pass_work(w, host, table_grad: bool) -> dict:
             if w.backward and table_grad:
                 out[("bwd", g)] = (0.0, float(rows * 4 * H))
             continue
-        G = gen.NUM_GATES[op.kind]
+        G = live_gates(op)
         din = w.params[op.param_set].in_dim if op.has_input else 0
         has_c = op.kind in (gen.KIND_TREELSTM, gen.KIND_LSTM, gen.KIND_PROJ)
         s_node = H * (bh + (4 if has_c else 0))
@@ -200,7 +209,7 @@ def pass_work(w, host, table_grad: bool) -> dict:
             op = w.ops[o]
             if op.kind == gen.KIND_EMBED:
                 continue
-            G = gen.NUM_GATES[op.kind]
+            G = live_gates(op)
             k_in = (w.params[op.param_set].in_dim if op.has_input else 0) + op.arity * H
             out[("wgrad", o)] = (2.0 * count * k_in * G * H,
                                  float(count * (k_in + G * H) * bh + (k_in + 1) * G * H * 4))

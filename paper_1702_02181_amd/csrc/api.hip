@@ -88,6 +88,9 @@ int fail(int code, const std::string& msg) {
 
 bool valid_kind(int k) { return k >= FOLD_EMBED && k <= FOLD_PROJ; }
 
+// a Tree-LSTM operation without children: its cells run on the live gates only
+bool is_tree_lstm_leaf(const fold_op& op) { return op.kind == FOLD_TREELSTM && op.arity == 0; }
+
 // child slots an operation family's recurrent weights cover
 int slots_of(int kind) {
   switch (kind) {
@@ -259,11 +262,33 @@ int32_t pack_impl(const fold_params* prm, hipStream_t st, fold_packed** out) {
       if (!dalloc(nf * es, &ps.Wf) || !dalloc(nbr * es, &ps.Wb_rec) || !dalloc(nbi * es, &ps.Wb_in) ||
           !dalloc((size_t)ps.G * P.HP * sizeof(float), reinterpret_cast<void**>(&ps.bias)))
         return bail(FOLD_E_NOMEM, "fold_pack_params: out of device memory");
-      launch_pack(P.dtype, 0, ps.G, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr, ps.Wf, nf, st);
-      if (nbr) launch_pack(P.dtype, 1, ps.G, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr, ps.Wb_rec, nbr, st);
-      if (nbi) launch_pack(P.dtype, 2, ps.G, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr, ps.Wb_in, nbi, st);
-      launch_pack(P.dtype, 3, ps.G, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, nullptr, nullptr, s.bias, ps.bias,
-                  (size_t)ps.G * P.HP, st);
+      const int G = ps.G, gid = gate_code_identity(G);
+      launch_pack(P.dtype, 0, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr, ps.Wf,
+                  nf, st);
+      if (nbr)
+        launch_pack(P.dtype, 1, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr,
+                    ps.Wb_rec, nbr, st);
+      if (nbi)
+        launch_pack(P.dtype, 2, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr,
+                    ps.Wb_in, nbi, st);
+      launch_pack(P.dtype, 3, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, nullptr, nullptr, s.bias,
+                  ps.bias, (size_t)G * P.HP, st);
+      if (s.kind == FOLD_TREELSTM) {
+        // leaf operations of this set: the live gates only, input segment only
+        const int GL = gates_of(kTreeLstmLeaf);
+        const size_t nfl = (size_t)GL * P.HP * ps.INP, nbl = (size_t)ps.INP * GL * P.HP;
+        if (!dalloc(nfl * es, &ps.Wf_leaf) || !dalloc(nbl * es, &ps.Wb_in_leaf) ||
+            !dalloc((size_t)GL * P.HP * sizeof(float), reinterpret_cast<void**>(&ps.bias_leaf)))
+          return bail(FOLD_E_NOMEM, "fold_pack_params: out of device memory");
+        if (nfl)
+          launch_pack(P.dtype, 0, GL, G, kTreeLstmLeafGates, P.H, P.HP, s.in_dim, ps.INP, 0, ps.INP, s.W_in, nullptr,
+                      nullptr, ps.Wf_leaf, nfl, st);
+        if (nbl)
+          launch_pack(P.dtype, 2, GL, G, kTreeLstmLeafGates, P.H, P.HP, s.in_dim, ps.INP, 0, ps.INP, s.W_in, nullptr,
+                      nullptr, ps.Wb_in_leaf, nbl, st);
+        launch_pack(P.dtype, 3, GL, G, kTreeLstmLeafGates, P.H, P.HP, s.in_dim, ps.INP, 0, ps.INP, nullptr, nullptr,
+                    s.bias, ps.bias_leaf, (size_t)GL * P.HP, st);
+      }
     }
     P.sets.push_back(ps);
   }
@@ -336,7 +361,14 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
     a.gstride = L.gstride;
     a.zero = p.zero;
     a.zpart = zpart;
-    launch_cell_fwd(p.dtype, op.kind, a, st);
+    int kind = op.kind;
+    if (is_tree_lstm_leaf(op)) {  // live gates only, input segment only
+      kind = kTreeLstmLeaf;
+      a.Wf = ps.Wf_leaf;
+      a.Kf = ps.INP;
+      a.bias = ps.bias_leaf;
+    }
+    launch_cell_fwd(p.dtype, kind, a, st);
   }
   prof_tag(-1, -1);
   if (roots_out) launch_roots(p.dtype, s.R, p.ld, s.root_pos, h_pool, roots_out, st);
@@ -385,7 +417,8 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     b.d_table = d_table;
     b.tld = tld;
     b.dz_bf16 = p.dtype == FOLD_BF16;
-    launch_cell_bwd(op.kind, b, st);
+    const bool leaf = is_tree_lstm_leaf(op);
+    launch_cell_bwd(leaf ? kTreeLstmLeaf : op.kind, b, st);
     if (op.kind == FOLD_EMBED) continue;
     DxArgs d;
     d.rows = b.rows;
@@ -396,7 +429,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     d.HP = p.HP;
     d.ld = p.ld;
     d.gstride = L.gstride;
-    d.Kb = ps.G * p.HP;
+    d.Kb = (leaf ? gates_of(kTreeLstmLeaf) : ps.G) * p.HP;
     d.dz = gates;
     d.dh = dh;
     d.child_pos = s.child_pos;
@@ -416,7 +449,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     if (op.has_input && d_table && ps.INP > 0) {
       d.mode = 1;
       d.Nb = ps.INP;
-      d.Wb = ps.Wb_in;
+      d.Wb = leaf ? ps.Wb_in_leaf : ps.Wb_in;
       launch_bwd_dx(p.dtype, d, st);
     }
   }
@@ -430,7 +463,11 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       if (count <= 0) continue;
       const PackedSet& ps = p.sets[op.param_set];
       const fold_param_grads& pg = grads->sets[op.param_set];
-      const int Nw = ps.G * p.HP;
+      // dz columns: the canonical gate blocks, or the live ones of a Tree-LSTM leaf (dead columns get +0)
+      const bool leaf = is_tree_lstm_leaf(op);
+      const int Gz = leaf ? gates_of(kTreeLstmLeaf) : ps.G;
+      const int gcode = leaf ? kTreeLstmLeafGates : gate_code_identity(ps.G);
+      const int Nw = Gz * p.HP;
       const int off = s.h_op_row_ptr[o];
       WgArgs w;
       w.op_rows = s.op_rows + off;
@@ -458,9 +495,9 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
         w.wide = sp.wide;
         w.bpart = (pg.dbias && !bias_done) ? bpart : nullptr;
         launch_wgrad(p.dtype, w, st);
-        launch_wgrad_reduce(part, sp.nchunk, Kw, Nw, seg, p.H, p.HP, ps.in_dim, ps.G, dW, st);
+        launch_wgrad_reduce(part, sp.nchunk, Kw, Nw, seg, p.H, p.HP, ps.in_dim, ps.G, gcode, dW, st);
         if (w.bpart) {
-          launch_bias_reduce(bpart, sp.bparts, Nw, p.H, p.HP, pg.dbias, st);
+          launch_bias_reduce(bpart, sp.bparts, Nw, p.H, p.HP, gcode, pg.dbias, st);
           bias_done = true;
         }
       };
@@ -469,7 +506,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       if (pg.dbias && !bias_done) {
         const int chunk = 512, nchunk = (count + chunk - 1) / chunk;
         launch_bias_partial(w.op_rows, count, chunk, nchunk, gates, L.gstride, Nw, p.dtype == FOLD_BF16, bpart, st);
-        launch_bias_reduce(bpart, nchunk, Nw, p.H, p.HP, pg.dbias, st);
+        launch_bias_reduce(bpart, nchunk, Nw, p.H, p.HP, gcode, pg.dbias, st);
       }
     }
   }

@@ -15,6 +15,8 @@
 //   TREELSTM (i|f_l|f_r|o|u): c = i*u + f_l*c_l + f_r*c_r, h = o*tanh(c)   (Tai et al. N-ary, N = 2)
 //   LSTM     (i|f|o|u):       c = i*u + f*c_p,             h = o*tanh(c)
 //   TREERNN / PROJ:           h = tanh(z); PROJ passes the child's c through
+//   Tree-LSTM leaf (i|o|u):   c = i*u, h = o*tanh(c)  (the forget gates of a leaf multiply the zero
+//                             state: they are neither computed nor saved nor differentiated)
 
 #include <hip/hip_runtime.h>
 
@@ -43,7 +45,7 @@ __device__ __forceinline__ void scatter_add(float* dst, float v, bool single) {
 
 template <int KIND>
 struct Gates {
-  static constexpr int G = KIND == FOLD_TREELSTM ? 5 : (KIND == FOLD_LSTM ? 4 : 1);
+  static constexpr int G = KIND == FOLD_TREELSTM ? 5 : (KIND == FOLD_LSTM ? 4 : (KIND == kTreeLstmLeaf ? 3 : 1));
 };
 
 // ---------------------------------------------------------------- forward
@@ -120,6 +122,17 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
       gs[2 * a.HP] = fr;
       gs[3 * a.HP] = o;
       gs[4 * a.HP] = u;
+    }
+  } else if constexpr (KIND == kTreeLstmLeaf) {
+    const float i_ = sigmoidf_(z[0]), o = sigmoidf_(z[1]), u = tanhf_(z[2]);
+    (void)cl;
+    (void)cr;
+    c = i_ * u;
+    h = o * tanhf_(c);
+    if (gs) {
+      gs[0] = i_;
+      gs[a.HP] = o;
+      gs[2 * a.HP] = u;
     }
   } else if constexpr (KIND == FOLD_LSTM) {
     const float i_ = sigmoidf_(z[0]), f = sigmoidf_(z[1]), o = sigmoidf_(z[2]);
@@ -527,6 +540,14 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       put(4, j, dct * i_ * (1.f - u * u));
       if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dct * fl, s0);
       if (c1 >= 0) scatter_add(&a.dc[(size_t)c1 * a.ld + j], dct * fr, s1);
+    } else if constexpr (KIND == kTreeLstmLeaf) {
+      const float dc = a.dc[p * a.ld + j];
+      const float i_ = gate(0, j), o = gate(1, j), u = gate(2, j);
+      const float tc = tanhf_(a.c_pool[p * a.ld + j]);
+      const float dct = dc + dh * o * (1.f - tc * tc);
+      put(0, j, dct * u * i_ * (1.f - i_));
+      put(1, j, dh * tc * o * (1.f - o));
+      put(2, j, dct * i_ * (1.f - u * u));
     } else if constexpr (KIND == FOLD_LSTM) {
       const float dc = a.dc[p * a.ld + j];
       const float i_ = gate(0, j), f = gate(1, j), o = gate(2, j), u = gate(3, j);
@@ -779,6 +800,7 @@ template <typename T>
 void cell_fwd_t(int kind, const FwdArgs& a, hipStream_t st) {
   switch (kind) {
     case FOLD_TREELSTM: cell_fwd_kind<T, FOLD_TREELSTM>(a, st); break;
+    case kTreeLstmLeaf: cell_fwd_kind<T, kTreeLstmLeaf>(a, st); break;
     case FOLD_LSTM: cell_fwd_kind<T, FOLD_LSTM>(a, st); break;
     case FOLD_TREERNN: cell_fwd_kind<T, FOLD_TREERNN>(a, st); break;
     case FOLD_PROJ: cell_fwd_kind<T, FOLD_PROJ>(a, st); break;
@@ -793,6 +815,7 @@ const char* kind_name(int kind, int dtype) {
                               "cell_fwd.lstm.f32", "cell_fwd.proj.f32"};
   static const char* n16[] = {"cell_fwd.embed.bf16", "cell_fwd.treernn.bf16", "cell_fwd.treelstm.bf16",
                               "cell_fwd.lstm.bf16", "cell_fwd.proj.bf16"};
+  if (kind == kTreeLstmLeaf) kind = FOLD_TREELSTM;  // one class per operation family
   if (kind < 0 || kind > 4) return "cell_fwd";
   return dtype == FOLD_BF16 ? n16[kind] : n32[kind];
 }
@@ -849,8 +872,8 @@ void launch_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* d
 void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
   if (a.rows <= 0) return;
   static const char* names[] = {"cell_bwd.embed", "cell_bwd.treernn", "cell_bwd.treelstm", "cell_bwd.lstm",
-                                "cell_bwd.proj"};
-  ProfScope prof(kind >= 0 && kind <= 4 ? names[kind] : "cell_bwd", st);
+                                "cell_bwd.proj", "cell_bwd.treelstm"};
+  ProfScope prof(kind >= 0 && kind <= kTreeLstmLeaf ? names[kind] : "cell_bwd", st);
   dim3 grid(a.rows), block(256);
   const size_t lds = a.dz_bf16 ? (size_t)gates_of(kind) * a.HP * sizeof(uint16_t) : 0;
 #define FOLD_CB(K_)                                                                          \
@@ -860,6 +883,7 @@ void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
     case FOLD_EMBED: hipLaunchKernelGGL((k_cell_bwd<FOLD_EMBED, false>), grid, block, 0, st, a); break;
     case FOLD_TREERNN: FOLD_CB(FOLD_TREERNN) break;
     case FOLD_TREELSTM: FOLD_CB(FOLD_TREELSTM) break;
+    case kTreeLstmLeaf: FOLD_CB(kTreeLstmLeaf) break;
     case FOLD_LSTM: FOLD_CB(FOLD_LSTM) break;
     case FOLD_PROJ: FOLD_CB(FOLD_PROJ) break;
     default: break;

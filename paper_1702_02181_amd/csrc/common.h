@@ -22,15 +22,30 @@ constexpr int kMaxHidden = 4096;   // the backward stages one row's bf16 dz (G *
 inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 inline int64_t round_up64(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
+// Internal cell kind of a Tree-LSTM operation without children (a leaf: arity 0).  Its child cell states
+// are the zero state, so the forget gates multiply zero and cannot change c, h or any gradient; the leaf
+// kernels compute, save and differentiate only the live gates (i | o | u), in that compact order.
+constexpr int kTreeLstmLeaf = 5;
+
 inline int gates_of(int kind) {
   switch (kind) {
     case FOLD_TREERNN: return 1;
     case FOLD_TREELSTM: return 5;
     case FOLD_LSTM: return 4;
     case FOLD_PROJ: return 1;
+    case kTreeLstmLeaf: return 3;
     default: return 0;
   }
 }
+
+// Gate map of a compact gate layout: canonical gate index of compact gate g in bits [3g, 3g + 3).
+inline int gate_code_identity(int G) {
+  int c = 0;
+  for (int g = 0; g < G; ++g) c |= g << (3 * g);
+  return c;
+}
+constexpr int kTreeLstmLeafGates = 0 | (3 << 3) | (4 << 6);  // i, o, u of (i | f_l | f_r | o | u)
+__host__ __device__ inline int gate_of_code(int code, int g) { return (code >> (3 * g)) & 7; }
 
 // Row stride of every row the kernels read (pools, leaf table, gradients): whole K segments, so a stage
 // of 128 bytes never runs past a row and the pad columns (zero) meet zero weights.
@@ -105,6 +120,10 @@ struct PackedSet {
   void* Wb_rec = nullptr;  // [arity * HP][G * HP]
   void* Wb_in = nullptr;   // [INP][G * HP]
   float* bias = nullptr;   // [G * HP] fp32, zero padded
+  // Tree-LSTM sets: the same three for leaf operations, over the live gates (i | o | u) only
+  void* Wf_leaf = nullptr;     // [3 * HP interleaved per kUnit units][INP]
+  void* Wb_in_leaf = nullptr;  // [INP][3 * HP]
+  float* bias_leaf = nullptr;  // [3 * HP]
 };
 
 struct Packed {

@@ -189,18 +189,21 @@ struct WgArgs {
   const void* zero;  // a zero row at least 16 bytes past any column the kernels read
 };
 void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st);
+// Sum the partial tiles into the canonical dW ([rows][G * H]); partial column n is gate block n / HP of
+// the dz layout, canonical gate gate_of_code(gcode, n / HP).
 void launch_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP, int in_dim,
-                         int G, float* dW, hipStream_t st);
+                         int G, int gcode, float* dW, hipStream_t st);
 void launch_bias_partial(const int* op_rows, int count, int chunk, int nchunk, const float* dz, int gstride,
                          int Nw, int bf, float* bpart, hipStream_t st);
-void launch_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, float* dbias, hipStream_t st);
+void launch_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, int gcode, float* dbias,
+                        hipStream_t st);
 
 // ---- achievable-peak probes (diag.hip) ----
 int32_t probe_mfma(int dtype, hipStream_t st, double* tflops);
 int32_t probe_copy(void* dst, const void* src, size_t bytes, hipStream_t st, double* gbs);
 
 // ---- packing (pack.hip) ----
-void launch_pack(int dtype, int mode, int G, int H, int HP, int in_dim, int INP, int arity, int Kf,
+void launch_pack(int dtype, int mode, int G, int GC, int gcode, int H, int HP, int in_dim, int INP, int arity, int Kf,
                  const void* W_in, const void* W_rec, const float* bias, void* dst, size_t count,
                  hipStream_t st);
 

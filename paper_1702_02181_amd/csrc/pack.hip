@@ -7,7 +7,9 @@
 //   mode 1  backward  Wb_rec[c*HP + jin][g*HP + j] = W_rec[c*H + jin][g*H + j]  (n-major for dz . W^T)
 //   mode 2  backward  Wb_in[jin][g*HP + j]          = W_in[jin][g*H + j]
 //   mode 3  bias      b[g*HP + j]                   = bias[g*H + j]
-// Padding entries are zero.
+// The gate blocks packed are the canonical gates named by a gate code (gate_of_code): all G of them, or a
+// subset in a compact order (the live gates of Tree-LSTM leaves); the canonical matrices have GC gate
+// blocks.  Padding entries are zero.
 
 #include <hip/hip_runtime.h>
 
@@ -22,15 +24,16 @@ namespace fold {
 namespace {
 
 template <typename T>
-__global__ void k_pack(int mode, int G, int H, int HP, int in_dim, int INP, int arity, int Kf, const T* W_in,
-                       const T* W_rec, T* dst, size_t count) {
+__global__ void k_pack(int mode, int G, int GC, int gcode, int H, int HP, int in_dim, int INP, int arity, int Kf,
+                       const T* W_in, const T* W_rec, T* dst, size_t count) {
   for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < count;
        idx += (size_t)gridDim.x * blockDim.x) {
     float v = 0.f;
-    const int GH = G * H;
+    const int GH = GC * H;
     if (mode == 0) {
       const int np = (int)(idx / Kf), kp = (int)(idx - (size_t)np * Kf);
-      const int ub = np / (G * 32), rem = np - ub * G * 32, g = rem / 32, j = ub * 32 + (rem & 31);
+      const int ub = np / (G * 32), rem = np - ub * G * 32, j = ub * 32 + (rem & 31);
+      const int g = gate_of_code(gcode, rem / 32);
       if (j < H) {
         if (kp < INP) {
           if (kp < in_dim) v = to_f32<T>(W_in[(size_t)kp * GH + g * H + j]);
@@ -42,7 +45,7 @@ __global__ void k_pack(int mode, int G, int H, int HP, int in_dim, int INP, int 
     } else {
       const int KB = G * HP;
       const int n = (int)(idx / KB), kk = (int)(idx - (size_t)n * KB);
-      const int g = kk / HP, j = kk - g * HP;
+      const int gc = kk / HP, j = kk - gc * HP, g = gate_of_code(gcode, gc);
       if (j < H) {
         if (mode == 1) {
           const int c = n / HP, jin = n - c * HP;
@@ -56,32 +59,32 @@ __global__ void k_pack(int mode, int G, int H, int HP, int in_dim, int INP, int 
   }
 }
 
-__global__ void k_pack_bias(int G, int H, int HP, const float* bias, float* dst) {
+__global__ void k_pack_bias(int G, int gcode, int H, int HP, const float* bias, float* dst) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= G * HP) return;
-  const int g = idx / HP, j = idx - g * HP;
-  dst[idx] = j < H ? bias[g * H + j] : 0.f;
+  const int gc = idx / HP, j = idx - gc * HP;
+  dst[idx] = j < H ? bias[gate_of_code(gcode, gc) * H + j] : 0.f;
 }
 
 }  // namespace
 
-void launch_pack(int dtype, int mode, int G, int H, int HP, int in_dim, int INP, int arity, int Kf,
+void launch_pack(int dtype, int mode, int G, int GC, int gcode, int H, int HP, int in_dim, int INP, int arity, int Kf,
                  const void* W_in, const void* W_rec, const float* bias, void* dst, size_t count, hipStream_t st) {
   if (count == 0) return;
   if (mode == 3) {
-    hipLaunchKernelGGL(k_pack_bias, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st, G, H, HP, bias,
+    hipLaunchKernelGGL(k_pack_bias, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st, G, gcode, H, HP, bias,
                        static_cast<float*>(dst));
     return;
   }
   const unsigned blocks = (unsigned)std::min<size_t>((count + 255) / 256, 65536);
   if (dtype == FOLD_BF16)
-    hipLaunchKernelGGL(k_pack<uint16_t>, dim3(blocks), dim3(256), 0, st, mode, G, H, HP, in_dim, INP, arity, Kf,
-                       static_cast<const uint16_t*>(W_in), static_cast<const uint16_t*>(W_rec),
+    hipLaunchKernelGGL(k_pack<uint16_t>, dim3(blocks), dim3(256), 0, st, mode, G, GC, gcode, H, HP, in_dim, INP,
+                       arity, Kf, static_cast<const uint16_t*>(W_in), static_cast<const uint16_t*>(W_rec),
                        static_cast<uint16_t*>(dst), count);
   else
-    hipLaunchKernelGGL(k_pack<float>, dim3(blocks), dim3(256), 0, st, mode, G, H, HP, in_dim, INP, arity, Kf,
-                       static_cast<const float*>(W_in), static_cast<const float*>(W_rec), static_cast<float*>(dst),
-                       count);
+    hipLaunchKernelGGL(k_pack<float>, dim3(blocks), dim3(256), 0, st, mode, G, GC, gcode, H, HP, in_dim, INP, arity,
+                       Kf, static_cast<const float*>(W_in), static_cast<const float*>(W_rec),
+                       static_cast<float*>(dst), count);
 }
 
 }  // namespace fold

@@ -528,12 +528,12 @@ __global__ __launch_bounds__(wide::kThreads) void k_wgrad_bf16_w(WgArgs a) {
 
 // dW[row, col] += sum over chunks of partial[chunk, m, n], (m, n) in the padded layout
 __global__ void k_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP,
-                               int in_dim, int G, float* dW) {
+                               int in_dim, int G, int gcode, float* dW) {
   const size_t total = (size_t)Kw * Nw;
   for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
        idx += (size_t)gridDim.x * blockDim.x) {
     const int m = (int)(idx / Nw), n = (int)(idx - (size_t)m * Nw);
-    const int g = n / HP, j = n - g * HP;
+    const int gz = n / HP, j = n - gz * HP, g = gate_of_code(gcode, gz);
     if (j >= H) continue;
     int row;
     if (seg) {
@@ -567,7 +567,7 @@ __global__ void k_bias_partial(const int* op_rows, int count, int chunk, const f
 
 // db[col] += sum over partial rows, 64 columns per block: four thread groups sum interleaved partial
 // rows, then the four sums are added in a fixed order (the result does not depend on scheduling)
-__global__ void k_bias_reduce(const float* bpart, int nparts, int Nw, int H, int HP, float* dbias) {
+__global__ void k_bias_reduce(const float* bpart, int nparts, int Nw, int H, int HP, int gcode, float* dbias) {
   __shared__ float red[4][64];
   const int cg = threadIdx.x & 63, pg = threadIdx.x >> 6;
   const int n = blockIdx.x * 64 + cg;
@@ -577,9 +577,9 @@ __global__ void k_bias_reduce(const float* bpart, int nparts, int Nw, int H, int
   red[pg][cg] = s;
   __syncthreads();
   if (pg != 0 || n >= Nw) return;
-  const int g = n / HP, j = n - g * HP;
+  const int gz = n / HP, j = n - gz * HP;
   if (j >= H) return;
-  dbias[g * H + j] += (red[0][cg] + red[1][cg]) + (red[2][cg] + red[3][cg]);
+  dbias[gate_of_code(gcode, gz) * H + j] += (red[0][cg] + red[1][cg]) + (red[2][cg] + red[3][cg]);
 }
 
 }  // namespace
@@ -634,12 +634,12 @@ void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st) {
 }
 
 void launch_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP, int in_dim,
-                         int G, float* dW, hipStream_t st) {
+                         int G, int gcode, float* dW, hipStream_t st) {
   ProfScope prof("wgrad_reduce", st);
   const size_t total = (size_t)Kw * Nw;
   const unsigned blocks = (unsigned)std::min<size_t>((total + 255) / 256, 65536);
   hipLaunchKernelGGL(k_wgrad_reduce, dim3(blocks), dim3(256), 0, st, partial, nchunk, Kw, Nw, seg, H, HP, in_dim,
-                     G, dW);
+                     G, gcode, dW);
 }
 
 void launch_bias_partial(const int* op_rows, int count, int chunk, int nchunk, const float* dz, int gstride, int Nw,
@@ -650,10 +650,11 @@ void launch_bias_partial(const int* op_rows, int count, int chunk, int nchunk, c
                      gstride, Nw, bf, bpart);
 }
 
-void launch_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, float* dbias, hipStream_t st) {
+void launch_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, int gcode, float* dbias,
+                        hipStream_t st) {
   if (nchunk <= 0) return;
   ProfScope prof("bias_reduce", st);
-  hipLaunchKernelGGL(k_bias_reduce, dim3((Nw + 63) / 64), dim3(256), 0, st, bpart, nchunk, Nw, H, HP, dbias);
+  hipLaunchKernelGGL(k_bias_reduce, dim3((Nw + 63) / 64), dim3(256), 0, st, bpart, nchunk, Nw, H, HP, gcode, dbias);
 }
 
 }  // namespace fold

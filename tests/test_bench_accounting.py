@@ -20,15 +20,15 @@ def test_pass_work_treelstm_counts():
     host = dict(group_op=[0, 1], group_rows=[4, 2])
     work = bench.pass_work(w, host, table_grad=False)
     S, Sg = 8 * H, 8 * H  # fp32 h + fp32 c; fp32 gradients of both
-    # leaf: 4 rows, input width H, 5 gates
-    assert work[("fwd", 0)] == (2.0 * 4 * H * 5 * H, 4 * (4 * H + S) + H * 5 * H * 4 + 5 * H * 4)
+    # leaf: 4 rows, input width H, the 3 live gates (a leaf's forget gates multiply the zero state)
+    assert work[("fwd", 0)] == (2.0 * 4 * H * 3 * H, 4 * (4 * H + S) + H * 3 * H * 4 + 3 * H * 4)
     # leaf backward without a trainable table: only the cell's elementwise part
     assert work[("bwd", 0)] == (0.0, 4 * Sg)
     # internal: 2 rows, two children
     assert work[("fwd", 1)] == (2.0 * 2 * 2 * H * 5 * H, 2 * (2 * S + S) + 2 * H * 5 * H * 4 + 5 * H * 4)
     assert work[("bwd", 1)] == (2.0 * 2 * 5 * H * 2 * H, 2 * (Sg + 2 * (S + Sg)) + 2 * H * 5 * H * 4)
     # weight gradients per op over all its rows
-    assert work[("wgrad", 0)][0] == 2.0 * 4 * H * 5 * H
+    assert work[("wgrad", 0)][0] == 2.0 * 4 * H * 3 * H
     assert work[("wgrad", 1)][0] == 2.0 * 2 * 2 * H * 5 * H
 
 
@@ -38,9 +38,9 @@ def test_pass_work_bf16_state_bytes_and_table_grad():
     host = dict(group_op=[0], group_rows=[3])
     work = bench.pass_work(w, host, table_grad=True)
     S = H * (2 + 4)  # bf16 h, fp32 c
-    assert work[("fwd", 0)][1] == 3 * (2 * H + S) + H * 5 * H * 2 + 5 * H * 4
+    assert work[("fwd", 0)][1] == 3 * (2 * H + S) + H * 3 * H * 2 + 3 * H * 4
     # with a trainable table the leaf backward contracts dz with W_in^T and writes the table row
-    assert work[("bwd", 0)] == (2.0 * 3 * 5 * H * H, 3 * (8 * H + 4 * H) + H * 5 * H * 2)
+    assert work[("bwd", 0)] == (2.0 * 3 * 3 * H * H, 3 * (8 * H + 4 * H) + H * 3 * H * 2)
 
 
 def test_pass_of_routes_launches():

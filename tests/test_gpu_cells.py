@@ -39,6 +39,20 @@ def test_config2_per_node_upstream_gradients():
     C.compare_all(w, g, o)
 
 
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_leaf_forget_columns_of_w_in_get_exactly_zero(cfg):
+    """Tree-LSTM leaves have zero child states, so the forget-gate columns of W_in receive exactly zero
+    gradient (internal nodes of these workloads read no input). The leaf kernels skip those gates entirely:
+    the columns must stay at the caller's zeros, bit for bit, while the live columns match the oracle."""
+    w = gen.config2(num_graphs=3, leaves=24) if cfg == 2 else gen.config3(num_graphs=8)
+    g, o = C.run_device(w, table_grad=(cfg == 3)), C.run_oracle(w, table_grad=(cfg == 3))
+    H = w.hidden
+    dW = g["grads"][0]["W_in"]
+    assert np.all(dW[:, H:3 * H] == 0)
+    assert np.all(o["grads"][0]["W_in"][:, H:3 * H] == 0)
+    C.compare_all(w, g, o, table_grad=(cfg == 3))
+
+
 def test_config3_shape_bf16_h300():
     w = gen.config3(num_graphs=24)
     g, o = C.run_device(w, table_grad=True), C.run_oracle(w, table_grad=True)
