@@ -629,6 +629,8 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
   }
   const int nst = a.Kb * (int)sizeof(T) / 128, per = (nst + a.ksplit - 1) / a.ksplit;
   const int c0 = min(nst, kz * per), c1 = min(nst, c0 + per);
+  // an empty trailing K slice adds nothing (and its epilogue would read the target table unpublished)
+  if (c1 <= c0) return;
   const int lr = row_of_lane(lane);
   const char* zero = static_cast<const char*>(a.zero);
   FixedRowsIssue<PA, PB> issue;
@@ -713,6 +715,7 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
 
   const int nst_all = a.Kb * (int)sizeof(T) / 64, per = (nst_all + a.ksplit - 1) / a.ksplit;
   const int c0 = min(nst_all, (int)blockIdx.y * per), nst = min(nst_all, c0 + per) - c0;
+  if (nst <= 0) return;  // an empty K slice adds nothing (its epilogue would read the tables unpublished)
   const bool split = a.ksplit > 1;
   const bool loads = wave < 4;
   const char* zero = static_cast<const char*>(a.zero);
