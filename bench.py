@@ -51,6 +51,8 @@ CLASS_SOURCES = {
 COPY_KERNEL = "k_probe_copy"
 TRAFFIC_TAG = "traffic-record:"
 KIND_IDS = {"embed": 0, "treernn": 1, "treelstm": 2, "lstm": 3, "proj": 4}
+# template kind ids of a class's kernels: Tree-LSTM leaves run as their own kind (live gates only)
+KERNEL_KINDS = {"treelstm": (2, 5)}
 CTYPE = {"f32": "float", "bf16": "unsigned short"}
 
 
@@ -65,10 +67,10 @@ def rocprof_role(kernel_class: str, name: str):
     parts = kernel_class.split(".")
     cls, dt = parts[0], CTYPE[parts[-1]]
     if cls == "cell_fwd":
-        kind = KIND_IDS[parts[1]]
-        if re.search(rf"k_cell_fwd(_w)?<{dt}, {kind}[,>]", name):
+        kinds = "|".join(str(k) for k in KERNEL_KINDS.get(parts[1], (KIND_IDS[parts[1]],)))
+        if re.search(rf"k_cell_fwd(_w)?<{dt}, ({kinds})[,>]", name):
             return "main"
-        if re.search(rf"k_cell_epi<{dt}, {kind}>", name):
+        if re.search(rf"k_cell_epi<{dt}, ({kinds})>", name):
             return "extra"
     elif cls == "bwd_dx":
         if re.search(rf"k_bwd_dx(2|_w)<{dt}[,>]", name):

@@ -81,3 +81,19 @@ def test_level_classes_split_and_fractions():
     assert c["gather"]["achieved_gbs"] == pytest.approx(1e7 / 25e-6 / 1e9, rel=1e-3)
     assert c["narrow"]["passes"] == 1 and c["narrow"]["us_per_pass"] == pytest.approx(4.0)
     assert c["other_ms_per_step"] == pytest.approx(0.002)
+
+
+def test_rocprof_roles_of_kernel_names():
+    f = "cell_fwd.treelstm.f32"
+    assert bench.rocprof_role(f, "void fold::(anonymous namespace)::k_cell_fwd_w<float, 2>(fold::FwdArgs)") == "main"
+    assert bench.rocprof_role(f, "void k_cell_fwd_w<float, 5>(fold::FwdArgs)") == "main"  # leaf kind
+    assert bench.rocprof_role(f, "void k_cell_fwd<float, 5, 1, true>(fold::FwdArgs)") == "main"
+    assert bench.rocprof_role(f, "void k_cell_epi<float, 5>(fold::FwdArgs, int)") == "extra"
+    assert bench.rocprof_role(f, "void k_cell_fwd<float, 3, 1, false>(fold::FwdArgs)") is None  # LSTM
+    assert bench.rocprof_role(f, "void k_cell_fwd_w<unsigned short, 2>(fold::FwdArgs)") is None  # bf16
+    assert bench.rocprof_role("cell_fwd.lstm.bf16", "void k_cell_fwd<unsigned short, 3, 2, false>(x)") == "main"
+    assert bench.rocprof_role("bwd_dx.bf16", "void k_bwd_dx_w<unsigned short>(fold::DxArgs)") == "main"
+    assert bench.rocprof_role("bwd_dx.f32", "void k_bwd_dx2<float, 1, true>(fold::DxArgs)") == "main"
+    assert bench.rocprof_role("wgrad.bf16", "void k_wgrad_bf16_w(fold::WgArgs)") == "main"
+    assert bench.rocprof_role("wgrad.f32", "void k_wgrad_f32<128>(fold::WgArgs)") == "main"
+    assert bench.rocprof_role("wgrad.f32", "k_wgrad_reduce(float const*, int)") is None
