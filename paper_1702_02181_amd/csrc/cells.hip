@@ -439,12 +439,24 @@ __global__ void k_cell_epi(FwdArgs a, int nsplit) {
       if (j < a.ld) pad_out<T>(a, row, j);
       continue;
     }
+    // the slices are added in slice order; their loads go out eight slices (of every gate) at a time
+    // rather than one after another (absent slices add an exact 0)
+    constexpr int U = 8;
     float z[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float v = a.bias[g * a.HP + j];
-      for (int sp = 0; sp < nsplit; ++sp) v += a.zpart[((size_t)sp * a.rows + row) * zs + g * a.HP + j];
-      z[g] = v;
+    for (int g = 0; g < G; ++g) z[g] = a.bias[g * a.HP + j];
+    const float* zp = a.zpart + (size_t)row * zs + j;
+    const size_t slice = (size_t)a.rows * zs;
+    for (int s0 = 0; s0 < nsplit; s0 += U) {
+      float t[G][U];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int g = 0; g < G; ++g) t[g][u] = s0 + u < nsplit ? zp[(size_t)(s0 + u) * slice + g * a.HP] : 0.f;
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int g = 0; g < G; ++g) z[g] += t[g][u];
     }
     cell_out<T, KIND>(a, row, j, z, c0r[j], c1r[j]);
   }
