@@ -101,6 +101,11 @@ struct DxPlan {
   int mt = 1, ksplit = 1;
   bool wide = false;  // 256 x 256 tiles per workgroup of 8 waves
 };
+// at most this many K slices: beyond it the atomic adds of the slices cost more than the shorter K loops
+// save (measured on levels of 30-400 rows, H = 512: 8 beats 2, 4 and 16-20)
+constexpr int kDxMaxSplit = 8;
+// levels with fewer narrow tiles than this split K (measured: 256 beats 192, the same as 384 or 512)
+constexpr int kDxSplitBelow = 256;
 inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
   const int BK = esize == 4 ? 32 : 64;
   const int nst = Kb / BK;
@@ -122,9 +127,9 @@ inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
   // fp32: 128-row tiles, two workgroups per compute unit; bf16: 256-row tiles on wide levels
   p.mt = esize == 4 ? 1 : (((long long)(rows + 255) / 256) * nb >= 256 ? 2 : 1);
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * nb;
-  if (can_split && base < 192 && nst >= 4) {
+  if (can_split && base < kDxSplitBelow && nst >= 4) {
     const long long want = (256 + base - 1) / base;
-    p.ksplit = (int)std::min<long long>(want, nst / 2);
+    p.ksplit = (int)std::min<long long>(std::min<long long>(want, nst / 2), kDxMaxSplit);
   }
   return p;
 }
