@@ -791,7 +791,7 @@ void cell_fwd_kind(const FwdArgs& a0, hipStream_t st) {
     const int R = (int)cdiv(a.rows, wide::kRows), NU = a.HP / 64;
     a.ksplit = 1;
     a.map = NU % 8 == 0 ? kMapOwnCols : kMapRows;
-    dim3 grid(a.map == kMapOwnCols ? NU * R : xcd_grid(NU, R));
+    dim3 grid(a.map == kMapOwnCols ? xcd_cols_grid(NU, R) : xcd_grid(NU, R));
     hipLaunchKernelGGL((k_cell_fwd_w<T, KIND>), grid, dim3(wide::kThreads), 0, st, a);
     return;
   }
@@ -916,7 +916,7 @@ void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
     a.ksplit = pl.ksplit;
     a.map = NT % 8 == 0 ? kMapOwnCols : kMapRows;
     // K slices along y: gridDim.x is a multiple of 8, so every slice of a tile runs on the tile's XCD
-    dim3 grid(a.map == kMapOwnCols ? NT * R : xcd_grid(NT, R), pl.ksplit);
+    dim3 grid(a.map == kMapOwnCols ? xcd_cols_grid(NT, R) : xcd_grid(NT, R), pl.ksplit);
     if (dtype == FOLD_BF16)
       hipLaunchKernelGGL(k_bwd_dx_w<uint16_t>, grid, dim3(wide::kThreads), 0, st, a);
     else
