@@ -586,12 +586,17 @@ __global__ void k_bias_reduce(const float* bpart, int nparts, int Nw, int H, int
 
 // Chunks of an op's rows: a multiple of 8 (each XCD reduces whole chunks, all tiles of a chunk on one
 // XCD) chosen so that an XCD's workgroups fill its resident slots in whole rounds (a launch of 2.2 rounds
-// runs as 3), with chunks of at least min_rows rows.
-static int wgrad_chunks(long long tiles, int count, int min_rows, int slots_per_xcd) {
+// runs as 3), with chunks of at least min_rows and (if possible) at most max_rows rows.  Short chunks keep
+// the workgroups that an XCD runs at once on the same rows, so the rows they share stay in its L2
+// (measured on 1.25 M rows: 64 chunks of ~20 k rows cut the contraction from 44.6 to 42.2 ms against 8
+// chunks; more chunks gain nothing and cost more in the partial-tile reduction).
+static int wgrad_chunks(long long tiles, int count, int min_rows, int max_rows, int slots_per_xcd) {
   const long long most8 = std::max(1, count / (8 * min_rows));  // chunks per XCD at most
-  int best = 1;
+  const long long least8 = std::min<long long>(most8, std::max<long long>(1, ((long long)count + 8LL * max_rows - 1) /
+                                                                                 (8LL * max_rows)));
+  int best = (int)least8;
   double best_eff = 0.0;
-  for (int c8 = 1; c8 <= std::min<long long>(most8, 32); ++c8) {
+  for (int c8 = (int)least8; c8 <= std::max<long long>(least8, std::min<long long>(most8, 32)); ++c8) {
     const long long wg = tiles * c8;
     const double eff = (double)wg / (double)(((wg + slots_per_xcd - 1) / slots_per_xcd) * slots_per_xcd);
     if (eff > best_eff + 1e-9) {
@@ -610,7 +615,7 @@ WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype) {
   w.wide = dtype == FOLD_BF16 && count >= 65536;
   const long long tiles = w.wide ? (long long)((Kw + 255) / 256) * ((Nw + 255) / 256)
                                  : (long long)((Kw + kTM - 1) / kTM) * ((Nw + 127) / 128);
-  w.nchunk = wgrad_chunks(tiles, count, w.wide ? 1024 : 512, w.wide ? 32 : 64);
+  w.nchunk = wgrad_chunks(tiles, count, w.wide ? 1024 : 512, w.wide ? 20480 : (1 << 30), w.wide ? 32 : 64);
   w.chunk = round_up((count + w.nchunk - 1) / w.nchunk, 64);
   w.nchunk = (count + w.chunk - 1) / w.chunk;
   // bias partial rows: one per (chunk, weight-row tile, thread group)
