@@ -21,6 +21,7 @@ inside it); the same step issued call by call is timed beside it.
 from __future__ import annotations
 
 import argparse
+import collections
 import csv
 import glob
 import hashlib
@@ -138,6 +139,49 @@ def live_gates(op) -> int:
     if op.kind == gen.KIND_TREELSTM and op.arity == 0:
         return 3
     return gen.NUM_GATES[op.kind]
+
+
+def counters_table(mfma_csv: str, fetch_csv: str, write_csv: str, trace_csv: str, top: int = 14) -> str:
+    """Per-kernel table from four rocprofv3 runs of the same bench command: a counter pass with MfmaUtil,
+    GRBM_GUI_ACTIVE and the MFMA op counts, a FETCH_SIZE pass, a WRITE_SIZE pass (KiB per dispatch, each
+    scaled by what it reads for the copy probe) and a kernel trace (durations).  MFMA utilisation is
+    weighted by each dispatch's active cycles; GB/s = HBM bytes / summed duration."""
+    def rows(path):
+        return list(csv.DictReader(open(path)))
+    mfma = collections.defaultdict(lambda: [0, 0.0, 0.0, 0.0])  # dispatches, cycles, util*cycles, mfma flops
+    disp = collections.defaultdict(dict)
+    for r in rows(mfma_csv):
+        disp[(r["Dispatch_Id"], r["Kernel_Name"])][r["Counter_Name"]] = float(r["Counter_Value"])
+    for (_, name), v in disp.items():
+        m = mfma[name]
+        g = v.get("GRBM_GUI_ACTIVE", 0.0)
+        m[0] += 1
+        m[1] += g
+        m[2] += v.get("MfmaUtil", 0.0) * g
+        m[3] += 512.0 * (v.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) + v.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0))
+    hbm = {}
+    for what, path in (("fetch", fetch_csv), ("write", write_csv)):
+        tot = collections.defaultdict(float)
+        copy = []
+        for r in rows(path):
+            tot[r["Kernel_Name"]] += float(r["Counter_Value"])
+            if COPY_KERNEL in r["Kernel_Name"]:
+                copy.append(float(r["Counter_Value"]))
+        factor = (PROBE_BYTES / 1024.0) / statistics.median(copy)
+        hbm[what] = {k: v * 1024.0 * factor for k, v in tot.items()}
+    dur = collections.defaultdict(float)
+    for r in rows(trace_csv):
+        dur[r["Kernel_Name"]] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+    out = ["| kernel | dispatches | total ms | MFMA busy % | MFMA TFLOP/s executed | HBM read GB | HBM write GB | HBM GB/s |",
+           "|---|---:|---:|---:|---:|---:|---:|---:|"]
+    for name in sorted(dur, key=lambda k: -dur[k])[:top]:
+        m = mfma.get(name, [0, 0.0, 0.0, 0.0])
+        t = dur[name]
+        rd, wr = hbm["fetch"].get(name, 0.0), hbm["write"].get(name, 0.0)
+        short = re.sub(r"fold::\(anonymous namespace\)::", "", name)[:70]
+        out.append(f"| `{short}` | {m[0]} | {t * 1e3:.1f} | {m[2] / max(m[1], 1.0):.1f} | {m[3] / t / 1e12:.0f} | "
+                   f"{rd / 1e9:.1f} | {wr / 1e9:.1f} | {(rd + wr) / t / 1e9:.0f} |")
+    return "\n".join(out)
 
 
 def flops_by_kernel(w, sched_host, table_grad: bool) -> dict:
@@ -324,7 +368,12 @@ def main():
     ap.add_argument("--profile-only", action="store_true", help="skip the oracle leg and the schedule timing")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--traffic-kernel", default=None)
+    ap.add_argument("--counters-from", nargs=4, metavar=("MFMA_CSV", "FETCH_CSV", "WRITE_CSV", "TRACE_CSV"),
+                    help="print the per-kernel MFMA utilisation / HBM bandwidth table of four rocprofv3 runs")
     args = ap.parse_args()
+    if args.counters_from:
+        print(counters_table(*args.counters_from))
+        return
     if args.traffic_from:
         from paper_1702_02181_amd import gen as _gen
         w = _gen.make_config(args.config)

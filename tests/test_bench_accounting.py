@@ -97,3 +97,35 @@ def test_rocprof_roles_of_kernel_names():
     assert bench.rocprof_role("wgrad.bf16", "void k_wgrad_bf16_w(fold::WgArgs)") == "main"
     assert bench.rocprof_role("wgrad.f32", "void k_wgrad_f32<128>(fold::WgArgs)") == "main"
     assert bench.rocprof_role("wgrad.f32", "k_wgrad_reduce(float const*, int)") is None
+
+
+def test_counters_table_from_rocprof_csvs(tmp_path):
+    """Per-kernel MFMA utilisation (weighted by active cycles) and HBM rate from four rocprofv3 csv files;
+    the copy probe's counter value calibrates the byte counters."""
+    import csv as _csv
+
+    def write(name, header, rows):
+        p = tmp_path / name
+        with open(p, "w", newline="") as f:
+            wr = _csv.writer(f)
+            wr.writerow(header)
+            wr.writerows(rows)
+        return str(p)
+
+    H = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    probe = "k_probe_copy(uint4 const*, uint4*, unsigned long)"
+    kib = bench.PROBE_BYTES / 1024.0
+    mfma = write("m.csv", H, [
+        [1, "k_a", "GRBM_GUI_ACTIVE", 100], [1, "k_a", "MfmaUtil", 50], [1, "k_a", "SQ_INSTS_VALU_MFMA_MOPS_BF16", 1e6],
+        [2, "k_a", "GRBM_GUI_ACTIVE", 300], [2, "k_a", "MfmaUtil", 10], [2, "k_a", "SQ_INSTS_VALU_MFMA_MOPS_BF16", 1e6]])
+    fetch = write("f.csv", H, [[3, probe, "FETCH_SIZE", kib / 2], [1, "k_a", "FETCH_SIZE", 1e6], [2, "k_a", "FETCH_SIZE", 1e6]])
+    wsz = write("w.csv", H, [[3, probe, "WRITE_SIZE", kib], [1, "k_a", "WRITE_SIZE", 5e5], [2, "k_a", "WRITE_SIZE", 5e5]])
+    trace = write("t.csv", ["Kernel_Name", "Start_Timestamp", "End_Timestamp"],
+                  [["k_a", 0, 1_000_000], ["k_a", 5_000_000, 6_000_000], [probe, 0, 10]])
+    table = bench.counters_table(mfma, fetch, wsz, trace)
+    row = [l for l in table.splitlines() if "`k_a`" in l][0].split("|")
+    assert row[2].strip() == "2" and row[3].strip() == "2.0"         # dispatches, total ms
+    assert row[4].strip() == "20.0"                                    # (50*100 + 10*300) / 400
+    assert row[5].strip() == f"{2 * 512e6 / 2e-3 / 1e12:.0f}"          # executed MFMA TFLOP/s
+    assert row[6].strip() == f"{2e6 * 1024 * 2 / 1e9:.1f}"             # FETCH_SIZE scaled by 2
+    assert row[7].strip() == f"{1e6 * 1024 / 1e9:.1f}"                 # WRITE_SIZE scaled by 1
