@@ -20,6 +20,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "internal.h"
 #include "dma.h"
@@ -804,7 +806,7 @@ void cell_fwd_kind(const FwdArgs& a0, hipStream_t st) {
   if (pl.ksplit > 1) {
     if (pl.mt == 2) hipLaunchKernelGGL((k_cell_fwd<T, KIND, 2, true>), grid, dim3(kThreads), 0, st, a);
     else hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, true>), grid, dim3(kThreads), 0, st, a);
-    hipLaunchKernelGGL((k_cell_epi<T, KIND>), dim3(a.rows), dim3(256), 0, st, a, pl.ksplit);
+    hipLaunchKernelGGL((k_cell_epi<T, KIND>), dim3(a.rows), dim3(std::min(a.HP, 1024)), 0, st, a, pl.ksplit);
   } else {
     if (pl.mt == 2) hipLaunchKernelGGL((k_cell_fwd<T, KIND, 2, false>), grid, dim3(kThreads), 0, st, a);
     else hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, false>), grid, dim3(kThreads), 0, st, a);
@@ -889,7 +891,8 @@ void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
   static const char* names[] = {"cell_bwd.embed", "cell_bwd.treernn", "cell_bwd.treelstm", "cell_bwd.lstm",
                                 "cell_bwd.proj", "cell_bwd.treelstm"};
   ProfScope prof(kind >= 0 && kind <= kTreeLstmLeaf ? names[kind] : "cell_bwd", st);
-  dim3 grid(a.rows), block(256);
+  // one thread per hidden unit (up to 1024): every load of a row is in flight at once
+  dim3 grid(a.rows), block(std::min(a.HP, 1024));
   const size_t lds = a.dz_bf16 ? (size_t)gates_of(kind) * a.HP * sizeof(uint16_t) : 0;
 #define FOLD_CB(K_)                                                                          \
   if (a.dz_bf16) hipLaunchKernelGGL((k_cell_bwd<K_, true>), grid, block, lds, st, a);        \
