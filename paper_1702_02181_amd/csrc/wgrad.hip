@@ -544,8 +544,16 @@ __global__ void k_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw,
       if (m >= in_dim) continue;
       row = m;
     }
+    // chunk order; the loads of eight chunks go out at once (absent chunks add an exact 0)
+    constexpr int U = 8;
     float s = 0.f;
-    for (int c = 0; c < nchunk; ++c) s += partial[(size_t)c * total + idx];
+    for (int c0 = 0; c0 < nchunk; c0 += U) {
+      float t[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) t[u] = c0 + u < nchunk ? partial[(size_t)(c0 + u) * total + idx] : 0.f;
+#pragma unroll
+      for (int u = 0; u < U; ++u) s += t[u];
+    }
     dW[(size_t)row * G * H + g * H + j] += s;
   }
 }
@@ -572,8 +580,16 @@ __global__ void k_bias_reduce(const float* bpart, int nparts, int Nw, int H, int
   const int cg = threadIdx.x & 63, pg = threadIdx.x >> 6;
   const int n = blockIdx.x * 64 + cg;
   float s = 0.f;
-  if (n < Nw)
-    for (int c = pg; c < nparts; c += 4) s += bpart[(size_t)c * Nw + n];
+  if (n < Nw) {
+    constexpr int U = 8;  // partial rows pg, pg + 4, ... in order, eight loads in flight
+    for (int c0 = pg; c0 < nparts; c0 += 4 * U) {
+      float t[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) t[u] = c0 + 4 * u < nparts ? bpart[(size_t)(c0 + 4 * u) * Nw + n] : 0.f;
+#pragma unroll
+      for (int u = 0; u < U; ++u) s += t[u];
+    }
+  }
   red[pg][cg] = s;
   __syncthreads();
   if (pg != 0 || n >= Nw) return;
