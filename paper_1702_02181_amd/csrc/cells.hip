@@ -45,6 +45,16 @@ __device__ __forceinline__ void scatter_add(float* dst, float v, bool single) {
     unsafeAtomicAdd(dst, v);
 }
 
+// Old values of the read-add-write targets among the 16 rows of one 32 x 32 result block that a lane holds
+// (column jin of pool rows t[r] where one[r]).  Such targets have a single parent edge, so they are
+// distinct rows: all 16 loads are issued before any store, instead of each waiting behind the previous
+// row's store.
+__device__ __forceinline__ void read_targets16(const float* dh, int ld, int jin, const int (&t)[16],
+                                               const bool (&one)[16], float (&old)[16]) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) old[r] = one[r] ? dh[(size_t)t[r] * ld + jin] : 0.f;
+}
+
 template <int KIND>
 struct Gates {
   static constexpr int G = KIND == FOLD_TREELSTM ? 5 : (KIND == FOLD_LSTM ? 4 : (KIND == kTreeLstmLeaf ? 3 : 1));
@@ -675,17 +685,28 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
       if (n >= a.Nb) continue;
       const int k = a.mode == 0 ? n / a.HP : 0, jin = a.mode == 0 ? n - k * a.HP : n;
       if (jin >= (a.mode == 0 ? a.H : a.in_dim)) continue;
+      // K slices of one element add into it concurrently: atomics whenever K is split
+      int tr[16];
+      bool one[16];
+      float old[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int rl = wave * 32 * MT + tm * 32 + acc_row(r, lane), row = m0 + rl;
-        if (row >= a.rows) continue;
-        // K slices of one element add into it concurrently: atomics whenever K is split
-        const int t = tgt[k][rl];
+        tr[r] = row < a.rows ? tgt[k][rl] : -1;
+        one[r] = !SPLIT && a.mode == 0 && tr[r] >= 0 && sgl[k][rl];
+      }
+      read_targets16(a.dh, a.ld, jin, tr, one, old);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int t = tr[r];
         if (t < 0) continue;
-        if (a.mode == 0)
-          scatter_add(&a.dh[(size_t)t * a.ld + jin], acc[tm][tn][r], !SPLIT && sgl[k][rl]);
-        else
+        if (a.mode == 0) {
+          float* dst = &a.dh[(size_t)t * a.ld + jin];
+          if (one[r]) *dst = old[r] + acc[tm][tn][r];
+          else unsafeAtomicAdd(dst, acc[tm][tn][r]);
+        } else {
           unsafeAtomicAdd(&a.d_table[(size_t)t * a.tld + jin], acc[tm][tn][r]);
+        }
       }
     }
   }
@@ -769,16 +790,27 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
       if (n >= a.Nb) continue;
       const int k = a.mode == 0 ? n / a.HP : 0, jin = a.mode == 0 ? n - k * a.HP : n;
       if (jin >= (a.mode == 0 ? a.H : a.in_dim)) continue;
+      int tr[16];
+      bool one[16];
+      float old[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int rl = wr * 64 + tm * 32 + acc_row(r, lane), row = m0 + rl;
-        if (row >= a.rows) continue;
-        const int t = tgt[k][rl];
+        tr[r] = row < a.rows ? tgt[k][rl] : -1;
+        one[r] = !split && a.mode == 0 && tr[r] >= 0 && sgl[k][rl];
+      }
+      read_targets16(a.dh, a.ld, jin, tr, one, old);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int t = tr[r];
         if (t < 0) continue;
-        if (a.mode == 0)
-          scatter_add(&a.dh[(size_t)t * a.ld + jin], acc[tm][tn][r], !split && sgl[k][rl]);
-        else
+        if (a.mode == 0) {
+          float* dst = &a.dh[(size_t)t * a.ld + jin];
+          if (one[r]) *dst = old[r] + acc[tm][tn][r];
+          else unsafeAtomicAdd(dst, acc[tm][tn][r]);
+        } else {
           unsafeAtomicAdd(&a.d_table[(size_t)t * a.tld + jin], acc[tm][tn][r]);
+        }
       }
     }
   }
