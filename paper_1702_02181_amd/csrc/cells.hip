@@ -36,11 +36,10 @@ constexpr int kThreads = 256;
 
 inline unsigned cdiv(long long a, long long b) { return (unsigned)((a + b - 1) / b); }
 
-// dst += v for a node-gradient element: a plain read-add-write when the element has exactly one
-// writer in the launch (a child with one parent edge), else a hardware fp32 atomic add.
-__device__ __forceinline__ void scatter_add(float* dst, float v, bool single) {
+// dst += v given dst's old value (read ahead) when it has a single writer, else a hardware fp32 atomic add
+__device__ __forceinline__ void add_into(float* dst, float old, float v, bool single) {
   if (single)
-    *dst += v;
+    *dst = old + v;
   else
     unsafeAtomicAdd(dst, v);
 }
@@ -556,14 +555,17 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cl = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
       const float cr = c1 >= 0 ? a.c_pool[(size_t)c1 * a.ld + j] : 0.f;
+      // the children's dc read with the other loads, ahead of this row's stores
+      const float dc0 = c0 >= 0 && s0 ? a.dc[(size_t)c0 * a.ld + j] : 0.f;
+      const float dc1 = c1 >= 0 && s1 ? a.dc[(size_t)c1 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
       put(0, j, dct * u * i_ * (1.f - i_));
       put(1, j, dct * cl * fl * (1.f - fl));
       put(2, j, dct * cr * fr * (1.f - fr));
       put(3, j, dh * tc * o * (1.f - o));
       put(4, j, dct * i_ * (1.f - u * u));
-      if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dct * fl, s0);
-      if (c1 >= 0) scatter_add(&a.dc[(size_t)c1 * a.ld + j], dct * fr, s1);
+      if (c0 >= 0) add_into(&a.dc[(size_t)c0 * a.ld + j], dc0, dct * fl, s0);
+      if (c1 >= 0) add_into(&a.dc[(size_t)c1 * a.ld + j], dc1, dct * fr, s1);
     } else if constexpr (KIND == kTreeLstmLeaf) {
       const float dc = a.dc[p * a.ld + j];
       const float i_ = gate(0, j), o = gate(1, j), u = gate(2, j);
@@ -577,19 +579,25 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       const float i_ = gate(0, j), f = gate(1, j), o = gate(2, j), u = gate(3, j);
       const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cp = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
+      const float dc0 = c0 >= 0 && s0 ? a.dc[(size_t)c0 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
       put(0, j, dct * u * i_ * (1.f - i_));
       put(1, j, dct * cp * f * (1.f - f));
       put(2, j, dh * tc * o * (1.f - o));
       put(3, j, dct * i_ * (1.f - u * u));
-      if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dct * f, s0);
+      if (c0 >= 0) add_into(&a.dc[(size_t)c0 * a.ld + j], dc0, dct * f, s0);
     } else {
       const float h = gate(0, j);
+      float dc = 0.f, dc0 = 0.f;
+      if constexpr (KIND == FOLD_PROJ) {
+        dc = a.dc[p * a.ld + j];
+        dc0 = c0 >= 0 && s0 ? a.dc[(size_t)c0 * a.ld + j] : 0.f;
+      }
       put(0, j, dh * (1.f - h * h));
       if constexpr (KIND == FOLD_PROJ) {
-        const float dc = a.dc[p * a.ld + j];
-        if (c0 >= 0) scatter_add(&a.dc[(size_t)c0 * a.ld + j], dc, s0);
+        if (c0 >= 0) add_into(&a.dc[(size_t)c0 * a.ld + j], dc0, dc, s0);
       }
+      (void)dc0;
     }
   }
   if constexpr (BF && KIND != FOLD_EMBED) {
