@@ -413,7 +413,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     b.dc = dc;
     b.child_pos = s.child_pos;
     b.input_idx = s.input_idx;
-    b.npar = s.pos_npar;
+    b.child_one = s.child_one;
     b.d_table = d_table;
     b.tld = tld;
     b.dz_bf16 = p.dtype == FOLD_BF16;
@@ -437,7 +437,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     d.input_idx = s.input_idx;
     d.in_dim = ps.in_dim;
     d.tld = tld;
-    d.npar = s.pos_npar;
+    d.child_one = s.child_one;
     d.can_split = 1;
     d.zero = p.zero;
     if (op.arity > 0) {

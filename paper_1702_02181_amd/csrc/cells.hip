@@ -529,9 +529,15 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
   float* gb = a.gates + p * a.gstride;
   auto gate = [&](int g, int j) -> float { return gb[g * a.HP + j]; };  // saved activations (fp32)
   int c0 = -1, c1 = -1;
-  if (a.arity >= 1) c0 = a.child_pos[a.idx_off + row * a.arity];
-  if (a.arity >= 2) c1 = a.child_pos[a.idx_off + row * a.arity + 1];
-  const bool s0 = c0 >= 0 && a.npar[c0] == 1, s1 = c1 >= 0 && a.npar[c1] == 1;
+  bool s0 = false, s1 = false;
+  if (a.arity >= 1) {
+    c0 = a.child_pos[a.idx_off + row * a.arity];
+    s0 = a.child_one[a.idx_off + row * a.arity] != 0;
+  }
+  if (a.arity >= 2) {
+    c1 = a.child_pos[a.idx_off + row * a.arity + 1];
+    s1 = a.child_one[a.idx_off + row * a.arity + 1] != 0;
+  }
   auto put = [&](int g, int j, float v) {
     if constexpr (BF)
       sdz[g * a.HP + j] = f2bf(v);
@@ -649,7 +655,7 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
         if (a.mode == 0) {
           if (k < a.arity) {
             t = a.child_pos[a.idx_off + row * a.arity + k];
-            one = t >= 0 && a.npar[t] == 1;
+            one = a.child_one[a.idx_off + row * a.arity + k] != 0;
           }
         } else if (k == 0) {
           t = a.input_idx[a.row_begin + row];
@@ -745,7 +751,7 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
       if (a.mode == 0) {
         if (k < a.arity) {
           t = a.child_pos[a.idx_off + row * a.arity + k];
-          one = t >= 0 && a.npar[t] == 1;
+          one = a.child_one[a.idx_off + row * a.arity + k] != 0;
         }
       } else if (k == 0) {
         t = a.input_idx[a.row_begin + row];

@@ -100,6 +100,7 @@ struct Sched {
   int32_t *child_pos = nullptr, *input_idx = nullptr, *root_pos = nullptr;
   int32_t *pos_group = nullptr;   // [N] group of every pool row
   int32_t *pos_npar = nullptr;    // [N] number of parent edges of every pool row
+  int32_t *child_one = nullptr;   // [E] beside child_pos: 1 if that child has exactly one parent edge
   int32_t *op_rows = nullptr;     // [N] pool rows sorted by (op, row)
   int32_t *op_cpos = nullptr;     // [2N] child pool rows of op_rows[q] at 2q + k (-1 past the arity)
   int32_t *op_inp = nullptr;      // [N] leaf-table row of op_rows[q], or -1

@@ -148,7 +148,7 @@ struct BwdCellArgs {
   float* dc;
   const int* child_pos;
   const int* input_idx;
-  const int* npar;  // parent edges per pool row: 1 -> plain read-add-write, else atomic add
+  const int* child_one;  // beside child_pos: the child has one parent edge -> plain read-add-write
   float* d_table;
   int tld;
   int dz_bf16;  // write dz as bf16 (the operand type of bf16 parameters)
@@ -169,7 +169,7 @@ struct DxArgs {
   float* d_table;
   const int* input_idx;
   int in_dim, tld;
-  const int* npar;  // parent edges per pool row
+  const int* child_one;  // beside child_pos: the child has one parent edge
   int can_split;    // K may be split across workgroups (slices add into the targets atomically)
   int ksplit;       // set by the launcher
   int map;          // set by the launcher: workgroup order over the XCDs (kMapRows, kMapCols, kMapOwnCols)

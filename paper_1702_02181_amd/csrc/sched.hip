@@ -399,7 +399,7 @@ __global__ void k_group_rows(const int* ng_ptr, int N, const int* g_row_begin, c
 __global__ void k_emit(const int* pos_node, const int* node_pos, const int* gid, const int* g_row_begin,
                        const int* g_op, const int* g_idx_off, const int* cp, const int* ci,
                        const int* node_input, const int* indeg, int N, OpTable ops, int* child_pos,
-                       int* input_idx, int* pos_npar) {
+                       int* child_one, int* input_idx, int* pos_npar) {
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= N) return;
   const int v = pos_node[p];
@@ -410,6 +410,7 @@ __global__ void k_emit(const int* pos_node, const int* node_pos, const int* gid,
   for (int k = 0; k < a; ++k) {
     const int c = ci[c0 + k];
     child_pos[off + k] = c >= 0 ? node_pos[c] : -1;
+    child_one[off + k] = c >= 0 && indeg[c] == 1 ? 1 : 0;
   }
   input_idx[p] = node_input[v];
   pos_npar[p] = indeg[v];
@@ -535,7 +536,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   };
 
   // persistent arrays sized by N and E
-  const size_t n1 = (size_t)N * 11 + (size_t)E + 8;
+  const size_t n1 = (size_t)N * 11 + 2 * (size_t)E + 8;
   if (hipMalloc(&s.blob, n1 * sizeof(int)) != hipSuccess) {
     set_error("fold_schedule: out of device memory");
     return fail(FOLD_E_NOMEM);
@@ -547,6 +548,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   s.input_idx = q; q += N;
   s.root_pos = q; q += N;
   s.child_pos = q; q += E;
+  s.child_one = q; q += E;
   s.pos_group = q; q += N;
   s.pos_npar = q; q += N;
   s.op_rows = q; q += N;
@@ -674,7 +676,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
     scan_exclusive(d_edges, d_idx_off, (int)cap, m2 + 2, scan_tmp, st);
     hipLaunchKernelGGL(k_emit, grid_for(N), dim3(kBlock), 0, st, s.pos_node, s.node_pos, gid, d_row_begin,
                        d_op, d_idx_off, b->child_ptr, b->child_idx, b->node_input, indeg, N, ops, s.child_pos,
-                       s.input_idx, s.pos_npar);
+                       s.child_one, s.input_idx, s.pos_npar);
     hipLaunchKernelGGL(k_root_flags, grid_for(N), dim3(kBlock), 0, st, indeg, N, flag);
     scan_exclusive(flag, exs, N, m2 + 1, scan_tmp, st);
     hipLaunchKernelGGL(k_root_emit, grid_for(N), dim3(kBlock), 0, st, flag, exs, s.node_pos, N, s.root_pos);
