@@ -329,6 +329,55 @@ def level_classes(work: dict, launches: list, steps: int, peak_tflops: float, hb
     return out
 
 
+TABLE1_BATCHES = (1, 32, 64, 128, 256, 512, 1024)
+
+
+def table1(batches, steps: int, warmup: int, dtype: str = "f32") -> dict:
+    """The inference timing protocol of Section 2.1 (Table 1) on this GPU: batches of 127-node random trees
+    (H = 1024, embedding-lookup leaves), forward only, timed as HIP-graph replays.  "manual" runs one batched
+    group per tree node (one operation per node position), "dynamic" one group per (depth, op) over trees of
+    one shape, "full" the same over trees of random shapes.  cost ratio = dynamic / manual time per batch;
+    speedup ratio = manual time per tree at batch size 1 / full-dynamic time per tree."""
+    import torch
+
+    from paper_1702_02181_amd import gen
+    from paper_1702_02181_amd.runner import DeviceRun
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    rows = []
+    for B in batches:
+        row = {"batch": B}
+        for mode in ("manual", "dynamic", "full"):
+            w = gen.table1(B, mode, dtype=dtype)
+            dev = DeviceRun(w)
+            graph = dev.make_graph(backward=False)
+            ms = timed(graph.launch)
+            row[mode] = {"batch_ms": round(ms, 4), "tree_ms": round(ms / B, 5),
+                         "groups": len(dev.sched.host_groups()["group_op"]), "kernels": graph.num_nodes}
+            del graph, dev
+        row["cost_ratio"] = round(row["dynamic"]["batch_ms"] / row["manual"]["batch_ms"], 3)
+        rows.append(row)
+        print(f"[table1] batch {B}: manual {row['manual']['batch_ms']:.3f} ms, dynamic "
+              f"{row['dynamic']['batch_ms']:.3f} ms, full {row['full']['batch_ms']:.3f} ms", file=sys.stderr, flush=True)
+    base = next((r["manual"]["tree_ms"] for r in rows if r["batch"] == 1), None)
+    for r in rows:
+        r["speedup_ratio"] = None if base is None else round(base / r["full"]["tree_ms"], 2)
+    return {"table1": rows, "tree_nodes": 127, "hidden": 1024, "dtype": dtype, "pass": "forward",
+            "steps": steps, "warmup": warmup}
+
+
 def cpu_baseline(w, budget_s: float):
     """The oracle as it stands, single thread, on whole graphs of the workload until ~budget_s."""
     from threadpoolctl import threadpool_limits
@@ -368,6 +417,8 @@ def main():
     ap.add_argument("--profile-only", action="store_true", help="skip the oracle leg and the schedule timing")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--traffic-kernel", default=None)
+    ap.add_argument("--table1", action="store_true",
+                    help="run the Table 1 protocol (manual / dynamic / full-dynamic batching) instead")
     ap.add_argument("--counters-from", nargs=4, metavar=("MFMA_CSV", "FETCH_CSV", "WRITE_CSV", "TRACE_CSV"),
                     help="print the per-kernel MFMA utilisation / HBM bandwidth table of four rocprofv3 runs")
     args = ap.parse_args()
@@ -379,6 +430,11 @@ def main():
         w = _gen.make_config(args.config)
         rec = traffic_from_counters(args.traffic_from[0], args.traffic_from[1], args.traffic_kernel, w.name)
         print(TRAFFIC_TAG, json.dumps(rec))
+        return
+    if args.table1:
+        import torch
+        torch.cuda.set_device(0)
+        print(json.dumps(table1(TABLE1_BATCHES, args.steps, args.warmup)), flush=True)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the dynamic-batching path here is a single-GPU build "

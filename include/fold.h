@@ -95,7 +95,7 @@ typedef struct {
   int32_t num_graphs;        /* G >= 0 */
   int32_t num_nodes;         /* N >= 0 */
   int32_t num_edges;         /* E >= 0, = child_ptr[N] */
-  int32_t num_ops;           /* >= 1 */
+  int32_t num_ops;           /* 1 .. 256 (more: FOLD_E_INVALID) */
   int32_t num_inputs;        /* rows of the leaf table that node_input may name */
   const int32_t* graph_ptr;  /* device [G+1], graph_ptr[0] = 0, graph_ptr[G] = N, nondecreasing */
   const int32_t* node_op;    /* device [N] */

@@ -26,7 +26,7 @@ namespace {
 
 constexpr unsigned long long kNoErr = ~0ull;
 constexpr int kBlock = 256;
-constexpr int kMaxOps = 64;
+constexpr int kMaxOps = 256;  // the op table travels as a kernel argument (2 KB)
 constexpr int kDepthLdsInts = 8192;  // 32 KiB per workgroup; larger graphs use global scratch
 constexpr int kScanItems = 8;        // items per thread in device-wide scans
 constexpr int kScanTile = kBlock * kScanItems;
@@ -513,7 +513,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
       return FOLD_E_INVALID;
     }
   if (K > kMaxOps) {
-    set_error("fold_schedule: at most 64 operations are supported");
+    set_error("fold_schedule: at most 256 operations are supported");
     return FOLD_E_INVALID;
   }
   OpTable ops{};

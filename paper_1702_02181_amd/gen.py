@@ -488,6 +488,47 @@ def config5(seed: int = 5, num_graphs: int = 4096, hidden: int = 1024, vocab: in
 CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
 
 
+def table1(batch: int, mode: str, seed: int = 7, leaves: int = 64, hidden: int = 1024, vocab: int = 10000,
+           dtype: str = "f32") -> Workload:
+    """The inference timing benchmark of Section 2.1 (Table 1): `batch` random binary trees of `leaves` leaves
+    (2 leaves - 1 nodes: 64 leaves = 127 nodes, the table's tree size of 128), leaves looked up in an embedding
+    table, internal nodes a binary Tree-LSTM with state size `hidden`; forward only.
+      "dynamic": every tree has the same random shape; two operations (leaf, internal node).
+      "full":    every tree has a random shape of its own ("full dynamic").
+      "manual":  the same shape as "dynamic", and every node position of the tree is an operation of its own,
+                 all sharing one parameter set: the schedule then has one batched group per tree node, which is
+                 what manual batching runs (one batched kernel per node of the tree's static graph).
+    Tokens ~ U{0..vocab-1}; table ~ N(0, 0.1^2); weights U(-0.1, 0.1)."""
+    if mode not in ("dynamic", "full", "manual"):
+        raise ValueError(mode)
+    rng = np.random.default_rng(seed)
+    H = hidden
+    toks = rng.integers(0, vocab, size=(batch, leaves))
+    shape_rng = np.random.default_rng(seed + 1)
+    graphs = []
+    base = None
+    for t in range(batch):
+        b = _GraphBuilder()
+        # same shape: replay the same split choices for every tree
+        r = shape_rng if mode == "full" else np.random.default_rng(seed + 1)
+        random_split_tree(b, leaves, r, 0, 1, toks[t])
+        op, cnt, kids, inp = b.arrays()
+        if mode == "manual":
+            if base is None:
+                base = op.copy()
+            op = np.arange(op.shape[0], dtype=np.int32)  # node position = operation id
+        graphs.append((op, cnt, kids, inp))
+    csr = assemble(graphs)
+    if mode == "manual":
+        ops = [OpSpec(KIND_TREELSTM, 0, 1, 0) if k == 0 else OpSpec(KIND_TREELSTM, 2, 0, 0) for k in base]
+    else:
+        ops = [OpSpec(KIND_TREELSTM, 0, 1, 0), OpSpec(KIND_TREELSTM, 2, 0, 0)]
+    E = _finish_values(0.1 * rng.standard_normal((vocab, H)), dtype)
+    params = [make_param_set(rng, KIND_TREELSTM, H, 2, H, dtype)]
+    return _finish(f"table1_{mode}_b{batch}_n{2 * leaves - 1}_h{H}_{dtype}", dtype, H, csr, ops, params, E, rng,
+                   backward=False)
+
+
 def make_config(k: int, **kw) -> Workload:
     return CONFIGS[k](**kw)
 

@@ -51,3 +51,33 @@ def test_config5_small_shape():
     assert np.all(gen.roots_per_graph(w.graph_ptr, w.child_idx) == 1)
     indeg = np.bincount(w.child_idx[w.child_idx >= 0], minlength=w.num_nodes)
     assert indeg.max() >= 2                     # some sub-expressions are shared
+
+
+def test_table1_workloads():
+    """Table 1 (Section 2.1): trees of 127 nodes (64 leaves) with embedding-lookup leaves; "dynamic" repeats one
+    random shape, "full" draws a shape per tree, "manual" is the dynamic batch with one operation per node
+    position.  The reference scheduler then gives one group per tree node for "manual" and one per (depth, op)
+    otherwise, and the fp64 oracle computes identical states for "manual" and "dynamic"."""
+    from oracle import evaluate as EV
+    from oracle import schedule as OS
+    from tests._helpers import oracle_batch, oracle_params
+    B = 6
+    d, m, f = (gen.table1(B, k, hidden=4, vocab=30) for k in ("dynamic", "manual", "full"))
+    for w in (d, m, f):
+        assert w.num_graphs == B and np.all(np.diff(w.graph_ptr) == 127) and not w.backward
+    assert np.array_equal(d.child_idx, m.child_idx) and np.array_equal(d.node_input, m.node_input)
+    assert np.all(d.child_idx.reshape(B, -1) - d.child_idx.reshape(B, -1)[0] == (np.arange(B) * 127)[:, None])
+    assert not np.array_equal(f.child_idx, d.child_idx)
+    assert m.num_ops == 127 and sorted(set(m.node_op.tolist())) == list(range(127))
+    def sched(w):
+        b = oracle_batch(w)
+        return OS.reference_schedule(b["node_op"], b["child_ptr"], b["child_idx"], b["node_input"], b["ops"])
+    sm = sched(m)
+    assert len(sm["group_rows"]) == 127 and all(int(r) == B for r in sm["group_rows"])
+    sd = sched(d)
+    # one group per (depth, op): at most two per depth, every group a multiple of the batch
+    assert sd["num_levels"] <= len(sd["group_rows"]) <= 2 * sd["num_levels"]
+    assert all(int(r) % B == 0 for r in sd["group_rows"])
+    hd = EV.forward(oracle_batch(d), oracle_params(d), d.hidden, d.leaf_table)["h"]
+    hm = EV.forward(oracle_batch(m), oracle_params(m), m.hidden, m.leaf_table)["h"]
+    assert np.array_equal(hd, hm)

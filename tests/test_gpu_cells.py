@@ -81,3 +81,12 @@ def test_batching_invariance_on_gpu():
         assert C.compare_all.__module__  # keep the import live
         from oracle.compare import rel_err
         assert rel_err(gk["h"], g["h"][gp[k]:gp[k + 1]]) <= 1e-2
+
+
+@pytest.mark.parametrize("mode", ["manual", "dynamic", "full"])
+def test_table1_workloads_forward(mode):
+    """The three schedules of the Table 1 protocol (one group per tree node; per (depth, op); random shapes)
+    compute the fp64 oracle's states of the same trees (fp32, H = 1024 as in the table)."""
+    w = gen.table1(3, mode, hidden=1024, vocab=200)
+    g, o = C.run_device(w), C.run_oracle(w)
+    C.compare_all(w, g, o)

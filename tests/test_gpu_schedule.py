@@ -111,3 +111,19 @@ def test_empty_batch():
                      leaf_table=np.zeros((1, 2), np.float32), dh_roots=np.zeros((0, 2), np.float32))
     g = _gpu_sched(w)
     assert g["num_levels"] == 0 and g["num_groups"] == 0 and g["num_roots"] == 0
+
+
+def test_many_operations_one_group_per_tree_node():
+    """Table 1's manual-batching emulation: every node position of a 127-node tree is an operation of its
+    own, so the schedule has one group per tree node, bit-exact against the reference scheduler; 256
+    operations are accepted and 257 rejected."""
+    w = gen.table1(5, "manual", hidden=8, vocab=50)
+    assert w.num_ops == 127
+    g = _gpu_sched(w)
+    C.assert_schedule_equal(g, C.oracle_schedule(w))
+    assert g["num_groups"] == 127 and list(g["host"]["group_rows"]) == [5] * 127
+    many = gen.subset(w, range(5))
+    many.ops = list(w.ops) + [gen.OpSpec(gen.KIND_TREELSTM, 2, 0, 0)] * (256 - 127)
+    C.assert_schedule_equal(_gpu_sched(many), C.oracle_schedule(many))
+    many.ops = many.ops + [gen.OpSpec(gen.KIND_TREELSTM, 2, 0, 0)]
+    assert _err(many) == -1
