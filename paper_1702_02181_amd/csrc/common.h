@@ -161,9 +161,14 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
 
 // Gate nonlinearities on the hardware exp2 / reciprocal units (v_exp_f32, v_rcp_f32, about one ulp
 // each): sigma(x) = 1 / (1 + e^-x); for x -> -inf, e^-x overflows to +inf and the reciprocal gives 0.
-// tanh(x) = 2 sigma(2x) - 1, absolute error a few 1e-7 (relative error grows only as tanh -> 0).
+// tanh(x) = 2 sigma(2x) - 1 (absolute error a few 1e-7) for |x| >= 1/8; below, where that difference would lose
+// the relative accuracy, the odd Taylor series x - x^3/3 + 2x^5/15 - 17x^7/315 (truncation < 2e-10 relative).
 __device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
 __device__ __forceinline__ float sigmoidf_(float x) { return __builtin_amdgcn_rcpf(1.f + fast_exp(-x)); }
-__device__ __forceinline__ float tanhf_(float x) { return 2.f * sigmoidf_(2.f * x) - 1.f; }
+__device__ __forceinline__ float tanhf_(float x) {
+  const float x2 = x * x;
+  const float series = x * (1.f + x2 * (-1.f / 3.f + x2 * (2.f / 15.f + x2 * (-17.f / 315.f))));
+  return fabsf(x) < 0.125f ? series : 2.f * sigmoidf_(2.f * x) - 1.f;
+}
 
 }  // namespace fold
