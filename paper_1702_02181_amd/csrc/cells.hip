@@ -844,18 +844,15 @@ void cell_fwd_kind(const FwdArgs& a0, hipStream_t st) {
     return;
   }
   a.ksplit = pl.ksplit;
-  const int BM = 128 * pl.mt;
   const int G = Gates<KIND>::G;
-  const int R = (int)cdiv(a.rows, BM), UB = a.HP / 32;
+  const int R = (int)cdiv(a.rows, 128), UB = a.HP / 32;  // 128-row tiles of one unit block
   a.map = a.rows >= G * a.HP ? kMapRows : kMapCols;  // gathered rows outweigh the weights: share row tiles
   dim3 grid(a.map == kMapRows ? xcd_grid(UB * pl.ksplit, R) : xcd_grid(R * pl.ksplit, UB));
   if (pl.ksplit > 1) {
-    if (pl.mt == 2) hipLaunchKernelGGL((k_cell_fwd<T, KIND, 2, true>), grid, dim3(kThreads), 0, st, a);
-    else hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, true>), grid, dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, true>), grid, dim3(kThreads), 0, st, a);
     hipLaunchKernelGGL((k_cell_epi<T, KIND>), dim3(a.rows), dim3(std::min(a.HP, 1024)), 0, st, a, pl.ksplit);
   } else {
-    if (pl.mt == 2) hipLaunchKernelGGL((k_cell_fwd<T, KIND, 2, false>), grid, dim3(kThreads), 0, st, a);
-    else hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, false>), grid, dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, false>), grid, dim3(kThreads), 0, st, a);
   }
 }
 

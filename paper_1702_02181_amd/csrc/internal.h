@@ -75,7 +75,7 @@ void launch_cell_fwd(int dtype, int kind, const FwdArgs& a, hipStream_t st);
 // unit block and, if still short of workgroups, split K (partial sums in the workspace, then an
 // epilogue kernel).
 struct FwdPlan {
-  int mt = 1, ksplit = 1;
+  int ksplit = 1;
   bool wide = false;  // 256 rows x 2 unit blocks per workgroup of 8 waves
 };
 inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bool can_split) {
@@ -87,7 +87,7 @@ inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bo
   // partial sums through the workspace costs more than a wide tile gains)
   p.wide = ((long long)(rows + 255) / 256) * (ub / 2) >= 256;
   if (p.wide) return p;
-  const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * ub;
+  const long long base = ((long long)(rows + 127) / 128) * ub;
   if (can_split && base < 192 && nst >= 4) {
     const long long want = (256 + base - 1) / base;
     p.ksplit = (int)std::min<long long>(want, nst / 2);
