@@ -29,6 +29,7 @@ constexpr int kThreads = 256;
 // Workgroup tile: 128 weight rows (m) x 256 gate columns (n); waves 2 x 2, each 64 x 128.
 constexpr int kTM = 128;  // weight rows per tile
 constexpr int kWgNW = 128;  // fp32 tile columns (two workgroups per compute unit)
+constexpr int kWgWideF32Rows = 32768;  // fp32 ops with at least this many rows may use 256 x 256 tiles
 
 // ---------------------------------------------------------------- fp32: direct loads into LDS
 // A stage is 32 op rows.  X^T tile: the 32 rows x 128 weight rows (512 bytes a row), dz^T tile: the 32
@@ -526,6 +527,170 @@ __global__ __launch_bounds__(wide::kThreads) void k_wgrad_bf16_w(WgArgs a) {
   if (do_bias && n0 + bc < a.Nw) a.bpart[((size_t)chunk_id * 2 + bg) * a.Nw + n0 + bc] = bsum;
 }
 
+// ---------------------------------------------------------------- fp32, wide: 256 x 256 tiles
+// Ops with many rows: 256 weight rows x 256 gate columns per workgroup of 8 waves (wave tile 64 x 128),
+// twice the operand reuse of the 128 x 128 tiles above, so each matrix instruction needs half the
+// L2 -> LDS feed.  A stage is 16 op rows: X^T (16 x 256) and dz^T (16 x 256), 16 KB each, row-major in the
+// op rows, one op row (1 KB) per direct-load instruction; odd rows have their 16-byte units permuted by
+// ^ 8 as in the 128-column kernel.  Four stage slots keep three stages in flight (waves 0-3 load, four
+// op rows of X and four of dz each); the op rows' indices reach LDS through an index ring six stages
+// ahead of the data, loaded by wave 4 alone (one 4-byte-per-lane direct load per stage), so every wait
+// counts only its own loads.
+__global__ __launch_bounds__(wide::kThreads) void k_wgrad_f32_w(WgArgs a) {
+  constexpr int TB = 256, TM = 2, TN = 4, NL = 8, RS = 16;
+  constexpr int ABYTES = RS * TB * 4, SLOT = 2 * ABYTES;  // X^T then dz^T
+  constexpr int NIDX = 8;  // index ring: per stage [op_rows 16 | op_inp 16 | op_cpos 32] ints
+  __shared__ __attribute__((aligned(16))) char ring[wide::kSlots * SLOT];
+  __shared__ __attribute__((aligned(16))) int iring[NIDX][64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
+  const int wr = wave & 3, wc = wave >> 2, h = lane >> 5, l32 = lane & 31;
+  const int NT = (a.Nw + TB - 1) / TB, MTm = (a.Kw + TB - 1) / TB;
+  int tx, chunk_id;
+  if (!xcd_tile(MTm * NT, a.nchunk, tx, chunk_id)) return;
+  const int mt_ = tx % MTm, nt = tx / MTm;
+  const int m0 = mt_ * TB, n0 = nt * TB;
+  const int lo = chunk_id * a.chunk, hi = min(a.count, lo + a.chunk);
+  const int nst = (hi - lo + RS - 1) / RS;
+  const char* zero = static_cast<const char*>(a.zero);
+  const char* xbase = static_cast<const char*>(a.src);
+  const char* dzbase = reinterpret_cast<const char*>(a.dz);
+  const size_t xstride = (size_t)(a.seg ? a.ld : a.tld) * 4, dstride = (size_t)a.gstride * 4;
+
+  // index loads (wave 4): stage c's indices into ring slot c % NIDX (rows past the chunk clamped to its
+  // last row)
+  auto issue_idx = [&](int c) {
+    const int q0 = lo + c * RS;
+    const int* src;
+    if (lane < 32) {
+      const int q = min(q0 + (lane & 15), hi - 1);
+      src = lane < 16 ? a.op_rows + q : a.op_inp + q;
+    } else {
+      src = a.op_cpos + min(2 * q0 + (lane - 32), 2 * hi - 1);
+    }
+    dma4_untracked(src, iring[c % NIDX]);
+  };
+  // waves 0-3: op rows 4 wr .. 4 wr + 3 of stage c; lane l fetches global unit l ^ 8 (r & 1) of each row
+  // (the wave's indices come in four 16-byte reads, all before the first load)
+  auto issue = [&](int c, char* sl) {
+    const int* ix = iring[c % NIDX];
+    const int q0 = lo + c * RS;
+    int rw[4], inp[4], cp[8];
+    *reinterpret_cast<int4*>(rw) = *reinterpret_cast<const int4*>(ix + 4 * wr);
+    *reinterpret_cast<int4*>(inp) = *reinterpret_cast<const int4*>(ix + 16 + 4 * wr);
+    *reinterpret_cast<int4*>(cp) = *reinterpret_cast<const int4*>(ix + 32 + 8 * wr);
+    *reinterpret_cast<int4*>(cp + 4) = *reinterpret_cast<const int4*>(ix + 36 + 8 * wr);
+    const char* xs[4];
+    const char* ds[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * wr + i;
+      const int gu = lane ^ (8 * (r & 1));
+      const bool live = q0 + r < hi;
+      // X^T: weight rows m0 + 4 gu .. + 3
+      const int m = m0 + 4 * gu;
+      const int child = a.seg ? min(m / a.HP, 1) : 0;
+      const int xi = a.seg ? (child ? cp[2 * i + 1] : cp[2 * i]) : inp[i];
+      const int col = a.seg ? m - child * a.HP : m;
+      xs[i] = live && m < a.Kw && xi >= 0 ? xbase + (size_t)xi * xstride + (size_t)col * 4 : zero;
+      // dz^T: gate columns n0 + 4 gu .. + 3
+      const int n = n0 + 4 * gu;
+      ds[i] = live && n < a.Nw ? dzbase + (size_t)rw[i] * dstride + (size_t)n * 4 : zero;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      dma16_untracked(xs[i], sl + (4 * wr + i) * 1024);
+      dma16_untracked(ds[i], sl + ABYTES + (4 * wr + i) * 1024);
+    }
+  };
+  // fragment byte offsets: K value h of step s is op row 2 s + h
+  int aoff[TM], boff[TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int kw = wr * 64 + tm * 32 + l32;
+    aoff[tm] = h * 1024 + ((kw >> 2) ^ (8 * h)) * 16 + (kw & 3) * 4;
+  }
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+    const int n = wc * 128 + tn * 32 + l32;
+    boff[tn] = h * 1024 + ((n >> 2) ^ (8 * h)) * 16 + (n & 3) * 4;
+  }
+  // bias column sums (tiles of the first weight-row tile only): thread t sums column t % 256 over the
+  // stage rows 8 (t / 256) .. + 7
+  const bool do_bias = a.bpart != nullptr && mt_ == 0;
+  const int bc = tid & 255, bg = tid >> 8;
+  float bsum = 0.f;
+
+  f32x16 acc[TM][TN];
+  zero_acc(acc);
+  const bool dloads = wave < 4, iloads = wave == 4;
+  if (nst > 0) {
+    if (iloads) {
+      for (int c = 0; c < min(nst, 6); ++c) issue_idx(c);
+      if (nst > 5) vm_wait_n<3>();  // indices of stages 0-2 landed, 3-5 in flight
+      else if (nst > 4) vm_wait_n<2>();
+      else if (nst > 3) vm_wait_n<1>();
+      else vm_wait();
+    }
+    wg_barrier();
+    if (dloads)
+      for (int c = 0; c < min(nst, 3); ++c) issue(c, ring + c * SLOT);
+    for (int c = 0; c < nst; ++c) {
+      if (dloads) {
+        if (c + 2 < nst) vm_wait_n<2 * NL>();
+        else if (c + 1 < nst) vm_wait_n<NL>();
+        else vm_wait();
+      }
+      if (iloads) {  // indices of stage c + 3 (issued at stage c - 3) landed; c + 4, c + 5 may be in flight
+        const int later = min(2, max(0, nst - 1 - (c + 3)));
+        if (later == 2) vm_wait_n<2>();
+        else if (later == 1) vm_wait_n<1>();
+        else vm_wait();
+      }
+      // the previous stage's LDS reads (bias sums included) are done before its slot is refilled
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      wg_barrier();
+      if (dloads && c + 3 < nst) issue(c + 3, ring + ((c + 3) & 3) * SLOT);
+      if (iloads && c + 6 < nst) issue_idx(c + 6);
+      __builtin_amdgcn_sched_barrier(0);
+      const char* As = ring + (c & 3) * SLOT;
+      const char* Bs = As + ABYTES;
+#pragma unroll
+      for (int s = 0; s < RS / 2; ++s) {
+        float av[TM], bv[TN];
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) av[tm] = *reinterpret_cast<const float*>(As + aoff[tm] + s * 2048);
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) bv[tn] = *reinterpret_cast<const float*>(Bs + boff[tn] + s * 2048);
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+            acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[tm], bv[tn], acc[tm][tn], 0, 0, 0);
+      }
+      if (do_bias) {
+#pragma unroll
+        for (int r = 8 * bg; r < 8 * bg + 8; ++r)
+          bsum += *reinterpret_cast<const float*>(Bs + r * 1024 + (((bc >> 2) ^ (8 * (r & 1))) * 16) + (bc & 3) * 4);
+      }
+    }
+  }
+
+  float* out = a.partial + (size_t)chunk_id * a.Kw * a.Nw;
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int n = n0 + wc * 128 + tn * 32 + l32;
+      if (n >= a.Nw) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wr * 64 + tm * 32 + acc_row(r, lane);
+        if (m < a.Kw) out[(size_t)m * a.Nw + n] = acc[tm][tn][r];
+      }
+    }
+  if (do_bias && n0 + bc < a.Nw) a.bpart[((size_t)chunk_id * 2 + bg) * a.Nw + n0 + bc] = bsum;
+}
+
 // dW[row, col] += sum over chunks of partial[chunk, m, n], (m, n) in the padded layout
 __global__ void k_wgrad_reduce(const float* partial, int nchunk, int Kw, int Nw, int seg, int H, int HP,
                                int in_dim, int G, int gcode, float* dW) {
@@ -606,7 +771,8 @@ __global__ void k_bias_reduce(const float* bpart, int nparts, int Nw, int H, int
 // the workgroups that an XCD runs at once on the same rows, so the rows they share stay in its L2
 // (measured on 1.25 M rows: 64 chunks of ~20 k rows cut the contraction from 44.6 to 42.2 ms against 8
 // chunks; more chunks gain nothing and cost more in the partial-tile reduction).
-static int wgrad_chunks(long long tiles, int count, int min_rows, int max_rows, int slots_per_xcd) {
+static int wgrad_chunks(long long tiles, int count, int min_rows, int max_rows, int slots_per_xcd,
+                        double* fill = nullptr) {
   const long long most8 = std::max(1, count / (8 * min_rows));  // chunks per XCD at most
   const long long least8 = std::min<long long>(most8, std::max<long long>(1, ((long long)count + 8LL * max_rows - 1) /
                                                                                  (8LL * max_rows)));
@@ -621,16 +787,26 @@ static int wgrad_chunks(long long tiles, int count, int min_rows, int max_rows, 
     }
     if (eff >= 0.9 && wg >= slots_per_xcd) break;
   }
+  if (fill) *fill = best_eff;
   return 8 * best;
 }
 
 WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype) {
   WgradSplit w;
   if (count <= 0 || Kw <= 0 || Nw <= 0) return w;
-  // bf16 ops with many rows: 256 x 256 tiles (twice the operand reuse of 128 x 128), one workgroup per CU
-  w.wide = dtype == FOLD_BF16 && count >= 65536;
-  const long long tiles = w.wide ? (long long)((Kw + 255) / 256) * ((Nw + 255) / 256)
-                                 : (long long)((Kw + kTM - 1) / kTM) * ((Nw + 127) / 128);
+  // ops with many rows: 256 x 256 tiles (twice the operand reuse of 128 x 128), one workgroup per CU.
+  // fp32 takes them only where their workgroups fill the compute units' slots (at least 90 %): on 65 k
+  // rows, H = 256, the node weights' 10 tiles gain 5 % over 128 x 128, the leaf weights' 3 tiles (75 %
+  // full) lose 11 %
+  const long long wtiles = (long long)((Kw + 255) / 256) * ((Nw + 255) / 256);
+  if (dtype == FOLD_BF16) {
+    w.wide = count >= 65536;
+  } else if (count >= kWgWideF32Rows) {
+    double fill = 0.0;
+    wgrad_chunks(wtiles, count, 1024, 20480, 32, &fill);
+    w.wide = fill >= 0.9;
+  }
+  const long long tiles = w.wide ? wtiles : (long long)((Kw + kTM - 1) / kTM) * ((Nw + 127) / 128);
   w.nchunk = wgrad_chunks(tiles, count, w.wide ? 1024 : 512, w.wide ? 20480 : (1 << 30), w.wide ? 32 : 64);
   w.chunk = round_up((count + w.nchunk - 1) / w.nchunk, 64);
   w.nchunk = (count + w.chunk - 1) / w.chunk;
@@ -644,7 +820,8 @@ void launch_wgrad(int dtype, const WgArgs& a, hipStream_t st) {
   ProfScope prof(dtype == FOLD_BF16 ? "wgrad.bf16" : "wgrad.f32", st);
   if (a.wide) {
     dim3 grid(xcd_grid(((a.Kw + 255) / 256) * ((a.Nw + 255) / 256), a.nchunk));
-    hipLaunchKernelGGL(k_wgrad_bf16_w, grid, dim3(wide::kThreads), 0, st, a);
+    if (dtype == FOLD_BF16) hipLaunchKernelGGL(k_wgrad_bf16_w, grid, dim3(wide::kThreads), 0, st, a);
+    else hipLaunchKernelGGL(k_wgrad_f32_w, grid, dim3(wide::kThreads), 0, st, a);
   } else if (dtype == FOLD_BF16) {
     dim3 grid(xcd_grid(((a.Kw + kTM - 1) / kTM) * ((a.Nw + 127) / 128), a.nchunk));
     hipLaunchKernelGGL(k_wgrad_bf16, grid, dim3(kThreads), 0, st, a);

@@ -132,3 +132,14 @@ def test_wide_dx_two_k_slices_bf16():
     assert any(128 <= t < 256 for t in tiles), tiles
     sizes = np.diff(w.graph_ptr)
     _sampled_parity(w, [0, 1 + 2 * int(np.argmax(sizes[1::2]))], table_grad=True)
+
+
+def test_wide_weight_gradients_f32_ragged_tiles():
+    """fp32 ops of at least 32 k rows whose 256 x 256 weight-gradient tiles fill the compute units take
+    them.  H = 300 (padded to 320) leaves ragged tiles on every side: the leaves' 300-wide inputs (two
+    weight-row tiles, the second partial) against 3 x 320 gate columns, and the children's rows 2 x 320
+    (the second child's rows start inside the second weight-row tile) against 5 x 320 gate columns
+    (partial last column tiles).  160 balanced trees: 40,960 leaves and 40,800 internal nodes, row counts
+    that are no multiple of a stage.  Sampled parity as above, with the leaf-table gradient."""
+    w = gen.config2(num_graphs=160, hidden=300)
+    _sampled_parity(w, [0, 77, 159], table_grad=True)
