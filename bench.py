@@ -378,6 +378,54 @@ def table1(batches, steps: int, warmup: int, dtype: str = "f32") -> dict:
             "steps": steps, "warmup": warmup}
 
 
+def train_bench(config: int, steps: int, warmup: int, classes: int = 5) -> dict:
+    """Training steps of Section 3.3's setting on one workload: a class label on every node (uniform, seeded),
+    forward, the per-node softmax cross-entropy head, backward from the head's gradients, Adam on every
+    parameter tensor (weights, biases, the leaf table where it is trained, the classifier) and the in-place
+    re-pack of the weights, issued call by call.  The batch is the same every step, so the mean loss falls."""
+    import numpy as np
+    import torch
+
+    from paper_1702_02181_amd import fold as F
+    from paper_1702_02181_amd import gen
+    from paper_1702_02181_amd.runner import TrainStep
+    stream = torch.cuda.current_stream()
+    w = gen.make_config(config)
+    labels = np.random.default_rng(11).integers(0, classes, w.num_nodes).astype(np.int32)
+    ts = TrainStep(w, labels, classes, train_table=config in (3, 5))
+    mean_loss = lambda: float(ts.node_loss[:w.num_nodes].sum().item() * ts.scale)
+    ts.step()
+    torch.cuda.synchronize()
+    first = mean_loss()
+    for _ in range(max(0, warmup - 1)):
+        ts.step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        ts.step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    last = mean_loss()
+    F.fold_profile_enable(True)
+    for _ in range(steps):
+        ts.step()
+    torch.cuda.synchronize()
+    stats = F.fold_profile_read()
+    F.fold_profile_enable(False)
+    kernels = {k: {"launches_per_step": n / steps, "ms_per_step": round(tot / steps, 4)}
+               for k, (n, tot, _mx) in stats.items()}
+    return {"metric": "training graph nodes/sec (Tree-LSTM, per-node softmax loss, Adam; 1 GPU)",
+            "value": round(w.num_nodes / (ms * 1e-3), 1), "unit": "graph nodes/s", "n_gpus": 1, "steps": steps,
+            "warmup": warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "dtype": w.dtype,
+            "data": "synthetic", "config": {"workload": w.name, "nodes": w.num_nodes, "hidden": w.hidden,
+                                            "classes": classes, "optimizer": "adam lr 1e-3 (0.9, 0.999, 1e-8)",
+                                            "trained_leaf_table": config in (3, 5)},
+            "mean_loss": {"step_1": round(first, 5), f"step_{ts.t - steps}": round(last, 5)},
+            "kernels": kernels}
+
+
 def cpu_baseline(w, budget_s: float):
     """The oracle as it stands, single thread, on whole graphs of the workload until ~budget_s."""
     from threadpoolctl import threadpool_limits
@@ -419,6 +467,8 @@ def main():
     ap.add_argument("--traffic-kernel", default=None)
     ap.add_argument("--table1", action="store_true",
                     help="run the Table 1 protocol (manual / dynamic / full-dynamic batching) instead")
+    ap.add_argument("--train", action="store_true",
+                    help="time training steps (per-node softmax loss, Adam, re-pack) instead; default config 3")
     ap.add_argument("--counters-from", nargs=4, metavar=("MFMA_CSV", "FETCH_CSV", "WRITE_CSV", "TRACE_CSV"),
                     help="print the per-kernel MFMA utilisation / HBM bandwidth table of four rocprofv3 runs")
     args = ap.parse_args()
@@ -430,6 +480,12 @@ def main():
         w = _gen.make_config(args.config)
         rec = traffic_from_counters(args.traffic_from[0], args.traffic_from[1], args.traffic_kernel, w.name)
         print(TRAFFIC_TAG, json.dumps(rec))
+        return
+    if args.train:
+        import torch
+        torch.cuda.set_device(0)
+        cfg = args.config if "--config" in sys.argv else 3
+        print(json.dumps(train_bench(cfg, args.steps, args.warmup)), flush=True)
         return
     if args.table1:
         import torch

@@ -38,8 +38,9 @@
  *     (pools) and must hold zeros in inputs (the leaf table): the kernels
  *     load whole 128-byte row segments and meet those columns with zero
  *     weights, so any finite value there is harmless and NaN / Inf is not.
- *   - Handles are immutable after creation and may be shared by concurrent
- *     calls on different streams that use different output buffers.
+ *   - Handles are immutable after creation (fold_pack_update aside, which
+ *     rewrites a packed handle's weights in place) and may be shared by
+ *     concurrent calls on different streams that use different output buffers.
  */
 #ifndef FOLD_H_
 #define FOLD_H_
@@ -178,6 +179,16 @@ typedef struct {
 int32_t fold_pack_params(const fold_params* params, hipStream_t stream, fold_packed** out);
 int32_t fold_packed_free(fold_packed* packed);
 
+/* Re-pack new values of the same parameters into an existing handle (a
+ * training loop after each optimizer step): `params` must match the handle
+ * in dtype, hidden, number of sets and each set's kind, in_dim and arity
+ * (FOLD_E_MISMATCH otherwise; FOLD_E_INVALID for the checks of
+ * fold_pack_params).  Enqueued on `stream`; asynchronous; allocates
+ * nothing; the packed buffers keep their addresses, so HIP graphs recorded
+ * with the handle stay valid.  The caller orders it after every pass that
+ * still reads the old weights and before every pass that needs the new. */
+int32_t fold_pack_update(fold_packed* packed, const fold_params* params, hipStream_t stream);
+
 /* Row stride, in elements, that the library uses for a row of `width`
  * elements (pools, root outputs, gradients of node states, leaf tables):
  * width rounded up to a multiple of 64. */
@@ -239,6 +250,60 @@ int32_t fold_backward(const fold_sched* sched, const fold_packed* packed,
                       const float* dh_roots, const float* dh_nodes,
                       const fold_grads* grads, float* dh_out, float* dc_out,
                       void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---- the training step around the path ------------------------------------
+ * Section 3.3 trains the binary Tree-LSTM on trees whose every node carries a
+ * class label: a linear layer and a softmax on every node's state h, the
+ * cross entropy against the node's label, summed over the nodes, minimised
+ * with TensorFlow's Adam optimizer (Section 3.1).  These two calls are that
+ * step's loss head and update; fold_backward takes the head's dh_nodes.
+ *
+ * fold_loss_softmax_ce: per node v with label y_v >= 0
+ *     z_v = h_v W_cls + b_cls,  loss_v = log sum_c exp(z_vc) - z_{v,y_v}
+ * and the gradients of L = scale * sum_v loss_v:
+ *     dz_v = scale (softmax(z_v) - onehot(y_v)),  dh_v = dz_v W_cls^T,
+ *     dW_cls += h^T dz,  db_cls += sum_v dz_v;
+ * a node with label -1 has loss 0 and dh 0.  fp32 arithmetic on h of the
+ * packed parameters' dtype.
+ *   h_pool     device [N, fold_row_ld(H)] pool (as left by fold_forward)
+ *   labels     device [N] int32 in NODE order: class 0..num_classes-1, or -1
+ *   num_classes  2..8, 10, 16 or 32, with H * num_classes <= 8000
+ *   W_cls      device [H, num_classes] fp32 row-major; b_cls device [num_classes] fp32
+ *   node_loss  device [N] fp32, NODE order (written)
+ *   dh_nodes   device [N, fold_row_ld(H)] fp32, POOL order (written, pad
+ *              columns zero): the dh_nodes argument of fold_backward
+ *   dW_cls, db_cls  device, fp32, accumulated (+=; the caller zeroes them);
+ *              partial sums per block of rows are added in a fixed order, so
+ *              the result is the same in every run
+ *   ws         device workspace of >= fold_loss_workspace_size bytes (the
+ *              per-block partial sums; contents on entry do not matter)
+ * FOLD_E_INVALID for an unsupported class count, H * num_classes above
+ * 8000, a non-finite scale or a NULL buffer (N > 0); FOLD_E_MISMATCH for a
+ * workspace that is too small, and as fold_forward for a schedule and
+ * parameters that do not belong together.  Asynchronous; allocates nothing.
+ * fold_loss_workspace_size fails with FOLD_E_INVALID as above. */
+int32_t fold_loss_workspace_size(const fold_packed* packed, int32_t num_classes, size_t* bytes);
+int32_t fold_loss_softmax_ce(const fold_sched* sched, const fold_packed* packed, const void* h_pool,
+                             const int32_t* labels, int32_t num_classes, const float* W_cls, const float* b_cls,
+                             float scale, float* node_loss, float* dh_nodes, float* dW_cls, float* db_cls,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* fold_adam_step: step `step` (1, 2, ...) of Adam (Kingma and Ba) in the
+ * form of TensorFlow's optimizer, elementwise over n fp32 values:
+ *     m = beta1 m + (1 - beta1) g,  v = beta2 v + (1 - beta2) g^2,
+ *     p = p - lr_t m / (sqrt(v) + eps),
+ *     lr_t = lr sqrt(1 - beta2^step) / (1 - beta1^step)
+ * in fp32, with lr_t, 1 - beta1 and 1 - beta2 computed in double first (the
+ * hyperparameters are double so that 1 - 0.999 keeps its value).
+ * param, m, v are device fp32 arrays updated in place (m, v start at zero);
+ * grad is read; param_bf16, if not NULL, receives param rounded to bf16
+ * (round to nearest even) for models whose weights are bf16.  Any flat
+ * tensor works (weights, biases, a padded leaf table whose pad columns hold
+ * zero parameters and gradients, which stay zero).  FOLD_E_INVALID for n < 0,
+ * step < 1, beta outside [0, 1), eps < 0, a non-finite lr or a NULL buffer
+ * (n > 0).  Asynchronous; allocates nothing. */
+int32_t fold_adam_step(int64_t n, float* param, uint16_t* param_bf16, const float* grad, float* m, float* v,
+                       double lr, double beta1, double beta2, double eps, int32_t step, hipStream_t stream);
 
 /* ---- a whole step as one HIP graph ----------------------------------------
  * The level loop (Section 2: one batched iteration per depth, so a batch of

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <atomic>
 #include <cstring>
 #include <exception>
@@ -225,6 +226,41 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
   return w;
 }
 
+// Packing kernels of every set into the handle's buffers (allocated to the parameters' shapes).
+static void pack_launch(const Packed& P, const fold_params* prm, hipStream_t st) {
+  for (int i = 0; i < prm->num_sets; ++i) {
+    const fold_param_set& s = prm->sets[i];
+    const PackedSet& ps = P.sets[i];
+    if (s.kind == FOLD_EMBED) continue;
+    const size_t nf = (size_t)ps.Nf * ps.Kf;
+    const size_t nbr = (size_t)s.arity * P.HP * ps.G * P.HP;
+    const size_t nbi = (size_t)ps.INP * ps.G * P.HP;
+    const int G = ps.G, gid = gate_code_identity(G);
+    launch_pack(P.dtype, 0, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr, ps.Wf,
+                nf, st);
+    if (nbr)
+      launch_pack(P.dtype, 1, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr,
+                  ps.Wb_rec, nbr, st);
+    if (nbi)
+      launch_pack(P.dtype, 2, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr,
+                  ps.Wb_in, nbi, st);
+    launch_pack(P.dtype, 3, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, nullptr, nullptr, s.bias,
+                ps.bias, (size_t)G * P.HP, st);
+    if (s.kind == FOLD_TREELSTM) {
+      const int GL = gates_of(kTreeLstmLeaf);
+      const size_t nfl = (size_t)GL * P.HP * ps.INP, nbl = (size_t)ps.INP * GL * P.HP;
+      if (nfl)
+        launch_pack(P.dtype, 0, GL, G, kTreeLstmLeafGates, P.H, P.HP, s.in_dim, ps.INP, 0, ps.INP, s.W_in, nullptr,
+                    nullptr, ps.Wf_leaf, nfl, st);
+      if (nbl)
+        launch_pack(P.dtype, 2, GL, G, kTreeLstmLeafGates, P.H, P.HP, s.in_dim, ps.INP, 0, ps.INP, s.W_in, nullptr,
+                    nullptr, ps.Wb_in_leaf, nbl, st);
+      launch_pack(P.dtype, 3, GL, G, kTreeLstmLeafGates, P.H, P.HP, s.in_dim, ps.INP, 0, ps.INP, nullptr, nullptr,
+                  s.bias, ps.bias_leaf, (size_t)GL * P.HP, st);
+    }
+  }
+}
+
 int32_t pack_impl(const fold_params* prm, hipStream_t st, fold_packed** out) {
   auto* h = new fold_packed();
   Packed& P = h->p;
@@ -262,17 +298,6 @@ int32_t pack_impl(const fold_params* prm, hipStream_t st, fold_packed** out) {
       if (!dalloc(nf * es, &ps.Wf) || !dalloc(nbr * es, &ps.Wb_rec) || !dalloc(nbi * es, &ps.Wb_in) ||
           !dalloc((size_t)ps.G * P.HP * sizeof(float), reinterpret_cast<void**>(&ps.bias)))
         return bail(FOLD_E_NOMEM, "fold_pack_params: out of device memory");
-      const int G = ps.G, gid = gate_code_identity(G);
-      launch_pack(P.dtype, 0, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr, ps.Wf,
-                  nf, st);
-      if (nbr)
-        launch_pack(P.dtype, 1, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr,
-                    ps.Wb_rec, nbr, st);
-      if (nbi)
-        launch_pack(P.dtype, 2, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, s.W_in, s.W_rec, nullptr,
-                    ps.Wb_in, nbi, st);
-      launch_pack(P.dtype, 3, G, G, gid, P.H, P.HP, s.in_dim, ps.INP, s.arity, ps.Kf, nullptr, nullptr, s.bias,
-                  ps.bias, (size_t)G * P.HP, st);
       if (s.kind == FOLD_TREELSTM) {
         // leaf operations of this set: the live gates only, input segment only
         const int GL = gates_of(kTreeLstmLeaf);
@@ -280,18 +305,11 @@ int32_t pack_impl(const fold_params* prm, hipStream_t st, fold_packed** out) {
         if (!dalloc(nfl * es, &ps.Wf_leaf) || !dalloc(nbl * es, &ps.Wb_in_leaf) ||
             !dalloc((size_t)GL * P.HP * sizeof(float), reinterpret_cast<void**>(&ps.bias_leaf)))
           return bail(FOLD_E_NOMEM, "fold_pack_params: out of device memory");
-        if (nfl)
-          launch_pack(P.dtype, 0, GL, G, kTreeLstmLeafGates, P.H, P.HP, s.in_dim, ps.INP, 0, ps.INP, s.W_in, nullptr,
-                      nullptr, ps.Wf_leaf, nfl, st);
-        if (nbl)
-          launch_pack(P.dtype, 2, GL, G, kTreeLstmLeafGates, P.H, P.HP, s.in_dim, ps.INP, 0, ps.INP, s.W_in, nullptr,
-                      nullptr, ps.Wb_in_leaf, nbl, st);
-        launch_pack(P.dtype, 3, GL, G, kTreeLstmLeafGates, P.H, P.HP, s.in_dim, ps.INP, 0, ps.INP, nullptr, nullptr,
-                    s.bias, ps.bias_leaf, (size_t)GL * P.HP, st);
       }
     }
     P.sets.push_back(ps);
   }
+  pack_launch(P, prm, st);
   // the zero row spans the widest K any kernel reads: G * HP (dz rows), INP, HP
   size_t zw = (size_t)P.HP;
   for (const PackedSet& ps : P.sets) zw = std::max(zw, (size_t)std::max(ps.G * P.HP, ps.INP));
@@ -698,18 +716,15 @@ int32_t fold_sched_free(fold_sched* h) {
   FOLD_GUARD_END
 }
 
-int32_t fold_pack_params(const fold_params* prm, hipStream_t st, fold_packed** out) {
-  FOLD_GUARD_BEGIN
-  clear_error();
-  if (!out) return fail(FOLD_E_INVALID, "fold_pack_params: out is NULL");
-  *out = nullptr;
-  if (!prm || !prm->sets || prm->num_sets < 1) return fail(FOLD_E_INVALID, "fold_pack_params: no parameter sets");
-  if (prm->dtype != FOLD_F32 && prm->dtype != FOLD_BF16) return fail(FOLD_E_INVALID, "fold_pack_params: bad dtype");
+static int check_params(const fold_params* prm, const char* who) {
+  const std::string w = std::string(who) + ": ";
+  if (!prm || !prm->sets || prm->num_sets < 1) return fail(FOLD_E_INVALID, w + "no parameter sets");
+  if (prm->dtype != FOLD_F32 && prm->dtype != FOLD_BF16) return fail(FOLD_E_INVALID, w + "bad dtype");
   if (prm->hidden < 1 || prm->hidden > kMaxHidden)
-    return fail(FOLD_E_INVALID, "fold_pack_params: hidden must be in 1.." + std::to_string(kMaxHidden));
+    return fail(FOLD_E_INVALID, w + "hidden must be in 1.." + std::to_string(kMaxHidden));
   for (int i = 0; i < prm->num_sets; ++i) {
     const fold_param_set& s = prm->sets[i];
-    const std::string at = "fold_pack_params: set " + std::to_string(i) + ": ";
+    const std::string at = w + "set " + std::to_string(i) + ": ";
     if (!valid_kind(s.kind)) return fail(FOLD_E_INVALID, at + "bad kind");
     if (s.in_dim < 0) return fail(FOLD_E_INVALID, at + "negative in_dim");
     if (s.kind == FOLD_EMBED) {
@@ -721,7 +736,105 @@ int32_t fold_pack_params(const fold_params* prm, hipStream_t st, fold_packed** o
     if (s.in_dim > 0 && !s.W_in) return fail(FOLD_E_INVALID, at + "W_in is NULL");
     if (!s.W_rec) return fail(FOLD_E_INVALID, at + "W_rec is NULL");
   }
+  return FOLD_OK;
+}
+
+int32_t fold_pack_params(const fold_params* prm, hipStream_t st, fold_packed** out) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!out) return fail(FOLD_E_INVALID, "fold_pack_params: out is NULL");
+  *out = nullptr;
+  const int rc = check_params(prm, "fold_pack_params");
+  if (rc != FOLD_OK) return rc;
   return pack_impl(prm, st, out);
+  FOLD_GUARD_END
+}
+
+int32_t fold_pack_update(fold_packed* h, const fold_params* prm, hipStream_t st) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!h) return fail(FOLD_E_INVALID, "fold_pack_update: NULL handle");
+  const int rc = check_params(prm, "fold_pack_update");
+  if (rc != FOLD_OK) return rc;
+  const Packed& P = h->p;
+  if (prm->dtype != P.dtype || prm->hidden != P.H || prm->num_sets != (int)P.sets.size())
+    return fail(FOLD_E_MISMATCH, "fold_pack_update: dtype, hidden or number of sets differ from the handle's");
+  for (int i = 0; i < prm->num_sets; ++i) {
+    const fold_param_set& s = prm->sets[i];
+    const PackedSet& ps = P.sets[i];
+    if (s.kind != ps.kind || s.in_dim != ps.in_dim || (s.kind != FOLD_EMBED && s.arity != ps.arity))
+      return fail(FOLD_E_MISMATCH, "fold_pack_update: set " + std::to_string(i) + " differs in kind, in_dim or arity");
+  }
+  int dev = -1;
+  FOLD_HIP_CHECK(hipGetDevice(&dev));
+  if (dev != P.device) return fail(FOLD_E_MISMATCH, "fold_pack_update: the handle belongs to another device");
+  pack_launch(P, prm, st);
+  FOLD_HIP_CHECK(hipGetLastError());
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
+static int check_loss_classes(const Packed& p, int num_classes, const char* who) {
+  if (!loss_classes_supported(num_classes))
+    return fail(FOLD_E_INVALID, std::string(who) + ": num_classes must be 2..8, 10, 16 or 32");
+  if ((long long)p.H * num_classes > kLossMaxHC)
+    return fail(FOLD_E_INVALID, std::string(who) + ": hidden * num_classes must be at most " +
+                                    std::to_string(kLossMaxHC));
+  return FOLD_OK;
+}
+
+int32_t fold_loss_workspace_size(const fold_packed* ph, int32_t num_classes, size_t* bytes) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!ph || !bytes) return fail(FOLD_E_INVALID, "fold_loss_workspace_size: NULL argument");
+  const int rc = check_loss_classes(ph->p, num_classes, "fold_loss_workspace_size");
+  if (rc != FOLD_OK) return rc;
+  *bytes = loss_workspace_bytes(ph->p.H, num_classes);
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
+int32_t fold_loss_softmax_ce(const fold_sched* sh, const fold_packed* ph, const void* h_pool, const int32_t* labels,
+                             int32_t num_classes, const float* W_cls, const float* b_cls, float scale,
+                             float* node_loss, float* dh_nodes, float* dW_cls, float* db_cls, void* ws,
+                             size_t ws_bytes, hipStream_t st) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!sh || !ph) return fail(FOLD_E_INVALID, "fold_loss_softmax_ce: NULL handle");
+  const Sched& s = sh->s;
+  const Packed& p = ph->p;
+  int rc = check_compat(s, p);
+  if (rc != FOLD_OK) return rc;
+  rc = check_loss_classes(p, num_classes, "fold_loss_softmax_ce");
+  if (rc != FOLD_OK) return rc;
+  if (!std::isfinite(scale)) return fail(FOLD_E_INVALID, "fold_loss_softmax_ce: scale is not finite");
+  if (s.N == 0) return FOLD_OK;
+  if (!h_pool || !labels || !W_cls || !b_cls || !node_loss || !dh_nodes || !dW_cls || !db_cls || !ws)
+    return fail(FOLD_E_INVALID, "fold_loss_softmax_ce: NULL buffer");
+  if (ws_bytes < loss_workspace_bytes(p.H, num_classes))
+    return fail(FOLD_E_MISMATCH, "fold_loss_softmax_ce: workspace smaller than fold_loss_workspace_size");
+  launch_loss_ce(p.dtype, s.N, p.H, p.ld, num_classes, h_pool, s.pos_node, labels, W_cls, b_cls, scale, node_loss,
+                 dh_nodes, dW_cls, db_cls, static_cast<float*>(ws), st);
+  FOLD_HIP_CHECK(hipGetLastError());
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
+int32_t fold_adam_step(int64_t n, float* param, uint16_t* param_bf16, const float* grad, float* m, float* v,
+                       double lr, double beta1, double beta2, double eps, int32_t step, hipStream_t st) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (n < 0) return fail(FOLD_E_INVALID, "fold_adam_step: negative count");
+  if (step < 1) return fail(FOLD_E_INVALID, "fold_adam_step: step counts from 1");
+  if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) || !(eps >= 0.0) || !std::isfinite(lr))
+    return fail(FOLD_E_INVALID, "fold_adam_step: need 0 <= beta1, beta2 < 1, eps >= 0 and a finite lr");
+  if (n == 0) return FOLD_OK;
+  if (!param || !grad || !m || !v) return fail(FOLD_E_INVALID, "fold_adam_step: NULL buffer");
+  // the bias corrections folded into the step size, in double
+  const double lr_t = lr * std::sqrt(1.0 - std::pow(beta2, step)) / (1.0 - std::pow(beta1, step));
+  launch_adam((size_t)n, param, param_bf16, grad, m, v, beta1, beta2, lr_t, eps, st);
+  FOLD_HIP_CHECK(hipGetLastError());
+  return FOLD_OK;
   FOLD_GUARD_END
 }
 

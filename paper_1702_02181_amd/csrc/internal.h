@@ -203,6 +203,16 @@ void launch_bias_partial(const int* op_rows, int count, int chunk, int nchunk, c
 void launch_bias_reduce(const float* bpart, int nchunk, int Nw, int H, int HP, int gcode, float* dbias,
                         hipStream_t st);
 
+// ---- training step (train.hip) ----
+bool loss_classes_supported(int C);
+constexpr int kLossMaxHC = 8000;  // hidden * classes: W, the partial dW and db of a block within 64 KB of LDS
+size_t loss_workspace_bytes(int H, int C);
+void launch_loss_ce(int dtype, int N, int H, int ld, int C, const void* h_pool, const int* pos_node, const int* labels,
+                    const float* W, const float* b, float scale, float* node_loss, float* dh, float* dW, float* db,
+                    float* ws, hipStream_t st);
+void launch_adam(size_t n, float* p, uint16_t* p_bf16, const float* g, float* m, float* v, double b1, double b2,
+                 double lr_t, double eps, hipStream_t st);
+
 // ---- achievable-peak probes (diag.hip) ----
 int32_t probe_mfma(int dtype, hipStream_t st, double* tflops);
 int32_t probe_copy(void* dst, const void* src, size_t bytes, hipStream_t st, double* gbs);

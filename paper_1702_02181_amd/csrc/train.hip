@@ -1,0 +1,314 @@
+// The training step around the batched path (gfx950): the per-node softmax cross-entropy head and the
+// Adam update.
+//
+// Section 3.3 trains the binary Tree-LSTM on trees in which every node carries a class label: a linear
+// layer and a softmax on every node's state, the cross entropy against the node's label, the sum over the
+// nodes as the loss (Section 3.1 attaches a sparse softmax cross entropy to the model's output), and
+// TensorFlow's Adam optimizer (Section 3.1).
+//
+// k_loss_ce   one wave per 1-4 pool rows at a time (grid-stride; at most 256 blocks of 8 waves; the rows'
+//             indices, labels and states all loaded before their first use): the C logits z = h W + b as C
+//             dot products over each row's H values (W and the block's share of dW held in LDS), softmax
+//             and loss in fp32 on every lane, dz = scale (p - onehot(y)), then dh = dz W^T written over the
+//             whole padded row (zeros past H, and the whole row for an unlabelled node), and h^T dz, sum dz
+//             added into the block's LDS sums, which the block writes to its row of the workspace.
+//             HBM-bound: it reads each h row twice (the second time mostly from L2) and writes each dh row
+//             once.
+// k_loss_reduce  dW, db += the blocks' partial sums in block order (no atomics: every address would take
+//             one from each block, one after another, and the result is the same in every run).
+// k_adam      elementwise, four values per thread: m, v and the fp32 parameters updated in place, plus an
+//             optional bf16 copy of the parameters (the operand type of bf16 models).
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "common.h"
+#include "internal.h"
+
+namespace fold {
+
+namespace {
+
+constexpr int kLossThreads = 512;  // 8 waves share one LDS copy of W and of the partial dW
+constexpr int kLossBlocks = 256;   // at most one block per compute unit
+
+template <typename T>
+__device__ __forceinline__ float load_h(const T* p);
+template <>
+__device__ __forceinline__ float load_h<float>(const float* p) { return *p; }
+template <>
+__device__ __forceinline__ float load_h<uint16_t>(const uint16_t* p) { return bf2f(*p); }
+
+// Rows a wave takes at a time (their index, label and state loads all go out before the first use).
+template <int C>
+constexpr int loss_rows() { return C <= 8 ? 4 : (C <= 16 ? 2 : 1); }
+
+template <typename T, int C>
+__global__ __launch_bounds__(kLossThreads) void k_loss_ce(int N, int H, int ld, const T* h_pool, const int* pos_node,
+                                                          const int* labels, const float* W, const float* b,
+                                                          float scale, float* node_loss, float* dh,
+                                                          float* partial) {
+  constexpr int R = loss_rows<C>(), U = 8;  // U: 64-column slices of a row loaded at once
+  extern __shared__ float lds[];
+  float* sW = lds;           // [H][C]
+  float* sdW = lds + H * C;  // [H][C]
+  __shared__ float sdb[C];
+  const int tid = threadIdx.x, lane = tid & 63;
+  for (int i = tid; i < H * C; i += kLossThreads) {
+    sW[i] = W[i];
+    sdW[i] = 0.f;
+  }
+  if (tid < C) sdb[tid] = 0.f;
+  __syncthreads();
+  float bias[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) bias[c] = b[c];
+  const int waves = gridDim.x * (kLossThreads / 64);
+  for (int p0 = (blockIdx.x * (kLossThreads / 64) + (tid >> 6)) * R; p0 < N; p0 += waves * R) {
+    // every load below is unconditional, from a clamped (valid) address, and masked afterwards: a load
+    // under a branch would be waited for inside the branch, one after another
+    int node[R], y[R];
+#pragma unroll
+    for (int k = 0; k < R; ++k) node[k] = pos_node[min(p0 + k, N - 1)];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+      const int lab = labels[node[k]];
+      y[k] = p0 + k < N ? lab : -1;
+      node[k] = p0 + k < N ? node[k] : -1;
+    }
+    auto load_row = [&](int k, int j) {
+      const float v = load_h<T>(h_pool + (size_t)min(p0 + k, N - 1) * ld + (j < H ? j : 0));
+      return y[k] >= 0 && j < H ? v : 0.f;
+    };
+    // logits of the R rows (unlabelled rows read nothing and get zero logits)
+    float z[R][C];
+#pragma unroll
+    for (int k = 0; k < R; ++k)
+#pragma unroll
+      for (int c = 0; c < C; ++c) z[k][c] = 0.f;
+    for (int j0 = 0; j0 < H; j0 += 64 * U) {
+      float hv[R][U];
+#pragma unroll
+      for (int k = 0; k < R; ++k)
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          hv[k][u] = load_row(k, j0 + 64 * u + lane);
+        }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = j0 + 64 * u + lane;
+        if (j < H)
+#pragma unroll
+          for (int c = 0; c < C; ++c) {
+            const float wv = sW[j * C + c];
+#pragma unroll
+            for (int k = 0; k < R; ++k) z[k][c] += hv[k][u] * wv;
+          }
+      }
+    }
+    // softmax without the cancellations of 1 - p_y and lse - z_y when the label's class dominates:
+    // with m = max z (first at class a) and S = sum over c != a of e^(z_c - m), lse = m + log1p(S) and
+    // loss = (m - z_y) + log1p(S); dz_c = scale p_c for c != y and dz_y = -scale (sum over c != y of p_c)
+    float d[R][C];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) z[k][c] += __shfl_xor(z[k][c], o, 64);
+        z[k][c] += bias[c];
+      }
+      int a = 0;
+      float zmax = z[k][0];
+#pragma unroll
+      for (int c = 1; c < C; ++c)
+        if (z[k][c] > zmax) {
+          zmax = z[k][c];
+          a = c;
+        }
+      float e[C], S = 0.f;
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        e[c] = expf(z[k][c] - zmax);
+        S += c == a ? 0.f : e[c];
+      }
+      const float inv = 1.f / (1.f + S);
+      float zy = 0.f, rest = 0.f;
+#pragma unroll
+      for (int c = 0; c < C; ++c) {
+        zy = c == y[k] ? z[k][c] : zy;
+        d[k][c] = y[k] >= 0 ? scale * (e[c] * inv) : 0.f;
+        rest += c == y[k] ? 0.f : d[k][c];
+      }
+#pragma unroll
+      for (int c = 0; c < C; ++c) d[k][c] = c == y[k] ? -rest : d[k][c];
+      if (lane == 0 && node[k] >= 0) node_loss[node[k]] = y[k] >= 0 ? (zmax - zy) + log1pf(S) : 0.f;
+    }
+    // dh = dz W^T over the whole padded row; h^T dz and sum dz of the R rows into the block's LDS sums
+    for (int j0 = 0; j0 < ld; j0 += 64 * U) {
+      float hv[R][U];
+#pragma unroll
+      for (int k = 0; k < R; ++k)
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          hv[k][u] = load_row(k, j0 + 64 * u + lane);
+        }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = j0 + 64 * u + lane;
+        if (j >= ld) continue;
+        float g[R];
+#pragma unroll
+        for (int k = 0; k < R; ++k) g[k] = 0.f;
+        if (j < H) {
+#pragma unroll
+          for (int c = 0; c < C; ++c) {
+            const float wv = sW[j * C + c];
+            float acc = 0.f;
+#pragma unroll
+            for (int k = 0; k < R; ++k) {
+              g[k] += d[k][c] * wv;
+              acc += hv[k][u] * d[k][c];
+            }
+            atomicAdd(&sdW[j * C + c], acc);
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < R; ++k)
+          if (p0 + k < N) dh[(size_t)(p0 + k) * ld + j] = g[k];
+      }
+    }
+    if (lane < C) {
+      float dl = 0.f;
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int k = 0; k < R; ++k) dl += c == lane ? d[k][c] : 0.f;
+      atomicAdd(&sdb[lane], dl);
+    }
+  }
+  __syncthreads();
+  // the block's partial sums: [H * C dW | C db] at block row blockIdx.x of the workspace
+  float* part = partial + (size_t)blockIdx.x * (H * C + C);
+  for (int i = tid; i < H * C; i += kLossThreads) part[i] = sdW[i];
+  if (tid < C) part[H * C + tid] = sdb[tid];
+}
+
+// dW (entries 0 .. H C - 1) and db (the next C) += the blocks' partial sums, added in block order
+__global__ void k_loss_reduce(const float* partial, int nblocks, int HC, int C, float* dW, float* db) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= HC + C) return;
+  const int stride = HC + C;
+  constexpr int U = 8;  // eight loads in flight (absent blocks add an exact 0)
+  float s = 0.f;
+  for (int b0 = 0; b0 < nblocks; b0 += U) {
+    float t[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) t[u] = b0 + u < nblocks ? partial[(size_t)(b0 + u) * stride + i] : 0.f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) s += t[u];
+  }
+  if (i < HC) dW[i] += s;
+  else db[i - HC] += s;
+}
+
+template <typename T>
+void launch_loss_c(int C, dim3 grid, size_t lds, hipStream_t st, int N, int H, int ld, const T* h, const int* pos_node,
+                   const int* labels, const float* W, const float* b, float scale, float* loss, float* dh,
+                   float* partial) {
+#define FOLD_LOSS_CASE(CC)                                                                                      \
+  case CC:                                                                                                      \
+    hipLaunchKernelGGL((k_loss_ce<T, CC>), grid, dim3(kLossThreads), lds, st, N, H, ld, h, pos_node, labels, W, b, \
+                       scale, loss, dh, partial);                                                               \
+    break;
+  switch (C) {
+    FOLD_LOSS_CASE(2)
+    FOLD_LOSS_CASE(3)
+    FOLD_LOSS_CASE(4)
+    FOLD_LOSS_CASE(5)
+    FOLD_LOSS_CASE(6)
+    FOLD_LOSS_CASE(7)
+    FOLD_LOSS_CASE(8)
+    FOLD_LOSS_CASE(10)
+    FOLD_LOSS_CASE(16)
+    FOLD_LOSS_CASE(32)
+    default: break;
+  }
+#undef FOLD_LOSS_CASE
+}
+
+__global__ void k_adam(size_t n, float* p, uint16_t* p_bf16, const float* g, float* m, float* v, float b1, float c1,
+                       float b2, float c2, float lr_t, float eps) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x * 4;
+  for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4; i < n; i += stride) {
+    const int cnt = (int)std::min<size_t>(4, n - i);
+    if (cnt == 4 && (((uintptr_t)(p + i) | (uintptr_t)(g + i) | (uintptr_t)(m + i) | (uintptr_t)(v + i)) & 15) == 0) {
+      float4 pv = *reinterpret_cast<const float4*>(p + i), gv = *reinterpret_cast<const float4*>(g + i);
+      float4 mv = *reinterpret_cast<const float4*>(m + i), vv = *reinterpret_cast<const float4*>(v + i);
+      float* pa = &pv.x;
+      float* ga = &gv.x;
+      float* ma = &mv.x;
+      float* va = &vv.x;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        ma[k] = b1 * ma[k] + c1 * ga[k];
+        va[k] = b2 * va[k] + c2 * ga[k] * ga[k];
+        pa[k] -= lr_t * ma[k] / (sqrtf(va[k]) + eps);
+      }
+      *reinterpret_cast<float4*>(p + i) = pv;
+      *reinterpret_cast<float4*>(m + i) = mv;
+      *reinterpret_cast<float4*>(v + i) = vv;
+      if (p_bf16)
+        for (int k = 0; k < 4; ++k) p_bf16[i + k] = f2bf(pa[k]);
+    } else {
+      for (int k = 0; k < cnt; ++k) {
+        const float gk = g[i + k];
+        const float mk = b1 * m[i + k] + c1 * gk;
+        const float vk = b2 * v[i + k] + c2 * gk * gk;
+        const float pk = p[i + k] - lr_t * mk / (sqrtf(vk) + eps);
+        m[i + k] = mk;
+        v[i + k] = vk;
+        p[i + k] = pk;
+        if (p_bf16) p_bf16[i + k] = f2bf(pk);
+      }
+    }
+  }
+}
+
+}  // namespace
+
+bool loss_classes_supported(int C) {
+  return C == 2 || C == 3 || C == 4 || C == 5 || C == 6 || C == 7 || C == 8 || C == 10 || C == 16 || C == 32;
+}
+
+size_t loss_workspace_bytes(int H, int C) { return (size_t)kLossBlocks * (H * C + C) * sizeof(float); }
+
+void launch_loss_ce(int dtype, int N, int H, int ld, int C, const void* h_pool, const int* pos_node, const int* labels,
+                    const float* W, const float* b, float scale, float* node_loss, float* dh, float* dW, float* db,
+                    float* ws, hipStream_t st) {
+  if (N <= 0) return;
+  ProfScope prof("loss_ce", st);
+  const unsigned blocks = (unsigned)std::min<long long>(((long long)N + 8LL * 4 - 1) / (8LL * 4), kLossBlocks);
+  const size_t lds = (size_t)2 * H * C * sizeof(float);
+  if (dtype == FOLD_BF16)
+    launch_loss_c<uint16_t>(C, dim3(blocks), lds, st, N, H, ld, static_cast<const uint16_t*>(h_pool), pos_node,
+                            labels, W, b, scale, node_loss, dh, ws);
+  else
+    launch_loss_c<float>(C, dim3(blocks), lds, st, N, H, ld, static_cast<const float*>(h_pool), pos_node, labels, W,
+                         b, scale, node_loss, dh, ws);
+  const int total = H * C + C;
+  hipLaunchKernelGGL(k_loss_reduce, dim3((total + 255) / 256), dim3(256), 0, st, ws, (int)blocks, H * C, C, dW, db);
+}
+
+void launch_adam(size_t n, float* p, uint16_t* p_bf16, const float* g, float* m, float* v, double b1, double b2,
+                 double lr_t, double eps, hipStream_t st) {
+  if (n == 0) return;
+  ProfScope prof("adam", st);
+  const unsigned blocks = (unsigned)std::min<size_t>((n + 1023) / 1024, 4096);
+  hipLaunchKernelGGL(k_adam, dim3(blocks), dim3(256), 0, st, n, p, p_bf16, g, m, v, (float)b1, (float)(1.0 - b1),
+                     (float)b2, (float)(1.0 - b2), (float)lr_t, (float)eps);
+}
+
+}  // namespace fold

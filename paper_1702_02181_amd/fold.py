@@ -27,6 +27,7 @@ FOLD_OK = 0
 ERRORS = {-1: "FOLD_E_INVALID", -2: "FOLD_E_OP", -3: "FOLD_E_ARITY", -4: "FOLD_E_CHILD",
           -5: "FOLD_E_INPUT", -6: "FOLD_E_CYCLE", -7: "FOLD_E_NOMEM", -8: "FOLD_E_DEVICE",
           -9: "FOLD_E_MISMATCH"}
+FOLD_E_INVALID, FOLD_E_MISMATCH = -1, -9
 FOLD_EMBED, FOLD_TREERNN, FOLD_TREELSTM, FOLD_LSTM, FOLD_PROJ = 0, 1, 2, 3, 4
 FOLD_F32, FOLD_BF16 = 0, 1
 GATES = {FOLD_EMBED: 0, FOLD_TREERNN: 1, FOLD_TREELSTM: 5, FOLD_LSTM: 4, FOLD_PROJ: 1}
@@ -107,7 +108,8 @@ EXPORTS = ["fold_schedule", "fold_sched_get_info", "fold_sched_free", "fold_pack
            "fold_backward", "fold_last_error", "fold_profile_enable", "fold_profile_read",
            "fold_profile_read_launches",
            "fold_probe_mfma", "fold_probe_copy", "fold_graph_create", "fold_graph_launch",
-           "fold_graph_num_nodes", "fold_graph_free"]
+           "fold_graph_num_nodes", "fold_graph_free", "fold_pack_update", "fold_loss_softmax_ce",
+           "fold_loss_workspace_size", "fold_adam_step"]
 
 _lib = None
 
@@ -161,6 +163,17 @@ def lib():
     L.fold_probe_mfma.argtypes = [c_int32, c_void_p, POINTER(ctypes.c_double)]
     L.fold_probe_copy.restype = c_int32
     L.fold_probe_copy.argtypes = [c_void_p, c_void_p, c_size_t, c_void_p, POINTER(ctypes.c_double)]
+    L.fold_pack_update.restype = c_int32
+    L.fold_pack_update.argtypes = [c_void_p, POINTER(fold_params), c_void_p]
+    L.fold_loss_softmax_ce.restype = c_int32
+    L.fold_loss_softmax_ce.argtypes = [c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
+                                       ctypes.c_float, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_size_t,
+                                       c_void_p]
+    L.fold_loss_workspace_size.restype = c_int32
+    L.fold_loss_workspace_size.argtypes = [c_void_p, c_int32, POINTER(c_size_t)]
+    L.fold_adam_step.restype = c_int32
+    L.fold_adam_step.argtypes = [c_int64, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, ctypes.c_double,
+                                 ctypes.c_double, ctypes.c_double, ctypes.c_double, c_int32, c_void_p]
     _lib = L
     return L
 
@@ -247,6 +260,28 @@ def fold_pack_params(params: fold_params, stream=None) -> c_void_p:
     h = c_void_p()
     _check(lib().fold_pack_params(byref(params), _stream(stream), byref(h)))
     return h
+
+
+def fold_pack_update(handle, params: fold_params, stream=None):
+    _check(lib().fold_pack_update(handle, byref(params), _stream(stream)))
+
+
+def fold_loss_workspace_size(packed, num_classes) -> int:
+    n = c_size_t()
+    _check(lib().fold_loss_workspace_size(packed, int(num_classes), byref(n)))
+    return int(n.value)
+
+
+def fold_loss_softmax_ce(sched, packed, h_pool, labels, num_classes, W_cls, b_cls, scale, node_loss, dh_nodes,
+                         dW_cls, db_cls, ws, ws_bytes, stream=None):
+    _check(lib().fold_loss_softmax_ce(sched, packed, _ptr(h_pool), _ptr(labels), int(num_classes), _ptr(W_cls),
+                                      _ptr(b_cls), float(scale), _ptr(node_loss), _ptr(dh_nodes), _ptr(dW_cls),
+                                      _ptr(db_cls), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def fold_adam_step(n, param, param_bf16, grad, m, v, lr, beta1, beta2, eps, step, stream=None):
+    _check(lib().fold_adam_step(int(n), _ptr(param), _ptr(param_bf16), _ptr(grad), _ptr(m), _ptr(v), float(lr),
+                                float(beta1), float(beta2), float(eps), int(step), _stream(stream)))
 
 
 def fold_packed_free(handle):
@@ -386,6 +421,15 @@ class Packed:
         p = fold_params(dtype, hidden, len(sets), arr)
         self.handle = fold_pack_params(p, stream)
         self.dtype, self.hidden, self.num_sets = dtype, hidden, len(sets)
+
+    def update(self, sets, stream=None):
+        """fold_pack_update: re-pack new values of the same parameters (same shapes) in place."""
+        arr = (fold_param_set * len(sets))()
+        for k, s in enumerate(sets):
+            arr[k] = fold_param_set(s["kind"], s["in_dim"], s["arity"], _ptr(s.get("W_in")),
+                                    _ptr(s.get("W_rec")), _ptr(s.get("bias")))
+        fold_pack_update(self.handle, fold_params(self.dtype, self.hidden, len(sets), arr), stream)
+        self._keep, self._sets = sets, arr
 
     def __del__(self):
         h = getattr(self, "handle", None)

@@ -146,3 +146,70 @@ class DeviceRun:
                         for k, x in zip(("W_in", "W_rec", "bias"), t)})
         dt = None if self.d_table is None else self.d_table.cpu().numpy()[:, :self.w.leaf_table.shape[1]].astype(np.float64)
         return out, dt
+
+
+class TrainStep:
+    """One training step of a workload through the C ABI (Section 3.3's setting: a class label on every node,
+    softmax cross entropy on every node's state, Adam): zero the gradients, fold_forward,
+    fold_loss_softmax_ce, fold_backward from the head's dh alone, fold_adam_step on every parameter tensor
+    (the weights of every set, the biases, the leaf table if trained, the classifier), fold_pack_update.
+
+    fp32 master copies of the weights are kept here; for bf16 workloads Adam also writes the bf16 weights
+    that fold_pack_update packs.  The loss is the mean over the labelled nodes (scale = 1 / their count)."""
+
+    def __init__(self, w: gen.Workload, labels: np.ndarray, num_classes: int, train_table: bool, seed: int = 0,
+                 lr: float = 1e-3, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8):
+        self.dev = dev = DeviceRun(w)
+        self.C = num_classes
+        self.hyper = (lr, beta1, beta2, eps)
+        self.t = 0
+        rng = np.random.default_rng(seed)
+        cuda = lambda a, dt=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to(dtype=dt, device=dev.device)
+        self.labels = cuda(labels, torch.int32)
+        self.scale = 1.0 / max(1, int((labels >= 0).sum()))
+        self.W_cls = cuda((0.1 * rng.standard_normal((w.hidden, num_classes))).astype(np.float32))
+        self.b_cls = torch.zeros(num_classes, dtype=torch.float32, device=dev.device)
+        self.dW_cls = torch.zeros_like(self.W_cls)
+        self.db_cls = torch.zeros_like(self.b_cls)
+        self.node_loss = torch.zeros(max(dev.N, 1), dtype=torch.float32, device=dev.device)
+        self.dh_nodes = torch.zeros((max(dev.N, 1), dev.ld), dtype=torch.float32, device=dev.device)
+        self.loss_ws_bytes = F.fold_loss_workspace_size(dev.packed.handle, num_classes)
+        self.loss_ws = torch.empty(self.loss_ws_bytes, dtype=torch.uint8, device=dev.device)
+        dev.alloc_grads(train_table)
+        dev.set_upstream(np.zeros_like(w.dh_roots))
+        dev.dh_nodes = self.dh_nodes
+        # (fp32 master, bf16 copy or None, gradient) of every trained tensor
+        self.tensors = []
+        for p, st, gt in zip(w.params, dev.set_tensors, dev.grad_tensors):
+            if p.kind == gen.KIND_EMBED:
+                continue
+            for name, g in zip(("W_in", "W_rec", "bias"), gt):
+                if g is None:
+                    continue
+                cur = st[name]
+                if cur.dtype == torch.float32:
+                    self.tensors.append((cur, None, g))
+                else:
+                    self.tensors.append((cur.float(), cur, g))
+        if train_table:
+            self.tensors.append((dev.table.float(), dev.table if dev.bf16 else None, dev.d_table))
+            if not dev.bf16:
+                self.tensors[-1] = (dev.table, None, dev.d_table)
+        self.tensors += [(self.W_cls, None, self.dW_cls), (self.b_cls, None, self.db_cls)]
+        self.moments = [(torch.zeros_like(m), torch.zeros_like(m)) for m, _, _ in self.tensors]
+
+    def step(self):
+        dev = self.dev
+        self.t += 1
+        dev.zero_grads()
+        self.dW_cls.zero_()
+        self.db_cls.zero_()
+        dev.forward()
+        F.fold_loss_softmax_ce(dev.sched.handle, dev.packed.handle, dev.h_pool, self.labels, self.C, self.W_cls,
+                               self.b_cls, self.scale, self.node_loss, self.dh_nodes, self.dW_cls, self.db_cls,
+                               self.loss_ws, self.loss_ws_bytes, dev.stream)
+        dev.backward()
+        lr, b1, b2, eps = self.hyper
+        for (master, low, grad), (m, v) in zip(self.tensors, self.moments):
+            F.fold_adam_step(master.numel(), master, low, grad, m, v, lr, b1, b2, eps, self.t, dev.stream)
+        dev.packed.update(dev.set_tensors, dev.stream)
