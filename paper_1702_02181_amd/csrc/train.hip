@@ -6,15 +6,16 @@
 // nodes as the loss (Section 3.1 attaches a sparse softmax cross entropy to the model's output), and
 // TensorFlow's Adam optimizer (Section 3.1).
 //
-// k_loss_ce   one wave per 1-4 pool rows at a time (grid-stride; at most 256 blocks of 8 waves; the rows'
-//             indices, labels and states all loaded before their first use): the C logits z = h W + b as C
-//             dot products over each row's H values (W and the block's share of dW held in LDS), softmax
-//             and loss in fp32 on every lane, dz = scale (p - onehot(y)), then dh = dz W^T written over the
-//             whole padded row (zeros past H, and the whole row for an unlabelled node), and h^T dz, sum dz
-//             added into the block's LDS sums, which the block writes to its row of the workspace.
-//             HBM-bound: it reads each h row twice (the second time mostly from L2) and writes each dh row
-//             once.
-// k_loss_reduce  dW, db += the blocks' partial sums in block order (no atomics: every address would take
+// k_loss_ce   one wave per 1-2 pool rows at a time (grid-stride; at most 1,024 blocks of 4 waves; the rows'
+//             states all loaded before their first use, the next rows' positions and labels meanwhile): the C
+//             logits z = h W + b as C dot products over each row's H values (W held in LDS), softmax and loss
+//             in fp32 on every lane, dz = scale (p - onehot(y)), then dh = dz W^T written over the whole
+//             padded row (zeros past H, and the whole row for an unlabelled node); h^T dz and sum dz are
+//             summed over the wave's rows in registers (H <= 512, C <= 8; otherwise per row group into LDS),
+//             then over the block's waves in LDS, and the block writes its sums to its row of the workspace.
+//             HBM-bound: it reads each h row once (up to 512 columns kept in registers for the second pass)
+//             and writes each dh row once.
+// k_loss_reduce  dW, db += the blocks' partial sums in a fixed order (no atomics: every address would take
 //             one from each block, one after another, and the result is the same in every run).
 // k_adam      elementwise, four values per thread: m, v and the fp32 parameters updated in place, plus an
 //             optional bf16 copy of the parameters (the operand type of bf16 models).
@@ -31,8 +32,8 @@ namespace fold {
 
 namespace {
 
-constexpr int kLossThreads = 512;  // 8 waves share one LDS copy of W and of the partial dW
-constexpr int kLossBlocks = 256;   // at most one block per compute unit
+constexpr int kLossThreads = 256;  // 4 waves share one LDS copy of W and of the partial dW
+constexpr int kLossBlocks = 1024;  // four blocks per compute unit: enough waves to cover the load latency
 
 template <typename T>
 __device__ __forceinline__ float load_h(const T* p);
@@ -43,7 +44,7 @@ __device__ __forceinline__ float load_h<uint16_t>(const uint16_t* p) { return bf
 
 // Rows a wave takes at a time (their index, label and state loads all go out before the first use).
 template <int C>
-constexpr int loss_rows() { return C <= 8 ? 4 : (C <= 16 ? 2 : 1); }
+constexpr int loss_rows() { return C <= 8 ? 2 : 1; }
 
 template <typename T, int C>
 __global__ __launch_bounds__(kLossThreads) void k_loss_ce(int N, int H, int ld, const T* h_pool, const int* pos_node,
@@ -65,23 +66,52 @@ __global__ __launch_bounds__(kLossThreads) void k_loss_ce(int N, int H, int ld, 
   float bias[C];
 #pragma unroll
   for (int c = 0; c < C; ++c) bias[c] = b[c];
-  const int waves = gridDim.x * (kLossThreads / 64);
-  for (int p0 = (blockIdx.x * (kLossThreads / 64) + (tid >> 6)) * R; p0 < N; p0 += waves * R) {
-    // every load below is unconditional, from a clamped (valid) address, and masked afterwards: a load
-    // under a branch would be waited for inside the branch, one after another
-    int node[R], y[R];
+  const int step = gridDim.x * (kLossThreads / 64) * R;
+  // dW and db of the wave's rows: in registers (columns lane + 64 u) when the row fits one set of slices and
+  // C <= 8, else added per row group into the block's LDS sums
+  constexpr bool kRegAcc = C <= 8;
+  const bool reg = H <= 64 * U;
+  float wacc[kRegAcc ? U : 1][kRegAcc ? C : 1], bacc[C];
 #pragma unroll
-    for (int k = 0; k < R; ++k) node[k] = pos_node[min(p0 + k, N - 1)];
+  for (int u = 0; u < (kRegAcc ? U : 1); ++u)
+#pragma unroll
+    for (int c = 0; c < (kRegAcc ? C : 1); ++c) wacc[u][c] = 0.f;
+#pragma unroll
+  for (int c = 0; c < C; ++c) bacc[c] = 0.f;
+  // Every load below is unconditional, from a clamped (valid) address, and masked afterwards: a load under
+  // a branch would be waited for inside the branch, one after another.  The next rows' positions and
+  // labels are loaded while the current rows are processed.
+  auto fetch_labels = [&](int q0, int (&node)[R], int (&y)[R]) {
+#pragma unroll
+    for (int k = 0; k < R; ++k) node[k] = pos_node[min(q0 + k, N - 1)];
 #pragma unroll
     for (int k = 0; k < R; ++k) {
       const int lab = labels[node[k]];
-      y[k] = p0 + k < N ? lab : -1;
-      node[k] = p0 + k < N ? node[k] : -1;
+      y[k] = q0 + k < N ? lab : -1;
+      node[k] = q0 + k < N ? node[k] : -1;
+    }
+  };
+  int p0 = (blockIdx.x * (kLossThreads / 64) + (tid >> 6)) * R;
+  int nnode[R], ny[R];
+  fetch_labels(min(p0, N - 1), nnode, ny);
+  for (; p0 < N; p0 += step) {
+    int node[R], y[R];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+      node[k] = nnode[k];
+      y[k] = ny[k];
     }
     auto load_row = [&](int k, int j) {
       const float v = load_h<T>(h_pool + (size_t)min(p0 + k, N - 1) * ld + (j < H ? j : 0));
       return y[k] >= 0 && j < H ? v : 0.f;
     };
+    // the first 64 U columns stay in registers for the second pass
+    float h0[R][U];
+#pragma unroll
+    for (int k = 0; k < R; ++k)
+#pragma unroll
+      for (int u = 0; u < U; ++u) h0[k][u] = load_row(k, 64 * u + lane);
+    if (p0 + step < N) fetch_labels(p0 + step, nnode, ny);
     // logits of the R rows (unlabelled rows read nothing and get zero logits)
     float z[R][C];
 #pragma unroll
@@ -93,9 +123,7 @@ __global__ __launch_bounds__(kLossThreads) void k_loss_ce(int N, int H, int ld, 
 #pragma unroll
       for (int k = 0; k < R; ++k)
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          hv[k][u] = load_row(k, j0 + 64 * u + lane);
-        }
+        for (int u = 0; u < U; ++u) hv[k][u] = j0 == 0 ? h0[k][u] : load_row(k, j0 + 64 * u + lane);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int j = j0 + 64 * u + lane;
@@ -152,9 +180,7 @@ __global__ __launch_bounds__(kLossThreads) void k_loss_ce(int N, int H, int ld, 
 #pragma unroll
       for (int k = 0; k < R; ++k)
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          hv[k][u] = load_row(k, j0 + 64 * u + lane);
-        }
+        for (int u = 0; u < U; ++u) hv[k][u] = j0 == 0 ? h0[k][u] : load_row(k, j0 + 64 * u + lane);
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int j = j0 + 64 * u + lane;
@@ -172,7 +198,12 @@ __global__ __launch_bounds__(kLossThreads) void k_loss_ce(int N, int H, int ld, 
               g[k] += d[k][c] * wv;
               acc += hv[k][u] * d[k][c];
             }
-            atomicAdd(&sdW[j * C + c], acc);
+            if constexpr (kRegAcc) {
+              if (reg) wacc[u][c] += acc;
+              else atomicAdd(&sdW[j * C + c], acc);
+            } else {
+              atomicAdd(&sdW[j * C + c], acc);
+            }
           }
         }
 #pragma unroll
@@ -180,14 +211,27 @@ __global__ __launch_bounds__(kLossThreads) void k_loss_ce(int N, int H, int ld, 
           if (p0 + k < N) dh[(size_t)(p0 + k) * ld + j] = g[k];
       }
     }
-    if (lane < C) {
-      float dl = 0.f;
 #pragma unroll
-      for (int c = 0; c < C; ++c)
+    for (int c = 0; c < C; ++c)
 #pragma unroll
-        for (int k = 0; k < R; ++k) dl += c == lane ? d[k][c] : 0.f;
-      atomicAdd(&sdb[lane], dl);
-    }
+      for (int k = 0; k < R; ++k) bacc[c] += d[k][c];
+  }
+  // the wave's sums into the block's: one LDS atomic per entry and wave
+  if constexpr (kRegAcc) {
+    if (reg)
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int j = 64 * u + lane;
+        if (j < H)
+#pragma unroll
+          for (int c = 0; c < C; ++c) atomicAdd(&sdW[j * C + c], wacc[u][c]);
+      }
+  }
+  if (lane < C) {
+    float dl = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) dl = c == lane ? bacc[c] : dl;
+    atomicAdd(&sdb[lane], dl);
   }
   __syncthreads();
   // the block's partial sums: [H * C dW | C db] at block row blockIdx.x of the workspace
@@ -196,22 +240,38 @@ __global__ __launch_bounds__(kLossThreads) void k_loss_ce(int N, int H, int ld, 
   if (tid < C) part[H * C + tid] = sdb[tid];
 }
 
-// dW (entries 0 .. H C - 1) and db (the next C) += the blocks' partial sums, added in block order
-__global__ void k_loss_reduce(const float* partial, int nblocks, int HC, int C, float* dW, float* db) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= HC + C) return;
+// dW (entries 0 .. H C - 1) and db (the next C) += the blocks' partial sums.  A block of 1,024 threads
+// takes 64 entries: its 16 thread groups sum every 16th partial row (eight loads in flight), then the 16
+// group sums are added in group order, so the result does not depend on scheduling.
+constexpr int kReduceGroups = 16;
+__global__ __launch_bounds__(64 * kReduceGroups) void k_loss_reduce(const float* partial, int nblocks, int HC, int C,
+                                                                    float* dW, float* db) {
+  __shared__ float red[kReduceGroups][64];
+  const int e = threadIdx.x & 63, grp = threadIdx.x >> 6;
+  const int i = blockIdx.x * 64 + e;
   const int stride = HC + C;
-  constexpr int U = 8;  // eight loads in flight (absent blocks add an exact 0)
   float s = 0.f;
-  for (int b0 = 0; b0 < nblocks; b0 += U) {
-    float t[U];
+  if (i < stride) {
+    constexpr int U = 8;  // absent rows add an exact 0
+    for (int b0 = grp; b0 < nblocks; b0 += kReduceGroups * U) {
+      float t[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) t[u] = b0 + u < nblocks ? partial[(size_t)(b0 + u) * stride + i] : 0.f;
+      for (int u = 0; u < U; ++u) {
+        const int b = b0 + kReduceGroups * u;
+        t[u] = b < nblocks ? partial[(size_t)b * stride + i] : 0.f;
+      }
 #pragma unroll
-    for (int u = 0; u < U; ++u) s += t[u];
+      for (int u = 0; u < U; ++u) s += t[u];
+    }
   }
-  if (i < HC) dW[i] += s;
-  else db[i - HC] += s;
+  red[grp][e] = s;
+  __syncthreads();
+  if (grp != 0 || i >= stride) return;
+  float tot = 0.f;
+#pragma unroll
+  for (int g = 0; g < kReduceGroups; ++g) tot += red[g][e];
+  if (i < HC) dW[i] += tot;
+  else db[i - HC] += tot;
 }
 
 template <typename T>
@@ -290,7 +350,7 @@ void launch_loss_ce(int dtype, int N, int H, int ld, int C, const void* h_pool, 
                     float* ws, hipStream_t st) {
   if (N <= 0) return;
   ProfScope prof("loss_ce", st);
-  const unsigned blocks = (unsigned)std::min<long long>(((long long)N + 8LL * 4 - 1) / (8LL * 4), kLossBlocks);
+  const unsigned blocks = (unsigned)std::min<long long>(((long long)N + 4LL * 2 - 1) / (4LL * 2), kLossBlocks);
   const size_t lds = (size_t)2 * H * C * sizeof(float);
   if (dtype == FOLD_BF16)
     launch_loss_c<uint16_t>(C, dim3(blocks), lds, st, N, H, ld, static_cast<const uint16_t*>(h_pool), pos_node,
@@ -299,7 +359,8 @@ void launch_loss_ce(int dtype, int N, int H, int ld, int C, const void* h_pool, 
     launch_loss_c<float>(C, dim3(blocks), lds, st, N, H, ld, static_cast<const float*>(h_pool), pos_node, labels, W,
                          b, scale, node_loss, dh, ws);
   const int total = H * C + C;
-  hipLaunchKernelGGL(k_loss_reduce, dim3((total + 255) / 256), dim3(256), 0, st, ws, (int)blocks, H * C, C, dW, db);
+  hipLaunchKernelGGL(k_loss_reduce, dim3((total + 63) / 64), dim3(64 * kReduceGroups), 0, st, ws, (int)blocks, H * C,
+                     C, dW, db);
 }
 
 void launch_adam(size_t n, float* p, uint16_t* p_bf16, const float* g, float* m, float* v, double b1, double b2,
