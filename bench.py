@@ -426,6 +426,59 @@ def train_bench(config: int, steps: int, warmup: int, classes: int = 5) -> dict:
             "kernels": kernels}
 
 
+def blocks_bench(steps: int, warmup: int, num_trees: int = 1024, hidden: int = 300, vocab: int = 20000) -> dict:
+    """The combinator front end on sentiment-tree-shaped input: nested-tuple binary trees with U[5, 60] leaves
+    (random splits, uniform tokens) compiled by the recursive Tree-LSTM block expression of Section 3.3, then the
+    compiled batch's forward + backward step (HIP-graph replay).  Reports the host compile time beside the step."""
+    import numpy as np
+    import torch
+
+    from paper_1702_02181_amd import blocks as B
+    from paper_1702_02181_amd import gen
+    from paper_1702_02181_amd.runner import DeviceRun
+    rng = np.random.default_rng(17)
+
+    def tree(n):
+        if n == 1:
+            return int(rng.integers(0, vocab))
+        k = int(rng.integers(1, n))
+        return (tree(k), tree(n - k))
+
+    trees = [tree(int(n)) for n in rng.integers(5, 61, num_trees)]
+    expr = B.ForwardDeclaration()
+    word = B.AllOf(B.Scalar(), B.Zeros())
+    pair = B.AllOf(B.Zeros(), B.Record([(0, expr()), (1, expr())]))
+    expr.resolve_to(B.OneOf(lambda t: isinstance(t, tuple), {False: word, True: pair}) >> B.Op(gen.KIND_TREELSTM, 0))
+    table = gen._finish_values(0.1 * rng.standard_normal((vocab, hidden)), "bf16")
+    params = [gen.make_param_set(rng, gen.KIND_TREELSTM, hidden, 2, hidden, "bf16")]
+    t0 = time.perf_counter()
+    comp = B.Compiler(expr())
+    w, _ = comp.build(trees, params, hidden, table, dtype="bf16", name="blocks_treelstm_h300_bf16")
+    build_s = time.perf_counter() - t0
+    dev = DeviceRun(w)
+    dev.alloc_grads(True)
+    dev.set_upstream(w.dh_roots)
+    graph = dev.make_graph(backward=True, zero_grads=True)
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        graph.launch()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        graph.launch()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    return {"metric": "graph nodes/sec (Tree-LSTM fwd+bwd of a front-end-compiled batch, 1 GPU)",
+            "value": round(w.num_nodes / (ms * 1e-3), 1), "unit": "graph nodes/s", "ms_per_step": round(ms, 4),
+            "steps": steps, "warmup": warmup, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": w.name, "trees": num_trees, "nodes": w.num_nodes, "hidden": hidden,
+                       "ops": len(comp.ops)},
+            "host_compile_ms": round(build_s * 1e3, 1),
+            "host_compile_nodes_per_s": round(w.num_nodes / build_s, 1)}
+
+
 def cpu_baseline(w, budget_s: float):
     """The oracle as it stands, single thread, on whole graphs of the workload until ~budget_s."""
     from threadpoolctl import threadpool_limits
@@ -469,6 +522,8 @@ def main():
                     help="run the Table 1 protocol (manual / dynamic / full-dynamic batching) instead")
     ap.add_argument("--train", action="store_true",
                     help="time training steps (per-node softmax loss, Adam, re-pack) instead; default config 3")
+    ap.add_argument("--blocks", action="store_true",
+                    help="compile sentiment-shaped trees with the combinator front end and time the compiled batch")
     ap.add_argument("--counters-from", nargs=4, metavar=("MFMA_CSV", "FETCH_CSV", "WRITE_CSV", "TRACE_CSV"),
                     help="print the per-kernel MFMA utilisation / HBM bandwidth table of four rocprofv3 runs")
     args = ap.parse_args()
@@ -480,6 +535,11 @@ def main():
         w = _gen.make_config(args.config)
         rec = traffic_from_counters(args.traffic_from[0], args.traffic_from[1], args.traffic_kernel, w.name)
         print(TRAFFIC_TAG, json.dumps(rec))
+        return
+    if args.blocks:
+        import torch
+        torch.cuda.set_device(0)
+        print(json.dumps(blocks_bench(args.steps, args.warmup)), flush=True)
         return
     if args.train:
         import torch
