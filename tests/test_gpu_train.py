@@ -10,7 +10,7 @@
   * Adam against the oracle's update at steps 1 and 7 from seeded moments (vector and scalar paths, a
     ragged tail), the bf16 copy equal to the round-to-nearest-even of the fp32 result;
   * fold_pack_update: a forward after re-packing new weights in place equals, bit for bit, the forward of
-    a handle packed from the new weights;
+    a handle packed from the new weights, also when replayed from a HIP graph recorded before the update;
   * two whole training steps (runner.TrainStep: forward, head, backward, Adam on every tensor, re-pack)
     against two steps of the oracle's chain and Adam;
   * argument errors of the three calls.
@@ -247,3 +247,29 @@ def test_two_training_steps_match_oracle():
         g = g.reshape(o.shape[0], -1)[:, :o.reshape(o.shape[0], -1).shape[1]].reshape(o.shape)  # table pad columns
         # an update moves a value by at most about 2 lr over two steps; fp32 gradients shift it by far less
         np.testing.assert_allclose(g, o, rtol=0, atol=lr * 1e-3, err_msg=f"tensor {k}")
+
+
+def test_pack_update_seen_by_a_recorded_graph():
+    """A step graph recorded before fold_pack_update reads the new weights on its next replay."""
+    import torch
+    from paper_1702_02181_amd.runner import DeviceRun
+    w = _workload(64, "bf16", seed=4)
+    dev = DeviceRun(w, with_backward=False)
+    graph = dev.make_graph(backward=False)
+    graph.launch()
+    torch.cuda.synchronize()
+    before = dev.h_pool.clone()
+    rng = np.random.default_rng(12)
+    new_params = [gen.make_param_set(rng, p.kind, p.in_dim, p.arity, w.hidden, "bf16") for p in w.params]
+    fresh = DeviceRun(gen.Workload(**{**w.__dict__, "params": new_params}), with_backward=False)
+    fresh.forward()
+    sets = [dict(kind=p.kind, in_dim=p.in_dim, arity=p.arity,
+                 W_in=None if p.W_in is None else dev._wt(p.W_in), W_rec=None if p.W_rec is None else dev._wt(p.W_rec),
+                 bias=None if p.kind == gen.KIND_EMBED else torch.from_numpy(p.bias.astype(np.float32)).to("cuda"))
+            for p in new_params]
+    dev.packed.update(sets)
+    for _ in range(2):
+        graph.launch()
+        torch.cuda.synchronize()
+        assert torch.equal(dev.h_pool, fresh.h_pool) and torch.equal(dev.c_pool, fresh.c_pool)
+    assert not torch.equal(before, dev.h_pool)
