@@ -143,3 +143,23 @@ def test_wide_weight_gradients_f32_ragged_tiles():
     that are no multiple of a stage.  Sampled parity as above, with the leaf-table gradient."""
     w = gen.config2(num_graphs=160, hidden=300)
     _sampled_parity(w, [0, 77, 159], table_grad=True)
+
+
+def test_maximum_hidden_size():
+    """H = 4096, the largest hidden size the library accepts (the backward stages a row's bf16 dz, G x 4096
+    halves, in LDS): bf16 LSTM chains of 2 and 1 steps (64-wide inputs), forward and backward with an upstream
+    gradient on every node and the leaf-table gradient, against the oracle.  (A Tree-LSTM at this size needs
+    a 8192 x 20480 recurrent matrix, too slow for the fp64 oracle in test time.)"""
+    from tests._helpers import make_workload
+    rng = np.random.default_rng(4096)
+    H = 4096
+    ops = [gen.OpSpec(gen.KIND_LSTM, 1, 1, 0)]
+    params = [gen.make_param_set(rng, gen.KIND_LSTM, 64, 1, H, "bf16")]
+    table = gen._finish_values(0.5 * rng.standard_normal((5, 64)), "bf16")
+    w = make_workload([[(0, [-1], 0), (0, [0], 1)], [(0, [-1], 2)]], ops, params, H, table, dtype="bf16", seed=2,
+                      name="lstm_h4096")
+    w.backward = True
+    dh = rng.standard_normal((w.num_nodes, H))
+    g = C.run_device(w, dh_nodes=dh, table_grad=True)
+    o = C.run_oracle(w, dh_nodes=dh, table_grad=True)
+    C.compare_all(w, g, o, table_grad=True)
