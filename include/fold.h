@@ -263,10 +263,11 @@ int32_t fold_backward(const fold_sched* sched, const fold_packed* packed,
  * and the gradients of L = scale * sum_v loss_v:
  *     dz_v = scale (softmax(z_v) - onehot(y_v)),  dh_v = dz_v W_cls^T,
  *     dW_cls += h^T dz,  db_cls += sum_v dz_v;
- * a node with label -1 has loss 0 and dh 0.  fp32 arithmetic on h of the
- * packed parameters' dtype.
+ * a node with label -1 (or any label outside [0, num_classes)) has loss 0
+ * and dh 0.  fp32 arithmetic on h of the packed parameters' dtype.
  *   h_pool     device [N, fold_row_ld(H)] pool (as left by fold_forward)
  *   labels     device [N] int32 in NODE order: class 0..num_classes-1, or -1
+ *              (no label)
  *   num_classes  2..8, 10, 16 or 32, with H * num_classes <= 8000
  *   W_cls      device [H, num_classes] fp32 row-major; b_cls device [num_classes] fp32
  *   node_loss  device [N] fp32, NODE order (written)

@@ -87,7 +87,7 @@ __global__ __launch_bounds__(kLossThreads) void k_loss_ce(int N, int H, int ld, 
 #pragma unroll
     for (int k = 0; k < R; ++k) {
       const int lab = labels[node[k]];
-      y[k] = q0 + k < N ? lab : -1;
+      y[k] = q0 + k < N && lab >= 0 && lab < C ? lab : -1;  // labels outside [0, C) count as unlabelled
       node[k] = q0 + k < N ? node[k] : -1;
     }
   };

@@ -72,11 +72,16 @@ def test_loss_head_on_seeded_states(H, dtype, Cn, unlabelled):
     pool[:, :H] = hp
     h_pool = (bf16_tensor(pool) if dtype == "bf16" else torch.from_numpy(pool)).to("cuda")
     y = _labels(rng, N, Cn, unlabelled)
+    y_dev = y.copy()
+    if unlabelled not in (0.0, 1.0):  # labels outside [0, C) count as unlabelled
+        off = np.nonzero(y < 0)[0]
+        y_dev[off[::3]] = Cn
+        y_dev[off[1::3]] = -7
     W = 0.3 * rng.standard_normal((H, Cn))
     b = 0.2 * rng.standard_normal(Cn)
     W, b = W.astype(np.float32).astype(np.float64), b.astype(np.float32).astype(np.float64)
     scale = 1.0 / max(1, int((y >= 0).sum()))
-    loss, dh, dW, db = _head_device(dev, h_pool, y, W, b, scale)
+    loss, dh, dW, db = _head_device(dev, h_pool, y_dev, W, b, scale)
     node_pos = np.asarray(C.oracle_schedule(w)["node_pos"])
     o_loss, o_dh, o_dW, o_db = OT.softmax_ce(hp[node_pos].astype(np.float64), y, W, b, scale)
     assert np.all(dh[:, H:] == 0)
