@@ -6,7 +6,7 @@
 // nodes as the loss (Section 3.1 attaches a sparse softmax cross entropy to the model's output), and
 // TensorFlow's Adam optimizer (Section 3.1).
 //
-// k_loss_ce   one wave per 1-2 pool rows at a time (grid-stride; at most 1,024 blocks of 4 waves; the rows'
+// k_loss_ce   one wave per 1-2 pool rows at a time (grid-stride; at most 768 blocks of 4 waves; the rows'
 //             states all loaded before their first use, the next rows' positions and labels meanwhile): the C
 //             logits z = h W + b as C dot products over each row's H values (W held in LDS), softmax and loss
 //             in fp32 on every lane, dz = scale (p - onehot(y)), then dh = dz W^T written over the whole
@@ -33,7 +33,7 @@ namespace fold {
 namespace {
 
 constexpr int kLossThreads = 256;  // 4 waves share one LDS copy of W and of the partial dW
-constexpr int kLossBlocks = 1024;  // four blocks per compute unit: enough waves to cover the load latency
+constexpr int kLossBlocks = 768;   // three blocks of 4 waves per compute unit (the registers' occupancy): one round
 
 template <typename T>
 __device__ __forceinline__ float load_h(const T* p);
@@ -41,6 +41,24 @@ template <>
 __device__ __forceinline__ float load_h<float>(const float* p) { return *p; }
 template <>
 __device__ __forceinline__ float load_h<uint16_t>(const uint16_t* p) { return bf2f(*p); }
+
+// Sum over the 64 lanes of a wave with DPP moves (no LDS traffic): pairs, quads, half rows and rows of 16
+// lanes, then rows 0+1 and 2+3 by row broadcasts of lane 15 and lane 31; the total ends in lane 63 and is
+// read back as a wave-uniform value.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_moved(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROW_MASK, 0xf,
+                                                               false));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_moved<0xb1, 0xf>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp_moved<0x4e, 0xf>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp_moved<0x141, 0xf>(v);  // row_half_mirror
+  v += dpp_moved<0x140, 0xf>(v);  // row_mirror: every lane of a row holds the row's sum
+  v += dpp_moved<0x142, 0xa>(v);  // row_bcast:15 into rows 1 and 3
+  v += dpp_moved<0x143, 0xc>(v);  // row_bcast:31 into rows 2 and 3: lane 63 holds the total
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
 
 // Rows a wave takes at a time (their index, label and state loads all go out before the first use).
 template <int C>
@@ -144,9 +162,7 @@ __global__ __launch_bounds__(kLossThreads) void k_loss_ce(int N, int H, int ld, 
     for (int k = 0; k < R; ++k) {
 #pragma unroll
       for (int c = 0; c < C; ++c) {
-#pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) z[k][c] += __shfl_xor(z[k][c], o, 64);
-        z[k][c] += bias[c];
+        z[k][c] = wave_sum(z[k][c]) + bias[c];
       }
       int a = 0;
       float zmax = z[k][0];
