@@ -198,9 +198,9 @@ class TrainStep:
         self.tensors += [(self.W_cls, None, self.dW_cls), (self.b_cls, None, self.db_cls)]
         self.moments = [(torch.zeros_like(m), torch.zeros_like(m)) for m, _, _ in self.tensors]
 
-    def step(self):
+    def gradients(self):
+        """Zero the gradients, forward, head, backward (kernel launches only: capturable as a graph)."""
         dev = self.dev
-        self.t += 1
         dev.zero_grads()
         self.dW_cls.zero_()
         self.db_cls.zero_()
@@ -209,6 +209,23 @@ class TrainStep:
                                self.b_cls, self.scale, self.node_loss, self.dh_nodes, self.dW_cls, self.db_cls,
                                self.loss_ws, self.loss_ws_bytes, dev.stream)
         dev.backward()
+
+    def capture_gradients(self):
+        """Record gradients() once as a graph (torch.cuda.CUDAGraph over the library's launches on the capture
+        stream); step(graph=True) then replays it.  Adam and the re-pack stay outside: their step count changes."""
+        self.graph = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(self.graph):
+            self.gradients()
+        torch.cuda.synchronize()
+
+    def step(self, graph: bool = False):
+        dev = self.dev
+        self.t += 1
+        if graph:
+            self.graph.replay()
+        else:
+            self.gradients()
         lr, b1, b2, eps = self.hyper
         for (master, low, grad), (m, v) in zip(self.tensors, self.moments):
             F.fold_adam_step(master.numel(), master, low, grad, m, v, lr, b1, b2, eps, self.t, dev.stream)

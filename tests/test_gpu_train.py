@@ -12,7 +12,8 @@
   * fold_pack_update: a forward after re-packing new weights in place equals, bit for bit, the forward of
     a handle packed from the new weights, also when replayed from a HIP graph recorded before the update;
   * two whole training steps (runner.TrainStep: forward, head, backward, Adam on every tensor, re-pack)
-    against two steps of the oracle's chain and Adam;
+    against two steps of the oracle's chain and Adam; the gradient pass captured as a graph and replayed
+    between eager steps gives the eager pass's gradients at every replay (up to fp32 atomic order);
   * argument errors of the three calls.
 """
 import numpy as np
@@ -278,3 +279,30 @@ def test_pack_update_seen_by_a_recorded_graph():
         torch.cuda.synchronize()
         assert torch.equal(dev.h_pool, fresh.h_pool) and torch.equal(dev.c_pool, fresh.c_pool)
     assert not torch.equal(before, dev.h_pool)
+
+
+def test_captured_gradient_pass_replays_match_eager():
+    """TrainStep's gradient pass (zero, forward, head, backward) recorded once as a graph: replayed several
+    times, with eager Adam steps and re-packs between the replays, every replay's gradients equal those of the
+    eager pass on the same weights up to the order of fp32 atomic additions (K-split slices of dz . W^T add into
+    the children's dh in any order, so two eager passes differ in the last bits too): 1e-6 relative."""
+    import torch
+    from paper_1702_02181_amd.runner import TrainStep
+    w = _workload(64, "bf16", seed=31)
+    y = _labels(np.random.default_rng(6), w.num_nodes, 5)
+    ts = TrainStep(w, y, 5, train_table=True, seed=2)
+    ts.capture_gradients()
+    grads = lambda: [g.clone() for _, _, g in ts.tensors] + [ts.node_loss.clone(), ts.dh_nodes.clone()]
+    for it in range(3):
+        ts.gradients()
+        torch.cuda.synchronize()
+        eager = grads()
+        ts.graph.replay()
+        torch.cuda.synchronize()
+        replay = grads()
+        for k, (a, b) in enumerate(zip(eager, replay)):
+            err = compare.rel_err(b.cpu().numpy().reshape(a.shape[0], -1), a.cpu().numpy().reshape(a.shape[0], -1),
+                                  whole=True)
+            assert err <= 1e-6, (it, k, err)
+        ts.step(graph=True)  # the weights move between the checks
+        torch.cuda.synchronize()
