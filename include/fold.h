@@ -175,7 +175,9 @@ typedef struct {
 
 /* Copy the parameters into the library's MFMA-friendly layouts (gate blocks
  * interleaved per 32 hidden units, K padded per input segment, transposed
- * copies for the backward).  Reads the caller's arrays once; synchronises. */
+ * copies for the backward).  Reads the caller's arrays once; synchronises.
+ * FOLD_E_INVALID for a set whose packed matrix, G * H' * (in_dim' + arity * H')
+ * entries (primes: rounded up to 64), would reach 2^32. */
 int32_t fold_pack_params(const fold_params* params, hipStream_t stream, fold_packed** out);
 int32_t fold_packed_free(fold_packed* packed);
 

@@ -735,6 +735,10 @@ static int check_params(const fold_params* prm, const char* who) {
     if (!s.bias) return fail(FOLD_E_INVALID, at + "bias is NULL");
     if (s.in_dim > 0 && !s.W_in) return fail(FOLD_E_INVALID, at + "W_in is NULL");
     if (!s.W_rec) return fail(FOLD_E_INVALID, at + "W_rec is NULL");
+    // the packing kernels index every packed matrix with 32-bit arithmetic
+    const long long HP = round_up(prm->hidden, kPadK), INP = round_up(s.in_dim, kPadK);
+    if ((long long)gates_of(s.kind) * HP * (INP + s.arity * HP) >= (1LL << 32))
+      return fail(FOLD_E_INVALID, at + "too large: a packed weight matrix would hold 2^32 entries or more");
   }
   return FOLD_OK;
 }

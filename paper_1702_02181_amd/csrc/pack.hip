@@ -30,8 +30,9 @@ __global__ void k_pack(int mode, int G, int GC, int gcode, int H, int HP, int in
        idx += (size_t)gridDim.x * blockDim.x) {
     float v = 0.f;
     const int GH = GC * H;
+    const unsigned i32 = (unsigned)idx;  // packed matrices have fewer than 2^32 entries: 32-bit divisions
     if (mode == 0) {
-      const int np = (int)(idx / Kf), kp = (int)(idx - (size_t)np * Kf);
+      const int np = (int)(i32 / (unsigned)Kf), kp = (int)(i32 - (unsigned)np * (unsigned)Kf);
       const int ub = np / (G * 32), rem = np - ub * G * 32, j = ub * 32 + (rem & 31);
       const int g = gate_of_code(gcode, rem / 32);
       if (j < H) {
@@ -44,7 +45,7 @@ __global__ void k_pack(int mode, int G, int GC, int gcode, int H, int HP, int in
       }
     } else {
       const int KB = G * HP;
-      const int n = (int)(idx / KB), kk = (int)(idx - (size_t)n * KB);
+      const int n = (int)(i32 / (unsigned)KB), kk = (int)(i32 - (unsigned)n * (unsigned)KB);
       const int gc = kk / HP, j = kk - gc * HP, g = gate_of_code(gcode, gc);
       if (j < H) {
         if (mode == 1) {
