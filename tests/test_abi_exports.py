@@ -46,3 +46,38 @@ def test_library_loads_and_binding_matches(lib_path):
     # pure host helpers, no device work
     assert F.fold_row_ld(300) == 320 and F.fold_row_ld(256) == 256 and F.fold_row_ld(1) == 64
     assert F.fold_last_error() == ""
+
+
+def test_argument_checks_before_any_device_work(lib_path):
+    """Host-side validation that returns before any HIP call: argument errors of fold_pack_params (including a
+    set whose packed matrix would reach 2^32 entries), fold_adam_step and fold_loss_workspace_size."""
+    from ctypes import c_void_p
+    from paper_1702_02181_amd import fold as F
+    fake = c_void_p(256)  # never dereferenced: validation fails first
+    bias = c_void_p(512)
+    null_stream = type("Stream", (), {"cuda_stream": 0})()  # the calls fail before using it
+    ft = type("FakeTensor", (), {"data_ptr": lambda self: 256})()  # binding marshals tensors by data_ptr()
+
+    def pack(kind, in_dim, arity, hidden, dtype=F.FOLD_F32):
+        sets = (F.fold_param_set * 1)()
+        sets[0] = F.fold_param_set(kind, in_dim, arity, fake, fake, bias)
+        return F.fold_pack_params(F.fold_params(dtype, hidden, 1, sets), null_stream)
+
+    for args in ((F.FOLD_TREELSTM, 1_000_000, 2, 4096), (F.FOLD_TREELSTM, 64, 2, 4097),
+                 (F.FOLD_TREELSTM, 64, 1, 64), (F.FOLD_LSTM, -1, 1, 64)):
+        with pytest.raises(F.FoldError) as e:
+            pack(*args)
+        assert e.value.code == F.FOLD_E_INVALID, args
+    with pytest.raises(F.FoldError) as e:
+        pack(F.FOLD_TREELSTM, 1_000_000, 2, 4096)
+    assert "2^32" in str(e.value)
+    for args in ((16, ft, None, ft, ft, ft, 1e-3, 0.9, 0.999, 1e-8, 0),
+                 (16, ft, None, ft, ft, ft, 1e-3, 0.9, 1.0, 1e-8, 1),
+                 (16, ft, None, ft, ft, ft, float("inf"), 0.9, 0.999, 1e-8, 1),
+                 (16, ft, None, ft, ft, ft, 1e-3, 0.9, 0.999, -1.0, 1)):
+        with pytest.raises(F.FoldError) as e:
+            F.fold_adam_step(*args, stream=null_stream)
+        assert e.value.code == F.FOLD_E_INVALID, args
+    with pytest.raises(F.FoldError) as e:
+        F.fold_loss_workspace_size(None, 5)
+    assert e.value.code == F.FOLD_E_INVALID
