@@ -58,8 +58,13 @@ def pre_activation(P, H, x, hs):
     return z
 
 
-def forward_node(kind, P, H, x, hs, cs):
-    """Return (h, c, cache) of one node."""
+def forward_node(kind, P, H, x, hs, cs, m=None):
+    """Return (h, c, cache) of one node.
+
+    m: the node's recurrent-dropout mask [H] or None. Section 3.3 trains with the recurrent dropout of
+    Semeniuta et al.: the mask multiplies the candidate update u where it enters the memory cell,
+    c = i*(m*u) + sum_k f_k*c_k, so the forget paths of the cell state are never dropped. The mask's values
+    (0, or 1/(1-p) for inverted dropout) are drawn by the caller; the LSTM kinds use it, the others ignore it."""
     if kind == EMBED:
         return np.array(x, dtype=np.float64), np.zeros(H), {}
     z = pre_activation(P, H, x, hs)
@@ -73,19 +78,21 @@ def forward_node(kind, P, H, x, hs, cs):
         fr = sigmoid(z[2 * H:3 * H])
         o = sigmoid(z[3 * H:4 * H])
         u = np.tanh(z[4 * H:5 * H])
+        um = u if m is None else u * m
         cl, cr = cs
-        c = i * u + fl * cl + fr * cr
+        c = i * um + fl * cl + fr * cr
         h = o * np.tanh(c)
-        return h, c, {"i": i, "fl": fl, "fr": fr, "o": o, "u": u, "c": c}
+        return h, c, {"i": i, "fl": fl, "fr": fr, "o": o, "u": u, "c": c, "m": m}
     if kind == LSTM:
         i = sigmoid(z[0:H])
         f = sigmoid(z[H:2 * H])
         o = sigmoid(z[2 * H:3 * H])
         u = np.tanh(z[3 * H:4 * H])
+        um = u if m is None else u * m
         (cp,) = cs
-        c = i * u + f * cp
+        c = i * um + f * cp
         h = o * np.tanh(c)
-        return h, c, {"i": i, "f": f, "o": o, "u": u, "c": c}
+        return h, c, {"i": i, "f": f, "o": o, "u": u, "c": c, "m": m}
     raise ValueError(f"unknown kind {kind}")
 
 
@@ -100,27 +107,29 @@ def backward_node(kind, P, H, x, hs, cs, cache, dh, dc):
         dcs = [np.array(dc, dtype=np.float64)] if kind == PROJ else [np.zeros(H) for _ in hs]
     elif kind == TREELSTM:
         i, fl, fr, o, u, c = (cache[k] for k in ("i", "fl", "fr", "o", "u", "c"))
+        m = cache["m"] if cache["m"] is not None else 1.0
         cl, cr = cs
         tc = np.tanh(c)
         dct = dc + dh * o * (1.0 - tc * tc)
         dz = np.concatenate([
-            dct * u * i * (1.0 - i),
+            dct * (m * u) * i * (1.0 - i),
             dct * cl * fl * (1.0 - fl),
             dct * cr * fr * (1.0 - fr),
             dh * tc * o * (1.0 - o),
-            dct * i * (1.0 - u * u),
+            dct * i * m * (1.0 - u * u),
         ])
         dcs = [dct * fl, dct * fr]
     elif kind == LSTM:
         i, f, o, u, c = (cache[k] for k in ("i", "f", "o", "u", "c"))
+        m = cache["m"] if cache["m"] is not None else 1.0
         (cp,) = cs
         tc = np.tanh(c)
         dct = dc + dh * o * (1.0 - tc * tc)
         dz = np.concatenate([
-            dct * u * i * (1.0 - i),
+            dct * (m * u) * i * (1.0 - i),
             dct * cp * f * (1.0 - f),
             dh * tc * o * (1.0 - o),
-            dct * i * (1.0 - u * u),
+            dct * i * m * (1.0 - u * u),
         ])
         dcs = [dct * f]
     else:

@@ -40,8 +40,11 @@ def _node_args(batch, params, H, table, v, h, c):
     return kind, P, x, hs, cs
 
 
-def forward(batch, params, H, table):
-    """Return dict(h [N,H], c [N,H], cache [N]) in node order."""
+def forward(batch, params, H, table, u_mask=None):
+    """Return dict(h [N,H], c [N,H], cache [N]) in node order.
+
+    u_mask: [N, H] recurrent-dropout mask in node order (see cells.forward_node), or None; backward
+    reads it back from the cache."""
     n = len(batch["node_op"])
     if n == 0:
         return dict(h=np.zeros((0, H)), c=np.zeros((0, H)), cache=[])
@@ -57,7 +60,8 @@ def forward(batch, params, H, table):
             if k >= 0:
                 evaluate(k)
         kind, P, x, hs, cs = _node_args(batch, params, H, table, v, h, c)
-        h[v], c[v], cache[v] = cells.forward_node(kind, P, H, x, hs, cs)
+        m = None if u_mask is None else np.asarray(u_mask[v], dtype=np.float64)
+        h[v], c[v], cache[v] = cells.forward_node(kind, P, H, x, hs, cs, m)
 
     old = sys.getrecursionlimit()
     sys.setrecursionlimit(max(old, 20000))

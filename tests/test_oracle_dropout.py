@@ -1,0 +1,136 @@
+"""Pins of the oracle's recurrent dropout (Section 3.3 trains the Tree-LSTM with the recurrent dropout of
+Semeniuta et al.: a mask on the candidate update u where it enters the memory cell, c = i*(m*u) + sum f_k*c_k).
+
+* an all-ones mask is no dropout (bit for bit);
+* c of a node is affine in that node's own mask with slope i*u, and the mask of one node changes nothing
+  below it (the dropped term never reaches the forget paths or the gates);
+* a zero mask on a Tree-LSTM leaf gives c = 0 and h = 0 exactly, and no gradient reaches the i and u columns
+  of its weights;
+* central finite differences of the whole batch's loss, with a fixed random mask, match every gradient."""
+import numpy as np
+
+from oracle import evaluate as EV
+from paper_1702_02181_amd import gen
+from tests._helpers import make_workload, oracle_batch, oracle_params, random_params
+
+TL, LS, PJ = gen.KIND_TREELSTM, gen.KIND_LSTM, gen.KIND_PROJ
+
+
+def _tree(H=3, D_in=2, seed=31):
+    rng = np.random.default_rng(seed)
+    p = random_params(rng, TL, D_in, 2, H)
+    ops = [gen.OpSpec(TL, 0, 1, 0), gen.OpSpec(TL, 2, 0, 0)]
+    table = rng.standard_normal((3, D_in)).astype(np.float32)
+    g = [(0, [], 0), (0, [], 1), (1, [0, 1], -1)]
+    return make_workload([g], ops, [p], H, table, seed=seed), rng
+
+
+def _fwd(w, mask):
+    return EV.forward(oracle_batch(w), oracle_params(w), w.hidden, w.leaf_table, mask)
+
+
+def test_all_ones_mask_is_no_dropout():
+    w, _ = _tree()
+    a, b = _fwd(w, None), _fwd(w, np.ones((w.num_nodes, w.hidden)))
+    assert np.array_equal(a["h"], b["h"]) and np.array_equal(a["c"], b["c"])
+
+
+def test_root_cell_state_is_affine_in_its_own_mask():
+    w, rng = _tree()
+    n, H = w.num_nodes, w.hidden
+    ones = np.ones((n, H))
+    m0, m1, ms = ones.copy(), ones.copy(), ones.copy()
+    m0[2] = 0.0
+    s = rng.uniform(0.0, 2.5, H)
+    ms[2] = s
+    f0, f1, fs = _fwd(w, m0), _fwd(w, m1), _fwd(w, ms)
+    np.testing.assert_allclose(fs["c"][2], f0["c"][2] + s * (f1["c"][2] - f0["c"][2]), rtol=0, atol=1e-14)
+    # slope i*u, intercept the forget terms alone
+    i, u = f1["cache"][2]["i"], f1["cache"][2]["u"]
+    np.testing.assert_allclose(f1["c"][2] - f0["c"][2], i * u, rtol=0, atol=1e-15)
+    for v in (0, 1):  # the leaves below do not see the root's mask
+        assert np.array_equal(fs["h"][v], f1["h"][v]) and np.array_equal(fs["c"][v], f1["c"][v])
+
+
+def test_zero_mask_on_a_leaf():
+    w, rng = _tree()
+    n, H = w.num_nodes, w.hidden
+    m = np.ones((n, H))
+    m[0] = 0.0
+    b, P = oracle_batch(w), oracle_params(w)
+    f = EV.forward(b, P, H, w.leaf_table, m)
+    assert np.all(f["c"][0] == 0.0) and np.all(f["h"][0] == 0.0)
+    # a graph that is the lone leaf: no gradient reaches the i and u columns (gate order i | o | u ... of the
+    # canonical five-gate block: i = [0, H), u = [4H, 5H))
+    g = [(0, [], 0)]
+    wl = make_workload([g], w.ops, w.params, H, w.leaf_table, seed=1)
+    fl = EV.forward(oracle_batch(wl), oracle_params(wl), H, wl.leaf_table, np.zeros((1, H)))
+    bw = EV.backward(oracle_batch(wl), oracle_params(wl), H, wl.leaf_table, fl, np.ones((1, H)))
+    dW = bw["grads"][0]["W_in"]
+    assert np.all(dW[:, 0:H] == 0.0) and np.all(dW[:, 4 * H:5 * H] == 0.0)
+    assert np.all(bw["grads"][0]["bias"][0:H] == 0.0)
+
+
+def _fd(w, mask, dh_nodes, eps=1e-6, tol=1e-6):
+    b = oracle_batch(w)
+
+    def loss():
+        P = oracle_params(w)
+        f = EV.forward(b, P, w.hidden, w.leaf_table, mask)
+        L = sum(float(np.dot(w.dh_roots[r], f["h"][v])) for r, v in enumerate(EV.roots(b)))
+        return L + float((dh_nodes * f["h"]).sum())
+
+    w.leaf_table = w.leaf_table.astype(np.float64)
+    for p in w.params:
+        for name in ("W_in", "W_rec", "bias"):
+            if getattr(p, name) is not None:
+                setattr(p, name, getattr(p, name).astype(np.float64))
+    P = oracle_params(w)
+    f = EV.forward(b, P, w.hidden, w.leaf_table, mask)
+    bw = EV.backward(b, P, w.hidden, w.leaf_table, f, w.dh_roots.astype(np.float64), dh_nodes)
+    targets = [(getattr(p, nm), bw["grads"][si][nm]) for si, p in enumerate(w.params)
+               for nm in ("W_in", "W_rec", "bias") if getattr(p, nm) is not None and getattr(p, nm).size]
+    targets.append((w.leaf_table, bw["d_table"]))
+    checked = 0
+    for arr, an in targets:
+        for idx in np.ndindex(arr.shape):
+            old = arr[idx]
+            arr[idx] = old + eps; lp = loss()
+            arr[idx] = old - eps; lm = loss()
+            arr[idx] = old
+            num = (lp - lm) / (2 * eps)
+            assert abs(num - an[idx]) <= tol * max(1.0, abs(num)), (idx, num, an[idx])
+            checked += 1
+    return checked
+
+
+def _mask(rng, n, H, p=0.3):
+    return np.where(rng.random((n, H)) < p, 0.0, 1.0 / (1.0 - p))
+
+
+def test_fd_treelstm_with_dropout():
+    H, D_in = 2, 2
+    rng = np.random.default_rng(41)
+    p = random_params(rng, TL, D_in, 2, H)
+    ops = [gen.OpSpec(TL, 0, 1, 0), gen.OpSpec(TL, 2, 0, 0)]
+    table = rng.standard_normal((3, D_in)).astype(np.float32)
+    g1 = [(0, [], 0), (0, [], 1), (1, [0, 1], -1), (0, [], 2), (1, [2, 3], -1)]
+    g2 = [(0, [], 1), (1, [0, 0], -1), (1, [1, 0], -1), (1, [2, -1], -1)]
+    w = make_workload([g1, g2], ops, [p], H, table, seed=3)
+    mask = _mask(rng, w.num_nodes, H)
+    assert (mask == 0).any() and (mask > 0).any()
+    assert _fd(w, mask, rng.standard_normal((w.num_nodes, H))) > 50
+
+
+def test_fd_mixed_lstm_treelstm_proj_with_dropout():
+    H, D_in = 2, 2
+    rng = np.random.default_rng(42)
+    pl = random_params(rng, LS, D_in, 1, H)
+    pt = random_params(rng, TL, 0, 2, H)
+    pp = random_params(rng, PJ, 0, 1, H)
+    ops = [gen.OpSpec(LS, 1, 1, 0), gen.OpSpec(TL, 2, 0, 1), gen.OpSpec(PJ, 1, 0, 2)]
+    table = rng.standard_normal((3, D_in)).astype(np.float32)
+    g = [(0, [-1], 0), (0, [0], 1), (0, [1], 2), (1, [0, 1], -1), (2, [3], -1), (1, [4, 2], -1)]
+    w = make_workload([g], ops, [pl, pt, pp], H, table, seed=5)
+    mask = _mask(rng, w.num_nodes, H, p=0.4)
+    assert _fd(w, mask, rng.standard_normal((w.num_nodes, H))) > 40
