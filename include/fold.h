@@ -253,6 +253,33 @@ int32_t fold_backward(const fold_sched* sched, const fold_packed* packed,
                       const fold_grads* grads, float* dh_out, float* dc_out,
                       void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Recurrent dropout (Section 3.3 trains the Tree-LSTM with the recurrent
+ * dropout of Semeniuta et al., "Recurrent dropout without memory loss"):
+ * the forward and backward passes above with a mask on the candidate update
+ * u where it enters the memory cell, c = i*(m*u) + sum_k f_k*c_k, so the
+ * forget paths of the cell state are never dropped.  Operations of kind
+ * FOLD_TREELSTM (leaf and internal) and FOLD_LSTM use the mask; the other
+ * kinds ignore it.
+ *   u_mask  device [N, fold_row_ld(H)] fp32, pool order (row p = node
+ *           pos_node[p]); any multiplier (0 or 1/(1-p) for inverted
+ *           dropout, drawn by the caller).  Caller-owned, read only; the
+ *           backward must get the same mask as the forward.  NULL is
+ *           FOLD_E_INVALID (use fold_forward / fold_backward instead).
+ * Every other argument, error and the asynchrony are as in fold_forward /
+ * fold_backward. */
+int32_t fold_forward_dropout(const fold_sched* sched, const fold_packed* packed,
+                             const void* leaf_table, int64_t leaf_rows,
+                             void* h_pool, float* c_pool, void* roots_out,
+                             const float* u_mask, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+int32_t fold_backward_dropout(const fold_sched* sched, const fold_packed* packed,
+                              const void* leaf_table, int64_t leaf_rows,
+                              const void* h_pool, const float* c_pool,
+                              const float* u_mask, const float* dh_roots,
+                              const float* dh_nodes, const fold_grads* grads,
+                              float* dh_out, float* dc_out,
+                              void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* ---- the training step around the path ------------------------------------
  * Section 3.3 trains the binary Tree-LSTM on trees whose every node carries a
  * class label: a linear layer and a softmax on every node's state h, the

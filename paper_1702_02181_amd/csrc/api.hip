@@ -335,7 +335,7 @@ struct TagScope {
 };
 
 int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, void* h_pool,
-                     float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st) {
+                     float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st, const float* u_mask) {
   const WsLayout L = workspace_layout(s, p);
   TagScope tags;
   float* gates = nullptr;
@@ -377,6 +377,7 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
     a.bias = ps.bias;
     a.gates = gates;
     a.gstride = L.gstride;
+    a.u_mask = u_mask;
     a.zero = p.zero;
     a.zpart = zpart;
     int kind = op.kind;
@@ -397,7 +398,8 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
 
 int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, const void* h_pool,
                       const float* c_pool, const float* dh_roots, const float* dh_nodes, const fold_grads* grads,
-                      float* dh_out, float* dc_out, void* ws, size_t ws_bytes, hipStream_t st) {
+                      float* dh_out, float* dc_out, void* ws, size_t ws_bytes, hipStream_t st,
+                      const float* u_mask) {
   const WsLayout L = workspace_layout(s, p);
   if (!ws || ws_bytes < L.bwd_bytes) return fail(FOLD_E_MISMATCH, "fold_backward: workspace too small");
   TagScope tags;
@@ -427,6 +429,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     b.gstride = L.gstride;
     b.c_pool = c_pool;
     b.gates = gates;
+    b.u_mask = u_mask;
     b.dh = dh;
     b.dc = dc;
     b.child_pos = s.child_pos;
@@ -889,6 +892,40 @@ int32_t fold_backward(const fold_sched* sh, const fold_packed* ph, const void* t
   if (rc != FOLD_OK) return rc;
   return backward_impl(s, p, table, table_rows, h_pool, c_pool, dh_roots, dh_nodes, grads, dh_out, dc_out, ws,
                        ws_bytes, st);
+  FOLD_GUARD_END
+}
+
+int32_t fold_forward_dropout(const fold_sched* sh, const fold_packed* ph, const void* table, int64_t table_rows,
+                             void* h_pool, float* c_pool, void* roots_out, const float* u_mask, void* ws,
+                             size_t ws_bytes, hipStream_t st) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!sh || !ph) return fail(FOLD_E_INVALID, "fold_forward_dropout: NULL handle");
+  if (!u_mask) return fail(FOLD_E_INVALID, "fold_forward_dropout: u_mask is NULL");
+  const Sched& s = sh->s;
+  const Packed& p = ph->p;
+  int rc = check_forward_args(s, p, table, table_rows, h_pool, c_pool, "fold_forward_dropout");
+  if (rc != FOLD_OK) return rc;
+  return forward_impl(s, p, table, table_rows, h_pool, c_pool, roots_out, ws, ws_bytes, st, u_mask);
+  FOLD_GUARD_END
+}
+
+int32_t fold_backward_dropout(const fold_sched* sh, const fold_packed* ph, const void* table, int64_t table_rows,
+                              const void* h_pool, const float* c_pool, const float* u_mask, const float* dh_roots,
+                              const float* dh_nodes, const fold_grads* grads, float* dh_out, float* dc_out, void* ws,
+                              size_t ws_bytes, hipStream_t st) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!sh || !ph) return fail(FOLD_E_INVALID, "fold_backward_dropout: NULL handle");
+  if (!u_mask) return fail(FOLD_E_INVALID, "fold_backward_dropout: u_mask is NULL");
+  const Sched& s = sh->s;
+  const Packed& p = ph->p;
+  int rc = check_forward_args(s, p, table, table_rows, h_pool, c_pool, "fold_backward_dropout");
+  if (rc != FOLD_OK) return rc;
+  rc = check_grads(p, grads, "fold_backward_dropout");
+  if (rc != FOLD_OK) return rc;
+  return backward_impl(s, p, table, table_rows, h_pool, c_pool, dh_roots, dh_nodes, grads, dh_out, dc_out, ws,
+                       ws_bytes, st, u_mask);
   FOLD_GUARD_END
 }
 

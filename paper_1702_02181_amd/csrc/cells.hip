@@ -125,7 +125,8 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
   if constexpr (KIND == FOLD_TREELSTM) {
     const float i_ = sigmoidf_(z[0]), fl = sigmoidf_(z[1]), fr = sigmoidf_(z[2]), o = sigmoidf_(z[3]);
     const float u = tanhf_(z[4]);
-    c = i_ * u + fl * cl + fr * cr;
+    const float um = a.u_mask ? u * a.u_mask[p * a.ld + j] : u;
+    c = i_ * um + fl * cl + fr * cr;
     h = o * tanhf_(c);
     if (gs) {
       gs[0] = i_;
@@ -138,7 +139,7 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
     const float i_ = sigmoidf_(z[0]), o = sigmoidf_(z[1]), u = tanhf_(z[2]);
     (void)cl;
     (void)cr;
-    c = i_ * u;
+    c = i_ * (a.u_mask ? u * a.u_mask[p * a.ld + j] : u);
     h = o * tanhf_(c);
     if (gs) {
       gs[0] = i_;
@@ -148,7 +149,8 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
   } else if constexpr (KIND == FOLD_LSTM) {
     const float i_ = sigmoidf_(z[0]), f = sigmoidf_(z[1]), o = sigmoidf_(z[2]);
     const float u = tanhf_(z[3]);
-    c = i_ * u + f * cl;
+    const float um = a.u_mask ? u * a.u_mask[p * a.ld + j] : u;
+    c = i_ * um + f * cl;
     h = o * tanhf_(c);
     if (gs) {
       gs[0] = i_;
@@ -558,6 +560,7 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
     } else if constexpr (KIND == FOLD_TREELSTM) {
       const float dc = a.dc[p * a.ld + j];
       const float i_ = gate(0, j), fl = gate(1, j), fr = gate(2, j), o = gate(3, j), u = gate(4, j);
+      const float m = a.u_mask ? a.u_mask[p * a.ld + j] : 1.f;
       const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cl = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
       const float cr = c1 >= 0 ? a.c_pool[(size_t)c1 * a.ld + j] : 0.f;
@@ -565,32 +568,34 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
       const float dc0 = c0 >= 0 && s0 ? a.dc[(size_t)c0 * a.ld + j] : 0.f;
       const float dc1 = c1 >= 0 && s1 ? a.dc[(size_t)c1 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
-      put(0, j, dct * u * i_ * (1.f - i_));
+      put(0, j, dct * (m * u) * i_ * (1.f - i_));
       put(1, j, dct * cl * fl * (1.f - fl));
       put(2, j, dct * cr * fr * (1.f - fr));
       put(3, j, dh * tc * o * (1.f - o));
-      put(4, j, dct * i_ * (1.f - u * u));
+      put(4, j, dct * i_ * m * (1.f - u * u));
       if (c0 >= 0) add_into(&a.dc[(size_t)c0 * a.ld + j], dc0, dct * fl, s0);
       if (c1 >= 0) add_into(&a.dc[(size_t)c1 * a.ld + j], dc1, dct * fr, s1);
     } else if constexpr (KIND == kTreeLstmLeaf) {
       const float dc = a.dc[p * a.ld + j];
       const float i_ = gate(0, j), o = gate(1, j), u = gate(2, j);
+      const float m = a.u_mask ? a.u_mask[p * a.ld + j] : 1.f;
       const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float dct = dc + dh * o * (1.f - tc * tc);
-      put(0, j, dct * u * i_ * (1.f - i_));
+      put(0, j, dct * (m * u) * i_ * (1.f - i_));
       put(1, j, dh * tc * o * (1.f - o));
-      put(2, j, dct * i_ * (1.f - u * u));
+      put(2, j, dct * i_ * m * (1.f - u * u));
     } else if constexpr (KIND == FOLD_LSTM) {
       const float dc = a.dc[p * a.ld + j];
       const float i_ = gate(0, j), f = gate(1, j), o = gate(2, j), u = gate(3, j);
+      const float m = a.u_mask ? a.u_mask[p * a.ld + j] : 1.f;
       const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cp = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
       const float dc0 = c0 >= 0 && s0 ? a.dc[(size_t)c0 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
-      put(0, j, dct * u * i_ * (1.f - i_));
+      put(0, j, dct * (m * u) * i_ * (1.f - i_));
       put(1, j, dct * cp * f * (1.f - f));
       put(2, j, dh * tc * o * (1.f - o));
-      put(3, j, dct * i_ * (1.f - u * u));
+      put(3, j, dct * i_ * m * (1.f - u * u));
       if (c0 >= 0) add_into(&a.dc[(size_t)c0 * a.ld + j], dc0, dct * f, s0);
     } else {
       const float h = gate(0, j);

@@ -42,11 +42,11 @@ int leaf_table_width(const Sched& s, const Packed& p);
 void set_capturing(bool on);
 
 int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, void* h_pool,
-                     float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st);
+                     float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st, const float* u_mask = nullptr);
 int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows,
                       const void* h_pool, const float* c_pool, const float* dh_roots, const float* dh_nodes,
                       const fold_grads* grads, float* dh_out, float* dc_out, void* ws, size_t ws_bytes,
-                      hipStream_t st);
+                      hipStream_t st, const float* u_mask = nullptr);
 
 // ---- kernel launchers (cells.hip) ----
 struct FwdArgs {
@@ -67,6 +67,7 @@ struct FwdArgs {
   float* zpart;  // workspace for K-split partial sums, or NULL (no split)
   int ksplit;    // set by the launcher
   int map;         // set by the launcher: workgroup order over the XCDs (kMapRows, kMapCols, kMapOwnCols)
+  const float* u_mask = nullptr;  // recurrent dropout: [N, ld] fp32 multiplier of u in pool order, or NULL
 };
 void launch_cell_fwd(int dtype, int kind, const FwdArgs& a, hipStream_t st);
 
@@ -152,6 +153,7 @@ struct BwdCellArgs {
   float* d_table;
   int tld;
   int dz_bf16;  // write dz as bf16 (the operand type of bf16 parameters)
+  const float* u_mask = nullptr;  // the forward's recurrent-dropout mask, or NULL
 };
 void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st);
 void launch_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* dh_roots, const int* root_pos,

@@ -109,7 +109,7 @@ EXPORTS = ["fold_schedule", "fold_sched_get_info", "fold_sched_free", "fold_pack
            "fold_profile_read_launches",
            "fold_probe_mfma", "fold_probe_copy", "fold_graph_create", "fold_graph_launch",
            "fold_graph_num_nodes", "fold_graph_free", "fold_pack_update", "fold_loss_softmax_ce",
-           "fold_loss_workspace_size", "fold_adam_step"]
+           "fold_loss_workspace_size", "fold_adam_step", "fold_forward_dropout", "fold_backward_dropout"]
 
 _lib = None
 
@@ -145,6 +145,13 @@ def lib():
     L.fold_backward.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,
                                 c_void_p, POINTER(fold_grads), c_void_p, c_void_p, c_void_p, c_size_t,
                                 c_void_p]
+    L.fold_forward_dropout.restype = c_int32
+    L.fold_forward_dropout.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,
+                                       c_void_p, c_void_p, c_size_t, c_void_p]
+    L.fold_backward_dropout.restype = c_int32
+    L.fold_backward_dropout.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,
+                                        c_void_p, c_void_p, POINTER(fold_grads), c_void_p, c_void_p, c_void_p,
+                                        c_size_t, c_void_p]
     L.fold_graph_create.restype = c_int32
     L.fold_graph_create.argtypes = [c_void_p, c_void_p, POINTER(fold_step_buffers), c_int32, POINTER(c_void_p)]
     L.fold_graph_launch.restype = c_int32
@@ -304,6 +311,20 @@ def fold_backward(sched, packed, leaf_table, leaf_rows, h_pool, c_pool, dh_roots
     _check(lib().fold_backward(sched, packed, _ptr(leaf_table), int(leaf_rows), _ptr(h_pool), _ptr(c_pool),
                                _ptr(dh_roots), _ptr(dh_nodes), None if grads is None else byref(grads),
                                _ptr(dh_out), _ptr(dc_out), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def fold_forward_dropout(sched, packed, leaf_table, leaf_rows, h_pool, c_pool, roots_out, u_mask, ws, ws_bytes,
+                         stream=None):
+    _check(lib().fold_forward_dropout(sched, packed, _ptr(leaf_table), int(leaf_rows), _ptr(h_pool), _ptr(c_pool),
+                                      _ptr(roots_out), _ptr(u_mask), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def fold_backward_dropout(sched, packed, leaf_table, leaf_rows, h_pool, c_pool, u_mask, dh_roots, dh_nodes, grads,
+                          dh_out, dc_out, ws, ws_bytes, stream=None):
+    _check(lib().fold_backward_dropout(sched, packed, _ptr(leaf_table), int(leaf_rows), _ptr(h_pool), _ptr(c_pool),
+                                       _ptr(u_mask), _ptr(dh_roots), _ptr(dh_nodes),
+                                       None if grads is None else byref(grads), _ptr(dh_out), _ptr(dc_out), _ptr(ws),
+                                       int(ws_bytes), _stream(stream)))
 
 
 def fold_graph_create(sched, packed, buffers: fold_step_buffers, flags: int) -> c_void_p:

@@ -73,7 +73,12 @@ class DeviceRun:
         return (bf16_tensor(a) if self.bf16 else torch.from_numpy(a)).to(self.device)
 
     # ------------------------------------------------------------------ calls
-    def forward(self):
+    def forward(self, u_mask=None):
+        """u_mask: recurrent-dropout mask [N, ld] fp32 in pool order (fold_forward_dropout), or None."""
+        if u_mask is not None:
+            F.fold_forward_dropout(self.sched.handle, self.packed.handle, self.table, self.leaf_rows, self.h_pool,
+                                   self.c_pool, self.roots, u_mask, self.ws, self.ws_bytes, self.stream)
+            return
         F.fold_forward(self.sched.handle, self.packed.handle, self.table, self.leaf_rows, self.h_pool,
                        self.c_pool, self.roots, self.ws, self.ws_bytes, self.stream)
 
@@ -111,7 +116,12 @@ class DeviceRun:
         if self.d_table is not None:
             self.d_table.zero_()
 
-    def backward(self, dh_out=None, dc_out=None):
+    def backward(self, dh_out=None, dc_out=None, u_mask=None):
+        if u_mask is not None:
+            F.fold_backward_dropout(self.sched.handle, self.packed.handle, self.table, self.leaf_rows, self.h_pool,
+                                    self.c_pool, u_mask, self.dh_roots, self.dh_nodes, self.grads, dh_out, dc_out,
+                                    self.ws, self.ws_bytes, self.stream)
+            return
         F.fold_backward(self.sched.handle, self.packed.handle, self.table, self.leaf_rows, self.h_pool,
                         self.c_pool, self.dh_roots, self.dh_nodes, self.grads, dh_out, dc_out, self.ws,
                         self.ws_bytes, self.stream)

@@ -28,19 +28,25 @@ def assert_schedule_equal(gpu: dict, ref: dict):
         assert np.array_equal(host[k], ref[k]), "host " + k
 
 
-def run_device(w, dh_nodes=None, table_grad=False, backward=None):
+def run_device(w, dh_nodes=None, table_grad=False, backward=None, u_mask=None):
+    """u_mask: recurrent-dropout mask [N, H] in node order (placed into pool order here), or None."""
     import torch
     from paper_1702_02181_amd.runner import DeviceRun
     backward = w.backward if backward is None else backward
     dev = DeviceRun(w, with_backward=backward)
-    dev.forward()
+    mask = None
+    if u_mask is not None:
+        pool = np.zeros((dev.N, dev.ld), np.float32)
+        pool[dev.sched_arrays()["node_pos"], :dev.H] = u_mask
+        mask = torch.from_numpy(pool).cuda()
+    dev.forward(mask)
     out = {}
     if backward:
         dev.alloc_grads(table_grad)
         dev.set_upstream(w.dh_roots, dh_nodes)
         dh_out = torch.zeros((dev.N, dev.ld), dtype=torch.float32, device="cuda")
         dc_out = torch.zeros_like(dh_out)
-        dev.backward(dh_out, dc_out)
+        dev.backward(dh_out, dc_out, mask)
         torch.cuda.synchronize()
         node_pos = dev.sched_arrays()["node_pos"]
         out["dh"] = dh_out.cpu().numpy()[:, :dev.H][node_pos].astype(np.float64)
@@ -56,10 +62,10 @@ def run_device(w, dh_nodes=None, table_grad=False, backward=None):
     return out
 
 
-def run_oracle(w, dh_nodes=None, table_grad=False, backward=None):
+def run_oracle(w, dh_nodes=None, table_grad=False, backward=None, u_mask=None):
     backward = w.backward if backward is None else backward
     b, P = oracle_batch(w), oracle_params(w)
-    f = EV.forward(b, P, w.hidden, w.leaf_table)
+    f = EV.forward(b, P, w.hidden, w.leaf_table, u_mask)
     out = {"h": f["h"], "c": f["c"], "roots_nodes": EV.roots(b)}
     if backward:
         bw = EV.backward(b, P, w.hidden, w.leaf_table, f, w.dh_roots.astype(np.float64), dh_nodes,

@@ -15,17 +15,17 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 MUTATIONS = [
-    ("cells.py", "c = i * u + fl * cl + fr * cr", "c = i * u + fl * cl + fl * cr"),
+    ("cells.py", "c = i * um + fl * cl + fr * cr", "c = i * um + fl * cl + fl * cr"),
     ("cells.py", 'z += h @ P["W_rec"][k * H:(k + 1) * H]', 'z += h @ P["W_rec"][0:H]'),
     ("cells.py", 'z = np.array(P["bias"], dtype=np.float64, copy=True)',
      'z = 0 * np.array(P["bias"], dtype=np.float64, copy=True)'),
     ("cells.py", "o = sigmoid(z[2 * H:3 * H])\n        u = np.tanh(z[3 * H:4 * H])",
      "u = np.tanh(z[2 * H:3 * H])\n        o = sigmoid(z[3 * H:4 * H])"),
-    ("cells.py", "            dh * tc * o * (1.0 - o),\n            dct * i * (1.0 - u * u),\n        ])\n        dcs = [dct * fl, dct * fr]",
-     "            -dh * tc * o * (1.0 - o),\n            dct * i * (1.0 - u * u),\n        ])\n        dcs = [dct * fl, dct * fr]"),
+    ("cells.py", "            dh * tc * o * (1.0 - o),\n            dct * i * m * (1.0 - u * u),\n        ])\n        dcs = [dct * fl, dct * fr]",
+     "            -dh * tc * o * (1.0 - o),\n            dct * i * m * (1.0 - u * u),\n        ])\n        dcs = [dct * fl, dct * fr]"),
     ("cells.py", "dcs = [dct * fl, dct * fr]", "dcs = [dct * fr, dct * fl]"),
-    ("cells.py", "dct = dc + dh * o * (1.0 - tc * tc)\n        dz = np.concatenate([\n            dct * u * i * (1.0 - i),\n            dct * cl",
-     "dct = dh * o * (1.0 - tc * tc)\n        dz = np.concatenate([\n            dct * u * i * (1.0 - i),\n            dct * cl"),
+    ("cells.py", "dct = dc + dh * o * (1.0 - tc * tc)\n        dz = np.concatenate([\n            dct * (m * u) * i * (1.0 - i),\n            dct * cl",
+     "dct = dh * o * (1.0 - tc * tc)\n        dz = np.concatenate([\n            dct * (m * u) * i * (1.0 - i),\n            dct * cl"),
     ("cells.py", 'grads["W_in"] = np.outer(x, dz)', 'grads["W_in"] = np.outer(x, dz) * (1 + 1e-3)'),
     ("cells.py", "dz = dh * (1.0 - h * h)", "dz = dh * (1.0 - h)"),
     ("cells.py", "dcs = [np.array(dc, dtype=np.float64)] if kind == PROJ", "dcs = [np.zeros(H)] if kind == PROJ"),
