@@ -4,7 +4,9 @@ block, a dropped bias, swapped gate columns, a sign flip, swapped child
 gradients, a dropped upstream term, a scaled weight gradient, a wrong tanh
 derivative, a lost cell-state pass-through, wrong sort keys and tie-breaks,
 min instead of max in the depth rule, node ids instead of positions as edge
-labels, and overwriting instead of summing fan-out contributions."""
+labels, overwriting instead of summing fan-out contributions, and in the parity metric: the per-row
+floor dropped, min instead of max over rows, the row norm taken as a min, whole= ignored, rows cut along
+the last axis, and NaN rows skipped."""
 import os
 import shutil
 import subprocess
@@ -36,6 +38,16 @@ MUTATIONS = [
     ("schedule.py", "child_pos.append(node_pos[c] if c >= 0 else -1)", "child_pos.append(c if c >= 0 else -1)"),
     ("evaluate.py", "dh[k] += dhs[j]", "dh[k] = dhs[j]"),
     ("evaluate.py", 'd_table[int(batch["node_input"][v])] += dx', 'd_table[int(batch["node_input"][v])] = dx'),
+    ("compare.py", "row_ref = np.maximum(np.abs(R).max(axis=1), 1e-3 * scale)", "row_ref = np.abs(R).max(axis=1)"),
+    ("compare.py", "return float((np.abs(T - R).max(axis=1) / row_ref).max())",
+     "return float((np.abs(T - R).max(axis=1) / row_ref).min())"),
+    ("compare.py", "row_ref = np.maximum(np.abs(R).max(axis=1), 1e-3 * scale)",
+     "row_ref = np.maximum(np.abs(R).min(axis=1), 1e-3 * scale)"),
+    ("compare.py", "if whole or R.ndim == 1:", "if R.ndim == 1:"),
+    ("compare.py", "T = T.reshape(R.shape[0], -1)\n        R = R.reshape(R.shape[0], -1)",
+     "T = T.reshape(-1, R.shape[-1])\n        R = R.reshape(-1, R.shape[-1])"),
+    ("compare.py", "return float((np.abs(T - R).max(axis=1) / row_ref).max())",
+     "return float(np.nanmax(np.abs(T - R).max(axis=1) / row_ref))"),
 ]
 
 
@@ -51,6 +63,7 @@ def test_planted_mistake_is_caught(i, tmp_path):
     assert old in src, "mutation site moved; update the table"
     p.write_text(src.replace(old, new, 1))
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:randomly",
-                        "tests/test_oracle_schedule.py", "tests/test_oracle_cells.py"],
+                        "tests/test_oracle_schedule.py", "tests/test_oracle_cells.py",
+                        "tests/test_oracle_compare.py"],
                        cwd=tmp_path, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"pins missed mutation {i}: {new!r}"
