@@ -379,7 +379,7 @@ def table1(batches, steps: int, warmup: int, dtype: str = "f32") -> dict:
 
 
 def train_bench(config: int, steps: int, warmup: int, classes: int = 5) -> dict:
-    """Training steps of Section 3.3's setting on one workload: a class label on every node (uniform, seeded),
+    """Training steps of Section 3.5's setting on one workload: a class label on every node (uniform, seeded),
     forward, the per-node softmax cross-entropy head, backward from the head's gradients, Adam on every
     parameter tensor (weights, biases, the leaf table where it is trained, the classifier) and the in-place
     re-pack of the weights; the gradient pass (zero, forward, head, backward) is replayed as one recorded graph, Adam
@@ -430,7 +430,7 @@ def train_bench(config: int, steps: int, warmup: int, classes: int = 5) -> dict:
 
 def blocks_bench(steps: int, warmup: int, num_trees: int = 1024, hidden: int = 300, vocab: int = 20000) -> dict:
     """The combinator front end on sentiment-tree-shaped input: nested-tuple binary trees with U[5, 60] leaves
-    (random splits, uniform tokens) compiled by the recursive Tree-LSTM block expression of Section 3.3, then the
+    (random splits, uniform tokens) compiled by the recursive Tree-LSTM block expression of Section 3.5, then the
     compiled batch's forward + backward step (HIP-graph replay).  Reports the host compile time beside the step."""
     import numpy as np
     import torch

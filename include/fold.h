@@ -253,7 +253,7 @@ int32_t fold_backward(const fold_sched* sched, const fold_packed* packed,
                       const fold_grads* grads, float* dh_out, float* dc_out,
                       void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* Recurrent dropout (Section 3.3 trains the Tree-LSTM with the recurrent
+/* Recurrent dropout (Section 3.5 trains the Tree-LSTM with the recurrent
  * dropout of Semeniuta et al., "Recurrent dropout without memory loss"):
  * the forward and backward passes above with a mask on the candidate update
  * u where it enters the memory cell, c = i*(m*u) + sum_k f_k*c_k, so the
@@ -281,10 +281,10 @@ int32_t fold_backward_dropout(const fold_sched* sched, const fold_packed* packed
                               void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ---- the training step around the path ------------------------------------
- * Section 3.3 trains the binary Tree-LSTM on trees whose every node carries a
+ * Section 3.5 trains the binary Tree-LSTM on trees whose every node carries a
  * class label: a linear layer and a softmax on every node's state h, the
  * cross entropy against the node's label, summed over the nodes, minimised
- * with TensorFlow's Adam optimizer (Section 3.1).  These two calls are that
+ * with TensorFlow's Adam optimizer (Section 3.3).  These two calls are that
  * step's loss head and update; fold_backward takes the head's dh_nodes.
  *
  * fold_loss_softmax_ce: per node v with label y_v >= 0

@@ -18,7 +18,7 @@ Operations (the paper's experiments, Sections 2.1 and 3.3):
               i, f_l, f_r, o = sigmoid(.),  u = tanh(.)
               c = i*u + f_l*c_l + f_r*c_r,  h = o*tanh(c)
             a leaf is TreeLSTM(Embedding(word), 0, 0), an internal node
-            TreeLSTM(0, h_l, h_r) (the two equations of Section 3.3); the
+            TreeLSTM(0, h_l, h_r) (the two equations of Section 3.5); the
             forget-gate biases are not tied.
   LSTM      one step of the chain that Fold(g, z = 0) builds: gates
             (i | f | o | u), c = i*u + f*c_p, h = o*tanh(c)
@@ -61,7 +61,7 @@ def pre_activation(P, H, x, hs):
 def forward_node(kind, P, H, x, hs, cs, m=None):
     """Return (h, c, cache) of one node.
 
-    m: the node's recurrent-dropout mask [H] or None. Section 3.3 trains with the recurrent dropout of
+    m: the node's recurrent-dropout mask [H] or None. Section 3.5 trains with the recurrent dropout of
     Semeniuta et al.: the mask multiplies the candidate update u where it enters the memory cell,
     c = i*(m*u) + sum_k f_k*c_k, so the forget paths of the cell state are never dropped. The mask's values
     (0, or 1/(1-p) for inverted dropout) are drawn by the caller; the LSTM kinds use it, the others ignore it."""

@@ -1,9 +1,9 @@
 """The training step around the batched path, fp64 (test infrastructure only).
 
-Section 3.3 trains the binary Tree-LSTM on sentiment trees in which every node carries a class label:
+Section 3.5 trains the binary Tree-LSTM on sentiment trees in which every node carries a class label:
 each node's state feeds a linear layer and a softmax, the loss is the cross entropy against the node's
-label (a sparse softmax cross entropy, Section 3.1's pipeline example), and the parameters are updated by
-TensorFlow's Adam optimizer (Section 3.1).
+label (a sparse softmax cross entropy, Section 3.3's pipeline example), and the parameters are updated by
+TensorFlow's Adam optimizer (Section 3.3).
 
 ``softmax_ce``  per-node head over the nodes' states h [N, H]:
                     z = h W + b,  p = softmax(z),  loss_v = log sum_c exp(z_vc) - z_{v, y_v}

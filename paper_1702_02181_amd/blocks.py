@@ -1,14 +1,14 @@
 """Combinator front end (Section 3 of the paper): blocks that turn Python inputs into the op table and CSR
 graphs the library schedules, so a model over trees or sequences is written once as a block expression.
 
-Types of the values that flow between blocks (Section 3.2, in the library's terms):
+Types of the values that flow between blocks (Section 3.1, in the library's terms):
   * host objects (any Python value): what ``InputTransform`` and ``Record`` see;
   * ``Row(i)``: a row of the leaf table, the tensor an operation with an input reads (``Scalar`` makes one);
   * ``Node``: the state (h, c) of a node of the graph being built;
   * ``ZERO``: the zero state / absent input (``Zeros``);
   * tuples (``Record``, ``AllOf``) and lists (``Map``) of these.
 
-Blocks (Section 3.3): ``b1 >> b2`` composition, ``InputTransform(fn)``, ``Scalar()``, ``Zeros()``, ``Map(b)``,
+Blocks (Section 3.2): ``b1 >> b2`` composition, ``InputTransform(fn)``, ``Scalar()``, ``Zeros()``, ``Map(b)``,
 ``Fold(g, z)`` (g(... g(g(z, x1), x2) ..., xn), a leftward chain), ``Reduce(g)`` (g over the two halves split at
 floor(n / 2), a balanced tree), ``Record(fields)``, ``AllOf(*blocks)``, ``OneOf(key_fn, cases)``, ``Optional(b)``,
 ``ForwardDeclaration`` (recursion), and ``Op(kind, param_set)``, the library operation as a block (the paper's

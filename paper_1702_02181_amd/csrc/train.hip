@@ -1,10 +1,10 @@
 // The training step around the batched path (gfx950): the per-node softmax cross-entropy head and the
 // Adam update.
 //
-// Section 3.3 trains the binary Tree-LSTM on trees in which every node carries a class label: a linear
+// Section 3.5 trains the binary Tree-LSTM on trees in which every node carries a class label: a linear
 // layer and a softmax on every node's state, the cross entropy against the node's label, the sum over the
-// nodes as the loss (Section 3.1 attaches a sparse softmax cross entropy to the model's output), and
-// TensorFlow's Adam optimizer (Section 3.1).
+// nodes as the loss (Section 3.3 attaches a sparse softmax cross entropy to the model's output), and
+// TensorFlow's Adam optimizer (Section 3.3).
 //
 // k_loss_ce   one wave per 1-2 pool rows at a time (grid-stride; at most 768 blocks of 4 waves; the rows'
 //             states all loaded before their first use, the next rows' positions and labels meanwhile): the C

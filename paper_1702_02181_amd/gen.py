@@ -10,7 +10,7 @@ without sharing any code.
 The workloads stand in for the paper's two settings: the synthetic speed
 benchmark of Section 2.1 (random binary trees, embedding-lookup leaves,
 a Tree-LSTM variant at the non-terminals) and the sentiment experiment of
-Section 3.3 (binarised parse trees whose leaves are word embeddings).  No
+Section 3.5 (binarised parse trees whose leaves are word embeddings).  No
 dataset is read; token frequencies follow a Zipf law as a stand-in for
 natural-language text.
 

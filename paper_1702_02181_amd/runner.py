@@ -159,7 +159,7 @@ class DeviceRun:
 
 
 class TrainStep:
-    """One training step of a workload through the C ABI (Section 3.3's setting: a class label on every node,
+    """One training step of a workload through the C ABI (Section 3.5's setting: a class label on every node,
     softmax cross entropy on every node's state, Adam): zero the gradients, fold_forward,
     fold_loss_softmax_ce, fold_backward from the head's dh alone, fold_adam_step on every parameter tensor
     (the weights of every set, the biases, the leaf table if trained, the classifier), fold_pack_update.

@@ -1,4 +1,4 @@
-"""Pins of the oracle's recurrent dropout (Section 3.3 trains the Tree-LSTM with the recurrent dropout of
+"""Pins of the oracle's recurrent dropout (Section 3.5 trains the Tree-LSTM with the recurrent dropout of
 Semeniuta et al.: a mask on the candidate update u where it enters the memory cell, c = i*(m*u) + sum f_k*c_k).
 
 * an all-ones mask is no dropout (bit for bit);
