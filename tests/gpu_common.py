@@ -94,3 +94,47 @@ def compare_all(w, g, o, tol=None, check_backward=None, table_grad=False):
     bad = {k: v for k, v in errs.items() if not (v <= tol)}
     assert not bad, f"over tolerance {tol}: {bad} (all: {errs})"
     return errs
+
+
+def sampled_parity(w, sample, table_grad, u_mask=None, dh_nodes=None):
+    """Parity of a full-size batch on sampled graphs, for batches too large for the node-by-node oracle.
+
+    Two properties that hold at any size carry it: batching invariance (a graph's states inside the batch
+    equal those of the graph alone, so the sampled graphs' states are compared with the oracle on them
+    alone) and linearity of the backward pass in the upstream gradient (with zero root and node gradients
+    on every other graph, those graphs contribute exactly nothing: the full-batch weight gradients equal
+    the oracle's on the sampled graphs alone, and every other node's gradient is exactly 0).
+    u_mask, dh_nodes: [N, H] in node order (recurrent-dropout mask, per-node upstream gradient) or None;
+    dh_nodes is zeroed outside the sampled graphs here."""
+    from paper_1702_02181_amd import gen
+    tol = TOL[w.dtype]
+    rpg = gen.roots_per_graph(w.graph_ptr, w.child_idx)
+    roff = np.concatenate([[0], np.cumsum(rpg)])
+    dh = np.zeros_like(w.dh_roots)
+    for g in sample:
+        dh[roff[g]:roff[g + 1]] = w.dh_roots[roff[g]:roff[g + 1]]
+    w.dh_roots = dh
+    gp = w.graph_ptr
+    rows = np.concatenate([np.arange(gp[g], gp[g + 1]) for g in sample])
+    if dh_nodes is not None:
+        keep = np.zeros((w.num_nodes, w.hidden), np.float32)
+        keep[rows] = dh_nodes[rows]
+        dh_nodes = keep
+    g_out = run_device(w, dh_nodes=dh_nodes, table_grad=table_grad, u_mask=u_mask)
+    sub = gen.subset(w, sample)
+    o = run_oracle(sub, dh_nodes=None if dh_nodes is None else dh_nodes[rows].astype(np.float64),
+                   table_grad=table_grad, u_mask=None if u_mask is None else u_mask[rows])
+    errs = {k: compare.rel_err(g_out[k][rows], o[k]) for k in ("h", "c", "dh", "dc")}
+    others = np.ones(w.num_nodes, bool)
+    others[rows] = False
+    assert np.all(g_out["dh"][others] == 0) and np.all(g_out["dc"][others] == 0)
+    for s, (gg, oo) in enumerate(zip(g_out["grads"], o["grads"])):
+        for name in ("W_in", "W_rec", "bias"):
+            if gg.get(name) is None or oo.get(name) is None:
+                continue
+            errs[f"set{s}.{name}"] = compare.rel_err(gg[name], oo[name], whole=True)
+    if table_grad:
+        errs["d_table"] = compare.rel_err(g_out["d_table"], o["d_table"], whole=True)
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, (bad, errs)
+    return errs

@@ -20,37 +20,7 @@ pytestmark = pytest.mark.gpu
 
 
 def _sampled_parity(w, sample, table_grad):
-    tol = C.TOL[w.dtype]
-    rpg = gen.roots_per_graph(w.graph_ptr, w.child_idx)
-    roff = np.concatenate([[0], np.cumsum(rpg)])
-    dh = np.zeros_like(w.dh_roots)
-    for g in sample:
-        dh[roff[g]:roff[g + 1]] = w.dh_roots[roff[g]:roff[g + 1]]
-    w.dh_roots = dh
-    g_out = C.run_device(w, table_grad=table_grad)
-    sub = gen.subset(w, sample)
-    o = C.run_oracle(sub, table_grad=table_grad)
-    gp = w.graph_ptr
-    rows = np.concatenate([np.arange(gp[g], gp[g + 1]) for g in sample])
-    errs = {
-        "h": compare.rel_err(g_out["h"][rows], o["h"]),
-        "c": compare.rel_err(g_out["c"][rows], o["c"]),
-        "dh": compare.rel_err(g_out["dh"][rows], o["dh"]),
-        "dc": compare.rel_err(g_out["dc"][rows], o["dc"]),
-    }
-    mask = np.ones(w.num_nodes, bool)
-    mask[rows] = False
-    assert np.all(g_out["dh"][mask] == 0) and np.all(g_out["dc"][mask] == 0)
-    for s, (gg, oo) in enumerate(zip(g_out["grads"], o["grads"])):
-        for name in ("W_in", "W_rec", "bias"):
-            if gg.get(name) is None or oo.get(name) is None:
-                continue
-            errs[f"set{s}.{name}"] = compare.rel_err(gg[name], oo[name], whole=True)
-    if table_grad:
-        errs["d_table"] = compare.rel_err(g_out["d_table"], o["d_table"], whole=True)
-    bad = {k: v for k, v in errs.items() if not v <= tol}
-    assert not bad, (bad, errs)
-    return errs
+    return C.sampled_parity(w, sample, table_grad)
 
 
 def test_config2_full_bench_workload():

@@ -56,8 +56,9 @@ def test_large_graph_uses_global_scratch():
     C.assert_schedule_equal(_gpu_sched(w), C.oracle_schedule(w))
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 4])
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
 def test_full_config_schedules(k):
+    """All five workloads at full size, config 5's 2.0 M-node batch of 4,096 DAGs included."""
     w = gen.make_config(k)
     C.assert_schedule_equal(_gpu_sched(w), C.oracle_schedule(w))
 
