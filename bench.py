@@ -378,12 +378,13 @@ def table1(batches, steps: int, warmup: int, dtype: str = "f32") -> dict:
             "steps": steps, "warmup": warmup}
 
 
-def train_bench(config: int, steps: int, warmup: int, classes: int = 5) -> dict:
+def train_bench(config: int, steps: int, warmup: int, classes: int = 5, dropout: float = 0.0) -> dict:
     """Training steps of Section 3.5's setting on one workload: a class label on every node (uniform, seeded),
     forward, the per-node softmax cross-entropy head, backward from the head's gradients, Adam on every
     parameter tensor (weights, biases, the leaf table where it is trained, the classifier) and the in-place
     re-pack of the weights; the gradient pass (zero, forward, head, backward) is replayed as one recorded graph, Adam
-    and the re-pack are issued call by call.  The batch is the same every step, so the mean loss falls."""
+    and the re-pack are issued call by call.  The batch is the same every step, so the mean loss falls.  With
+    dropout > 0 every step first draws a fresh recurrent-dropout mask on the GPU (fold_dropout_mask)."""
     import numpy as np
     import torch
 
@@ -393,7 +394,7 @@ def train_bench(config: int, steps: int, warmup: int, classes: int = 5) -> dict:
     stream = torch.cuda.current_stream()
     w = gen.make_config(config)
     labels = np.random.default_rng(11).integers(0, classes, w.num_nodes).astype(np.int32)
-    ts = TrainStep(w, labels, classes, train_table=config in (3, 5))
+    ts = TrainStep(w, labels, classes, train_table=config in (3, 5), dropout=dropout, dropout_seed=17)
     mean_loss = lambda: float(ts.node_loss[:w.num_nodes].sum().item() * ts.scale)
     ts.step()
     ts.capture_gradients()  # the gradient pass replays as one graph; Adam and the re-pack run call by call
@@ -423,7 +424,8 @@ def train_bench(config: int, steps: int, warmup: int, classes: int = 5) -> dict:
             "warmup": warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "dtype": w.dtype,
             "data": "synthetic", "config": {"workload": w.name, "nodes": w.num_nodes, "hidden": w.hidden,
                                             "classes": classes, "optimizer": "adam lr 1e-3 (0.9, 0.999, 1e-8)",
-                                            "trained_leaf_table": config in (3, 5)},
+                                            "trained_leaf_table": config in (3, 5),
+                                            "recurrent_dropout": dropout},
             "mean_loss": {"step_1": round(first, 5), f"step_{ts.t - steps}": round(last, 5)},
             "kernels": kernels}
 
@@ -481,32 +483,220 @@ def blocks_bench(steps: int, warmup: int, num_trees: int = 1024, hidden: int = 3
             "host_compile_nodes_per_s": round(w.num_nodes / build_s, 1)}
 
 
+def _oracle_graph(w, g: int) -> int:
+    """The oracle, as it stands, on graph g of the workload alone (fp64 forward, + backward if the workload
+    has one); returns the graph's node count."""
+    from oracle import evaluate as EV
+    from paper_1702_02181_amd import gen
+    from tests._helpers import oracle_batch, oracle_params
+    sub = gen.subset(w, [g])
+    b = oracle_batch(sub)
+    P = oracle_params(sub)
+    f = EV.forward(b, P, w.hidden, w.leaf_table)
+    if w.backward:
+        EV.backward(b, P, w.hidden, w.leaf_table, f, sub.dh_roots.astype("float64"), None, want_table_grad=False)
+    return sub.num_nodes
+
+
 def cpu_baseline(w, budget_s: float):
     """The oracle as it stands, single thread, on whole graphs of the workload until ~budget_s."""
     from threadpoolctl import threadpool_limits
 
-    from oracle import evaluate as EV
-    from paper_1702_02181_amd import gen
-    from tests._helpers import oracle_batch, oracle_params
-
-    P = oracle_params(w)
     nodes = 0
     graphs = 0
     t0 = time.perf_counter()
     with threadpool_limits(limits=1):
         while graphs < w.num_graphs and (time.perf_counter() - t0) < budget_s:
-            sub = gen.subset(w, [graphs])
-            b = oracle_batch(sub)
-            f = EV.forward(b, P, w.hidden, w.leaf_table)
-            if w.backward:
-                EV.backward(b, P, w.hidden, w.leaf_table, f, sub.dh_roots.astype("float64"), None,
-                            want_table_grad=False)
-            nodes += sub.num_nodes
+            nodes += _oracle_graph(w, graphs)
             graphs += 1
     dt = time.perf_counter() - t0
     return {"value": nodes / dt, "unit": "graph nodes/s", "cores": 1, "kind": "oracle",
-            "sample": f"{graphs} of {w.num_graphs} graphs ({nodes} nodes), fp64 "
-                      f"{'forward+backward' if w.backward else 'forward'}, {dt:.1f} s"}
+            "sample": f"graphs 0..{graphs - 1} of {w.num_graphs} ({nodes} nodes), fp64 "
+                      f"{'forward+backward' if w.backward else 'forward'}, one thread, {dt:.1f} s"}
+
+
+_POOL_W = None
+
+
+def _pool_init(config: int):
+    global _POOL_W
+    from threadpoolctl import threadpool_limits
+    from paper_1702_02181_amd import gen
+    threadpool_limits(limits=1)
+    _POOL_W = gen.make_config(config)
+
+
+def _pool_ready(_):
+    time.sleep(0.05)
+    return os.getpid()
+
+
+def _pool_graph(g: int) -> int:
+    return _oracle_graph(_POOL_W, g)
+
+
+def cpu_baseline_allcore(config: int, w, rate_1core: float, budget_s: float, max_workers: int = 16):
+    """The same oracle over a process pool of single-threaded workers (graphs are independent), one worker
+    per host core up to the machine's CPU share; graphs 0..K-1 with K sized from the one-core rate so that the
+    timed map takes about budget_s.  Workers build the workload themselves before the timed region.  Runs
+    before anything touches the GPU (workers are started by spawn from a process with no GPU state)."""
+    import multiprocessing as mp
+    workers = max(1, min(max_workers, os.cpu_count() or 1))
+    per_graph = w.num_nodes / max(1, w.num_graphs)
+    rounds = max(1, round(rate_1core * budget_s / per_graph))  # graphs per worker
+    K = int(min(w.num_graphs, rounds * workers))
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(workers, initializer=_pool_init, initargs=(config,)) as pool:
+        pids = set(pool.map(_pool_ready, range(8 * workers), chunksize=1))
+        t0 = time.perf_counter()
+        nodes = sum(pool.map(_pool_graph, range(K), chunksize=1))
+        dt = time.perf_counter() - t0
+    return {"value": nodes / dt, "unit": "graph nodes/s", "cores": workers, "kind": "oracle",
+            "host_cores": os.cpu_count(), "workers_started": len(pids),
+            "sample": f"graphs 0..{K - 1} of {w.num_graphs} ({nodes} nodes), fp64 "
+                      f"{'forward+backward' if w.backward else 'forward'}, {workers} single-threaded processes, "
+                      f"{dt:.1f} s"}
+
+
+def reference_schedule_ms(w) -> float:
+    """The oracle's reference scheduler (validation, memoised depth recursion, stable sort, edge labels;
+    Python) on the whole batch, in ms."""
+    from tests import gpu_common as C
+    t0 = time.perf_counter()
+    C.oracle_schedule(w)
+    return (time.perf_counter() - t0) * 1e3
+
+
+def measure(w, steps: int, warmup: int, table_grad: bool, schedule_reps: int = 5, tag: str = "") -> dict:
+    """One workload on the GPU: fold_schedule time, the step (forward + backward, or forward only) issued
+    call by call and as a HIP-graph replay, per-launch HIP-event durations by kernel class, the roofline of
+    the dominant kernel class and of every class of level pass."""
+    import torch
+
+    from paper_1702_02181_amd import fold as F
+    from paper_1702_02181_amd.runner import DeviceRun
+
+    dev = DeviceRun(w)
+    host = dev.sched.host_groups()
+    N = w.num_nodes
+    sched_ms = []
+    for _ in range(schedule_reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        s = F.Schedule(dev.graph_ptr, dev.node_op, dev.child_ptr, dev.child_idx, dev.node_input, dev.ops,
+                       dev.leaf_rows)
+        torch.cuda.synchronize()
+        sched_ms.append((time.perf_counter() - t0) * 1e3)
+        del s
+    schedule_ms = statistics.median(sched_ms) if sched_ms else None
+
+    if w.backward:
+        dev.alloc_grads(table_grad)
+        dev.set_upstream(w.dh_roots)
+
+    def step():
+        if w.backward:
+            dev.zero_grads()
+        dev.forward()
+        if w.backward:
+            dev.backward()
+
+    print(f"[bench{tag}] {w.name}: N={N} levels={dev.sched.num_levels} groups={len(host['group_op'])} "
+          f"warmup={warmup} steps={steps}", file=sys.stderr, flush=True)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    # the step as issued call by call, then recorded once as a HIP graph and replayed
+    eager_ms = timed(step)
+    graph = dev.make_graph(backward=w.backward, zero_grads=True)
+    graph_ms = timed(graph.launch)
+    print(f"[bench{tag}] timed {steps} steps: graph {graph_ms:.3f} ms/step, eager {eager_ms:.3f} ms/step "
+          f"({graph.num_nodes} graph nodes)", file=sys.stderr, flush=True)
+
+    # per-kernel durations over a second timed region (event pair around every launch, on the stream the
+    # kernels run on)
+    F.fold_profile_enable(True)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    launch_times = F.fold_profile_read_launches()
+    F.fold_profile_enable(False)
+    stats = {}
+    for name, _g, _o, ms in launch_times:
+        n, tot, mx = stats.get(name, (0, 0.0, 0.0))
+        stats[name] = (n + 1, tot + ms, max(mx, ms))
+    flops = flops_by_kernel(w, host, table_grad)
+    kernels = {}
+    for name, (launches, total_ms, max_ms) in stats.items():
+        per_step_ms = total_ms / steps
+        kernels[name] = {"launches_per_step": launches / steps, "ms_per_step": round(per_step_ms, 4),
+                         "avg_launch_us": round(1e3 * total_ms / max(launches, 1), 2)}
+        if name in flops:
+            kernels[name]["tflops"] = round(flops[name] / (per_step_ms * 1e-3) / 1e12, 2)
+    mfma_kernels = [k for k in kernels if k in flops]
+    dom = max(mfma_kernels, key=lambda k: kernels[k]["ms_per_step"]) if mfma_kernels else None
+    roofline = None
+    if dom:
+        peak = PEAKS["bf16_mfma_tflops"] if dom.endswith("bf16") else PEAKS["f32_mfma_tflops"]
+        launches = stats[dom][0] / steps
+        avg_s = (stats[dom][1] / steps) / launches * 1e-3
+        per_launch = flops[dom] / launches
+        ach = per_launch / avg_s / 1e12
+        rec = traffic_record(dom, w.name)
+        roofline = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                    "frac": round(ach / peak, 4), "traffic": None if rec is None else rec["bytes_per_launch"],
+                    "traffic_unit": "bytes per launch (HBM read + write, rocprofv3 FETCH_SIZE / WRITE_SIZE "
+                                    "scaled by the copy probe)",
+                    "flops_per_launch": per_launch, "launches_per_step": launches,
+                    "avg_launch_us": round(avg_s * 1e6, 2)}
+        # algorithmic HBM bytes per launch of the class (the level passes it runs in, weights once per pass)
+        kind = {"cell_fwd": "fwd", "bwd_dx": "bwd", "wgrad": "wgrad"}[class_of(dom)]
+        alg = 0.0
+        for (pk, key), (_fl, by) in pass_work(w, host, table_grad).items():
+            if pk != kind:
+                continue
+            if kind == "fwd":
+                from paper_1702_02181_amd import gen as _g
+                if f"cell_fwd.{_g.KIND_NAMES[w.ops[int(host['group_op'][key])].kind]}." not in dom + ".":
+                    continue
+            alg += by
+        roofline["algorithmic_bytes_per_launch"] = round(alg / launches)
+        if rec is not None:
+            roofline["traffic_vs_algorithmic"] = round(rec["bytes_per_launch"] / (alg / launches), 3)
+    total_flops = sum(flops.values())
+    step_peak = PEAKS["bf16_mfma_tflops"] if w.dtype == "bf16" else PEAKS["f32_mfma_tflops"]
+    classes = level_classes(pass_work(w, host, table_grad), launch_times, steps, step_peak, PEAKS["hbm_gbs"])
+    out = {
+        "value": round(N / (graph_ms * 1e-3), 1),
+        "ms_per_step": round(graph_ms, 4),
+        "eager_ms_per_step": round(eager_ms, 4),
+        "dtype": "f32" if w.dtype == "f32" else "bf16",
+        "config": {"workload": w.name, "graphs": w.num_graphs, "nodes": N, "levels": dev.sched.num_levels,
+                   "groups": len(host["group_op"]), "hidden": w.hidden,
+                   "pass": "forward+backward" if w.backward else "forward",
+                   "leaf_table_grad": bool(w.backward and table_grad)},
+        "schedule_ms": None if schedule_ms is None else round(schedule_ms, 3),
+        "graph_nodes": graph.num_nodes,
+        "roofline": roofline,
+        "step_mfma_frac": round(total_flops / (graph_ms * 1e-3) / 1e12 / step_peak, 4),
+        "level_classes": classes,
+        "kernels": kernels,
+    }
+    del graph, dev
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -515,15 +705,18 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=2)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=8.0, help="time of each oracle leg (one core, all cores)")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--profile-only", action="store_true", help="skip the oracle leg and the schedule timing")
+    ap.add_argument("--profile-only", action="store_true", help="skip the oracle legs and the other workloads")
+    ap.add_argument("--extra-configs", default="3,5",
+                    help="workloads measured after the headline one, reported under 'configs' ('' for none)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--traffic-kernel", default=None)
     ap.add_argument("--table1", action="store_true",
                     help="run the Table 1 protocol (manual / dynamic / full-dynamic batching) instead")
     ap.add_argument("--train", action="store_true",
                     help="time training steps (per-node softmax loss, Adam, re-pack) instead; default config 3")
+    ap.add_argument("--dropout", type=float, default=0.0, help="recurrent dropout probability of --train")
     ap.add_argument("--blocks", action="store_true",
                     help="compile sentiment-shaped trees with the combinator front end and time the compiled batch")
     ap.add_argument("--counters-from", nargs=4, metavar=("MFMA_CSV", "FETCH_CSV", "WRITE_CSV", "TRACE_CSV"),
@@ -547,7 +740,7 @@ def main():
         import torch
         torch.cuda.set_device(0)
         cfg = args.config if "--config" in sys.argv else 3
-        print(json.dumps(train_bench(cfg, args.steps, args.warmup)), flush=True)
+        print(json.dumps(train_bench(cfg, args.steps, args.warmup, dropout=args.dropout)), flush=True)
         return
     if args.table1:
         import torch
@@ -560,12 +753,30 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
+    from paper_1702_02181_amd import gen
+
+    print(f"[bench] generating config {args.config}", file=sys.stderr, flush=True)
+    w = gen.make_config(args.config)
+    table_grad = args.config in (3, 5)  # trainable embedding tables; config 2 / 4 leaf rows are data
+
+    # host legs first, before anything touches the GPU: the oracle on one core and on a process pool, and
+    # the oracle's reference scheduler on the whole batch
+    cpu = None
+    sched_ref_ms = None
+    if not args.no_cpu and not args.profile_only:
+        print(f"[bench] oracle on host cores ({args.cpu_seconds:.0f} s one core, then a process pool)",
+              file=sys.stderr, flush=True)
+        one = cpu_baseline(w, args.cpu_seconds)
+        cpu = cpu_baseline_allcore(args.config, w, one["value"], args.cpu_seconds)
+        cpu["single_core"] = one
+        print(f"[bench] oracle: {one['value']:.0f} nodes/s on one core, {cpu['value']:.0f} on {cpu['cores']}",
+              file=sys.stderr, flush=True)
+        sched_ref_ms = reference_schedule_ms(w)
+        print(f"[bench] reference scheduler: {sched_ref_ms:.0f} ms", file=sys.stderr, flush=True)
+
     import torch
 
     from paper_1702_02181_amd import fold as F
-    from paper_1702_02181_amd import gen
-    from paper_1702_02181_amd.runner import DeviceRun
 
     torch.cuda.set_device(0)
     # achievable peaks on this GPU (MFMA loop, stream copy), next to the datasheet figures
@@ -582,130 +793,48 @@ def main():
     except Exception as e:  # probes are diagnostics; the bench line does not depend on them
         probes["error"] = str(e)
     print(f"[bench] probes {probes}", file=sys.stderr, flush=True)
-    print(f"[bench] generating config {args.config}", file=sys.stderr, flush=True)
-    w = gen.make_config(args.config)
-    table_grad = args.config in (3, 5)  # trainable embedding tables; config 2 / 4 leaf rows are data
-    dev = DeviceRun(w)
-    host = dev.sched.host_groups()
-    N = w.num_nodes
 
-    # schedule time: fold_schedule end to end (validate, depth, sort, emit, read-back)
-    sched_ms = []
+    head = measure(w, args.steps, args.warmup, table_grad, schedule_reps=0 if args.profile_only else 5)
+    del w
+    extra = {}
     if not args.profile_only:
-        for _ in range(5):
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            s = F.Schedule(dev.graph_ptr, dev.node_op, dev.child_ptr, dev.child_idx, dev.node_input, dev.ops,
-                           dev.leaf_rows)
-            torch.cuda.synchronize()
-            sched_ms.append((time.perf_counter() - t0) * 1e3)
-            del s
-    schedule_ms = statistics.median(sched_ms) if sched_ms else None
+        for k in [int(x) for x in args.extra_configs.split(",") if x.strip()]:
+            if k == args.config:
+                continue
+            print(f"[bench] generating config {k}", file=sys.stderr, flush=True)
+            wk = gen.make_config(k)
+            # config 5 steps take ~0.2 s: fewer steps keep the whole run within minutes
+            steps_k = min(args.steps, 5) if wk.num_nodes > 1_000_000 else args.steps
+            mk = measure(wk, steps_k, min(args.warmup, 2), k in (3, 5), schedule_reps=3, tag=f" cfg{k}")
+            mk["steps"] = steps_k
+            extra[wk.name] = mk
+            del wk
 
-    if w.backward:
-        dev.alloc_grads(table_grad)
-        dev.set_upstream(w.dh_roots)
-
-    def step():
-        if w.backward:
-            dev.zero_grads()
-        dev.forward()
-        if w.backward:
-            dev.backward()
-
-    print(f"[bench] N={N} levels={dev.sched.num_levels} groups={len(host['group_op'])} warmup={args.warmup}",
-          file=sys.stderr, flush=True)
-    stream = torch.cuda.current_stream()
-
-    def timed(fn):
-        for _ in range(args.warmup):
-            fn()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(args.steps):
-            fn()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / args.steps
-
-    # the step as issued call by call, then recorded once as a HIP graph and replayed
-    eager_ms = timed(step)
-    graph = dev.make_graph(backward=w.backward, zero_grads=True)
-    graph_ms = timed(graph.launch)
-    ms_per_step = graph_ms
-    print(f"[bench] timed {args.steps} steps: graph {graph_ms:.3f} ms/step, eager {eager_ms:.3f} ms/step "
-          f"({graph.num_nodes} graph nodes)", file=sys.stderr, flush=True)
-
-    # per-kernel durations over a second timed region (event pair around every launch)
-    F.fold_profile_enable(True)
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    launch_times = F.fold_profile_read_launches()
-    F.fold_profile_enable(False)
-    stats = {}
-    for name, _g, _o, ms in launch_times:
-        n, tot, mx = stats.get(name, (0, 0.0, 0.0))
-        stats[name] = (n + 1, tot + ms, max(mx, ms))
-    flops = flops_by_kernel(w, host, table_grad)
-    kernels = {}
-    for name, (launches, total_ms, max_ms) in stats.items():
-        per_step_ms = total_ms / args.steps
-        kernels[name] = {"launches_per_step": launches / args.steps, "ms_per_step": round(per_step_ms, 4),
-                         "avg_launch_us": round(1e3 * total_ms / max(launches, 1), 2)}
-        if name in flops:
-            kernels[name]["tflops"] = round(flops[name] / (per_step_ms * 1e-3) / 1e12, 2)
-    mfma_kernels = [k for k in kernels if k in flops]
-    dom = max(mfma_kernels, key=lambda k: kernels[k]["ms_per_step"]) if mfma_kernels else None
-    roofline = None
-    if dom:
-        peak = PEAKS["bf16_mfma_tflops"] if dom.endswith("bf16") else PEAKS["f32_mfma_tflops"]
-        launches = stats[dom][0] / args.steps
-        avg_s = (stats[dom][1] / args.steps) / launches * 1e-3
-        per_launch = flops[dom] / launches
-        ach = per_launch / avg_s / 1e12
-        rec = traffic_record(dom, w.name)
-        roofline = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
-                    "frac": round(ach / peak, 4), "traffic": None if rec is None else rec["bytes_per_launch"],
-                    "traffic_unit": "bytes per launch (HBM read + write, rocprofv3 FETCH_SIZE / WRITE_SIZE "
-                                    "scaled by the copy probe)",
-                    "flops_per_launch": per_launch, "launches_per_step": launches,
-                    "avg_launch_us": round(avg_s * 1e6, 2)}
-    total_flops = sum(flops.values())
-    step_peak = PEAKS["bf16_mfma_tflops"] if w.dtype == "bf16" else PEAKS["f32_mfma_tflops"]
-    classes = level_classes(pass_work(w, host, table_grad), launch_times, args.steps, step_peak, PEAKS["hbm_gbs"])
-
-    cpu = None
-    if not args.no_cpu and not args.profile_only:
-        print(f"[bench] oracle on host cores (~{args.cpu_seconds:.0f} s)", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(w, args.cpu_seconds)
-
-    value = N / (ms_per_step * 1e-3)
     out = {
         "metric": "graph nodes/sec (TreeLSTM fwd+bwd, 1 GPU)",
-        "value": round(value, 1),
+        "value": head["value"],
         "unit": "graph nodes/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
-        "eager_ms_per_step": round(eager_ms, 4),
+        "ms_per_step": head["ms_per_step"],
+        "eager_ms_per_step": head["eager_ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if w.dtype == "f32" else "bf16",
+        "dtype": head["dtype"],
         "data": "synthetic",
-        "config": {"workload": w.name, "graphs": w.num_graphs, "nodes": N, "levels": dev.sched.num_levels,
-                   "hidden": w.hidden, "pass": "forward+backward" if w.backward else "forward"},
-        "schedule_ms": None if schedule_ms is None else round(schedule_ms, 3),
-        "graph_nodes": graph.num_nodes,
+        "config": head["config"],
+        "schedule_ms": head["schedule_ms"],
+        "schedule_ms_oracle": None if sched_ref_ms is None else round(sched_ref_ms, 1),
+        "graph_nodes": head["graph_nodes"],
         "peaks": {"datasheet": PEAKS, "measured": probes},
-        "roofline": roofline,
-        "step_mfma_frac": round(total_flops / (ms_per_step * 1e-3) / 1e12 / step_peak, 4),
-        "level_classes": classes,
-        "kernels": kernels,
+        "roofline": head["roofline"],
+        "step_mfma_frac": head["step_mfma_frac"],
+        "level_classes": head["level_classes"],
+        "kernels": head["kernels"],
         "cpu_baseline": cpu,
+        "configs": extra,
     }
     print(json.dumps(out), flush=True)
 

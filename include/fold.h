@@ -280,6 +280,27 @@ int32_t fold_backward_dropout(const fold_sched* sched, const fold_packed* packed
                               float* dh_out, float* dc_out,
                               void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* fold_dropout_mask: draws the recurrent-dropout mask of one training step
+ * (the u_mask of fold_forward_dropout / fold_backward_dropout) on the GPU
+ * from the counter-based generator Philox4x32-10 (Salmon, Moraes, Dror and
+ * Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011).  For node
+ * v and hidden unit j < hidden, with r the (j mod 4)-th output word of the
+ * call on counter (v, j / 4, low and high 32 bits of step) under the key
+ * (low and high 32 bits of seed):
+ *     mask[pos(v)][j] = 0 if r < min(floor(p 2^32), 2^32 - 1), else (float)(1 / (1 - p))
+ * (inverted dropout: kept units are scaled so the expected multiplier is 1).
+ *   mask    device [N, fold_row_ld(hidden)] fp32, POOL order (row q = node
+ *           pos_node[q]), 16-byte aligned; written whole, pad columns 0.
+ *           Caller-owned.
+ *   p       drop probability in [0, 1); p = 0 gives all ones.
+ *   seed, step  any 64-bit values; a node's row depends only on (v, seed,
+ *           step, p), not on the batch around it.
+ * FOLD_E_INVALID for a NULL schedule, hidden outside 1..4096, p outside
+ * [0, 1), or a NULL or misaligned mask (N > 0).  Asynchronous; allocates
+ * nothing. */
+int32_t fold_dropout_mask(const fold_sched* sched, int32_t hidden, double p, uint64_t seed, uint64_t step,
+                          float* mask, hipStream_t stream);
+
 /* ---- the training step around the path ------------------------------------
  * Section 3.5 trains the binary Tree-LSTM on trees whose every node carries a
  * class label: a linear layer and a softmax on every node's state h, the
@@ -303,8 +324,10 @@ int32_t fold_backward_dropout(const fold_sched* sched, const fold_packed* packed
  *   dh_nodes   device [N, fold_row_ld(H)] fp32, POOL order (written, pad
  *              columns zero): the dh_nodes argument of fold_backward
  *   dW_cls, db_cls  device, fp32, accumulated (+=; the caller zeroes them);
- *              partial sums per block of rows are added in a fixed order, so
- *              the result is the same in every run
+ *              partial sums per block of rows are added in a fixed order,
+ *              but the four waves of a block meet in LDS in arrival order,
+ *              so the result is reproducible up to the order of those fp32
+ *              additions, not bit for bit
  *   ws         device workspace of >= fold_loss_workspace_size bytes (the
  *              per-block partial sums; contents on entry do not matter)
  * FOLD_E_INVALID for an unsupported class count, H * num_classes above

@@ -845,6 +845,28 @@ int32_t fold_adam_step(int64_t n, float* param, uint16_t* param_bf16, const floa
   FOLD_GUARD_END
 }
 
+int32_t fold_dropout_mask(const fold_sched* sh, int32_t hidden, double p, uint64_t seed, uint64_t step, float* mask,
+                          hipStream_t st) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!sh) return fail(FOLD_E_INVALID, "fold_dropout_mask: NULL schedule");
+  if (hidden < 1 || hidden > kMaxHidden) return fail(FOLD_E_INVALID, "fold_dropout_mask: hidden size out of range");
+  if (!(p >= 0.0 && p < 1.0)) return fail(FOLD_E_INVALID, "fold_dropout_mask: need 0 <= p < 1");
+  const Sched& s = sh->s;
+  if (s.N == 0) return FOLD_OK;
+  if (!mask) return fail(FOLD_E_INVALID, "fold_dropout_mask: NULL mask");
+  if (reinterpret_cast<uintptr_t>(mask) & 15)
+    return fail(FOLD_E_INVALID, "fold_dropout_mask: mask must be 16-byte aligned");
+  // drop where the word is below floor(p 2^32); kept units carry 1 / (1 - p) (inverted dropout)
+  const double t = std::min(std::floor(p * 4294967296.0), 4294967295.0);
+  const float scale = (float)(1.0 / (1.0 - p));
+  launch_dropout_mask(s.pos_node, s.N, hidden, row_ld(hidden), (unsigned)t, scale, (unsigned long long)seed,
+                      (unsigned long long)step, mask, st);
+  FOLD_HIP_CHECK(hipGetLastError());
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
 int32_t fold_packed_free(fold_packed* h) {
   FOLD_GUARD_BEGIN
   packed_destroy_impl(h);

@@ -212,6 +212,8 @@ size_t loss_workspace_bytes(int H, int C);
 void launch_loss_ce(int dtype, int N, int H, int ld, int C, const void* h_pool, const int* pos_node, const int* labels,
                     const float* W, const float* b, float scale, float* node_loss, float* dh, float* dW, float* db,
                     float* ws, hipStream_t st);
+void launch_dropout_mask(const int* pos_node, int N, int H, int ld, unsigned thresh, float scale,
+                         unsigned long long seed, unsigned long long step, float* mask, hipStream_t st);
 void launch_adam(size_t n, float* p, uint16_t* p_bf16, const float* g, float* m, float* v, double b1, double b2,
                  double lr_t, double eps, hipStream_t st);
 

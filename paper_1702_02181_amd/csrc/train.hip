@@ -16,9 +16,15 @@
 //             HBM-bound: it reads each h row once (up to 512 columns kept in registers for the second pass)
 //             and writes each dh row once.
 // k_loss_reduce  dW, db += the blocks' partial sums in a fixed order (no atomics: every address would take
-//             one from each block, one after another, and the result is the same in every run).
+//             one from each block, one after another).  Inside a block the four waves' sums meet in LDS by
+//             atomic adds in whatever order the waves arrive, so dW and db are reproducible up to the order
+//             of those fp32 additions, not bit for bit.
 // k_adam      elementwise, four values per thread: m, v and the fp32 parameters updated in place, plus an
 //             optional bf16 copy of the parameters (the operand type of bf16 models).
+// k_dropout_mask  the recurrent-dropout mask of a step (Section 3.5 trains with recurrent dropout), drawn
+//             from the counter-based generator Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC 2011): one
+//             generator call per (node, block of 4 hidden units), its four 32-bit words deciding the four
+//             units; written in pool order as one 16-byte store per call.
 
 #include <hip/hip_runtime.h>
 
@@ -353,7 +359,55 @@ __global__ void k_adam(size_t n, float* p, uint16_t* p_bf16, const float* g, flo
   }
 }
 
+// Philox4x32-10: ten rounds of (c0, c1, c2, c3) -> (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1,
+// lo(M0 c0)), the key advancing by the Weyl constants between rounds.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, unsigned k0, unsigned k1) {
+  constexpr unsigned M0 = 0xD2511F53u, M1 = 0xCD9E8D57u, W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += W0;
+      k1 += W1;
+    }
+    const unsigned hi0 = __umulhi(M0, c.x), lo0 = M0 * c.x;
+    const unsigned hi1 = __umulhi(M1, c.z), lo1 = M1 * c.z;
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+  }
+  return c;
+}
+
+// mask[q][4 b .. 4 b + 3] of pool row q (node v = pos_node[q]) from the call on counter (v, b, step_lo,
+// step_hi) under the key (seed_lo, seed_hi): 0 where the word is below thresh, else scale; pad units
+// (>= H) are 0.  One thread per (row, 4-unit block); blocks4 = ld / 4.
+__global__ __launch_bounds__(256) void k_dropout_mask(const int* pos_node, long long total, int blocks4, int H,
+                                                      unsigned thresh, float scale, unsigned k0, unsigned k1,
+                                                      unsigned s0, unsigned s1, float* mask) {
+  const long long t = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= total) return;
+  const long long q = t / blocks4;
+  const int b = (int)(t - q * blocks4);
+  const unsigned v = (unsigned)pos_node[q];
+  const uint4 r = philox4x32_10(make_uint4(v, (unsigned)b, s0, s1), k0, k1);
+  const unsigned w[4] = {r.x, r.y, r.z, r.w};
+  float out[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = (4 * b + i < H && w[i] >= thresh) ? scale : 0.f;
+  *reinterpret_cast<float4*>(mask + (size_t)t * 4) = make_float4(out[0], out[1], out[2], out[3]);
+}
+
 }  // namespace
+
+void launch_dropout_mask(const int* pos_node, int N, int H, int ld, unsigned thresh, float scale,
+                         unsigned long long seed, unsigned long long step, float* mask, hipStream_t st) {
+  if (N <= 0) return;
+  ProfScope prof("dropout_mask", st);
+  const int blocks4 = ld / 4;
+  const long long total = (long long)N * blocks4;
+  const unsigned grid = (unsigned)((total + 255) / 256);
+  hipLaunchKernelGGL(k_dropout_mask, dim3(grid), dim3(256), 0, st, pos_node, total, blocks4, H, thresh, scale,
+                     (unsigned)(seed & 0xffffffffu), (unsigned)(seed >> 32), (unsigned)(step & 0xffffffffu),
+                     (unsigned)(step >> 32), mask);
+}
 
 bool loss_classes_supported(int C) {
   return C == 2 || C == 3 || C == 4 || C == 5 || C == 6 || C == 7 || C == 8 || C == 10 || C == 16 || C == 32;

@@ -165,11 +165,20 @@ class TrainStep:
     (the weights of every set, the biases, the leaf table if trained, the classifier), fold_pack_update.
 
     fp32 master copies of the weights are kept here; for bf16 workloads Adam also writes the bf16 weights
-    that fold_pack_update packs.  The loss is the mean over the labelled nodes (scale = 1 / their count)."""
+    that fold_pack_update packs.  The loss is the mean over the labelled nodes (scale = 1 / their count).
+
+    dropout > 0 trains with recurrent dropout (Section 3.5): every step first draws a fresh mask on the GPU
+    (fold_dropout_mask with counter = (node, unit block, step number), key = dropout_seed) and runs
+    fold_forward_dropout / fold_backward_dropout with it."""
 
     def __init__(self, w: gen.Workload, labels: np.ndarray, num_classes: int, train_table: bool, seed: int = 0,
-                 lr: float = 1e-3, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8):
+                 lr: float = 1e-3, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+                 dropout: float = 0.0, dropout_seed: int = 0):
         self.dev = dev = DeviceRun(w)
+        self.dropout = float(dropout)
+        self.dropout_seed = int(dropout_seed)
+        self.u_mask = (torch.zeros((max(dev.N, 1), dev.ld), dtype=torch.float32, device=dev.device)
+                       if self.dropout > 0 else None)
         self.C = num_classes
         self.hyper = (lr, beta1, beta2, eps)
         self.t = 0
@@ -208,21 +217,28 @@ class TrainStep:
         self.tensors += [(self.W_cls, None, self.dW_cls), (self.b_cls, None, self.db_cls)]
         self.moments = [(torch.zeros_like(m), torch.zeros_like(m)) for m, _, _ in self.tensors]
 
+    def draw_mask(self):
+        """The recurrent-dropout mask of step self.t into self.u_mask (pool order)."""
+        F.fold_dropout_mask(self.dev.sched.handle, self.dev.H, self.dropout, self.dropout_seed, self.t, self.u_mask,
+                            self.dev.stream)
+
     def gradients(self):
-        """Zero the gradients, forward, head, backward (kernel launches only: capturable as a graph)."""
+        """Zero the gradients, forward, head, backward (kernel launches only: capturable as a graph).  With
+        dropout they read the mask that step() draws first."""
         dev = self.dev
         dev.zero_grads()
         self.dW_cls.zero_()
         self.db_cls.zero_()
-        dev.forward()
+        dev.forward(self.u_mask)
         F.fold_loss_softmax_ce(dev.sched.handle, dev.packed.handle, dev.h_pool, self.labels, self.C, self.W_cls,
                                self.b_cls, self.scale, self.node_loss, self.dh_nodes, self.dW_cls, self.db_cls,
                                self.loss_ws, self.loss_ws_bytes, dev.stream)
-        dev.backward()
+        dev.backward(u_mask=self.u_mask)
 
     def capture_gradients(self):
         """Record gradients() once as a graph (torch.cuda.CUDAGraph over the library's launches on the capture
-        stream); step(graph=True) then replays it.  Adam and the re-pack stay outside: their step count changes."""
+        stream); step(graph=True) then replays it.  Adam, the re-pack and the mask draw stay outside: the step
+        count enters each of them."""
         self.graph = torch.cuda.CUDAGraph()
         torch.cuda.synchronize()
         with torch.cuda.graph(self.graph):
@@ -232,6 +248,8 @@ class TrainStep:
     def step(self, graph: bool = False):
         dev = self.dev
         self.t += 1
+        if self.u_mask is not None:
+            self.draw_mask()
         if graph:
             self.graph.replay()
         else:

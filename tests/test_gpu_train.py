@@ -306,3 +306,82 @@ def test_captured_gradient_pass_replays_match_eager():
             assert err <= 1e-6, (it, k, err)
         ts.step(graph=True)  # the weights move between the checks
         torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("H,p,seed,step", [(1, 0.5, 0, 1), (7, 0.25, 12345, 2), (300, 0.25, (9 << 40) | 77, 3),
+                                           (64, 0.0, 5, 1), (1024, 0.9, 3, (1 << 33) + 5), (130, 0.5, 1, 0)])
+def test_dropout_mask_matches_oracle_bit_for_bit(H, p, seed, step):
+    """fold_dropout_mask (Philox4x32-10 on the GPU) against the oracle's own Philox draw, every element: the
+    counter layout (node, 4-unit block, step), the key (seed), the integer threshold and the scale, pool
+    order with zero pad columns; node ids shuffled within graphs so that pool order differs from node order."""
+    import torch
+    from oracle import philox as PX
+    from paper_1702_02181_amd.runner import DeviceRun
+    w = gen.shuffle_within_graphs(gen.config3(seed=4, num_graphs=40, hidden=H, vocab=50, emb_dim=8), 3)
+    dev = DeviceRun(w, with_backward=False)
+    mask = torch.full((dev.N, dev.ld), float("nan"), dtype=torch.float32, device="cuda")
+    F.fold_dropout_mask(dev.sched.handle, H, p, seed, step, mask)
+    got = mask.cpu().numpy()
+    assert np.all(got[:, H:] == 0)
+    want = PX.dropout_mask(w.num_nodes, H, p, seed, step)
+    node_pos = dev.sched_arrays()["node_pos"]
+    assert np.array_equal(got[node_pos, :H], want)
+
+
+def test_dropout_mask_argument_errors():
+    import torch
+    from paper_1702_02181_amd.runner import DeviceRun
+    w = gen.config3(seed=4, num_graphs=3, hidden=8, vocab=20, emb_dim=8)
+    dev = DeviceRun(w, with_backward=False)
+    mask = torch.zeros((dev.N, dev.ld), dtype=torch.float32, device="cuda")
+    for args in ((8, 1.0), (8, -0.1), (8, float("nan")), (0, 0.5), (4097, 0.5)):
+        with pytest.raises(F.FoldError) as e:
+            F.fold_dropout_mask(dev.sched.handle, args[0], args[1], 1, 1, mask)
+        assert e.value.code == F.FOLD_E_INVALID
+    with pytest.raises(F.FoldError) as e:
+        F.fold_dropout_mask(dev.sched.handle, 8, 0.5, 1, 1, None)
+    assert e.value.code == F.FOLD_E_INVALID
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("graph", [False, True])
+def test_training_steps_with_recurrent_dropout_match_oracle(graph):
+    """Three TrainStep steps with recurrent dropout (p = 0.3, a fresh GPU-drawn mask every step; eagerly, and
+    with the gradient pass replayed from a graph recorded once while the mask is redrawn outside it), fp32,
+    against three oracle steps whose masks the oracle draws itself (same generator, counter and key): every
+    parameter tensor after Adam."""
+    dtype = "f32"
+    from oracle import philox as PX
+    from paper_1702_02181_amd.runner import TrainStep
+    w = _workload(33, dtype, seed=23)
+    H, Cn, lr, eps, p, dseed = w.hidden, 5, 1e-2, 1e-4, 0.3, 991
+    y = _labels(np.random.default_rng(6), w.num_nodes, Cn)
+    ts = TrainStep(w, y, Cn, train_table=True, seed=3, lr=lr, eps=eps, dropout=p, dropout_seed=dseed)
+    if graph:
+        ts.capture_gradients()
+    Wc, bc = ts.W_cls.cpu().numpy().astype(np.float64), np.zeros(Cn)
+    P = oracle_params(w)
+    table = w.leaf_table.astype(np.float64)
+    ob = oracle_batch(w)
+    keys = [(s, name) for s, pp in enumerate(P) for name in ("W_in", "W_rec", "bias") if pp.get(name) is not None]
+    mom = {k: (0.0, 0.0) for k in keys + ["table", "Wc", "bc"]}
+    for t in (1, 2, 3):
+        ts.step(graph=graph)
+        m = PX.dropout_mask(w.num_nodes, H, p, dseed, t)
+        f = EV.forward(ob, P, H, table, m)
+        _, dh, dWc, dbc = OT.softmax_ce(f["h"], y, Wc, bc, ts.scale)
+        bw = EV.backward(ob, P, H, table, f, np.zeros_like(w.dh_roots, dtype=np.float64), dh, want_table_grad=True)
+        for s, name in keys:
+            P[s][name], *mom[(s, name)] = OT.adam_step(P[s][name], bw["grads"][s][name], *mom[(s, name)], t=t, lr=lr,
+                                                      eps=eps)
+        table, *mom["table"] = OT.adam_step(table, bw["d_table"], *mom["table"], t=t, lr=lr, eps=eps)
+        Wc, *mom["Wc"] = OT.adam_step(Wc, dWc, *mom["Wc"], t=t, lr=lr, eps=eps)
+        bc, *mom["bc"] = OT.adam_step(bc, dbc, *mom["bc"], t=t, lr=lr, eps=eps)
+    want = [P[s][name] for s, name in keys] + [table, Wc, bc]
+    got = [mm.cpu().numpy() for mm, _, _ in ts.tensors]
+    assert len(got) == len(want)
+    # an update moves a value by at most about 2 lr a step; fp32 gradients shift it by far less
+    atol = lr * 1e-3
+    for k, (g, o) in enumerate(zip(got, want)):
+        g = g.reshape(o.shape[0], -1)[:, :o.reshape(o.shape[0], -1).shape[1]].reshape(o.shape)
+        np.testing.assert_allclose(g, o, rtol=0, atol=atol, err_msg=f"tensor {k}")
