@@ -92,7 +92,7 @@ struct Sched {
   int N = 0, E = 0, G = 0, num_ops = 0, D = 0, num_groups = 0, R = 0, max_parents = 0, num_inputs = 0;
   int device = 0;
   std::vector<fold_op> ops;
-  // one device allocation holds every int array below
+  // one device allocation holds every int array below (the level and group tables included)
   void* blob = nullptr;
   int32_t *depth = nullptr, *node_pos = nullptr, *pos_node = nullptr, *level_ptr = nullptr;
   int32_t *g_level = nullptr, *g_op = nullptr, *g_row_begin = nullptr, *g_rows = nullptr,
@@ -104,7 +104,6 @@ struct Sched {
   int32_t *op_rows = nullptr;     // [N] pool rows sorted by (op, row)
   int32_t *op_cpos = nullptr;     // [2N] child pool rows of op_rows[q] at 2q + k (-1 past the arity)
   int32_t *op_inp = nullptr;      // [N] leaf-table row of op_rows[q], or -1
-  void* blob3 = nullptr;          // level / group table (device copy)
   std::vector<int32_t> h_level_ptr, h_level, h_op, h_row_begin, h_rows, h_idx_off;
   std::vector<int32_t> h_op_row_ptr;  // [num_ops + 1] ranges of op_rows
 };

@@ -9,8 +9,14 @@
 //   sort       stable LSD radix sort (8-bit digits) of the node ids by the key
 //              (depth - 1) * num_ops + op: ties stay in node-id order
 //   emit       group table, level_ptr, child_pos (pool rows of every edge),
-//              input_idx and root rows
-// All results are integers and bit-exact by construction.
+//              input_idx and root rows; the rows of every op in (op, row) order
+//              for the deferred weight gradients (one more stable radix pass,
+//              keyed by op)
+// All results are integers and bit-exact by construction.  Everything runs on
+// the stream without a host round trip until one read-back at the end: arrays
+// are sized by N (levels and groups never outnumber nodes), the radix passes
+// the actual depth needs are decided on the device, and every kernel after
+// validation returns at once when the error word is set.
 
 #include <hip/hip_runtime.h>
 
@@ -25,6 +31,8 @@ namespace fold {
 namespace {
 
 constexpr unsigned long long kNoErr = ~0ull;
+constexpr int kTooDeep = 0x7fffffff;  // error-word node of "depth * num_ops too large for the sort keys"
+constexpr long long kMaxKeys = 1LL << 30;
 constexpr int kBlock = 256;
 constexpr int kMaxOps = 256;  // the op table travels as a kernel argument (2 KB)
 constexpr int kDepthLdsInts = 8192;  // 32 KiB per workgroup; larger graphs use global scratch
@@ -286,15 +294,35 @@ void scan_exclusive(const int* in, int* out, int n, int* total, int* temp, hipSt
 // ---------------------------------------------------------------- stable LSD radix sort
 
 __global__ void k_make_keys(const int* depth, const int* node_op, int N, int num_ops, unsigned* keys,
-                            int* vals) {
+                            int* vals, const unsigned long long* err) {
+  if (*err != kNoErr) return;
   const int v = blockIdx.x * blockDim.x + threadIdx.x;
   if (v >= N) return;
   keys[v] = (unsigned)((depth[v] - 1) * num_ops + node_op[v]);
   vals[v] = v;
 }
 
-// counts[d * B + b] = number of items of tile b whose digit is d
-__global__ void k_radix_count(const unsigned* keys, int n, int shift, int* counts, int B) {
+// number of 8-bit radix passes the keys (depth - 1) * num_ops + op need, from the depth found on the
+// device: meta[0] = D, written to *passes (at least 1); a depth whose keys would pass kMaxKeys is an error
+__global__ void k_sort_plan(const int* meta, int num_ops, unsigned long long* err, int* passes) {
+  if (threadIdx.x != 0) return;
+  const long long nk = (long long)meta[0] * num_ops;
+  if (nk > kMaxKeys) {
+    report(err, kTooDeep, FOLD_E_INVALID);
+    *passes = 0;
+    return;
+  }
+  unsigned long long mx = nk > 0 ? (unsigned long long)(nk - 1) : 0ull;
+  int bits = 1;
+  while (bits < 32 && (mx >> bits)) ++bits;
+  *passes = (bits + 7) / 8;
+}
+
+// counts[d * B + b] = number of items of tile b whose digit is d.  Pass `pass` runs only below *passes
+// (passes == nullptr: always) and when no error is set.
+__global__ void k_radix_count(const unsigned* keys, int n, int shift, int* counts, int B, const unsigned long long* err,
+                              const int* passes, int pass) {
+  if (*err != kNoErr || (passes && pass >= *passes)) return;
   __shared__ int hist[256];
   const int b = blockIdx.x, t = threadIdx.x;
   hist[t] = 0;
@@ -310,13 +338,28 @@ __global__ void k_radix_count(const unsigned* keys, int n, int shift, int* count
 
 // Scatter in tile order.  Items of a round are ranked among equal digits by a wave-level match
 // (one ballot per digit bit) plus the counts of earlier waves; rounds go in item order, so the
-// scatter is stable.
+// scatter is stable.  A pass at or above *passes copies its tile unchanged (the keys are already
+// sorted), so the host can launch the most passes N * num_ops could need and the result still ends in
+// the output buffer of the last pass.
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(const unsigned* keys_in, const int* vals_in,
                                                           unsigned* keys_out, int* vals_out,
-                                                          const int* offsets, int n, int shift, int B) {
+                                                          const int* offsets, int n, int shift, int B,
+                                                          const unsigned long long* err, const int* passes,
+                                                          int pass) {
+  if (*err != kNoErr) return;
   __shared__ int base[256];
   __shared__ int wcnt[kBlock / kWave][256];
   const int b = blockIdx.x, t = threadIdx.x, lane = t & (kWave - 1), w = t / kWave;
+  if (passes && pass >= *passes) {
+    for (int r = 0; r < kRadixItems; ++r) {
+      const long long i = (long long)b * kRadixTile + (long long)r * kBlock + t;
+      if (i < n) {
+        keys_out[i] = keys_in[i];
+        vals_out[i] = vals_in[i];
+      }
+    }
+    return;
+  }
   base[t] = offsets[t * B + b];
   for (int i = 0; i < kBlock / kWave; ++i) wcnt[i][t] = 0;
   __syncthreads();
@@ -354,7 +397,8 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(const unsigned* keys_i
 // ---------------------------------------------------------------- emission
 
 __global__ void k_post_sort(const unsigned* keys, const int* vals, int N, int num_ops, int* pos_node,
-                            int* node_pos, int* flag, int* level_ptr) {
+                            int* node_pos, int* flag, int* level_ptr, const unsigned long long* err) {
+  if (*err != kNoErr) return;
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= N) return;
   const int v = vals[p];
@@ -369,7 +413,8 @@ __global__ void k_post_sort(const unsigned* keys, const int* vals, int N, int nu
 }
 
 __global__ void k_group_starts(const unsigned* keys, const int* flag, const int* exs, int N, int num_ops,
-                               int* gid, int* g_level, int* g_op, int* g_row_begin) {
+                               int* gid, int* g_level, int* g_op, int* g_row_begin, const unsigned long long* err) {
+  if (*err != kNoErr) return;
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= N) return;
   const int g = exs[p] + flag[p] - 1;
@@ -381,10 +426,11 @@ __global__ void k_group_starts(const unsigned* keys, const int* flag, const int*
   }
 }
 
-// ng = number of groups (device); rows and rows * arity of each group
+// ng = number of groups (device); rows and rows * arity of each group (g_edges has N entries)
 __global__ void k_group_rows(const int* ng_ptr, int N, const int* g_row_begin, const int* g_op, OpTable ops,
-                             int* g_rows, int* g_edges) {
+                             int* g_rows, int* g_edges, const unsigned long long* err) {
   const int g = blockIdx.x * blockDim.x + threadIdx.x;
+  if (*err != kNoErr || g >= N) return;
   const int ng = *ng_ptr;
   if (g >= ng) {
     g_edges[g] = 0;
@@ -399,7 +445,8 @@ __global__ void k_group_rows(const int* ng_ptr, int N, const int* g_row_begin, c
 __global__ void k_emit(const int* pos_node, const int* node_pos, const int* gid, const int* g_row_begin,
                        const int* g_op, const int* g_idx_off, const int* cp, const int* ci,
                        const int* node_input, const int* indeg, int N, OpTable ops, int* child_pos,
-                       int* child_one, int* input_idx, int* pos_npar) {
+                       int* child_one, int* input_idx, int* pos_npar, const unsigned long long* err) {
+  if (*err != kNoErr) return;
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= N) return;
   const int v = pos_node[p];
@@ -416,29 +463,73 @@ __global__ void k_emit(const int* pos_node, const int* node_pos, const int* gid,
   pos_npar[p] = indeg[v];
 }
 
-__global__ void k_root_flags(const int* indeg, int N, int* flag) {
+__global__ void k_root_flags(const int* indeg, int N, int* flag, const unsigned long long* err) {
+  if (*err != kNoErr) return;
   const int v = blockIdx.x * blockDim.x + threadIdx.x;
   if (v < N) flag[v] = indeg[v] == 0 ? 1 : 0;
 }
 
-__global__ void k_root_emit(const int* flag, const int* rank, const int* node_pos, int N, int* root_pos) {
+__global__ void k_root_emit(const int* flag, const int* rank, const int* node_pos, int N, int* root_pos,
+                            const unsigned long long* err) {
+  if (*err != kNoErr) return;
   const int v = blockIdx.x * blockDim.x + threadIdx.x;
   if (v < N && flag[v]) root_pos[rank[v]] = node_pos[v];
 }
 
-__global__ void k_op_rows(const int* pos_group, const int* g_row_begin, const int* g_oprow, const int* g_op,
-                          const int* g_idx_off, const int* child_pos, const int* input_idx, OpTable ops, int N,
-                          int* op_rows, int* op_cpos, int* op_inp) {
+// error word "none", meta zero
+__global__ void k_init_meta(void* em) {
+  if (threadIdx.x == 0) *static_cast<unsigned long long*>(em) = kNoErr;
+  int* meta = reinterpret_cast<int*>(static_cast<unsigned long long*>(em) + 1);
+  if (threadIdx.x < 8) meta[threadIdx.x] = 0;
+}
+
+// keys of the second sort: the op of every pool row, with the row as its value; a stable sort by op
+// lists every op's rows in (op, row) order
+__global__ void k_op_keys(const int* gid, const int* g_op, int N, unsigned* keys, int* vals,
+                          const unsigned long long* err) {
+  if (*err != kNoErr) return;
   const int p = blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= N) return;
-  const int g = pos_group[p];
+  keys[p] = (unsigned)g_op[gid[p]];
+  vals[p] = p;
+}
+
+// for entry q of the (op, row) list: the row's children and leaf-table row
+__global__ void k_op_rows(const int* op_rows, const int* gid, const int* g_row_begin, const int* g_op,
+                          const int* g_idx_off, const int* child_pos, const int* input_idx, OpTable ops, int N,
+                          int* op_cpos, int* op_inp, const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int q = blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= N) return;
+  const int p = op_rows[q];
+  const int g = gid[p];
   const int r = p - g_row_begin[g];
-  const int q = g_oprow[g] + r;
   const int a = ops.arity[g_op[g]];
-  op_rows[q] = p;
   op_cpos[2 * q] = a > 0 ? child_pos[g_idx_off[g] + r * a] : -1;
   op_cpos[2 * q + 1] = a > 1 ? child_pos[g_idx_off[g] + r * a + 1] : -1;
   op_inp[q] = input_idx[p];
+}
+
+// The one read-back of a schedule: the error word and meta, then the first lcap + 1 entries of level_ptr
+// and the first gcap groups of each group array, side by side.
+constexpr int kHdr = 16;
+struct GroupArrays {
+  const int* a[5];  // level, op, row_begin, rows, idx_off
+};
+__global__ void k_compact(const unsigned long long* err, const int* meta, const int* level_ptr, GroupArrays garr,
+                          int lcap, int gcap, int* out) {
+  const unsigned long long e = *err;
+  if (threadIdx.x == 0) {
+    out[0] = (int)(unsigned)(e & 0xffffffffull);
+    out[1] = (int)(unsigned)(e >> 32);
+    for (int i = 0; i < 8; ++i) out[2 + i] = meta[i];
+  }
+  if (e != kNoErr) return;
+  const int nl = min(meta[0] + 1, lcap + 1), ng = min(meta[4], gcap);
+  for (int i = threadIdx.x; i < nl; i += blockDim.x) out[kHdr + i] = level_ptr[i];
+  int* go = out + kHdr + lcap + 1;
+  for (int k = 0; k < 5; ++k)
+    for (int i = threadIdx.x; i < ng; i += blockDim.x) go[k * gcap + i] = garr.a[k][i];
 }
 
 inline dim3 grid_for(long long n) { return dim3((unsigned)std::max(1LL, (n + kBlock - 1) / kBlock)); }
@@ -475,6 +566,10 @@ struct Temp {
 int decode_error(unsigned long long w, std::string* msg) {
   const int code = -(int)(w & 0xffull);
   const long long node = (long long)(w >> 8) - 1;
+  if ((long long)(w >> 8) == kTooDeep) {
+    *msg = "fold_schedule: depth * num_ops exceeds 2^30 (the sort keys)";
+    return code;
+  }
   const char* what = "invalid batch";
   switch (code) {
     case FOLD_E_INVALID: what = "graph_ptr / child_ptr malformed"; break;
@@ -535,12 +630,14 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
     return code;
   };
 
-  // persistent arrays sized by N and E
-  const size_t n1 = (size_t)N * 11 + 2 * (size_t)E + 8;
+  // persistent arrays sized by N and E; the level and group tables take N + 1 and 5 x N entries (there are
+  // at most N levels and N groups), so nothing waits for the depth to be known on the host
+  const size_t n1 = (size_t)N * 17 + 2 * (size_t)E + 16;
   if (hipMalloc(&s.blob, n1 * sizeof(int)) != hipSuccess) {
     set_error("fold_schedule: out of device memory");
     return fail(FOLD_E_NOMEM);
   }
+  const size_t cap = std::max<size_t>(N, 1);
   int* q = static_cast<int*>(s.blob);
   s.depth = q; q += N;
   s.node_pos = q; q += N;
@@ -554,79 +651,38 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   s.op_rows = q; q += N;
   s.op_cpos = q; q += 2 * (size_t)N;
   s.op_inp = q; q += N;
+  s.level_ptr = q; q += cap + 1;
+  s.g_level = q; q += cap;
+  s.g_op = q; q += cap;
+  s.g_row_begin = q; q += cap;
+  s.g_rows = q; q += cap;
+  s.g_idx_off = q; q += cap;
 
+  // temporaries of the whole schedule, one pooled allocation
   Temp tmp(st);
-  // the error word and meta (max depth, max parents, num groups, num roots) side by side: one read-back
+  // err, then meta: [0] max depth, [1] max parents, [2] radix passes, [3] scratch total, [4] groups, [5] roots,
+  // [6] scratch total
   struct ErrMeta {
     unsigned long long err;
-    int meta[4];
+    int meta[8];
   };
   ErrMeta* em = nullptr;
-  int* node_graph = nullptr;
-  int* indeg = nullptr;
-  int* scratch = nullptr;
-  const long long scratch_ints = 6LL * N + G + E + 1;
-  tmp.reserve(&em, 1);
-  tmp.reserve(&node_graph, N);
-  tmp.reserve(&indeg, N);
-  tmp.reserve(&scratch, (size_t)scratch_ints);
-  if (tmp.commit() != hipSuccess) {
-    set_error("fold_schedule: out of device memory (temporaries)");
-    return fail(FOLD_E_NOMEM);
-  }
-  unsigned long long* err = &em->err;
-  int* meta = em->meta;
-  const ErrMeta em0{~0ull, {0, 0, 0, 0}};
-  if (hipMemcpyAsync(em, &em0, sizeof(em0), hipMemcpyHostToDevice, st) != hipSuccess) {
-    set_error("fold_schedule: could not initialise the error word");
-    return fail(FOLD_E_DEVICE);
-  }
-  hipLaunchKernelGGL(k_check_struct, grid_for(std::max(G + 1, N + 1)), dim3(kBlock), 0, st, b->graph_ptr, G,
-                     b->child_ptr, N, E, err);
-  if (G > 0)
-    hipLaunchKernelGGL(k_node_graph, dim3(G), dim3(kBlock), 0, st, b->graph_ptr, node_graph, err);
-  if (N > 0) {
-    hipLaunchKernelGGL(k_check_nodes, grid_for(N), dim3(kBlock), 0, st, b->node_op, b->child_ptr,
-                       b->child_idx, b->node_input, node_graph, N, b->num_inputs, ops, err);
-  }
-  if (G > 0)
-    hipLaunchKernelGGL(k_depth, dim3(G), dim3(kBlock), kDepthLdsInts * sizeof(int), st, b->graph_ptr,
-                       b->child_ptr, b->child_idx, s.depth, indeg, scratch, err, meta);
-  if (hipGetLastError() != hipSuccess) {
-    set_error("fold_schedule: kernel launch failed");
-    return fail(FOLD_E_DEVICE);
-  }
-  ErrMeta hb{};
-  if (hipMemcpyAsync(&hb, em, sizeof(hb), hipMemcpyDeviceToHost, st) != hipSuccess ||
-      hipStreamSynchronize(st) != hipSuccess) {
-    set_error("fold_schedule: device error while validating");
-    return fail(FOLD_E_DEVICE);
-  }
-  if (hb.err != kNoErr) {
-    std::string msg;
-    int code = decode_error(hb.err, &msg);
-    set_error(msg);
-    return fail(code);
-  }
-  const int D = (N > 0) ? hb.meta[0] : 0;
-  s.D = D;
-  s.max_parents = hb.meta[1];
-
-  // level / group table (sized by D), laid out contiguously for one read-back
-  const long long cap = std::max(1LL, (long long)D * K);
-  if (cap > (1LL << 30)) {
-    set_error("fold_schedule: depth * num_ops too large");
-    return fail(FOLD_E_INVALID);
-  }
-  const size_t n2 = 4 + (size_t)(D + 1) + 6 * (size_t)cap;
-  int* blob2 = nullptr;
+  int *node_graph = nullptr, *indeg = nullptr, *scratch = nullptr, *edges = nullptr, *stage = nullptr;
   unsigned *ka = nullptr, *kb = nullptr;
   int *va = nullptr, *vb = nullptr, *flag = nullptr, *exs = nullptr, *radix_counts = nullptr, *scan_tmp = nullptr;
+  const long long scratch_ints = 6LL * N + G + E + 1;
   const int B = (N + kRadixTile - 1) / kRadixTile;
-  const long long rc = 256LL * B;
-  const long long scan_tmp_n = std::max<long long>(std::max<long long>(rc, N), cap) / kScanTile + 2;
-  tmp.reserve(&blob2, n2);
+  const long long rc = 256LL * std::max(B, 1);
+  const long long scan_tmp_n = std::max<long long>(rc, N) / kScanTile + 2;
+  constexpr int kLcap = 4096, kGcap = 4096;  // levels and groups read back with the error word
+  const size_t stage_n = kHdr + (kLcap + 1) + 5 * (size_t)kGcap;
+  tmp.reserve(&em, 1);
+  tmp.reserve(&stage, stage_n);
   if (N > 0) {
+    tmp.reserve(&node_graph, N);
+    tmp.reserve(&indeg, N);
+    tmp.reserve(&scratch, (size_t)scratch_ints);
+    tmp.reserve(&edges, N);
     tmp.reserve(&ka, N);
     tmp.reserve(&kb, N);
     tmp.reserve(&va, N);
@@ -637,128 +693,127 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
     tmp.reserve(&scan_tmp, scan_tmp_n);
   }
   if (tmp.commit() != hipSuccess) {
-    set_error("fold_schedule: out of device memory");
+    set_error("fold_schedule: out of device memory (temporaries)");
     return fail(FOLD_E_NOMEM);
   }
-  int* m2 = blob2;  // [0] num groups, [1] num roots
-  int* d_level_ptr = m2 + 4;
-  int* d_level = d_level_ptr + (D + 1);
-  int* d_op = d_level + cap;
-  int* d_row_begin = d_op + cap;
-  int* d_rows = d_row_begin + cap;
-  int* d_idx_off = d_rows + cap;
-  int* d_edges = d_idx_off + cap;
-
+  unsigned long long* err = &em->err;
+  int* meta = em->meta;
+  hipLaunchKernelGGL(k_init_meta, dim3(1), dim3(64), 0, st, em);
+  hipLaunchKernelGGL(k_check_struct, grid_for(std::max(G + 1, N + 1)), dim3(kBlock), 0, st, b->graph_ptr, G,
+                     b->child_ptr, N, E, err);
   if (N > 0) {
-    int* gid = s.pos_group;
-    hipLaunchKernelGGL(k_make_keys, grid_for(N), dim3(kBlock), 0, st, s.depth, b->node_op, N, K, ka, va);
-    const unsigned long long max_key = (unsigned long long)D * K - 1;
+    if (G > 0)
+      hipLaunchKernelGGL(k_node_graph, dim3(G), dim3(kBlock), 0, st, b->graph_ptr, node_graph, err);
+    hipLaunchKernelGGL(k_check_nodes, grid_for(N), dim3(kBlock), 0, st, b->node_op, b->child_ptr,
+                       b->child_idx, b->node_input, node_graph, N, b->num_inputs, ops, err);
+    if (G > 0)
+      hipLaunchKernelGGL(k_depth, dim3(G), dim3(kBlock), kDepthLdsInts * sizeof(int), st, b->graph_ptr,
+                         b->child_ptr, b->child_idx, s.depth, indeg, scratch, err, meta);
+
+    // sort by (depth - 1) * num_ops + op: as many 8-bit passes as N * num_ops could need are launched; the
+    // ones the actual depth does not need copy their tile
+    hipLaunchKernelGGL(k_sort_plan, dim3(1), dim3(64), 0, st, meta, K, err, meta + 2);
+    hipLaunchKernelGGL(k_make_keys, grid_for(N), dim3(kBlock), 0, st, s.depth, b->node_op, N, K, ka, va, err);
+    const unsigned long long max_key = std::min<unsigned long long>((unsigned long long)N * K,
+                                                                    (unsigned long long)kMaxKeys) - 1;
     int bits = 1;
     while (bits < 32 && (max_key >> bits)) ++bits;
     const int passes = (bits + 7) / 8;
     for (int ps = 0; ps < passes; ++ps) {
       const int shift = 8 * ps;
-      hipLaunchKernelGGL(k_radix_count, dim3(B), dim3(kBlock), 0, st, ka, N, shift, radix_counts, B);
-      scan_exclusive(radix_counts, radix_counts, (int)rc, meta + 2, scan_tmp, st);
-      hipLaunchKernelGGL(k_radix_scatter, dim3(B), dim3(kBlock), 0, st, ka, va, kb, vb, radix_counts, N,
-                         shift, B);
+      hipLaunchKernelGGL(k_radix_count, dim3(B), dim3(kBlock), 0, st, ka, N, shift, radix_counts, B, err,
+                         meta + 2, ps);
+      scan_exclusive(radix_counts, radix_counts, (int)rc, meta + 3, scan_tmp, st);
+      hipLaunchKernelGGL(k_radix_scatter, dim3(B), dim3(kBlock), 0, st, ka, va, kb, vb, radix_counts, N, shift, B,
+                         err, meta + 2, ps);
       std::swap(ka, kb);
       std::swap(va, vb);
     }
+    int* gid = s.pos_group;
     hipLaunchKernelGGL(k_post_sort, grid_for(N), dim3(kBlock), 0, st, ka, va, N, K, s.pos_node, s.node_pos,
-                       flag, d_level_ptr);
-    scan_exclusive(flag, exs, N, m2 + 0, scan_tmp, st);
-    hipLaunchKernelGGL(k_group_starts, grid_for(N), dim3(kBlock), 0, st, ka, flag, exs, N, K, gid, d_level,
-                       d_op, d_row_begin);
-    hipLaunchKernelGGL(k_group_rows, grid_for(cap), dim3(kBlock), 0, st, m2 + 0, N, d_row_begin, d_op, ops,
-                       d_rows, d_edges);
-    // idx_off = exclusive scan of rows * arity over the groups (entries past num_groups are unused)
-    scan_exclusive(d_edges, d_idx_off, (int)cap, m2 + 2, scan_tmp, st);
-    hipLaunchKernelGGL(k_emit, grid_for(N), dim3(kBlock), 0, st, s.pos_node, s.node_pos, gid, d_row_begin,
-                       d_op, d_idx_off, b->child_ptr, b->child_idx, b->node_input, indeg, N, ops, s.child_pos,
-                       s.child_one, s.input_idx, s.pos_npar);
-    hipLaunchKernelGGL(k_root_flags, grid_for(N), dim3(kBlock), 0, st, indeg, N, flag);
-    scan_exclusive(flag, exs, N, m2 + 1, scan_tmp, st);
-    hipLaunchKernelGGL(k_root_emit, grid_for(N), dim3(kBlock), 0, st, flag, exs, s.node_pos, N, s.root_pos);
-    if (hipGetLastError() != hipSuccess) {
-      set_error("fold_schedule: kernel launch failed");
-      return fail(FOLD_E_DEVICE);
-    }
-  }
-  std::vector<int> hbuf(n2, 0);
-  if (N > 0) {
-    if (hipMemcpyAsync(hbuf.data(), blob2, n2 * sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
-        hipStreamSynchronize(st) != hipSuccess) {
-      set_error("fold_schedule: device error while scheduling");
-      return fail(FOLD_E_DEVICE);
-    }
-  }
-  const int ng = N > 0 ? hbuf[0] : 0;
-  s.num_groups = ng;
-  s.R = N > 0 ? hbuf[1] : 0;
-  const int* hl = hbuf.data() + 4;
-  s.h_level_ptr.assign(hl, hl + D + 1);
-  const int* hg = hl + (D + 1);
-  s.h_level.assign(hg, hg + ng);
-  s.h_op.assign(hg + cap, hg + cap + ng);
-  s.h_row_begin.assign(hg + 2 * cap, hg + 2 * cap + ng);
-  s.h_rows.assign(hg + 3 * cap, hg + 3 * cap + ng);
-  s.h_idx_off.assign(hg + 4 * cap, hg + 4 * cap + ng);
-  if (N == 0) s.h_level_ptr.assign(1, 0);
+                       flag, s.level_ptr, err);
+    scan_exclusive(flag, exs, N, meta + 4, scan_tmp, st);
+    hipLaunchKernelGGL(k_group_starts, grid_for(N), dim3(kBlock), 0, st, ka, flag, exs, N, K, gid, s.g_level,
+                       s.g_op, s.g_row_begin, err);
+    hipLaunchKernelGGL(k_group_rows, grid_for(N), dim3(kBlock), 0, st, meta + 4, N, s.g_row_begin, s.g_op, ops,
+                       s.g_rows, edges, err);
+    // idx_off = exclusive scan of rows * arity over the groups (entries past the group count are unused)
+    scan_exclusive(edges, s.g_idx_off, N, meta + 6, scan_tmp, st);
+    hipLaunchKernelGGL(k_emit, grid_for(N), dim3(kBlock), 0, st, s.pos_node, s.node_pos, gid, s.g_row_begin,
+                       s.g_op, s.g_idx_off, b->child_ptr, b->child_idx, b->node_input, indeg, N, ops, s.child_pos,
+                       s.child_one, s.input_idx, s.pos_npar, err);
+    hipLaunchKernelGGL(k_root_flags, grid_for(N), dim3(kBlock), 0, st, indeg, N, flag, err);
+    scan_exclusive(flag, exs, N, meta + 5, scan_tmp, st);
+    hipLaunchKernelGGL(k_root_emit, grid_for(N), dim3(kBlock), 0, st, flag, exs, s.node_pos, N, s.root_pos, err);
 
-  // rows of every op in (op, row) order: per-group offsets into op_rows
-  const int ngc = std::max(ng, 1);
-  std::vector<int> oprow_off(ngc, 0);
+    // rows of every op in (op, row) order: one stable pass keyed by op (at most 256 ops: one digit)
+    hipLaunchKernelGGL(k_op_keys, grid_for(N), dim3(kBlock), 0, st, gid, s.g_op, N, kb, vb, err);
+    hipLaunchKernelGGL(k_radix_count, dim3(B), dim3(kBlock), 0, st, kb, N, 0, radix_counts, B, err,
+                       (const int*)nullptr, 0);
+    scan_exclusive(radix_counts, radix_counts, (int)rc, meta + 3, scan_tmp, st);
+    hipLaunchKernelGGL(k_radix_scatter, dim3(B), dim3(kBlock), 0, st, kb, vb, ka, s.op_rows, radix_counts, N, 0, B,
+                       err, (const int*)nullptr, 0);
+    hipLaunchKernelGGL(k_op_rows, grid_for(N), dim3(kBlock), 0, st, s.op_rows, gid, s.g_row_begin, s.g_op,
+                       s.g_idx_off, s.child_pos, s.input_idx, ops, N, s.op_cpos, s.op_inp, err);
+  }
+  GroupArrays ga{{s.g_level, s.g_op, s.g_row_begin, s.g_rows, s.g_idx_off}};
+  hipLaunchKernelGGL(k_compact, dim3(1), dim3(kBlock), 0, st, err, meta, s.level_ptr, ga, kLcap, kGcap, stage);
+  if (hipGetLastError() != hipSuccess) {
+    set_error("fold_schedule: kernel launch failed");
+    return fail(FOLD_E_DEVICE);
+  }
+  // the one synchronisation: error word, meta, and the level / group tables up to kLcap / kGcap entries
+  std::vector<int> hb(stage_n, 0);
+  if (hipMemcpyAsync(hb.data(), stage, stage_n * sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess) {
+    set_error("fold_schedule: device error while scheduling");
+    return fail(FOLD_E_DEVICE);
+  }
+  const unsigned long long ew = (unsigned long long)(unsigned)hb[0] | ((unsigned long long)(unsigned)hb[1] << 32);
+  if (ew != kNoErr) {
+    std::string msg;
+    int code = decode_error(ew, &msg);
+    set_error(msg);
+    return fail(code);
+  }
+  const int* hm = hb.data() + 2;
+  const int D = N > 0 ? hm[0] : 0;
+  const int ng = N > 0 ? hm[4] : 0;
+  s.D = D;
+  s.max_parents = N > 0 ? hm[1] : 0;
+  s.num_groups = ng;
+  s.R = N > 0 ? hm[5] : 0;
+  if (N == 0) {
+    s.h_level_ptr.assign(1, 0);
+  } else if (D + 1 <= kLcap + 1 && ng <= kGcap) {
+    const int* hl = hb.data() + kHdr;
+    s.h_level_ptr.assign(hl, hl + D + 1);
+    const int* hg = hl + kLcap + 1;
+    s.h_level.assign(hg, hg + ng);
+    s.h_op.assign(hg + kGcap, hg + kGcap + ng);
+    s.h_row_begin.assign(hg + 2 * kGcap, hg + 2 * kGcap + ng);
+    s.h_rows.assign(hg + 3 * kGcap, hg + 3 * kGcap + ng);
+    s.h_idx_off.assign(hg + 4 * kGcap, hg + 4 * kGcap + ng);
+  } else {
+    // more levels or groups than the first read-back holds: read the whole tables (a second synchronisation)
+    s.h_level_ptr.resize(D + 1);
+    std::vector<int>* dst[5] = {&s.h_level, &s.h_op, &s.h_row_begin, &s.h_rows, &s.h_idx_off};
+    bool ok = hipMemcpyAsync(s.h_level_ptr.data(), s.level_ptr, (size_t)(D + 1) * sizeof(int),
+                             hipMemcpyDeviceToHost, st) == hipSuccess;
+    for (int k = 0; k < 5; ++k) {
+      dst[k]->resize(ng);
+      ok = ok && hipMemcpyAsync(dst[k]->data(), ga.a[k], (size_t)ng * sizeof(int), hipMemcpyDeviceToHost, st) ==
+                     hipSuccess;
+    }
+    if (!ok || hipStreamSynchronize(st) != hipSuccess) {
+      set_error("fold_schedule: device error while reading the group table");
+      return fail(FOLD_E_DEVICE);
+    }
+  }
+  // ranges of op_rows per op
   s.h_op_row_ptr.assign(K + 1, 0);
   for (int g = 0; g < ng; ++g) s.h_op_row_ptr[s.h_op[g] + 1] += s.h_rows[g];
   for (int o = 0; o < K; ++o) s.h_op_row_ptr[o + 1] += s.h_op_row_ptr[o];
-  {
-    std::vector<int> fillp(s.h_op_row_ptr.begin(), s.h_op_row_ptr.end() - 1);
-    for (int g = 0; g < ng; ++g) {
-      oprow_off[g] = fillp[s.h_op[g]];
-      fillp[s.h_op[g]] += s.h_rows[g];
-    }
-  }
-
-  // compact device copy of the level / group table owned by the schedule
-  const size_t n3 = (size_t)(D + 1) + 6 * (size_t)ngc;
-  void* blob3 = nullptr;
-  if (hipMalloc(&blob3, n3 * sizeof(int)) != hipSuccess) {
-    set_error("fold_schedule: out of device memory");
-    return fail(FOLD_E_NOMEM);
-  }
-  s.blob3 = blob3;
-  std::vector<int> pack(n3, 0);
-  std::copy(s.h_level_ptr.begin(), s.h_level_ptr.end(), pack.begin());
-  int* pp = pack.data() + (D + 1);
-  std::copy(s.h_level.begin(), s.h_level.end(), pp);
-  std::copy(s.h_op.begin(), s.h_op.end(), pp + ngc);
-  std::copy(s.h_row_begin.begin(), s.h_row_begin.end(), pp + 2 * ngc);
-  std::copy(s.h_rows.begin(), s.h_rows.end(), pp + 3 * ngc);
-  std::copy(s.h_idx_off.begin(), s.h_idx_off.end(), pp + 4 * ngc);
-  std::copy(oprow_off.begin(), oprow_off.end(), pp + 5 * ngc);
-  // stream-ordered upload (a pageable source is staged before the call returns); the final
-  // synchronisation below covers it
-  if (hipMemcpyAsync(blob3, pack.data(), n3 * sizeof(int), hipMemcpyHostToDevice, st) != hipSuccess) {
-    set_error("fold_schedule: copy of the group table failed");
-    return fail(FOLD_E_DEVICE);
-  }
-  int* b3 = static_cast<int*>(blob3);
-  s.level_ptr = b3;
-  s.g_level = b3 + (D + 1);
-  s.g_op = s.g_level + ngc;
-  s.g_row_begin = s.g_op + ngc;
-  s.g_rows = s.g_row_begin + ngc;
-  s.g_idx_off = s.g_rows + ngc;
-  const int* g_oprow = s.g_idx_off + ngc;
-  if (N > 0) {
-    hipLaunchKernelGGL(k_op_rows, grid_for(N), dim3(kBlock), 0, st, s.pos_group, s.g_row_begin, g_oprow, s.g_op,
-                       s.g_idx_off, s.child_pos, s.input_idx, ops, N, s.op_rows, s.op_cpos, s.op_inp);
-  }
-  if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess) {
-    set_error("fold_schedule: device error while listing rows per op");
-    return fail(FOLD_E_DEVICE);
-  }
   *out = h;
   return FOLD_OK;
 }
@@ -766,7 +821,6 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
 void sched_destroy_impl(fold_sched* h) {
   if (!h) return;
   if (h->s.blob) (void)hipFree(h->s.blob);
-  if (h->s.blob3) (void)hipFree(h->s.blob3);
   delete h;
 }
 

@@ -56,6 +56,19 @@ def test_large_graph_uses_global_scratch():
     C.assert_schedule_equal(_gpu_sched(w), C.oracle_schedule(w))
 
 
+def test_more_levels_than_the_first_read_back():
+    """A 5,000-step caterpillar: 5,001 levels and groups, more than fold_schedule reads back with its error
+    word (4,096), so it reads the rest of the level and group tables in a second copy."""
+    b = gen._GraphBuilder()
+    gen.caterpillar(b, 5000, 0, 1, range(5001))
+    csr = gen.assemble([b.arrays()])
+    w = gen.Workload("deep", "f32", 2, ops=[gen.OpSpec(2, 0, 1, 0), gen.OpSpec(2, 2, 0, 0)], params=[],
+                     leaf_table=np.zeros((5001, 2), np.float32), dh_roots=np.zeros((1, 2), np.float32), **csr)
+    ref = C.oracle_schedule(w)
+    assert ref["num_levels"] == 5001 and len(ref["group_op"]) > 4096
+    C.assert_schedule_equal(_gpu_sched(w), ref)
+
+
 @pytest.mark.parametrize("k", [1, 2, 3, 4, 5])
 def test_full_config_schedules(k):
     """All five workloads at full size, config 5's 2.0 M-node batch of 4,096 DAGs included."""
