@@ -253,6 +253,27 @@ int32_t fold_backward(const fold_sched* sched, const fold_packed* packed,
                       const fold_grads* grads, float* dh_out, float* dc_out,
                       void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* fold_forward_noalloc: fold_forward for callers that cannot allocate --
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  It computes the same states as fold_forward (inference: no
+ * activations are saved for a backward pass) and takes no workspace: the
+ * K-split partial sums of narrow levels go to a library-owned 16 MiB device
+ * array per GPU (a static __device__ array, held until the process ends).
+ * A level whose K split would need more than that splits into fewer slices,
+ * or none, so no batch is rejected for its size; results stay within the
+ * tolerance of fold_forward's (slices may differ, so not always bit-equal).
+ * Arguments, errors and asynchrony are those of fold_forward without ws;
+ * FOLD_E_MISMATCH if the handles belong to another device than the current
+ * one, FOLD_E_DEVICE if the array's address cannot be looked up.  It calls
+ * no hipMalloc, hipFree or allocating routine.  Every call on one GPU shares
+ * that GPU's array, so calls that overlap on one GPU (two streams, two host
+ * threads) race: serialise them.  No contents carry over between calls that
+ * matter (every slice writes its partial sums before they are read). */
+int32_t fold_forward_noalloc(const fold_sched* sched, const fold_packed* packed,
+                             const void* leaf_table, int64_t leaf_rows,
+                             void* h_pool, float* c_pool, void* roots_out,
+                             hipStream_t stream);
+
 /* Recurrent dropout (Section 3.5 trains the Tree-LSTM with the recurrent
  * dropout of Semeniuta et al., "Recurrent dropout without memory loss"):
  * the forward and backward passes above with a mask on the candidate update

@@ -335,12 +335,15 @@ struct TagScope {
 };
 
 int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, void* h_pool,
-                     float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st, const float* u_mask) {
+                     float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st, const float* u_mask,
+                     float* zpart_direct, size_t zcap) {
   const WsLayout L = workspace_layout(s, p);
   TagScope tags;
   float* gates = nullptr;
   float* zpart = nullptr;
-  if (ws) {
+  if (zpart_direct) {
+    zpart = zpart_direct;
+  } else if (ws) {
     if (ws_bytes < L.fwd_bytes) return fail(FOLD_E_MISMATCH, "fold_forward: workspace too small");
     gates = reinterpret_cast<float*>(static_cast<char*>(ws) + L.gates_off);
     zpart = reinterpret_cast<float*>(static_cast<char*>(ws) + L.zpart_off);
@@ -380,6 +383,7 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
     a.u_mask = u_mask;
     a.zero = p.zero;
     a.zpart = zpart;
+    a.zcap = zpart_direct ? zcap : 0;
     int kind = op.kind;
     if (is_tree_lstm_leaf(op)) {  // live gates only, input segment only
       kind = kTreeLstmLeaf;
@@ -534,6 +538,37 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
   (void)table_rows;
   if (hipGetLastError() != hipSuccess) return fail(FOLD_E_DEVICE, "fold_backward: kernel launch failed");
   return FOLD_OK;
+}
+
+// ---------------------------------------------------------------- allocation-free inference
+// fold_forward_noalloc keeps the K-split partial sums of narrow levels in this array instead of a caller
+// workspace.  Host code never uses its name as an address (on the host it is only a stand-in symbol): the
+// device address of each GPU's copy is looked up once per device with hipGetSymbolAddress and kept.
+constexpr size_t kScratchBytes = size_t(16) << 20;  // 16 MiB per GPU, held until the process ends
+static __device__ __align__(256) float scratch[kScratchBytes / sizeof(float)];
+
+namespace {
+std::mutex g_scratch_mu;
+std::map<int, float*> g_scratch_ptr;  // device ordinal -> device address of that device's scratch
+}  // namespace
+
+// the current device's scratch address (looked up on its first use), or nullptr with the error set
+float* scratch_address() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    set_error("fold_forward_noalloc: no current device");
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  auto it = g_scratch_ptr.find(dev);
+  if (it != g_scratch_ptr.end()) return it->second;
+  float* ptr = nullptr;
+  if (hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+    set_error("fold_forward_noalloc: hipGetSymbolAddress of the scratch array failed");
+    return nullptr;
+  }
+  g_scratch_ptr[dev] = ptr;
+  return ptr;
 }
 
 }  // namespace fold
@@ -896,6 +931,27 @@ int32_t fold_forward(const fold_sched* sh, const fold_packed* ph, const void* ta
   int rc = check_forward_args(s, p, table, table_rows, h_pool, c_pool, "fold_forward");
   if (rc != FOLD_OK) return rc;
   return forward_impl(s, p, table, table_rows, h_pool, c_pool, roots_out, ws, ws_bytes, st);
+  FOLD_GUARD_END
+}
+
+int32_t fold_forward_noalloc(const fold_sched* sh, const fold_packed* ph, const void* table, int64_t table_rows,
+                             void* h_pool, float* c_pool, void* roots_out, hipStream_t st) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!sh || !ph) return fail(FOLD_E_INVALID, "fold_forward_noalloc: NULL handle");
+  const Sched& s = sh->s;
+  const Packed& p = ph->p;
+  int rc = check_forward_args(s, p, table, table_rows, h_pool, c_pool, "fold_forward_noalloc");
+  if (rc != FOLD_OK) return rc;
+  int dev = 0;
+  FOLD_HIP_CHECK(hipGetDevice(&dev));
+  if (dev != s.device || dev != p.device)
+    return fail(FOLD_E_MISMATCH, "fold_forward_noalloc: the schedule and parameters belong to another device "
+                                 "than the current one");
+  float* zp = scratch_address();
+  if (!zp) return FOLD_E_DEVICE;
+  return forward_impl(s, p, table, table_rows, h_pool, c_pool, roots_out, nullptr, 0, st, nullptr, zp,
+                      kScratchBytes / sizeof(float));
   FOLD_GUARD_END
 }
 

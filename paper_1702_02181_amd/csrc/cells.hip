@@ -850,12 +850,17 @@ void cell_fwd_kind(const FwdArgs& a0, hipStream_t st) {
   }
   a.ksplit = pl.ksplit;
   const int G = Gates<KIND>::G;
+  if (a.ksplit > 1 && a.zcap > 0) {  // partial sums capped: as many slices as fit (none if fewer than two)
+    const size_t fit = a.zcap / ((size_t)a.rows * G * a.HP);
+    a.ksplit = (int)std::min<size_t>((size_t)a.ksplit, fit);
+    if (a.ksplit < 2) a.ksplit = 1;
+  }
   const int R = (int)cdiv(a.rows, 128), UB = a.HP / 32;  // 128-row tiles of one unit block
   a.map = a.rows >= G * a.HP ? kMapRows : kMapCols;  // gathered rows outweigh the weights: share row tiles
-  dim3 grid(a.map == kMapRows ? xcd_grid(UB * pl.ksplit, R) : xcd_grid(R * pl.ksplit, UB));
-  if (pl.ksplit > 1) {
+  dim3 grid(a.map == kMapRows ? xcd_grid(UB * a.ksplit, R) : xcd_grid(R * a.ksplit, UB));
+  if (a.ksplit > 1) {
     hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, true>), grid, dim3(kThreads), 0, st, a);
-    hipLaunchKernelGGL((k_cell_epi<T, KIND>), dim3(a.rows), dim3(std::min(a.HP, 1024)), 0, st, a, pl.ksplit);
+    hipLaunchKernelGGL((k_cell_epi<T, KIND>), dim3(a.rows), dim3(std::min(a.HP, 1024)), 0, st, a, a.ksplit);
   } else {
     hipLaunchKernelGGL((k_cell_fwd<T, KIND, 1, false>), grid, dim3(kThreads), 0, st, a);
   }

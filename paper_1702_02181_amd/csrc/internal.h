@@ -41,8 +41,11 @@ int leaf_table_width(const Sched& s, const Packed& p);
 // While set on this thread, kernel launchers record no profiling events (stream capture in progress).
 void set_capturing(bool on);
 
+// zpart_direct: K-split partial sums go there (at most zcap floats) and nothing is saved for the backward;
+// ws is then ignored
 int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, void* h_pool,
-                     float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st, const float* u_mask = nullptr);
+                     float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st,
+                     const float* u_mask = nullptr, float* zpart_direct = nullptr, size_t zcap = 0);
 int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows,
                       const void* h_pool, const float* c_pool, const float* dh_roots, const float* dh_nodes,
                       const fold_grads* grads, float* dh_out, float* dc_out, void* ws, size_t ws_bytes,
@@ -65,6 +68,8 @@ struct FwdArgs {
   int gstride;
   const void* zero;  // a zero row at least as wide as any K the kernels read (16-byte aligned)
   float* zpart;  // workspace for K-split partial sums, or NULL (no split)
+  size_t zcap = 0;  // floats zpart holds (0: as many as the plan needs); a level whose split needs more
+                    // splits into fewer slices
   int ksplit;    // set by the launcher
   int map;         // set by the launcher: workgroup order over the XCDs (kMapRows, kMapCols, kMapOwnCols)
   const float* u_mask = nullptr;  // recurrent dropout: [N, ld] fp32 multiplier of u in pool order, or NULL

@@ -110,7 +110,7 @@ EXPORTS = ["fold_schedule", "fold_sched_get_info", "fold_sched_free", "fold_pack
            "fold_probe_mfma", "fold_probe_copy", "fold_graph_create", "fold_graph_launch",
            "fold_graph_num_nodes", "fold_graph_free", "fold_pack_update", "fold_loss_softmax_ce",
            "fold_loss_workspace_size", "fold_adam_step", "fold_forward_dropout", "fold_backward_dropout",
-           "fold_dropout_mask"]
+           "fold_dropout_mask", "fold_forward_noalloc"]
 
 _lib = None
 
@@ -153,6 +153,8 @@ def lib():
     L.fold_backward_dropout.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,
                                         c_void_p, c_void_p, POINTER(fold_grads), c_void_p, c_void_p, c_void_p,
                                         c_size_t, c_void_p]
+    L.fold_forward_noalloc.restype = c_int32
+    L.fold_forward_noalloc.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p, c_void_p]
     L.fold_dropout_mask.restype = c_int32
     L.fold_dropout_mask.argtypes = [c_void_p, c_int32, ctypes.c_double, ctypes.c_uint64, ctypes.c_uint64, c_void_p,
                                     c_void_p]
@@ -293,6 +295,11 @@ def fold_loss_softmax_ce(sched, packed, h_pool, labels, num_classes, W_cls, b_cl
 def fold_adam_step(n, param, param_bf16, grad, m, v, lr, beta1, beta2, eps, step, stream=None):
     _check(lib().fold_adam_step(int(n), _ptr(param), _ptr(param_bf16), _ptr(grad), _ptr(m), _ptr(v), float(lr),
                                 float(beta1), float(beta2), float(eps), int(step), _stream(stream)))
+
+
+def fold_forward_noalloc(sched, packed, table, table_rows, h_pool, c_pool, roots, stream=None):
+    _check(lib().fold_forward_noalloc(sched, packed, _ptr(table), int(table_rows), _ptr(h_pool), _ptr(c_pool),
+                                      _ptr(roots), _stream(stream)))
 
 
 def fold_dropout_mask(sched, hidden, p, seed, step, mask, stream=None):
