@@ -335,8 +335,10 @@ TABLE1_BATCHES = (1, 32, 64, 128, 256, 512, 1024)
 def table1(batches, steps: int, warmup: int, dtype: str = "f32") -> dict:
     """The inference timing protocol of Section 2.1 (Table 1) on this GPU: batches of 127-node random trees
     (H = 1024, embedding-lookup leaves), forward only, timed as HIP-graph replays.  "manual" runs one batched
-    group per tree node (one operation per node position), "dynamic" one group per (depth, op) over trees of
-    one shape, "full" the same over trees of random shapes.  cost ratio = dynamic / manual time per batch;
+    group per tree node (one operation per node position) whose children are the consecutive rows of the child
+    position's group, addressed as base + row with no gather index (the static graph's layout), "dynamic" one
+    group per (depth, op) over trees of one shape, gathering children by index, "full" the same over trees of
+    random shapes.  cost ratio = dynamic / manual time per batch;
     speedup ratio = manual time per tree at batch size 1 / full-dynamic time per tree."""
     import torch
 
@@ -364,8 +366,12 @@ def table1(batches, steps: int, warmup: int, dtype: str = "f32") -> dict:
             dev = DeviceRun(w)
             graph = dev.make_graph(backward=False)
             ms = timed(graph.launch)
+            host = dev.sched.host_groups()
+            slots = [(host[f"group_child_base{k}"][g] >= 0)
+                     for g, op in enumerate(host["group_op"]) for k in range(w.ops[int(op)].arity)]
             row[mode] = {"batch_ms": round(ms, 4), "tree_ms": round(ms / B, 5),
-                         "groups": len(dev.sched.host_groups()["group_op"]), "kernels": graph.num_nodes}
+                         "groups": len(host["group_op"]), "kernels": graph.num_nodes,
+                         "gather_free_child_slots": f"{sum(slots)}/{len(slots)}"}
             del graph, dev
         row["cost_ratio"] = round(row["dynamic"]["batch_ms"] / row["manual"]["batch_ms"], 3)
         rows.append(row)

@@ -137,6 +137,17 @@ typedef struct {
   const int32_t* h_group_row_begin;
   const int32_t* h_group_rows;
   const int32_t* h_group_idx_off;
+  /* Static-graph layout, per group and child slot k = 0, 1: the pool row of the
+   * slot's first child when the slot's children are the consecutive rows
+   * base .. base + rows - 1 and each has exactly one parent edge (a batch of
+   * identically shaped graphs with one operation per node position, i.e.
+   * manual batching, has it on every slot); -1 otherwise.  The forward
+   * kernels address such children as base + row, with no child_pos load.
+   * Device [num_groups] each, and host copies. */
+  const int32_t* group_child_base0;
+  const int32_t* group_child_base1;
+  const int32_t* h_group_child_base0;
+  const int32_t* h_group_child_base1;
 } fold_sched_info;
 
 /* Schedule a batch (Section 2, the greedy scheduling algorithm):

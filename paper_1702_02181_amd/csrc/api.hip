@@ -384,6 +384,8 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
     a.zero = p.zero;
     a.zpart = zpart;
     a.zcap = zpart_direct ? zcap : 0;
+    a.cbase[0] = op.arity > 0 ? s.h_cbase0[g] : -1;
+    a.cbase[1] = op.arity > 1 ? s.h_cbase1[g] : -1;
     int kind = op.kind;
     if (is_tree_lstm_leaf(op)) {  // live gates only, input segment only
       kind = kTreeLstmLeaf;
@@ -737,6 +739,10 @@ int32_t fold_sched_get_info(const fold_sched* h, fold_sched_info* o) {
   o->child_pos = s.child_pos;
   o->input_idx = s.input_idx;
   o->root_pos = s.root_pos;
+  o->group_child_base0 = s.g_cbase0;
+  o->group_child_base1 = s.g_cbase1;
+  o->h_group_child_base0 = s.h_cbase0.data();
+  o->h_group_child_base1 = s.h_cbase1.data();
   o->h_level_ptr = s.h_level_ptr.data();
   o->h_group_level = s.h_level.data();
   o->h_group_op = s.h_op.data();

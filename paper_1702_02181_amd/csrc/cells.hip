@@ -215,7 +215,7 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
     for (int r = tid; r < BM; r += kThreads) {
       const int row = m0 + r;
       int sr = -1;
-      if (row < a.rows) sr = is_in ? a.input_idx[a.row_begin + row] : a.child_pos[a.idx_off + row * a.arity + k];
+      if (row < a.rows) sr = is_in ? a.input_idx[a.row_begin + row] : fwd_child(a, row, k);
       srow[seg][r] = sr;
     }
   }
@@ -372,7 +372,7 @@ __global__ __launch_bounds__(wide::kThreads) void k_cell_fwd_w(FwdArgs a) {
     const bool is_in = a.has_input && seg == 0;
     int sr = -1;
     if (row < a.rows)
-      sr = is_in ? a.input_idx[a.row_begin + row] : a.child_pos[a.idx_off + row * a.arity + (seg - a.has_input)];
+      sr = is_in ? a.input_idx[a.row_begin + row] : fwd_child(a, row, seg - a.has_input);
     srow[seg][r] = sr;
   }
   __syncthreads();
@@ -442,8 +442,8 @@ __global__ void k_cell_epi(FwdArgs a, int nsplit) {
   constexpr int G = Gates<KIND>::G;
   const int row = blockIdx.x;
   const int zs = G * a.HP;
-  const int p0 = a.arity >= 1 ? a.child_pos[a.idx_off + row * a.arity] : -1;
-  const int p1 = a.arity >= 2 ? a.child_pos[a.idx_off + row * a.arity + 1] : -1;
+  const int p0 = a.arity >= 1 ? fwd_child(a, row, 0) : -1;
+  const int p1 = a.arity >= 2 ? fwd_child(a, row, 1) : -1;
   const float* zf = static_cast<const float*>(a.zero);
   const float* c0r = p0 >= 0 ? a.c_pool + (size_t)p0 * a.ld : zf;
   const float* c1r = p1 >= 0 ? a.c_pool + (size_t)p1 * a.ld : zf;

@@ -104,7 +104,10 @@ struct Sched {
   int32_t *op_rows = nullptr;     // [N] pool rows sorted by (op, row)
   int32_t *op_cpos = nullptr;     // [2N] child pool rows of op_rows[q] at 2q + k (-1 past the arity)
   int32_t *op_inp = nullptr;      // [N] leaf-table row of op_rows[q], or -1
-  std::vector<int32_t> h_level_ptr, h_level, h_op, h_row_begin, h_rows, h_idx_off;
+  // [num_groups] per child slot k: first pool row of the slot's children when they are the consecutive
+  // rows base .. base + rows - 1, each with one parent edge (a static-graph layout), else -1
+  int32_t *g_cbase0 = nullptr, *g_cbase1 = nullptr;
+  std::vector<int32_t> h_level_ptr, h_level, h_op, h_row_begin, h_rows, h_idx_off, h_cbase0, h_cbase1;
   std::vector<int32_t> h_op_row_ptr;  // [num_ops + 1] ranges of op_rows
 };
 

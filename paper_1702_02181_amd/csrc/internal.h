@@ -73,7 +73,12 @@ struct FwdArgs {
   int ksplit;    // set by the launcher
   int map;         // set by the launcher: workgroup order over the XCDs (kMapRows, kMapCols, kMapOwnCols)
   const float* u_mask = nullptr;  // recurrent dropout: [N, ld] fp32 multiplier of u in pool order, or NULL
+  int cbase[2] = {-1, -1};  // child slot k's rows are cbase[k] + row (static-graph layout), or -1: child_pos
 };
+// pool row of child slot k of group row `row` (-1: the zero state)
+__device__ __forceinline__ int fwd_child(const FwdArgs& a, int row, int k) {
+  return a.cbase[k] >= 0 ? a.cbase[k] + row : a.child_pos[a.idx_off + row * a.arity + k];
+}
 void launch_cell_fwd(int dtype, int kind, const FwdArgs& a, hipStream_t st);
 
 // Tiling of one forward group.  Wide groups (at least one workgroup per compute unit) use the wide

@@ -510,11 +510,45 @@ __global__ void k_op_rows(const int* op_rows, const int* gid, const int* g_row_b
   op_inp[q] = input_idx[p];
 }
 
+// Static-graph layout of a group's child slot k: its children are the consecutive pool rows base .. base +
+// rows - 1 and each has exactly one parent edge.  A batch of identically shaped graphs with one operation per
+// node position (manual batching) has it on every slot; the kernels then address those children by
+// base + row instead of loading child_pos.  First every group proposes its first child as the base ...
+__global__ void k_cbase_init(const int* ng_ptr, int N, const int* g_op, const int* g_idx_off, const int* child_pos,
+                             const int* child_one, OpTable ops, int* cb0, int* cb1, const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int g = blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= N || g >= *ng_ptr) return;
+  const int a = ops.arity[g_op[g]], off = g_idx_off[g];
+  int b[2] = {-1, -1};
+  for (int k = 0; k < a && k < 2; ++k) b[k] = child_one[off + k] ? child_pos[off + k] : -1;
+  cb0[g] = b[0];
+  cb1[g] = b[1];
+}
+
+// ... then every row withdraws it (-1) where its child is not base + r or has another parent edge
+__global__ void k_cbase_check(int N, const int* gid, const int* g_row_begin, const int* g_op, const int* g_idx_off,
+                              const int* child_pos, const int* child_one, OpTable ops, int* cb0, int* cb1,
+                              const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= N) return;
+  const int g = gid[p], r = p - g_row_begin[g], a = ops.arity[g_op[g]];
+  for (int k = 0; k < a && k < 2; ++k) {
+    int* cb = k == 0 ? cb0 : cb1;
+    const int base = cb[g];
+    if (base < 0) continue;
+    const int e = g_idx_off[g] + r * a + k;
+    if (child_pos[e] != base + r || !child_one[e]) cb[g] = -1;
+  }
+}
+
 // The one read-back of a schedule: the error word and meta, then the first lcap + 1 entries of level_ptr
 // and the first gcap groups of each group array, side by side.
 constexpr int kHdr = 16;
+constexpr int kGroupArrays = 7;
 struct GroupArrays {
-  const int* a[5];  // level, op, row_begin, rows, idx_off
+  const int* a[kGroupArrays];  // level, op, row_begin, rows, idx_off, child base of slot 0, of slot 1
 };
 __global__ void k_compact(const unsigned long long* err, const int* meta, const int* level_ptr, GroupArrays garr,
                           int lcap, int gcap, int* out) {
@@ -528,7 +562,7 @@ __global__ void k_compact(const unsigned long long* err, const int* meta, const 
   const int nl = min(meta[0] + 1, lcap + 1), ng = min(meta[4], gcap);
   for (int i = threadIdx.x; i < nl; i += blockDim.x) out[kHdr + i] = level_ptr[i];
   int* go = out + kHdr + lcap + 1;
-  for (int k = 0; k < 5; ++k)
+  for (int k = 0; k < kGroupArrays; ++k)
     for (int i = threadIdx.x; i < ng; i += blockDim.x) go[k * gcap + i] = garr.a[k][i];
 }
 
@@ -632,7 +666,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
 
   // persistent arrays sized by N and E; the level and group tables take N + 1 and 5 x N entries (there are
   // at most N levels and N groups), so nothing waits for the depth to be known on the host
-  const size_t n1 = (size_t)N * 17 + 2 * (size_t)E + 16;
+  const size_t n1 = (size_t)N * 19 + 2 * (size_t)E + 16;
   if (hipMalloc(&s.blob, n1 * sizeof(int)) != hipSuccess) {
     set_error("fold_schedule: out of device memory");
     return fail(FOLD_E_NOMEM);
@@ -657,6 +691,8 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   s.g_row_begin = q; q += cap;
   s.g_rows = q; q += cap;
   s.g_idx_off = q; q += cap;
+  s.g_cbase0 = q; q += cap;
+  s.g_cbase1 = q; q += cap;
 
   // temporaries of the whole schedule, one pooled allocation
   Temp tmp(st);
@@ -675,7 +711,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   const long long rc = 256LL * std::max(B, 1);
   const long long scan_tmp_n = std::max<long long>(rc, N) / kScanTile + 2;
   constexpr int kLcap = 4096, kGcap = 4096;  // levels and groups read back with the error word
-  const size_t stage_n = kHdr + (kLcap + 1) + 5 * (size_t)kGcap;
+  const size_t stage_n = kHdr + (kLcap + 1) + kGroupArrays * (size_t)kGcap;
   tmp.reserve(&em, 1);
   tmp.reserve(&stage, stage_n);
   if (N > 0) {
@@ -755,8 +791,12 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
                        err, (const int*)nullptr, 0);
     hipLaunchKernelGGL(k_op_rows, grid_for(N), dim3(kBlock), 0, st, s.op_rows, gid, s.g_row_begin, s.g_op,
                        s.g_idx_off, s.child_pos, s.input_idx, ops, N, s.op_cpos, s.op_inp, err);
+    hipLaunchKernelGGL(k_cbase_init, grid_for(N), dim3(kBlock), 0, st, meta + 4, N, s.g_op, s.g_idx_off,
+                       s.child_pos, s.child_one, ops, s.g_cbase0, s.g_cbase1, err);
+    hipLaunchKernelGGL(k_cbase_check, grid_for(N), dim3(kBlock), 0, st, N, gid, s.g_row_begin, s.g_op,
+                       s.g_idx_off, s.child_pos, s.child_one, ops, s.g_cbase0, s.g_cbase1, err);
   }
-  GroupArrays ga{{s.g_level, s.g_op, s.g_row_begin, s.g_rows, s.g_idx_off}};
+  GroupArrays ga{{s.g_level, s.g_op, s.g_row_begin, s.g_rows, s.g_idx_off, s.g_cbase0, s.g_cbase1}};
   hipLaunchKernelGGL(k_compact, dim3(1), dim3(kBlock), 0, st, err, meta, s.level_ptr, ga, kLcap, kGcap, stage);
   if (hipGetLastError() != hipSuccess) {
     set_error("fold_schedule: kernel launch failed");
@@ -794,13 +834,16 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
     s.h_row_begin.assign(hg + 2 * kGcap, hg + 2 * kGcap + ng);
     s.h_rows.assign(hg + 3 * kGcap, hg + 3 * kGcap + ng);
     s.h_idx_off.assign(hg + 4 * kGcap, hg + 4 * kGcap + ng);
+    s.h_cbase0.assign(hg + 5 * kGcap, hg + 5 * kGcap + ng);
+    s.h_cbase1.assign(hg + 6 * kGcap, hg + 6 * kGcap + ng);
   } else {
     // more levels or groups than the first read-back holds: read the whole tables (a second synchronisation)
     s.h_level_ptr.resize(D + 1);
-    std::vector<int>* dst[5] = {&s.h_level, &s.h_op, &s.h_row_begin, &s.h_rows, &s.h_idx_off};
+    std::vector<int>* dst[kGroupArrays] = {&s.h_level, &s.h_op, &s.h_row_begin, &s.h_rows, &s.h_idx_off,
+                                           &s.h_cbase0, &s.h_cbase1};
     bool ok = hipMemcpyAsync(s.h_level_ptr.data(), s.level_ptr, (size_t)(D + 1) * sizeof(int),
                              hipMemcpyDeviceToHost, st) == hipSuccess;
-    for (int k = 0; k < 5; ++k) {
+    for (int k = 0; k < kGroupArrays; ++k) {
       dst[k]->resize(ng);
       ok = ok && hipMemcpyAsync(dst[k]->data(), ga.a[k], (size_t)ng * sizeof(int), hipMemcpyDeviceToHost, st) ==
                      hipSuccess;

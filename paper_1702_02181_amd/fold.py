@@ -57,7 +57,9 @@ class fold_sched_info(ctypes.Structure):
                 ("input_idx", _I32P), ("root_pos", _I32P),
                 ("h_level_ptr", POINTER(c_int32)), ("h_group_level", POINTER(c_int32)),
                 ("h_group_op", POINTER(c_int32)), ("h_group_row_begin", POINTER(c_int32)),
-                ("h_group_rows", POINTER(c_int32)), ("h_group_idx_off", POINTER(c_int32))]
+                ("h_group_rows", POINTER(c_int32)), ("h_group_idx_off", POINTER(c_int32)),
+                ("group_child_base0", _I32P), ("group_child_base1", _I32P),
+                ("h_group_child_base0", POINTER(c_int32)), ("h_group_child_base1", POINTER(c_int32))]
 
 
 class fold_param_set(ctypes.Structure):
@@ -428,7 +430,9 @@ class Schedule:
             return np.ctypeslib.as_array(p, shape=(n,)).copy() if n else np.zeros(0, np.int32)
         return dict(level_ptr=arr(i.h_level_ptr, i.num_levels + 1), group_level=arr(i.h_group_level, ng),
                     group_op=arr(i.h_group_op, ng), group_row_begin=arr(i.h_group_row_begin, ng),
-                    group_rows=arr(i.h_group_rows, ng), group_idx_off=arr(i.h_group_idx_off, ng))
+                    group_rows=arr(i.h_group_rows, ng), group_idx_off=arr(i.h_group_idx_off, ng),
+                    group_child_base0=arr(i.h_group_child_base0, ng),
+                    group_child_base1=arr(i.h_group_child_base1, ng))
 
     def arrays(self) -> dict:
         """Every schedule array, copied to host numpy (device arrays and the host group table)."""
@@ -437,7 +441,8 @@ class Schedule:
         out = dict(num_levels=D, num_groups=ng, num_roots=R, max_parents=i.max_parents)
         for name, cnt in (("depth", n), ("node_pos", n), ("pos_node", n), ("level_ptr", D + 1),
                           ("group_level", ng), ("group_op", ng), ("group_row_begin", ng), ("group_rows", ng),
-                          ("group_idx_off", ng), ("child_pos", e), ("input_idx", n), ("root_pos", R)):
+                          ("group_idx_off", ng), ("child_pos", e), ("input_idx", n), ("root_pos", R),
+                          ("group_child_base0", ng), ("group_child_base1", ng)):
             p = getattr(i, name)
             out[name] = _dev_copy_to_host(p, cnt) if p else np.zeros(0, np.int32)
         out["host"] = self.host_groups()

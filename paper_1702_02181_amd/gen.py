@@ -497,7 +497,9 @@ def table1(batch: int, mode: str, seed: int = 7, leaves: int = 64, hidden: int =
       "full":    every tree has a random shape of its own ("full dynamic").
       "manual":  the same shape as "dynamic", and every node position of the tree is an operation of its own,
                  all sharing one parameter set: the schedule then has one batched group per tree node, which is
-                 what manual batching runs (one batched kernel per node of the tree's static graph).
+                 what manual batching runs (one batched kernel per node of the tree's static graph), and each
+                 group's children are the consecutive rows of the child position's group, which the scheduler
+                 recognises as the static layout (children addressed by base + row, no gather index).
     Tokens ~ U{0..vocab-1}; table ~ N(0, 0.1^2); weights U(-0.1, 0.1)."""
     if mode not in ("dynamic", "full", "manual"):
         raise ValueError(mode)

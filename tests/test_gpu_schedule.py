@@ -141,3 +141,48 @@ def test_many_operations_one_group_per_tree_node():
     C.assert_schedule_equal(_gpu_sched(many), C.oracle_schedule(many))
     many.ops = many.ops + [gen.OpSpec(gen.KIND_TREELSTM, 2, 0, 0)]
     assert _err(many) == -1
+
+
+def _expected_child_bases(w, ref):
+    """Per group and child slot: the first child row when the slot's children are consecutive pool rows with
+    one parent edge each, else -1 (computed here from the reference schedule and the CSR)."""
+    indeg = np.zeros(w.num_nodes, np.int64)
+    kids = w.child_idx[w.child_idx >= 0]
+    np.add.at(indeg, kids, 1)
+    pos_node = np.asarray(ref["pos_node"])
+    out = np.full((2, len(ref["group_op"])), -1, np.int64)
+    cp = np.asarray(ref["child_pos"])
+    for g, (op, rb, rows, off) in enumerate(zip(ref["group_op"], ref["group_row_begin"], ref["group_rows"],
+                                                ref["group_idx_off"])):
+        a = w.ops[int(op)].arity
+        for k in range(min(a, 2)):
+            c = cp[int(off) + np.arange(int(rows)) * a + k]
+            if c[0] < 0 or not np.array_equal(c, c[0] + np.arange(int(rows))):
+                continue
+            if np.all(indeg[pos_node[c]] == 1):
+                out[k, g] = c[0]
+    return out
+
+
+@pytest.mark.parametrize("case", ["manual", "dynamic", "full", "cfg2", "cfg4", "dag"])
+def test_static_layout_child_bases(case):
+    """The per-slot child bases the forward kernels use to skip child_pos: every slot of a manual-batching
+    schedule (one operation per node position of identically shaped trees) has one; the gathered layouts
+    have them only where their children happen to be consecutive single-parent rows."""
+    if case in ("manual", "dynamic", "full"):
+        w = gen.table1(8, case, hidden=8, vocab=50)
+    elif case == "cfg2":
+        w = gen.config2(num_graphs=3, leaves=16, hidden=8)
+    elif case == "cfg4":
+        w = gen.config4(num_graphs=5, max_chain=20, hidden=8, in_dim=8)
+    else:
+        w = random_dag(np.random.default_rng(5), n_graphs=20, max_nodes=40)
+    g = _gpu_sched(w)
+    ref = C.oracle_schedule(w)
+    want = _expected_child_bases(w, ref)
+    got = np.stack([g["host"]["group_child_base0"], g["host"]["group_child_base1"]])
+    assert np.array_equal(got, want)
+    assert np.array_equal(np.stack([g["group_child_base0"], g["group_child_base1"]]), want)
+    if case == "manual":
+        internal = [i for i, op in enumerate(ref["group_op"]) if w.ops[int(op)].arity == 2]
+        assert internal and np.all(want[:, internal] >= 0)
