@@ -6,7 +6,9 @@ derivative, a lost cell-state pass-through, wrong sort keys and tie-breaks,
 min instead of max in the depth rule, node ids instead of positions as edge
 labels, overwriting instead of summing fan-out contributions, and in the parity metric: the per-row
 floor dropped, min instead of max over rows, the row norm taken as a min, whole= ignored, rows cut along
-the last axis, and NaN rows skipped."""
+the last axis, and NaN rows skipped; in the paper-form schedule: pass-throughs numbered among the user
+operations, a pass-through one depth too early, labels into the reader's own depth, and a concatenation
+taken row by row instead of output slot by output slot."""
 import os
 import shutil
 import subprocess
@@ -48,6 +50,12 @@ MUTATIONS = [
      "T = T.reshape(-1, R.shape[-1])\n        R = R.reshape(-1, R.shape[-1])"),
     ("compare.py", "return float((np.abs(T - R).max(axis=1) / row_ref).max())",
      "return float(np.nanmax(np.abs(T - R).max(axis=1) / row_ref))"),
+    ("paper_schedule.py", "items.append((d, K + t, (1, u, k)", "items.append((d, t, (1, u, k)"),
+    ("paper_schedule.py", "for d in range(depth[u] + 1, last.get((u, k), 0))",
+     "for d in range(depth[u], last.get((u, k), 0))"),
+    ("paper_schedule.py", "src_d = d - 1", "src_d = d"),
+    ("paper_schedule.py", "        for slot, t in enumerate(its[0][4]):\n            for it in its:",
+     "        for it in its:\n            for slot, t in enumerate(its[0][4]):"),
 ]
 
 
@@ -64,6 +72,6 @@ def test_planted_mistake_is_caught(i, tmp_path):
     p.write_text(src.replace(old, new, 1))
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:randomly",
                         "tests/test_oracle_schedule.py", "tests/test_oracle_cells.py",
-                        "tests/test_oracle_compare.py"],
+                        "tests/test_oracle_compare.py", "tests/test_oracle_paper_schedule.py"],
                        cwd=tmp_path, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"pins missed mutation {i}: {new!r}"
