@@ -164,6 +164,93 @@ int32_t fold_schedule(const fold_batch* batch, hipStream_t stream, fold_sched** 
 int32_t fold_sched_get_info(const fold_sched* sched, fold_sched_info* out);
 int32_t fold_sched_free(fold_sched* sched);
 
+/* ---- the paper's own form of the schedule ---------------------------------
+ * Section 2 schedules a typed DAG: source nodes are constants of a tensor
+ * type, other nodes invoke operations whose inputs and outputs have fixed
+ * tensor types, and an edge connects output k of node u to input j of node
+ * v.  Its five steps: (1) depth (constants 0, an operation node 1 + the
+ * largest depth it reads); (2) pass-through (identity) operations, so that a
+ * node at depth d + 1 reads only results of depth d; (3) one batch per
+ * (depth, operation); (4) at each depth the outputs of one type concatenated
+ * in the operations' enumeration order; (5) every edge labelled (d, t, i),
+ * the depth and type of the value it reads and its index into that
+ * concatenation; the schedule is the indices i grouped by depth and
+ * operation.  fold_schedule above is the special case of one state type
+ * (node and child states travel together) with pass-throughs elided; this
+ * call produces the general form, including an int-typed state such as the
+ * word ids of Figure 1.
+ *
+ * Readings (the paper is silent): pass-throughs are operations too, one per
+ * type t, numbered num_ops + t (after the caller's operations), with one
+ * input and one output of type t; one pass-through per value and depth,
+ * shared by all readers of that value; a batch lists its operation nodes in
+ * ascending node id and its pass-through instances in ascending value order
+ * (node id, then output slot); an operation's outputs of one type enter
+ * that type's concatenation in slot order, each with the whole batch in
+ * batch order; the depth-0 state of type t holds the constants of type t in
+ * ascending node id. */
+typedef struct {
+  int32_t num_inputs, num_outputs; /* 1..8 each */
+  const int32_t* in_type;          /* host [num_inputs], 0..num_types-1 */
+  const int32_t* out_type;         /* host [num_outputs] */
+} fold_typed_op;
+
+typedef struct {
+  int32_t num_graphs, num_nodes, num_edges;
+  int32_t num_ops;    /* 1..64 */
+  int32_t num_types;  /* 1..16 */
+  const int32_t* graph_ptr; /* device [G+1]: graph g is nodes graph_ptr[g] .. graph_ptr[g+1]-1 */
+  const int32_t* node_op;   /* device [N]: operation id, or -1 - t for a constant of type t */
+  const int32_t* in_ptr;    /* device [N+1]: node v's inputs are edges in_ptr[v] .. in_ptr[v+1]-1 */
+  const int32_t* in_node;   /* device [E]: source node of the edge (same graph) */
+  const int32_t* in_slot;   /* device [E]: source output slot */
+  const fold_typed_op* ops; /* host [num_ops] */
+} fold_typed_batch;
+
+typedef struct fold_typed_sched fold_typed_sched;
+
+typedef struct {
+  int32_t num_levels;   /* D: the largest depth */
+  int32_t num_batches;  /* non-empty (depth, operation) batches, pass-throughs included */
+  int32_t num_passes;   /* pass-through instances */
+  int32_t num_items;    /* operation nodes + pass-through instances */
+  int32_t num_gather;   /* entries of gather */
+  int32_t num_ops, num_types;
+  /* device, int32 */
+  const int32_t* depth;             /* [N] */
+  const int32_t* batch_depth;       /* [num_batches] ascending (depth, operation) */
+  const int32_t* batch_op;          /* [num_batches] operation, or num_ops + t: pass-through of type t */
+  const int32_t* batch_rows;        /* [num_batches] */
+  const int32_t* batch_gather_off;  /* [num_batches] input j of row r at gather[off + j * rows + r] */
+  const int32_t* batch_item_begin;  /* [num_batches] first entry in item_node */
+  const int32_t* item_node;         /* [num_items] node id, or -1 - p for pass-through instance p */
+  const int32_t* gather;            /* [num_gather] indices i into the (depth - 1, input type) state */
+  const int32_t* pass_node;         /* [num_passes] the value (node, output slot) carried, and the */
+  const int32_t* pass_slot;         /*   depth of the instance; ascending value, then depth */
+  const int32_t* pass_depth;
+  const int32_t* state_size;        /* [(D + 1) * num_types]: rows of the state (d, t) at d * T + t */
+  const int32_t* edge_index;        /* [E] label index i of every input edge (its d is the reader's
+                                       depth - 1, its t the input's type) */
+  /* host copies */
+  const int32_t* h_batch_depth;
+  const int32_t* h_batch_op;
+  const int32_t* h_batch_rows;
+  const int32_t* h_batch_gather_off;
+  const int32_t* h_state_size;
+} fold_typed_sched_info;
+
+/* fold_schedule_typed: validates the batch (FOLD_E_INVALID for a malformed
+ * op table, graph_ptr / in_ptr, an edge from a missing node or output or of
+ * the wrong type, a constant with inputs or an operation node with the wrong
+ * input count; FOLD_E_CHILD for an edge across graphs; FOLD_E_OP for an
+ * operation or constant type out of range; FOLD_E_CYCLE), then schedules it
+ * on the GPU.  The library allocates and owns the result.  Synchronises
+ * `stream` twice: once to size the pass-through arrays, once at the end. */
+int32_t fold_schedule_typed(const fold_typed_batch* batch, hipStream_t stream, fold_typed_sched** out);
+int32_t fold_typed_sched_get_info(const fold_typed_sched* sched, fold_typed_sched_info* out);
+int32_t fold_typed_sched_free(fold_typed_sched* sched);
+
+
 /* Parameters of one operation family, canonical row-major layout, device
  * memory, element type fold_params.dtype (bias always fp32).  G gate blocks
  * (Tree-LSTM 5, LSTM 4, TreeRNN / PROJ 1, EMBED 0) of `hidden` columns each,

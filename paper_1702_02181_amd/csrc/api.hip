@@ -760,6 +760,61 @@ int32_t fold_sched_free(fold_sched* h) {
   FOLD_GUARD_END
 }
 
+int32_t fold_schedule_typed(const fold_typed_batch* b, hipStream_t st, fold_typed_sched** out) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!out) return fail(FOLD_E_INVALID, "fold_schedule_typed: out is NULL");
+  *out = nullptr;
+  if (!b) return fail(FOLD_E_INVALID, "fold_schedule_typed: batch is NULL");
+  if (b->num_graphs < 0 || b->num_nodes < 0 || b->num_edges < 0)
+    return fail(FOLD_E_INVALID, "fold_schedule_typed: negative count");
+  if (!b->ops || !b->graph_ptr || !b->in_ptr || (b->num_nodes > 0 && !b->node_op) ||
+      (b->num_edges > 0 && (!b->in_node || !b->in_slot)))
+    return fail(FOLD_E_INVALID, "fold_schedule_typed: NULL array");
+  return schedule_typed_impl(b, st, out);
+  FOLD_GUARD_END
+}
+
+int32_t fold_typed_sched_get_info(const fold_typed_sched* h, fold_typed_sched_info* o) {
+  FOLD_GUARD_BEGIN
+  if (!h || !o) return fail(FOLD_E_INVALID, "fold_typed_sched_get_info: NULL argument");
+  const TypedSched& s = h->t;
+  o->num_levels = s.D;
+  o->num_batches = s.nb;
+  o->num_passes = s.P;
+  o->num_items = s.M;
+  o->num_gather = s.ngather;
+  o->num_ops = s.K;
+  o->num_types = s.T;
+  o->depth = s.depth;
+  o->batch_depth = s.batch_depth;
+  o->batch_op = s.batch_op;
+  o->batch_rows = s.batch_rows;
+  o->batch_gather_off = s.batch_goff;
+  o->batch_item_begin = s.batch_begin;
+  o->item_node = s.item_node;
+  o->gather = s.gather;
+  o->pass_node = s.pass_node;
+  o->pass_slot = s.pass_slot;
+  o->pass_depth = s.pass_depth;
+  o->state_size = s.state_size;
+  o->edge_index = s.edge_index;
+  o->h_batch_depth = s.h_depth_b.data();
+  o->h_batch_op = s.h_op_b.data();
+  o->h_batch_rows = s.h_rows_b.data();
+  o->h_batch_gather_off = s.h_goff_b.data();
+  o->h_state_size = s.h_state_size.data();
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
+int32_t fold_typed_sched_free(fold_typed_sched* h) {
+  FOLD_GUARD_BEGIN
+  typed_sched_destroy_impl(h);
+  return FOLD_OK;
+  FOLD_GUARD_END
+}
+
 static int check_params(const fold_params* prm, const char* who) {
   const std::string w = std::string(who) + ": ";
   if (!prm || !prm->sets || prm->num_sets < 1) return fail(FOLD_E_INVALID, w + "no parameter sets");

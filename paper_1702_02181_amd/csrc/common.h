@@ -111,6 +111,17 @@ struct Sched {
   std::vector<int32_t> h_op_row_ptr;  // [num_ops + 1] ranges of op_rows
 };
 
+// The paper's own form of a schedule (typed per-depth states, pass-through operations), fold_schedule_typed.
+struct TypedSched {
+  int N = 0, E = 0, K = 0, T = 0, D = 0, nb = 0, P = 0, M = 0, ngather = 0;
+  void* blob = nullptr;  // every device array below
+  int32_t *depth = nullptr, *batch_depth = nullptr, *batch_op = nullptr, *batch_rows = nullptr,
+          *batch_goff = nullptr, *batch_begin = nullptr, *item_node = nullptr, *gather = nullptr,
+          *pass_node = nullptr, *pass_slot = nullptr, *pass_depth = nullptr, *state_size = nullptr,
+          *edge_index = nullptr;
+  std::vector<int32_t> h_depth_b, h_op_b, h_rows_b, h_goff_b, h_state_size;
+};
+
 // Packed weights of one parameter set.
 struct PackedSet {
   int kind = 0, in_dim = 0, arity = 0, G = 0;
@@ -141,6 +152,7 @@ struct Packed {
 }  // namespace fold
 
 struct fold_sched { fold::Sched s; };
+struct fold_typed_sched { fold::TypedSched t; };
 struct fold_packed { fold::Packed p; };
 
 // ---------------------------------------------------------------- device helpers

@@ -9,6 +9,8 @@ namespace fold {
 
 int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out);
 void sched_destroy_impl(fold_sched* h);
+int32_t schedule_typed_impl(const fold_typed_batch* b, hipStream_t st, fold_typed_sched** out);
+void typed_sched_destroy_impl(fold_typed_sched* h);
 
 int32_t pack_impl(const fold_params* p, hipStream_t st, fold_packed** out);
 void packed_destroy_impl(fold_packed* h);

@@ -476,6 +476,15 @@ __global__ void k_root_emit(const int* flag, const int* rank, const int* node_po
   if (v < N && flag[v]) root_pos[rank[v]] = node_pos[v];
 }
 
+__global__ void k_zero_ints(int* p, int n) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0;
+}
+
+__global__ void k_fill_ints(int* p, long long n, int v) {
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
 // error word "none", meta zero
 __global__ void k_init_meta(void* em) {
   if (threadIdx.x == 0) *static_cast<unsigned long long*>(em) = kNoErr;
@@ -865,6 +874,555 @@ void sched_destroy_impl(fold_sched* h) {
   if (!h) return;
   if (h->s.blob) (void)hipFree(h->s.blob);
   delete h;
+}
+
+// ================================================================ the paper's form: typed states
+// Section 2's five steps on a typed DAG (constants of a tensor type as sources, operations with typed inputs
+// and outputs, edges from a specific output), with the pass-throughs and per-(depth, type) concatenations
+// made explicit.  Phase 1 validates, takes depths (the per-graph depth kernel above, whose constants sit at
+// 1: the paper's depth is one less), lists the values (node, output slot), finds each value's deepest
+// reader and counts its pass-through instances; one read-back sizes phase 2.  Phase 2 emits the
+// pass-through instances, sorts operation nodes and pass-throughs by (depth, operation) (stable: node ids,
+// then value order), cuts the batches, lays out each depth's concatenation per type (operation order, then
+// output slot, then batch order) and writes every gather index.
+
+namespace {
+
+constexpr int kMaxTypedOps = 64, kMaxTypes = 16, kMaxSlots = 8;
+
+struct TypedOpTable {
+  int K, T;
+  unsigned char nin[kMaxTypedOps], nout[kMaxTypedOps];
+  unsigned char in_type[kMaxTypedOps][kMaxSlots], out_type[kMaxTypedOps][kMaxSlots];
+  unsigned char out_rank[kMaxTypedOps][kMaxSlots];  // rank of output k among the op's outputs of its type
+  unsigned char nout_t[kMaxTypedOps][kMaxTypes];    // the op's outputs of type t
+};
+
+__device__ __forceinline__ int t_nout(const TypedOpTable& o, int op) { return op < 0 ? 1 : o.nout[op]; }
+
+__global__ void k_typed_check(const int* node_op, const int* in_ptr, const int* in_node, const int* in_slot,
+                              const int* node_graph, int N, TypedOpTable ops, unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= N) return;
+  const int op = node_op[v], a = in_ptr[v], b = in_ptr[v + 1];
+  if (op < 0) {
+    if (-1 - op >= ops.T) report(err, v + 1, FOLD_E_OP);
+    else if (b != a) report(err, v + 1, FOLD_E_INVALID);
+    return;
+  }
+  if (op >= ops.K) { report(err, v + 1, FOLD_E_OP); return; }
+  if (b - a != ops.nin[op]) { report(err, v + 1, FOLD_E_INVALID); return; }
+  for (int j = 0; j < b - a; ++j) {
+    const int u = in_node[a + j], k = in_slot[a + j];
+    if (u < 0 || u >= N) { report(err, v + 1, FOLD_E_INVALID); return; }
+    if (node_graph[u] != node_graph[v]) { report(err, v + 1, FOLD_E_CHILD); return; }
+    const int uop = node_op[u];
+    if (uop >= ops.K || (uop < 0 && -1 - uop >= ops.T)) continue;  // that node reports its own error
+    if (k < 0 || k >= t_nout(ops, uop)) { report(err, v + 1, FOLD_E_INVALID); return; }
+    const int tu = uop < 0 ? -1 - uop : ops.out_type[uop][k];
+    if (tu != ops.in_type[op][j]) { report(err, v + 1, FOLD_E_INVALID); return; }
+  }
+}
+
+// paper depth (constants 0), the number of values of each node, the number of constants of each type
+__global__ void k_typed_nodes(const int* kdepth, const int* node_op, int N, TypedOpTable ops, int* depth,
+                              int* nout_v, int* meta, const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= N) return;
+  const int op = node_op[v];
+  depth[v] = kdepth[v] - 1;
+  nout_v[v] = t_nout(ops, op);
+  if (op < 0) atomicAdd(&meta[8 + (-1 - op)], 1);
+}
+
+// last[value] = the deepest depth that reads it (its own depth if nobody does)
+__global__ void k_typed_last_init(const int* depth, const int* nout_v, const int* val_ptr, int N, int* last,
+                                  const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= N) return;
+  for (int k = 0; k < nout_v[v]; ++k) last[val_ptr[v] + k] = depth[v];
+}
+
+__global__ void k_typed_last(const int* depth, const int* in_ptr, const int* in_node, const int* in_slot,
+                             const int* val_ptr, int N, int* last, const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= N) return;
+  for (int e = in_ptr[v]; e < in_ptr[v + 1]; ++e) atomicMax(&last[val_ptr[in_node[e]] + in_slot[e]], depth[v]);
+}
+
+// pass-through instances of every value: one per depth strictly between its own and its deepest reader's
+__global__ void k_typed_npass(const int* depth, const int* nout_v, const int* val_ptr, const int* last, int N,
+                              int* npass, const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= N) return;
+  for (int k = 0; k < nout_v[v]; ++k) {
+    const int q = val_ptr[v] + k;
+    npass[q] = max(0, last[q] - depth[v] - 1);
+  }
+}
+
+__global__ void k_typed_pass_emit(const int* depth, const int* nout_v, const int* val_ptr, const int* npass,
+                                  const int* pass_ptr, int N, int* pass_node, int* pass_slot, int* pass_depth) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= N) return;
+  for (int k = 0; k < nout_v[v]; ++k) {
+    const int q = val_ptr[v] + k, p0 = pass_ptr[q];
+    for (int j = 0; j < npass[q]; ++j) {
+      pass_node[p0 + j] = v;
+      pass_slot[p0 + j] = k;
+      pass_depth[p0 + j] = depth[v] + 1 + j;
+    }
+  }
+}
+
+// sort keys (depth - 1) * (K + T) + op of operation nodes and pass-throughs (op K + t); constants get `sent`,
+// past every real key, and sort to the end
+__global__ void k_typed_keys(const int* depth, const int* node_op, int N, const int* pass_node, const int* pass_slot,
+                             const int* pass_depth, int P, TypedOpTable ops, unsigned sent, unsigned* keys,
+                             int* vals) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int KT = ops.K + ops.T;
+  if (i < N) {
+    const int op = node_op[i];
+    keys[i] = op < 0 ? sent : (unsigned)((depth[i] - 1) * KT + op);
+    vals[i] = i;
+  } else if (i < N + P) {
+    const int p = i - N, u = pass_node[p], uop = node_op[u];
+    const int t = uop < 0 ? -1 - uop : ops.out_type[uop][pass_slot[p]];
+    keys[i] = (unsigned)((pass_depth[p] - 1) * KT + ops.K + t);
+    vals[i] = i;
+  }
+}
+
+__global__ void k_typed_items(const unsigned* keys, const int* vals, int M, int N, int* item_node, int* flag) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= M) return;
+  const int x = vals[i];
+  item_node[i] = x < N ? x : -1 - (x - N);
+  flag[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1 : 0;
+}
+
+__global__ void k_typed_batches(const unsigned* keys, const int* flag, const int* exs, int M, int KT, int* bidx,
+                                int* b_begin, int* b_depth, int* b_op) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= M) return;
+  const int b = exs[i] + flag[i] - 1;
+  bidx[i] = b;
+  if (flag[i]) {
+    b_begin[b] = i;
+    b_depth[b] = (int)(keys[i] / (unsigned)KT) + 1;
+    b_op[b] = (int)(keys[i] % (unsigned)KT);
+  }
+}
+
+// per batch (entries past the batch count get zeros): rows, gather entries, and per type t its outputs of
+// type t (rows * the op's outputs of type t) at cnt[t * M + b]
+__global__ void k_typed_batch_sizes(const int* nb_ptr, int M, const int* b_begin, const int* b_op, TypedOpTable ops,
+                                    int* b_rows, int* gcount, int* cnt) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= M) return;
+  const int nb = *nb_ptr;
+  if (b >= nb) {
+    gcount[b] = 0;
+    for (int t = 0; t < ops.T; ++t) cnt[(size_t)t * M + b] = 0;
+    return;
+  }
+  const int rows = (b + 1 < nb ? b_begin[b + 1] : M) - b_begin[b];
+  const int op = b_op[b];
+  b_rows[b] = rows;
+  gcount[b] = rows * (op < ops.K ? ops.nin[op] : 1);
+  for (int t = 0; t < ops.T; ++t)
+    cnt[(size_t)t * M + b] = rows * (op < ops.K ? ops.nout_t[op][t] : (op - ops.K == t ? 1 : 0));
+}
+
+// first and last batch of every depth
+__global__ void k_typed_depth_span(const int* nb_ptr, const int* b_depth, int* dfirst, int* dlast) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  const int nb = *nb_ptr;
+  if (b >= nb) return;
+  const int d = b_depth[b];
+  if (b == 0 || b_depth[b - 1] != d) dfirst[d] = b;
+  if (b == nb - 1 || b_depth[b + 1] != d) dlast[d] = b;
+}
+
+// state sizes: depth 0 from the constants per type (meta[8 + t]), deeper ones from the batch scans
+__global__ void k_typed_state_size(int D, int M, int T, const int* dfirst, const int* dlast, const int* cnt,
+                                   const int* cscan, const int* meta, int* size) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (D + 1) * T) return;
+  const int d = i / T, t = i - d * T;
+  if (d == 0) {
+    size[i] = meta[8 + t];
+    return;
+  }
+  const size_t o = (size_t)t * M;
+  size[i] = cscan[o + dlast[d]] + cnt[o + dlast[d]] - cscan[o + dfirst[d]];
+}
+
+// concatenation index of every constant: its rank among the constants of its type (flag scan of type t)
+__global__ void k_typed_const_flag(const int* node_op, int N, int t, int* flag) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v < N) flag[v] = node_op[v] == -1 - t ? 1 : 0;
+}
+__global__ void k_typed_const_idx(const int* flag, const int* exs, const int* val_ptr, int N, int* vidx) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v < N && flag[v]) vidx[val_ptr[v]] = exs[v];
+}
+
+// concatenation index of every item's outputs at the item's depth: vidx[value] for operation nodes,
+// pidx[p] for pass-through instance p
+__global__ void k_typed_out_idx(const int* item_node, const int* bidx, const int* b_begin, const int* b_depth,
+                                const int* b_op, const int* b_rows, const int* dfirst, const int* cscan, int M,
+                                const int* val_ptr, TypedOpTable ops, int* vidx, int* pidx) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= M) return;
+  const int b = bidx[i], r = i - b_begin[b], op = b_op[b], rows = b_rows[b], f = dfirst[b_depth[b]];
+  const int x = item_node[i];
+  if (op < ops.K) {
+    for (int k = 0; k < ops.nout[op]; ++k) {
+      const size_t o = (size_t)ops.out_type[op][k] * M;
+      vidx[val_ptr[x] + k] = cscan[o + b] - cscan[o + f] + ops.out_rank[op][k] * rows + r;
+    }
+  } else {
+    const size_t o = (size_t)(op - ops.K) * M;
+    pidx[-1 - x] = cscan[o + b] - cscan[o + f] + r;
+  }
+}
+
+// the label index of value (u, k) read at depth d: the value itself if it was made at d - 1, else its
+// pass-through instance at d - 1
+__device__ __forceinline__ int typed_label(const int* depth, const int* val_ptr, const int* vidx, const int* pass_ptr,
+                                           const int* pidx, int u, int k, int d) {
+  const int du = depth[u], q = val_ptr[u] + k;
+  return du == d - 1 ? vidx[q] : pidx[pass_ptr[q] + (d - 2 - du)];
+}
+
+__global__ void k_typed_gather(const int* item_node, const int* bidx, const int* b_begin, const int* b_depth,
+                               const int* b_op, const int* b_rows, const int* b_goff, int M, const int* depth,
+                               const int* in_ptr, const int* in_node, const int* in_slot, const int* val_ptr,
+                               const int* vidx, const int* pass_ptr, const int* pidx, const int* pass_node,
+                               const int* pass_slot, TypedOpTable ops, int* gather, int* edge_index) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= M) return;
+  const int b = bidx[i], r = i - b_begin[b], d = b_depth[b], rows = b_rows[b];
+  const int x = item_node[i];
+  int* g = gather + b_goff[b] + r;
+  if (b_op[b] < ops.K) {
+    for (int e = in_ptr[x], j = 0; e < in_ptr[x + 1]; ++e, ++j) {
+      const int lab = typed_label(depth, val_ptr, vidx, pass_ptr, pidx, in_node[e], in_slot[e], d);
+      g[j * rows] = lab;
+      edge_index[e] = lab;
+    }
+  } else {
+    const int p = -1 - x;
+    g[0] = typed_label(depth, val_ptr, vidx, pass_ptr, pidx, pass_node[p], pass_slot[p], d);
+  }
+}
+
+__global__ void k_typed_compact(const unsigned long long* err, const int* meta, const int* b_depth, const int* b_op,
+                                const int* b_rows, const int* b_goff, const int* size, int nb, int nsize, int cap,
+                                int* out) {
+  const unsigned long long e = *err;
+  if (threadIdx.x == 0) {
+    out[0] = (int)(unsigned)(e & 0xffffffffull);
+    out[1] = (int)(unsigned)(e >> 32);
+    for (int i = 0; i < 14; ++i) out[2 + i] = meta[i];
+  }
+  if (e != kNoErr) return;
+  const int n = min(nb, cap), ns = min(nsize, cap);
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    out[kHdr + i] = b_depth[i];
+    out[kHdr + cap + i] = b_op[i];
+    out[kHdr + 2 * cap + i] = b_rows[i];
+    out[kHdr + 3 * cap + i] = b_goff[i];
+  }
+  for (int i = threadIdx.x; i < ns; i += blockDim.x) out[kHdr + 4 * cap + i] = size[i];
+}
+
+}  // namespace
+
+void typed_sched_destroy_impl(fold_typed_sched* h) {
+  if (!h) return;
+  if (h->t.blob) (void)hipFree(h->t.blob);
+  delete h;
+}
+
+int32_t schedule_typed_impl(const fold_typed_batch* b, hipStream_t st, fold_typed_sched** out) {
+  const int N = b->num_nodes, E = b->num_edges, G = b->num_graphs, K = b->num_ops, T = b->num_types;
+  if (K < 1 || K > kMaxTypedOps || T < 1 || T > kMaxTypes) {
+    set_error("fold_schedule_typed: need 1..64 operations and 1..16 types");
+    return FOLD_E_INVALID;
+  }
+  TypedOpTable ops{};
+  ops.K = K;
+  ops.T = T;
+  for (int o = 0; o < K; ++o) {
+    const fold_typed_op& op = b->ops[o];
+    if (op.num_inputs < 1 || op.num_inputs > kMaxSlots || op.num_outputs < 1 || op.num_outputs > kMaxSlots ||
+        !op.in_type || !op.out_type) {
+      set_error("fold_schedule_typed: operation " + std::to_string(o) + " needs 1..8 inputs and 1..8 outputs");
+      return FOLD_E_INVALID;
+    }
+    ops.nin[o] = (unsigned char)op.num_inputs;
+    ops.nout[o] = (unsigned char)op.num_outputs;
+    for (int j = 0; j < op.num_inputs; ++j) {
+      if (op.in_type[j] < 0 || op.in_type[j] >= T) {
+        set_error("fold_schedule_typed: operation " + std::to_string(o) + " has an input type out of range");
+        return FOLD_E_INVALID;
+      }
+      ops.in_type[o][j] = (unsigned char)op.in_type[j];
+    }
+    for (int k = 0; k < op.num_outputs; ++k) {
+      const int t = op.out_type[k];
+      if (t < 0 || t >= T) {
+        set_error("fold_schedule_typed: operation " + std::to_string(o) + " has an output type out of range");
+        return FOLD_E_INVALID;
+      }
+      ops.out_type[o][k] = (unsigned char)t;
+      ops.out_rank[o][k] = ops.nout_t[o][t]++;
+    }
+  }
+  int device = 0;
+  FOLD_HIP_CHECK(hipGetDevice(&device));
+  init_pool_once(device);
+  auto* h = new fold_typed_sched();
+  TypedSched& s = h->t;
+  s.N = N; s.E = E; s.K = K; s.T = T;
+  auto fail = [&](int code) {
+    typed_sched_destroy_impl(h);
+    return code;
+  };
+  auto device_error = [&](const char* what) {
+    set_error(std::string("fold_schedule_typed: ") + what);
+    return fail(FOLD_E_DEVICE);
+  };
+
+  // phase 1 temporaries (kept to the end): N-sized, and values (at most 8 per node)
+  const long long Vmax = 8LL * std::max(N, 1);
+  Temp tmp1(st);
+  struct ErrMeta {
+    unsigned long long err;
+    int meta[8 + kMaxTypes];  // [0] max depth + 1, [1] max parents, [2] values, [3] pass-throughs,
+                              // [4] batches, [5] gather entries, [6, 7] scratch totals, [8 + t] constants of type t
+  };
+  static_assert(offsetof(ErrMeta, meta) == sizeof(unsigned long long), "k_init_meta's layout");
+  ErrMeta* em = nullptr;
+  int *node_graph = nullptr, *indeg = nullptr, *scratch = nullptr, *kdepth = nullptr, *depth = nullptr,
+      *nout_v = nullptr, *val_ptr = nullptr, *last = nullptr, *npass = nullptr, *pass_ptr = nullptr,
+      *scan_tmp1 = nullptr;
+  tmp1.reserve(&em, 1);
+  tmp1.reserve(&node_graph, N);
+  tmp1.reserve(&indeg, N);
+  tmp1.reserve(&scratch, (size_t)(6LL * N + G + E + 1));
+  tmp1.reserve(&kdepth, N);
+  tmp1.reserve(&depth, N);
+  tmp1.reserve(&nout_v, N);
+  tmp1.reserve(&val_ptr, N);
+  tmp1.reserve(&last, Vmax);
+  tmp1.reserve(&npass, Vmax);
+  tmp1.reserve(&pass_ptr, Vmax);
+  tmp1.reserve(&scan_tmp1, (size_t)(Vmax / kScanTile + 2));
+  if (tmp1.commit() != hipSuccess) {
+    set_error("fold_schedule_typed: out of device memory (temporaries)");
+    return fail(FOLD_E_NOMEM);
+  }
+  unsigned long long* err = &em->err;
+  int* meta = em->meta;
+  hipLaunchKernelGGL(k_init_meta, dim3(1), dim3(64), 0, st, em);
+  hipLaunchKernelGGL(k_zero_ints, dim3(1), dim3(64), 0, st, meta + 8, kMaxTypes);
+  // pass counts of values past the last one stay 0, so the scan over the largest possible value count
+  // yields the exact total
+  hipLaunchKernelGGL(k_fill_ints, grid_for(std::min<long long>(Vmax, 1 << 20)), dim3(kBlock), 0, st, npass, Vmax, 0);
+  hipLaunchKernelGGL(k_check_struct, grid_for(std::max(G + 1, N + 1)), dim3(kBlock), 0, st, b->graph_ptr, G,
+                     b->in_ptr, N, E, err);
+  if (N > 0) {
+    if (G > 0) hipLaunchKernelGGL(k_node_graph, dim3(G), dim3(kBlock), 0, st, b->graph_ptr, node_graph, err);
+    hipLaunchKernelGGL(k_typed_check, grid_for(N), dim3(kBlock), 0, st, b->node_op, b->in_ptr, b->in_node,
+                       b->in_slot, node_graph, N, ops, err);
+    if (G > 0)
+      hipLaunchKernelGGL(k_depth, dim3(G), dim3(kBlock), kDepthLdsInts * sizeof(int), st, b->graph_ptr, b->in_ptr,
+                         b->in_node, kdepth, indeg, scratch, err, meta);
+    hipLaunchKernelGGL(k_typed_nodes, grid_for(N), dim3(kBlock), 0, st, kdepth, b->node_op, N, ops, depth, nout_v,
+                       meta, err);
+    scan_exclusive(nout_v, val_ptr, N, meta + 2, scan_tmp1, st);
+    hipLaunchKernelGGL(k_typed_last_init, grid_for(N), dim3(kBlock), 0, st, depth, nout_v, val_ptr, N, last, err);
+    hipLaunchKernelGGL(k_typed_last, grid_for(N), dim3(kBlock), 0, st, depth, b->in_ptr, b->in_node, b->in_slot,
+                       val_ptr, N, last, err);
+    hipLaunchKernelGGL(k_typed_npass, grid_for(N), dim3(kBlock), 0, st, depth, nout_v, val_ptr, last, N, npass, err);
+    scan_exclusive(npass, pass_ptr, (int)Vmax, meta + 3, scan_tmp1, st);
+  }
+  if (hipGetLastError() != hipSuccess) return device_error("kernel launch failed");
+  // first synchronisation: the error word, the depth, and the sizes of phase 2
+  ErrMeta hm{};
+  if (hipMemcpyAsync(&hm, em, sizeof(hm), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return device_error("device error while validating");
+  if (hm.err != kNoErr) {
+    std::string msg;
+    int code = decode_error(hm.err, &msg);
+    set_error("fold_schedule_typed" + msg.substr(msg.find(':')));
+    return fail(code);
+  }
+  const int D = N > 0 ? hm.meta[0] - 1 : 0;
+  const int V = N > 0 ? hm.meta[2] : 0;
+  const int P = N > 0 ? hm.meta[3] : 0;
+  if ((long long)(D + 1) * (K + T) > kMaxKeys) {
+    set_error("fold_schedule_typed: depth * (operations + types) exceeds 2^30 (the sort keys)");
+    return fail(FOLD_E_INVALID);
+  }
+  int nconst = 0;
+  for (int t = 0; t < T; ++t) nconst += hm.meta[8 + t];
+  const int M = N - nconst + P;  // items: operation nodes and pass-through instances
+  s.D = D; s.P = P; s.M = M;
+  const int ngather = E + P;
+  s.ngather = ngather;
+
+  // persistent arrays, now that P is known
+  const size_t nsize = (size_t)(D + 1) * T;
+  const size_t Mc = std::max(M, 1);
+  const size_t n_int = (size_t)N + 6 * Mc + (size_t)std::max(ngather, 1) + 3 * (size_t)std::max(P, 1) + nsize +
+                       (size_t)std::max(E, 1) + 16;
+  if (hipMalloc(&s.blob, n_int * sizeof(int)) != hipSuccess) {
+    set_error("fold_schedule_typed: out of device memory");
+    return fail(FOLD_E_NOMEM);
+  }
+  int* q = static_cast<int*>(s.blob);
+  s.depth = q; q += N;
+  s.batch_depth = q; q += Mc;
+  s.batch_op = q; q += Mc;
+  s.batch_rows = q; q += Mc;
+  s.batch_goff = q; q += Mc;
+  s.batch_begin = q; q += Mc;
+  s.item_node = q; q += Mc;
+  s.gather = q; q += std::max(ngather, 1);
+  s.pass_node = q; q += std::max(P, 1);
+  s.pass_slot = q; q += std::max(P, 1);
+  s.pass_depth = q; q += std::max(P, 1);
+  s.state_size = q; q += nsize;
+  s.edge_index = q; q += std::max(E, 1);
+  if (N > 0 && hipMemcpyAsync(s.depth, depth, (size_t)N * sizeof(int), hipMemcpyDeviceToDevice, st) != hipSuccess)
+    return device_error("copy of the depths failed");
+
+  // phase 2
+  const int NI = N + P;  // sort entries: every node (constants sort last) and every pass-through
+  const int B = (NI + kRadixTile - 1) / kRadixTile;
+  const long long rc = 256LL * std::max(B, 1);
+  Temp tmp2(st);
+  unsigned *ka = nullptr, *kb = nullptr;
+  int *va = nullptr, *vb = nullptr, *flag = nullptr, *exs = nullptr, *radix_counts = nullptr, *scan_tmp = nullptr;
+  int *bidx = nullptr, *gcount = nullptr, *cnt = nullptr, *cscan = nullptr, *dspan = nullptr, *vidx = nullptr,
+      *pidx = nullptr, *stage = nullptr;
+  constexpr int kCap = 4096;  // batches and state sizes read back with the final error word
+  const size_t stage_n = kHdr + 5 * (size_t)kCap;
+  const long long scan_n = std::max<long long>(std::max<long long>(rc, NI), (long long)T * Mc);
+  tmp2.reserve(&stage, stage_n);
+  tmp2.reserve(&ka, std::max(NI, 1));
+  tmp2.reserve(&kb, std::max(NI, 1));
+  tmp2.reserve(&va, std::max(NI, 1));
+  tmp2.reserve(&vb, std::max(NI, 1));
+  tmp2.reserve(&flag, std::max(NI, 1));
+  tmp2.reserve(&exs, std::max(NI, 1));
+  tmp2.reserve(&radix_counts, rc);
+  tmp2.reserve(&scan_tmp, (size_t)(scan_n / kScanTile + 2));
+  tmp2.reserve(&bidx, Mc);
+  tmp2.reserve(&gcount, Mc);
+  tmp2.reserve(&cnt, (size_t)T * Mc);
+  tmp2.reserve(&cscan, (size_t)T * Mc);
+  tmp2.reserve(&dspan, 2 * (size_t)(D + 1));
+  tmp2.reserve(&vidx, std::max(V, 1));
+  tmp2.reserve(&pidx, std::max(P, 1));
+  if (tmp2.commit() != hipSuccess) {
+    set_error("fold_schedule_typed: out of device memory (temporaries)");
+    return fail(FOLD_E_NOMEM);
+  }
+  int* dfirst = dspan;
+  int* dlast = dspan + (D + 1);
+  const int KT = K + T;
+  if (N > 0) {
+    if (P > 0)
+      hipLaunchKernelGGL(k_typed_pass_emit, grid_for(N), dim3(kBlock), 0, st, depth, nout_v, val_ptr, npass, pass_ptr,
+                         N, s.pass_node, s.pass_slot, s.pass_depth);
+    const unsigned sent = (unsigned)(D * KT);
+    hipLaunchKernelGGL(k_typed_keys, grid_for(NI), dim3(kBlock), 0, st, depth, b->node_op, N, s.pass_node,
+                       s.pass_slot, s.pass_depth, P, ops, sent, ka, va);
+    int bits = 1;
+    while (bits < 32 && ((unsigned long long)sent >> bits)) ++bits;
+    const int passes = (bits + 7) / 8;
+    for (int ps = 0; ps < passes; ++ps) {
+      hipLaunchKernelGGL(k_radix_count, dim3(B), dim3(kBlock), 0, st, ka, NI, 8 * ps, radix_counts, B, err,
+                         (const int*)nullptr, 0);
+      scan_exclusive(radix_counts, radix_counts, (int)rc, meta + 6, scan_tmp, st);
+      hipLaunchKernelGGL(k_radix_scatter, dim3(B), dim3(kBlock), 0, st, ka, va, kb, vb, radix_counts, NI, 8 * ps, B,
+                         err, (const int*)nullptr, 0);
+      std::swap(ka, kb);
+      std::swap(va, vb);
+    }
+    if (M > 0) {
+      hipLaunchKernelGGL(k_typed_items, grid_for(M), dim3(kBlock), 0, st, ka, va, M, N, s.item_node, flag);
+      scan_exclusive(flag, exs, M, meta + 4, scan_tmp, st);
+      hipLaunchKernelGGL(k_typed_batches, grid_for(M), dim3(kBlock), 0, st, ka, flag, exs, M, KT, bidx,
+                         s.batch_begin, s.batch_depth, s.batch_op);
+      hipLaunchKernelGGL(k_typed_batch_sizes, grid_for(M), dim3(kBlock), 0, st, meta + 4, M, s.batch_begin,
+                         s.batch_op, ops, s.batch_rows, gcount, cnt);
+      scan_exclusive(gcount, s.batch_goff, M, meta + 5, scan_tmp, st);
+      for (int t = 0; t < T; ++t)
+        scan_exclusive(cnt + (size_t)t * M, cscan + (size_t)t * M, M, meta + 7, scan_tmp, st);
+      hipLaunchKernelGGL(k_typed_depth_span, grid_for(M), dim3(kBlock), 0, st, meta + 4, s.batch_depth, dfirst, dlast);
+    }
+    hipLaunchKernelGGL(k_typed_state_size, grid_for((long long)nsize), dim3(kBlock), 0, st, D, std::max(M, 1), T,
+                       dfirst, dlast, cnt, cscan, meta, s.state_size);
+    for (int t = 0; t < T; ++t) {
+      hipLaunchKernelGGL(k_typed_const_flag, grid_for(N), dim3(kBlock), 0, st, b->node_op, N, t, flag);
+      scan_exclusive(flag, exs, N, meta + 7, scan_tmp, st);
+      hipLaunchKernelGGL(k_typed_const_idx, grid_for(N), dim3(kBlock), 0, st, flag, exs, val_ptr, N, vidx);
+    }
+    if (M > 0) {
+      hipLaunchKernelGGL(k_typed_out_idx, grid_for(M), dim3(kBlock), 0, st, s.item_node, bidx, s.batch_begin,
+                         s.batch_depth, s.batch_op, s.batch_rows, dfirst, cscan, M, val_ptr, ops, vidx, pidx);
+      hipLaunchKernelGGL(k_typed_gather, grid_for(M), dim3(kBlock), 0, st, s.item_node, bidx, s.batch_begin,
+                         s.batch_depth, s.batch_op, s.batch_rows, s.batch_goff, M, depth, b->in_ptr, b->in_node,
+                         b->in_slot, val_ptr, vidx, pass_ptr, pidx, s.pass_node, s.pass_slot, ops, s.gather,
+                         s.edge_index);
+    }
+  }
+  // batches <= items; read back the batch table and the state sizes up to kCap entries each
+  hipLaunchKernelGGL(k_typed_compact, dim3(1), dim3(kBlock), 0, st, err, meta, s.batch_depth, s.batch_op,
+                     s.batch_rows, s.batch_goff, s.state_size, M, (int)nsize, kCap, stage);
+  if (hipGetLastError() != hipSuccess) return device_error("kernel launch failed");
+  std::vector<int> hb(stage_n, 0);
+  if (hipMemcpyAsync(hb.data(), stage, stage_n * sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return device_error("device error while scheduling");
+  const int nb = M > 0 ? hb[2 + 4] : 0;
+  s.nb = nb;
+  if (nb <= kCap && (int)nsize <= kCap) {
+    const int* hs = hb.data() + kHdr;
+    s.h_depth_b.assign(hs, hs + nb);
+    s.h_op_b.assign(hs + kCap, hs + kCap + nb);
+    s.h_rows_b.assign(hs + 2 * kCap, hs + 2 * kCap + nb);
+    s.h_goff_b.assign(hs + 3 * kCap, hs + 3 * kCap + nb);
+    s.h_state_size.assign(hs + 4 * kCap, hs + 4 * kCap + nsize);
+  } else {
+    std::vector<int>* dst[4] = {&s.h_depth_b, &s.h_op_b, &s.h_rows_b, &s.h_goff_b};
+    const int* src[4] = {s.batch_depth, s.batch_op, s.batch_rows, s.batch_goff};
+    bool ok = true;
+    for (int k = 0; k < 4; ++k) {
+      dst[k]->resize(nb);
+      ok = ok && hipMemcpyAsync(dst[k]->data(), src[k], (size_t)nb * sizeof(int), hipMemcpyDeviceToHost, st) ==
+                     hipSuccess;
+    }
+    s.h_state_size.resize(nsize);
+    ok = ok && hipMemcpyAsync(s.h_state_size.data(), s.state_size, nsize * sizeof(int), hipMemcpyDeviceToHost, st) ==
+                   hipSuccess;
+    if (!ok || hipStreamSynchronize(st) != hipSuccess) return device_error("device error while reading the batches");
+  }
+  *out = h;
+  return FOLD_OK;
 }
 
 }  // namespace fold

@@ -27,7 +27,8 @@ FOLD_OK = 0
 ERRORS = {-1: "FOLD_E_INVALID", -2: "FOLD_E_OP", -3: "FOLD_E_ARITY", -4: "FOLD_E_CHILD",
           -5: "FOLD_E_INPUT", -6: "FOLD_E_CYCLE", -7: "FOLD_E_NOMEM", -8: "FOLD_E_DEVICE",
           -9: "FOLD_E_MISMATCH"}
-FOLD_E_INVALID, FOLD_E_MISMATCH = -1, -9
+FOLD_E_INVALID, FOLD_E_OP, FOLD_E_ARITY, FOLD_E_CHILD, FOLD_E_INPUT, FOLD_E_CYCLE = -1, -2, -3, -4, -5, -6
+FOLD_E_NOMEM, FOLD_E_DEVICE, FOLD_E_MISMATCH = -7, -8, -9
 FOLD_EMBED, FOLD_TREERNN, FOLD_TREELSTM, FOLD_LSTM, FOLD_PROJ = 0, 1, 2, 3, 4
 FOLD_F32, FOLD_BF16 = 0, 1
 GATES = {FOLD_EMBED: 0, FOLD_TREERNN: 1, FOLD_TREELSTM: 5, FOLD_LSTM: 4, FOLD_PROJ: 1}
@@ -60,6 +61,29 @@ class fold_sched_info(ctypes.Structure):
                 ("h_group_rows", POINTER(c_int32)), ("h_group_idx_off", POINTER(c_int32)),
                 ("group_child_base0", _I32P), ("group_child_base1", _I32P),
                 ("h_group_child_base0", POINTER(c_int32)), ("h_group_child_base1", POINTER(c_int32))]
+
+
+class fold_typed_op(ctypes.Structure):
+    _fields_ = [("num_inputs", c_int32), ("num_outputs", c_int32), ("in_type", POINTER(c_int32)),
+                ("out_type", POINTER(c_int32))]
+
+
+class fold_typed_batch(ctypes.Structure):
+    _fields_ = [("num_graphs", c_int32), ("num_nodes", c_int32), ("num_edges", c_int32), ("num_ops", c_int32),
+                ("num_types", c_int32), ("graph_ptr", c_void_p), ("node_op", c_void_p), ("in_ptr", c_void_p),
+                ("in_node", c_void_p), ("in_slot", c_void_p), ("ops", POINTER(fold_typed_op))]
+
+
+class fold_typed_sched_info(ctypes.Structure):
+    _fields_ = [("num_levels", c_int32), ("num_batches", c_int32), ("num_passes", c_int32),
+                ("num_items", c_int32), ("num_gather", c_int32), ("num_ops", c_int32), ("num_types", c_int32),
+                ("depth", _I32P), ("batch_depth", _I32P), ("batch_op", _I32P), ("batch_rows", _I32P),
+                ("batch_gather_off", _I32P), ("batch_item_begin", _I32P), ("item_node", _I32P),
+                ("gather", _I32P), ("pass_node", _I32P), ("pass_slot", _I32P), ("pass_depth", _I32P),
+                ("state_size", _I32P), ("edge_index", _I32P),
+                ("h_batch_depth", POINTER(c_int32)), ("h_batch_op", POINTER(c_int32)),
+                ("h_batch_rows", POINTER(c_int32)), ("h_batch_gather_off", POINTER(c_int32)),
+                ("h_state_size", POINTER(c_int32))]
 
 
 class fold_param_set(ctypes.Structure):
@@ -112,7 +136,8 @@ EXPORTS = ["fold_schedule", "fold_sched_get_info", "fold_sched_free", "fold_pack
            "fold_probe_mfma", "fold_probe_copy", "fold_graph_create", "fold_graph_launch",
            "fold_graph_num_nodes", "fold_graph_free", "fold_pack_update", "fold_loss_softmax_ce",
            "fold_loss_workspace_size", "fold_adam_step", "fold_forward_dropout", "fold_backward_dropout",
-           "fold_dropout_mask", "fold_forward_noalloc"]
+           "fold_dropout_mask", "fold_forward_noalloc", "fold_schedule_typed", "fold_typed_sched_get_info",
+           "fold_typed_sched_free"]
 
 _lib = None
 
@@ -155,6 +180,12 @@ def lib():
     L.fold_backward_dropout.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,
                                         c_void_p, c_void_p, POINTER(fold_grads), c_void_p, c_void_p, c_void_p,
                                         c_size_t, c_void_p]
+    L.fold_schedule_typed.restype = c_int32
+    L.fold_schedule_typed.argtypes = [POINTER(fold_typed_batch), c_void_p, POINTER(c_void_p)]
+    L.fold_typed_sched_get_info.restype = c_int32
+    L.fold_typed_sched_get_info.argtypes = [c_void_p, POINTER(fold_typed_sched_info)]
+    L.fold_typed_sched_free.restype = c_int32
+    L.fold_typed_sched_free.argtypes = [c_void_p]
     L.fold_forward_noalloc.restype = c_int32
     L.fold_forward_noalloc.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p, c_void_p]
     L.fold_dropout_mask.restype = c_int32
@@ -446,6 +477,57 @@ class Schedule:
             p = getattr(i, name)
             out[name] = _dev_copy_to_host(p, cnt) if p else np.zeros(0, np.int32)
         out["host"] = self.host_groups()
+        return out
+
+
+class TypedSchedule:
+    """fold_schedule_typed over CUDA int32 tensors (the paper's form: typed per-depth states, pass-throughs).
+    ops: list of (in_types, out_types)."""
+
+    def __init__(self, graph_ptr, node_op, in_ptr, in_node, in_slot, ops, num_types, stream=None):
+        self._keep = [graph_ptr, node_op, in_ptr, in_node, in_slot]
+        self._types = []
+        arr = (fold_typed_op * len(ops))()
+        for k, (ins, outs) in enumerate(ops):
+            a = (c_int32 * max(1, len(ins)))(*ins)
+            b = (c_int32 * max(1, len(outs)))(*outs)
+            self._types += [a, b]
+            arr[k] = fold_typed_op(len(ins), len(outs), a, b)
+        self._ops = arr
+        bt = fold_typed_batch(int(graph_ptr.numel()) - 1, int(node_op.numel()), int(in_node.numel()), len(ops),
+                              int(num_types), _ptr(graph_ptr), _ptr(node_op), _ptr(in_ptr), _ptr(in_node),
+                              _ptr(in_slot), arr)
+        h = c_void_p()
+        _check(lib().fold_schedule_typed(ctypes.byref(bt), _stream(stream), ctypes.byref(h)))
+        self.handle = h
+        self.info = fold_typed_sched_info()
+        _check(lib().fold_typed_sched_get_info(h, ctypes.byref(self.info)))
+        self.num_nodes, self.num_edges = int(node_op.numel()), int(in_node.numel())
+
+    def __del__(self):
+        if getattr(self, "handle", None) is not None and _lib is not None:
+            _lib.fold_typed_sched_free(self.handle)
+            self.handle = None
+
+    def arrays(self) -> dict:
+        i = self.info
+        D, T, nb, P, M, G = i.num_levels, i.num_types, i.num_batches, i.num_passes, i.num_items, i.num_gather
+
+        def dev(name, n):
+            p = getattr(i, name)
+            return _dev_copy_to_host(p, n) if (p and n) else np.zeros(0, np.int32)
+
+        def host(p, n):
+            return np.ctypeslib.as_array(p, shape=(n,)).copy() if n else np.zeros(0, np.int32)
+        out = dict(num_levels=D, num_batches=nb, num_passes=P, num_items=M, num_gather=G)
+        for name, n in (("depth", self.num_nodes), ("batch_depth", nb), ("batch_op", nb), ("batch_rows", nb),
+                        ("batch_gather_off", nb), ("batch_item_begin", nb), ("item_node", M), ("gather", G),
+                        ("pass_node", P), ("pass_slot", P), ("pass_depth", P), ("state_size", (D + 1) * T),
+                        ("edge_index", self.num_edges)):
+            out[name] = dev(name, n)
+        out["host"] = dict(batch_depth=host(i.h_batch_depth, nb), batch_op=host(i.h_batch_op, nb),
+                           batch_rows=host(i.h_batch_rows, nb), batch_gather_off=host(i.h_batch_gather_off, nb),
+                           state_size=host(i.h_state_size, (D + 1) * T))
         return out
 
 

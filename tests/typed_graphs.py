@@ -88,3 +88,44 @@ def random_typed_batch(rng, num_types, ops, n_graphs, max_nodes, const_frac=0.3)
         in_ptr[v + 1] = len(in_node)
     return (np.array(graph_ptr, np.int32), np.array(node_op, np.int32), in_ptr, np.array(in_node, np.int32),
             np.array(in_slot, np.int32))
+
+
+def tree_lstm_paper_form(w):
+    """A binary Tree-LSTM batch (leaves with a leaf-table row, internal nodes of arity 2) in the paper's typed
+    form: type 0 = int word id (the leaf-table row, a constant), type 1 = float state; operations 0 = embed
+    (int -> float), 1 = leaf Tree-LSTM (embedding -> h, c), 2 = internal Tree-LSTM (h_l, c_l, h_r, c_r -> h, c)
+    -- as in Section 3.5, where a word is TreeLSTM(Embedding(word), 0, 0).  Returns (graph_ptr, node_op,
+    in_ptr, in_node, in_slot), ops, num_types."""
+    ops = [([0], [1]), ([1], [1, 1]), ([1, 1, 1, 1], [1, 1])]
+    node_op, ins, graph_ptr = [], [], [0]
+    cp, ci, ni = w.child_ptr, w.child_idx, w.node_input
+    for g in range(w.num_graphs):
+        a, b = int(w.graph_ptr[g]), int(w.graph_ptr[g + 1])
+        local = {}
+        order = []
+
+        def add(op, inputs):
+            node_op.append(op)
+            ins.append(inputs)
+            return len(node_op) - 1
+
+        for v in range(a, b):  # generator graphs list children before parents
+            kids = [int(c) for c in ci[cp[v]:cp[v + 1]]]
+            if not kids:
+                tok = add(-1, [])
+                emb = add(0, [(tok, 0)])
+                local[v] = add(1, [(emb, 0)])
+            else:
+                l, r = local[kids[0]], local[kids[1]]
+                local[v] = add(2, [(l, 0), (l, 1), (r, 0), (r, 1)])
+            order.append(v)
+        graph_ptr.append(len(node_op))
+    in_ptr = np.zeros(len(node_op) + 1, np.int32)
+    in_node, in_slot = [], []
+    for v, lst in enumerate(ins):
+        for (u, k) in lst:
+            in_node.append(u)
+            in_slot.append(k)
+        in_ptr[v + 1] = len(in_node)
+    return ((np.array(graph_ptr, np.int32), np.array(node_op, np.int32), in_ptr, np.array(in_node, np.int32),
+             np.array(in_slot, np.int32)), ops, 2)
