@@ -263,15 +263,18 @@ def pass_work(w, host, table_grad: bool) -> dict:
 
 
 def pass_of(name: str, group: int, op: int):
-    """The level pass a profiled launch belongs to (None: set-up, roots)."""
+    """The level passes a profiled launch belongs to ([]: set-up, roots).  A level launch runs several
+    consecutive groups of one level (tagged with its first group and op = -1 - span); its time is shared
+    equally among them."""
     cls = class_of(name)
+    groups = [group] if op >= -1 else list(range(group, group - 1 - op))
     if group >= 0 and cls in ("cell_fwd", "embed_fwd"):
-        return ("fwd", group)
+        return [("fwd", g) for g in groups]
     if group >= 0 and cls in ("cell_bwd", "bwd_dx"):
-        return ("bwd", group)
+        return [("bwd", g) for g in groups]
     if group < 0 and op >= 0 and cls in ("wgrad", "wgrad_reduce", "bias_partial", "bias_reduce"):
-        return ("wgrad", op)
-    return None
+        return [("wgrad", op)]
+    return []
 
 
 def level_classes(work: dict, launches: list, steps: int, peak_tflops: float, hbm_gbs: float) -> dict:
@@ -282,11 +285,11 @@ def level_classes(work: dict, launches: list, steps: int, peak_tflops: float, hb
     meas = {}
     other = 0.0
     for name, group, op, ms in launches:
-        key = pass_of(name, group, op)
-        if key is None:
+        keys = pass_of(name, group, op)
+        if not keys:
             other += ms
-        else:
-            meas[key] = meas.get(key, 0.0) + ms / steps
+        for key in keys:
+            meas[key] = meas.get(key, 0.0) + ms / steps / len(keys)
     cls = {c: {"passes": 0, "ms_per_step": 0.0, "roofline_ms": 0.0, "flops": 0.0, "bytes": 0.0, "by_pass": {}}
            for c in ("wide", "gather", "narrow")}
     for key, (F, B) in work.items():
@@ -358,13 +361,18 @@ def table1(batches, steps: int, warmup: int, dtype: str = "f32") -> dict:
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / steps
 
+    from paper_1702_02181_amd import fold as F
     rows = []
     for B in batches:
         row = {"batch": B}
-        for mode in ("manual", "dynamic", "full"):
-            w = gen.table1(B, mode, dtype=dtype)
+        for mode in ("manual", "manual_level", "dynamic", "full"):
+            # manual: one launch per node position, as a static graph runs; manual_level: the same schedule with
+            # the independent node positions of a depth in shared launches (the library's default)
+            w = gen.table1(B, "manual" if mode == "manual_level" else mode, dtype=dtype)
+            prev = F.fold_level_launches(mode != "manual")
             dev = DeviceRun(w)
             graph = dev.make_graph(backward=False)
+            F.fold_level_launches(prev)
             ms = timed(graph.launch)
             host = dev.sched.host_groups()
             slots = [(host[f"group_child_base{k}"][g] >= 0)
@@ -375,8 +383,9 @@ def table1(batches, steps: int, warmup: int, dtype: str = "f32") -> dict:
             del graph, dev
         row["cost_ratio"] = round(row["dynamic"]["batch_ms"] / row["manual"]["batch_ms"], 3)
         rows.append(row)
-        print(f"[table1] batch {B}: manual {row['manual']['batch_ms']:.3f} ms, dynamic "
-              f"{row['dynamic']['batch_ms']:.3f} ms, full {row['full']['batch_ms']:.3f} ms", file=sys.stderr, flush=True)
+        print(f"[table1] batch {B}: manual {row['manual']['batch_ms']:.3f} ms (level launches "
+              f"{row['manual_level']['batch_ms']:.3f} ms), dynamic {row['dynamic']['batch_ms']:.3f} ms, full "
+              f"{row['full']['batch_ms']:.3f} ms", file=sys.stderr, flush=True)
     base = next((r["manual"]["tree_ms"] for r in rows if r["batch"] == 1), None)
     for r in rows:
         r["speedup_ratio"] = None if base is None else round(base / r["full"]["tree_ms"], 2)

@@ -529,6 +529,19 @@ int32_t fold_graph_launch(const fold_graph* graph, hipStream_t stream);
 int32_t fold_graph_num_nodes(const fold_graph* graph, int32_t* nodes); /* kernel nodes recorded */
 int32_t fold_graph_free(fold_graph* graph);
 
+/* ---- level launches --------------------------------------------------------
+ * The groups of one depth are independent, so by default the narrow groups of
+ * a level (up to four) run as one launch per kernel stage (one for their
+ * contractions, one for their K-split epilogues, one for their cell
+ * backwards, one for their dz . W^T), which removes the dependent launches of
+ * levels with several operations.  fold_level_launches(0) turns this off for
+ * every later call in the process (each group then launches alone, as a static
+ * graph of one batched operation per node would run); fold_level_launches(1)
+ * turns it back on.  Returns the previous setting (1 or 0).  Results are the
+ * same either way up to the order of the atomic additions of shared
+ * children. */
+int32_t fold_level_launches(int32_t on);
+
 /* ---- per-kernel timing (profiling aid) ----------------------------------
  * While enabled, every kernel the library launches is bracketed by a pair of
  * HIP events recorded on the launch stream, under a short kernel-class name

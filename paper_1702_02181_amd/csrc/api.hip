@@ -54,6 +54,7 @@ hipEvent_t prof_event() {
 
 namespace {
 thread_local bool g_capturing = false;  // launches are being recorded into a graph: no event pairs
+std::atomic<bool> g_level_launches{true};  // narrow groups of one level in one launch
 }
 
 void set_capturing(bool on) { g_capturing = on; }
@@ -183,14 +184,44 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
   auto al = [](size_t x) { return (x + 255) / 256 * 256; };
   w.gates_off = 0;
   w.gates_bytes = al(N * w.gstride * sizeof(float));
-  size_t zp = 0;
+  // the forward's launches and the partial sums each K-split group needs (a level launch's groups side by side)
+  size_t zp = 0, run = 0;
+  int nb = 0, in_batch = 0, prev_level = -1;
+  w.batch.assign(s.num_groups, -1);
+  w.zoff.assign(s.num_groups, 0);
+  w.zneed.assign(s.num_groups, 0);
   for (int g = 0; g < s.num_groups; ++g) {
     const fold_op& op = s.ops[s.h_op[g]];
-    if (op.kind == FOLD_EMBED || op.param_set >= (int)p.sets.size()) continue;
+    const bool new_level = s.h_level[g] != prev_level;
+    prev_level = s.h_level[g];
+    if (new_level || in_batch == kMaxMerge) {
+      if (in_batch > 0) ++nb;
+      in_batch = 0;
+      run = 0;
+    }
+    if (op.kind == FOLD_EMBED || op.param_set >= (int)p.sets.size()) {
+      if (in_batch > 0) ++nb;
+      in_batch = 0;
+      run = 0;
+      continue;
+    }
     const PackedSet& ps = p.sets[op.param_set];
     const FwdPlan pl = fwd_plan(s.h_rows[g], p.HP, op.has_input ? ps.INP : 0, op.arity,
                                 p.dtype == FOLD_BF16 ? 2 : 4, true);
-    if (pl.ksplit > 1) zp = std::max(zp, (size_t)pl.ksplit * s.h_rows[g] * ps.G * p.HP);
+    const size_t need = pl.ksplit > 1 ? (size_t)pl.ksplit * s.h_rows[g] * ps.G * p.HP : 0;
+    w.zneed[g] = need;
+    if (pl.wide) {
+      if (in_batch > 0) ++nb;
+      in_batch = 0;
+      run = 0;
+      zp = std::max(zp, need);
+      continue;
+    }
+    w.batch[g] = nb;
+    w.zoff[g] = run;
+    run += need;
+    ++in_batch;
+    zp = std::max(zp, run);
   }
   w.zpart_off = w.gates_bytes;
   w.zpart_bytes = al(zp * sizeof(float));
@@ -350,11 +381,32 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
   }
   const int tw = table_width(s, p);
   const int tld = row_ld(tw);
+  // Consecutive narrow groups of one level run as one launch (level launches); a wide group or an
+  // embedding launches alone.  Merged launches are tagged with their first group and op = -1 - n.
+  int pend_g0 = -1, pend_batch = -1;
+  std::vector<int> pend_kind;
+  std::vector<FwdArgs> pend_args;
+  auto flush = [&]() {
+    const int n = (int)pend_args.size();
+    if (n == 1) {
+      prof_tag(pend_g0, s.h_op[pend_g0]);
+      launch_cell_fwd(p.dtype, pend_kind[0], pend_args[0], st);
+    } else if (n > 1) {
+      prof_tag(pend_g0, -1 - n);
+      launch_level_fwd(p.dtype, pend_kind.data(), pend_args.data(), n, st);
+    }
+    pend_kind.clear();
+    pend_args.clear();
+    pend_g0 = -1;
+  };
   for (int g = 0; g < s.num_groups; ++g) {
     const fold_op& op = s.ops[s.h_op[g]];
     const PackedSet& ps = p.sets[op.param_set];
-    prof_tag(g, s.h_op[g]);
+    if (L.batch[g] != pend_batch) flush();
+    pend_batch = L.batch[g];
     if (op.kind == FOLD_EMBED) {
+      flush();
+      prof_tag(g, s.h_op[g]);
       launch_embed_fwd(p.dtype, s.h_rows[g], s.h_row_begin[g], p.H, p.ld, tld, table, s.input_idx, h_pool, c_pool, st);
       continue;
     }
@@ -393,8 +445,35 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
       a.Kf = ps.INP;
       a.bias = ps.bias_leaf;
     }
-    launch_cell_fwd(p.dtype, kind, a, st);
+    if (L.batch[g] < 0 || !g_level_launches.load(std::memory_order_relaxed)) {  // launched alone
+      flush();
+      prof_tag(g, s.h_op[g]);
+      launch_cell_fwd(p.dtype, kind, a, st);
+      continue;
+    }
+    // a level launch's groups run at once: each takes its own part of the partial sums
+    if (zpart && !zpart_direct) {
+      a.zpart = zpart + L.zoff[g];
+    } else if (zpart_direct) {
+      // the fixed scratch: parts in proportion to their needs when the level's needs exceed it
+      size_t total = 0;
+      for (int h = g; h >= 0 && L.batch[h] == L.batch[g]; --h) total = std::max(total, L.zoff[h] + L.zneed[h]);
+      for (int h = g + 1; h < s.num_groups && L.batch[h] == L.batch[g]; ++h)
+        total = std::max(total, L.zoff[h] + L.zneed[h]);
+      if (total > zcap) {
+        a.zpart = zpart + (size_t)((double)L.zoff[g] * zcap / total);
+        a.zcap = (size_t)((double)L.zneed[g] * zcap / total);
+        if (a.zcap == 0) a.zcap = 1;  // a nonzero cap: the split is clamped to what fits (none)
+      } else {
+        a.zpart = zpart + L.zoff[g];
+        a.zcap = std::max<size_t>(L.zneed[g], 1);
+      }
+    }
+    if (pend_args.empty()) pend_g0 = g;
+    pend_kind.push_back(kind);
+    pend_args.push_back(a);
   }
+  flush();
   prof_tag(-1, -1);
   if (roots_out) launch_roots(p.dtype, s.R, p.ld, s.root_pos, h_pool, roots_out, st);
   (void)table_rows;
@@ -420,65 +499,114 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
   float* d_table = grads ? grads->d_leaf_table : nullptr;
 
   launch_bwd_init(s.N, s.R, p.ld, dh_nodes, dh_roots, s.root_pos, dh, dc, st);
-  for (int g = s.num_groups - 1; g >= 0; --g) {
-    const fold_op& op = s.ops[s.h_op[g]];
-    const PackedSet& ps = p.sets[op.param_set];
-    prof_tag(g, s.h_op[g]);
-    BwdCellArgs b;
-    b.rows = s.h_rows[g];
-    b.row_begin = s.h_row_begin[g];
-    b.idx_off = s.h_idx_off[g];
-    b.arity = op.arity;
-    b.H = p.H;
-    b.HP = p.HP;
-    b.ld = p.ld;
-    b.gstride = L.gstride;
-    b.c_pool = c_pool;
-    b.gates = gates;
-    b.u_mask = u_mask;
-    b.dh = dh;
-    b.dc = dc;
-    b.child_pos = s.child_pos;
-    b.input_idx = s.input_idx;
-    b.child_one = s.child_one;
-    b.d_table = d_table;
-    b.tld = tld;
-    b.dz_bf16 = p.dtype == FOLD_BF16;
-    const bool leaf = is_tree_lstm_leaf(op);
-    launch_cell_bwd(leaf ? kTreeLstmLeaf : op.kind, b, st);
-    if (op.kind == FOLD_EMBED) continue;
-    DxArgs d;
-    d.rows = b.rows;
-    d.row_begin = b.row_begin;
-    d.idx_off = b.idx_off;
-    d.arity = op.arity;
-    d.H = p.H;
-    d.HP = p.HP;
-    d.ld = p.ld;
-    d.gstride = L.gstride;
-    d.Kb = (leaf ? gates_of(kTreeLstmLeaf) : ps.G) * p.HP;
-    d.dz = gates;
-    d.dh = dh;
-    d.child_pos = s.child_pos;
-    d.d_table = d_table;
-    d.input_idx = s.input_idx;
-    d.in_dim = ps.in_dim;
-    d.tld = tld;
-    d.child_one = s.child_one;
-    d.can_split = 1;
-    d.zero = p.zero;
-    if (op.arity > 0) {
-      d.mode = 0;
-      d.Nb = op.arity * p.HP;
-      d.Wb = ps.Wb_rec;
-      launch_bwd_dx(p.dtype, d, st);
+  // Level by level from the top.  The groups of a level are independent (their children are at lower
+  // levels), so all their cell backwards run first and then all their dz . W^T; narrow ones of a level run
+  // as level launches (tagged with the first group of the span and op = -1 - span).
+  for (int g_hi = s.num_groups; g_hi > 0;) {
+    int g_lo = g_hi - 1;
+    while (g_lo > 0 && s.h_level[g_lo - 1] == s.h_level[g_hi - 1]) --g_lo;
+    std::vector<int> ckind;
+    std::vector<BwdCellArgs> cargs;
+    std::vector<DxArgs> dargs;
+    std::vector<int> dgroup;
+    for (int g = g_lo; g < g_hi; ++g) {
+      const fold_op& op = s.ops[s.h_op[g]];
+      const PackedSet& ps = p.sets[op.param_set];
+      BwdCellArgs b;
+      b.rows = s.h_rows[g];
+      b.row_begin = s.h_row_begin[g];
+      b.idx_off = s.h_idx_off[g];
+      b.arity = op.arity;
+      b.H = p.H;
+      b.HP = p.HP;
+      b.ld = p.ld;
+      b.gstride = L.gstride;
+      b.c_pool = c_pool;
+      b.gates = gates;
+      b.u_mask = u_mask;
+      b.dh = dh;
+      b.dc = dc;
+      b.child_pos = s.child_pos;
+      b.input_idx = s.input_idx;
+      b.child_one = s.child_one;
+      b.d_table = d_table;
+      b.tld = tld;
+      b.dz_bf16 = p.dtype == FOLD_BF16;
+      const bool leaf = is_tree_lstm_leaf(op);
+      ckind.push_back(leaf ? kTreeLstmLeaf : op.kind);
+      cargs.push_back(b);
+      if (op.kind == FOLD_EMBED) continue;
+      DxArgs d;
+      d.rows = b.rows;
+      d.row_begin = b.row_begin;
+      d.idx_off = b.idx_off;
+      d.arity = op.arity;
+      d.H = p.H;
+      d.HP = p.HP;
+      d.ld = p.ld;
+      d.gstride = L.gstride;
+      d.Kb = (leaf ? gates_of(kTreeLstmLeaf) : ps.G) * p.HP;
+      d.dz = gates;
+      d.dh = dh;
+      d.child_pos = s.child_pos;
+      d.d_table = d_table;
+      d.input_idx = s.input_idx;
+      d.in_dim = ps.in_dim;
+      d.tld = tld;
+      d.child_one = s.child_one;
+      d.can_split = 1;
+      d.zero = p.zero;
+      if (op.arity > 0) {
+        d.mode = 0;
+        d.Nb = op.arity * p.HP;
+        d.Wb = ps.Wb_rec;
+        dargs.push_back(d);
+        dgroup.push_back(g);
+      }
+      if (op.has_input && d_table && ps.INP > 0) {
+        d.mode = 1;
+        d.Nb = ps.INP;
+        d.Wb = leaf ? ps.Wb_in_leaf : ps.Wb_in;
+        dargs.push_back(d);
+        dgroup.push_back(g);
+      }
     }
-    if (op.has_input && d_table && ps.INP > 0) {
-      d.mode = 1;
-      d.Nb = ps.INP;
-      d.Wb = leaf ? ps.Wb_in_leaf : ps.Wb_in;
-      launch_bwd_dx(p.dtype, d, st);
+    // cell backwards: the level's groups in chunks of at most kMaxMerge
+    const int merge = g_level_launches.load(std::memory_order_relaxed) ? kMaxMerge : 1;
+    for (int k0 = 0; k0 < (int)cargs.size(); k0 += merge) {
+      const int n = std::min<int>(merge, (int)cargs.size() - k0);
+      if (n == 1) {
+        prof_tag(g_lo + k0, s.h_op[g_lo + k0]);
+        launch_cell_bwd(ckind[k0], cargs[k0], st);
+      } else {
+        prof_tag(g_lo + k0, -1 - n);
+        launch_level_cbwd(ckind.data() + k0, cargs.data() + k0, n, st);
+      }
     }
+    // dz . W^T: wide calls alone, narrow ones merged
+    std::vector<DxArgs> nargs;
+    std::vector<int> ngroup;
+    for (size_t k = 0; k < dargs.size(); ++k) {
+      if (bwd_dx_is_narrow(p.dtype, dargs[k])) {
+        nargs.push_back(dargs[k]);
+        ngroup.push_back(dgroup[k]);
+      } else {
+        prof_tag(dgroup[k], s.h_op[dgroup[k]]);
+        launch_bwd_dx(p.dtype, dargs[k], st);
+      }
+    }
+    for (int k0 = 0; k0 < (int)nargs.size(); k0 += merge) {
+      const int n = std::min<int>(merge, (int)nargs.size() - k0);
+      if (n == 1) {
+        prof_tag(ngroup[k0], s.h_op[ngroup[k0]]);
+        launch_bwd_dx(p.dtype, nargs[k0], st);
+      } else {
+        const int span = ngroup[k0 + n - 1] - ngroup[k0] + 1;
+        prof_tag(ngroup[k0], -1 - span);
+        launch_level_dx(p.dtype, nargs.data() + k0, n, st);
+      }
+    }
+    g_hi = g_lo;
   }
   // weight gradients: one deferred contraction per (op, input segment)
   if (grads) {
@@ -630,6 +758,10 @@ int32_t fold_probe_copy(void* dst, const void* src, size_t bytes, hipStream_t st
     return fail(FOLD_E_INVALID, "fold_probe_copy: NULL, unaligned or non-multiple-of-16 buffers");
   return probe_copy(dst, src, bytes, st, gbs);
   FOLD_GUARD_END
+}
+
+int32_t fold_level_launches(int32_t on) {
+  return fold::g_level_launches.exchange(on != 0) ? 1 : 0;
 }
 
 int32_t fold_profile_enable(int32_t on) {

@@ -180,15 +180,18 @@ __device__ __forceinline__ void pad_out(const FwdArgs& a, int row, int j) {
 // SPLIT: the K loop is cut into gridDim.z slices; each workgroup writes its partial z (no bias) to
 // a.zpart[slice][row][g * HP + j] and k_cell_epi finishes the cell.  Used for narrow levels, whose
 // few row tiles would otherwise leave most compute units idle for a whole K loop.
+// The body of the narrow forward for workgroup L of its grid.  LDS comes in as separate arrays (two stages of A,
+// BM rows, and of B, G gate blocks of 32 units, 128 bytes of K each; the source row of every tile row per input
+// segment, -1: zero row): as distinct objects the compiler sees that the loads in flight into one stage buffer
+// do not touch the other, and adds no wait between them.
 template <typename T, int KIND, int MT, bool SPLIT>
-__global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
+__device__ __forceinline__ void cell_fwd_body(const FwdArgs a, unsigned L, char* A0, char* A1, char* B0, char* B1,
+                                              int (*srow)[4 * 32 * MT]) {
   constexpr int G = Gates<KIND>::G;
   constexpr int BM = 4 * 32 * MT;  // four waves stacked along the rows
   constexpr int BN = G * 32;       // G gate blocks of 32 units
   constexpr int PA = BM / 32, PB = BN / 32;  // direct-load instructions per wave and stage
   constexpr int BK = 128 / sizeof(T);
-  __shared__ __attribute__((aligned(16))) char A0[BM * 128], A1[BM * 128], B0[BN * 128], B1[BN * 128];
-  __shared__ int srow[3][BM];  // source row of every tile row, per input segment (-1: zero row)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
   // co-locate on one XCD the workgroups that share the larger operand: the gathered rows of a row tile
@@ -196,12 +199,12 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
   const int R = (a.rows + BM - 1) / BM, UB = a.HP / 32;
   int tx, ty, ub, rt, kz;
   if (a.map == kMapRows) {
-    if (!xcd_tile(UB * a.ksplit, R, tx, ty)) return;
+    if (!xcd_tile_at(L, UB * a.ksplit, R, tx, ty)) return;
     rt = ty;
     ub = tx % UB;
     kz = tx / UB;
   } else {
-    if (!xcd_tile(R * a.ksplit, UB, tx, ty)) return;
+    if (!xcd_tile_at(L, R * a.ksplit, UB, tx, ty)) return;
     ub = ty;
     rt = tx % R;
     kz = tx / R;
@@ -293,6 +296,14 @@ __global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
       cell_out<T, KIND>(a, row, j, z, cl, cr);
     }
   }
+}
+
+template <typename T, int KIND, int MT, bool SPLIT>
+__global__ __launch_bounds__(kThreads) void k_cell_fwd(FwdArgs a) {
+  constexpr int BM = 4 * 32 * MT, BN = Gates<KIND>::G * 32;
+  __shared__ __attribute__((aligned(16))) char A0[BM * 128], A1[BM * 128], B0[BN * 128], B1[BN * 128];
+  __shared__ int srow[3][BM];
+  cell_fwd_body<T, KIND, MT, SPLIT>(a, blockIdx.x, A0, A1, B0, B1, srow);
 }
 
 // ---------------------------------------------------------------- forward, wide levels
@@ -438,9 +449,8 @@ __global__ __launch_bounds__(wide::kThreads) void k_cell_fwd_w(FwdArgs a) {
 
 // finish a K-split level: sum the slices' partial z, add the bias, apply the cell
 template <typename T, int KIND>
-__global__ void k_cell_epi(FwdArgs a, int nsplit) {
+__device__ __forceinline__ void cell_epi_body(const FwdArgs a, int row, int nsplit) {
   constexpr int G = Gates<KIND>::G;
-  const int row = blockIdx.x;
   const int zs = G * a.HP;
   const int p0 = a.arity >= 1 ? fwd_child(a, row, 0) : -1;
   const int p1 = a.arity >= 2 ? fwd_child(a, row, 1) : -1;
@@ -473,6 +483,11 @@ __global__ void k_cell_epi(FwdArgs a, int nsplit) {
     }
     cell_out<T, KIND>(a, row, j, z, c0r[j], c1r[j]);
   }
+}
+
+template <typename T, int KIND>
+__global__ void k_cell_epi(FwdArgs a, int nsplit) {
+  cell_epi_body<T, KIND>(a, blockIdx.x, nsplit);
 }
 
 template <typename T>
@@ -523,10 +538,8 @@ __global__ void k_bwd_roots(int ld, const float* dh_roots, const int* root_pos, 
 // slots of the row, the matrix-core operand of dz . W^T and of the weight gradients; the row is first
 // read completely, the bf16 values are staged in LDS (dynamic, G*HP halves) and then written out.
 template <int KIND, bool BF>
-__global__ void k_cell_bwd(BwdCellArgs a) {
+__device__ __forceinline__ void cell_bwd_body(const BwdCellArgs a, int row, uint16_t* sdz) {
   constexpr int G = Gates<KIND>::G;
-  extern __shared__ __attribute__((aligned(16))) uint16_t sdz[];
-  const int row = blockIdx.x;
   const size_t p = (size_t)(a.row_begin + row);
   float* gb = a.gates + p * a.gstride;
   auto gate = [&](int g, int j) -> float { return gb[g * a.HP + j]; };  // saved activations (fp32)
@@ -619,32 +632,39 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
   }
 }
 
+template <int KIND, bool BF>
+__global__ void k_cell_bwd(BwdCellArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t sdz[];
+  cell_bwd_body<KIND, BF>(a, blockIdx.x, sdz);
+}
+
 // ---------------------------------------------------------------- backward, dz . W^T
 
 
 // dz . W^T for one tile of 128 * MT rows x 128 columns of the children's (or the input's) gradient:
 // dz rows (fp32, or bf16 at the start of each row for bf16 parameters) and the packed W^T rows are
 // loaded straight into LDS.
+// The body of the narrow dz . W^T for workgroup L of its grid; LDS as separate arrays (see cell_fwd_body):
+// tgt = per tile row child k's pool row (mode 0) or the leaf-table row (mode 1), sgl = the child has one parent
+// edge (plain read-add-write)
 template <typename T, int MT, bool SPLIT>
-__global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
+__device__ __forceinline__ void bwd_dx2_body(const DxArgs a, unsigned L, char* A0, char* A1, char* B0, char* B1,
+                                             int (*tgt)[4 * 32 * MT], char (*sgl)[4 * 32 * MT]) {
   constexpr int TN = 4;
   constexpr int BM = 4 * 32 * MT, BN = 32 * TN;  // four waves of 32*MT rows x 128 columns
   constexpr int PA = BM / 32, PB = BN / 32;
-  __shared__ __attribute__((aligned(16))) char A0[BM * 128], A1[BM * 128], B0[BN * 128], B1[BN * 128];
-  __shared__ int tgt[2][BM];  // per tile row: child k's pool row (mode 0) or the leaf-table row (mode 1)
-  __shared__ char sgl[2][BM];  // the child has one parent edge: plain read-add-write
   const int lane = threadIdx.x & 63, wave = wave_id();
   // co-locate the workgroups that share the larger operand (a row tile's dz rows or a column tile's
   // weight slice) on one XCD
   const int R = (a.rows + BM - 1) / BM, NT = (a.Nb + BN - 1) / BN;
   int tx, ty, nt, rt, kz;
   if (a.map == kMapRows) {
-    if (!xcd_tile(NT * a.ksplit, R, tx, ty)) return;
+    if (!xcd_tile_at(L, NT * a.ksplit, R, tx, ty)) return;
     rt = ty;
     nt = tx % NT;
     kz = tx / NT;
   } else {
-    if (!xcd_tile(R * a.ksplit, NT, tx, ty)) return;
+    if (!xcd_tile_at(L, R * a.ksplit, NT, tx, ty)) return;
     nt = ty;
     rt = tx % R;
     kz = tx / R;
@@ -729,6 +749,15 @@ __global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
       }
     }
   }
+}
+
+template <typename T, int MT, bool SPLIT>
+__global__ __launch_bounds__(kThreads) void k_bwd_dx2(DxArgs a) {
+  constexpr int BM = 4 * 32 * MT, BN = 128;
+  __shared__ __attribute__((aligned(16))) char A0[BM * 128], A1[BM * 128], B0[BN * 128], B1[BN * 128];
+  __shared__ int tgt[2][BM];
+  __shared__ char sgl[2][BM];
+  bwd_dx2_body<T, MT, SPLIT>(a, blockIdx.x, A0, A1, B0, B1, tgt, sgl);
 }
 
 // dz . W^T on wide levels: 256 rows x 256 columns per workgroup of 8 waves (each 64 x 128), 64-byte K
@@ -835,6 +864,117 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
   }
 }
 
+
+// ---------------------------------------------------------------- several groups of one level, one launch
+// The groups of one depth are independent (each reads only rows of lower depths), so the narrow groups of a
+// level can run as one launch: its grid is the groups' grids back to back (each a multiple of 8 workgroups,
+// which keeps every group's XCD order) and each workgroup runs the body of its group's kernel variant.  On
+// levels of several operations this replaces one dependent launch per group by one per level.
+
+template <typename FA>
+struct Merged {
+  int n;
+  int begin[kMaxMerge + 1];  // first workgroup (or row) of each part; begin[n] = total
+  int variant[kMaxMerge];
+  FA a[kMaxMerge];
+};
+
+__device__ __forceinline__ int merged_part(const int* begin, int n, int bid) {
+  int i = 0;
+  while (i + 1 < n && bid >= begin[i + 1]) ++i;
+  return i;
+}
+
+// variant = 2 * kind + (K split); the LDS arrays are sized for the widest tile (5 gate blocks)
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_level_fwd(Merged<FwdArgs> m) {
+  constexpr int BM = 128, BN = 5 * 32;
+  __shared__ __attribute__((aligned(16))) char A0[BM * 128], A1[BM * 128], B0[BN * 128], B1[BN * 128];
+  __shared__ int srow[3][BM];
+  const int i = merged_part(m.begin, m.n, blockIdx.x);
+  const unsigned bid = blockIdx.x - (unsigned)m.begin[i];
+  const FwdArgs a = m.a[i];  // by value: the bodies then read it as values, not through a pointer
+  switch (m.variant[i]) {
+#define FOLD_V(K)                                                                      \
+  case 2 * K: cell_fwd_body<T, K, 1, false>(a, bid, A0, A1, B0, B1, srow); break;     \
+  case 2 * K + 1: cell_fwd_body<T, K, 1, true>(a, bid, A0, A1, B0, B1, srow); break;
+    FOLD_V(FOLD_TREERNN)
+    FOLD_V(FOLD_TREELSTM)
+    FOLD_V(FOLD_LSTM)
+    FOLD_V(FOLD_PROJ)
+    FOLD_V(kTreeLstmLeaf)
+#undef FOLD_V
+    default: break;
+  }
+}
+
+// K-split epilogues of a level: one workgroup per row, parts in rows; variant = kind
+template <typename T>
+__global__ void k_level_epi(Merged<FwdArgs> m) {
+  const int i = merged_part(m.begin, m.n, blockIdx.x);
+  const int row = blockIdx.x - m.begin[i];
+  const FwdArgs a = m.a[i];
+  switch (m.variant[i]) {
+    case FOLD_TREERNN: cell_epi_body<T, FOLD_TREERNN>(a, row, a.ksplit); break;
+    case FOLD_TREELSTM: cell_epi_body<T, FOLD_TREELSTM>(a, row, a.ksplit); break;
+    case FOLD_LSTM: cell_epi_body<T, FOLD_LSTM>(a, row, a.ksplit); break;
+    case FOLD_PROJ: cell_epi_body<T, FOLD_PROJ>(a, row, a.ksplit); break;
+    case kTreeLstmLeaf: cell_epi_body<T, kTreeLstmLeaf>(a, row, a.ksplit); break;
+    default: break;
+  }
+}
+
+// cell backward of a level: one workgroup per row; variant = kind (the embedding writes no dz)
+template <bool BF>
+__global__ void k_level_cbwd(Merged<BwdCellArgs> m) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t sdz[];
+  const int i = merged_part(m.begin, m.n, blockIdx.x);
+  const int row = blockIdx.x - m.begin[i];
+  const BwdCellArgs a = m.a[i];
+  switch (m.variant[i]) {
+    case FOLD_EMBED: cell_bwd_body<FOLD_EMBED, false>(a, row, sdz); break;
+    case FOLD_TREERNN: cell_bwd_body<FOLD_TREERNN, BF>(a, row, sdz); break;
+    case FOLD_TREELSTM: cell_bwd_body<FOLD_TREELSTM, BF>(a, row, sdz); break;
+    case FOLD_LSTM: cell_bwd_body<FOLD_LSTM, BF>(a, row, sdz); break;
+    case FOLD_PROJ: cell_bwd_body<FOLD_PROJ, BF>(a, row, sdz); break;
+    case kTreeLstmLeaf: cell_bwd_body<kTreeLstmLeaf, BF>(a, row, sdz); break;
+    default: break;
+  }
+}
+
+// dz . W^T of a level; variant = 2 * mt + (K split), mt <= MTMAX (the LDS is sized for MTMAX)
+template <typename T, int MTMAX>
+__global__ __launch_bounds__(kThreads) void k_level_dx(Merged<DxArgs> m) {
+  constexpr int BM = 4 * 32 * MTMAX, BN = 128;
+  __shared__ __attribute__((aligned(16))) char A0[BM * 128], A1[BM * 128], B0[BN * 128], B1[BN * 128];
+  __shared__ int tgt[2][BM];
+  __shared__ char sgl[2][BM];
+  const int i = merged_part(m.begin, m.n, blockIdx.x);
+  const unsigned bid = blockIdx.x - (unsigned)m.begin[i];
+  const DxArgs a = m.a[i];
+  // a part with mt = 1 uses the first 128 rows of every row array (same strides for A and B)
+  switch (m.variant[i]) {
+    case 2:
+      bwd_dx2_body<T, 1, false>(a, bid, A0, A1, B0, B1, reinterpret_cast<int(*)[128]>(&tgt[0][0]),
+                                reinterpret_cast<char(*)[128]>(&sgl[0][0]));
+      break;
+    case 3:
+      bwd_dx2_body<T, 1, true>(a, bid, A0, A1, B0, B1, reinterpret_cast<int(*)[128]>(&tgt[0][0]),
+                               reinterpret_cast<char(*)[128]>(&sgl[0][0]));
+      break;
+    case 4:
+      if constexpr (MTMAX >= 2)
+        bwd_dx2_body<T, 2, false>(a, bid, A0, A1, B0, B1, reinterpret_cast<int(*)[4 * 32 * 2]>(&tgt[0][0]),
+                                  reinterpret_cast<char(*)[4 * 32 * 2]>(&sgl[0][0]));
+      break;
+    case 5:
+      if constexpr (MTMAX >= 2)
+        bwd_dx2_body<T, 2, true>(a, bid, A0, A1, B0, B1, reinterpret_cast<int(*)[4 * 32 * 2]>(&tgt[0][0]),
+                                 reinterpret_cast<char(*)[4 * 32 * 2]>(&sgl[0][0]));
+      break;
+    default: break;
+  }
+}
 
 template <typename T, int KIND>
 void cell_fwd_kind(const FwdArgs& a0, hipStream_t st) {
@@ -994,6 +1134,116 @@ void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
     else { if (split) FOLD_DX(float, 1, true); else FOLD_DX(float, 1, false); }
   }
 #undef FOLD_DX
+}
+
+// ---------------------------------------------------------------- level launches (host)
+
+void launch_level_fwd(int dtype, const int* kinds, const FwdArgs* args, int n, hipStream_t st) {
+  Merged<FwdArgs> m{};
+  Merged<FwdArgs> e{};  // the K-split parts' epilogues
+  m.n = 0;
+  e.n = 0;
+  int total = 0, erows = 0, hp = 0;
+  for (int k = 0; k < n; ++k) {
+    FwdArgs a = args[k];
+    if (a.rows <= 0) continue;
+    const int esize = dtype == FOLD_BF16 ? 2 : 4;
+    const FwdPlan pl = fwd_plan(a.rows, a.HP, a.has_input ? a.INP : 0, a.arity, esize, a.zpart != nullptr);
+    const int G = gates_of(kinds[k]);
+    a.ksplit = pl.ksplit;
+    if (a.ksplit > 1 && a.zcap > 0) {
+      const size_t fit = a.zcap / ((size_t)a.rows * G * a.HP);
+      a.ksplit = (int)std::min<size_t>((size_t)a.ksplit, fit);
+      if (a.ksplit < 2) a.ksplit = 1;
+    }
+    const int R = (int)cdiv(a.rows, 128), UB = a.HP / 32;
+    a.map = a.rows >= G * a.HP ? kMapRows : kMapCols;
+    const int grid = a.map == kMapRows ? xcd_grid(UB * a.ksplit, R) : xcd_grid(R * a.ksplit, UB);
+    m.begin[m.n] = total;
+    m.variant[m.n] = 2 * kinds[k] + (a.ksplit > 1 ? 1 : 0);
+    m.a[m.n++] = a;
+    total += grid;
+    if (a.ksplit > 1) {
+      e.begin[e.n] = erows;
+      e.variant[e.n] = kinds[k];
+      e.a[e.n++] = a;
+      erows += a.rows;
+    }
+    hp = a.HP;
+  }
+  if (m.n == 0) return;
+  m.begin[m.n] = total;
+  e.begin[e.n] = erows;
+  ProfScope prof(dtype == FOLD_BF16 ? "cell_fwd.level.bf16" : "cell_fwd.level.f32", st);
+  if (dtype == FOLD_BF16) {
+    hipLaunchKernelGGL(k_level_fwd<uint16_t>, dim3(total), dim3(kThreads), 0, st, m);
+    if (e.n) hipLaunchKernelGGL(k_level_epi<uint16_t>, dim3(erows), dim3(std::min(hp, 1024)), 0, st, e);
+  } else {
+    hipLaunchKernelGGL(k_level_fwd<float>, dim3(total), dim3(kThreads), 0, st, m);
+    if (e.n) hipLaunchKernelGGL(k_level_epi<float>, dim3(erows), dim3(std::min(hp, 1024)), 0, st, e);
+  }
+}
+
+void launch_level_cbwd(const int* kinds, const BwdCellArgs* args, int n, hipStream_t st) {
+  Merged<BwdCellArgs> m{};
+  m.n = 0;
+  int total = 0, hp = 0;
+  bool bf = false;
+  size_t lds = 0;
+  for (int k = 0; k < n; ++k) {
+    if (args[k].rows <= 0) continue;
+    m.begin[m.n] = total;
+    m.variant[m.n] = kinds[k];
+    m.a[m.n++] = args[k];
+    total += args[k].rows;
+    hp = args[k].HP;
+    if (kinds[k] != FOLD_EMBED && args[k].dz_bf16) {
+      bf = true;
+      lds = std::max(lds, (size_t)gates_of(kinds[k]) * args[k].HP * sizeof(uint16_t));
+    }
+  }
+  if (m.n == 0) return;
+  m.begin[m.n] = total;
+  ProfScope prof("cell_bwd.level", st);
+  if (bf)
+    hipLaunchKernelGGL(k_level_cbwd<true>, dim3(total), dim3(std::min(hp, 1024)), lds, st, m);
+  else
+    hipLaunchKernelGGL(k_level_cbwd<false>, dim3(total), dim3(std::min(hp, 1024)), 0, st, m);
+}
+
+bool bwd_dx_is_narrow(int dtype, const DxArgs& a) {
+  if (a.rows <= 0 || a.Nb <= 0) return false;
+  return !dx_plan(a.rows, a.Nb, a.Kb, dtype == FOLD_BF16 ? 2 : 4, a.can_split != 0).wide;
+}
+
+void launch_level_dx(int dtype, const DxArgs* args, int n, hipStream_t st) {
+  Merged<DxArgs> m{};
+  m.n = 0;
+  int total = 0, mtmax = 1;
+  for (int k = 0; k < n; ++k) {
+    DxArgs a = args[k];
+    if (a.rows <= 0 || a.Nb <= 0) continue;
+    const DxPlan pl = dx_plan(a.rows, a.Nb, a.Kb, dtype == FOLD_BF16 ? 2 : 4, a.can_split != 0);
+    a.ksplit = pl.ksplit;
+    const int R = (int)cdiv(a.rows, 128 * pl.mt), NT = (int)cdiv(a.Nb, 128);
+    a.map = a.rows >= a.Nb ? kMapRows : kMapCols;
+    const int grid = a.map == kMapRows ? xcd_grid(NT * pl.ksplit, R) : xcd_grid(R * pl.ksplit, NT);
+    m.begin[m.n] = total;
+    m.variant[m.n] = 2 * pl.mt + (pl.ksplit > 1 ? 1 : 0);
+    m.a[m.n++] = a;
+    total += grid;
+    mtmax = std::max(mtmax, pl.mt);
+  }
+  if (m.n == 0) return;
+  m.begin[m.n] = total;
+  ProfScope prof(dtype == FOLD_BF16 ? "bwd_dx.level.bf16" : "bwd_dx.level.f32", st);
+#define FOLD_LDX(T_, M_) hipLaunchKernelGGL((k_level_dx<T_, M_>), dim3(total), dim3(kThreads), 0, st, m)
+  if (dtype == FOLD_BF16) {
+    if (mtmax == 2) FOLD_LDX(uint16_t, 2); else FOLD_LDX(uint16_t, 1);
+  } else {
+    if (mtmax == 2) FOLD_LDX(float, 2); else FOLD_LDX(float, 1);
+  }
+#undef FOLD_LDX
 }
 
 }  // namespace fold

@@ -16,6 +16,8 @@ int32_t pack_impl(const fold_params* p, hipStream_t st, fold_packed** out);
 void packed_destroy_impl(fold_packed* h);
 
 // Workspace layout shared by the forward and backward passes.
+constexpr int kMaxMerge = 4;  // groups of one level in one launch
+
 struct WsLayout {
   int gstride = 0;           // floats per pool row of saved gates / dz: Gmax * HP
   size_t gates_off = 0, gates_bytes = 0;
@@ -24,6 +26,12 @@ struct WsLayout {
   size_t part_off = 0, part_bytes = 0;   // weight-gradient partial tiles
   size_t bpart_off = 0, bpart_bytes = 0; // bias partial sums
   size_t fwd_bytes = 0, bwd_bytes = 0;
+  // The forward's launches: batch[g] = the level launch group g belongs to (consecutive narrow groups of one
+  // level, at most kMaxMerge to a launch), or -1 for a group launched alone (an embedding, a wide group).
+  // Groups of one level launch run at once, so each has its own part of the K-split partial sums: zoff[g]
+  // (floats from the region's start) and zneed[g] (floats, 0 when it does not split).
+  std::vector<int> batch;
+  std::vector<size_t> zoff, zneed;
 };
 WsLayout workspace_layout(const Sched& s, const Packed& p);
 
@@ -82,6 +90,9 @@ __device__ __forceinline__ int fwd_child(const FwdArgs& a, int row, int k) {
   return a.cbase[k] >= 0 ? a.cbase[k] + row : a.child_pos[a.idx_off + row * a.arity + k];
 }
 void launch_cell_fwd(int dtype, int kind, const FwdArgs& a, hipStream_t st);
+// The narrow groups of one level (at most kMaxMerge, every one narrow by fwd_plan) as one launch, plus one for
+// their K-split epilogues; kinds as for launch_cell_fwd.
+void launch_level_fwd(int dtype, const int* kinds, const FwdArgs* args, int n, hipStream_t st);
 
 // Tiling of one forward group.  Wide groups (at least one workgroup per compute unit) use the wide
 // kernel: 256 rows x 2 unit blocks per workgroup of 8 waves.  Narrower groups use 128-row tiles of one
@@ -168,6 +179,7 @@ struct BwdCellArgs {
   const float* u_mask = nullptr;  // the forward's recurrent-dropout mask, or NULL
 };
 void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st);
+void launch_level_cbwd(const int* kinds, const BwdCellArgs* args, int n, hipStream_t st);
 void launch_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* dh_roots, const int* root_pos,
                      float* dh, float* dc, hipStream_t st);
 
@@ -189,6 +201,9 @@ struct DxArgs {
   int map;          // set by the launcher: workgroup order over the XCDs (kMapRows, kMapCols, kMapOwnCols)
 };
 void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st);
+// true if launch_bwd_dx would run this call on narrow tiles (the ones a level launch can merge)
+bool bwd_dx_is_narrow(int dtype, const DxArgs& a);
+void launch_level_dx(int dtype, const DxArgs* args, int n, hipStream_t st);
 
 // ---- weight gradients (wgrad.hip) ----
 struct WgArgs {

@@ -46,13 +46,17 @@ struct Mma<uint16_t> {
 // on the same XCD and are dispatched back to back there: XCD k owns y in [k*Y8/8, (k+1)*Y8/8).  The
 // operand those X workgroups share (a row tile's gathered rows, a weight slice, a row chunk) is then
 // fetched into that XCD's L2 once.  Returns false for the padding workgroups (y >= Y), which exit.
-__device__ __forceinline__ bool xcd_tile(int X, int Y, int& x, int& y) {
-  const int L = blockIdx.x;
-  const int per = (Y + 7) >> 3, xcd = L & 7, slot = L >> 3;
-  x = slot % X;
-  y = xcd * per + slot / X;
+// (L: the workgroup's index in its launch; a launch that runs several such grids back to back passes each
+// workgroup's index within its own grid, which keeps the XCD assignment when every grid starts at a multiple
+// of 8)
+__device__ __forceinline__ bool xcd_tile_at(unsigned L, int X, int Y, int& x, int& y) {
+  // unsigned arithmetic: the indices are never negative, and unsigned division is the cheaper sequence
+  const unsigned per = ((unsigned)Y + 7u) >> 3, xcd = L & 7u, slot = L >> 3;
+  x = (int)(slot % (unsigned)X);
+  y = (int)(xcd * per + slot / (unsigned)X);
   return y < Y;
 }
+__device__ __forceinline__ bool xcd_tile(int X, int Y, int& x, int& y) { return xcd_tile_at(blockIdx.x, X, Y, x, y); }
 inline int xcd_grid(int X, int Y) { return X * (((Y + 7) >> 3) << 3); }
 
 // Wide launches over C column tiles (C a multiple of 8) and R row tiles, launched as C * R2 workgroups

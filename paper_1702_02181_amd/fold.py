@@ -137,7 +137,7 @@ EXPORTS = ["fold_schedule", "fold_sched_get_info", "fold_sched_free", "fold_pack
            "fold_graph_num_nodes", "fold_graph_free", "fold_pack_update", "fold_loss_softmax_ce",
            "fold_loss_workspace_size", "fold_adam_step", "fold_forward_dropout", "fold_backward_dropout",
            "fold_dropout_mask", "fold_forward_noalloc", "fold_schedule_typed", "fold_typed_sched_get_info",
-           "fold_typed_sched_free"]
+           "fold_typed_sched_free", "fold_level_launches"]
 
 _lib = None
 
@@ -149,6 +149,9 @@ def lib():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_1702_02181_amd.build_lib.build()")
+    # torch first: its HIP runtime (same soname) is then the one the library's calls reach.  Loaded the other
+    # way round, the process would map two HIP runtimes and the library's would see no device.
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     L.fold_last_error.restype = ctypes.c_char_p
     L.fold_last_error.argtypes = []
@@ -180,6 +183,8 @@ def lib():
     L.fold_backward_dropout.argtypes = [c_void_p, c_void_p, c_void_p, c_int64, c_void_p, c_void_p, c_void_p,
                                         c_void_p, c_void_p, POINTER(fold_grads), c_void_p, c_void_p, c_void_p,
                                         c_size_t, c_void_p]
+    L.fold_level_launches.restype = c_int32
+    L.fold_level_launches.argtypes = [c_int32]
     L.fold_schedule_typed.restype = c_int32
     L.fold_schedule_typed.argtypes = [POINTER(fold_typed_batch), c_void_p, POINTER(c_void_p)]
     L.fold_typed_sched_get_info.restype = c_int32
@@ -328,6 +333,11 @@ def fold_loss_softmax_ce(sched, packed, h_pool, labels, num_classes, W_cls, b_cl
 def fold_adam_step(n, param, param_bf16, grad, m, v, lr, beta1, beta2, eps, step, stream=None):
     _check(lib().fold_adam_step(int(n), _ptr(param), _ptr(param_bf16), _ptr(grad), _ptr(m), _ptr(v), float(lr),
                                 float(beta1), float(beta2), float(eps), int(step), _stream(stream)))
+
+
+def fold_level_launches(on) -> bool:
+    """Turn level launches on or off for later calls; returns the previous setting."""
+    return bool(lib().fold_level_launches(1 if on else 0))
 
 
 def fold_forward_noalloc(sched, packed, table, table_rows, h_pool, c_pool, roots, stream=None):

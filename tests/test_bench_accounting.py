@@ -44,14 +44,18 @@ def test_pass_work_bf16_state_bytes_and_table_grad():
 
 
 def test_pass_of_routes_launches():
-    assert bench.pass_of("cell_fwd.treelstm.f32", 3, 1) == ("fwd", 3)
-    assert bench.pass_of("embed_fwd", 0, 0) == ("fwd", 0)
-    assert bench.pass_of("cell_bwd.treelstm", 3, 1) == ("bwd", 3)
-    assert bench.pass_of("bwd_dx.bf16", 2, 1) == ("bwd", 2)
-    assert bench.pass_of("wgrad.bf16", -1, 1) == ("wgrad", 1)
-    assert bench.pass_of("wgrad_reduce", -1, 0) == ("wgrad", 0)
-    assert bench.pass_of("bwd_init", -1, -1) is None
-    assert bench.pass_of("roots", -1, -1) is None
+    assert bench.pass_of("cell_fwd.treelstm.f32", 3, 1) == [("fwd", 3)]
+    assert bench.pass_of("embed_fwd", 0, 0) == [("fwd", 0)]
+    assert bench.pass_of("cell_bwd.treelstm", 3, 1) == [("bwd", 3)]
+    assert bench.pass_of("bwd_dx.bf16", 2, 1) == [("bwd", 2)]
+    assert bench.pass_of("wgrad.bf16", -1, 1) == [("wgrad", 1)]
+    assert bench.pass_of("wgrad_reduce", -1, 0) == [("wgrad", 0)]
+    assert bench.pass_of("bwd_init", -1, -1) == []
+    assert bench.pass_of("roots", -1, -1) == []
+    # a level launch over groups 4, 5, 6 (op = -1 - 3)
+    assert bench.pass_of("cell_fwd.level.bf16", 4, -4) == [("fwd", 4), ("fwd", 5), ("fwd", 6)]
+    assert bench.pass_of("cell_bwd.level", 4, -3) == [("bwd", 4), ("bwd", 5)]
+    assert bench.pass_of("bwd_dx.level.bf16", 7, -2) == [("bwd", 7)]
 
 
 def test_level_classes_split_and_fractions():

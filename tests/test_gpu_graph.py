@@ -166,7 +166,8 @@ def test_graph_argument_errors():
 
 def test_profile_launch_records_carry_group_and_op():
     """Per-launch timing records name the (depth, op) group of every forward and backward cell launch in
-    schedule order (backward in reverse), and the op of every weight-gradient launch."""
+    schedule order (backward level by level from the top), a level launch its span of groups, and the op of
+    every weight-gradient launch."""
     import torch
     from paper_1702_02181_amd.runner import DeviceRun
     w = gen.config4(num_graphs=6)
@@ -188,14 +189,30 @@ def test_profile_launch_records_carry_group_and_op():
     finally:
         F.fold_profile_enable(False)
     assert F.fold_profile_read_launches() == []
-    fwd = [(g, o) for n, g, o, _ in recs if n.startswith("cell_fwd.")]
-    assert fwd == [(g, int(host["group_op"][g])) for g in range(ng)]
-    bwd_cell = [(g, o) for n, g, o, _ in recs if n.startswith("cell_bwd.")]
-    assert bwd_cell == [(g, int(host["group_op"][g])) for g in reversed(range(ng))]
+
+    def groups_of(g, o):
+        # a level launch (several groups of one level) is tagged with its first group and op = -1 - span
+        return [g] if o >= -1 else list(range(g, g - 1 - o))
+
+    def expanded(prefix):
+        out = []
+        for n, g, o, _ in recs:
+            if n.startswith(prefix):
+                assert o >= 0 or o <= -3, (n, g, o)  # an op id, or a level launch of two or more groups
+                if o >= 0:
+                    assert o == int(host["group_op"][g])
+                out += groups_of(g, o)
+        return out
+    levels = host["group_level"]
+    assert expanded("cell_fwd.") == list(range(ng))
+    # backward: levels from the top, the groups of a level in order
+    want = [g for lv in sorted(set(levels.tolist()), reverse=True) for g in range(ng) if levels[g] == lv]
+    assert expanded("cell_bwd.") == want
+    assert any(n.endswith(".level.bf16") or n == "cell_bwd.level" for n, _, _, _ in recs)  # config 4 merges
     for n, g, o, ms in recs:
         assert ms >= 0.0
         if n.startswith("bwd_dx."):
-            assert 0 <= g < ng and o == int(host["group_op"][g])
+            assert 0 <= g < ng and (o == int(host["group_op"][g]) or (o <= -2 and g - 1 - o <= ng))
         if n.startswith("wgrad"):
             assert g == -1 and 0 <= o < len(w.ops)
         if n in ("bwd_init", "roots", "zero_grads"):
