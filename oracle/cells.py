@@ -24,6 +24,20 @@ Operations (the paper's experiments, Sections 2.1 and 3.3):
             (i | f | o | u), c = i*u + f*c_p, h = o*tanh(c)
   PROJ      h = tanh(h_c . P + b), c = c_c (a unary projection)
 
+Feed-forward attention (Section 3.4, Appendix A): e_t = a(h_t), alpha = softmax(e), c = sum_t alpha_t h_t,
+with the scorer a(h) = w . h + b (W_rec = w as an [H, 1] matrix, bias = [b]).  The sums over t (the normaliser
+and the weighted sum; Appendix A's two Sums) are carried together as the aggregate of a set of items,
+    (m, s, acc) = (max_t e_t,  sum_t exp(e_t - m),  sum_t exp(e_t - m) h_t),
+kept in the node's state as h = acc and c = [m, s, 0, ...] (H >= 2):
+  ATTN_SCORE  one item from its child's h: (e, 1, h_child), e = w . h_child + b
+  ATTN_SUM    the union of its two children's sets: m = max(m_1, m_2), x_k = exp(m_k - m),
+              s = x_1 s_1 + x_2 s_2, acc = x_1 acc_1 + x_2 acc_2; a child with s = 0 (the zero state
+              among them) is the empty set and takes no part, and the union of two empty sets is the
+              zero state
+  ATTN_OUT    c_att = acc / s as the node's h (c = 0); attention over the empty set is the zero vector
+The aggregate's value does not depend on m (it scales s and acc alike and cancels in acc / s), so the
+gradients hold m fixed: they are the exact derivatives of acc / s.
+
 The gradient functions are the chain rule written out by hand for each of
 these; the tests pin them with central finite differences.
 """
@@ -32,10 +46,64 @@ from __future__ import annotations
 import numpy as np
 
 EMBED, TREERNN, TREELSTM, LSTM, PROJ = 0, 1, 2, 3, 4
+ATTN_SCORE, ATTN_SUM, ATTN_OUT = 5, 6, 7
+ATTN = (ATTN_SCORE, ATTN_SUM, ATTN_OUT)
 
 # number of child slots and of gate blocks of each kind
-SLOTS = {EMBED: 0, TREERNN: 2, TREELSTM: 2, LSTM: 1, PROJ: 1}
+SLOTS = {EMBED: 0, TREERNN: 2, TREELSTM: 2, LSTM: 1, PROJ: 1, ATTN_SCORE: 1, ATTN_SUM: 2, ATTN_OUT: 1}
 GATES = {EMBED: 0, TREERNN: 1, TREELSTM: 5, LSTM: 4, PROJ: 1}
+
+
+def _attn_forward(kind, P, H, hs, cs):
+    if kind == ATTN_SCORE:
+        (hc,) = hs
+        e = float(hc @ P["W_rec"][:, 0] + P["bias"][0])
+        c = np.zeros(H)
+        c[0], c[1] = e, 1.0
+        return np.array(hc, dtype=np.float64), c, {"hc": np.array(hc, dtype=np.float64)}
+    if kind == ATTN_SUM:
+        live = [k for k in range(2) if cs[k][1] != 0.0]
+        c = np.zeros(H)
+        if not live:
+            return np.zeros(H), c, {"x": [0.0, 0.0]}
+        m = max(cs[k][0] for k in live)
+        x = [np.exp(cs[k][0] - m) if k in live else 0.0 for k in range(2)]
+        c[0] = m
+        c[1] = sum(x[k] * cs[k][1] for k in range(2))
+        acc = sum(x[k] * hs[k] for k in range(2))
+        return acc, c, {"x": x}
+    if kind == ATTN_OUT:
+        (acc,), (cc,) = hs, cs
+        s = float(cc[1])
+        h = np.zeros(H) if s == 0.0 else np.asarray(acc, dtype=np.float64) / s
+        return h, np.zeros(H), {"acc": np.array(acc, dtype=np.float64), "s": s}
+    raise ValueError(kind)
+
+
+def _attn_backward(kind, P, H, cache, dh, dc):
+    """(dhs, dcs, grads) with m held fixed (see the module docstring)."""
+    if kind == ATTN_SCORE:
+        hc = cache["hc"]
+        # acc = h_child exp(e - m), s = exp(e - m) at e = m: d/de acc = acc, d/de s = s = 1
+        de = float(dh @ hc) + float(dc[1])
+        w = P["W_rec"][:, 0]
+        return [dh + de * w], [np.zeros(H)], {"W_rec": (de * hc)[:, None], "bias": np.array([de])}
+    if kind == ATTN_SUM:
+        x = cache["x"]
+        dcs = []
+        for k in range(2):
+            d = np.zeros(H)
+            d[1] = x[k] * dc[1]
+            dcs.append(d)
+        return [x[k] * dh for k in range(2)], dcs, {}
+    if kind == ATTN_OUT:
+        acc, s = cache["acc"], cache["s"]
+        d = np.zeros(H)
+        if s == 0.0:
+            return [np.zeros(H)], [d], {}
+        d[1] = -float(dh @ acc) / (s * s)
+        return [dh / s], [d], {}
+    raise ValueError(kind)
 
 
 def sigmoid(x):
@@ -67,6 +135,8 @@ def forward_node(kind, P, H, x, hs, cs, m=None):
     (0, or 1/(1-p) for inverted dropout) are drawn by the caller; the LSTM kinds use it, the others ignore it."""
     if kind == EMBED:
         return np.array(x, dtype=np.float64), np.zeros(H), {}
+    if kind in ATTN:
+        return _attn_forward(kind, P, H, hs, cs)
     z = pre_activation(P, H, x, hs)
     if kind in (TREERNN, PROJ):
         h = np.tanh(z)
@@ -101,6 +171,9 @@ def backward_node(kind, P, H, x, hs, cs, cache, dh, dc):
     (dx or None, [dh_k], [dc_k], {"W_in": .., "W_rec": .., "bias": ..})."""
     if kind == EMBED:
         return np.array(dh, dtype=np.float64), [], [], {}
+    if kind in ATTN:
+        dhs, dcs, grads = _attn_backward(kind, P, H, cache, dh, dc)
+        return None, dhs, dcs, grads
     if kind in (TREERNN, PROJ):
         h = cache["h"]
         dz = dh * (1.0 - h * h)

@@ -42,12 +42,20 @@ KIND_TREERNN = 1
 KIND_TREELSTM = 2
 KIND_LSTM = 3
 KIND_PROJ = 4
+KIND_ATTN_SCORE = 5
+KIND_ATTN_SUM = 6
+KIND_ATTN_OUT = 7
+ATTN_KINDS = (KIND_ATTN_SCORE, KIND_ATTN_SUM, KIND_ATTN_OUT)
 
 KIND_NAMES = {KIND_EMBED: "embed", KIND_TREERNN: "treernn", KIND_TREELSTM: "treelstm",
-              KIND_LSTM: "lstm", KIND_PROJ: "proj"}
+              KIND_LSTM: "lstm", KIND_PROJ: "proj", KIND_ATTN_SCORE: "attn_score",
+              KIND_ATTN_SUM: "attn_sum", KIND_ATTN_OUT: "attn_out"}
 
-# Gate blocks per kind: the width of z is NUM_GATES[kind] * hidden.
-NUM_GATES = {KIND_EMBED: 0, KIND_TREERNN: 1, KIND_TREELSTM: 5, KIND_LSTM: 4, KIND_PROJ: 1}
+# Gate blocks per kind: the width of z is NUM_GATES[kind] * hidden (the attention kinds have no z).
+NUM_GATES = {KIND_EMBED: 0, KIND_TREERNN: 1, KIND_TREELSTM: 5, KIND_LSTM: 4, KIND_PROJ: 1,
+             KIND_ATTN_SCORE: 0, KIND_ATTN_SUM: 0, KIND_ATTN_OUT: 0}
+# Child slots of the attention kinds (their parameter sets' arity).
+ATTN_SLOTS = {KIND_ATTN_SCORE: 1, KIND_ATTN_SUM: 2, KIND_ATTN_OUT: 1}
 
 
 # --------------------------------------------------------------------------
@@ -91,6 +99,8 @@ class ParamSet:
     ``bias``  [G*H]
     Gate blocks are in canonical order along the columns:
     Tree-LSTM (i | f_l | f_r | o | u), LSTM (i | f | o | u), TreeRNN / PROJ one block.
+    The attention scorer (ATTN_SCORE) has W_rec [H, 1] (the vector w) and bias [1]; the ATTN_SUM and
+    ATTN_OUT sets hold no values (W_rec None, bias empty).
     """
     kind: int
     in_dim: int
@@ -331,6 +341,30 @@ def lstm_chain_reduce(b: _GraphBuilder, n: int, rng, row0: int, p_proj: float,
     return reduce(chain)
 
 
+def attention_sequence(b: _GraphBuilder, n: int, row0: int, op_embed: int, op_f: int, op_score: int,
+                       op_sum: int, op_out: int, op_g: int = -1) -> int:
+    """Feed-forward attention over a sequence of n token rows (Section 3.4): h_t = f(x_t) for every
+    element (an embedding lookup, then a PROJ layer f), one scorer node per element, the scored items
+    summed by a balanced Reduce (the left half gets floor(n/2) items), the attention output c, and
+    optionally a PROJ layer g on c."""
+    items = []
+    for i in range(n):
+        x = b.add(op_embed, (), row0 + i)
+        h = b.add(op_f, (x,))
+        items.append(b.add(op_score, (h,)))
+
+    def reduce(seq):
+        if len(seq) == 1:
+            return seq[0]
+        m = len(seq) // 2
+        left = reduce(seq[:m])
+        right = reduce(seq[m:])
+        return b.add(op_sum, (left, right))
+
+    c = b.add(op_out, (reduce(items),))
+    return b.add(op_g, (c,)) if op_g >= 0 else c
+
+
 # --------------------------------------------------------------------------
 # Value generators
 # --------------------------------------------------------------------------
@@ -354,6 +388,10 @@ def make_param_set(rng, kind: int, in_dim: int, arity: int, hidden: int, dtype: 
     g = NUM_GATES[kind]
     if kind == KIND_EMBED:
         return ParamSet(kind, in_dim, 0, None, None, np.zeros(0, np.float32))
+    if kind == KIND_ATTN_SCORE:
+        return ParamSet(kind, 0, 1, None, _finish_values(_uniform(rng, (hidden, 1)), dtype), _uniform(rng, (1,)))
+    if kind in (KIND_ATTN_SUM, KIND_ATTN_OUT):
+        return ParamSet(kind, 0, ATTN_SLOTS[kind], None, None, np.zeros(0, np.float32))
     W_in = _finish_values(_uniform(rng, (in_dim, g * hidden)), dtype) if in_dim > 0 else None
     W_rec = _finish_values(_uniform(rng, (arity * hidden, g * hidden)), dtype) if arity > 0 else None
     bias = _uniform(rng, (g * hidden,))
@@ -529,6 +567,37 @@ def table1(batch: int, mode: str, seed: int = 7, leaves: int = 64, hidden: int =
     params = [make_param_set(rng, KIND_TREELSTM, H, 2, H, dtype)]
     return _finish(f"table1_{mode}_b{batch}_n{2 * leaves - 1}_h{H}_{dtype}", dtype, H, csr, ops, params, E, rng,
                    backward=False)
+
+
+def attention(seed: int = 6, num_graphs: int = 1024, length=(50, 100), hidden: int = 256,
+              dtype: str = "bf16") -> Workload:
+    """Feed-forward attention (Section 3.4, Appendix A): `num_graphs` sequences of T ~ U{length} elements,
+    each element a row of a table of token vectors (N(0, 1) entries, one distinct row per element), the
+    model of attention_sequence with a PROJ output layer g.  Ops: EMBED, PROJ f, ATTN_SCORE, ATTN_SUM,
+    ATTN_OUT, PROJ g; weights U(-0.1, 0.1) except the scorer, U(-1, 1) (so that the attention weights are
+    far from uniform); forward and backward."""
+    rng = np.random.default_rng(seed)
+    H = hidden
+    graphs = []
+    row = 0
+    for _ in range(num_graphs):
+        n = int(rng.integers(length[0], length[1] + 1))
+        b = _GraphBuilder()
+        attention_sequence(b, n, row, 0, 1, 2, 3, 4, 5)
+        row += n
+        graphs.append(b.arrays())
+    csr = assemble(graphs)
+    ops = [OpSpec(KIND_EMBED, 0, 1, 0), OpSpec(KIND_PROJ, 1, 0, 1), OpSpec(KIND_ATTN_SCORE, 1, 0, 2),
+           OpSpec(KIND_ATTN_SUM, 2, 0, 3), OpSpec(KIND_ATTN_OUT, 1, 0, 4), OpSpec(KIND_PROJ, 1, 0, 5)]
+    X = _finish_values(rng.standard_normal((row, H)), dtype)
+    score = make_param_set(rng, KIND_ATTN_SCORE, 0, 1, H, dtype)
+    score.W_rec = _finish_values(rng.uniform(-1.0, 1.0, size=(H, 1)), dtype)
+    params = [make_param_set(rng, KIND_EMBED, H, 0, H, dtype), make_param_set(rng, KIND_PROJ, 0, 1, H, dtype),
+              score, make_param_set(rng, KIND_ATTN_SUM, 0, 2, H, dtype),
+              make_param_set(rng, KIND_ATTN_OUT, 0, 1, H, dtype), make_param_set(rng, KIND_PROJ, 0, 1, H, dtype)]
+    lo, hi = length
+    return _finish(f"ffattn_b{num_graphs}_t{lo}-{hi}_h{H}_{dtype}", dtype, H, csr, ops, params, X, rng,
+                   backward=True)
 
 
 def make_config(k: int, **kw) -> Workload:

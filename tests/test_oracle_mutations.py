@@ -8,7 +8,10 @@ labels, overwriting instead of summing fan-out contributions, and in the parity 
 floor dropped, min instead of max over rows, the row norm taken as a min, whole= ignored, rows cut along
 the last axis, and NaN rows skipped; in the paper-form schedule: pass-throughs numbered among the user
 operations, a pass-through one depth too early, labels into the reader's own depth, and a concatenation
-taken row by row instead of output slot by output slot."""
+taken row by row instead of output slot by output slot; in feed-forward attention: the merge exponent's
+sign flipped, min instead of max as the running maximum, the scorer's bias dropped, the score gradient's
+cell-state term dropped, the pass-through term of the scored item's gradient dropped, an unscaled sum
+gradient, and the output's normaliser gradient with the wrong sign."""
 import os
 import shutil
 import subprocess
@@ -56,6 +59,13 @@ MUTATIONS = [
     ("paper_schedule.py", "src_d = d - 1", "src_d = d"),
     ("paper_schedule.py", "        for slot, t in enumerate(its[0][4]):\n            for it in its:",
      "        for it in its:\n            for slot, t in enumerate(its[0][4]):"),
+    ("cells.py", "x = [np.exp(cs[k][0] - m) if k in live", "x = [np.exp(m - cs[k][0]) if k in live"),
+    ("cells.py", "m = max(cs[k][0] for k in live)", "m = min(cs[k][0] for k in live)"),
+    ("cells.py", 'e = float(hc @ P["W_rec"][:, 0] + P["bias"][0])', 'e = float(hc @ P["W_rec"][:, 0])'),
+    ("cells.py", "de = float(dh @ hc) + float(dc[1])", "de = float(dh @ hc)"),
+    ("cells.py", "return [dh + de * w], [np.zeros(H)]", "return [de * w], [np.zeros(H)]"),
+    ("cells.py", "d[1] = x[k] * dc[1]", "d[1] = dc[1]"),
+    ("cells.py", "d[1] = -float(dh @ acc) / (s * s)", "d[1] = float(dh @ acc) / (s * s)"),
 ]
 
 
@@ -72,6 +82,7 @@ def test_planted_mistake_is_caught(i, tmp_path):
     p.write_text(src.replace(old, new, 1))
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:randomly",
                         "tests/test_oracle_schedule.py", "tests/test_oracle_cells.py",
-                        "tests/test_oracle_compare.py", "tests/test_oracle_paper_schedule.py"],
+                        "tests/test_oracle_compare.py", "tests/test_oracle_paper_schedule.py",
+                        "tests/test_oracle_attention.py"],
                        cwd=tmp_path, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"pins missed mutation {i}: {new!r}"
