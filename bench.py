@@ -199,7 +199,7 @@ def flops_by_kernel(w, sched_host, table_grad: bool) -> dict:
         rows_of_op[int(op_id)] = rows_of_op.get(int(op_id), 0) + int(rows)
     for op_id, rows in rows_of_op.items():
         op = w.ops[op_id]
-        if op.kind == gen.KIND_EMBED:
+        if op.kind == gen.KIND_EMBED or op.kind in gen.ATTN_KINDS:
             continue
         G = live_gates(op)
         ps = w.params[op.param_set]
@@ -213,6 +213,46 @@ def flops_by_kernel(w, sched_host, table_grad: bool) -> dict:
 
 
 NARROW_S = 2e-6  # a level pass whose roofline time is below this is reported as time per pass
+
+
+def attn_bytes(w, op, rows: int, kind: str) -> float:
+    """Algorithmic HBM bytes of `rows` nodes of a feed-forward attention operation (Section 3.4), pass `kind`
+    ("fwd", "bwd") or the scorer's weight gradient ("wgrad").  A node's state is its aggregate: acc (h, H values
+    of the pool type) and (m, s) (8 bytes); its gradient is dh (fp32, H values) and ds (4 bytes).
+      score  fwd: read the item h, write (h, e, 1)       bwd: read dh, ds, the item h; write the item's dh, de
+      sum    fwd: read two aggregates, write one         bwd: read dh, ds, the children's (m, s); write both
+                                                              children's (dh, ds)
+      out    fwd: read one aggregate, write h            bwd: read dh, the child's acc and s; write its (dh, ds)
+    plus the scorer vector once per pass; wgrad reads de and the item h per row and writes H + 1 floats."""
+    from paper_1702_02181_amd import gen
+    H = w.hidden
+    bh = 2 if w.dtype == "bf16" else 4
+    agg, grad = H * bh + 8, H * 4 + 4
+    if kind == "wgrad":
+        return float(rows * (4 + H * bh) + (H + 1) * 4)
+    if op.kind == gen.KIND_ATTN_SCORE:
+        per = (H * bh + agg) if kind == "fwd" else (grad + H * bh + grad)
+        return float(rows * per + H * bh)
+    if op.kind == gen.KIND_ATTN_SUM:
+        return float(rows * ((2 * agg + agg) if kind == "fwd" else (grad + 16 + 2 * grad)))
+    return float(rows * ((agg + H * bh) if kind == "fwd" else (H * 4 + agg + grad)))
+
+
+def attn_kernel_bytes(w, host) -> dict:
+    """Algorithmic HBM bytes of one step by attention kernel class ("attn_fwd.score", ...)."""
+    from paper_1702_02181_amd import gen
+    names = {gen.KIND_ATTN_SCORE: "score", gen.KIND_ATTN_SUM: "sum", gen.KIND_ATTN_OUT: "out"}
+    out = {}
+    for op_id, rows in zip(host["group_op"], host["group_rows"]):
+        op = w.ops[int(op_id)]
+        if op.kind not in names:
+            continue
+        for kind in ("fwd", "bwd") if w.backward else ("fwd",):
+            k = f"attn_{kind}.{names[op.kind]}"
+            out[k] = out.get(k, 0.0) + attn_bytes(w, op, int(rows), kind)
+        if w.backward and op.kind == gen.KIND_ATTN_SCORE:
+            out["attn_wgrad"] = out.get("attn_wgrad", 0.0) + attn_bytes(w, op, int(rows), "wgrad")
+    return out
 
 
 def pass_work(w, host, table_grad: bool) -> dict:
@@ -232,6 +272,12 @@ def pass_work(w, host, table_grad: bool) -> dict:
     for g, (op_id, rows) in enumerate(zip(host["group_op"], host["group_rows"])):
         op, rows = w.ops[int(op_id)], int(rows)
         op_rows[int(op_id)] = op_rows.get(int(op_id), 0) + rows
+        if op.kind in gen.ATTN_KINDS:
+            out[("fwd", g)] = (2.0 * rows * H if op.kind == gen.KIND_ATTN_SCORE else 0.0,
+                               attn_bytes(w, op, rows, "fwd"))
+            if w.backward:
+                out[("bwd", g)] = (0.0, attn_bytes(w, op, rows, "bwd"))
+            continue
         if op.kind == gen.KIND_EMBED:
             out[("fwd", g)] = (0.0, float(rows * 2 * H * bh))
             if w.backward and table_grad:
@@ -253,7 +299,9 @@ def pass_work(w, host, table_grad: bool) -> dict:
     if w.backward:
         for o, count in op_rows.items():
             op = w.ops[o]
-            if op.kind == gen.KIND_EMBED:
+            if op.kind == gen.KIND_ATTN_SCORE:
+                out[("wgrad", o)] = (2.0 * count * H, attn_bytes(w, op, count, "wgrad"))
+            if op.kind == gen.KIND_EMBED or op.kind in gen.ATTN_KINDS:
                 continue
             G = live_gates(op)
             k_in = (w.params[op.param_set].in_dim if op.has_input else 0) + op.arity * H
@@ -268,11 +316,11 @@ def pass_of(name: str, group: int, op: int):
     equally among them."""
     cls = class_of(name)
     groups = [group] if op >= -1 else list(range(group, group - 1 - op))
-    if group >= 0 and cls in ("cell_fwd", "embed_fwd"):
+    if group >= 0 and cls in ("cell_fwd", "embed_fwd", "attn_fwd"):
         return [("fwd", g) for g in groups]
-    if group >= 0 and cls in ("cell_bwd", "bwd_dx"):
+    if group >= 0 and cls in ("cell_bwd", "bwd_dx", "attn_bwd"):
         return [("bwd", g) for g in groups]
-    if group < 0 and op >= 0 and cls in ("wgrad", "wgrad_reduce", "bias_partial", "bias_reduce"):
+    if group < 0 and op >= 0 and cls in ("wgrad", "wgrad_reduce", "bias_partial", "bias_reduce", "attn_wgrad"):
         return [("wgrad", op)]
     return []
 
@@ -498,6 +546,31 @@ def blocks_bench(steps: int, warmup: int, num_trees: int = 1024, hidden: int = 3
             "host_compile_nodes_per_s": round(w.num_nodes / build_s, 1)}
 
 
+def attention_bench(steps: int, warmup: int) -> dict:
+    """Feed-forward attention (Section 3.4, Appendix A) as a dynamic-batching workload: 1024 sequences of
+    U{50..100} token rows, h_t = PROJ f(x_t), scored, merged by a balanced Reduce, attended, PROJ g on top;
+    H = 256, bf16, forward + backward (the token rows are data: no leaf-table gradient).  The attention
+    kernels are HBM-bound: each reports its algorithmic bytes per step over its measured time."""
+    import torch
+
+    from paper_1702_02181_amd import gen
+    torch.cuda.set_device(0)
+    print("[bench attention] generating", file=sys.stderr, flush=True)
+    w = gen.attention()
+    m = measure(w, steps, warmup, False, schedule_reps=3, tag=" attention")
+    attn = {k: v for k, v in m["kernels"].items() if k.startswith("attn_")}
+    by = sum(v.get("alg_bytes_per_step", 0) for v in attn.values())
+    t = sum(v["ms_per_step"] for v in attn.values())
+    return {"metric": "graph nodes/sec (feed-forward attention fwd+bwd, 1 GPU)", "value": m["value"],
+            "unit": "graph nodes/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+            "ms_per_step": m["ms_per_step"], "eager_ms_per_step": m["eager_ms_per_step"], "higher_is_better": True,
+            "dtype": m["dtype"], "data": "synthetic", "config": m["config"], "schedule_ms": m["schedule_ms"],
+            "attention_kernels": {"ms_per_step": round(t, 4), "alg_bytes_per_step": by,
+                                  "gbs": round(by / (t * 1e-3) / 1e9, 1),
+                                  "hbm_frac": round(by / (t * 1e-3) / 1e9 / PEAKS["hbm_gbs"], 4)},
+            "roofline": m["roofline"], "level_classes": m["level_classes"], "kernels": m["kernels"]}
+
+
 def _oracle_graph(w, g: int) -> int:
     """The oracle, as it stands, on graph g of the workload alone (fp64 forward, + backward if the workload
     has one); returns the graph's node count."""
@@ -689,6 +762,12 @@ def measure(w, steps: int, warmup: int, table_grad: bool, schedule_reps: int = 5
         roofline["algorithmic_bytes_per_launch"] = round(alg / launches)
         if rec is not None:
             roofline["traffic_vs_algorithmic"] = round(rec["bytes_per_launch"] / (alg / launches), 3)
+    # attention kernels: algorithmic bytes over their measured time, against the HBM peak
+    for name, by in attn_kernel_bytes(w, host).items():
+        if name in kernels:
+            gbs = by / (kernels[name]["ms_per_step"] * 1e-3) / 1e9
+            kernels[name].update(alg_bytes_per_step=round(by), gbs=round(gbs, 1),
+                                 hbm_frac=round(gbs / PEAKS["hbm_gbs"], 4))
     total_flops = sum(flops.values())
     step_peak = PEAKS["bf16_mfma_tflops"] if w.dtype == "bf16" else PEAKS["f32_mfma_tflops"]
     classes = level_classes(pass_work(w, host, table_grad), launch_times, steps, step_peak, PEAKS["hbm_gbs"])
@@ -732,6 +811,8 @@ def main():
     ap.add_argument("--train", action="store_true",
                     help="time training steps (per-node softmax loss, Adam, re-pack) instead; default config 3")
     ap.add_argument("--dropout", type=float, default=0.0, help="recurrent dropout probability of --train")
+    ap.add_argument("--attention", action="store_true",
+                    help="time the feed-forward attention workload (1024 sequences of 50-100 items, H = 256, bf16)")
     ap.add_argument("--blocks", action="store_true",
                     help="compile sentiment-shaped trees with the combinator front end and time the compiled batch")
     ap.add_argument("--counters-from", nargs=4, metavar=("MFMA_CSV", "FETCH_CSV", "WRITE_CSV", "TRACE_CSV"),
@@ -750,6 +831,9 @@ def main():
         import torch
         torch.cuda.set_device(0)
         print(json.dumps(blocks_bench(args.steps, args.warmup)), flush=True)
+        return
+    if args.attention:
+        print(json.dumps(attention_bench(args.steps, args.warmup)), flush=True)
         return
     if args.train:
         import torch

@@ -73,7 +73,20 @@ enum {
   FOLD_TREELSTM = 2, /* binary N-ary Tree-LSTM, gates (i|f_l|f_r|o|u); arity 0 with input = leaf
                         TreeLSTM(x, 0, 0), arity 2 = internal TreeLSTM(x?, h_l, h_r) */
   FOLD_LSTM = 3,     /* one LSTM step, gates (i|f|o|u), arity 1 (child -1 = zero start state) */
-  FOLD_PROJ = 4      /* h = tanh(h_c P + b), c = c_c            (unary projection, arity 1) */
+  FOLD_PROJ = 4,     /* h = tanh(h_c P + b), c = c_c            (unary projection, arity 1) */
+  /* Feed-forward attention (Section 3.4, Appendix A): e_t = a(h_t), alpha = softmax(e),
+   * c = sum_t alpha_t h_t, with the scorer a(h) = w . h + b.  The two sums over t are carried as one
+   * aggregate of a set of scored items, (m, s, acc) = (max e, sum exp(e - m), sum exp(e - m) h), held in
+   * a node's state as h = acc and c = [m, s, 0, ...] (needs hidden >= 2), so that a Reduce over the items
+   * batches like any other operation.  Gradients hold m fixed (the value acc / s does not depend on it). */
+  FOLD_ATTN_SCORE = 5, /* one item from the child's h: e = w . h_c + b, h = h_c, c = [e, 1, 0..]
+                          (arity 1; parameters: W_rec = w as [H, 1], bias = [b]) */
+  FOLD_ATTN_SUM = 6,   /* union of the two children's sets: m = max(m_1, m_2), x_k = exp(m_k - m),
+                          s = x_1 s_1 + x_2 s_2, acc = x_1 acc_1 + x_2 acc_2; a child with s = 0 (the
+                          zero state, an empty set) takes no part; two empty sets give the zero state
+                          (arity 2, no parameters: W_rec and bias may be NULL) */
+  FOLD_ATTN_OUT = 7    /* the attention output: h = acc / s (the zero vector for an empty set), c = 0
+                          (arity 1, no parameters) */
 };
 
 /* ---- element types of weights, leaf table and h pool ------------------- */
@@ -83,7 +96,7 @@ enum { FOLD_F32 = 0, FOLD_BF16 = 1 };
  * specified and enumerated in advance (Section 2); the op id is the index in
  * the table, and groups of one depth are ordered by it. */
 typedef struct {
-  int32_t kind;      /* FOLD_EMBED .. FOLD_PROJ */
+  int32_t kind;      /* FOLD_EMBED .. FOLD_ATTN_OUT */
   int32_t arity;     /* number of node children (CSR entries) */
   int32_t has_input; /* 1: reads leaf-table row node_input[v] */
   int32_t param_set; /* index into fold_params.sets */
@@ -254,7 +267,13 @@ int32_t fold_typed_sched_free(fold_typed_sched* sched);
 /* Parameters of one operation family, canonical row-major layout, device
  * memory, element type fold_params.dtype (bias always fp32).  G gate blocks
  * (Tree-LSTM 5, LSTM 4, TreeRNN / PROJ 1, EMBED 0) of `hidden` columns each,
- * in the order given under FOLD_TREELSTM / FOLD_LSTM. */
+ * in the order given under FOLD_TREELSTM / FOLD_LSTM.  Attention sets
+ * (in_dim 0): FOLD_ATTN_SCORE has arity 1, W_rec = the scorer vector w as
+ * [hidden, 1] and bias = [b] (one float); FOLD_ATTN_SUM (arity 2) and
+ * FOLD_ATTN_OUT (arity 1) hold no values (W_rec and bias may be NULL).  Their
+ * gradients (fold_param_grads) are dW_rec [hidden] and dbias [1] for the
+ * scorer, none for the other two.  hidden must be at least 2 once an
+ * attention set is present. */
 typedef struct {
   int32_t kind;
   int32_t in_dim;    /* width of the leaf-table rows the ops read (EMBED: = hidden) */

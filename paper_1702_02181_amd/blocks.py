@@ -227,11 +227,17 @@ class _Ref(Block):
 
 # operation variants of each kind: (arity, has_input) in the order they enter the op table
 _VARIANTS = {gen.KIND_EMBED: [(0, 1)], gen.KIND_TREELSTM: [(0, 1), (2, 0)], gen.KIND_LSTM: [(1, 1)],
-             gen.KIND_TREERNN: [(2, 0)], gen.KIND_PROJ: [(1, 0)]}
+             gen.KIND_TREERNN: [(2, 0)], gen.KIND_PROJ: [(1, 0)], gen.KIND_ATTN_SCORE: [(1, 0)],
+             gen.KIND_ATTN_SUM: [(2, 0)], gen.KIND_ATTN_OUT: [(1, 0)]}
 
 
 class Op(Block):
-    """A library operation of the given kind on parameter set ``param_set``."""
+    """A library operation of the given kind on parameter set ``param_set``.  Arguments: EMBED a Row; PROJ,
+    ATTN_SCORE and ATTN_OUT one state; TREERNN and ATTN_SUM a pair of states; LSTM Fold's (state, Row);
+    TREELSTM (Row or ZERO, ZERO or a pair of states).  Feed-forward attention over a sequence (Section 3.4) is
+    then Map(... >> Op(ATTN_SCORE)) >> Reduce(Op(ATTN_SUM)) >> Op(ATTN_OUT): the scored items, their softmax
+    normaliser and weighted sum carried together through the merges (Appendix A's Sum, Broadcast and ZipWith
+    in one aggregate)."""
 
     def __init__(self, kind: int, param_set: int):
         self.kind, self.param_set = kind, param_set
@@ -243,9 +249,9 @@ class Op(Block):
         if self.kind == gen.KIND_LSTM:  # Fold's (state, x)
             s, r = x
             return r, (s,)
-        if self.kind == gen.KIND_PROJ:
+        if self.kind in (gen.KIND_PROJ, gen.KIND_ATTN_SCORE, gen.KIND_ATTN_OUT):
             return None, (x,)
-        if self.kind == gen.KIND_TREERNN:
+        if self.kind in (gen.KIND_TREERNN, gen.KIND_ATTN_SUM):  # a pair (Reduce's)
             return None, tuple(x)
         r, kids = x  # Tree-LSTM: (x, children)
         kids = () if kids is ZERO else tuple(kids)

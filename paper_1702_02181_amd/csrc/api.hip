@@ -88,7 +88,7 @@ int fail(int code, const std::string& msg) {
   return code;
 }
 
-bool valid_kind(int k) { return k >= FOLD_EMBED && k <= FOLD_PROJ; }
+bool valid_kind(int k) { return k >= FOLD_EMBED && k <= FOLD_ATTN_OUT; }
 
 // a Tree-LSTM operation without children: its cells run on the live gates only
 bool is_tree_lstm_leaf(const fold_op& op) { return op.kind == FOLD_TREELSTM && op.arity == 0; }
@@ -100,6 +100,9 @@ int slots_of(int kind) {
     case FOLD_TREELSTM: return 2;
     case FOLD_LSTM: return 1;
     case FOLD_PROJ: return 1;
+    case FOLD_ATTN_SCORE: return 1;
+    case FOLD_ATTN_SUM: return 2;
+    case FOLD_ATTN_OUT: return 1;
     default: return 0;
   }
 }
@@ -116,6 +119,9 @@ int check_op_table(const fold_op* ops, int n) {
       case FOLD_TREELSTM: ok = (o.arity == 2) || (o.arity == 0 && o.has_input == 1); break;
       case FOLD_LSTM: ok = o.arity == 1; break;
       case FOLD_PROJ: ok = o.arity == 1 && o.has_input == 0; break;
+      case FOLD_ATTN_SCORE:
+      case FOLD_ATTN_SUM:
+      case FOLD_ATTN_OUT: ok = o.arity == slots_of(o.kind) && o.has_input == 0; break;
       default: ok = false;
     }
     if (!ok) return fail(FOLD_E_INVALID, "op " + std::to_string(i) + ": arity / has_input not valid for its kind");
@@ -199,7 +205,7 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
       in_batch = 0;
       run = 0;
     }
-    if (op.kind == FOLD_EMBED || op.param_set >= (int)p.sets.size()) {
+    if (op.kind == FOLD_EMBED || is_attn(op.kind) || op.param_set >= (int)p.sets.size()) {
       if (in_batch > 0) ++nb;
       in_batch = 0;
       run = 0;
@@ -233,6 +239,10 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
     const fold_op& op = s.ops[o];
     if (op.kind == FOLD_EMBED || op.param_set >= (int)p.sets.size()) continue;
     const int count = s.h_op_row_ptr[o + 1] - s.h_op_row_ptr[o];
+    if (is_attn(op.kind)) {  // the scorer's chunked partial sums
+      if (op.kind == FOLD_ATTN_SCORE) part = std::max(part, (size_t)attn_wgrad_chunks(count) * (p.HP + kPadK));
+      continue;
+    }
     const PackedSet& ps = p.sets[op.param_set];
     const int Nw = ps.G * p.HP;
     size_t nb = (size_t)((count + 511) / 512);
@@ -262,7 +272,11 @@ static void pack_launch(const Packed& P, const fold_params* prm, hipStream_t st)
   for (int i = 0; i < prm->num_sets; ++i) {
     const fold_param_set& s = prm->sets[i];
     const PackedSet& ps = P.sets[i];
-    if (s.kind == FOLD_EMBED) continue;
+    if (s.kind == FOLD_EMBED || s.kind == FOLD_ATTN_SUM || s.kind == FOLD_ATTN_OUT) continue;
+    if (s.kind == FOLD_ATTN_SCORE) {
+      launch_pack_score(P.dtype, P.H, P.HP, s.W_rec, s.bias, ps.Wf, ps.bias, st);
+      continue;
+    }
     const size_t nf = (size_t)ps.Nf * ps.Kf;
     const size_t nbr = (size_t)s.arity * P.HP * ps.G * P.HP;
     const size_t nbi = (size_t)ps.INP * ps.G * P.HP;
@@ -319,7 +333,11 @@ int32_t pack_impl(const fold_params* prm, hipStream_t st, fold_packed** out) {
     ps.in_dim = s.in_dim;
     ps.arity = s.arity;
     ps.G = gates_of(s.kind);
-    if (s.kind != FOLD_EMBED) {
+    if (s.kind == FOLD_ATTN_SCORE) {  // the scorer vector (HP entries) and its bias (64 floats, [0] = b)
+      if (!dalloc((size_t)P.HP * es, &ps.Wf) ||
+          !dalloc((size_t)kPadK * sizeof(float), reinterpret_cast<void**>(&ps.bias)))
+        return bail(FOLD_E_NOMEM, "fold_pack_params: out of device memory");
+    } else if (s.kind != FOLD_EMBED && !is_attn(s.kind)) {
       ps.INP = (s.in_dim > 0) ? round_up(s.in_dim, kPadK) : 0;
       ps.Kf = ps.INP + s.arity * P.HP;
       ps.Nf = ps.G * P.HP;
@@ -365,6 +383,25 @@ struct TagScope {
   ~TagScope() { prof_tag(-1, -1); }
 };
 
+// arguments of an attention group's launches (the forward's; the backward adds its accumulators)
+static AttnArgs attn_args(const Sched& s, const Packed& p, int g, void* h_pool, float* c_pool) {
+  const fold_op& op = s.ops[s.h_op[g]];
+  const PackedSet& ps = p.sets[op.param_set];
+  AttnArgs a{};
+  a.rows = s.h_rows[g];
+  a.row_begin = s.h_row_begin[g];
+  a.idx_off = s.h_idx_off[g];
+  a.H = p.H;
+  a.ld = p.ld;
+  a.h_pool = h_pool;
+  a.c_pool = c_pool;
+  a.child_pos = s.child_pos;
+  a.child_one = s.child_one;
+  a.w = ps.Wf;
+  a.bias = ps.bias;
+  return a;
+}
+
 int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t table_rows, void* h_pool,
                      float* c_pool, void* roots_out, void* ws, size_t ws_bytes, hipStream_t st, const float* u_mask,
                      float* zpart_direct, size_t zcap) {
@@ -408,6 +445,12 @@ int32_t forward_impl(const Sched& s, const Packed& p, const void* table, int64_t
       flush();
       prof_tag(g, s.h_op[g]);
       launch_embed_fwd(p.dtype, s.h_rows[g], s.h_row_begin[g], p.H, p.ld, tld, table, s.input_idx, h_pool, c_pool, st);
+      continue;
+    }
+    if (is_attn(op.kind)) {
+      flush();
+      prof_tag(g, s.h_op[g]);
+      launch_attn_fwd(p.dtype, op.kind, attn_args(s, p, g, h_pool, c_pool), st);
       continue;
     }
     FwdArgs a;
@@ -509,6 +552,8 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
     std::vector<BwdCellArgs> cargs;
     std::vector<DxArgs> dargs;
     std::vector<int> dgroup;
+    std::vector<AttnArgs> attn;
+    std::vector<int> attn_kind, attn_group;
     for (int g = g_lo; g < g_hi; ++g) {
       const fold_op& op = s.ops[s.h_op[g]];
       const PackedSet& ps = p.sets[op.param_set];
@@ -532,6 +577,17 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       b.d_table = d_table;
       b.tld = tld;
       b.dz_bf16 = p.dtype == FOLD_BF16;
+      if (is_attn(op.kind)) {  // adds into the children itself: no dz . W^T
+        AttnArgs at = attn_args(s, p, g, const_cast<void*>(h_pool), const_cast<float*>(c_pool));
+        at.dh = dh;
+        at.dc = dc;
+        at.gates = gates;
+        at.gstride = L.gstride;
+        attn.push_back(at);
+        attn_kind.push_back(op.kind);
+        attn_group.push_back(g);
+        continue;
+      }
       const bool leaf = is_tree_lstm_leaf(op);
       ckind.push_back(leaf ? kTreeLstmLeaf : op.kind);
       cargs.push_back(b);
@@ -570,6 +626,10 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
         dargs.push_back(d);
         dgroup.push_back(g);
       }
+    }
+    for (size_t k = 0; k < attn.size(); ++k) {
+      prof_tag(attn_group[k], s.h_op[attn_group[k]]);
+      launch_attn_bwd(p.dtype, attn_kind[k], attn[k], st);
     }
     // cell backwards: the level's groups in chunks of at most kMaxMerge
     const int merge = g_level_launches.load(std::memory_order_relaxed) ? kMaxMerge : 1;
@@ -618,6 +678,12 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       if (count <= 0) continue;
       const PackedSet& ps = p.sets[op.param_set];
       const fold_param_grads& pg = grads->sets[op.param_set];
+      if (is_attn(op.kind)) {
+        if (op.kind == FOLD_ATTN_SCORE)
+          launch_attn_wgrad(p.dtype, s.op_rows + s.h_op_row_ptr[o], s.op_cpos + 2 * (size_t)s.h_op_row_ptr[o], count,
+                            p.H, p.HP, p.ld, h_pool, gates, L.gstride, part, pg.dW_rec, pg.dbias, st);
+        continue;
+      }
       // dz columns: the canonical gate blocks, or the live ones of a Tree-LSTM leaf (dead columns get +0)
       const bool leaf = is_tree_lstm_leaf(op);
       const int Gz = leaf ? gates_of(kTreeLstmLeaf) : ps.G;
@@ -960,6 +1026,14 @@ static int check_params(const fold_params* prm, const char* who) {
     if (s.in_dim < 0) return fail(FOLD_E_INVALID, at + "negative in_dim");
     if (s.kind == FOLD_EMBED) {
       if (s.in_dim != prm->hidden) return fail(FOLD_E_INVALID, at + "embedding width must equal hidden");
+      continue;
+    }
+    if (is_attn(s.kind)) {
+      if (s.in_dim != 0 || s.arity != slots_of(s.kind))
+        return fail(FOLD_E_INVALID, at + "attention sets have in_dim 0 and the kind's child slots");
+      if (prm->hidden < 2) return fail(FOLD_E_INVALID, at + "attention needs hidden >= 2 (c holds m and s)");
+      if (s.kind == FOLD_ATTN_SCORE && (!s.W_rec || !s.bias))
+        return fail(FOLD_E_INVALID, at + "the scorer needs W_rec (w) and bias (b)");
       continue;
     }
     if (s.arity != slots_of(s.kind)) return fail(FOLD_E_INVALID, at + "arity must be the kind's child slots");

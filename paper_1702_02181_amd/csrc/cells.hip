@@ -1082,8 +1082,9 @@ void launch_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* d
 void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
   if (a.rows <= 0) return;
   static const char* names[] = {"cell_bwd.embed", "cell_bwd.treernn", "cell_bwd.treelstm", "cell_bwd.lstm",
-                                "cell_bwd.proj", "cell_bwd.treelstm"};
-  ProfScope prof(kind >= 0 && kind <= kTreeLstmLeaf ? names[kind] : "cell_bwd", st);
+                                "cell_bwd.proj"};
+  const int nk = kind == kTreeLstmLeaf ? FOLD_TREELSTM : kind;  // one class per operation family
+  ProfScope prof(nk >= 0 && nk <= FOLD_PROJ ? names[nk] : "cell_bwd", st);
   // one thread per hidden unit (up to 1024): every load of a row is in flight at once
   dim3 grid(a.rows), block(std::min(a.HP, 1024));
   const size_t lds = a.dz_bf16 ? (size_t)gates_of(kind) * a.HP * sizeof(uint16_t) : 0;

@@ -25,7 +25,10 @@ inline int64_t round_up64(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 // Internal cell kind of a Tree-LSTM operation without children (a leaf: arity 0).  Its child cell states
 // are the zero state, so the forget gates multiply zero and cannot change c, h or any gradient; the leaf
 // kernels compute, save and differentiate only the live gates (i | o | u), in that compact order.
-constexpr int kTreeLstmLeaf = 5;
+constexpr int kTreeLstmLeaf = 8;
+
+// the feed-forward attention operations: elementwise kernels of their own, no matrix-core contraction
+inline bool is_attn(int kind) { return kind >= FOLD_ATTN_SCORE && kind <= FOLD_ATTN_OUT; }
 
 inline int gates_of(int kind) {
   switch (kind) {

@@ -67,7 +67,12 @@ void record_zero_grads(const Sched& s, const Packed& p, const fold_grads* g, int
     const PackedSet& ps = p.sets[i];
     const fold_param_grads& pg = g->sets[i];
     const size_t cols = (size_t)ps.G * p.H;
-    if (ps.kind == FOLD_EMBED) continue;
+    if (ps.kind == FOLD_EMBED || ps.kind == FOLD_ATTN_SUM || ps.kind == FOLD_ATTN_OUT) continue;
+    if (ps.kind == FOLD_ATTN_SCORE) {  // dw [H], db [1]
+      launch_zero_f32(pg.dW_rec, (size_t)p.H, st);
+      launch_zero_f32(pg.dbias, 1, st);
+      continue;
+    }
     launch_zero_f32(pg.dW_in, (size_t)ps.in_dim * cols, st);
     launch_zero_f32(pg.dW_rec, (size_t)ps.arity * p.H * cols, st);
     launch_zero_f32(pg.dbias, cols, st);

@@ -205,6 +205,33 @@ void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st);
 bool bwd_dx_is_narrow(int dtype, const DxArgs& a);
 void launch_level_dx(int dtype, const DxArgs* args, int n, hipStream_t st);
 
+// ---- feed-forward attention operations (attn.hip) ----
+struct AttnArgs {
+  int rows, row_begin, idx_off;
+  int H, ld;
+  void* h_pool;         // [N, ld] of the params' type: the forward writes the group's rows, the backward reads
+  float* c_pool;        // [N, ld] (m, s) in columns 0 and 1
+  const int* child_pos;
+  const int* child_one;  // backward: the child has one parent edge (plain read-add-write)
+  const void* w;        // scorer: w, HP entries of the params' type (zero padded)
+  const float* bias;    // scorer: [0] = b
+  float* dh;            // backward: per-node gradient accumulators [N, ld]
+  float* dc;
+  float* gates;         // backward: the scorer saves de at gates[p * gstride] (NULL: not saved)
+  int gstride;
+};
+// rows of the scorer's weight gradient reduced by one workgroup (chunk order is fixed)
+constexpr int kAttnWgradChunk = 512;
+int attn_wgrad_chunks(int count);
+void launch_attn_fwd(int dtype, int kind, const AttnArgs& a, hipStream_t st);
+void launch_attn_bwd(int dtype, int kind, const AttnArgs& a, hipStream_t st);
+// dw [H] += sum_r de_r h_c(r), db[0] += sum_r de_r over the op's rows; part holds chunks * (HP + 64) floats
+void launch_attn_wgrad(int dtype, const int* op_rows, const int* op_cpos, int count, int H, int HP, int ld,
+                       const void* h_pool, const float* gates, int gstride, float* part, float* dw, float* db,
+                       hipStream_t st);
+void launch_pack_score(int dtype, int H, int HP, const void* w, const float* b, void* wdst, float* bdst,
+                       hipStream_t st);
+
 // ---- weight gradients (wgrad.hip) ----
 struct WgArgs {
   const int* op_rows;  // rows of this op (pool rows), count of them

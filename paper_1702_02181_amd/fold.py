@@ -30,8 +30,10 @@ ERRORS = {-1: "FOLD_E_INVALID", -2: "FOLD_E_OP", -3: "FOLD_E_ARITY", -4: "FOLD_E
 FOLD_E_INVALID, FOLD_E_OP, FOLD_E_ARITY, FOLD_E_CHILD, FOLD_E_INPUT, FOLD_E_CYCLE = -1, -2, -3, -4, -5, -6
 FOLD_E_NOMEM, FOLD_E_DEVICE, FOLD_E_MISMATCH = -7, -8, -9
 FOLD_EMBED, FOLD_TREERNN, FOLD_TREELSTM, FOLD_LSTM, FOLD_PROJ = 0, 1, 2, 3, 4
+FOLD_ATTN_SCORE, FOLD_ATTN_SUM, FOLD_ATTN_OUT = 5, 6, 7
 FOLD_F32, FOLD_BF16 = 0, 1
-GATES = {FOLD_EMBED: 0, FOLD_TREERNN: 1, FOLD_TREELSTM: 5, FOLD_LSTM: 4, FOLD_PROJ: 1}
+GATES = {FOLD_EMBED: 0, FOLD_TREERNN: 1, FOLD_TREELSTM: 5, FOLD_LSTM: 4, FOLD_PROJ: 1,
+         FOLD_ATTN_SCORE: 0, FOLD_ATTN_SUM: 0, FOLD_ATTN_OUT: 0}
 
 
 class fold_op(ctypes.Structure):

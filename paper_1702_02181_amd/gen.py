@@ -574,8 +574,9 @@ def attention(seed: int = 6, num_graphs: int = 1024, length=(50, 100), hidden: i
     """Feed-forward attention (Section 3.4, Appendix A): `num_graphs` sequences of T ~ U{length} elements,
     each element a row of a table of token vectors (N(0, 1) entries, one distinct row per element), the
     model of attention_sequence with a PROJ output layer g.  Ops: EMBED, PROJ f, ATTN_SCORE, ATTN_SUM,
-    ATTN_OUT, PROJ g; weights U(-0.1, 0.1) except the scorer, U(-1, 1) (so that the attention weights are
-    far from uniform); forward and backward."""
+    ATTN_OUT, PROJ g; weights U(-0.1, 0.1), the scorer's too (scores of standard deviation ~0.5, so that the
+    attention weights of one sequence spread over a factor of ~3 between items one deviation apart); forward
+    and backward."""
     rng = np.random.default_rng(seed)
     H = hidden
     graphs = []
@@ -591,7 +592,6 @@ def attention(seed: int = 6, num_graphs: int = 1024, length=(50, 100), hidden: i
            OpSpec(KIND_ATTN_SUM, 2, 0, 3), OpSpec(KIND_ATTN_OUT, 1, 0, 4), OpSpec(KIND_PROJ, 1, 0, 5)]
     X = _finish_values(rng.standard_normal((row, H)), dtype)
     score = make_param_set(rng, KIND_ATTN_SCORE, 0, 1, H, dtype)
-    score.W_rec = _finish_values(rng.uniform(-1.0, 1.0, size=(H, 1)), dtype)
     params = [make_param_set(rng, KIND_EMBED, H, 0, H, dtype), make_param_set(rng, KIND_PROJ, 0, 1, H, dtype),
               score, make_param_set(rng, KIND_ATTN_SUM, 0, 2, H, dtype),
               make_param_set(rng, KIND_ATTN_OUT, 0, 1, H, dtype), make_param_set(rng, KIND_PROJ, 0, 1, H, dtype)]

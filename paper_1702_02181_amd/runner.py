@@ -49,7 +49,8 @@ class DeviceRun:
                 kind=p.kind, in_dim=p.in_dim, arity=p.arity,
                 W_in=None if p.W_in is None else self._wt(p.W_in),
                 W_rec=None if p.W_rec is None else self._wt(p.W_rec),
-                bias=None if p.kind == gen.KIND_EMBED else torch.from_numpy(p.bias.astype(np.float32)).to(device)))
+                bias=(None if p.kind == gen.KIND_EMBED or p.bias is None or p.bias.size == 0
+                      else torch.from_numpy(p.bias.astype(np.float32)).to(device))))
         self.packed = F.Packed(self.fdtype, H, self.set_tensors, stream)
         in_dim = int(w.leaf_table.shape[1])
         self.tld = F.fold_row_ld(in_dim)
@@ -86,10 +87,13 @@ class DeviceRun:
         sets = []
         for p in self.w.params:
             g = gen.NUM_GATES[p.kind] * self.H
-            if p.kind == gen.KIND_EMBED:
+            z = lambda *s: torch.zeros(s, dtype=torch.float32, device=self.device)
+            if p.kind == gen.KIND_ATTN_SCORE:  # dw as [H, 1], db [1]
+                sets.append((None, z(self.H, 1), z(1)))
+                continue
+            if p.kind == gen.KIND_EMBED or p.kind in gen.ATTN_KINDS:
                 sets.append((None, None, None))
                 continue
-            z = lambda *s: torch.zeros(s, dtype=torch.float32, device=self.device)
             sets.append((z(p.in_dim, g) if p.W_in is not None else None,
                          z(p.arity * self.H, g) if p.W_rec is not None else None, z(g)))
         self.grad_tensors = sets

@@ -74,16 +74,17 @@ def run_oracle(w, dh_nodes=None, table_grad=False, backward=None, u_mask=None):
     return out
 
 
-def compare_all(w, g, o, tol=None, check_backward=None, table_grad=False):
+def compare_all(w, g, o, tol=None, check_backward=None, table_grad=False, whole_keys=()):
+    """whole_keys: state tensors among h, c, dh, dc compared as one row (like the weight gradients)."""
     tol = TOL[w.dtype] if tol is None else tol
     errs = {}
-    errs["h"] = compare.rel_err(g["h"], o["h"])
-    errs["c"] = compare.rel_err(g["c"], o["c"])
+    errs["h"] = compare.rel_err(g["h"], o["h"], whole="h" in whole_keys)
+    errs["c"] = compare.rel_err(g["c"], o["c"], whole="c" in whole_keys)
     errs["roots"] = compare.rel_err(g["roots"], o["h"][o["roots_nodes"]])
     check_backward = w.backward if check_backward is None else check_backward
     if check_backward:
-        errs["dh"] = compare.rel_err(g["dh"], o["dh"])
-        errs["dc"] = compare.rel_err(g["dc"], o["dc"])
+        errs["dh"] = compare.rel_err(g["dh"], o["dh"], whole="dh" in whole_keys)
+        errs["dc"] = compare.rel_err(g["dc"], o["dc"], whole="dc" in whole_keys)
         for s, (gg, oo) in enumerate(zip(g["grads"], o["grads"])):
             for name in ("W_in", "W_rec", "bias"):
                 if gg.get(name) is None or oo.get(name) is None:
@@ -96,7 +97,7 @@ def compare_all(w, g, o, tol=None, check_backward=None, table_grad=False):
     return errs
 
 
-def sampled_parity(w, sample, table_grad, u_mask=None, dh_nodes=None):
+def sampled_parity(w, sample, table_grad, u_mask=None, dh_nodes=None, exclude=(), raw=False, whole_keys=()):
     """Parity of a full-size batch on sampled graphs, for batches too large for the node-by-node oracle.
 
     Two properties that hold at any size carry it: batching invariance (a graph's states inside the batch
@@ -105,7 +106,8 @@ def sampled_parity(w, sample, table_grad, u_mask=None, dh_nodes=None):
     on every other graph, those graphs contribute exactly nothing: the full-batch weight gradients equal
     the oracle's on the sampled graphs alone, and every other node's gradient is exactly 0).
     u_mask, dh_nodes: [N, H] in node order (recurrent-dropout mask, per-node upstream gradient) or None;
-    dh_nodes is zeroed outside the sampled graphs here."""
+    dh_nodes is zeroed outside the sampled graphs here.  exclude: gradient keys ("set<s>.<name>") left to the
+    caller, who gets (errs, the device results, the oracle's on the sample, the sample's node rows) with raw."""
     from paper_1702_02181_amd import gen
     tol = TOL[w.dtype]
     rpg = gen.roots_per_graph(w.graph_ptr, w.child_idx)
@@ -124,17 +126,33 @@ def sampled_parity(w, sample, table_grad, u_mask=None, dh_nodes=None):
     sub = gen.subset(w, sample)
     o = run_oracle(sub, dh_nodes=None if dh_nodes is None else dh_nodes[rows].astype(np.float64),
                    table_grad=table_grad, u_mask=None if u_mask is None else u_mask[rows])
-    errs = {k: compare.rel_err(g_out[k][rows], o[k]) for k in ("h", "c", "dh", "dc")}
+    errs = {k: compare.rel_err(g_out[k][rows], o[k], whole=k in whole_keys) for k in ("h", "c", "dh", "dc")}
     others = np.ones(w.num_nodes, bool)
     others[rows] = False
     assert np.all(g_out["dh"][others] == 0) and np.all(g_out["dc"][others] == 0)
     for s, (gg, oo) in enumerate(zip(g_out["grads"], o["grads"])):
         for name in ("W_in", "W_rec", "bias"):
-            if gg.get(name) is None or oo.get(name) is None:
+            if gg.get(name) is None or oo.get(name) is None or f"set{s}.{name}" in exclude:
                 continue
             errs[f"set{s}.{name}"] = compare.rel_err(gg[name], oo[name], whole=True)
     if table_grad:
         errs["d_table"] = compare.rel_err(g_out["d_table"], o["d_table"], whole=True)
     bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, (bad, errs)
-    return errs
+    return (errs, g_out, o, rows) if raw else errs
+
+
+def scorer_terms(w, o, pset):
+    """sum_r |de_r| over the attention-scorer rows of parameter set pset, de_r = dh_r . h_child(r) + dc_r[1]
+    (from the oracle's per-node gradients and states): the magnitude of the terms of the scorer's bias
+    gradient, the scale of that sum's rounding error."""
+    from paper_1702_02181_amd import gen
+    tot = 0.0
+    for v in range(w.num_nodes):
+        op = w.ops[int(w.node_op[v])]
+        if op.kind != gen.KIND_ATTN_SCORE or op.param_set != pset:
+            continue
+        c = int(w.child_idx[w.child_ptr[v]])
+        hc = o["h"][c] if c >= 0 else np.zeros(w.hidden)
+        tot += abs(float(np.dot(o["dh"][v], hc)) + float(o["dc"][v][1]))
+    return tot

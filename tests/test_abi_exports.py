@@ -71,6 +71,18 @@ def test_argument_checks_before_any_device_work(lib_path):
     with pytest.raises(F.FoldError) as e:
         pack(F.FOLD_TREELSTM, 1_000_000, 2, 4096)
     assert "2^32" in str(e.value)
+    # attention sets: in_dim 0, the kind's child slots, hidden >= 2 (c holds m and s), a scorer with w and b
+    for args in ((F.FOLD_ATTN_SCORE, 0, 1, 1), (F.FOLD_ATTN_SUM, 0, 2, 1), (F.FOLD_ATTN_SCORE, 8, 1, 64),
+                 (F.FOLD_ATTN_SCORE, 0, 2, 64), (F.FOLD_ATTN_SUM, 0, 1, 64), (F.FOLD_ATTN_OUT, 0, 2, 64),
+                 (8, 0, 1, 64)):
+        with pytest.raises(F.FoldError) as e:
+            pack(*args)
+        assert e.value.code == F.FOLD_E_INVALID, args
+    sets = (F.fold_param_set * 1)()
+    sets[0] = F.fold_param_set(F.FOLD_ATTN_SCORE, 0, 1, None, None, bias)
+    with pytest.raises(F.FoldError) as e:
+        F.fold_pack_params(F.fold_params(F.FOLD_F32, 64, 1, sets), null_stream)
+    assert e.value.code == F.FOLD_E_INVALID and "scorer" in str(e.value)
     for args in ((16, ft, None, ft, ft, ft, 1e-3, 0.9, 0.999, 1e-8, 0),
                  (16, ft, None, ft, ft, ft, 1e-3, 0.9, 1.0, 1e-8, 1),
                  (16, ft, None, ft, ft, ft, float("inf"), 0.9, 0.999, 1e-8, 1),

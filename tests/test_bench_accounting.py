@@ -133,3 +133,32 @@ def test_counters_table_from_rocprof_csvs(tmp_path):
     assert row[5].strip() == f"{2 * 512e6 / 2e-3 / 1e12:.0f}"          # executed MFMA TFLOP/s
     assert row[6].strip() == f"{2e6 * 1024 * 2 / 1e9:.1f}"             # FETCH_SIZE scaled by 2
     assert row[7].strip() == f"{1e6 * 1024 / 1e9:.1f}"                 # WRITE_SIZE scaled by 1
+
+
+def test_attention_pass_bytes():
+    """Feed-forward attention passes: an aggregate is acc (H pool values) + (m, s); a gradient dh (fp32) + ds."""
+    H = 16
+    w = types.SimpleNamespace(
+        hidden=H, dtype="bf16", backward=True,
+        ops=[gen.OpSpec(gen.KIND_ATTN_SCORE, 1, 0, 0), gen.OpSpec(gen.KIND_ATTN_SUM, 2, 0, 1),
+             gen.OpSpec(gen.KIND_ATTN_OUT, 1, 0, 2)],
+        params=[types.SimpleNamespace(in_dim=0)] * 3)
+    host = dict(group_op=[0, 1, 2], group_rows=[8, 4, 1])
+    work = bench.pass_work(w, host, table_grad=False)
+    agg, grad = 2 * H + 8, 4 * H + 4
+    assert work[("fwd", 0)] == (2.0 * 8 * H, 8 * (2 * H + agg) + 2 * H)     # item read, aggregate written, w
+    assert work[("bwd", 0)] == (0.0, 8 * (grad + 2 * H + grad) + 2 * H)    # dh, ds, item in; item's gradient out
+    assert work[("fwd", 1)] == (0.0, 4 * 3 * agg)                           # two aggregates in, one out
+    assert work[("bwd", 1)] == (0.0, 4 * (grad + 16 + 2 * grad))
+    assert work[("fwd", 2)] == (0.0, 1 * (agg + 2 * H))
+    assert work[("bwd", 2)] == (0.0, 1 * (4 * H + agg + grad))
+    assert work[("wgrad", 0)] == (2.0 * 8 * H, 8 * (4 + 2 * H) + (H + 1) * 4)
+    assert ("wgrad", 1) not in work and ("wgrad", 2) not in work
+    k = bench.attn_kernel_bytes(w, host)
+    assert k == {"attn_fwd.score": work[("fwd", 0)][1], "attn_bwd.score": work[("bwd", 0)][1],
+                 "attn_fwd.sum": work[("fwd", 1)][1], "attn_bwd.sum": work[("bwd", 1)][1],
+                 "attn_fwd.out": work[("fwd", 2)][1], "attn_bwd.out": work[("bwd", 2)][1],
+                 "attn_wgrad": work[("wgrad", 0)][1]}
+    assert bench.pass_of("attn_fwd.sum", 1, 1) == [("fwd", 1)]
+    assert bench.pass_of("attn_bwd.out", 2, 2) == [("bwd", 2)]
+    assert bench.pass_of("attn_wgrad", -1, 0) == [("wgrad", 0)]

@@ -160,3 +160,73 @@ def test_compiled_trees_on_gpu(dtype):
     ids = [out.id for out in outs]
     from oracle import compare
     assert compare.rel_err(g["h"][ids], o["h"][ids]) <= C.TOL[dtype]
+
+
+SC, SM, AO, PJ = gen.KIND_ATTN_SCORE, gen.KIND_ATTN_SUM, gen.KIND_ATTN_OUT, gen.KIND_PROJ
+
+
+def attention_expr():
+    """Feed-forward attention over a sequence of token rows (Section 3.4): h_t = f(x_t) (embedding, PROJ f),
+    scored, the scored items merged by a balanced Reduce, the attention output, then PROJ g."""
+    item = B.Scalar() >> B.Op(EMB, 0) >> B.Op(PJ, 1) >> B.Op(SC, 2)
+    return B.Map(item) >> B.Reduce(B.Op(SM, 3)) >> B.Op(AO, 4) >> B.Op(PJ, 5)
+
+
+def _attention_params(H, dtype="f32", seed=0):
+    rng = np.random.default_rng(seed)
+    return [gen.ParamSet(EMB, H, 0, None, None, np.zeros(0, np.float32)),
+            gen.make_param_set(rng, PJ, 0, 1, H, dtype),
+            gen.make_param_set(rng, SC, 0, 1, H, dtype),
+            gen.make_param_set(rng, SM, 0, 2, H, dtype),
+            gen.make_param_set(rng, AO, 0, 1, H, dtype),
+            gen.make_param_set(rng, PJ, 0, 1, H, dtype)]
+
+
+def test_attention_expression_matches_the_softmax_equation():
+    """The compiled attention model evaluated by the oracle equals g(softmax(w . f(x_t) + b) . f(x_t)) computed
+    directly from the equation on each whole sequence (scipy's softmax); the empty sequence gives g(0)."""
+    from scipy.special import softmax
+    H, V = 6, 30
+    c = B.Compiler(attention_expr())
+    assert c.ops == [gen.OpSpec(EMB, 0, 1, 0), gen.OpSpec(PJ, 1, 0, 1), gen.OpSpec(SC, 1, 0, 2),
+                     gen.OpSpec(SM, 2, 0, 3), gen.OpSpec(AO, 1, 0, 4), gen.OpSpec(PJ, 1, 0, 5)]
+    rng = np.random.default_rng(9)
+    table = rng.standard_normal((V, H)).astype(np.float32)
+    params = _attention_params(H, seed=9)
+    params[2].W_rec = rng.uniform(-1, 1, (H, 1)).astype(np.float32)  # peaked weights: a stronger check
+    seqs = [[int(x) for x in rng.integers(0, V, n)] for n in (1, 2, 5, 16, 33)] + [[]]
+    w, outs = c.build(seqs, params, H, table)
+    h = _oracle_states(w)
+    P = oracle_params(w)
+    f = lambda x: np.tanh(x @ P[1]["W_rec"] + P[1]["bias"])
+    g = lambda x: np.tanh(x @ P[5]["W_rec"] + P[5]["bias"])
+    for s, out in zip(seqs, outs):
+        if s:
+            hs = f(table[s].astype(np.float64))
+            e = hs @ P[2]["W_rec"][:, 0] + P[2]["bias"][0]
+            want = g(softmax(e) @ hs)
+        else:
+            want = g(np.zeros(H))
+        np.testing.assert_allclose(h[out.id], want, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_compiled_attention_on_gpu(dtype):
+    from tests import gpu_common as C
+    rng = np.random.default_rng(8)
+    H, V = 64, 300
+    seqs = [[int(x) for x in rng.integers(0, V, n)] for n in rng.integers(0, 60, 48)]
+    table = gen._finish_values(rng.standard_normal((V, H)), dtype)
+    w, outs = B.Compiler(attention_expr()).build(seqs, _attention_params(H, dtype, seed=4), H, table, dtype=dtype,
+                                                 seed=6)
+    g = C.run_device(w, table_grad=True)
+    C.assert_schedule_equal(g["sched"], C.oracle_schedule(w))
+    o = C.run_oracle(w, table_grad=True)
+    # the scorer's bias gradient is exactly 0 here (only the outputs carry a gradient and softmax ignores a
+    # common shift of the scores): compared against the magnitude of its terms instead of its own value; the
+    # gradient of an attention node's c (its one entry ds) as one tensor
+    db = float(g["grads"][2]["bias"][0])
+    g["grads"][2]["bias"] = None
+    C.compare_all(w, g, o, table_grad=True, whole_keys=("dc",))
+    assert abs(db - float(o["grads"][2]["bias"][0])) <= C.TOL[dtype] * C.scorer_terms(w, o, 2)
