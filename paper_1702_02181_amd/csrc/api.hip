@@ -185,7 +185,9 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
   WsLayout w;
   int gmax = 1;
   for (const fold_op& o : s.ops) gmax = std::max(gmax, gates_of(o.kind));
-  w.gstride = gmax * p.HP;
+  // a row's saved activations, then its dz: fp32 with fp32 parameters; fp16 activations and bf16 dz (G * HP
+  // halves) with bf16 parameters
+  w.gstride = p.dtype == FOLD_BF16 ? gmax * p.HP / 2 : gmax * p.HP;
   const size_t N = (size_t)s.N;
   auto al = [](size_t x) { return (x + 255) / 256 * 256; };
   w.gates_off = 0;

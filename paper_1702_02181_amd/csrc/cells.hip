@@ -113,15 +113,34 @@ struct CKids {
   static constexpr int N = KIND == FOLD_TREELSTM ? 2 : ((KIND == FOLD_LSTM || KIND == FOLD_PROJ) ? 1 : 0);
 };
 
+// Saved activation g of hidden unit j in a row's part of the workspace: fp32 with fp32 parameters; fp16 with
+// bf16 parameters (the backward then overwrites each with its bf16 dz in place).  fp16 keeps 11 significant
+// bits where bf16 keeps 8: the backward multiplies dc by the forget gates level after level, and over
+// 512-level chains bf16 gates would add ~1e-2 to dc's relative error, fp16 gates ~1e-3.
+template <typename T>
+struct SavedGates {
+  float* f;
+  uint16_t* h;
+  __device__ __forceinline__ SavedGates(float* row, int j) {
+    f = row ? row + j : nullptr;
+    h = row ? reinterpret_cast<uint16_t*>(row) + j : nullptr;
+  }
+  __device__ __forceinline__ explicit operator bool() const { return f != nullptr; }
+  __device__ __forceinline__ void put(int off, float v) const {
+    if constexpr (sizeof(T) == 4)
+      f[off] = v;
+    else
+      h[off] = __builtin_bit_cast(uint16_t, (_Float16)v);
+  }
+};
+
 // The cell on one (row, unit) given z (bias included) and the children's c (0 for the zero state):
 // writes h, c and the saved activations.
 template <typename T, int KIND>
 __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const float* z, float cl, float cr) {
   const size_t p = (size_t)(a.row_begin + row);
   float h, c;
-  // saved activations stay fp32 whatever the parameters' type: the backward multiplies dc by the
-  // forget gates level after level, so their rounding would accumulate along deep chains
-  float* gs = a.gates ? a.gates + p * a.gstride + j : nullptr;
+  const SavedGates<T> gs(a.gates ? a.gates + p * a.gstride : nullptr, j);
   if constexpr (KIND == FOLD_TREELSTM) {
     const float i_ = sigmoidf_(z[0]), fl = sigmoidf_(z[1]), fr = sigmoidf_(z[2]), o = sigmoidf_(z[3]);
     const float u = tanhf_(z[4]);
@@ -129,11 +148,11 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
     c = i_ * um + fl * cl + fr * cr;
     h = o * tanhf_(c);
     if (gs) {
-      gs[0] = i_;
-      gs[a.HP] = fl;
-      gs[2 * a.HP] = fr;
-      gs[3 * a.HP] = o;
-      gs[4 * a.HP] = u;
+      gs.put(0, i_);
+      gs.put(a.HP, fl);
+      gs.put(2 * a.HP, fr);
+      gs.put(3 * a.HP, o);
+      gs.put(4 * a.HP, u);
     }
   } else if constexpr (KIND == kTreeLstmLeaf) {
     const float i_ = sigmoidf_(z[0]), o = sigmoidf_(z[1]), u = tanhf_(z[2]);
@@ -142,9 +161,9 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
     c = i_ * (a.u_mask ? u * a.u_mask[p * a.ld + j] : u);
     h = o * tanhf_(c);
     if (gs) {
-      gs[0] = i_;
-      gs[a.HP] = o;
-      gs[2 * a.HP] = u;
+      gs.put(0, i_);
+      gs.put(a.HP, o);
+      gs.put(2 * a.HP, u);
     }
   } else if constexpr (KIND == FOLD_LSTM) {
     const float i_ = sigmoidf_(z[0]), f = sigmoidf_(z[1]), o = sigmoidf_(z[2]);
@@ -153,17 +172,17 @@ __device__ __forceinline__ void cell_out(const FwdArgs& a, int row, int j, const
     c = i_ * um + f * cl;
     h = o * tanhf_(c);
     if (gs) {
-      gs[0] = i_;
-      gs[a.HP] = f;
-      gs[2 * a.HP] = o;
-      gs[3 * a.HP] = u;
+      gs.put(0, i_);
+      gs.put(a.HP, f);
+      gs.put(2 * a.HP, o);
+      gs.put(3 * a.HP, u);
     }
   } else {
     h = tanhf_(z[0]);
     c = 0.f;
     if constexpr (KIND == FOLD_PROJ) c = cl;
     (void)cr;
-    if (gs) gs[0] = h;
+    if (gs) gs.put(0, h);
   }
   static_cast<T*>(a.h_pool)[p * a.ld + j] = from_f32<T>(h);
   a.c_pool[p * a.ld + j] = c;
@@ -533,16 +552,22 @@ __global__ void k_bwd_roots(int ld, const float* dh_roots, const int* root_pos, 
   for (int j = threadIdx.x; j < ld; j += blockDim.x) dh[p * ld + j] += dh_roots[(size_t)r * ld + j];
 }
 
-// dz of one row from its saved activations.  fp32 parameters: dz overwrites the activations in place
-// (each thread rewrites only the elements it read).  bf16 parameters: dz goes to the first G*HP bf16
-// slots of the row, the matrix-core operand of dz . W^T and of the weight gradients; the row is first
-// read completely, the bf16 values are staged in LDS (dynamic, G*HP halves) and then written out.
+// dz of one row from its saved activations, written over them in place (each thread rewrites only the
+// elements it read): fp32 dz over fp32 activations (fp32 parameters), or bf16 dz over fp16 activations
+// (bf16 parameters: the G*HP halves at the row's start, the matrix-core operand of dz . W^T and of the
+// weight gradients).
 template <int KIND, bool BF>
-__device__ __forceinline__ void cell_bwd_body(const BwdCellArgs a, int row, uint16_t* sdz) {
+__device__ __forceinline__ void cell_bwd_body(const BwdCellArgs a, int row) {
   constexpr int G = Gates<KIND>::G;
   const size_t p = (size_t)(a.row_begin + row);
   float* gb = a.gates + p * a.gstride;
-  auto gate = [&](int g, int j) -> float { return gb[g * a.HP + j]; };  // saved activations (fp32)
+  uint16_t* gh = reinterpret_cast<uint16_t*>(gb);
+  auto gate = [&](int g, int j) -> float {
+    if constexpr (BF)
+      return (float)__builtin_bit_cast(_Float16, gh[g * a.HP + j]);
+    else
+      return gb[g * a.HP + j];
+  };
   int c0 = -1, c1 = -1;
   bool s0 = false, s1 = false;
   if (a.arity >= 1) {
@@ -555,7 +580,7 @@ __device__ __forceinline__ void cell_bwd_body(const BwdCellArgs a, int row, uint
   }
   auto put = [&](int g, int j, float v) {
     if constexpr (BF)
-      sdz[g * a.HP + j] = f2bf(v);
+      gh[g * a.HP + j] = f2bf(v);
     else
       gb[g * a.HP + j] = v;
   };
@@ -624,18 +649,11 @@ __device__ __forceinline__ void cell_bwd_body(const BwdCellArgs a, int row, uint
       (void)dc0;
     }
   }
-  if constexpr (BF && KIND != FOLD_EMBED) {
-    __syncthreads();  // every read of the row's activations is done and the staged dz is complete
-    uint4* dst = reinterpret_cast<uint4*>(gb);
-    const uint4* src = reinterpret_cast<const uint4*>(sdz);
-    for (int v = threadIdx.x; v < G * a.HP / 8; v += blockDim.x) dst[v] = src[v];
-  }
 }
 
 template <int KIND, bool BF>
 __global__ void k_cell_bwd(BwdCellArgs a) {
-  extern __shared__ __attribute__((aligned(16))) uint16_t sdz[];
-  cell_bwd_body<KIND, BF>(a, blockIdx.x, sdz);
+  cell_bwd_body<KIND, BF>(a, blockIdx.x);
 }
 
 // ---------------------------------------------------------------- backward, dz . W^T
@@ -927,17 +945,16 @@ __global__ void k_level_epi(Merged<FwdArgs> m) {
 // cell backward of a level: one workgroup per row; variant = kind (the embedding writes no dz)
 template <bool BF>
 __global__ void k_level_cbwd(Merged<BwdCellArgs> m) {
-  extern __shared__ __attribute__((aligned(16))) uint16_t sdz[];
   const int i = merged_part(m.begin, m.n, blockIdx.x);
   const int row = blockIdx.x - m.begin[i];
   const BwdCellArgs a = m.a[i];
   switch (m.variant[i]) {
-    case FOLD_EMBED: cell_bwd_body<FOLD_EMBED, false>(a, row, sdz); break;
-    case FOLD_TREERNN: cell_bwd_body<FOLD_TREERNN, BF>(a, row, sdz); break;
-    case FOLD_TREELSTM: cell_bwd_body<FOLD_TREELSTM, BF>(a, row, sdz); break;
-    case FOLD_LSTM: cell_bwd_body<FOLD_LSTM, BF>(a, row, sdz); break;
-    case FOLD_PROJ: cell_bwd_body<FOLD_PROJ, BF>(a, row, sdz); break;
-    case kTreeLstmLeaf: cell_bwd_body<kTreeLstmLeaf, BF>(a, row, sdz); break;
+    case FOLD_EMBED: cell_bwd_body<FOLD_EMBED, false>(a, row); break;
+    case FOLD_TREERNN: cell_bwd_body<FOLD_TREERNN, BF>(a, row); break;
+    case FOLD_TREELSTM: cell_bwd_body<FOLD_TREELSTM, BF>(a, row); break;
+    case FOLD_LSTM: cell_bwd_body<FOLD_LSTM, BF>(a, row); break;
+    case FOLD_PROJ: cell_bwd_body<FOLD_PROJ, BF>(a, row); break;
+    case kTreeLstmLeaf: cell_bwd_body<kTreeLstmLeaf, BF>(a, row); break;
     default: break;
   }
 }
@@ -1087,9 +1104,8 @@ void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
   ProfScope prof(nk >= 0 && nk <= FOLD_PROJ ? names[nk] : "cell_bwd", st);
   // one thread per hidden unit (up to 1024): every load of a row is in flight at once
   dim3 grid(a.rows), block(std::min(a.HP, 1024));
-  const size_t lds = a.dz_bf16 ? (size_t)gates_of(kind) * a.HP * sizeof(uint16_t) : 0;
 #define FOLD_CB(K_)                                                                          \
-  if (a.dz_bf16) hipLaunchKernelGGL((k_cell_bwd<K_, true>), grid, block, lds, st, a);        \
+  if (a.dz_bf16) hipLaunchKernelGGL((k_cell_bwd<K_, true>), grid, block, 0, st, a);          \
   else hipLaunchKernelGGL((k_cell_bwd<K_, false>), grid, block, 0, st, a);
   switch (kind) {
     case FOLD_EMBED: hipLaunchKernelGGL((k_cell_bwd<FOLD_EMBED, false>), grid, block, 0, st, a); break;
@@ -1190,7 +1206,6 @@ void launch_level_cbwd(const int* kinds, const BwdCellArgs* args, int n, hipStre
   m.n = 0;
   int total = 0, hp = 0;
   bool bf = false;
-  size_t lds = 0;
   for (int k = 0; k < n; ++k) {
     if (args[k].rows <= 0) continue;
     m.begin[m.n] = total;
@@ -1198,16 +1213,13 @@ void launch_level_cbwd(const int* kinds, const BwdCellArgs* args, int n, hipStre
     m.a[m.n++] = args[k];
     total += args[k].rows;
     hp = args[k].HP;
-    if (kinds[k] != FOLD_EMBED && args[k].dz_bf16) {
-      bf = true;
-      lds = std::max(lds, (size_t)gates_of(kinds[k]) * args[k].HP * sizeof(uint16_t));
-    }
+    if (kinds[k] != FOLD_EMBED && args[k].dz_bf16) bf = true;
   }
   if (m.n == 0) return;
   m.begin[m.n] = total;
   ProfScope prof("cell_bwd.level", st);
   if (bf)
-    hipLaunchKernelGGL(k_level_cbwd<true>, dim3(total), dim3(std::min(hp, 1024)), lds, st, m);
+    hipLaunchKernelGGL(k_level_cbwd<true>, dim3(total), dim3(std::min(hp, 1024)), 0, st, m);
   else
     hipLaunchKernelGGL(k_level_cbwd<false>, dim3(total), dim3(std::min(hp, 1024)), 0, st, m);
 }

@@ -19,7 +19,7 @@ void packed_destroy_impl(fold_packed* h);
 constexpr int kMaxMerge = 4;  // groups of one level in one launch
 
 struct WsLayout {
-  int gstride = 0;           // floats per pool row of saved gates / dz: Gmax * HP
+  int gstride = 0;           // floats per pool row of saved gates / dz: Gmax * HP (fp32), Gmax * HP / 2 (bf16)
   size_t gates_off = 0, gates_bytes = 0;
   size_t zpart_off = 0, zpart_bytes = 0;  // K-split partial sums of narrow forward levels
   size_t dh_off = 0, dc_off = 0, acc_bytes = 0;
