@@ -13,11 +13,11 @@
 // acc / s with respect to the items and the scores.
 //
 // The operations are O(H) per node and HBM-bound: one wave per pool row (four rows per workgroup), each lane
-// owning the row's columns lane, lane + 64, ...; the dot products of the scorer and of the output's backward
-// are wave sums of a fixed butterfly order.  The backward adds into the children's dh / dc directly (a plain
+// owning four consecutive columns of every 256 (16-byte fp32, 8-byte bf16 accesses); the dot products of the
+// scorer and of the output's backward are wave sums of a fixed butterfly order.  The backward adds into the children's dh / dc directly (a plain
 // read-add-write for a child with one parent edge, a hardware fp32 atomic otherwise), so no dz . W^T pass
 // follows.  The scorer's weight gradient, dw = sum_r de_r h_c(r) and db = sum_r de_r, is reduced in fixed
-// chunk order from the de each row's backward saves.
+// order (rows within a chunk, chunks within a quarter, quarters) from the de each row's backward saves.
 
 #include <hip/hip_runtime.h>
 
@@ -41,11 +41,47 @@ __device__ __forceinline__ double wave_total(double v) {
   return v;
 }
 
-template <typename T>
-__device__ __forceinline__ float ld_h(const T* h, int row, int ld, int j) {
-  return row >= 0 ? to_f32<T>(h[(size_t)row * ld + j]) : 0.f;
+// four consecutive columns j .. j + 3 of a row (j a multiple of 4; rows are multiples of 64 wide)
+__device__ __forceinline__ void ld4(const float* p, float (&v)[4]) {
+  const float4 t = *reinterpret_cast<const float4*>(p);
+  v[0] = t.x, v[1] = t.y, v[2] = t.z, v[3] = t.w;
 }
-
+__device__ __forceinline__ void ld4(const uint16_t* p, float (&v)[4]) {
+  const uint2 t = *reinterpret_cast<const uint2*>(p);
+  v[0] = bf2f(t.x & 0xffff), v[1] = bf2f(t.x >> 16), v[2] = bf2f(t.y & 0xffff), v[3] = bf2f(t.y >> 16);
+}
+__device__ __forceinline__ void st4(float* p, const float (&v)[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void st4(uint16_t* p, const float (&v)[4]) {
+  *reinterpret_cast<uint2*>(p) = make_uint2(f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
+                                            f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+}
+// columns j .. j + 3 of pool row `row` (zero for the zero state and past H)
+template <typename T>
+__device__ __forceinline__ void ld_h4(const T* h, int row, int ld, int H, int j, float (&v)[4]) {
+  if (row >= 0) {
+    ld4(h + (size_t)row * ld + j, v);
+  } else {
+    v[0] = v[1] = v[2] = v[3] = 0.f;
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (j + e >= H) v[e] = 0.f;
+}
+// dst[0..3] += v: one read-add-write of four floats for a row with a single writer, else fp32 atomics
+__device__ __forceinline__ void add4(float* dst, const float (&v)[4], bool single) {
+  if (single) {
+    float o[4];
+    ld4(dst, o);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] += v[e];
+    st4(dst, o);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) unsafeAtomicAdd(dst + e, v[e]);
+  }
+}
 // dst += v (dst's old value read first) when it has a single writer, else a hardware fp32 atomic add
 __device__ __forceinline__ void add_to(float* dst, float v, bool single) {
   if (single)
@@ -53,7 +89,15 @@ __device__ __forceinline__ void add_to(float* dst, float v, bool single) {
   else
     unsafeAtomicAdd(dst, v);
 }
+// the c row of an attention node: (m, s) in columns 0 and 1, zeros after
+__device__ __forceinline__ void put_ms(float* co, int ld, int lane, float m, float s) {
+  for (int j = 4 * lane; j < ld; j += 4 * kWave) {
+    const float v[4] = {j == 0 ? m : 0.f, j == 0 ? s : 0.f, 0.f, 0.f};
+    st4(co + j, v);
+  }
+}
 
+// Lanes own four consecutive columns each, 256 columns a wave step.
 template <typename T, int KIND>
 __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_fwd(AttnArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
@@ -67,13 +111,16 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_fwd(AttnArgs a) {
     const int c0 = a.child_pos[a.idx_off + row];
     const T* w = static_cast<const T*>(a.w);
     double part = 0.0;
-    for (int j = lane; j < a.ld; j += kWave) {
-      const float v = j < a.H ? ld_h(hp, c0, a.ld, j) : 0.f;
-      if (j < a.H) part += (double)v * to_f32<T>(w[j]);
-      ho[j] = from_f32<T>(v);
+    for (int j = 4 * lane; j < a.ld; j += 4 * kWave) {
+      float v[4], wv[4];
+      ld_h4(hp, c0, a.ld, a.H, j, v);
+      ld4(w + j, wv);  // zero past H
+#pragma unroll
+      for (int e = 0; e < 4; ++e) part += (double)v[e] * wv[e];
+      st4(ho + j, v);
     }
     const float e = (float)(wave_total(part) + a.bias[0]);
-    for (int j = lane; j < a.ld; j += kWave) co[j] = j == 0 ? e : (j == 1 ? 1.f : 0.f);
+    put_ms(co, a.ld, lane, e, 1.f);
   } else if constexpr (KIND == FOLD_ATTN_SUM) {
     const int c0 = a.child_pos[a.idx_off + 2 * row], c1 = a.child_pos[a.idx_off + 2 * row + 1];
     const float m0 = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld] : 0.f, s0 = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + 1] : 0.f;
@@ -81,25 +128,26 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_fwd(AttnArgs a) {
     const bool l0 = s0 != 0.f, l1 = s1 != 0.f;
     const float m = l0 && l1 ? fmaxf(m0, m1) : (l0 ? m0 : m1);
     const float x0 = l0 ? fast_exp(m0 - m) : 0.f, x1 = l1 ? fast_exp(m1 - m) : 0.f;
-    for (int j = lane; j < a.ld; j += kWave) {
-      float v = 0.f;
-      if (j < a.H) {
-        if (l0) v += x0 * ld_h(hp, c0, a.ld, j);
-        if (l1) v += x1 * ld_h(hp, c1, a.ld, j);
-      }
-      ho[j] = from_f32<T>(v);
+    for (int j = 4 * lane; j < a.ld; j += 4 * kWave) {
+      float v0[4], v1[4], v[4];
+      ld_h4(hp, l0 ? c0 : -1, a.ld, a.H, j, v0);
+      ld_h4(hp, l1 ? c1 : -1, a.ld, a.H, j, v1);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = x0 * v0[e] + x1 * v1[e];
+      st4(ho + j, v);
     }
-    const bool any = l0 || l1;
-    const float s = x0 * s0 + x1 * s1;
-    for (int j = lane; j < a.ld; j += kWave) co[j] = j == 0 ? (any ? m : 0.f) : (j == 1 ? s : 0.f);
+    put_ms(co, a.ld, lane, l0 || l1 ? m : 0.f, x0 * s0 + x1 * s1);
   } else {  // FOLD_ATTN_OUT
     const int c0 = a.child_pos[a.idx_off + row];
     const float s = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + 1] : 0.f;
-    for (int j = lane; j < a.ld; j += kWave) {
-      const float v = (j < a.H && s != 0.f) ? ld_h(hp, c0, a.ld, j) / s : 0.f;
-      ho[j] = from_f32<T>(v);
-      co[j] = 0.f;
+    for (int j = 4 * lane; j < a.ld; j += 4 * kWave) {
+      float v[4];
+      ld_h4(hp, s != 0.f ? c0 : -1, a.ld, a.H, j, v);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = s != 0.f ? v[e] / s : 0.f;
+      st4(ho + j, v);
     }
+    put_ms(co, a.ld, lane, 0.f, 0.f);
   }
 }
 
@@ -117,27 +165,55 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_bwd(AttnArgs a) {
     const bool one = a.child_one[a.idx_off + row] != 0;
     const T* w = static_cast<const T*>(a.w);
     double part = 0.0;
-    for (int j = lane; j < a.H; j += kWave) part += (double)dh[j] * ld_h(hp, c0, a.ld, j);
+    for (int j = 4 * lane; j < a.ld; j += 4 * kWave) {
+      float g[4], v[4];
+      ld4(dh + j, g);
+      ld_h4(hp, c0, a.ld, a.H, j, v);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) part += (double)g[e] * v[e];
+    }
     const float de = (float)(wave_total(part) + a.dc[p * a.ld + 1]);
     if (lane == 0 && a.gates) a.gates[p * a.gstride] = de;
     if (c0 >= 0)
-      for (int j = lane; j < a.H; j += kWave)
-        add_to(&a.dh[(size_t)c0 * a.ld + j], dh[j] + de * to_f32<T>(w[j]), one);
+      for (int j = 4 * lane; j < a.ld; j += 4 * kWave) {
+        float g[4], wv[4];
+        ld4(dh + j, g);
+        ld4(w + j, wv);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) g[e] = j + e < a.H ? g[e] + de * wv[e] : 0.f;
+        add4(&a.dh[(size_t)c0 * a.ld + j], g, one);
+      }
   } else if constexpr (KIND == FOLD_ATTN_SUM) {
     // with m fixed, acc and s are linear in the children's: dh_k += x_k dh, ds_k += x_k ds
     const float m = a.c_pool[p * a.ld];
     const float ds = a.dc[p * a.ld + 1];
+    int ck[2];
+    float xk[2];
+    bool one[2];
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
-      const int ck = a.child_pos[a.idx_off + 2 * row + k];
-      if (ck < 0) continue;
-      const float sk = a.c_pool[(size_t)ck * a.ld + 1];
-      if (sk == 0.f) continue;  // an empty set: x_k = 0
-      const float xk = fast_exp(a.c_pool[(size_t)ck * a.ld] - m);  // the forward's x_k, bit for bit
-      const bool one = a.child_one[a.idx_off + 2 * row + k] != 0;
-      for (int j = lane; j < a.H; j += kWave) add_to(&a.dh[(size_t)ck * a.ld + j], xk * dh[j], one);
-      if (lane == 0) add_to(&a.dc[(size_t)ck * a.ld + 1], xk * ds, one);
+      ck[k] = a.child_pos[a.idx_off + 2 * row + k];
+      one[k] = a.child_one[a.idx_off + 2 * row + k] != 0;
+      // an empty set (s = 0) takes no part: x_k = 0; else the forward's x_k, bit for bit
+      xk[k] = ck[k] >= 0 && a.c_pool[(size_t)ck[k] * a.ld + 1] != 0.f ? fast_exp(a.c_pool[(size_t)ck[k] * a.ld] - m)
+                                                                      : 0.f;
     }
+    for (int j = 4 * lane; j < a.ld; j += 4 * kWave) {
+      float g[4];
+      ld4(dh + j, g);
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        if (xk[k] == 0.f) continue;
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = j + e < a.H ? xk[k] * g[e] : 0.f;
+        add4(&a.dh[(size_t)ck[k] * a.ld + j], v, one[k]);
+      }
+    }
+    if (lane == 0)
+#pragma unroll
+      for (int k = 0; k < 2; ++k)
+        if (xk[k] != 0.f) add_to(&a.dc[(size_t)ck[k] * a.ld + 1], xk[k] * ds, one[k]);
   } else {  // FOLD_ATTN_OUT: h = acc / s -> dacc = dh / s, ds = -(dh . acc) / s^2
     const int c0 = a.child_pos[a.idx_off + row];
     if (c0 < 0) return;
@@ -145,23 +221,34 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_bwd(AttnArgs a) {
     if (s == 0.f) return;
     const bool one = a.child_one[a.idx_off + row] != 0;
     double part = 0.0;
-    for (int j = lane; j < a.H; j += kWave) part += (double)dh[j] * ld_h(hp, c0, a.ld, j);
+    for (int j = 4 * lane; j < a.ld; j += 4 * kWave) {
+      float g[4], v[4];
+      ld4(dh + j, g);
+      ld_h4(hp, c0, a.ld, a.H, j, v);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        part += (double)g[e] * v[e];
+        g[e] = j + e < a.H ? g[e] / s : 0.f;
+      }
+      add4(&a.dh[(size_t)c0 * a.ld + j], g, one);
+    }
     const double tot = wave_total(part);
-    for (int j = lane; j < a.H; j += kWave) add_to(&a.dh[(size_t)c0 * a.ld + j], dh[j] / s, one);
     if (lane == 0) add_to(&a.dc[(size_t)c0 * a.ld + 1], (float)(-tot / ((double)s * s)), one);
   }
 }
 
-// Partial sums of the scorer's gradient over chunks of the op's rows: column j < H of chunk q is
-// sum_r de_r h_c(r)[j] over the chunk's rows in order, column H (stored at HP) is sum_r de_r.
+// Partial sums of the scorer's gradient over chunks of kAttnWgradChunk op rows (workgroup x), one column
+// per thread (workgroup y: 256 columns): column j < H of chunk q is sum_r de_r h_c(r)[j] over the chunk's rows
+// in order; column HP holds sum_r de_r (thread 0 of the first column block).
 template <typename T>
-__global__ __launch_bounds__(256) void k_attn_wgrad(const int* op_rows, const int* op_cpos, int count, int chunk,
-                                                    int H, int HP, int ld, const T* h_pool, const float* gates,
+__global__ __launch_bounds__(256) void k_attn_wgrad(const int* op_rows, const int* op_cpos, int count, int H,
+                                                    int HP, int ld, const T* h_pool, const float* gates,
                                                     int gstride, float* part) {
   const int j = blockIdx.y * blockDim.x + threadIdx.x;
-  if (j > H) return;
-  const int q0 = blockIdx.x * chunk, q1 = min(count, q0 + chunk);
-  float acc = 0.f;
+  const bool bias = blockIdx.y == 0 && threadIdx.x == 0;
+  if (j >= H && !bias) return;
+  const int q0 = blockIdx.x * kAttnWgradChunk, q1 = min(count, q0 + kAttnWgradChunk);
+  float acc = 0.f, bsum = 0.f;
   int q = q0;
   // eight rows' loads in flight, added in row order
   for (; q + 8 <= q1; q += 8) {
@@ -169,29 +256,56 @@ __global__ __launch_bounds__(256) void k_attn_wgrad(const int* op_rows, const in
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       de[u] = gates[(size_t)op_rows[q + u] * gstride];
-      v[u] = j < H ? ld_h(h_pool, op_cpos[2 * (size_t)(q + u)], ld, j) : 1.f;
+      const int c = op_cpos[2 * (size_t)(q + u)];
+      v[u] = j < H && c >= 0 ? to_f32<T>(h_pool[(size_t)c * ld + j]) : 0.f;
     }
 #pragma unroll
-    for (int u = 0; u < 8; ++u) acc += de[u] * v[u];
+    for (int u = 0; u < 8; ++u) {
+      acc += de[u] * v[u];
+      bsum += de[u];
+    }
   }
   for (; q < q1; ++q) {
     const float de = gates[(size_t)op_rows[q] * gstride];
-    acc += de * (j < H ? ld_h(h_pool, op_cpos[2 * (size_t)q], ld, j) : 1.f);
+    const int c = op_cpos[2 * (size_t)q];
+    acc += de * (j < H && c >= 0 ? to_f32<T>(h_pool[(size_t)c * ld + j]) : 0.f);
+    bsum += de;
   }
-  part[(size_t)blockIdx.x * (HP + kPadK) + (j < H ? j : HP)] = acc;
+  float* out = part + (size_t)blockIdx.x * (HP + kPadK);
+  if (j < H) out[j] = acc;
+  if (bias) out[HP] = bsum;
 }
 
+// Sum of the chunks' partials, 64 columns (column H: the bias) per workgroup: the four waves sum a quarter
+// of the chunks each, in chunk order, and their sums are added in wave order.
 __global__ __launch_bounds__(256) void k_attn_wgrad_reduce(const float* part, int nchunk, int H, int HP, float* dw,
                                                            float* db) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j > H) return;
-  const int col = j < H ? j : HP;
+  __shared__ float red[4][kWave];
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x >> 6;
+  const int jc = blockIdx.x * kWave + lane;  // 0 .. H (H: the bias)
+  const bool live = jc <= H;
+  const int col = jc < H ? jc : HP;
+  const int per = (nchunk + 3) / 4, q0 = min(nchunk, w * per), q1 = min(nchunk, q0 + per);
   float acc = 0.f;
-  for (int q = 0; q < nchunk; ++q) acc += part[(size_t)q * (HP + kPadK) + col];
-  if (j < H) {
-    if (dw) dw[j] += acc;
+  if (live) {
+    int q = q0;
+    for (; q + 8 <= q1; q += 8) {
+      float t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = part[(size_t)(q + u) * (HP + kPadK) + col];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc += t[u];
+    }
+    for (; q < q1; ++q) acc += part[(size_t)q * (HP + kPadK) + col];
+  }
+  red[w][lane] = acc;
+  __syncthreads();
+  if (w != 0 || !live) return;
+  const float tot = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+  if (jc < H) {
+    if (dw) dw[jc] += tot;
   } else if (db) {
-    db[0] += acc;
+    db[0] += tot;
   }
 }
 
@@ -261,15 +375,15 @@ void launch_attn_wgrad(int dtype, const int* op_rows, const int* op_cpos, int co
   if (count <= 0 || (!dw && !db)) return;
   ProfScope prof("attn_wgrad", st);
   const int nchunk = attn_wgrad_chunks(count);
-  const dim3 grid((unsigned)nchunk, (unsigned)((H + 1 + 255) / 256));
+  const dim3 grid((unsigned)nchunk, (unsigned)((H + 255) / 256));
   if (dtype == FOLD_BF16)
-    hipLaunchKernelGGL(k_attn_wgrad<uint16_t>, grid, dim3(256), 0, st, op_rows, op_cpos, count, kAttnWgradChunk, H,
-                       HP, ld, static_cast<const uint16_t*>(h_pool), gates, gstride, part);
+    hipLaunchKernelGGL(k_attn_wgrad<uint16_t>, grid, dim3(256), 0, st, op_rows, op_cpos, count, H, HP, ld,
+                       static_cast<const uint16_t*>(h_pool), gates, gstride, part);
   else
-    hipLaunchKernelGGL(k_attn_wgrad<float>, grid, dim3(256), 0, st, op_rows, op_cpos, count, kAttnWgradChunk, H, HP,
-                       ld, static_cast<const float*>(h_pool), gates, gstride, part);
-  hipLaunchKernelGGL(k_attn_wgrad_reduce, dim3((unsigned)((H + 1 + 255) / 256)), dim3(256), 0, st, part, nchunk, H,
-                     HP, dw, db);
+    hipLaunchKernelGGL(k_attn_wgrad<float>, grid, dim3(256), 0, st, op_rows, op_cpos, count, H, HP, ld,
+                       static_cast<const float*>(h_pool), gates, gstride, part);
+  hipLaunchKernelGGL(k_attn_wgrad_reduce, dim3((unsigned)((H + 1 + kWave - 1) / kWave)), dim3(256), 0, st, part,
+                     nchunk, H, HP, dw, db);
 }
 
 void launch_pack_score(int dtype, int H, int HP, const void* w, const float* b, void* wdst, float* bdst,

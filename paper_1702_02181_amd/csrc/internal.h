@@ -221,7 +221,7 @@ struct AttnArgs {
   int gstride;
 };
 // rows of the scorer's weight gradient reduced by one workgroup (chunk order is fixed)
-constexpr int kAttnWgradChunk = 512;
+constexpr int kAttnWgradChunk = 128;
 int attn_wgrad_chunks(int count);
 void launch_attn_fwd(int dtype, int kind, const AttnArgs& a, hipStream_t st);
 void launch_attn_bwd(int dtype, int kind, const AttnArgs& a, hipStream_t st);
