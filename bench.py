@@ -52,8 +52,9 @@ CLASS_SOURCES = {
 COPY_KERNEL = "k_probe_copy"
 TRAFFIC_TAG = "traffic-record:"
 KIND_IDS = {"embed": 0, "treernn": 1, "treelstm": 2, "lstm": 3, "proj": 4}
-# template kind ids of a class's kernels: Tree-LSTM leaves run as their own kind (live gates only)
-KERNEL_KINDS = {"treelstm": (2, 5)}
+# template kind ids of a class's kernels: Tree-LSTM leaves run as their own kind (live gates only), the library's
+# internal kind kTreeLstmLeaf = 8 (after the ABI's kinds 0-7)
+KERNEL_KINDS = {"treelstm": (2, 8)}
 CTYPE = {"f32": "float", "bf16": "unsigned short"}
 
 

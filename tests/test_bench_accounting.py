@@ -90,9 +90,9 @@ def test_level_classes_split_and_fractions():
 def test_rocprof_roles_of_kernel_names():
     f = "cell_fwd.treelstm.f32"
     assert bench.rocprof_role(f, "void fold::(anonymous namespace)::k_cell_fwd_w<float, 2>(fold::FwdArgs)") == "main"
-    assert bench.rocprof_role(f, "void k_cell_fwd_w<float, 5>(fold::FwdArgs)") == "main"  # leaf kind
-    assert bench.rocprof_role(f, "void k_cell_fwd<float, 5, 1, true>(fold::FwdArgs)") == "main"
-    assert bench.rocprof_role(f, "void k_cell_epi<float, 5>(fold::FwdArgs, int)") == "extra"
+    assert bench.rocprof_role(f, "void k_cell_fwd_w<float, 8>(fold::FwdArgs)") == "main"  # leaf kind
+    assert bench.rocprof_role(f, "void k_cell_fwd<float, 8, 1, true>(fold::FwdArgs)") == "main"
+    assert bench.rocprof_role(f, "void k_cell_epi<float, 8>(fold::FwdArgs, int)") == "extra"
     assert bench.rocprof_role(f, "void k_cell_fwd<float, 3, 1, false>(fold::FwdArgs)") is None  # LSTM
     assert bench.rocprof_role(f, "void k_cell_fwd_w<unsigned short, 2>(fold::FwdArgs)") is None  # bf16
     assert bench.rocprof_role("cell_fwd.lstm.bf16", "void k_cell_fwd<unsigned short, 3, 2, false>(x)") == "main"
@@ -162,3 +162,20 @@ def test_attention_pass_bytes():
     assert bench.pass_of("attn_fwd.sum", 1, 1) == [("fwd", 1)]
     assert bench.pass_of("attn_bwd.out", 2, 2) == [("bwd", 2)]
     assert bench.pass_of("attn_wgrad", -1, 0) == [("wgrad", 0)]
+
+
+def test_rocprof_roles_follow_the_library_kind_ids():
+    """The rocprof name matcher knows the Tree-LSTM leaf kernels by the library's internal leaf kind id."""
+    import os
+    import re
+    src = open(os.path.join(os.path.dirname(bench.__file__), "paper_1702_02181_amd", "csrc", "common.h")).read()
+    leaf = int(re.search(r"constexpr int kTreeLstmLeaf = (\d+);", src).group(1))
+    assert leaf in bench.KERNEL_KINDS["treelstm"]
+    ns = "void fold::(anonymous namespace)::"
+    assert bench.rocprof_role("cell_fwd.treelstm.f32", f"{ns}k_cell_fwd_w<float, {leaf}>(fold::FwdArgs)") == "main"
+    assert bench.rocprof_role("cell_fwd.treelstm.f32", f"{ns}k_cell_fwd_w<float, 2>(fold::FwdArgs)") == "main"
+    assert bench.rocprof_role("cell_fwd.treelstm.bf16",
+                              f"{ns}k_cell_fwd<unsigned short, 2, 1, true>(fold::FwdArgs)") == "main"
+    assert bench.rocprof_role("cell_fwd.treelstm.f32", f"{ns}k_cell_epi<float, {leaf}>(fold::FwdArgs, int)") == "extra"
+    assert bench.rocprof_role("cell_fwd.treelstm.f32", f"{ns}k_cell_fwd_w<float, 3>(fold::FwdArgs)") is None
+    assert bench.rocprof_role("cell_fwd.treelstm.f32", f"{ns}k_cell_fwd_w<unsigned short, 2>(fold::FwdArgs)") is None
