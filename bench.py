@@ -564,7 +564,8 @@ def attention_bench(steps: int, warmup: int) -> dict:
     t = sum(v["ms_per_step"] for v in attn.values())
     return {"metric": "graph nodes/sec (feed-forward attention fwd+bwd, 1 GPU)", "value": m["value"],
             "unit": "graph nodes/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
-            "ms_per_step": m["ms_per_step"], "eager_ms_per_step": m["eager_ms_per_step"], "higher_is_better": True,
+            "ms_per_step": m["ms_per_step"], "eager_ms_per_step": m["eager_ms_per_step"], "fwd_ms": m["fwd_ms"],
+            "bwd_ms": m["bwd_ms"], "higher_is_better": True,
             "dtype": m["dtype"], "data": "synthetic", "config": m["config"], "schedule_ms": m["schedule_ms"],
             "attention_kernels": {"ms_per_step": round(t, 4), "alg_bytes_per_step": by,
                                   "gbs": round(by / (t * 1e-3) / 1e9, 1),
@@ -712,6 +713,12 @@ def measure(w, steps: int, warmup: int, table_grad: bool, schedule_reps: int = 5
     graph_ms = timed(graph.launch)
     print(f"[bench{tag}] timed {steps} steps: graph {graph_ms:.3f} ms/step, eager {eager_ms:.3f} ms/step "
           f"({graph.num_nodes} graph nodes)", file=sys.stderr, flush=True)
+    # the forward alone, recorded and replayed the same way; the backward is the rest of the step
+    fwd_ms = graph_ms
+    if w.backward:
+        fgraph = dev.make_graph(backward=False)
+        fwd_ms = timed(fgraph.launch)
+        del fgraph
 
     # per-kernel durations over a second timed region (event pair around every launch, on the stream the
     # kernels run on)
@@ -776,6 +783,8 @@ def measure(w, steps: int, warmup: int, table_grad: bool, schedule_reps: int = 5
         "value": round(N / (graph_ms * 1e-3), 1),
         "ms_per_step": round(graph_ms, 4),
         "eager_ms_per_step": round(eager_ms, 4),
+        "fwd_ms": round(fwd_ms, 4),
+        "bwd_ms": round(graph_ms - fwd_ms, 4) if w.backward else None,
         "dtype": "f32" if w.dtype == "f32" else "bf16",
         "config": {"workload": w.name, "graphs": w.num_graphs, "nodes": N, "levels": dev.sched.num_levels,
                    "groups": len(host["group_op"]), "hidden": w.hidden,
@@ -919,6 +928,8 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": head["ms_per_step"],
         "eager_ms_per_step": head["eager_ms_per_step"],
+        "fwd_ms": head["fwd_ms"],
+        "bwd_ms": head["bwd_ms"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
