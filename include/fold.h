@@ -361,8 +361,10 @@ typedef struct {
  *   dh_roots             device [num_roots, ld(H)] fp32 or NULL
  *   dh_nodes             device [N, ld(H)] fp32 (pool order) or NULL
  *   dh_out, dc_out       device [N, ld(H)] fp32 (pool order) or NULL: receive every
- *                        node's total upstream gradient of h and c
- * Asynchronous; allocates nothing. */
+ *                        node's total upstream gradient of h and c (every row
+ *                        written whole)
+ * dh_roots, dh_nodes, dh_out, dc_out and ws must be 16-byte aligned
+ * (FOLD_E_INVALID otherwise).  Asynchronous; allocates nothing. */
 int32_t fold_backward(const fold_sched* sched, const fold_packed* packed,
                       const void* leaf_table, int64_t leaf_rows,
                       const void* h_pool, const float* c_pool,

@@ -532,6 +532,9 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
                       const float* u_mask) {
   const WsLayout L = workspace_layout(s, p);
   if (!ws || ws_bytes < L.bwd_bytes) return fail(FOLD_E_MISMATCH, "fold_backward: workspace too small");
+  const auto misaligned = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15) != 0; };
+  if (misaligned(dh_roots) || misaligned(dh_nodes) || misaligned(dh_out) || misaligned(dc_out) || misaligned(ws))
+    return fail(FOLD_E_INVALID, "fold_backward: dh_roots, dh_nodes, dh_out, dc_out and ws must be 16-byte aligned");
   TagScope tags;
   char* wsb = static_cast<char*>(ws);
   float* gates = reinterpret_cast<float*>(wsb + L.gates_off);
@@ -543,7 +546,11 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
   const int tld = row_ld(tw);
   float* d_table = grads ? grads->d_leaf_table : nullptr;
 
-  launch_bwd_init(s.N, s.R, p.ld, dh_nodes, dh_roots, s.root_pos, dh, dc, st);
+  // Rows of nodes with one parent edge are not initialised: that parent's backward stores them whole (dh
+  // rows only when no per-node upstream gradient has to be added to).
+  const int dh_fresh = dh_nodes == nullptr;
+  const int esize = p.dtype == FOLD_BF16 ? 2 : 4;
+  launch_bwd_init(s.N, s.R, p.ld, dh_nodes, dh_roots, s.root_pos, s.pos_npar, dh, dc, st);
   // Level by level from the top.  The groups of a level are independent (their children are at lower
   // levels), so all their cell backwards run first and then all their dz . W^T; narrow ones of a level run
   // as level launches (tagged with the first group of the span and op = -1 - span).
@@ -585,12 +592,16 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
         at.dc = dc;
         at.gates = gates;
         at.gstride = L.gstride;
+        at.dh_fresh = dh_fresh;
         attn.push_back(at);
         attn_kind.push_back(op.kind);
         attn_group.push_back(g);
         continue;
       }
       const bool leaf = is_tree_lstm_leaf(op);
+      const int Kb = (leaf ? gates_of(kTreeLstmLeaf) : ps.G) * p.HP;
+      // a dz . W^T whose K slices add into the children atomically needs their dh rows zeroed first
+      b.zero_child_dh = dh_fresh && op.arity > 0 && dx_plan(b.rows, op.arity * p.HP, Kb, esize, true).ksplit > 1;
       ckind.push_back(leaf ? kTreeLstmLeaf : op.kind);
       cargs.push_back(b);
       if (op.kind == FOLD_EMBED) continue;
@@ -603,7 +614,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       d.HP = p.HP;
       d.ld = p.ld;
       d.gstride = L.gstride;
-      d.Kb = (leaf ? gates_of(kTreeLstmLeaf) : ps.G) * p.HP;
+      d.Kb = Kb;
       d.dz = gates;
       d.dh = dh;
       d.child_pos = s.child_pos;
@@ -612,6 +623,7 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       d.in_dim = ps.in_dim;
       d.tld = tld;
       d.child_one = s.child_one;
+      d.dh_fresh = dh_fresh;
       d.can_split = 1;
       d.zero = p.zero;
       if (op.arity > 0) {

@@ -69,9 +69,20 @@ __device__ __forceinline__ void ld_h4(const T* h, int row, int ld, int H, int j,
   for (int e = 0; e < 4; ++e)
     if (j + e >= H) v[e] = 0.f;
 }
-// dst[0..3] += v: one read-add-write of four floats for a row with a single writer, else fp32 atomics
-__device__ __forceinline__ void add4(float* dst, const float (&v)[4], bool single) {
-  if (single) {
+// the c row of an attention node: (m, s) in columns 0 and 1, zeros after
+__device__ __forceinline__ void put_ms(float* co, int ld, int lane, float m, float s) {
+  for (int j = 4 * lane; j < ld; j += 4 * kWave) {
+    const float v[4] = {j == 0 ? m : 0.f, j == 0 ? s : 0.f, 0.f, 0.f};
+    st4(co + j, v);
+  }
+}
+
+// A child's gradient row gets v at columns j .. j + 3: stored when the child has one parent edge and its row
+// starts undefined (fresh), read-add-written when it has one parent edge, fp32 atomics on a zeroed row otherwise.
+__device__ __forceinline__ void add4(float* dst, const float (&v)[4], bool single, bool fresh) {
+  if (single && fresh) {
+    st4(dst, v);
+  } else if (single) {
     float o[4];
     ld4(dst, o);
 #pragma unroll
@@ -82,21 +93,15 @@ __device__ __forceinline__ void add4(float* dst, const float (&v)[4], bool singl
     for (int e = 0; e < 4; ++e) unsafeAtomicAdd(dst + e, v[e]);
   }
 }
-// dst += v (dst's old value read first) when it has a single writer, else a hardware fp32 atomic add
-__device__ __forceinline__ void add_to(float* dst, float v, bool single) {
-  if (single)
-    *dst += v;
-  else
-    unsafeAtomicAdd(dst, v);
-}
-// the c row of an attention node: (m, s) in columns 0 and 1, zeros after
-__device__ __forceinline__ void put_ms(float* co, int ld, int lane, float m, float s) {
-  for (int j = 4 * lane; j < ld; j += 4 * kWave) {
-    const float v[4] = {j == 0 ? m : 0.f, j == 0 ? s : 0.f, 0.f, 0.f};
-    st4(co + j, v);
+// A child's dc row, whose only nonzero entry is column 1 (ds): a child with one parent edge gets the whole row
+// stored (its row is never initialised), a shared child an atomic add of ds into its zeroed row.
+__device__ __forceinline__ void ds_to(float* row, int ld, int lane, float ds, bool single) {
+  if (single) {
+    put_ms(row, ld, lane, 0.f, ds);
+  } else if (lane == 0 && ds != 0.f) {
+    unsafeAtomicAdd(row + 1, ds);
   }
 }
-
 // Lanes own four consecutive columns each, 256 columns a wave step.
 template <typename T, int KIND>
 __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_fwd(AttnArgs a) {
@@ -174,15 +179,17 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_bwd(AttnArgs a) {
     }
     const float de = (float)(wave_total(part) + a.dc[p * a.ld + 1]);
     if (lane == 0 && a.gates) a.gates[p * a.gstride] = de;
-    if (c0 >= 0)
+    if (c0 >= 0) {
       for (int j = 4 * lane; j < a.ld; j += 4 * kWave) {
         float g[4], wv[4];
         ld4(dh + j, g);
         ld4(w + j, wv);
 #pragma unroll
         for (int e = 0; e < 4; ++e) g[e] = j + e < a.H ? g[e] + de * wv[e] : 0.f;
-        add4(&a.dh[(size_t)c0 * a.ld + j], g, one);
+        add4(&a.dh[(size_t)c0 * a.ld + j], g, one, a.dh_fresh);
       }
+      ds_to(a.dc + (size_t)c0 * a.ld, a.ld, lane, 0.f, one);  // an item passes no cell-state gradient down
+    }
   } else if constexpr (KIND == FOLD_ATTN_SUM) {
     // with m fixed, acc and s are linear in the children's: dh_k += x_k dh, ds_k += x_k ds
     const float m = a.c_pool[p * a.ld];
@@ -203,23 +210,23 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_bwd(AttnArgs a) {
       ld4(dh + j, g);
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
-        if (xk[k] == 0.f) continue;
+        // an empty set's gradient is zero: stored into a child's row that starts undefined, skipped otherwise
+        if (ck[k] < 0 || (xk[k] == 0.f && !(one[k] && a.dh_fresh))) continue;
         float v[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = j + e < a.H ? xk[k] * g[e] : 0.f;
-        add4(&a.dh[(size_t)ck[k] * a.ld + j], v, one[k]);
+        add4(&a.dh[(size_t)ck[k] * a.ld + j], v, one[k], a.dh_fresh);
       }
     }
-    if (lane == 0)
 #pragma unroll
-      for (int k = 0; k < 2; ++k)
-        if (xk[k] != 0.f) add_to(&a.dc[(size_t)ck[k] * a.ld + 1], xk[k] * ds, one[k]);
+    for (int k = 0; k < 2; ++k)
+      if (ck[k] >= 0) ds_to(a.dc + (size_t)ck[k] * a.ld, a.ld, lane, xk[k] * ds, one[k]);
   } else {  // FOLD_ATTN_OUT: h = acc / s -> dacc = dh / s, ds = -(dh . acc) / s^2
     const int c0 = a.child_pos[a.idx_off + row];
     if (c0 < 0) return;
     const float s = a.c_pool[(size_t)c0 * a.ld + 1];
-    if (s == 0.f) return;
     const bool one = a.child_one[a.idx_off + row] != 0;
+    if (s == 0.f && !(one && a.dh_fresh)) return;  // attention over the empty set: a zero gradient
     double part = 0.0;
     for (int j = 4 * lane; j < a.ld; j += 4 * kWave) {
       float g[4], v[4];
@@ -228,12 +235,12 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_bwd(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         part += (double)g[e] * v[e];
-        g[e] = j + e < a.H ? g[e] / s : 0.f;
+        g[e] = j + e < a.H && s != 0.f ? g[e] / s : 0.f;
       }
-      add4(&a.dh[(size_t)c0 * a.ld + j], g, one);
+      add4(&a.dh[(size_t)c0 * a.ld + j], g, one, a.dh_fresh);
     }
     const double tot = wave_total(part);
-    if (lane == 0) add_to(&a.dc[(size_t)c0 * a.ld + 1], (float)(-tot / ((double)s * s)), one);
+    ds_to(a.dc + (size_t)c0 * a.ld, a.ld, lane, s != 0.f ? (float)(-tot / ((double)s * s)) : 0.f, one);
   }
 }
 

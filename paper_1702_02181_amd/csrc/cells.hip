@@ -36,17 +36,9 @@ constexpr int kThreads = 256;
 
 inline unsigned cdiv(long long a, long long b) { return (unsigned)((a + b - 1) / b); }
 
-// dst += v given dst's old value (read ahead) when it has a single writer, else a hardware fp32 atomic add
-__device__ __forceinline__ void add_into(float* dst, float old, float v, bool single) {
-  if (single)
-    *dst = old + v;
-  else
-    unsafeAtomicAdd(dst, v);
-}
-
 // Old values of the read-add-write targets among the 16 rows of one 32 x 32 result block that a lane holds
-// (column jin of pool rows t[r] where one[r]).  Such targets have a single parent edge, so they are
-// distinct rows: all 16 loads are issued before any store, instead of each waiting behind the previous
+// (column jin of pool rows t[r] where one[r]; 0 elsewhere).  Such targets have a single parent edge, so they
+// are distinct rows: all 16 loads are issued before any store, instead of each waiting behind the previous
 // row's store.
 __device__ __forceinline__ void read_targets16(const float* dh, int ld, int jin, const int (&t)[16],
                                                const bool (&one)[16], float (&old)[16]) {
@@ -536,12 +528,18 @@ __global__ void k_roots(int ld, const int* root_pos, const T* h_pool, T* out) {
 
 // ---------------------------------------------------------------- backward, elementwise
 
-__global__ void k_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* dh_roots,
-                           const int* root_pos, float* dh, float* dc) {
-  const size_t total = (size_t)N * ld;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
-    dh[i] = dh_nodes ? dh_nodes[i] : 0.f;
-    dc[i] = 0.f;
+// Rows of nodes with exactly one parent edge are left alone unless per-node upstream gradients are given: the
+// parent's backward stores them whole.  Every other row (roots, children of several parents) starts at zero.
+__global__ void k_bwd_init(int N, int ld, const float* dh_nodes, const int* npar, float* dh, float* dc) {
+  for (int p = blockIdx.x; p < N; p += gridDim.x) {
+    const bool init = npar[p] != 1;
+    if (!init && !dh_nodes) continue;
+    const size_t o = (size_t)p * ld;
+    for (int j = 4 * threadIdx.x; j < ld; j += 4 * blockDim.x) {
+      const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+      *reinterpret_cast<float4*>(dh + o + j) = dh_nodes ? *reinterpret_cast<const float4*>(dh_nodes + o + j) : z;
+      if (init) *reinterpret_cast<float4*>(dc + o + j) = z;
+    }
   }
 }
 
@@ -584,7 +582,23 @@ __device__ __forceinline__ void cell_bwd_body(const BwdCellArgs a, int row) {
     else
       gb[g * a.HP + j] = v;
   };
+  // a child's gradient of c: stored whole by its only parent, added atomically into a zeroed row otherwise
+  auto dc_to = [&](int c, bool single, int j, float v) {
+    float* dst = &a.dc[(size_t)c * a.ld + j];
+    if (single)
+      *dst = v;
+    else
+      unsafeAtomicAdd(dst, v);
+  };
   for (int j = threadIdx.x; j < a.HP; j += blockDim.x) {
+    if (a.zero_child_dh) {  // this group's dz . W^T adds K slices atomically into its children's dh
+      if (c0 >= 0 && s0) a.dh[(size_t)c0 * a.ld + j] = 0.f;
+      if (c1 >= 0 && s1) a.dh[(size_t)c1 * a.ld + j] = 0.f;
+    }
+    if (j >= a.H || KIND == FOLD_TREERNN) {  // pad columns; a TreeRNN passes no cell state to its children
+      if (c0 >= 0 && s0) a.dc[(size_t)c0 * a.ld + j] = 0.f;
+      if (c1 >= 0 && s1) a.dc[(size_t)c1 * a.ld + j] = 0.f;
+    }
     if (j >= a.H) {
       if constexpr (KIND != FOLD_EMBED) {
 #pragma unroll
@@ -602,17 +616,14 @@ __device__ __forceinline__ void cell_bwd_body(const BwdCellArgs a, int row) {
       const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cl = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
       const float cr = c1 >= 0 ? a.c_pool[(size_t)c1 * a.ld + j] : 0.f;
-      // the children's dc read with the other loads, ahead of this row's stores
-      const float dc0 = c0 >= 0 && s0 ? a.dc[(size_t)c0 * a.ld + j] : 0.f;
-      const float dc1 = c1 >= 0 && s1 ? a.dc[(size_t)c1 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
       put(0, j, dct * (m * u) * i_ * (1.f - i_));
       put(1, j, dct * cl * fl * (1.f - fl));
       put(2, j, dct * cr * fr * (1.f - fr));
       put(3, j, dh * tc * o * (1.f - o));
       put(4, j, dct * i_ * m * (1.f - u * u));
-      if (c0 >= 0) add_into(&a.dc[(size_t)c0 * a.ld + j], dc0, dct * fl, s0);
-      if (c1 >= 0) add_into(&a.dc[(size_t)c1 * a.ld + j], dc1, dct * fr, s1);
+      if (c0 >= 0) dc_to(c0, s0, j, dct * fl);
+      if (c1 >= 0) dc_to(c1, s1, j, dct * fr);
     } else if constexpr (KIND == kTreeLstmLeaf) {
       const float dc = a.dc[p * a.ld + j];
       const float i_ = gate(0, j), o = gate(1, j), u = gate(2, j);
@@ -628,25 +639,18 @@ __device__ __forceinline__ void cell_bwd_body(const BwdCellArgs a, int row) {
       const float m = a.u_mask ? a.u_mask[p * a.ld + j] : 1.f;
       const float tc = tanhf_(a.c_pool[p * a.ld + j]);
       const float cp = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
-      const float dc0 = c0 >= 0 && s0 ? a.dc[(size_t)c0 * a.ld + j] : 0.f;
       const float dct = dc + dh * o * (1.f - tc * tc);
       put(0, j, dct * (m * u) * i_ * (1.f - i_));
       put(1, j, dct * cp * f * (1.f - f));
       put(2, j, dh * tc * o * (1.f - o));
       put(3, j, dct * i_ * m * (1.f - u * u));
-      if (c0 >= 0) add_into(&a.dc[(size_t)c0 * a.ld + j], dc0, dct * f, s0);
+      if (c0 >= 0) dc_to(c0, s0, j, dct * f);
     } else {
       const float h = gate(0, j);
-      float dc = 0.f, dc0 = 0.f;
-      if constexpr (KIND == FOLD_PROJ) {
-        dc = a.dc[p * a.ld + j];
-        dc0 = c0 >= 0 && s0 ? a.dc[(size_t)c0 * a.ld + j] : 0.f;
-      }
       put(0, j, dh * (1.f - h * h));
-      if constexpr (KIND == FOLD_PROJ) {
-        if (c0 >= 0) add_into(&a.dc[(size_t)c0 * a.ld + j], dc0, dc, s0);
+      if constexpr (KIND == FOLD_PROJ) {  // c = c_child: the child's dc is this row's
+        if (c0 >= 0) dc_to(c0, s0, j, a.dc[p * a.ld + j]);
       }
-      (void)dc0;
     }
   }
 }
@@ -664,7 +668,7 @@ __global__ void k_cell_bwd(BwdCellArgs a) {
 // loaded straight into LDS.
 // The body of the narrow dz . W^T for workgroup L of its grid; LDS as separate arrays (see cell_fwd_body):
 // tgt = per tile row child k's pool row (mode 0) or the leaf-table row (mode 1), sgl = the child has one parent
-// edge (plain read-add-write)
+// edge (its row stored whole when it starts undefined, else read-add-written; not atomic)
 template <typename T, int MT, bool SPLIT>
 __device__ __forceinline__ void bwd_dx2_body(const DxArgs a, unsigned L, char* A0, char* A1, char* B0, char* B1,
                                              int (*tgt)[4 * 32 * MT], char (*sgl)[4 * 32 * MT]) {
@@ -741,25 +745,28 @@ __device__ __forceinline__ void bwd_dx2_body(const DxArgs a, unsigned L, char* A
       const int n = n0 + tn * 32 + (lane & 31);
       if (n >= a.Nb) continue;
       const int k = a.mode == 0 ? n / a.HP : 0, jin = a.mode == 0 ? n - k * a.HP : n;
-      if (jin >= (a.mode == 0 ? a.H : a.in_dim)) continue;
+      // pad columns (their products are 0) are stored only into rows that start undefined
+      const bool pad = jin >= (a.mode == 0 ? a.H : a.in_dim);
+      if (pad && !(a.mode == 0 && a.dh_fresh && !SPLIT)) continue;
       // K slices of one element add into it concurrently: atomics whenever K is split
       int tr[16];
-      bool one[16];
+      bool one[16], rd[16];
       float old[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int rl = wave * 32 * MT + tm * 32 + acc_row(r, lane), row = m0 + rl;
         tr[r] = row < a.rows ? tgt[k][rl] : -1;
         one[r] = !SPLIT && a.mode == 0 && tr[r] >= 0 && sgl[k][rl];
+        rd[r] = one[r] && !a.dh_fresh;
       }
-      read_targets16(a.dh, a.ld, jin, tr, one, old);
+      read_targets16(a.dh, a.ld, jin, tr, rd, old);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int t = tr[r];
-        if (t < 0) continue;
+        if (t < 0 || (pad && !one[r])) continue;
         if (a.mode == 0) {
           float* dst = &a.dh[(size_t)t * a.ld + jin];
-          if (one[r]) *dst = old[r] + acc[tm][tn][r];
+          if (one[r]) *dst = old[r] + acc[tm][tn][r];  // old = 0 for a row that starts undefined
           else unsafeAtomicAdd(dst, acc[tm][tn][r]);
         } else {
           unsafeAtomicAdd(&a.d_table[(size_t)t * a.tld + jin], acc[tm][tn][r]);
@@ -788,7 +795,7 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
   constexpr int BOFF = BM * 64, SLOT = (BM + BN) * 64;
   __shared__ __attribute__((aligned(16))) char ring[wide::kSlots * SLOT];
   __shared__ int tgt[2][BM];   // per tile row: child k's pool row (mode 0) or the leaf-table row (mode 1)
-  __shared__ char sgl[2][BM];  // the child has one parent edge: plain read-add-write
+  __shared__ char sgl[2][BM];  // the child has one parent edge: stored (or read-add-written), not atomic
   const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
   const int wr = wave & 3, wc = wave >> 2;
   const int R = (a.rows + BM - 1) / BM, NT = (a.Nb + BN - 1) / BN;
@@ -855,24 +862,27 @@ __global__ __launch_bounds__(wide::kThreads) void k_bwd_dx_w(DxArgs a) {
       const int n = n0 + wc * 128 + tn * 32 + (lane & 31);
       if (n >= a.Nb) continue;
       const int k = a.mode == 0 ? n / a.HP : 0, jin = a.mode == 0 ? n - k * a.HP : n;
-      if (jin >= (a.mode == 0 ? a.H : a.in_dim)) continue;
+      // pad columns (their products are 0) are stored only into rows that start undefined
+      const bool pad = jin >= (a.mode == 0 ? a.H : a.in_dim);
+      if (pad && !(a.mode == 0 && a.dh_fresh && !split)) continue;
       int tr[16];
-      bool one[16];
+      bool one[16], rd[16];
       float old[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int rl = wr * 64 + tm * 32 + acc_row(r, lane), row = m0 + rl;
         tr[r] = row < a.rows ? tgt[k][rl] : -1;
         one[r] = !split && a.mode == 0 && tr[r] >= 0 && sgl[k][rl];
+        rd[r] = one[r] && !a.dh_fresh;
       }
-      read_targets16(a.dh, a.ld, jin, tr, one, old);
+      read_targets16(a.dh, a.ld, jin, tr, rd, old);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int t = tr[r];
-        if (t < 0) continue;
+        if (t < 0 || (pad && !one[r])) continue;
         if (a.mode == 0) {
           float* dst = &a.dh[(size_t)t * a.ld + jin];
-          if (one[r]) *dst = old[r] + acc[tm][tn][r];
+          if (one[r]) *dst = old[r] + acc[tm][tn][r];  // old = 0 for a row that starts undefined
           else unsafeAtomicAdd(dst, acc[tm][tn][r]);
         } else {
           unsafeAtomicAdd(&a.d_table[(size_t)t * a.tld + jin], acc[tm][tn][r]);
@@ -1087,12 +1097,11 @@ void launch_roots(int dtype, int R, int ld, const int* root_pos, const void* h_p
 }
 
 void launch_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* dh_roots, const int* root_pos,
-                     float* dh, float* dc, hipStream_t st) {
+                     const int* pos_npar, float* dh, float* dc, hipStream_t st) {
   if (N <= 0) return;
   ProfScope prof("bwd_init", st);
-  const size_t total = (size_t)N * ld;
-  const unsigned blocks = (unsigned)std::min<size_t>((total + 255) / 256, 65536);
-  hipLaunchKernelGGL(k_bwd_init, dim3(blocks), dim3(256), 0, st, N, R, ld, dh_nodes, dh_roots, root_pos, dh, dc);
+  hipLaunchKernelGGL(k_bwd_init, dim3((unsigned)std::min(N, 65536)), dim3(256), 0, st, N, ld, dh_nodes, pos_npar, dh,
+                     dc);
   if (dh_roots && R > 0) hipLaunchKernelGGL(k_bwd_roots, dim3(R), dim3(256), 0, st, ld, dh_roots, root_pos, dh);
 }
 

@@ -168,20 +168,28 @@ struct BwdCellArgs {
   int H, HP, ld, gstride;
   const float* c_pool;
   float* gates;  // saved activations in, dz out
-  const float* dh;
+  float* dh;
   float* dc;
   const int* child_pos;
   const int* input_idx;
-  const int* child_one;  // beside child_pos: the child has one parent edge -> plain read-add-write
+  // beside child_pos: the child has one parent edge.  Such a child's gradient rows start undefined (the
+  // initialisation skips them) and this row's backward stores its dc row whole (pad columns and kinds without a
+  // cell state included: zeros); a child with several parents gets fp32 atomic adds on zeroed rows.
+  const int* child_one;
   float* d_table;
   int tld;
   int dz_bf16;  // write dz as bf16 (the operand type of bf16 parameters)
   const float* u_mask = nullptr;  // the forward's recurrent-dropout mask, or NULL
+  // this group's dz . W^T adds K slices into its children's dh atomically: zero the dh rows of the children
+  // with one parent edge first (their rows are not initialised)
+  int zero_child_dh = 0;
 };
 void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st);
 void launch_level_cbwd(const int* kinds, const BwdCellArgs* args, int n, hipStream_t st);
+// dh = dh_nodes on every row (if given); otherwise dh and dc rows are zeroed only where a node does not have
+// exactly one parent edge (roots, shared children): every other row is stored whole by its parent's backward
 void launch_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* dh_roots, const int* root_pos,
-                     float* dh, float* dc, hipStream_t st);
+                     const int* pos_npar, float* dh, float* dc, hipStream_t st);
 
 struct DxArgs {
   int rows, row_begin, idx_off, arity;
@@ -196,6 +204,7 @@ struct DxArgs {
   const int* input_idx;
   int in_dim, tld;
   const int* child_one;  // beside child_pos: the child has one parent edge
+  int dh_fresh;     // such children's dh rows are not initialised: stored whole (pad columns too), not added to
   int can_split;    // K may be split across workgroups (slices add into the targets atomically)
   int ksplit;       // set by the launcher
   int map;          // set by the launcher: workgroup order over the XCDs (kMapRows, kMapCols, kMapOwnCols)
@@ -219,6 +228,7 @@ struct AttnArgs {
   float* dc;
   float* gates;         // backward: the scorer saves de at gates[p * gstride] (NULL: not saved)
   int gstride;
+  int dh_fresh;         // backward: the dh rows of children with one parent edge start undefined (stored whole)
 };
 // rows of the scorer's weight gradient reduced by one workgroup (chunk order is fixed)
 constexpr int kAttnWgradChunk = 128;
