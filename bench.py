@@ -803,6 +803,50 @@ def measure(w, steps: int, warmup: int, table_grad: bool, schedule_reps: int = 5
     return out
 
 
+# Plain library GEMMs (torch.matmul: hipBLASLt / rocBLAS) of the contraction shapes the workloads run, on random
+# operands: what a dense vendor GEMM of the same size sustains on this GPU, without the gathers, the fused cells
+# or the scatter-adds.  (M, N, K, dtype, label); K-major A for the weight-gradient shapes (X^T dz).
+GEMM_SHAPES = [
+    (32768, 1280, 512, "f32", "config 2 internal level (rows x 5H, K = 2H)", False),
+    (65536, 768, 256, "f32", "config 2 leaf level (rows x 3H, K = in)", False),
+    (32768, 512, 1280, "f32", "config 2 dz.W^T (rows x 2H, K = 5H)", False),
+    (512, 1280, 65280, "f32", "config 2 weight gradient (2H x 5H, K = rows)", True),
+    (131072, 5120, 2048, "bf16", "H = 1024 wide level (rows x 5H, K = 2H)", False),
+    (131072, 2048, 5120, "bf16", "H = 1024 wide dz.W^T (rows x 2H, K = 5H)", False),
+    (2048, 5120, 131072, "bf16", "H = 1024 weight gradient (2H x 5H, K = rows)", True),
+    (2048, 5120, 2048, "bf16", "H = 1024 mid-size level (2,048 rows)", False),
+    (8192, 8192, 8192, "bf16", "square 8192", False),
+]
+
+
+def gemm_ceiling(reps: int = 10) -> dict:
+    import torch
+    torch.cuda.set_device(0)
+    rows = []
+    for M, N, K, dt, label, kmajor in GEMM_SHAPES:
+        dtype = torch.bfloat16 if dt == "bf16" else torch.float32
+        g = torch.Generator(device="cuda").manual_seed(M + N + K)
+        a = torch.rand((K, M) if kmajor else (M, K), device="cuda", dtype=dtype, generator=g) * 2 - 1
+        b = torch.rand((K, N), device="cuda", dtype=dtype, generator=g) * 2 - 1
+        A = a.t() if kmajor else a
+        for _ in range(3):
+            torch.matmul(A, b)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            torch.matmul(A, b)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        tf = 2.0 * M * N * K / (ms * 1e-3) / 1e12
+        peak = PEAKS["bf16_mfma_tflops"] if dt == "bf16" else PEAKS["f32_mfma_tflops"]
+        rows.append({"shape": label, "M": M, "N": N, "K": K, "dtype": dt, "ms": round(ms, 4),
+                     "tflops": round(tf, 1), "frac_of_datasheet": round(tf / peak, 3)})
+        del a, b
+    return {"library_gemm": rows, "note": "torch.matmul on random operands in [-1, 1)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -825,11 +869,16 @@ def main():
                     help="time the feed-forward attention workload (1024 sequences of 50-100 items, H = 256, bf16)")
     ap.add_argument("--blocks", action="store_true",
                     help="compile sentiment-shaped trees with the combinator front end and time the compiled batch")
+    ap.add_argument("--gemm-ceiling", action="store_true",
+                    help="time plain library GEMMs (torch.matmul) of the workloads' contraction shapes instead")
     ap.add_argument("--counters-from", nargs=4, metavar=("MFMA_CSV", "FETCH_CSV", "WRITE_CSV", "TRACE_CSV"),
                     help="print the per-kernel MFMA utilisation / HBM bandwidth table of four rocprofv3 runs")
     args = ap.parse_args()
     if args.counters_from:
         print(counters_table(*args.counters_from))
+        return
+    if args.gemm_ceiling:
+        print(json.dumps(gemm_ceiling()), flush=True)
         return
     if args.traffic_from:
         from paper_1702_02181_amd import gen as _gen
@@ -894,6 +943,9 @@ def main():
         # the copy probe doubles as the calibration kernel of the HBM byte counters (PROBE_BYTES a dispatch)
         probes["mfma_f32_tflops"] = round(F.fold_probe_mfma(F.FOLD_F32), 1)
         probes["mfma_bf16_tflops"] = round(F.fold_probe_mfma(F.FOLD_BF16), 1)
+        # random operand bits: what the matrix cores sustain on the data the contractions multiply
+        probes["mfma_f32_random_tflops"] = round(F.fold_probe_mfma_random(F.FOLD_F32), 1)
+        probes["mfma_bf16_random_tflops"] = round(F.fold_probe_mfma_random(F.FOLD_BF16), 1)
         nbytes = PROBE_BYTES
         src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)

@@ -605,8 +605,15 @@ int32_t fold_profile_read_launches(fold_launch_time* out, int32_t capacity, int3
  * sustained dense TFLOP/s; fold_probe_copy copies `bytes` (a multiple of 16,
  * both buffers 16-byte aligned, caller-owned device memory) five times with
  * 16-byte loads and stores and returns read+write GB/s.  Both synchronise
- * `stream`; fold_probe_mfma allocates a small output buffer. */
+ * `stream`; fold_probe_mfma allocates a small output buffer.
+ * fold_probe_mfma_random is the same loop with random operand bits (four
+ * registers a side per lane, uniform in [-1, 1), cycled over the
+ * accumulators): the matrix cores' power draw, and so the clock the GPU
+ * holds, depends on the operand bits, and random data is what the
+ * contractions multiply.  FOLD_E_INVALID for a dtype other than FOLD_F32 /
+ * FOLD_BF16 or a NULL result pointer. */
 int32_t fold_probe_mfma(int32_t dtype, hipStream_t stream, double* tflops);
+int32_t fold_probe_mfma_random(int32_t dtype, hipStream_t stream, double* tflops);
 int32_t fold_probe_copy(void* dst, const void* src, size_t bytes, hipStream_t stream, double* gbs);
 
 /* Text of the last error on the calling thread ("" if none). */

@@ -826,7 +826,15 @@ int32_t fold_probe_mfma(int32_t dtype, hipStream_t st, double* tflops) {
   FOLD_GUARD_BEGIN
   clear_error();
   if (!tflops || (dtype != FOLD_F32 && dtype != FOLD_BF16)) return fail(FOLD_E_INVALID, "fold_probe_mfma: bad argument");
-  return probe_mfma(dtype, st, tflops);
+  return probe_mfma(dtype, false, st, tflops);
+  FOLD_GUARD_END
+}
+
+int32_t fold_probe_mfma_random(int32_t dtype, hipStream_t st, double* tflops) {
+  FOLD_GUARD_BEGIN
+  clear_error();
+  if (!tflops || (dtype != FOLD_F32 && dtype != FOLD_BF16)) return fail(FOLD_E_INVALID, "fold_probe_mfma_random: bad argument");
+  return probe_mfma(dtype, true, st, tflops);
   FOLD_GUARD_END
 }
 

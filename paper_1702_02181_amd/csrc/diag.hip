@@ -46,6 +46,50 @@ __global__ __launch_bounds__(256) void k_probe_mfma_bf16(float* out, int iters) 
   out[blockIdx.x * blockDim.x + threadIdx.x] = s;
 }
 
+// The same loops with operands of random bits: every lane holds four different operand registers per side
+// (uniform in [-1, 1)), cycled over the accumulators.  The matrix cores' power draw, and with it the clock the
+// GPU holds, depends on the operand bits; random data is what the contractions multiply.
+__device__ __forceinline__ float probe_rand(uint32_t& x) {
+  x ^= x >> 15;
+  x *= 2246822519u;
+  x ^= x >> 13;
+  x *= 3266489917u;
+  x ^= x >> 16;
+  return (float)(x & 0xffffu) * (1.f / 32768.f) - 1.f;
+}
+
+template <bool BF>
+__global__ __launch_bounds__(256) void k_probe_mfma_rand(float* out, int iters) {
+  f32x16 acc[kProbeAcc];
+  for (int t = 0; t < kProbeAcc; ++t)
+    for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
+  uint32_t x = (blockIdx.x * 256u + threadIdx.x) * 2654435761u + 12345u;
+  bf16x8 ab[4], bb[4];
+  float af[4], bfl[4];
+  for (int q = 0; q < 4; ++q) {
+    af[q] = probe_rand(x);
+    bfl[q] = probe_rand(x);
+    for (int e = 0; e < 8; ++e) {
+      ab[q][e] = (__bf16)probe_rand(x);
+      bb[q][e] = (__bf16)probe_rand(x);
+    }
+  }
+  for (int i = 0; i < iters; i += 4)
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int t = 0; t < kProbeAcc; ++t) {
+        if constexpr (BF)
+          acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ab[(t + u) & 3], bb[t & 3], acc[t], 0, 0, 0);
+        else
+          acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[(t + u) & 3], bfl[t & 3], acc[t], 0, 0, 0);
+      }
+  float s = 0.f;
+  for (int t = 0; t < kProbeAcc; ++t)
+    for (int r = 0; r < 16; ++r) s += acc[t][r];
+  out[blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
 __global__ void k_probe_copy(const uint4* __restrict__ src, uint4* __restrict__ dst, size_t n) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     dst[i] = src[i];
@@ -53,7 +97,7 @@ __global__ void k_probe_copy(const uint4* __restrict__ src, uint4* __restrict__ 
 
 }  // namespace
 
-int32_t probe_mfma(int dtype, hipStream_t st, double* tflops) {
+int32_t probe_mfma(int dtype, bool random_operands, hipStream_t st, double* tflops) {
   int dev = 0, cus = 0;
   FOLD_HIP_CHECK(hipGetDevice(&dev));
   FOLD_HIP_CHECK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
@@ -63,12 +107,18 @@ int32_t probe_mfma(int dtype, hipStream_t st, double* tflops) {
   hipEvent_t e0, e1;
   (void)hipEventCreate(&e0);
   (void)hipEventCreate(&e1);
-  const int iters = dtype == FOLD_BF16 ? 20000 : 4000;
+  const int iters = dtype == FOLD_BF16 ? 20000 : 4000;  // multiples of 4 (the random loops' unrolling)
   auto launch = [&]() {
-    if (dtype == FOLD_BF16)
+    if (random_operands) {
+      if (dtype == FOLD_BF16)
+        hipLaunchKernelGGL(k_probe_mfma_rand<true>, dim3(blocks), dim3(256), 0, st, out, iters);
+      else
+        hipLaunchKernelGGL(k_probe_mfma_rand<false>, dim3(blocks), dim3(256), 0, st, out, iters);
+    } else if (dtype == FOLD_BF16) {
       hipLaunchKernelGGL(k_probe_mfma_bf16, dim3(blocks), dim3(256), 0, st, out, iters);
-    else
+    } else {
       hipLaunchKernelGGL(k_probe_mfma_f32, dim3(blocks), dim3(256), 0, st, out, iters);
+    }
   };
   launch();  // warm-up
   (void)hipEventRecord(e0, st);

@@ -282,7 +282,7 @@ void launch_adam(size_t n, float* p, uint16_t* p_bf16, const float* g, float* m,
                  double lr_t, double eps, hipStream_t st);
 
 // ---- achievable-peak probes (diag.hip) ----
-int32_t probe_mfma(int dtype, hipStream_t st, double* tflops);
+int32_t probe_mfma(int dtype, bool random_operands, hipStream_t st, double* tflops);
 int32_t probe_copy(void* dst, const void* src, size_t bytes, hipStream_t st, double* gbs);
 
 // ---- packing (pack.hip) ----

@@ -135,7 +135,7 @@ EXPORTS = ["fold_schedule", "fold_sched_get_info", "fold_sched_free", "fold_pack
            "fold_packed_free", "fold_row_ld", "fold_workspace_size", "fold_forward",
            "fold_backward", "fold_last_error", "fold_profile_enable", "fold_profile_read",
            "fold_profile_read_launches",
-           "fold_probe_mfma", "fold_probe_copy", "fold_graph_create", "fold_graph_launch",
+           "fold_probe_mfma", "fold_probe_mfma_random", "fold_probe_copy", "fold_graph_create", "fold_graph_launch",
            "fold_graph_num_nodes", "fold_graph_free", "fold_pack_update", "fold_loss_softmax_ce",
            "fold_loss_workspace_size", "fold_adam_step", "fold_forward_dropout", "fold_backward_dropout",
            "fold_dropout_mask", "fold_forward_noalloc", "fold_schedule_typed", "fold_typed_sched_get_info",
@@ -214,6 +214,8 @@ def lib():
     L.fold_profile_read_launches.argtypes = [POINTER(fold_launch_time), c_int32, POINTER(c_int32)]
     L.fold_probe_mfma.restype = c_int32
     L.fold_probe_mfma.argtypes = [c_int32, c_void_p, POINTER(ctypes.c_double)]
+    L.fold_probe_mfma_random.restype = c_int32
+    L.fold_probe_mfma_random.argtypes = [c_int32, c_void_p, POINTER(ctypes.c_double)]
     L.fold_probe_copy.restype = c_int32
     L.fold_probe_copy.argtypes = [c_void_p, c_void_p, c_size_t, c_void_p, POINTER(ctypes.c_double)]
     L.fold_pack_update.restype = c_int32
@@ -268,6 +270,12 @@ def fold_profile_read_launches() -> list:
 def fold_probe_mfma(dtype: int, stream=None) -> float:
     t = ctypes.c_double()
     _check(lib().fold_probe_mfma(int(dtype), _stream(stream), byref(t)))
+    return float(t.value)
+
+
+def fold_probe_mfma_random(dtype: int, stream=None) -> float:
+    t = ctypes.c_double()
+    _check(lib().fold_probe_mfma_random(int(dtype), _stream(stream), byref(t)))
     return float(t.value)
 
 

@@ -44,13 +44,17 @@ def run_device(w, dh_nodes=None, table_grad=False, backward=None, u_mask=None):
     if backward:
         dev.alloc_grads(table_grad)
         dev.set_upstream(w.dh_roots, dh_nodes)
-        dh_out = torch.zeros((dev.N, dev.ld), dtype=torch.float32, device="cuda")
-        dc_out = torch.zeros_like(dh_out)
+        # NaN-filled: the backward writes every row of dh_out / dc_out whole (a row it skipped stays NaN)
+        dh_out = torch.full((dev.N, dev.ld), float("nan"), dtype=torch.float32, device="cuda")
+        dc_out = torch.full_like(dh_out, float("nan"))
         dev.backward(dh_out, dc_out, mask)
         torch.cuda.synchronize()
         node_pos = dev.sched_arrays()["node_pos"]
-        out["dh"] = dh_out.cpu().numpy()[:, :dev.H][node_pos].astype(np.float64)
-        out["dc"] = dc_out.cpu().numpy()[:, :dev.H][node_pos].astype(np.float64)
+        dhp, dcp = dh_out.cpu().numpy(), dc_out.cpu().numpy()
+        assert np.isfinite(dhp).all() and np.isfinite(dcp).all(), "gradient rows left unwritten"
+        assert not dhp[:, dev.H:].any() and not dcp[:, dev.H:].any(), "nonzero pad columns"
+        out["dh"] = dhp[:, :dev.H][node_pos].astype(np.float64)
+        out["dc"] = dcp[:, :dev.H][node_pos].astype(np.float64)
         out["grads"], out["d_table"] = dev.weight_grads()
     out["h"], out["c"] = dev.node_states()
     torch.cuda.synchronize()

@@ -135,3 +135,30 @@ def test_level_launches_match_one_launch_per_group(case):
         for k in ("dh", "dc"):
             assert compare.rel_err(merged[k], single[k]) <= tol, k
     C.compare_all(w, merged, C.run_oracle(w, table_grad=table_grad), table_grad=table_grad)
+
+
+def test_backward_rejects_misaligned_gradient_buffers():
+    """The backward's gradient rows are accessed 16 bytes at a time: dh_roots, dh_nodes, dh_out, dc_out and the
+    workspace must be 16-byte aligned, anything else is FOLD_E_INVALID before any work is queued."""
+    import torch
+    from paper_1702_02181_amd import fold as F
+    from paper_1702_02181_amd.runner import DeviceRun
+    w = gen.config2(num_graphs=2, leaves=8)
+    dev = DeviceRun(w, with_backward=True)
+    dev.forward()
+    dev.alloc_grads(False)
+    dev.set_upstream(w.dh_roots, None)
+    good = torch.zeros((dev.N + 1) * dev.ld, dtype=torch.float32, device="cuda")
+    bad = good[1:]  # 4 bytes past a 256-byte boundary
+    roots_bad = torch.zeros(dev.R * dev.ld + 1, dtype=torch.float32, device="cuda")[1:]
+    ws_bad = torch.empty(dev.ws_bytes + 16, dtype=torch.uint8, device="cuda")[8:]
+    cases = [dict(dh_out=bad), dict(dc_out=bad), dict(dh_nodes=bad), dict(dh_roots=roots_bad), dict(ws=ws_bad)]
+    for case in cases:
+        args = dict(dh_roots=dev.dh_roots, dh_nodes=None, dh_out=None, dc_out=None, ws=dev.ws)
+        args.update(case)
+        with pytest.raises(F.FoldError) as e:
+            F.fold_backward(dev.sched.handle, dev.packed.handle, dev.table, dev.leaf_rows, dev.h_pool, dev.c_pool,
+                            args["dh_roots"], args["dh_nodes"], dev.grads, args["dh_out"], args["dc_out"], args["ws"],
+                            dev.ws_bytes, dev.stream)
+        assert e.value.code == F.FOLD_E_INVALID and "aligned" in str(e.value), list(case)
+    torch.cuda.synchronize()
