@@ -226,7 +226,15 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_bwd(AttnArgs a) {
     if (c0 < 0) return;
     const float s = a.c_pool[(size_t)c0 * a.ld + 1];
     const bool one = a.child_one[a.idx_off + row] != 0;
-    if (s == 0.f && !(one && a.dh_fresh)) return;  // attention over the empty set: a zero gradient
+    if (s == 0.f) {  // attention over the empty set: a zero gradient, stored into rows nobody else writes
+      if (one) {
+        const float z[4] = {0.f, 0.f, 0.f, 0.f};
+        if (a.dh_fresh)
+          for (int j = 4 * lane; j < a.ld; j += 4 * kWave) st4(&a.dh[(size_t)c0 * a.ld + j], z);
+        put_ms(a.dc + (size_t)c0 * a.ld, a.ld, lane, 0.f, 0.f);
+      }
+      return;
+    }
     double part = 0.0;
     for (int j = 4 * lane; j < a.ld; j += 4 * kWave) {
       float g[4], v[4];
@@ -235,12 +243,12 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_bwd(AttnArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         part += (double)g[e] * v[e];
-        g[e] = j + e < a.H && s != 0.f ? g[e] / s : 0.f;
+        g[e] = j + e < a.H ? g[e] / s : 0.f;
       }
       add4(&a.dh[(size_t)c0 * a.ld + j], g, one, a.dh_fresh);
     }
     const double tot = wave_total(part);
-    ds_to(a.dc + (size_t)c0 * a.ld, a.ld, lane, s != 0.f ? (float)(-tot / ((double)s * s)) : 0.f, one);
+    ds_to(a.dc + (size_t)c0 * a.ld, a.ld, lane, (float)(-tot / ((double)s * s)), one);
   }
 }
 

@@ -97,7 +97,8 @@ void launch_level_fwd(int dtype, const int* kinds, const FwdArgs* args, int n, h
 // Tiling of one forward group.  Wide groups (at least one workgroup per compute unit) use the wide
 // kernel: 256 rows x 2 unit blocks per workgroup of 8 waves.  Narrower groups use 128-row tiles of one
 // unit block and, if still short of workgroups, split K (partial sums in the workspace, then an
-// epilogue kernel).
+// epilogue kernel).  (256-row narrow tiles, one workgroup per compute unit, measured slower on the
+// 1,838-row levels of H = 1,024: 58 -> 68 us a level.)
 struct FwdPlan {
   int ksplit = 1;
   bool wide = false;  // 256 rows x 2 unit blocks per workgroup of 8 waves
@@ -148,8 +149,12 @@ inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
     p.ksplit = 2;
     return p;
   }
-  // fp32: 128-row tiles, two workgroups per compute unit; bf16: 256-row tiles on wide levels
-  p.mt = esize == 4 ? 1 : (((long long)(rows + 255) / 256) * nb >= 256 ? 2 : 1);
+  // fp32: 128-row tiles, two workgroups per compute unit.  bf16: 256-row tiles on wide levels, and on levels
+  // with a long K (at least 64 stages of 64 bytes) whose 256-row tiles give half the compute units a tile
+  // (measured on the 1,024-4,095-row levels at H = 1,024: 78 -> 69 us a level; with the K of H = 300 the
+  // 128-row tiles were faster)
+  const long long t256 = ((long long)(rows + 255) / 256) * nb;
+  p.mt = esize == 4 ? 1 : (t256 >= 256 || (t256 >= 128 && Kb * esize / 64 >= 64) ? 2 : 1);
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * nb;
   if (can_split && base < kDxSplitBelow && nst >= 4) {
     const long long want = (256 + base - 1) / base;

@@ -104,6 +104,22 @@ def test_wide_dx_two_k_slices_bf16():
     _sampled_parity(w, [0, 1 + 2 * int(np.argmax(sizes[1::2]))], table_grad=True)
 
 
+def test_dx_256_row_tiles_two_k_slices_bf16():
+    """bf16 dz . W^T levels with a long K (at least 64 stages of 64 bytes) whose 256-row tiles give between
+    half and all of the compute units a tile run as 256 x 128 tiles with K in two slices, added atomically
+    into the children's dh.  H = 512 (K = 2,560): levels of 3,841-8,191 rows; config 5's shape at 128 graphs
+    has one in its balanced trees' third level (64 x 64 = 4,096 rows).  Sampled parity as above."""
+    from paper_1702_02181_amd.runner import DeviceRun
+    w = gen.config5(num_graphs=128, hidden=512, vocab=2000, spine_range=(200, 511))
+    dev = DeviceRun(w)
+    host = dev.sched.host_groups()
+    del dev
+    rows = [int(r) for r, op in zip(host["group_rows"], host["group_op"]) if w.ops[int(op)].arity == 2]
+    nb = 2 * w.hidden // 128
+    assert any(128 <= (r + 255) // 256 * nb < 256 and (r + 255) // 256 * 4 * 2 < 256 for r in rows), rows
+    _sampled_parity(w, [0, 1, 64], table_grad=True)
+
+
 def test_wide_weight_gradients_f32_ragged_tiles():
     """fp32 ops of at least 32 k rows whose 256 x 256 weight-gradient tiles fill the compute units take
     them.  H = 300 (padded to 320) leaves ragged tiles on every side: the leaves' 300-wide inputs (two
