@@ -528,17 +528,34 @@ __global__ void k_roots(int ld, const int* root_pos, const T* h_pool, T* out) {
 
 // ---------------------------------------------------------------- backward, elementwise
 
-// Rows of nodes with exactly one parent edge are left alone unless per-node upstream gradients are given: the
-// parent's backward stores them whole.  Every other row (roots, children of several parents) starts at zero.
-__global__ void k_bwd_init(int N, int ld, const float* dh_nodes, const int* npar, float* dh, float* dc) {
+// Rows of nodes with exactly one parent edge are stored whole by that parent's backward; every other row (roots,
+// children of several parents) starts at zero.  A wave reads the parent counts of 64 consecutive rows at once and
+// zeroes, all lanes together, only the rows that need it (a tree batch: its roots alone).
+__global__ __launch_bounds__(256) void k_bwd_init(int N, int ld, const int* npar, float* dh, float* dc) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int p0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kWave;
+  if (p0 >= N) return;
+  unsigned long long m = __ballot(p0 + lane < N && npar[p0 + lane] != 1);  // the same in every lane
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+  while (m) {
+    const int l = __ffsll((unsigned long long)m) - 1;
+    m &= m - 1;
+    const size_t o = (size_t)(p0 + l) * ld;
+    for (int j = 4 * lane; j < ld; j += 4 * kWave) {
+      *reinterpret_cast<float4*>(dh + o + j) = z;
+      *reinterpret_cast<float4*>(dc + o + j) = z;
+    }
+  }
+}
+
+// With per-node upstream gradients every dh row starts as that gradient; dc rows as above.
+__global__ void k_bwd_init_nodes(int N, int ld, const float* dh_nodes, const int* npar, float* dh, float* dc) {
   for (int p = blockIdx.x; p < N; p += gridDim.x) {
     const bool init = npar[p] != 1;
-    if (!init && !dh_nodes) continue;
     const size_t o = (size_t)p * ld;
     for (int j = 4 * threadIdx.x; j < ld; j += 4 * blockDim.x) {
-      const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-      *reinterpret_cast<float4*>(dh + o + j) = dh_nodes ? *reinterpret_cast<const float4*>(dh_nodes + o + j) : z;
-      if (init) *reinterpret_cast<float4*>(dc + o + j) = z;
+      *reinterpret_cast<float4*>(dh + o + j) = *reinterpret_cast<const float4*>(dh_nodes + o + j);
+      if (init) *reinterpret_cast<float4*>(dc + o + j) = make_float4(0.f, 0.f, 0.f, 0.f);
     }
   }
 }
@@ -1100,8 +1117,11 @@ void launch_bwd_init(int N, int R, int ld, const float* dh_nodes, const float* d
                      const int* pos_npar, float* dh, float* dc, hipStream_t st) {
   if (N <= 0) return;
   ProfScope prof("bwd_init", st);
-  hipLaunchKernelGGL(k_bwd_init, dim3((unsigned)std::min(N, 65536)), dim3(256), 0, st, N, ld, dh_nodes, pos_npar, dh,
-                     dc);
+  if (dh_nodes)
+    hipLaunchKernelGGL(k_bwd_init_nodes, dim3((unsigned)std::min(N, 65536)), dim3(256), 0, st, N, ld, dh_nodes,
+                       pos_npar, dh, dc);
+  else
+    hipLaunchKernelGGL(k_bwd_init, dim3(cdiv(N, 256)), dim3(256), 0, st, N, ld, pos_npar, dh, dc);
   if (dh_roots && R > 0) hipLaunchKernelGGL(k_bwd_roots, dim3(R), dim3(256), 0, st, ld, dh_roots, root_pos, dh);
 }
 
