@@ -127,8 +127,11 @@ struct DxPlan {
   bool wide = false;  // 256 x 256 tiles per workgroup of 8 waves
 };
 // at most this many K slices: beyond it the atomic adds of the slices cost more than the shorter K loops
-// save (measured on levels of 30-400 rows, H = 512: 8 beats 2, 4 and 16-20)
+// save.  fp32: 8 (config 2's top levels of 256-4,096 rows at H = 256: 8 beats 4).  bf16: 4 (config 4's level
+// launches of two or three groups of 50-500 rows at H = 512, up to 5.5 M atomic adds a level with 8 slices:
+// 4 beats 2, 3, 6 and 8 -- 6.34 -> 5.97 ms a step; configs 3 and 5 unchanged)
 constexpr int kDxMaxSplit = 8;
+constexpr int kDxMaxSplitBf16 = 4;
 // levels with fewer narrow tiles than this split K (measured: 256 beats 192, the same as 384 or 512)
 constexpr int kDxSplitBelow = 256;
 inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
@@ -158,7 +161,7 @@ inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * nb;
   if (can_split && base < kDxSplitBelow && nst >= 4) {
     const long long want = (256 + base - 1) / base;
-    p.ksplit = (int)std::min<long long>(std::min<long long>(want, nst / 2), kDxMaxSplit);
+    p.ksplit = (int)std::min<long long>(std::min<long long>(want, nst / 2), esize == 2 ? kDxMaxSplitBf16 : kDxMaxSplit);
   }
   return p;
 }
