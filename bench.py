@@ -185,6 +185,16 @@ def counters_table(mfma_csv: str, fetch_csv: str, write_csv: str, trace_csv: str
     return "\n".join(out)
 
 
+def table_runs(w) -> dict:
+    """Distinct leaf-table rows each operation with an input reads: the rows of its leaf-table gradient
+    contraction (dz is summed over the op's nodes of one leaf-table row before it is contracted)."""
+    import numpy as np
+    node_op = np.asarray(w.node_op)
+    node_input = np.asarray(w.node_input)
+    return {o: int(np.unique(node_input[(node_op == o) & (node_input >= 0)]).size)
+            for o, op in enumerate(w.ops) if op.has_input}
+
+
 def flops_by_kernel(w, sched_host, table_grad: bool) -> dict:
     """Algorithmic FLOPs of one forward + backward, by kernel class (2 FLOPs per multiply-add)."""
     from paper_1702_02181_amd import gen
@@ -198,6 +208,7 @@ def flops_by_kernel(w, sched_host, table_grad: bool) -> dict:
     rows_of_op = {}
     for op_id, rows in zip(sched_host["group_op"], sched_host["group_rows"]):
         rows_of_op[int(op_id)] = rows_of_op.get(int(op_id), 0) + int(rows)
+    runs = table_runs(w) if (w.backward and table_grad) else {}
     for op_id, rows in rows_of_op.items():
         op = w.ops[op_id]
         if op.kind == gen.KIND_EMBED or op.kind in gen.ATTN_KINDS:
@@ -208,7 +219,10 @@ def flops_by_kernel(w, sched_host, table_grad: bool) -> dict:
         name = gen.KIND_NAMES[op.kind]
         add(f"cell_fwd.{name}.{dt}", 2.0 * rows * k_in * G * H)
         if w.backward:
-            add(f"bwd_dx.{dt}", 2.0 * rows * G * H * (op.arity * H + (ps.in_dim if (op.has_input and table_grad) else 0)))
+            if op.arity > 0:
+                add(f"bwd_dx.{dt}", 2.0 * rows * G * H * op.arity * H)
+            if op_id in runs:
+                add(f"tgrad.{dt}", 2.0 * runs[op_id] * G * H * ps.in_dim)
             add(f"wgrad.{dt}", 2.0 * rows * k_in * G * H)
     return out
 
@@ -260,7 +274,8 @@ def pass_work(w, host, table_grad: bool) -> dict:
     """Algorithmic FLOPs and HBM bytes of every level pass of one step (weights counted once per pass).
 
     Keys: ("fwd", group), ("bwd", group) -- the cell's backward and dz . W^T of one (depth, op) group --
-    and ("wgrad", op), the deferred weight-gradient contraction of one operation over all its rows.
+    ("wgrad", op), the deferred weight-gradient contraction of one operation over all its rows, and ("tgrad",
+    op), its leaf-table gradient (dz summed per leaf-table row, then one contraction row per distinct row).
     Per node, with S = state bytes (h, plus fp32 c for cells that carry one) and S_g = its fp32
     gradient: forward reads the input row and the children's states and writes S; backward reads S_g
     and the children's states and writes the children's S_g (plus the leaf-table gradient row).
@@ -293,10 +308,19 @@ def pass_work(w, host, table_grad: bool) -> dict:
         out[("fwd", g)] = (2.0 * rows * k_in * G * H,
                            float(rows * (din * bh + op.arity * s_node + s_node) + k_in * G * H * bh + G * H * 4))
         if w.backward:
-            k_dx = op.arity * H + (din if table_grad else 0)
+            k_dx = op.arity * H
             out[("bwd", g)] = (2.0 * rows * G * H * k_dx,
-                               float(rows * (sg_node + op.arity * (s_node + sg_node) + (din * 4 if table_grad else 0))
-                                     + k_dx * G * H * bh))
+                               float(rows * (sg_node + op.arity * (s_node + sg_node)) + k_dx * G * H * bh))
+    if w.backward and table_grad:
+        runs = table_runs(w)
+        for o, count in op_rows.items():
+            op = w.ops[o]
+            if o not in runs or op.kind == gen.KIND_EMBED:
+                continue
+            G, din = live_gates(op), w.params[op.param_set].in_dim
+            # read every row's dz once, read and write each distinct leaf-table row, the weights once
+            out[("tgrad", o)] = (2.0 * runs[o] * G * H * din,
+                                 float(count * G * H * bh + runs[o] * din * 4 * 2 + din * G * H * bh))
     if w.backward:
         for o, count in op_rows.items():
             op = w.ops[o]
@@ -323,6 +347,8 @@ def pass_of(name: str, group: int, op: int):
         return [("bwd", g) for g in groups]
     if group < 0 and op >= 0 and cls in ("wgrad", "wgrad_reduce", "bias_partial", "bias_reduce", "attn_wgrad"):
         return [("wgrad", op)]
+    if group < 0 and op >= 0 and cls in ("tgrad", "tgrad_sum"):
+        return [("tgrad", op)]
     return []
 
 
@@ -757,7 +783,7 @@ def measure(w, steps: int, warmup: int, table_grad: bool, schedule_reps: int = 5
                     "flops_per_launch": per_launch, "launches_per_step": launches,
                     "avg_launch_us": round(avg_s * 1e6, 2)}
         # algorithmic HBM bytes per launch of the class (the level passes it runs in, weights once per pass)
-        kind = {"cell_fwd": "fwd", "bwd_dx": "bwd", "wgrad": "wgrad"}[class_of(dom)]
+        kind = {"cell_fwd": "fwd", "bwd_dx": "bwd", "wgrad": "wgrad", "tgrad": "tgrad"}[class_of(dom)]
         alg = 0.0
         for (pk, key), (_fl, by) in pass_work(w, host, table_grad).items():
             if pk != kind:

@@ -355,8 +355,11 @@ typedef struct {
  * given, dh_nodes on every pool row; the roots' cell states get none.
  * For each group: dz from the saved gates, dz . W^T scatter-added into the
  * children's (h, c) gradients (every parent lies at a greater depth, so a
- * child's gradient is complete before its own level runs) and into the leaf
- * table rows; then the weight gradients dW += X^T dz, db += sum dz.
+ * child's gradient is complete before its own level runs); then, per
+ * operation, the weight gradients dW += X^T dz, db += sum dz, and the
+ * leaf-table gradient: dz summed over the operation's rows of each
+ * leaf-table row, times W_in^T, added into that row (the same sum as adding
+ * every row's dz . W_in^T, in another order).
  *   h_pool, c_pool, ws   exactly as left by fold_forward with this schedule
  *   dh_roots             device [num_roots, ld(H)] fp32 or NULL
  *   dh_nodes             device [N, ld(H)] fp32 (pool order) or NULL

@@ -257,6 +257,12 @@ WsLayout workspace_layout(const Sched& s, const Packed& p) {
       WgradSplit sp = wgrad_split(count, ps.INP, Nw, p.dtype);
       part = std::max(part, (size_t)sp.nchunk * ps.INP * Nw);
       nb = std::max(nb, (size_t)sp.bparts);
+      // the leaf-table gradient's dz sums (fp32, and their bf16 copy) use the same region before the op's
+      // weight gradients: at most one row per distinct leaf-table row of the op, over its dz columns
+      const bool leaf = is_tree_lstm_leaf(op);
+      const size_t U = (size_t)std::min(count, std::max(s.num_inputs, 0));
+      const size_t Kb = (size_t)(leaf ? gates_of(kTreeLstmLeaf) : ps.G) * p.HP;
+      part = std::max(part, p.dtype == FOLD_BF16 ? U * Kb + (U * Kb + 1) / 2 : U * Kb);
     }
     bpart = std::max(bpart, nb * Nw);
   }
@@ -633,13 +639,6 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
         dargs.push_back(d);
         dgroup.push_back(g);
       }
-      if (op.has_input && d_table && ps.INP > 0) {
-        d.mode = 1;
-        d.Nb = ps.INP;
-        d.Wb = leaf ? ps.Wb_in_leaf : ps.Wb_in;
-        dargs.push_back(d);
-        dgroup.push_back(g);
-      }
     }
     for (size_t k = 0; k < attn.size(); ++k) {
       prof_tag(attn_group[k], s.h_op[attn_group[k]]);
@@ -704,6 +703,34 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
       const int gcode = leaf ? kTreeLstmLeafGates : gate_code_identity(ps.G);
       const int Nw = Gz * p.HP;
       const int off = s.h_op_row_ptr[o];
+      if (op.has_input && d_table && ps.INP > 0) {
+        // leaf-table gradient: dz summed over the op's rows of each leaf-table row (in the weight-gradient
+        // region, before this op's weight gradients use it), then one dz . W_in^T row per distinct leaf-table row
+        const int u0 = s.h_tok_ptr[o], U = s.h_tok_ptr[o + 1] - u0;
+        const bool bf = p.dtype == FOLD_BF16;
+        float* zsum = part;
+        uint16_t* zbf = reinterpret_cast<uint16_t*>(part + (size_t)U * Nw);
+        launch_tok_sum(p.dtype, s.tok_rows, s.tok_seg, s.tok_start, off, count, u0, U, gates, L.gstride, Nw, zsum,
+                       zbf, st);
+        DxArgs d{};
+        d.rows = U;
+        d.H = p.H;
+        d.HP = p.HP;
+        d.ld = p.ld;
+        d.gstride = bf ? Nw / 2 : Nw;
+        d.Kb = Nw;
+        d.Nb = ps.INP;
+        d.dz = bf ? reinterpret_cast<const float*>(zbf) : zsum;
+        d.Wb = leaf ? ps.Wb_in_leaf : ps.Wb_in;
+        d.zero = p.zero;
+        d.mode = 1;
+        d.d_table = d_table;
+        d.input_idx = s.tok_row + u0;
+        d.in_dim = ps.in_dim;
+        d.tld = tld;
+        d.can_split = 1;
+        launch_bwd_dx(p.dtype, d, st, bf ? "tgrad.bf16" : "tgrad.f32");
+      }
       WgArgs w;
       w.op_rows = s.op_rows + off;
       w.op_cpos = s.op_cpos + 2 * (size_t)off;

@@ -9,8 +9,9 @@
 // Backward:
 //   k_cell_bwd  elementwise dz of every row from the saved activations; dc of the children
 //               scatter-added; EMBED rows scatter dh into the leaf-table gradient
-//   k_bwd_dx    dz . W^T on the matrix cores, scatter-added into the children's dh (or into the
-//               leaf-table gradient for the input segment)
+//   k_bwd_dx    dz . W^T on the matrix cores, scatter-added into the children's dh; for the leaf-table
+//               gradient, after k_tok_sum has summed dz over the rows of every (op, leaf-table row), once per
+//               distinct leaf-table row
 // Cells (gate blocks in column order):
 //   TREELSTM (i|f_l|f_r|o|u): c = i*u + f_l*c_l + f_r*c_r, h = o*tanh(c)   (Tai et al. N-ary, N = 2)
 //   LSTM     (i|f|o|u):       c = i*u + f*c_p,             h = o*tanh(c)
@@ -1022,7 +1023,8 @@ __global__ __launch_bounds__(kThreads) void k_level_dx(Merged<DxArgs> m) {
 
 template <typename T, int KIND>
 void cell_fwd_kind(const FwdArgs& a0, hipStream_t st) {
-  const FwdPlan pl = fwd_plan(a0.rows, a0.HP, a0.has_input ? a0.INP : 0, a0.arity, sizeof(T), a0.zpart != nullptr);
+  const FwdPlan pl = fwd_plan(a0.rows, a0.HP, a0.has_input ? a0.INP : 0, a0.arity, sizeof(T), a0.zpart != nullptr,
+                              true);
   FwdArgs a = a0;
   if (pl.wide) {
     const int R = (int)cdiv(a.rows, wide::kRows), NU = a.HP / 64;
@@ -1060,6 +1062,84 @@ void cell_fwd_t(int kind, const FwdArgs& a, hipStream_t st) {
     case FOLD_PROJ: cell_fwd_kind<T, FOLD_PROJ>(a, st); break;
     default: break;
   }
+}
+
+// ---------------------------------------------------------------- leaf-table gradient
+// The leaf-table gradient of an op is sum over its rows of dz . W_in^T, added into each row's leaf-table row.
+// It is linear in dz, so dz is first summed over the rows of every run of equal (op, leaf-table row), and the
+// contraction then runs once per distinct leaf-table row (no two of its rows share a target).
+
+constexpr int kTokRows = 256;  // at most this many entries of the (op, leaf-table row) list per workgroup
+
+// A workgroup per `per` (at most kTokRows) consecutive entries of the op's list, a thread per four consecutive dz
+// columns.  A run
+// that lies inside the workgroup's entries is stored; the first and the last run may cross its ends and are then
+// added atomically into the zeroed sums.  Eight rows' loads go out before they are added.
+template <bool BF>
+__global__ __launch_bounds__(256) void k_tok_sum(const int* tok_rows, const int* tok_seg, const int* tok_start, int i0,
+                                                 int count, int per, int u0, const float* dz, int gstride,
+                                                 int Kb, float* zsum) {
+  __shared__ int srow[kTokRows], sseg[kTokRows];
+  const int b0 = i0 + blockIdx.x * per, b1 = min(i0 + count, b0 + per), n = b1 - b0;
+  for (int t = threadIdx.x; t < n; t += blockDim.x) {
+    srow[t] = tok_rows[b0 + t];
+    sseg[t] = tok_seg[b0 + t];
+  }
+  __syncthreads();
+  const int ufirst = sseg[0], ulast = sseg[n - 1];
+  const bool first_out = tok_start[ufirst] < b0, last_out = tok_start[ulast + 1] > b1;
+  auto load = [&](int t, int j, float (&v)[4]) {
+    const float* row = dz + (size_t)srow[t] * gstride;
+    if constexpr (BF) {
+      const uint2 x = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(row) + j);
+      v[0] = bf2f(x.x & 0xffff), v[1] = bf2f(x.x >> 16), v[2] = bf2f(x.y & 0xffff), v[3] = bf2f(x.y >> 16);
+    } else {
+      const float4 x = *reinterpret_cast<const float4*>(row + j);
+      v[0] = x.x, v[1] = x.y, v[2] = x.z, v[3] = x.w;
+    }
+  };
+  auto flush = [&](int u, int j, const float (&acc)[4]) {
+    float* dst = zsum + (size_t)(u - u0) * Kb + j;
+    if ((u == ufirst && first_out) || (u == ulast && last_out)) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) atomicAdd(dst + e, acc[e]);
+    } else {
+      *reinterpret_cast<float4*>(dst) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    }
+  };
+  for (int j = 4 * threadIdx.x; j < Kb; j += 4 * blockDim.x) {
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    int u = ufirst;
+    auto add = [&](int t, const float (&v)[4]) {
+      if (sseg[t] != u) {
+        flush(u, j, acc);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] = 0.f;
+        u = sseg[t];
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[e] += v[e];
+    };
+    int t = 0;
+    for (; t + 8 <= n; t += 8) {
+      float v[8][4];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) load(t + e, j, v[e]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) add(t + e, v[e]);
+    }
+    for (; t < n; ++t) {
+      float v[4];
+      load(t, j, v);
+      add(t, v);
+    }
+    flush(u, j, acc);
+  }
+}
+
+__global__ void k_tok_cast(const float* in, size_t n, uint16_t* out) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    out[i] = f2bf(in[i]);
 }
 
 }  // namespace
@@ -1148,10 +1228,31 @@ void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
 #undef FOLD_CB
 }
 
-void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st) {
+void launch_tok_sum(int dtype, const int* tok_rows, const int* tok_seg, const int* tok_start, int i0, int count,
+                    int u0, int U, const float* dz, int gstride, int Kb, float* zsum, uint16_t* zbf, hipStream_t st) {
+  if (count <= 0 || U <= 0) return;
+  ProfScope prof("tgrad_sum", st);
+  const size_t n = (size_t)U * Kb;
+  hipLaunchKernelGGL(k_zero_f32, dim3((unsigned)std::min<size_t>((n + 255) / 256, 8192)), dim3(256), 0, st, zsum, n);
+  // entries per workgroup: enough workgroups to fill the GPU a few times over (short runs that cross a
+  // workgroup's ends cost atomic adds, so no fewer than 32 entries)
+  const int per = std::max(32, std::min(kTokRows, count / 1024 / 8 * 8));
+  const dim3 grid(cdiv(count, per));
+  if (dtype == FOLD_BF16) {
+    hipLaunchKernelGGL(k_tok_sum<true>, grid, dim3(256), 0, st, tok_rows, tok_seg, tok_start, i0, count, per, u0, dz,
+                       gstride, Kb, zsum);
+    hipLaunchKernelGGL(k_tok_cast, dim3((unsigned)std::min<size_t>((n + 255) / 256, 8192)), dim3(256), 0, st, zsum,
+                       n, zbf);
+  } else {
+    hipLaunchKernelGGL(k_tok_sum<false>, grid, dim3(256), 0, st, tok_rows, tok_seg, tok_start, i0, count, per, u0,
+                       dz, gstride, Kb, zsum);
+  }
+}
+
+void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st, const char* name) {
   if (a0.rows <= 0 || a0.Nb <= 0) return;
   DxArgs a = a0;
-  ProfScope prof(dtype == FOLD_BF16 ? "bwd_dx.bf16" : "bwd_dx.f32", st);
+  ProfScope prof(name ? name : dtype == FOLD_BF16 ? "bwd_dx.bf16" : "bwd_dx.f32", st);
   const DxPlan pl = dx_plan(a.rows, a.Nb, a.Kb, dtype == FOLD_BF16 ? 2 : 4, a.can_split != 0);
   if (pl.wide) {
     const int R = (int)cdiv(a.rows, wide::kRows), NT = (int)cdiv(a.Nb, 256);

@@ -107,11 +107,15 @@ struct Sched {
   int32_t *op_rows = nullptr;     // [N] pool rows sorted by (op, row)
   int32_t *op_cpos = nullptr;     // [2N] child pool rows of op_rows[q] at 2q + k (-1 past the arity)
   int32_t *op_inp = nullptr;      // [N] leaf-table row of op_rows[q], or -1
+  // pool rows sorted by (op, leaf-table row), and the runs of equal (op, leaf-table row) in that list: run u is
+  // tok_rows[tok_start[u] .. tok_start[u + 1]), of leaf-table row tok_row[u]; tok_seg[i] = the run of entry i
+  int32_t *tok_rows = nullptr, *tok_seg = nullptr, *tok_start = nullptr, *tok_row = nullptr;
   // [num_groups] per child slot k: first pool row of the slot's children when they are the consecutive
   // rows base .. base + rows - 1, each with one parent edge (a static-graph layout), else -1
   int32_t *g_cbase0 = nullptr, *g_cbase1 = nullptr;
   std::vector<int32_t> h_level_ptr, h_level, h_op, h_row_begin, h_rows, h_idx_off, h_cbase0, h_cbase1;
-  std::vector<int32_t> h_op_row_ptr;  // [num_ops + 1] ranges of op_rows
+  std::vector<int32_t> h_op_row_ptr;  // [num_ops + 1] ranges of op_rows (and of tok_rows)
+  std::vector<int32_t> h_tok_ptr;     // [num_ops + 1] ranges of the runs of each op
 };
 
 // The paper's own form of a schedule (typed per-depth states, pass-through operations), fold_schedule_typed.

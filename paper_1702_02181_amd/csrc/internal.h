@@ -103,7 +103,8 @@ struct FwdPlan {
   int ksplit = 1;
   bool wide = false;  // 256 rows x 2 unit blocks per workgroup of 8 waves
 };
-inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bool can_split) {
+// alone: the group launches by itself (not in a level launch, whose groups' splits are cut together)
+inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bool can_split, bool alone = false) {
   const int BK = esize == 4 ? 32 : 64;
   const int nst = inp_used / BK + arity * (HP / BK);
   const long long ub = HP / 32;
@@ -114,7 +115,11 @@ inline FwdPlan fwd_plan(int rows, int HP, int inp_used, int arity, int esize, bo
   if (p.wide) return p;
   const long long base = ((long long)(rows + 127) / 128) * ub;
   if (can_split && base < 192 && nst >= 4) {
-    const long long want = (256 + base - 1) / base;
+    // aim at a workgroup per compute unit; a bf16 group alone with a short K (under 16 stages of 128 bytes) at
+    // half of that: its slices are short, and the partial sums cost more than the extra workgroups gain
+    // (config 3, H = 300: the forward 0.444 -> 0.423 ms a step; config 5's long K: no gain)
+    const long long aim = alone && esize == 2 && nst < 16 ? 128 : 256;
+    const long long want = (aim + base - 1) / base;
     p.ksplit = (int)std::min<long long>(want, nst / 2);
   }
   return p;
@@ -160,7 +165,10 @@ inline DxPlan dx_plan(int rows, int Nb, int Kb, int esize, bool can_split) {
   p.mt = esize == 4 ? 1 : (t256 >= 256 || (t256 >= 128 && Kb * esize / 64 >= 64) ? 2 : 1);
   const long long base = ((long long)(rows + 128 * p.mt - 1) / (128 * p.mt)) * nb;
   if (can_split && base < kDxSplitBelow && nst >= 4) {
-    const long long want = (256 + base - 1) / base;
+    // aim at a workgroup per compute unit; bf16 levels with a short K at half of that (config 3, H = 300: the
+    // dz.W^T 0.509 -> 0.489 ms a step; with config 5's long K the halved grid was far slower)
+    const long long aim = esize == 2 && Kb * esize / 64 < 64 ? 128 : 256;
+    const long long want = (aim + base - 1) / base;
     p.ksplit = (int)std::min<long long>(std::min<long long>(want, nst / 2), esize == 2 ? kDxMaxSplitBf16 : kDxMaxSplit);
   }
   return p;
@@ -217,7 +225,12 @@ struct DxArgs {
   int ksplit;       // set by the launcher
   int map;          // set by the launcher: workgroup order over the XCDs (kMapRows, kMapCols, kMapOwnCols)
 };
-void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st);
+// name: the profiling record's kernel class (NULL: bwd_dx.bf16 / bwd_dx.f32)
+void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st, const char* name = nullptr);
+// dz summed over the rows of every run of equal (op, leaf-table row): entries i0 .. i0 + count - 1 of tok_rows
+// (one op's), runs u0 .. u0 + U - 1, into zsum [U][Kb] fp32 (zeroed here), and for bf16 its bf16 copy zbf [U][Kb]
+void launch_tok_sum(int dtype, const int* tok_rows, const int* tok_seg, const int* tok_start, int i0, int count,
+                    int u0, int U, const float* dz, int gstride, int Kb, float* zsum, uint16_t* zbf, hipStream_t st);
 // true if launch_bwd_dx would run this call on narrow tiles (the ones a level launch can merge)
 bool bwd_dx_is_narrow(int dtype, const DxArgs& a);
 void launch_level_dx(int dtype, const DxArgs* args, int n, hipStream_t st);

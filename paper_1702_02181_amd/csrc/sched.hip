@@ -503,6 +503,54 @@ __global__ void k_op_keys(const int* gid, const int* g_op, int N, unsigned* keys
   vals[p] = p;
 }
 
+// The leaf-table gradient adds dz . W_in^T of every row into its leaf-table row; it is linear in dz, so the
+// backward first sums dz over the rows of each (op, leaf-table row) and contracts once per distinct row.  Third
+// sort: pool rows by (op, leaf-table row) -- stable passes over the leaf-table row (rows without one: 0), then
+// one by op -- and the runs of equal keys in the result.
+__global__ void k_tok_keys(const int* input_idx, int N, unsigned* keys, int* vals, const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int p = blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= N) return;
+  keys[p] = (unsigned)max(input_idx[p], 0);
+  vals[p] = p;
+}
+__global__ void k_tok_opkeys(const int* vals, const int* gid, const int* g_op, int N, unsigned* keys,
+                             const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  keys[i] = (unsigned)g_op[gid[vals[i]]];
+}
+__global__ void k_tok_flags(const int* tok_rows, const int* gid, const int* g_op, const int* input_idx, int N,
+                            int* flag, const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  const int p = tok_rows[i];
+  int f = 1;
+  if (i > 0) {
+    const int q = tok_rows[i - 1];
+    f = g_op[gid[p]] != g_op[gid[q]] || input_idx[p] != input_idx[q];
+  }
+  flag[i] = f;
+}
+__global__ void k_tok_emit(const int* flag, const int* exs, const int* tok_rows, const int* gid, const int* g_op,
+                           const int* input_idx, int N, int* tok_start, int* tok_row, int* tok_seg, int* op_runs,
+                           const unsigned long long* err) {
+  if (*err != kNoErr) return;
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= N) return;
+  const int p = tok_rows[i];
+  const int u = exs[i] + flag[i] - 1;
+  tok_seg[i] = u;
+  if (flag[i]) {
+    tok_start[u] = i;
+    tok_row[u] = input_idx[p];
+    atomicAdd(&op_runs[g_op[gid[p]]], 1);
+  }
+  if (i == N - 1) tok_start[u + 1] = N;
+}
+
 // for entry q of the (op, row) list: the row's children and leaf-table row
 __global__ void k_op_rows(const int* op_rows, const int* gid, const int* g_row_begin, const int* g_op,
                           const int* g_idx_off, const int* child_pos, const int* input_idx, OpTable ops, int N,
@@ -560,7 +608,7 @@ struct GroupArrays {
   const int* a[kGroupArrays];  // level, op, row_begin, rows, idx_off, child base of slot 0, of slot 1
 };
 __global__ void k_compact(const unsigned long long* err, const int* meta, const int* level_ptr, GroupArrays garr,
-                          int lcap, int gcap, int* out) {
+                          int lcap, int gcap, const int* op_runs, int num_ops, int* out) {
   const unsigned long long e = *err;
   if (threadIdx.x == 0) {
     out[0] = (int)(unsigned)(e & 0xffffffffull);
@@ -573,6 +621,7 @@ __global__ void k_compact(const unsigned long long* err, const int* meta, const 
   int* go = out + kHdr + lcap + 1;
   for (int k = 0; k < kGroupArrays; ++k)
     for (int i = threadIdx.x; i < ng; i += blockDim.x) go[k * gcap + i] = garr.a[k][i];
+  for (int o = threadIdx.x; o < num_ops; o += blockDim.x) go[kGroupArrays * gcap + o] = op_runs[o];
 }
 
 inline dim3 grid_for(long long n) { return dim3((unsigned)std::max(1LL, (n + kBlock - 1) / kBlock)); }
@@ -675,7 +724,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
 
   // persistent arrays sized by N and E; the level and group tables take N + 1 and 5 x N entries (there are
   // at most N levels and N groups), so nothing waits for the depth to be known on the host
-  const size_t n1 = (size_t)N * 19 + 2 * (size_t)E + 16;
+  const size_t n1 = (size_t)N * 23 + 2 * (size_t)E + 17;
   if (hipMalloc(&s.blob, n1 * sizeof(int)) != hipSuccess) {
     set_error("fold_schedule: out of device memory");
     return fail(FOLD_E_NOMEM);
@@ -694,6 +743,10 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   s.op_rows = q; q += N;
   s.op_cpos = q; q += 2 * (size_t)N;
   s.op_inp = q; q += N;
+  s.tok_rows = q; q += N;
+  s.tok_seg = q; q += N;
+  s.tok_start = q; q += N + 1;
+  s.tok_row = q; q += N;
   s.level_ptr = q; q += cap + 1;
   s.g_level = q; q += cap;
   s.g_op = q; q += cap;
@@ -720,9 +773,11 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   const long long rc = 256LL * std::max(B, 1);
   const long long scan_tmp_n = std::max<long long>(rc, N) / kScanTile + 2;
   constexpr int kLcap = 4096, kGcap = 4096;  // levels and groups read back with the error word
-  const size_t stage_n = kHdr + (kLcap + 1) + kGroupArrays * (size_t)kGcap;
+  const size_t stage_n = kHdr + (kLcap + 1) + kGroupArrays * (size_t)kGcap + kMaxOps;
+  int* op_runs = nullptr;  // [kMaxOps] runs of equal (op, leaf-table row) per op
   tmp.reserve(&em, 1);
   tmp.reserve(&stage, stage_n);
+  tmp.reserve(&op_runs, kMaxOps);
   if (N > 0) {
     tmp.reserve(&node_graph, N);
     tmp.reserve(&indeg, N);
@@ -744,6 +799,7 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
   unsigned long long* err = &em->err;
   int* meta = em->meta;
   hipLaunchKernelGGL(k_init_meta, dim3(1), dim3(64), 0, st, em);
+  hipLaunchKernelGGL(k_zero_ints, dim3(1), dim3(kBlock), 0, st, op_runs, kMaxOps);
   hipLaunchKernelGGL(k_check_struct, grid_for(std::max(G + 1, N + 1)), dim3(kBlock), 0, st, b->graph_ptr, G,
                      b->child_ptr, N, E, err);
   if (N > 0) {
@@ -804,9 +860,39 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
                        s.child_pos, s.child_one, ops, s.g_cbase0, s.g_cbase1, err);
     hipLaunchKernelGGL(k_cbase_check, grid_for(N), dim3(kBlock), 0, st, N, gid, s.g_row_begin, s.g_op,
                        s.g_idx_off, s.child_pos, s.child_one, ops, s.g_cbase0, s.g_cbase1, err);
+
+    // rows in (op, leaf-table row) order and their runs (only if some op reads the leaf table)
+    bool any_input = false;
+    for (int i = 0; i < K; ++i) any_input = any_input || b->ops[i].has_input;
+    if (any_input) {
+      int ibits = 1;
+      while (ibits < 31 && ((long long)std::max(b->num_inputs - 1, 0) >> ibits)) ++ibits;
+      hipLaunchKernelGGL(k_tok_keys, grid_for(N), dim3(kBlock), 0, st, s.input_idx, N, ka, va, err);
+      for (int ps = 0; ps < (ibits + 7) / 8; ++ps) {
+        hipLaunchKernelGGL(k_radix_count, dim3(B), dim3(kBlock), 0, st, ka, N, 8 * ps, radix_counts, B, err,
+                           (const int*)nullptr, 0);
+        scan_exclusive(radix_counts, radix_counts, (int)rc, meta + 3, scan_tmp, st);
+        hipLaunchKernelGGL(k_radix_scatter, dim3(B), dim3(kBlock), 0, st, ka, va, kb, vb, radix_counts, N, 8 * ps,
+                           B, err, (const int*)nullptr, 0);
+        std::swap(ka, kb);
+        std::swap(va, vb);
+      }
+      hipLaunchKernelGGL(k_tok_opkeys, grid_for(N), dim3(kBlock), 0, st, va, gid, s.g_op, N, ka, err);
+      hipLaunchKernelGGL(k_radix_count, dim3(B), dim3(kBlock), 0, st, ka, N, 0, radix_counts, B, err,
+                         (const int*)nullptr, 0);
+      scan_exclusive(radix_counts, radix_counts, (int)rc, meta + 3, scan_tmp, st);
+      hipLaunchKernelGGL(k_radix_scatter, dim3(B), dim3(kBlock), 0, st, ka, va, kb, s.tok_rows, radix_counts, N, 0,
+                         B, err, (const int*)nullptr, 0);
+      hipLaunchKernelGGL(k_tok_flags, grid_for(N), dim3(kBlock), 0, st, s.tok_rows, gid, s.g_op, s.input_idx, N,
+                         flag, err);
+      scan_exclusive(flag, exs, N, meta + 7, scan_tmp, st);
+      hipLaunchKernelGGL(k_tok_emit, grid_for(N), dim3(kBlock), 0, st, flag, exs, s.tok_rows, gid, s.g_op,
+                         s.input_idx, N, s.tok_start, s.tok_row, s.tok_seg, op_runs, err);
+    }
   }
   GroupArrays ga{{s.g_level, s.g_op, s.g_row_begin, s.g_rows, s.g_idx_off, s.g_cbase0, s.g_cbase1}};
-  hipLaunchKernelGGL(k_compact, dim3(1), dim3(kBlock), 0, st, err, meta, s.level_ptr, ga, kLcap, kGcap, stage);
+  hipLaunchKernelGGL(k_compact, dim3(1), dim3(kBlock), 0, st, err, meta, s.level_ptr, ga, kLcap, kGcap, op_runs, K,
+                     stage);
   if (hipGetLastError() != hipSuccess) {
     set_error("fold_schedule: kernel launch failed");
     return fail(FOLD_E_DEVICE);
@@ -862,10 +948,13 @@ int32_t schedule_impl(const fold_batch* b, hipStream_t st, fold_sched** out) {
       return fail(FOLD_E_DEVICE);
     }
   }
-  // ranges of op_rows per op
+  // ranges of op_rows per op, and of the runs of equal (op, leaf-table row) per op
   s.h_op_row_ptr.assign(K + 1, 0);
   for (int g = 0; g < ng; ++g) s.h_op_row_ptr[s.h_op[g] + 1] += s.h_rows[g];
   for (int o = 0; o < K; ++o) s.h_op_row_ptr[o + 1] += s.h_op_row_ptr[o];
+  s.h_tok_ptr.assign(K + 1, 0);
+  const int* hr = hb.data() + kHdr + (kLcap + 1) + kGroupArrays * kGcap;
+  for (int o = 0; o < K; ++o) s.h_tok_ptr[o + 1] = s.h_tok_ptr[o] + (N > 0 ? hr[o] : 0);
   *out = h;
   return FOLD_OK;
 }

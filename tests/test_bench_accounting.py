@@ -35,12 +35,19 @@ def test_pass_work_treelstm_counts():
 def test_pass_work_bf16_state_bytes_and_table_grad():
     H = 32
     w = _treelstm_workload(H, "bf16")
+    # three leaves reading leaf-table rows 5, 9, 5 (two distinct) and one internal node
+    w.node_op = [0, 0, 0, 1]
+    w.node_input = [5, 9, 5, -1]
     host = dict(group_op=[0], group_rows=[3])
     work = bench.pass_work(w, host, table_grad=True)
     S = H * (2 + 4)  # bf16 h, fp32 c
     assert work[("fwd", 0)][1] == 3 * (2 * H + S) + H * 3 * H * 2 + 3 * H * 4
-    # with a trainable table the leaf backward contracts dz with W_in^T and writes the table row
-    assert work[("bwd", 0)] == (2.0 * 3 * 3 * H * H, 3 * (8 * H + 4 * H) + H * 3 * H * 2)
+    # the leaf backward is the cell's elementwise part; the leaf-table gradient is a pass of its own: every
+    # row's dz read once, then one contraction row per distinct leaf-table row, read and written
+    assert work[("bwd", 0)] == (0.0, 3 * 8 * H)
+    assert work[("tgrad", 0)] == (2.0 * 2 * 3 * H * H, 3 * 3 * H * 2 + 2 * H * 4 * 2 + H * 3 * H * 2)
+    assert bench.table_runs(w) == {0: 2}
+    assert bench.flops_by_kernel(w, host, True)["tgrad.bf16"] == 2.0 * 2 * 3 * H * H
 
 
 def test_pass_of_routes_launches():
@@ -50,6 +57,8 @@ def test_pass_of_routes_launches():
     assert bench.pass_of("bwd_dx.bf16", 2, 1) == [("bwd", 2)]
     assert bench.pass_of("wgrad.bf16", -1, 1) == [("wgrad", 1)]
     assert bench.pass_of("wgrad_reduce", -1, 0) == [("wgrad", 0)]
+    assert bench.pass_of("tgrad.bf16", -1, 0) == [("tgrad", 0)]
+    assert bench.pass_of("tgrad_sum", -1, 0) == [("tgrad", 0)]
     assert bench.pass_of("bwd_init", -1, -1) == []
     assert bench.pass_of("roots", -1, -1) == []
     # a level launch over groups 4, 5, 6 (op = -1 - 3)

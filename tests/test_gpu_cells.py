@@ -162,3 +162,48 @@ def test_backward_rejects_misaligned_gradient_buffers():
                             dev.ws_bytes, dev.stream)
         assert e.value.code == F.FOLD_E_INVALID and "aligned" in str(e.value), list(case)
     torch.cuda.synchronize()
+
+
+def _table_runs_case(dtype, graphs=256, leaves=64, H=32, V=5, seed=21):
+    """Balanced trees of `leaves` Tree-LSTM leaves with an LSTM chain of three steps on each root; every leaf
+    and LSTM step reads one of V leaf-table rows, row 0 for 80 % of them."""
+    from tests._helpers import make_workload
+    rng = np.random.default_rng(seed)
+    ops = [gen.OpSpec(gen.KIND_TREELSTM, 0, 1, 0), gen.OpSpec(gen.KIND_TREELSTM, 2, 0, 0),
+           gen.OpSpec(gen.KIND_LSTM, 1, 1, 1)]
+    params = [gen.make_param_set(rng, gen.KIND_TREELSTM, H, 2, H, dtype),
+              gen.make_param_set(rng, gen.KIND_LSTM, H, 1, H, dtype)]
+    table = gen._finish_values(0.1 * rng.standard_normal((V, H)), dtype)
+
+    def token():
+        return 0 if rng.random() < 0.8 else int(rng.integers(1, V))
+    batch = []
+    for _ in range(graphs):
+        nodes = [(0, [], token()) for _ in range(leaves)]
+        level = list(range(leaves))
+        while len(level) > 1:
+            nxt = []
+            for a, b in zip(level[0::2], level[1::2]):
+                nodes.append((1, [a, b], -1))
+                nxt.append(len(nodes) - 1)
+            level = nxt
+        for _ in range(3):
+            nodes.append((2, [len(nodes) - 1], token()))
+        batch.append(nodes)
+    w = make_workload(batch, ops, params, H, table, dtype=dtype, seed=seed, name=f"table_runs_{dtype}")
+    w.backward = True
+    return w
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_leaf_table_gradient_long_runs(dtype):
+    """The leaf-table gradient sums dz over the rows of each (op, leaf-table row) before contracting once per
+    distinct leaf-table row.  16,384 leaves and 768 LSTM steps read 5 table rows (row 0 for 80 % of them): runs
+    of thousands of rows cross many summing workgroups (whose partial sums are added atomically), and two ops
+    add into the same table rows.  Every state and gradient against the oracle, the table gradient included."""
+    w = _table_runs_case(dtype)
+    g, o = C.run_device(w, table_grad=True), C.run_oracle(w, table_grad=True)
+    C.compare_all(w, g, o, table_grad=True)
+    # and row by row (the table's rows differ in size: row 0 sums 80 % of the rows)
+    from oracle import compare
+    assert compare.rel_err(g["d_table"], o["d_table"]) <= C.TOL[dtype]
