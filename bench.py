@@ -294,10 +294,8 @@ def pass_work(w, host, table_grad: bool) -> dict:
             if w.backward:
                 out[("bwd", g)] = (0.0, attn_bytes(w, op, rows, "bwd"))
             continue
-        if op.kind == gen.KIND_EMBED:
+        if op.kind == gen.KIND_EMBED:  # its leaf-table gradient is a ("tgrad", op) pass
             out[("fwd", g)] = (0.0, float(rows * 2 * H * bh))
-            if w.backward and table_grad:
-                out[("bwd", g)] = (0.0, float(rows * 4 * H))
             continue
         G = live_gates(op)
         din = w.params[op.param_set].in_dim if op.has_input else 0
@@ -315,7 +313,10 @@ def pass_work(w, host, table_grad: bool) -> dict:
         runs = table_runs(w)
         for o, count in op_rows.items():
             op = w.ops[o]
-            if o not in runs or op.kind == gen.KIND_EMBED:
+            if o not in runs:
+                continue
+            if op.kind == gen.KIND_EMBED:  # every row's dh read once, each distinct leaf-table row read and written
+                out[("tgrad", o)] = (0.0, float(count * 4 * H + runs[o] * H * 4 * 2))
                 continue
             G, din = live_gates(op), w.params[op.param_set].in_dim
             # read every row's dz once, read and write each distinct leaf-table row, the weights once
@@ -347,7 +348,7 @@ def pass_of(name: str, group: int, op: int):
         return [("bwd", g) for g in groups]
     if group < 0 and op >= 0 and cls in ("wgrad", "wgrad_reduce", "bias_partial", "bias_reduce", "attn_wgrad"):
         return [("wgrad", op)]
-    if group < 0 and op >= 0 and cls in ("tgrad", "tgrad_sum"):
+    if group < 0 and op >= 0 and cls in ("tgrad", "tgrad_sum", "tgrad_embed"):
         return [("tgrad", op)]
     return []
 

@@ -604,13 +604,14 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
         attn_group.push_back(g);
         continue;
       }
+      // an embedding has no children and no dz: its only gradient, the leaf table's, is added per op below
+      if (op.kind == FOLD_EMBED) continue;
       const bool leaf = is_tree_lstm_leaf(op);
       const int Kb = (leaf ? gates_of(kTreeLstmLeaf) : ps.G) * p.HP;
       // a dz . W^T whose K slices add into the children atomically needs their dh rows zeroed first
       b.zero_child_dh = dh_fresh && op.arity > 0 && dx_plan(b.rows, op.arity * p.HP, Kb, esize, true).ksplit > 1;
       ckind.push_back(leaf ? kTreeLstmLeaf : op.kind);
       cargs.push_back(b);
-      if (op.kind == FOLD_EMBED) continue;
       DxArgs d;
       d.rows = b.rows;
       d.row_begin = b.row_begin;
@@ -685,10 +686,15 @@ int32_t backward_impl(const Sched& s, const Packed& p, const void* table, int64_
   if (grads) {
     for (int o = 0; o < s.num_ops; ++o) {
       const fold_op& op = s.ops[o];
-      if (op.kind == FOLD_EMBED) continue;
       prof_tag(-1, o);
       const int count = s.h_op_row_ptr[o + 1] - s.h_op_row_ptr[o];
       if (count <= 0) continue;
+      if (op.kind == FOLD_EMBED) {  // the leaf-table gradient: dh summed over each leaf-table row's rows
+        if (d_table)
+          launch_tok_table(s.tok_rows, s.tok_seg, s.tok_start, s.tok_row, s.h_op_row_ptr[o], count, dh, p.ld, p.H,
+                           d_table, tld, st);
+        continue;
+      }
       const PackedSet& ps = p.sets[op.param_set];
       const fold_param_grads& pg = grads->sets[op.param_set];
       if (is_attn(op.kind)) {

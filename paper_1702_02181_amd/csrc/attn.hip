@@ -254,37 +254,42 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_bwd(AttnArgs a) {
 
 // Partial sums of the scorer's gradient over chunks of kAttnWgradChunk op rows (workgroup x), one column
 // per thread (workgroup y: 256 columns): column j < H of chunk q is sum_r de_r h_c(r)[j] over the chunk's rows
-// in order; column HP holds sum_r de_r (thread 0 of the first column block).
+// in order; column HP holds sum_r de_r (thread 0 of the first column block).  The chunk's de and child rows are
+// staged in LDS first (their loads all in flight at once), then each thread keeps eight rows' loads in flight.
 template <typename T>
 __global__ __launch_bounds__(256) void k_attn_wgrad(const int* op_rows, const int* op_cpos, int count, int H,
                                                     int HP, int ld, const T* h_pool, const float* gates,
                                                     int gstride, float* part) {
+  __shared__ float sde[kAttnWgradChunk];
+  __shared__ int sch[kAttnWgradChunk];
+  const int q0 = blockIdx.x * kAttnWgradChunk, n = min(count, q0 + kAttnWgradChunk) - q0;
+  for (int t = threadIdx.x; t < n; t += blockDim.x) {
+    sde[t] = gates[(size_t)op_rows[q0 + t] * gstride];
+    sch[t] = op_cpos[2 * (size_t)(q0 + t)];
+  }
+  __syncthreads();
   const int j = blockIdx.y * blockDim.x + threadIdx.x;
   const bool bias = blockIdx.y == 0 && threadIdx.x == 0;
   if (j >= H && !bias) return;
-  const int q0 = blockIdx.x * kAttnWgradChunk, q1 = min(count, q0 + kAttnWgradChunk);
   float acc = 0.f, bsum = 0.f;
-  int q = q0;
-  // eight rows' loads in flight, added in row order
-  for (; q + 8 <= q1; q += 8) {
-    float de[8], v[8];
+  int t = 0;
+  for (; t + 8 <= n; t += 8) {
+    float v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      de[u] = gates[(size_t)op_rows[q + u] * gstride];
-      const int c = op_cpos[2 * (size_t)(q + u)];
+      const int c = sch[t + u];
       v[u] = j < H && c >= 0 ? to_f32<T>(h_pool[(size_t)c * ld + j]) : 0.f;
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      acc += de[u] * v[u];
-      bsum += de[u];
+      acc += sde[t + u] * v[u];
+      bsum += sde[t + u];
     }
   }
-  for (; q < q1; ++q) {
-    const float de = gates[(size_t)op_rows[q] * gstride];
-    const int c = op_cpos[2 * (size_t)q];
-    acc += de * (j < H && c >= 0 ? to_f32<T>(h_pool[(size_t)c * ld + j]) : 0.f);
-    bsum += de;
+  for (; t < n; ++t) {
+    const int c = sch[t];
+    acc += sde[t] * (j < H && c >= 0 ? to_f32<T>(h_pool[(size_t)c * ld + j]) : 0.f);
+    bsum += sde[t];
   }
   float* out = part + (size_t)blockIdx.x * (HP + kPadK);
   if (j < H) out[j] = acc;

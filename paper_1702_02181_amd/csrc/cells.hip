@@ -503,14 +503,31 @@ __global__ void k_cell_epi(FwdArgs a, int nsplit) {
 }
 
 template <typename T>
-__global__ void k_embed_fwd(int rows, int row_begin, int H, int ld, int tld, const T* table,
-                            const int* input_idx, T* h_pool, float* c_pool) {
-  const int row = blockIdx.x;
+__global__ __launch_bounds__(256) void k_embed_fwd(int rows, int row_begin, int H, int ld, int tld, const T* table,
+                                                   const int* input_idx, T* h_pool, float* c_pool) {
+  // one wave per row, four rows a workgroup; a lane copies four consecutive elements (rows are whole 64-element
+  // segments, 16-byte aligned)
+  const int lane = threadIdx.x & 63, row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
   const size_t p = (size_t)(row_begin + row);
-  const int ti = input_idx[p];
-  for (int j = threadIdx.x; j < ld; j += blockDim.x) {
-    h_pool[p * ld + j] = j < H ? table[(size_t)ti * tld + j] : from_f32<T>(0.f);
-    c_pool[p * ld + j] = 0.f;
+  const T* src = table + (size_t)input_idx[p] * tld;
+  for (int j = 4 * lane; j < ld; j += 256) {
+    if constexpr (sizeof(T) == 4) {
+      float4 v = *reinterpret_cast<const float4*>(src + j);
+      if (j + 4 > H) {
+        v.x = j < H ? v.x : 0.f, v.y = j + 1 < H ? v.y : 0.f, v.z = j + 2 < H ? v.z : 0.f, v.w = 0.f;
+      }
+      *reinterpret_cast<float4*>(h_pool + p * ld + j) = v;
+    } else {
+      uint2 v = *reinterpret_cast<const uint2*>(src + j);
+      if (j + 4 > H) {
+        const uint32_t m0 = j < H ? (j + 1 < H ? 0xffffffffu : 0xffffu) : 0u;
+        const uint32_t m1 = j + 2 < H ? (j + 3 < H ? 0xffffffffu : 0xffffu) : 0u;
+        v.x &= m0, v.y &= m1;
+      }
+      *reinterpret_cast<uint2*>(h_pool + p * ld + j) = v;
+    }
+    *reinterpret_cast<float4*>(c_pool + p * ld + j) = make_float4(0.f, 0.f, 0.f, 0.f);
   }
 }
 
@@ -1071,15 +1088,19 @@ void cell_fwd_t(int kind, const FwdArgs& a, hipStream_t st) {
 
 constexpr int kTokRows = 256;  // at most this many entries of the (op, leaf-table row) list per workgroup
 
-// A workgroup per `per` (at most kTokRows) consecutive entries of the op's list, a thread per four consecutive dz
-// columns.  A run
-// that lies inside the workgroup's entries is stored; the first and the last run may cross its ends and are then
-// added atomically into the zeroed sums.  Eight rows' loads go out before they are added.
-template <bool BF>
-__global__ __launch_bounds__(256) void k_tok_sum(const int* tok_rows, const int* tok_seg, const int* tok_start, int i0,
-                                                 int count, int per, int u0, const float* dz, int gstride,
-                                                 int Kb, float* zsum) {
-  __shared__ int srow[kTokRows], sseg[kTokRows];
+// A workgroup per `per` (at most kTokRows) consecutive entries of the op's list, a thread per four consecutive
+// columns.  TABLE = false: dz (fp32, or bf16 at the start of each row) summed into zsum[run - u0][Kb]; a run that
+// lies inside the workgroup's entries is stored, the first and the last run, which may cross its ends, are added
+// atomically into the zeroed sums.  TABLE = true (an embedding op): its fp32 dh rows summed and added straight
+// into the leaf-table gradient's row of the run (columns < ncols, row stride tld): read-add-written inside the
+// workgroup's entries (each row once per op), atomically for the crossing runs.  Eight rows' loads go out before
+// they are added.
+template <bool BF, bool TABLE>
+__global__ __launch_bounds__(256) void k_tok_sum(const int* tok_rows, const int* tok_seg, const int* tok_start,
+                                                 const int* tok_row, int i0, int count, int per, int u0,
+                                                 const float* dz, int gstride, int Kb, int ncols, int tld,
+                                                 float* out) {
+  __shared__ int srow[kTokRows], sseg[kTokRows], strow[kTokRows];
   const int b0 = i0 + blockIdx.x * per, b1 = min(i0 + count, b0 + per), n = b1 - b0;
   for (int t = threadIdx.x; t < n; t += blockDim.x) {
     srow[t] = tok_rows[b0 + t];
@@ -1087,6 +1108,10 @@ __global__ __launch_bounds__(256) void k_tok_sum(const int* tok_rows, const int*
   }
   __syncthreads();
   const int ufirst = sseg[0], ulast = sseg[n - 1];
+  if constexpr (TABLE) {  // leaf-table rows of the workgroup's runs (at most one per entry)
+    for (int t = threadIdx.x; t <= ulast - ufirst; t += blockDim.x) strow[t] = tok_row[ufirst + t];
+    __syncthreads();
+  }
   const bool first_out = tok_start[ufirst] < b0, last_out = tok_start[ulast + 1] > b1;
   auto load = [&](int t, int j, float (&v)[4]) {
     const float* row = dz + (size_t)srow[t] * gstride;
@@ -1099,15 +1124,29 @@ __global__ __launch_bounds__(256) void k_tok_sum(const int* tok_rows, const int*
     }
   };
   auto flush = [&](int u, int j, const float (&acc)[4]) {
-    float* dst = zsum + (size_t)(u - u0) * Kb + j;
-    if ((u == ufirst && first_out) || (u == ulast && last_out)) {
+    const bool crossing = (u == ufirst && first_out) || (u == ulast && last_out);
+    if constexpr (TABLE) {
+      float* dst = out + (size_t)strow[u - ufirst] * tld + j;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) atomicAdd(dst + e, acc[e]);
+      for (int e = 0; e < 4; ++e) {
+        if (j + e >= ncols) break;
+        if (crossing)
+          atomicAdd(dst + e, acc[e]);
+        else
+          dst[e] += acc[e];
+      }
     } else {
-      *reinterpret_cast<float4*>(dst) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      float* dst = out + (size_t)(u - u0) * Kb + j;
+      if (crossing) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) atomicAdd(dst + e, acc[e]);
+      } else {
+        *reinterpret_cast<float4*>(dst) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+      }
     }
   };
-  for (int j = 4 * threadIdx.x; j < Kb; j += 4 * blockDim.x) {
+  const int cols = TABLE ? ncols : Kb;
+  for (int j = 4 * threadIdx.x; j < cols; j += 4 * blockDim.x) {
     float acc[4] = {0.f, 0.f, 0.f, 0.f};
     int u = ufirst;
     auto add = [&](int t, const float (&v)[4]) {
@@ -1168,10 +1207,10 @@ void launch_embed_fwd(int dtype, int rows, int row_begin, int H, int ld, int tld
   if (rows <= 0) return;
   ProfScope prof("embed_fwd", st);
   if (dtype == FOLD_BF16)
-    hipLaunchKernelGGL(k_embed_fwd<uint16_t>, dim3(rows), dim3(256), 0, st, rows, row_begin, H, ld, tld,
+    hipLaunchKernelGGL(k_embed_fwd<uint16_t>, dim3(cdiv(rows, 4)), dim3(256), 0, st, rows, row_begin, H, ld, tld,
                        static_cast<const uint16_t*>(table), input_idx, static_cast<uint16_t*>(h_pool), c_pool);
   else
-    hipLaunchKernelGGL(k_embed_fwd<float>, dim3(rows), dim3(256), 0, st, rows, row_begin, H, ld, tld,
+    hipLaunchKernelGGL(k_embed_fwd<float>, dim3(cdiv(rows, 4)), dim3(256), 0, st, rows, row_begin, H, ld, tld,
                        static_cast<const float*>(table), input_idx, static_cast<float*>(h_pool), c_pool);
 }
 
@@ -1228,25 +1267,36 @@ void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
 #undef FOLD_CB
 }
 
+// entries of the (op, leaf-table row) list per summing workgroup: enough workgroups to fill the GPU a few times
+// over (short runs that cross a workgroup's ends cost atomic adds, so no fewer than 32 entries)
+static int tok_per(int count) { return std::max(32, std::min(kTokRows, count / 1024 / 8 * 8)); }
+
 void launch_tok_sum(int dtype, const int* tok_rows, const int* tok_seg, const int* tok_start, int i0, int count,
                     int u0, int U, const float* dz, int gstride, int Kb, float* zsum, uint16_t* zbf, hipStream_t st) {
   if (count <= 0 || U <= 0) return;
   ProfScope prof("tgrad_sum", st);
   const size_t n = (size_t)U * Kb;
   hipLaunchKernelGGL(k_zero_f32, dim3((unsigned)std::min<size_t>((n + 255) / 256, 8192)), dim3(256), 0, st, zsum, n);
-  // entries per workgroup: enough workgroups to fill the GPU a few times over (short runs that cross a
-  // workgroup's ends cost atomic adds, so no fewer than 32 entries)
-  const int per = std::max(32, std::min(kTokRows, count / 1024 / 8 * 8));
+  const int per = tok_per(count);
   const dim3 grid(cdiv(count, per));
   if (dtype == FOLD_BF16) {
-    hipLaunchKernelGGL(k_tok_sum<true>, grid, dim3(256), 0, st, tok_rows, tok_seg, tok_start, i0, count, per, u0, dz,
-                       gstride, Kb, zsum);
+    hipLaunchKernelGGL((k_tok_sum<true, false>), grid, dim3(256), 0, st, tok_rows, tok_seg, tok_start, nullptr, i0,
+                       count, per, u0, dz, gstride, Kb, 0, 0, zsum);
     hipLaunchKernelGGL(k_tok_cast, dim3((unsigned)std::min<size_t>((n + 255) / 256, 8192)), dim3(256), 0, st, zsum,
                        n, zbf);
   } else {
-    hipLaunchKernelGGL(k_tok_sum<false>, grid, dim3(256), 0, st, tok_rows, tok_seg, tok_start, i0, count, per, u0,
-                       dz, gstride, Kb, zsum);
+    hipLaunchKernelGGL((k_tok_sum<false, false>), grid, dim3(256), 0, st, tok_rows, tok_seg, tok_start, nullptr, i0,
+                       count, per, u0, dz, gstride, Kb, 0, 0, zsum);
   }
+}
+
+void launch_tok_table(const int* tok_rows, const int* tok_seg, const int* tok_start, const int* tok_row, int i0,
+                      int count, const float* dh, int ld, int H, float* d_table, int tld, hipStream_t st) {
+  if (count <= 0) return;
+  ProfScope prof("tgrad_embed", st);
+  const int per = tok_per(count);
+  hipLaunchKernelGGL((k_tok_sum<false, true>), dim3(cdiv(count, per)), dim3(256), 0, st, tok_rows, tok_seg, tok_start,
+                     tok_row, i0, count, per, 0, dh, ld, 0, H, tld, d_table);
 }
 
 void launch_bwd_dx(int dtype, const DxArgs& a0, hipStream_t st, const char* name) {

@@ -231,6 +231,10 @@ void launch_bwd_dx(int dtype, const DxArgs& a, hipStream_t st, const char* name 
 // (one op's), runs u0 .. u0 + U - 1, into zsum [U][Kb] fp32 (zeroed here), and for bf16 its bf16 copy zbf [U][Kb]
 void launch_tok_sum(int dtype, const int* tok_rows, const int* tok_seg, const int* tok_start, int i0, int count,
                     int u0, int U, const float* dz, int gstride, int Kb, float* zsum, uint16_t* zbf, hipStream_t st);
+// an embedding op's leaf-table gradient: its fp32 dh rows (stride ld) summed over the runs of entries i0 ..
+// i0 + count - 1 and added into the runs' leaf-table rows (columns < H, stride tld)
+void launch_tok_table(const int* tok_rows, const int* tok_seg, const int* tok_start, const int* tok_row, int i0,
+                      int count, const float* dh, int ld, int H, float* d_table, int tld, hipStream_t st);
 // true if launch_bwd_dx would run this call on narrow tiles (the ones a level launch can merge)
 bool bwd_dx_is_narrow(int dtype, const DxArgs& a);
 void launch_level_dx(int dtype, const DxArgs* args, int n, hipStream_t st);
