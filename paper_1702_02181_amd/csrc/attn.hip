@@ -252,48 +252,59 @@ __global__ __launch_bounds__(kRowsPerBlock* kWave) void k_attn_bwd(AttnArgs a) {
   }
 }
 
-// Partial sums of the scorer's gradient over chunks of kAttnWgradChunk op rows (workgroup x), one column
-// per thread (workgroup y: 256 columns): column j < H of chunk q is sum_r de_r h_c(r)[j] over the chunk's rows
-// in order; column HP holds sum_r de_r (thread 0 of the first column block).  The chunk's de and child rows are
-// staged in LDS first (their loads all in flight at once), then each thread keeps eight rows' loads in flight.
+// Partial sums of the scorer's gradient over chunks of kAttnWgradChunk op rows (workgroup x) and 256 columns
+// (workgroup y): column j < H of chunk q is sum_r de_r h_c(r)[j]; column HP holds sum_r de_r (first column
+// block).  The chunk's de and child rows are staged in LDS first; then each of the four waves sums a quarter of
+// the rows in order, a lane over four consecutive columns (sixteen rows' loads in flight), and the waves' sums
+// are added in wave order.
 template <typename T>
 __global__ __launch_bounds__(256) void k_attn_wgrad(const int* op_rows, const int* op_cpos, int count, int H,
                                                     int HP, int ld, const T* h_pool, const float* gates,
                                                     int gstride, float* part) {
+  constexpr int kQ = kAttnWgradChunk / 4;  // rows per wave
   __shared__ float sde[kAttnWgradChunk];
   __shared__ int sch[kAttnWgradChunk];
+  __shared__ float red[4][256];
   const int q0 = blockIdx.x * kAttnWgradChunk, n = min(count, q0 + kAttnWgradChunk) - q0;
   for (int t = threadIdx.x; t < n; t += blockDim.x) {
     sde[t] = gates[(size_t)op_rows[q0 + t] * gstride];
     sch[t] = op_cpos[2 * (size_t)(q0 + t)];
   }
   __syncthreads();
-  const int j = blockIdx.y * blockDim.x + threadIdx.x;
-  const bool bias = blockIdx.y == 0 && threadIdx.x == 0;
-  if (j >= H && !bias) return;
-  float acc = 0.f, bsum = 0.f;
-  int t = 0;
-  for (; t + 8 <= n; t += 8) {
-    float v[8];
+  const int lane = threadIdx.x & (kWave - 1), w = threadIdx.x >> 6;
+  const int jl = 4 * lane, j = blockIdx.y * 256 + jl;  // this lane's four columns (j < ld: rows are 64-wide)
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  const int t0 = w * kQ, t1 = min(n, t0 + kQ);
+  if (j < H) {
+    for (int t = t0; t < t1; t += 16) {
+      float v[16][4];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int c = sch[t + u];
-      v[u] = j < H && c >= 0 ? to_f32<T>(h_pool[(size_t)c * ld + j]) : 0.f;
-    }
+      for (int u = 0; u < 16; ++u) {
+        const int c = t + u < t1 ? sch[t + u] : -1;
+        if (c >= 0)
+          ld4(h_pool + (size_t)c * ld + j, v[u]);
+        else
+          v[u][0] = v[u][1] = v[u][2] = v[u][3] = 0.f;
+      }
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      acc += sde[t + u] * v[u];
-      bsum += sde[t + u];
+      for (int u = 0; u < 16; ++u) {
+        const float d = t + u < t1 ? sde[t + u] : 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] += d * v[u][e];
+      }
     }
   }
-  for (; t < n; ++t) {
-    const int c = sch[t];
-    acc += sde[t] * (j < H && c >= 0 ? to_f32<T>(h_pool[(size_t)c * ld + j]) : 0.f);
-    bsum += sde[t];
-  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) red[w][jl + e] = acc[e];
+  __syncthreads();
   float* out = part + (size_t)blockIdx.x * (HP + kPadK);
-  if (j < H) out[j] = acc;
-  if (bias) out[HP] = bsum;
+  const int c = blockIdx.y * 256 + threadIdx.x;
+  if (c < H) out[c] = ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
+  if (blockIdx.y == 0 && threadIdx.x == 0) {
+    float bsum = 0.f;
+    for (int t = 0; t < n; ++t) bsum += sde[t];
+    out[HP] = bsum;
+  }
 }
 
 // Sum of the chunks' partials, 64 columns (column H: the bias) per workgroup: the four waves sum a quarter
