@@ -588,103 +588,96 @@ __global__ void k_bwd_roots(int ld, const float* dh_roots, const int* root_pos, 
 // dz of one row from its saved activations, written over them in place (each thread rewrites only the
 // elements it read): fp32 dz over fp32 activations (fp32 parameters), or bf16 dz over fp16 activations
 // (bf16 parameters: the G*HP halves at the row's start, the matrix-core operand of dz . W^T and of the
-// weight gradients).
+// weight gradients).  A thread takes two adjacent columns (j even; rows are whole 64-column segments), so every
+// access is a 4-byte (fp16 / bf16 pair) or 8-byte (fp32 pair) one; columns past H give zeros.
 template <int KIND, bool BF>
 __device__ __forceinline__ void cell_bwd_body(const BwdCellArgs a, int row) {
+  static_assert(KIND != FOLD_EMBED, "an embedding has no cell backward (its leaf-table gradient runs per op)");
   constexpr int G = Gates<KIND>::G;
+  constexpr int NK = KIND == FOLD_TREELSTM || KIND == FOLD_TREERNN ? 2
+                     : (KIND == FOLD_LSTM || KIND == FOLD_PROJ ? 1 : 0);  // child slots
   const size_t p = (size_t)(a.row_begin + row);
   float* gb = a.gates + p * a.gstride;
   uint16_t* gh = reinterpret_cast<uint16_t*>(gb);
-  auto gate = [&](int g, int j) -> float {
-    if constexpr (BF)
-      return (float)__builtin_bit_cast(_Float16, gh[g * a.HP + j]);
-    else
-      return gb[g * a.HP + j];
-  };
-  int c0 = -1, c1 = -1;
-  bool s0 = false, s1 = false;
-  if (a.arity >= 1) {
-    c0 = a.child_pos[a.idx_off + row * a.arity];
-    s0 = a.child_one[a.idx_off + row * a.arity] != 0;
-  }
-  if (a.arity >= 2) {
-    c1 = a.child_pos[a.idx_off + row * a.arity + 1];
-    s1 = a.child_one[a.idx_off + row * a.arity + 1] != 0;
-  }
-  auto put = [&](int g, int j, float v) {
-    if constexpr (BF)
-      gh[g * a.HP + j] = f2bf(v);
-    else
-      gb[g * a.HP + j] = v;
-  };
-  // a child's gradient of c: stored whole by its only parent, added atomically into a zeroed row otherwise
-  auto dc_to = [&](int c, bool single, int j, float v) {
-    float* dst = &a.dc[(size_t)c * a.ld + j];
-    if (single)
-      *dst = v;
-    else
-      unsafeAtomicAdd(dst, v);
-  };
-  for (int j = threadIdx.x; j < a.HP; j += blockDim.x) {
-    if (a.zero_child_dh) {  // this group's dz . W^T adds K slices atomically into its children's dh
-      if (c0 >= 0 && s0) a.dh[(size_t)c0 * a.ld + j] = 0.f;
-      if (c1 >= 0 && s1) a.dh[(size_t)c1 * a.ld + j] = 0.f;
-    }
-    if (j >= a.H || KIND == FOLD_TREERNN) {  // pad columns; a TreeRNN passes no cell state to its children
-      if (c0 >= 0 && s0) a.dc[(size_t)c0 * a.ld + j] = 0.f;
-      if (c1 >= 0 && s1) a.dc[(size_t)c1 * a.ld + j] = 0.f;
-    }
-    if (j >= a.H) {
-      if constexpr (KIND != FOLD_EMBED) {
+  int ck[2] = {-1, -1};
+  bool sk[2] = {false, false};
 #pragma unroll
-        for (int g = 0; g < G; ++g) put(g, j, 0.f);
-      }
-      continue;
+  for (int k = 0; k < NK; ++k)
+    if (k < a.arity) {
+      ck[k] = a.child_pos[a.idx_off + row * a.arity + k];
+      sk[k] = a.child_one[a.idx_off + row * a.arity + k] != 0;
     }
-    const float dh = a.dh[p * a.ld + j];
-    if constexpr (KIND == FOLD_EMBED) {
-      if (a.d_table) unsafeAtomicAdd(&a.d_table[(size_t)a.input_idx[p] * a.tld + j], dh);
-    } else if constexpr (KIND == FOLD_TREELSTM) {
-      const float dc = a.dc[p * a.ld + j];
-      const float i_ = gate(0, j), fl = gate(1, j), fr = gate(2, j), o = gate(3, j), u = gate(4, j);
-      const float m = a.u_mask ? a.u_mask[p * a.ld + j] : 1.f;
-      const float tc = tanhf_(a.c_pool[p * a.ld + j]);
-      const float cl = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
-      const float cr = c1 >= 0 ? a.c_pool[(size_t)c1 * a.ld + j] : 0.f;
-      const float dct = dc + dh * o * (1.f - tc * tc);
-      put(0, j, dct * (m * u) * i_ * (1.f - i_));
-      put(1, j, dct * cl * fl * (1.f - fl));
-      put(2, j, dct * cr * fr * (1.f - fr));
-      put(3, j, dh * tc * o * (1.f - o));
-      put(4, j, dct * i_ * m * (1.f - u * u));
-      if (c0 >= 0) dc_to(c0, s0, j, dct * fl);
-      if (c1 >= 0) dc_to(c1, s1, j, dct * fr);
-    } else if constexpr (KIND == kTreeLstmLeaf) {
-      const float dc = a.dc[p * a.ld + j];
-      const float i_ = gate(0, j), o = gate(1, j), u = gate(2, j);
-      const float m = a.u_mask ? a.u_mask[p * a.ld + j] : 1.f;
-      const float tc = tanhf_(a.c_pool[p * a.ld + j]);
-      const float dct = dc + dh * o * (1.f - tc * tc);
-      put(0, j, dct * (m * u) * i_ * (1.f - i_));
-      put(1, j, dh * tc * o * (1.f - o));
-      put(2, j, dct * i_ * m * (1.f - u * u));
-    } else if constexpr (KIND == FOLD_LSTM) {
-      const float dc = a.dc[p * a.ld + j];
-      const float i_ = gate(0, j), f = gate(1, j), o = gate(2, j), u = gate(3, j);
-      const float m = a.u_mask ? a.u_mask[p * a.ld + j] : 1.f;
-      const float tc = tanhf_(a.c_pool[p * a.ld + j]);
-      const float cp = c0 >= 0 ? a.c_pool[(size_t)c0 * a.ld + j] : 0.f;
-      const float dct = dc + dh * o * (1.f - tc * tc);
-      put(0, j, dct * (m * u) * i_ * (1.f - i_));
-      put(1, j, dct * cp * f * (1.f - f));
-      put(2, j, dh * tc * o * (1.f - o));
-      put(3, j, dct * i_ * m * (1.f - u * u));
-      if (c0 >= 0) dc_to(c0, s0, j, dct * f);
-    } else {
-      const float h = gate(0, j);
-      put(0, j, dh * (1.f - h * h));
-      if constexpr (KIND == FOLD_PROJ) {  // c = c_child: the child's dc is this row's
-        if (c0 >= 0) dc_to(c0, s0, j, a.dc[p * a.ld + j]);
+  auto ld2 = [](const float* q, float (&v)[2]) {
+    const float2 t = *reinterpret_cast<const float2*>(q);
+    v[0] = t.x, v[1] = t.y;
+  };
+  const float* own = a.c_pool + p * a.ld;
+  for (int j = 2 * threadIdx.x; j < a.HP; j += 2 * blockDim.x) {
+    const bool live[2] = {j < a.H, j + 1 < a.H};
+    float g[G][2];
+#pragma unroll
+    for (int q = 0; q < G; ++q) {
+      if constexpr (BF) {
+        const uint32_t t = *reinterpret_cast<const uint32_t*>(gh + q * a.HP + j);
+        g[q][0] = (float)__builtin_bit_cast(_Float16, (uint16_t)(t & 0xffff));
+        g[q][1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(t >> 16));
+      } else {
+        ld2(gb + q * a.HP + j, g[q]);
+      }
+    }
+    float dh[2], dz[G][2], dck[2][2] = {{0.f, 0.f}, {0.f, 0.f}};  // dc passed to child slot k
+    ld2(a.dh + p * a.ld + j, dh);
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      if constexpr (KIND == FOLD_TREELSTM || KIND == kTreeLstmLeaf || KIND == FOLD_LSTM) {
+        const float dc = a.dc[p * a.ld + j + e];
+        const float m = a.u_mask ? a.u_mask[p * a.ld + j + e] : 1.f;
+        const float tc = tanhf_(own[j + e]);
+        // gate order: Tree-LSTM i f_l f_r o u; leaf i o u; LSTM i f o u
+        constexpr int GO = KIND == FOLD_TREELSTM ? 3 : (KIND == kTreeLstmLeaf ? 1 : 2);
+        const float i_ = g[0][e], o = g[GO][e], u = g[G - 1][e];
+        const float dct = dc + dh[e] * o * (1.f - tc * tc);
+        dz[0][e] = dct * (m * u) * i_ * (1.f - i_);
+        dz[GO][e] = dh[e] * tc * o * (1.f - o);
+        dz[G - 1][e] = dct * i_ * m * (1.f - u * u);
+#pragma unroll
+        for (int k = 0; k < NK; ++k) {  // the forget gates: f_l, f_r (Tree-LSTM) or f (LSTM), gates 1 .. NK
+          const float f = g[1 + k][e];
+          const float cc = ck[k] >= 0 ? a.c_pool[(size_t)ck[k] * a.ld + j + e] : 0.f;
+          dz[1 + k][e] = dct * cc * f * (1.f - f);
+          dck[k][e] = dct * f;
+        }
+      } else {  // TreeRNN, PROJ: h = tanh(z)
+        const float h = g[0][e];
+        dz[0][e] = dh[e] * (1.f - h * h);
+        if constexpr (KIND == FOLD_PROJ) dck[0][e] = a.dc[p * a.ld + j + e];  // c = c_child
+      }
+      if (!live[e]) {  // pad columns: zero dz and zero gradients for the children
+#pragma unroll
+        for (int q = 0; q < G; ++q) dz[q][e] = 0.f;
+        dck[0][e] = dck[1][e] = 0.f;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < G; ++q) {
+      if constexpr (BF)
+        *reinterpret_cast<uint32_t*>(gh + q * a.HP + j) = (uint32_t)f2bf(dz[q][0]) | ((uint32_t)f2bf(dz[q][1]) << 16);
+      else
+        *reinterpret_cast<float2*>(gb + q * a.HP + j) = make_float2(dz[q][0], dz[q][1]);
+    }
+    // a child's gradients: its dc stored whole by its only parent (a TreeRNN passes zeros), added atomically into
+    // a zeroed row otherwise; with K-split dz . W^T slices its dh row is zeroed here first
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
+      if (ck[k] < 0) continue;
+      float* dcr = a.dc + (size_t)ck[k] * a.ld + j;
+      if (sk[k]) {
+        *reinterpret_cast<float2*>(dcr) = make_float2(dck[k][0], dck[k][1]);
+        if (a.zero_child_dh) *reinterpret_cast<float2*>(a.dh + (size_t)ck[k] * a.ld + j) = make_float2(0.f, 0.f);
+      } else if (KIND != FOLD_TREERNN) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+          if (live[e]) unsafeAtomicAdd(dcr + e, dck[k][e]);
       }
     }
   }
@@ -994,7 +987,6 @@ __global__ void k_level_cbwd(Merged<BwdCellArgs> m) {
   const int row = blockIdx.x - m.begin[i];
   const BwdCellArgs a = m.a[i];
   switch (m.variant[i]) {
-    case FOLD_EMBED: cell_bwd_body<FOLD_EMBED, false>(a, row); break;
     case FOLD_TREERNN: cell_bwd_body<FOLD_TREERNN, BF>(a, row); break;
     case FOLD_TREELSTM: cell_bwd_body<FOLD_TREELSTM, BF>(a, row); break;
     case FOLD_LSTM: cell_bwd_body<FOLD_LSTM, BF>(a, row); break;
@@ -1250,13 +1242,12 @@ void launch_cell_bwd(int kind, const BwdCellArgs& a, hipStream_t st) {
                                 "cell_bwd.proj"};
   const int nk = kind == kTreeLstmLeaf ? FOLD_TREELSTM : kind;  // one class per operation family
   ProfScope prof(nk >= 0 && nk <= FOLD_PROJ ? names[nk] : "cell_bwd", st);
-  // one thread per hidden unit (up to 1024): every load of a row is in flight at once
-  dim3 grid(a.rows), block(std::min(a.HP, 1024));
+  // one thread per two hidden units (up to 1024 threads): every load of a row is in flight at once
+  dim3 grid(a.rows), block(std::min(std::max(a.HP / 2, kWave), 1024));
 #define FOLD_CB(K_)                                                                          \
   if (a.dz_bf16) hipLaunchKernelGGL((k_cell_bwd<K_, true>), grid, block, 0, st, a);          \
   else hipLaunchKernelGGL((k_cell_bwd<K_, false>), grid, block, 0, st, a);
   switch (kind) {
-    case FOLD_EMBED: hipLaunchKernelGGL((k_cell_bwd<FOLD_EMBED, false>), grid, block, 0, st, a); break;
     case FOLD_TREERNN: FOLD_CB(FOLD_TREERNN) break;
     case FOLD_TREELSTM: FOLD_CB(FOLD_TREELSTM) break;
     case kTreeLstmLeaf: FOLD_CB(kTreeLstmLeaf) break;
@@ -1414,9 +1405,9 @@ void launch_level_cbwd(const int* kinds, const BwdCellArgs* args, int n, hipStre
   m.begin[m.n] = total;
   ProfScope prof("cell_bwd.level", st);
   if (bf)
-    hipLaunchKernelGGL(k_level_cbwd<true>, dim3(total), dim3(std::min(hp, 1024)), 0, st, m);
+    hipLaunchKernelGGL(k_level_cbwd<true>, dim3(total), dim3(std::min(std::max(hp / 2, kWave), 1024)), 0, st, m);
   else
-    hipLaunchKernelGGL(k_level_cbwd<false>, dim3(total), dim3(std::min(hp, 1024)), 0, st, m);
+    hipLaunchKernelGGL(k_level_cbwd<false>, dim3(total), dim3(std::min(std::max(hp / 2, kWave), 1024)), 0, st, m);
 }
 
 bool bwd_dx_is_narrow(int dtype, const DxArgs& a) {
