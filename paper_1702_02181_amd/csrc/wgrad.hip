@@ -410,27 +410,43 @@ __global__ __launch_bounds__(wide::kThreads) void k_wgrad_bf16_w(WgArgs a) {
     const int qc = min(2 * q0 + lane, 2 * hi - 1);
     dma4_untracked(a.op_cpos + qc, slot + 64);
   };
-  // this lane's unit of an op row: weight-row column (A) and gate column (B) it fetches
+  // this lane's unit of an op row: weight-row column (A) and gate column (B) it fetches.  All but the
+  // rows' indices is fixed for the workgroup; a stage's index reads are issued together, ahead of its
+  // loads (each untracked load is a compiler barrier, so a read placed between two loads would wait alone)
   const int u = lane & 31;
+  int sr[4], sxi[4];
+  size_t sxcol[4], sdcol[4];
+  bool sxok[4], sdok[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 2 * (4 * wr + i) + (lane >> 5);  // op row within the stage
+    const int gu = u ^ (4 * (r & 3));              // global 16-byte unit of the tile row
+    const int m = m0 + 8 * gu;                     // X^T: weight rows m .. m + 7
+    const int child = a.seg ? min(m / a.HP, 1) : 0;
+    sr[i] = r;
+    sxi[i] = a.seg ? 64 + 2 * r + child : 32 + r;
+    sxcol[i] = (size_t)(a.seg ? m - child * a.HP : m) * 2;
+    sxok[i] = m < a.Kw;
+    const int n = n0 + 8 * gu;                     // dz^T: gate columns n .. n + 7
+    sdcol[i] = (size_t)n * 2;
+    sdok[i] = n < a.Nw;
+  }
   auto issue = [&](int c, char* sl) {
     const int* ix = iring[c % NIDX];
     const int q0 = lo + c * 32;
+    int xi[4], di[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = 2 * (4 * wr + i) + (lane >> 5);  // op row within the stage
-      const int gu = u ^ (4 * (r & 3));              // global 16-byte unit of the tile row
-      const bool live = q0 + r < hi;
-      // X^T: weight rows m0 + 8 gu .. + 7
-      const int m = m0 + 8 * gu;
-      const int child = a.seg ? min(m / a.HP, 1) : 0;
-      const int xi = a.seg ? ix[64 + 2 * r + child] : ix[32 + r];
-      const int col = a.seg ? m - child * a.HP : m;
-      const bool xa = live && m < a.Kw && xi >= 0;
-      dma16_untracked(xa ? xbase + (size_t)xi * xstride + (size_t)col * 2 : zero, sl + (4 * wr + i) * 1024);
-      // dz^T: gate columns n0 + 8 gu .. + 7
-      const int n = n0 + 8 * gu;
-      const bool da = live && n < a.Nw;
-      dma16_untracked(da ? reinterpret_cast<const char*>(a.dz) + (size_t)ix[r] * dstride + (size_t)n * 2 : zero,
+      xi[i] = ix[sxi[i]];
+      di[i] = ix[sr[i]];
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool live = q0 + sr[i] < hi;
+      const bool xa = live && sxok[i] && xi[i] >= 0;
+      dma16_untracked(xa ? xbase + (size_t)xi[i] * xstride + sxcol[i] : zero, sl + (4 * wr + i) * 1024);
+      const bool da = live && sdok[i];
+      dma16_untracked(da ? reinterpret_cast<const char*>(a.dz) + (size_t)di[i] * dstride + sdcol[i] : zero,
                       sl + ABYTES + (4 * wr + i) * 1024);
     }
   };
