@@ -813,10 +813,12 @@ WgradSplit wgrad_split(int count, int Kw, int Nw, int dtype) {
   // ops with many rows: 256 x 256 tiles (twice the operand reuse of 128 x 128), one workgroup per CU.
   // fp32 takes them only where their workgroups fill the compute units' slots (at least 90 %): on 65 k
   // rows, H = 256, the node weights' 10 tiles gain 5 % over 128 x 128, the leaf weights' 3 tiles (75 %
-  // full) lose 11 %
+  // full) lose 11 %.  bf16 takes them from 16 k rows on where at least 70 % of the 256 x 256 tiles' area
+  // is weight (H = 300: 74 %; the two ops of 32 k rows each, 0.27 -> 0.22 ms with their reductions)
   const long long wtiles = (long long)((Kw + 255) / 256) * ((Nw + 255) / 256);
   if (dtype == FOLD_BF16) {
-    w.wide = count >= 65536;
+    const double area = (double)Kw * Nw / ((double)wtiles * 65536.0);
+    w.wide = count >= 65536 || (count >= 16384 && area >= 0.7);
   } else if (count >= kWgWideF32Rows) {
     double fill = 0.0;
     wgrad_chunks(wtiles, count, 1024, 20480, 32, &fill);
