@@ -539,16 +539,31 @@ __global__ void k_tok_emit(const int* flag, const int* exs, const int* tok_rows,
                            const unsigned long long* err) {
   if (*err != kNoErr) return;
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= N) return;
-  const int p = tok_rows[i];
-  const int u = exs[i] + flag[i] - 1;
-  tok_seg[i] = u;
-  if (flag[i]) {
-    tok_start[u] = i;
-    tok_row[u] = input_idx[p];
-    atomicAdd(&op_runs[g_op[gid[p]]], 1);
+  bool f = false;
+  int op = -1;
+  if (i < N) {
+    const int p = tok_rows[i];
+    f = flag[i] != 0;
+    const int u = exs[i] + (f ? 1 : 0) - 1;
+    tok_seg[i] = u;
+    if (f) {
+      tok_start[u] = i;
+      tok_row[u] = input_idx[p];
+      op = g_op[gid[p]];
+    }
+    if (i == N - 1) tok_start[u + 1] = N;
   }
-  if (i == N - 1) tok_start[u + 1] = N;
+  // runs per operation, one atomic add per operation and wave: the list is sorted by operation, so a wave's
+  // run starts belong to one or a few of them (one add per run start would serialise on the same counter
+  // when every row is a run of its own)
+  unsigned long long m = __ballot(f);
+  while (m) {
+    const int leader = __ffsll((long long)m) - 1;
+    const int lop = __shfl(op, leader);
+    const unsigned long long same = __ballot(f && op == lop);
+    if ((int)(threadIdx.x & 63) == leader) atomicAdd(&op_runs[lop], __popcll(same));
+    m &= ~same;
+  }
 }
 
 // for entry q of the (op, row) list: the row's children and leaf-table row
