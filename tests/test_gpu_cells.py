@@ -164,18 +164,24 @@ def test_backward_rejects_misaligned_gradient_buffers():
     torch.cuda.synchronize()
 
 
-def _table_runs_case(dtype, graphs=256, leaves=64, H=32, V=5, seed=21):
+def _table_runs_case(dtype, graphs=256, leaves=64, H=32, V=5, seed=21, distinct=False):
     """Balanced trees of `leaves` Tree-LSTM leaves with an LSTM chain of three steps on each root; every leaf
-    and LSTM step reads one of V leaf-table rows, row 0 for 80 % of them."""
+    and LSTM step reads one of V leaf-table rows, row 0 for 80 % of them (distinct: a table row of its own)."""
     from tests._helpers import make_workload
     rng = np.random.default_rng(seed)
+    if distinct:
+        V = graphs * (leaves + 3)
     ops = [gen.OpSpec(gen.KIND_TREELSTM, 0, 1, 0), gen.OpSpec(gen.KIND_TREELSTM, 2, 0, 0),
            gen.OpSpec(gen.KIND_LSTM, 1, 1, 1)]
     params = [gen.make_param_set(rng, gen.KIND_TREELSTM, H, 2, H, dtype),
               gen.make_param_set(rng, gen.KIND_LSTM, H, 1, H, dtype)]
     table = gen._finish_values(0.1 * rng.standard_normal((V, H)), dtype)
 
+    rows = iter(rng.permutation(V).tolist())
+
     def token():
+        if distinct:
+            return next(rows)
         return 0 if rng.random() < 0.8 else int(rng.integers(1, V))
     batch = []
     for _ in range(graphs):
@@ -205,5 +211,18 @@ def test_leaf_table_gradient_long_runs(dtype):
     g, o = C.run_device(w, table_grad=True), C.run_oracle(w, table_grad=True)
     C.compare_all(w, g, o, table_grad=True)
     # and row by row (the table's rows differ in size: row 0 sums 80 % of the rows)
+    from oracle import compare
+    assert compare.rel_err(g["d_table"], o["d_table"]) <= C.TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_leaf_table_gradient_distinct_rows(dtype):
+    """Every leaf and LSTM step reads a table row of its own (37 graphs: 592 leaves and 111 steps, neither a
+    multiple of 64), so every row is a run of its own and the scheduler's per-operation run counts, added once
+    per operation and wave, meet an operation boundary inside a wave.  Table gradient row by row against the
+    oracle, every other state and gradient too."""
+    w = _table_runs_case(dtype, graphs=37, leaves=16, distinct=True)
+    g, o = C.run_device(w, table_grad=True), C.run_oracle(w, table_grad=True)
+    C.compare_all(w, g, o, table_grad=True)
     from oracle import compare
     assert compare.rel_err(g["d_table"], o["d_table"]) <= C.TOL[dtype]
