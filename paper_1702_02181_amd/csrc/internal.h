@@ -87,7 +87,10 @@ struct FwdArgs {
 };
 // pool row of child slot k of group row `row` (-1: the zero state)
 __device__ __forceinline__ int fwd_child(const FwdArgs& a, int row, int k) {
-  return a.cbase[k] >= 0 ? a.cbase[k] + row : a.child_pos[a.idx_off + row * a.arity + k];
+  // a select, not a[k]: k may differ between lanes, and an index into a struct held in registers (the merged
+  // level launches copy their group's arguments) would move the struct to scratch memory
+  const int cb = k == 0 ? a.cbase[0] : a.cbase[1];
+  return cb >= 0 ? cb + row : a.child_pos[a.idx_off + row * a.arity + k];
 }
 void launch_cell_fwd(int dtype, int kind, const FwdArgs& a, hipStream_t st);
 // The narrow groups of one level (at most kMaxMerge, every one narrow by fwd_plan) as one launch, plus one for
